@@ -1,0 +1,389 @@
+"""Pins for the CPU oracle: checks against things other than the oracle itself.
+
+- torch.nn.LSTM (fp64, CPU) forward and autograd backward: the textbook
+  library routine the dense case (S = 0) reduces to;
+- central finite differences of the oracle's own forward;
+- closed forms (zero weights; S = 0; S = R-1; equal scores; NaN);
+- brute force over every subset for the per-region selection, compared in
+  exact rational arithmetic;
+- the exact squared norm (fractions) within the fp64 summation error bound;
+- the sparsities of Table 1 (tests/golden);
+- invariants: 2^k scaling, never-kept rows exactly zero, masked autograd.
+"""
+import itertools
+import math
+import os
+from fractions import Fraction
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from paper_1806_00512_amd.inputs import make_layer, round_bf16_f32
+
+GOLDEN = os.path.join(os.path.dirname(__file__), "golden")
+
+
+def torch_lstm(x, W, b, h0, c0):
+    """torch.nn.LSTM in float64 with our layouts: x [T][I][B] -> h [T][H][B]."""
+    T, I, B = x.shape
+    H = W.shape[0] // 4
+    m = torch.nn.LSTM(I, H, dtype=torch.float64)
+    with torch.no_grad():
+        m.weight_ih_l0.copy_(torch.from_numpy(np.asarray(W[:, :I], np.float64)))
+        m.weight_hh_l0.copy_(torch.from_numpy(np.asarray(W[:, I:], np.float64)))
+        m.bias_ih_l0.copy_(torch.from_numpy(np.asarray(b, np.float64)))
+        m.bias_hh_l0.zero_()
+    return m
+
+
+def to_t(a, grad=False):
+    return torch.tensor(np.asarray(a, np.float64), dtype=torch.float64, requires_grad=grad)
+
+
+def autograd_lstm(x, W, b, h0, c0, dH_up, dhT, dcT, keep=None, P=4):
+    """Step-by-step fp64 LSTM differentiated by autograd.
+
+    With ``keep`` [T][4H/P], a hook zeroes the removed slices of the gradient
+    of the pre-activations, which is where the method sparsifies (dnet)."""
+    T, I, B = x.shape
+    H = W.shape[0] // 4
+    xt, Wt, bt = to_t(x, True), to_t(W, True), to_t(b, True)
+    h = to_t(h0 if h0 is not None else np.zeros((H, B)), True)
+    c = to_t(c0 if c0 is not None else np.zeros((H, B)), True)
+    h0t, c0t = h, c
+    pre_grads = [None] * T
+    loss = 0.0
+    for t in range(T):
+        a = Wt @ torch.cat([xt[t], h], 0) + bt[:, None]
+        if keep is not None:
+            rowmask = torch.from_numpy(np.repeat(keep[t], P).astype(np.float64))[:, None]
+            a.register_hook(lambda g, m=rowmask: g * m)
+
+        def save(g, t=t):
+            pre_grads[t] = g.detach().clone()
+        a.register_hook(save)
+        i, f, g, o = a[:H].sigmoid(), a[H:2 * H].sigmoid(), a[2 * H:3 * H].tanh(), a[3 * H:].sigmoid()
+        c = f * c + i * g
+        h = o * c.tanh()
+        loss = loss + (to_t(dH_up[t]) * h).sum()
+    if dhT is not None:
+        loss = loss + (to_t(dhT) * h).sum()
+    if dcT is not None:
+        loss = loss + (to_t(dcT) * c).sum()
+    loss.backward()
+    # the first hook registered sees the unmasked gradient when keep is given
+    return {"dX": xt.grad.numpy(), "dW": Wt.grad.numpy(), "db": bt.grad.numpy(),
+            "dh0": h0t.grad.numpy(), "dc0": c0t.grad.numpy(),
+            "pre": np.stack([p.numpy() for p in pre_grads])}
+
+
+def rel(a, b):
+    a, b = np.asarray(a, np.float64), np.asarray(b, np.float64)
+    n = np.linalg.norm(b)
+    return np.linalg.norm(a - b) / (n if n > 0 else 1.0)
+
+
+# --------------------------------------------------------------------------
+# forward / dense backward against the library routine
+# --------------------------------------------------------------------------
+@pytest.mark.parametrize("T,B,I,H", [(5, 3, 4, 6), (4, 2, 7, 3)])
+def test_forward_matches_torch_lstm(T, B, I, H):
+    d = make_layer(T, B, I, H, seed=1, w_scale=0.5, state=True)
+    gates, c, h = oracle.forward(d["x"], d["W"], d["b"], d["h0"], d["c0"])
+    m = torch_lstm(d["x"], d["W"], d["b"], d["h0"], d["c0"])
+    xs = to_t(d["x"]).permute(0, 2, 1)  # [T][B][I]
+    hx = (to_t(d["h0"]).T[None].contiguous(), to_t(d["c0"]).T[None].contiguous())
+    with torch.no_grad():
+        out, (hn, cn) = m(xs, hx)
+    assert np.abs(h[1:] - out.permute(0, 2, 1).numpy()).max() < 1e-12
+    assert np.abs(c[-1] - cn[0].T.numpy()).max() < 1e-12
+    assert np.array_equal(h[0], d["h0"]) and np.array_equal(c[0], d["c0"])
+
+
+@pytest.mark.parametrize("T,B,I,H", [(5, 3, 4, 6), (3, 5, 2, 8)])
+def test_dense_backward_matches_torch_autograd(T, B, I, H):
+    d = make_layer(T, B, I, H, seed=2, w_scale=0.5, state=True)
+    gates, c, h = oracle.forward(d["x"], d["W"], d["b"], d["h0"], d["c0"])
+    o = oracle.backward(d["x"], d["W"], gates, c, h, d["dH_up"], d["dhT"], d["dcT"],
+                        P=4, R=2, S=0, want_dG=True)
+    # library routine: torch.nn.LSTM autograd
+    m = torch_lstm(d["x"], d["W"], d["b"], d["h0"], d["c0"])
+    xs = to_t(d["x"]).permute(0, 2, 1).detach().requires_grad_(True)
+    h0t = to_t(d["h0"]).T[None].contiguous().requires_grad_(True)
+    c0t = to_t(d["c0"]).T[None].contiguous().requires_grad_(True)
+    out, (hn, cn) = m(xs, (h0t, c0t))
+    loss = (out * to_t(d["dH_up"]).permute(0, 2, 1)).sum()
+    loss = loss + (hn[0] * to_t(d["dhT"]).T).sum() + (cn[0] * to_t(d["dcT"]).T).sum()
+    loss.backward()
+    dW = np.concatenate([m.weight_ih_l0.grad.numpy(), m.weight_hh_l0.grad.numpy()], 1)
+    assert rel(o["dW"], dW) < 1e-12
+    assert rel(o["db"], m.bias_ih_l0.grad.numpy()) < 1e-12
+    assert rel(o["dX"], xs.grad.permute(0, 2, 1).numpy()) < 1e-12
+    assert rel(o["dh0"], h0t.grad[0].T.numpy()) < 1e-12
+    assert rel(o["dc0"], c0t.grad[0].T.numpy()) < 1e-12
+    # the gate gradient before sparsifying is the gradient of the pre-activations
+    ag = autograd_lstm(d["x"], d["W"], d["b"], d["h0"], d["c0"], d["dH_up"], d["dhT"], d["dcT"])
+    assert rel(o["dG"], ag["pre"]) < 1e-12
+
+
+def test_dense_backward_finite_differences():
+    T, B, I, H = 3, 2, 3, 4
+    d = make_layer(T, B, I, H, seed=3, w_scale=0.6, state=True)
+    x, W, b = (d[k].astype(np.float64) for k in ("x", "W", "b"))
+    h0, c0, dH, dhT, dcT = (d[k].astype(np.float64) for k in ("h0", "c0", "dH_up", "dhT", "dcT"))
+
+    def loss(x, W, h0, c0):
+        _, c, h = oracle.forward(x, W, b, h0, c0)
+        return float((dH * h[1:]).sum() + (dhT * h[-1]).sum() + (dcT * c[-1]).sum())
+
+    gates, c, h = oracle.forward(x, W, b, h0, c0)
+    o = oracle.backward(x, W, gates, c, h, dH, dhT, dcT, P=4, R=4, S=0)
+    eps = 1e-6
+    rng = np.random.default_rng(0)
+    for name, arr, grad in (("W", W, o["dW"]), ("x", x, o["dX"]), ("h0", h0, o["dh0"]),
+                            ("c0", c0, o["dc0"])):
+        for _ in range(8):
+            ix = tuple(rng.integers(0, s) for s in arr.shape)
+            args = {"x": x, "W": W, "h0": h0, "c0": c0}
+            p, m = arr.copy(), arr.copy()
+            p[ix] += eps
+            m[ix] -= eps
+            fd = (loss(**{**args, name: p}) - loss(**{**args, name: m})) / (2 * eps)
+            assert abs(fd - grad[ix]) <= 1e-6 * max(1.0, abs(fd)), (name, ix, fd, grad[ix])
+
+
+def test_closed_form_zero_weights():
+    """W = 0, b = 0: i = f = o = 1/2, g = 0, so c = h = 0 for all t; the only
+    nonzero gate gradient is dg = D_t / 2, where D_T = dh_T / 2 and
+    D_t = D_{t+1} / 2 + dh_t / 2 (the cell gradient after the output path)."""
+    T, B, I, H = 4, 3, 5, 8
+    rng = np.random.default_rng(5)
+    x = rng.standard_normal((T, I, B))
+    dH = rng.standard_normal((T, H, B))
+    W = np.zeros((4 * H, I + H))
+    gates, c, h = oracle.forward(x, W)
+    assert np.all(c == 0) and np.all(h == 0)
+    o = oracle.backward(x, W, gates, c, h, dH, P=4, R=2, S=0, want_dG=True)
+    D = np.zeros((T, H, B))
+    D[T - 1] = 0.5 * dH[T - 1]
+    for t in range(T - 2, -1, -1):
+        D[t] = 0.5 * D[t + 1] + 0.5 * dH[t]
+    for t in range(T):
+        exp = np.zeros((4 * H, B))
+        exp[2 * H:3 * H] = 0.5 * D[t]
+        assert np.array_equal(o["dG"][t], exp)
+    dW = np.zeros_like(W)
+    for t in range(T):
+        dW[2 * H:3 * H, :I] += (0.5 * D[t]) @ x[t].T
+    assert np.abs(o["dW"] - dW).max() < 1e-13
+    assert np.array_equal(o["dX"], np.zeros_like(x))
+    assert np.abs(o["dc0"] - 0.5 * D[0]).max() < 1e-15
+    # sparse, H a multiple of P*R: every region lies inside one gate block.
+    # Regions outside the g block hold only zeros (all scores tie), so they
+    # keep their first R-S slices (ties keep the lower index).
+    o2 = oracle.backward(x, W, gates, c, h, dH, P=4, R=2, S=1)
+    for t in range(T):
+        k = o2["keep"][t].reshape(-1, 2)
+        nz = slice(2 * H // 8, 3 * H // 8)  # regions covering the g block
+        zero_rows = np.ones(k.shape[0], bool)
+        zero_rows[nz] = False
+        assert np.all(k[zero_rows] == [1, 0])
+
+
+# --------------------------------------------------------------------------
+# selection and scores
+# --------------------------------------------------------------------------
+def brute_force_keep(scores, R, S):
+    """Keep the subset of each region with the largest exact score sum;
+    among equal sums the lexicographically smallest kept-index list."""
+    n = len(scores)
+    keep = np.zeros(n, np.uint8)
+    for r0 in range(0, n, R):
+        r = min(R, n - r0)
+        nk = r - (S * r) // R
+        best, best_set = None, None
+        for sub in itertools.combinations(range(r0, r0 + r), nk):
+            s = sum(Fraction(float(scores[i])) for i in sub)
+            if best is None or s > best or (s == best and list(sub) < list(best_set)):
+                best, best_set = s, sub
+        keep[list(best_set)] = 1
+    return keep
+
+
+@pytest.mark.parametrize("R,S", [(2, 1), (3, 1), (4, 2), (5, 3), (8, 2), (8, 4), (8, 6), (8, 7)])
+@pytest.mark.parametrize("tied", [False, True])
+def test_select_matches_brute_force(R, S, tied):
+    rng = np.random.default_rng(R * 10 + S + (100 if tied else 0))
+    for trial in range(20):
+        n = int(rng.integers(1, 3 * R + 1))  # includes partial regions
+        if tied:
+            sc = rng.integers(0, 3, n).astype(np.float64) * 0.25
+        else:
+            sc = rng.random(n) ** 3
+        assert np.array_equal(oracle.select(sc, R, S), brute_force_keep(sc, R, S)), (n, sc)
+
+
+def test_select_closed_forms():
+    rng = np.random.default_rng(7)
+    sc = rng.random(64)
+    assert np.all(oracle.select(sc, 8, 0) == 1)  # S = 0 keeps everything
+    k = oracle.select(sc, 8, 7).reshape(8, 8)  # S = R-1 keeps the argmax
+    assert np.array_equal(k.argmax(1), sc.reshape(8, 8).argmax(1)) and np.all(k.sum(1) == 1)
+    eq = np.full(24, 2.5)
+    assert np.array_equal(oracle.select(eq, 8, 3).reshape(3, 8),
+                          np.tile([1, 1, 1, 1, 1, 0, 0, 0], (3, 1)))
+    first_max = np.array([1.0, 3.0, 3.0, 0.5])
+    assert np.array_equal(oracle.select(first_max, 4, 3), [0, 1, 0, 0])
+    s = np.array([np.inf, np.nan, 5.0, np.nan])
+    assert np.array_equal(oracle.select(s, 4, 2), [0, 1, 0, 1])
+    assert np.array_equal(oracle.select(s, 4, 1), [1, 1, 0, 1])
+    assert np.array_equal(oracle.select(np.array([0.0, 0.0, 1.0]), 3, 1), [1, 0, 1])
+
+
+def test_table1_sparsities():
+    rows = [l.split() for l in open(os.path.join(GOLDEN, "table1_coarse_sparsity.txt"))
+            if l.strip() and not l.startswith("#")]
+    assert len(rows) == 6
+    rng = np.random.default_rng(11)
+    for R, S, sp in ((int(a), int(b), float(c)) for a, b, c in rows):
+        H, P = 512, 4  # the paper's 512-cell layers; P = 4 (section 4)
+        assert 4 * H // P == 4 * 128 * 4 // P  # 4H/P slices (H slices when P = 4 and 4H = 4*H)
+        kp = oracle.kept_rows(4 * H, P, R, S)
+        assert kp == round((1 - sp) * 4 * H)
+        keep = oracle.select(rng.random(4 * H // P), R, S)
+        assert keep.sum() * P == kp
+        assert np.all(keep.reshape(-1, R).sum(1) == R - S)
+
+
+def test_slice_count_paper_example():
+    # section 3: with P-element-wide slices, the 4H gate rows of a layer of H
+    # cells give H slices when P = 4
+    for H in (128, 512, 650):
+        assert oracle.kept_rows(4 * H, 4, 8, 0) // 4 == H
+
+
+def test_partial_region_rule():
+    # 4H/P = 650 slices (H = 650, P = 4): 81 full regions of 8 and one of 2,
+    # which removes floor(4 * 2 / 8) = 1
+    assert oracle.removed_in_region(2, 8, 4) == 1
+    assert oracle.kept_rows(2600, 4, 8, 4) == 4 * (81 * 4 + 1)
+    rng = np.random.default_rng(3)
+    keep = oracle.select(rng.random(650), 8, 4)
+    assert keep[:648].reshape(81, 8).sum(1).tolist() == [4] * 81 and keep[648:].sum() == 1
+
+
+@pytest.mark.parametrize("B,P", [(1, 4), (20, 4), (64, 4), (130, 2), (256, 1)])
+def test_scores_within_fp64_bound_of_exact(B, P):
+    rng = np.random.default_rng(B + P)
+    dG = (rng.standard_normal((8 * P, B)) * np.exp(rng.uniform(-20, 20, (8 * P, 1)))).astype(np.float32)
+    sc = oracle.scores(dG, P)
+    n = B * P
+    for j in range(8):
+        exact = sum(Fraction(float(v)) ** 2 for v in dG[j * P:(j + 1) * P].ravel())
+        err = abs(Fraction(sc[j]) - exact)
+        assert err <= exact * Fraction(n, 2 ** 52), (j, float(err / exact))
+    # small integers: every partial sum is exact, so the score is exact
+    di = rng.integers(-50, 50, (4 * P, B)).astype(np.float32)
+    exact = (di.astype(np.int64) ** 2).reshape(4, P * B).sum(1)
+    assert np.array_equal(oracle.scores(di, P), exact.astype(np.float64))
+
+
+def test_round_bf16_matches_torch():
+    rng = np.random.default_rng(9)
+    v = np.concatenate([rng.standard_normal(2000) * np.exp(rng.uniform(-80, 80, 2000)),
+                        [0.0, -0.0, 1.0 + 2 ** -8, 1.0 + 3 * 2 ** -8, 2 ** -130, 3.3e38]]).astype(np.float32)
+    ref = torch.from_numpy(v).to(torch.bfloat16).to(torch.float64).numpy()
+    assert np.array_equal(oracle.round_bf16(v), ref)
+    assert np.array_equal(round_bf16_f32(v).astype(np.float64), ref)
+
+
+# --------------------------------------------------------------------------
+# sparse backward
+# --------------------------------------------------------------------------
+@pytest.mark.parametrize("H,R,S", [(8, 8, 4), (6, 4, 2), (5, 8, 4), (8, 2, 1)])
+def test_sparse_matches_masked_autograd(H, R, S):
+    T, B, I, P = 4, 3, 5, 4
+    d = make_layer(T, B, I, H, seed=H + R, w_scale=0.5, state=True)
+    gates, c, h = oracle.forward(d["x"], d["W"], d["b"], d["h0"], d["c0"])
+    o = oracle.backward(d["x"], d["W"], gates, c, h, d["dH_up"], d["dhT"], d["dcT"],
+                        P=P, R=R, S=S, want_dG=True)
+    # masks are chosen by the oracle's selector on its own dG (pinned above);
+    # given those masks, every gradient must equal autograd with dnet masked
+    ag = autograd_lstm(d["x"], d["W"], d["b"], d["h0"], d["c0"], d["dH_up"], d["dhT"],
+                       d["dcT"], keep=o["keep"], P=P)
+    for k in ("dX", "dW", "db", "dh0", "dc0"):
+        assert rel(o[k], ag[k]) < 1e-12, k
+    # the selector saw the unmasked dG of the same step
+    for t in range(T):
+        assert np.array_equal(o["keep"][t], oracle.select(oracle.scores(o["dG"][t], P), R, S))
+        assert np.array_equal(o["idx"][t], np.flatnonzero(o["keep"][t]))
+    kp = oracle.kept_rows(4 * H, P, R, S)
+    assert np.all(o["keep"].sum(1) * P == kp)
+
+
+def test_s0_equals_dense_exactly():
+    d = make_layer(5, 4, 6, 8, seed=21, state=True)
+    gates, c, h = oracle.forward(d["x"], d["W"], d["b"], d["h0"], d["c0"])
+    a = oracle.backward(d["x"], d["W"], gates, c, h, d["dH_up"], d["dhT"], d["dcT"], P=4, R=8, S=0)
+    allk = np.ones((5, 8), np.uint8)
+    b = oracle.backward(d["x"], d["W"], gates, c, h, d["dH_up"], d["dhT"], d["dcT"], P=4, R=8,
+                        S=4, forced_keep=allk)
+    for k in ("dX", "dW", "db", "dh0", "dc0"):
+        assert np.array_equal(a[k], b[k])
+    assert np.array_equal(a["idx"], np.tile(np.arange(8), (5, 1)))
+
+
+def test_power_of_two_scaling():
+    d = make_layer(6, 5, 4, 16, seed=4)
+    gates, c, h = oracle.forward(d["x"], d["W"])
+    a = oracle.backward(d["x"], d["W"], gates, c, h, d["dH_up"], P=4, R=4, S=2)
+    b = oracle.backward(d["x"], d["W"], gates, c, h, d["dH_up"] * 8.0, P=4, R=4, S=2)
+    assert np.array_equal(a["keep"], b["keep"])
+    for k in ("dX", "dW", "db", "dh0", "dc0"):
+        assert np.array_equal(a[k] * 8.0, b[k])
+
+
+def test_never_kept_rows_are_zero():
+    d = make_layer(2, 3, 4, 16, seed=8)
+    gates, c, h = oracle.forward(d["x"], d["W"])
+    o = oracle.backward(d["x"], d["W"], gates, c, h, d["dH_up"], P=4, R=8, S=6)
+    never = np.flatnonzero(o["keep"].sum(0) == 0)
+    assert never.size > 0
+    rows = (never[:, None] * 4 + np.arange(4)).ravel()
+    assert np.all(o["dW"][rows] == 0) and np.all(o["db"][rows] == 0)
+    ever = np.flatnonzero(o["keep"].sum(0) > 0)
+    assert np.all(np.abs(o["dW"][ever * 4]).sum(1) > 0)
+
+
+def test_bf16_mode_rounds_stored_operands():
+    d = make_layer(3, 4, 8, 8, seed=12, dtype="bf16")
+    gates, c, h = oracle.forward(d["x"], d["W"], bf16=True)
+    for a in (gates, h):
+        assert np.array_equal(oracle.round_bf16(a), a)
+    assert not np.array_equal(oracle.round_bf16(c[1:]), c[1:])
+    o = oracle.backward(d["x"], d["W"], gates, c, h, d["dH_up"], P=4, R=4, S=2, bf16=True,
+                        want_dG=True)
+    assert np.array_equal(oracle.round_bf16(o["dG"]), o["dG"])
+    ref = oracle.backward(d["x"], d["W"], gates, c, h, d["dH_up"], P=4, R=4, S=2, bf16=False,
+                          forced_keep=o["keep"], want_dG=True)
+    # at the last step (the first one processed, before any rounded dG has fed
+    # back through the recurrence) dG is the unrounded one rounded once
+    assert np.all(np.abs(o["dG"][-1] - ref["dG"][-1]) <= np.abs(ref["dG"][-1]) * 2.0 ** -8)
+    assert np.array_equal(o["dG"][-1], oracle.round_bf16(ref["dG"][-1]))
+
+
+def test_multi_layer_chain():
+    from paper_1806_00512_amd.inputs import WORKLOADS, make_inputs
+    wl = WORKLOADS["lstm1_h128_b16_t20_f32"]
+    small = type(wl)(**{**wl.__dict__, "layers": 2, "input_size": 12, "hidden": 8, "batch": 3,
+                        "steps": 4})
+    inp = make_inputs(small, seed=0)
+    caches = oracle.stack_forward(inp["x"], inp["Ws"])
+    outs = oracle.stack_backward(caches, inp["dH_up"], S=0)
+    # layer 1 (bottom) receives layer 2's dX as its upstream gradient
+    o1 = oracle.backward(caches[0]["x"], caches[0]["W"], caches[0]["gates"], caches[0]["c"],
+                         caches[0]["h"], outs[1]["dX"], S=0)
+    assert np.array_equal(o1["dW"], outs[0]["dW"])
+    assert math.isfinite(float(outs[0]["dX"].sum()))
