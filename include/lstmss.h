@@ -1,0 +1,157 @@
+/*
+ * lstmss — structurally sparsified LSTM backward pass on AMD Instinct MI355X
+ * (gfx950).  C ABI of liblstmss.so.
+ *
+ * Method: Zhu, Clemons, Pool, Rhu, Keckler, Xie, "Structurally Sparsified
+ * Backward Propagation for Faster Long Short-Term Memory Training",
+ * arXiv:1806.00512.  In the backward pass of an LSTM layer the gate gradient
+ * dnet (4H x B per time step) is cut into slices of P consecutive gate rows,
+ * R adjacent slices form a sparsifying region, and in every region the S
+ * slices with the smallest L2 norm are dropped (section 3; S/R is the
+ * sparsity, Table 1).  The kept slices form a dense matrix plus an offset
+ * index array (section 3, after Fig. 2), and the weight and data gradient
+ * products run on that compacted matrix (section 4, custom operation).
+ *
+ * Conventions for every entry point
+ *   - Tensor pointers are DEVICE pointers owned by the caller.  The library
+ *     never allocates device memory; scratch comes from the caller's
+ *     workspace `ws` of `ws_bytes` bytes (query the size first).
+ *   - Row-major, batch B is the contiguous (last) dimension everywhere.
+ *   - W = [W_x | W_h] is 4H x (I+H); its row blocks are the gates in the order
+ *     i, f, g, o (rows [0,H) = i, [H,2H) = f, [2H,3H) = g, [3H,4H) = o).
+ *   - `dtype` is the storage type of x, W, h_out and the cache's gates and h
+ *     (fp32 or bf16).  Accumulation is fp32.  Biases, h0, c0, every gradient
+ *     (dH_up, dX, dW, db, dh0, dc0) and the cell state are fp32.
+ *   - Work is enqueued on `stream` (a hipStream_t; NULL = the null stream)
+ *     and the calls return without synchronising the host.
+ *   - Calls return LSTMSS_OK (0) or a negative error code; nothing is
+ *     enqueued when an argument check fails.  lstmss_last_error() gives the
+ *     calling thread's detail message for the last failure.
+ *   - Calls that overlap in time on different streams must use different
+ *     workspaces and outputs.
+ */
+#ifndef LSTMSS_H
+#define LSTMSS_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define LSTMSS_VERSION 1
+
+typedef enum { LSTMSS_F32 = 0, LSTMSS_BF16 = 1 } lstmss_dtype;
+
+/* Sparsifying structure kinds (section 3).  Only COARSE is built; FINE (the
+ * M_y x M_x submatrix variant) returns LSTMSS_ERR_UNSUPPORTED. */
+typedef enum { LSTMSS_COARSE = 0, LSTMSS_FINE = 1 } lstmss_kind;
+
+enum {
+    LSTMSS_OK = 0,
+    LSTMSS_ERR_INVALID_ARG = -1, /* null required pointer, bad size or structure */
+    LSTMSS_ERR_UNSUPPORTED = -2, /* valid but not built (FINE, unknown dtype) */
+    LSTMSS_ERR_WORKSPACE = -3,   /* ws_bytes smaller than the size query returned */
+    LSTMSS_ERR_HIP = -4          /* a HIP runtime call failed (see lstmss_last_error) */
+};
+
+/* One layer over the whole sequence: T steps, batch B, input size I,
+ * hidden size H, storage dtype (lstmss_dtype). */
+typedef struct {
+    int32_t T, B, I, H;
+    int32_t dtype;
+} lstmss_dims;
+
+/* Coarse structure: P gate rows per slice, R slices per region (1 <= R <= 64).
+ * The number of slices removed per region is S = sparsity * R, which must be
+ * an integer (within 1e-6) with 0 <= S < R.  4H must be a multiple of P.
+ * When 4H/P is not a multiple of R, the last region has r < R slices and
+ * removes floor(S*r/R).  My, Mx are reserved for the FINE kind. */
+typedef struct {
+    int32_t kind;
+    int32_t P, R;
+    int32_t My, Mx;
+} lstmss_structure;
+
+int32_t lstmss_version(void);
+const char *lstmss_strerror(int32_t code);
+/* Detail of the calling thread's last failed call ("" if none). */
+const char *lstmss_last_error(void);
+
+/* Bytes of the forward cache written by lstm_fwd_cache and read by the
+ * backward calls: activated gates [T][4H][B] (dtype), cell state
+ * [T+1][H][B] (fp32) and hidden state [T+1][H][B] (dtype).  <0 on error. */
+int64_t lstmss_cache_bytes(const lstmss_dims *d);
+
+/* K' = P x (number of kept slices per step) for the given structure and
+ * sparsity; 4H when sparsity is 0.  <0 on error. */
+int64_t lstmss_kept_rows(const lstmss_dims *d, float sparsity, const lstmss_structure *s);
+
+/* Workspace bytes needed by lstm_bwd_structsparse with these arguments
+ * (sparsity 0 gives the size for lstm_bwd_dense).  <0 on error. */
+int64_t lstmss_workspace_bytes(const lstmss_dims *d, float sparsity, const lstmss_structure *s);
+
+/* Forward pass of one LSTM layer, keeping what the backward pass reads
+ * (the paper's forward computes the gate activations, section 4).
+ *   a_t = W [x_t; h_{t-1}] + b;  i, f, o = sigmoid, g = tanh of a_t's blocks;
+ *   c_t = f*c_{t-1} + i*g;  h_t = o*tanh(c_t).
+ *   x      [T][I][B] dtype            W [4H][I+H] dtype
+ *   b      [4H] fp32, NULL = 0        h0, c0 [H][B] fp32, NULL = 0
+ *   h_out  [T][H][B] dtype (h_1..h_T), may be NULL
+ *   cache  lstmss_cache_bytes(d) bytes, written. */
+int32_t lstm_fwd_cache(const lstmss_dims *d, const void *x, const void *W, const float *b,
+                       const float *h0, const float *c0, void *h_out, void *cache,
+                       void *stream);
+
+/* Dense backward pass through time of one layer (the paper's baseline, every
+ * gate-gradient row kept).  Loss convention: dH_up[t] = dL/dh_t from above,
+ * dhT, dcT = dL/dh_T, dL/dc_T from later time (NULL = 0).
+ *   x, W, cache as given to / written by lstm_fwd_cache
+ *   dH_up  [T][H][B] fp32
+ *   dX     [T][I][B] fp32 (dL/dx_t), NULL skips the input-gradient rows
+ *   dW     [4H][I+H] fp32, overwritten
+ *   db     [4H] fp32 or NULL, overwritten
+ *   dh0, dc0 [H][B] fp32 (dL/dh_0, dL/dc_0) or NULL
+ *   ws     lstmss_workspace_bytes(d, 0, s) bytes (any structure, or NULL s). */
+int32_t lstm_bwd_dense(const lstmss_dims *d, const void *x, const void *W, const void *cache,
+                       const float *dH_up, const float *dhT, const float *dcT, float *dX,
+                       float *dW, float *db, float *dh0, float *dc0, void *ws, size_t ws_bytes,
+                       void *stream);
+
+/* Structurally sparsified backward pass (section 3, coarse-grained).  At every
+ * time step the gate gradient is formed, each P-row slice is scored by its
+ * squared L2 norm (same ranking as the norm) summed in fp64 in a fixed order
+ * (64 strided partial sums over the batch, combined pairwise by index xor 32,
+ * 16, 8, 4, 2, 1; then the P rows in increasing order), the S lowest slices of
+ * every region are dropped (ties drop the higher slice index; NaN scores rank
+ * highest), the kept rows are compacted in ascending order and both gradient
+ * products run on the compacted rows.  The cell-state gradient recursion uses
+ * the unsparsified gradient.  With sparsity 0 the result equals
+ * lstm_bwd_dense.
+ * Arguments as lstm_bwd_dense, plus
+ *   sparsity, s    structure (see lstmss_structure)
+ *   idx_out        [T][K'/P] int32 kept slice indices per step, or NULL
+ *   dbg_dgates     [T][4H][B] dtype gate gradient before sparsifying (the
+ *                  exact values that were scored), or NULL
+ *   ws             lstmss_workspace_bytes(d, sparsity, s) bytes. */
+int32_t lstm_bwd_structsparse(const lstmss_dims *d, float sparsity, const lstmss_structure *s,
+                              const void *x, const void *W, const void *cache,
+                              const float *dH_up, const float *dhT, const float *dcT, float *dX,
+                              float *dW, float *db, float *dh0, float *dc0, int32_t *idx_out,
+                              void *dbg_dgates, void *ws, size_t ws_bytes, void *stream);
+
+/* Score, select and compact one given gate-gradient matrix (the selection
+ * step of lstm_bwd_structsparse on its own, same device code).
+ *   dG     [4H][B] dtype (d->T is ignored)
+ *   dG_c   [K'][B] dtype, kept rows in ascending order
+ *   idx    [K'/P] int32 kept slice indices
+ *   scores [4H/P] fp64 slice scores, or NULL */
+int32_t lstmss_select_compact(const lstmss_dims *d, float sparsity, const lstmss_structure *s,
+                              const void *dG, void *dG_c, int32_t *idx, double *scores,
+                              void *stream);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* LSTMSS_H */

@@ -1,0 +1,101 @@
+// Kernel parameter blocks and launchers (internal to liblstmss).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace lstmss {
+
+enum CellMode { CELL_DENSE = 0, CELL_SPARSE = 1, CELL_GIVEN = 2 };
+
+// One backward time step of the elementwise gate-gradient work, fused with
+// slice scoring, per-region selection and compaction of the kept rows.
+struct CellArgs {
+    int B, H, I;
+    int P, R, S;
+    long nslices;          // 4H / P
+    int regions_per_wg;    // work-group tile in regions
+    // inputs of step t (storage type is the kernel's template type)
+    const void *gates;     // [4H][B] activated i, f, g, o
+    const float *c_t;      // [H][B]
+    const float *c_prev;   // [H][B]
+    const float *dH_up;    // [H][B]
+    const float *dh_part;  // dh_rec as dh_nparts partial sums spaced dh_stride, or NULL
+    int dh_nparts;
+    long dh_stride;
+    const float *dc_in;    // [H][B] or NULL (zero)
+    float *dc_out;         // [H][B]
+    const void *dG_in;     // CELL_GIVEN only: [4H][B]
+    // outputs
+    void *dGc;             // [K'][B]
+    int32_t *idx;          // [K'/P] (sparse modes)
+    float *db;             // [4H] accumulated over kept rows, or NULL
+    void *dbg;             // [4H][B] or NULL
+    double *scores;        // [4H/P] or NULL
+    // reduction of the previous step's input gradient (dX[t+1]) from the
+    // split-K partials of the data-gradient product
+    const float *dx_part;
+    int dx_nparts;
+    long dx_stride;
+    float *dx_out;
+    long dx_n;
+};
+
+// Data gradient [dx_t; dh_{t-1}] = W_c^T dG_c, split over K into partials.
+struct Gemm1Args {
+    const void *W;         // [4H][ldw]
+    long ldw;              // I + H
+    const void *Gc;        // [Kp][N]
+    const int32_t *idx;    // [Kp/P] kept slices, or NULL for identity rows
+    int P;
+    long Kp;
+    int M, m_begin, N;     // output rows [m_begin, M), columns N = B
+    float *part;           // [splitk][M][N]
+    long part_stride;      // M * N
+    int splitk;
+    long k_chunk;
+};
+
+// Weight gradient dW[rows] += dG_c [x_t; h_{t-1}]^T (rows scattered by idx).
+struct Gemm2Args {
+    const void *Gc;        // [Kp][B]
+    const int32_t *idx;    // [Kp/P] or NULL
+    int P;
+    long Kp;
+    const void *xt;        // [I][B]
+    const void *hp;        // [H][B]
+    int I, H, B;
+    float *dW;             // [4H][I+H]
+};
+
+// One forward step: a = W [x_t; h_{t-1}] + b, activations, cell update.
+struct FwdArgs {
+    const void *W;
+    const float *bias;     // [4H] or NULL
+    const void *xt;        // [I][B]
+    const void *hp;        // [H][B]
+    const float *cp;       // [H][B]
+    int I, H, B;
+    void *gates;           // [4H][B]
+    float *cn;             // [H][B]
+    void *hn;              // [H][B]
+    void *hout;            // [H][B] or NULL
+};
+
+hipError_t launch_cell(const CellArgs &a, int mode, bool bf16, hipStream_t s);
+size_t cell_lds_bytes(const CellArgs &a, int mode);
+hipError_t launch_gemm1(const Gemm1Args &a, bool bf16, hipStream_t s);
+hipError_t launch_gemm2(const Gemm2Args &a, bool bf16, hipStream_t s);
+hipError_t launch_fwd_step(const FwdArgs &a, bool bf16, hipStream_t s);
+hipError_t launch_fill(float *p, long n, float v, hipStream_t s);
+hipError_t launch_copy_in(float *dst, const float *src, long n, hipStream_t s); // src NULL -> zero
+hipError_t launch_reduce_parts(float *out, const float *part, int nparts, long stride, long n,
+                               hipStream_t s);
+hipError_t launch_h0_store(void *dst, const float *src, long n, bool bf16, hipStream_t s);
+
+// Tile constants shared by the host-side sizing code.
+constexpr int GEMM1_TK = 32;
+int gemm1_tn(int N);
+int gemm1_tm(int N);
+
+} // namespace lstmss

@@ -1,0 +1,279 @@
+"""Python binding of liblstmss (ctypes): torch tensors in, device pointers out.
+
+Argument marshalling only: every step of the forward and backward passes runs
+in the HIP kernels of liblstmss.so.  torch provides device memory and the
+current stream.  The entry points mirror include/lstmss.h:
+
+  fwd_cache              -> lstm_fwd_cache
+  bwd_dense              -> lstm_bwd_dense
+  bwd_structsparse       -> lstm_bwd_structsparse
+  select_compact         -> lstmss_select_compact
+  cache_bytes / kept_rows / workspace_bytes -> the size queries
+
+Loading fails loudly (RuntimeError) when liblstmss.so has not been built;
+there is no fallback implementation.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+
+import torch
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "liblstmss.so")
+
+F32, BF16 = 0, 1
+COARSE, FINE = 0, 1
+ERR = {0: "ok", -1: "invalid argument", -2: "unsupported", -3: "workspace too small",
+       -4: "HIP runtime error"}
+
+# Exported symbols of include/lstmss.h
+SYMBOLS = ("lstmss_version", "lstmss_strerror", "lstmss_last_error", "lstmss_cache_bytes",
+           "lstmss_kept_rows", "lstmss_workspace_bytes", "lstm_fwd_cache", "lstm_bwd_dense",
+           "lstm_bwd_structsparse", "lstmss_select_compact")
+
+
+class Dims(ctypes.Structure):
+    _fields_ = [("T", ctypes.c_int32), ("B", ctypes.c_int32), ("I", ctypes.c_int32),
+                ("H", ctypes.c_int32), ("dtype", ctypes.c_int32)]
+
+
+class Structure(ctypes.Structure):
+    _fields_ = [("kind", ctypes.c_int32), ("P", ctypes.c_int32), ("R", ctypes.c_int32),
+                ("My", ctypes.c_int32), ("Mx", ctypes.c_int32)]
+
+
+class LstmssError(RuntimeError):
+    def __init__(self, code, what, detail):
+        super().__init__("%s: %s (%d): %s" % (what, ERR.get(code, "?"), code, detail))
+        self.code = code
+
+
+_lib = None
+
+
+def load():
+    """Load liblstmss.so (built in-tree by __graft_entry__.build())."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(LIB_PATH):
+        raise RuntimeError("liblstmss.so is not built (%s); run __graft_entry__.build()" % LIB_PATH)
+    lib = ctypes.CDLL(LIB_PATH)
+    vp, i32, i64, f = ctypes.c_void_p, ctypes.c_int32, ctypes.c_int64, ctypes.c_float
+    pd, ps = ctypes.POINTER(Dims), ctypes.POINTER(Structure)
+    lib.lstmss_version.restype = i32
+    lib.lstmss_strerror.argtypes = [i32]
+    lib.lstmss_strerror.restype = ctypes.c_char_p
+    lib.lstmss_last_error.restype = ctypes.c_char_p
+    lib.lstmss_cache_bytes.argtypes = [pd]
+    lib.lstmss_cache_bytes.restype = i64
+    lib.lstmss_kept_rows.argtypes = [pd, f, ps]
+    lib.lstmss_kept_rows.restype = i64
+    lib.lstmss_workspace_bytes.argtypes = [pd, f, ps]
+    lib.lstmss_workspace_bytes.restype = i64
+    lib.lstm_fwd_cache.argtypes = [pd, vp, vp, vp, vp, vp, vp, vp, vp]
+    lib.lstm_fwd_cache.restype = i32
+    lib.lstm_bwd_dense.argtypes = [pd, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp,
+                                   ctypes.c_size_t, vp]
+    lib.lstm_bwd_dense.restype = i32
+    lib.lstm_bwd_structsparse.argtypes = [pd, f, ps, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp,
+                                          vp, vp, vp, ctypes.c_size_t, vp]
+    lib.lstm_bwd_structsparse.restype = i32
+    lib.lstmss_select_compact.argtypes = [pd, f, ps, vp, vp, vp, vp, vp]
+    lib.lstmss_select_compact.restype = i32
+    _lib = lib
+    return lib
+
+
+def _check(code, what):
+    if code != 0:
+        detail = load().lstmss_last_error().decode()
+        raise LstmssError(code, what, detail)
+
+
+def _dt(dtype):
+    if dtype in (torch.float32, "f32", F32):
+        return F32
+    if dtype in (torch.bfloat16, "bf16", BF16):
+        return BF16
+    raise ValueError("unsupported storage dtype %r" % (dtype,))
+
+
+def torch_dtype(dt):
+    return torch.bfloat16 if _dt(dt) == BF16 else torch.float32
+
+
+def dims(T, B, I, H, dtype=F32) -> Dims:
+    return Dims(int(T), int(B), int(I), int(H), _dt(dtype))
+
+
+def structure(P=4, R=8, kind=COARSE) -> Structure:
+    return Structure(int(kind), int(P), int(R), 0, 0)
+
+
+def _ptr(t, dtype=None, shape=None, name="tensor"):
+    if t is None:
+        return None
+    if not isinstance(t, torch.Tensor):
+        raise TypeError("%s must be a torch tensor" % name)
+    if t.device.type != "cuda":
+        raise ValueError("%s must live on the GPU" % name)
+    if not t.is_contiguous():
+        raise ValueError("%s must be contiguous" % name)
+    if dtype is not None and t.dtype != dtype:
+        raise ValueError("%s has dtype %s, expected %s" % (name, t.dtype, dtype))
+    if shape is not None and tuple(t.shape) != tuple(shape):
+        raise ValueError("%s has shape %s, expected %s" % (name, tuple(t.shape), tuple(shape)))
+    return ctypes.c_void_p(t.data_ptr())
+
+
+def _stream(stream):
+    s = stream if stream is not None else torch.cuda.current_stream()
+    return ctypes.c_void_p(s.cuda_stream)
+
+
+def cache_bytes(d: Dims) -> int:
+    n = load().lstmss_cache_bytes(ctypes.byref(d))
+    _check(0 if n >= 0 else int(n), "lstmss_cache_bytes")
+    return int(n)
+
+
+def kept_rows(d: Dims, sparsity: float, s: Structure) -> int:
+    n = load().lstmss_kept_rows(ctypes.byref(d), float(sparsity), ctypes.byref(s))
+    _check(0 if n >= 0 else int(n), "lstmss_kept_rows")
+    return int(n)
+
+
+def workspace_bytes(d: Dims, sparsity: float = 0.0, s: Structure | None = None) -> int:
+    n = load().lstmss_workspace_bytes(ctypes.byref(d), float(sparsity),
+                                      ctypes.byref(s) if s is not None else None)
+    _check(0 if n >= 0 else int(n), "lstmss_workspace_bytes")
+    return int(n)
+
+
+def fwd_cache(x, W, b=None, h0=None, c0=None, h_out=None, cache=None, stream=None):
+    """x [T][I][B], W [4H][I+H] (fp32 or bf16) -> (h_out [T][H][B], cache bytes)."""
+    T, I, B = x.shape
+    H = W.shape[0] // 4
+    st = x.dtype
+    d = dims(T, B, I, H, st)
+    if cache is None:
+        cache = torch.empty(cache_bytes(d), dtype=torch.uint8, device=x.device)
+    if h_out is None:
+        h_out = torch.empty((T, H, B), dtype=st, device=x.device)
+    rc = load().lstm_fwd_cache(ctypes.byref(d), _ptr(x, st, name="x"),
+                               _ptr(W, st, (4 * H, I + H), "W"),
+                               _ptr(b, torch.float32, (4 * H,), "b"),
+                               _ptr(h0, torch.float32, (H, B), "h0"),
+                               _ptr(c0, torch.float32, (H, B), "c0"),
+                               _ptr(h_out, st, (T, H, B), "h_out"),
+                               _ptr(cache, torch.uint8, name="cache"), _stream(stream))
+    _check(rc, "lstm_fwd_cache")
+    return h_out, cache
+
+
+def _bwd_outputs(T, B, I, H, dev, want_dX, out):
+    out = dict(out or {})
+    f32 = torch.float32
+    if want_dX and out.get("dX") is None:
+        out["dX"] = torch.empty((T, I, B), dtype=f32, device=dev)
+    for k, shape in (("dW", (4 * H, I + H)), ("db", (4 * H,)), ("dh0", (H, B)), ("dc0", (H, B))):
+        if out.get(k) is None:
+            out[k] = torch.empty(shape, dtype=f32, device=dev)
+    return out
+
+
+def bwd_dense(x, W, cache, dH_up, dhT=None, dcT=None, want_dX=True, out=None, ws=None,
+              stream=None):
+    """Dense backward of one layer.  Returns dict(dX, dW, db, dh0, dc0)."""
+    T, I, B = x.shape
+    H = W.shape[0] // 4
+    st = x.dtype
+    d = dims(T, B, I, H, st)
+    o = _bwd_outputs(T, B, I, H, x.device, want_dX, out)
+    if ws is None:
+        ws = torch.empty(workspace_bytes(d, 0.0, None), dtype=torch.uint8, device=x.device)
+    f32 = torch.float32
+    rc = load().lstm_bwd_dense(
+        ctypes.byref(d), _ptr(x, st, name="x"), _ptr(W, st, (4 * H, I + H), "W"),
+        _ptr(cache, torch.uint8, name="cache"), _ptr(dH_up, f32, (T, H, B), "dH_up"),
+        _ptr(dhT, f32, (H, B), "dhT"), _ptr(dcT, f32, (H, B), "dcT"),
+        _ptr(o.get("dX"), f32, (T, I, B), "dX"), _ptr(o["dW"], f32, name="dW"),
+        _ptr(o["db"], f32, name="db"), _ptr(o["dh0"], f32, name="dh0"),
+        _ptr(o["dc0"], f32, name="dc0"), _ptr(ws, torch.uint8, name="ws"), ws.numel(),
+        _stream(stream))
+    _check(rc, "lstm_bwd_dense")
+    return o
+
+
+def bwd_structsparse(x, W, cache, dH_up, sparsity=0.5, P=4, R=8, dhT=None, dcT=None,
+                     want_dX=True, want_idx=True, want_dbg=False, out=None, ws=None, stream=None):
+    """Structurally sparsified backward of one layer.
+
+    Returns dict(dX, dW, db, dh0, dc0, idx [T][K'/P] int32, dbg [T][4H][B] or None)."""
+    T, I, B = x.shape
+    H = W.shape[0] // 4
+    st = x.dtype
+    d = dims(T, B, I, H, st)
+    s = structure(P, R)
+    o = _bwd_outputs(T, B, I, H, x.device, want_dX, out)
+    kp = kept_rows(d, sparsity, s)
+    if want_idx and o.get("idx") is None:
+        o["idx"] = torch.empty((T, kp // P), dtype=torch.int32, device=x.device)
+    if want_dbg and o.get("dbg") is None:
+        o["dbg"] = torch.empty((T, 4 * H, B), dtype=st, device=x.device)
+    if ws is None:
+        ws = torch.empty(workspace_bytes(d, sparsity, s), dtype=torch.uint8, device=x.device)
+    f32 = torch.float32
+    rc = load().lstm_bwd_structsparse(
+        ctypes.byref(d), float(sparsity), ctypes.byref(s), _ptr(x, st, name="x"),
+        _ptr(W, st, (4 * H, I + H), "W"), _ptr(cache, torch.uint8, name="cache"),
+        _ptr(dH_up, f32, (T, H, B), "dH_up"), _ptr(dhT, f32, (H, B), "dhT"),
+        _ptr(dcT, f32, (H, B), "dcT"), _ptr(o.get("dX"), f32, (T, I, B), "dX"),
+        _ptr(o["dW"], f32, name="dW"), _ptr(o["db"], f32, name="db"),
+        _ptr(o["dh0"], f32, name="dh0"), _ptr(o["dc0"], f32, name="dc0"),
+        _ptr(o.get("idx"), torch.int32, (T, kp // P), "idx"),
+        _ptr(o.get("dbg"), st, (T, 4 * H, B), "dbg"), _ptr(ws, torch.uint8, name="ws"),
+        ws.numel(), _stream(stream))
+    _check(rc, "lstm_bwd_structsparse")
+    return o
+
+
+def select_compact(dG, sparsity=0.5, P=4, R=8, want_scores=True, stream=None):
+    """Score / select / compact one gate-gradient matrix dG [4H][B]."""
+    G, B = dG.shape
+    H = G // 4
+    st = dG.dtype
+    d = dims(1, B, 1, H, st)
+    s = structure(P, R)
+    kp = kept_rows(d, sparsity, s)
+    dGc = torch.empty((kp, B), dtype=st, device=dG.device)
+    idx = torch.empty((kp // P,), dtype=torch.int32, device=dG.device)
+    sc = torch.empty((G // P,), dtype=torch.float64, device=dG.device) if want_scores else None
+    rc = load().lstmss_select_compact(ctypes.byref(d), float(sparsity), ctypes.byref(s),
+                                      _ptr(dG, st, name="dG"), _ptr(dGc), _ptr(idx), _ptr(sc),
+                                      _stream(stream))
+    _check(rc, "lstmss_select_compact")
+    return dGc, idx, sc
+
+
+def cache_views(cache, T, B, H, dtype):
+    """Views of a cache buffer: gates [T][4H][B], c [T+1][H][B] (fp32), h [T+1][H][B].
+
+    The layout (256-byte aligned sections in this order) is the one
+    lstmss_cache_bytes sizes."""
+    st = torch_dtype(dtype)
+    es = 2 if st == torch.bfloat16 else 4
+
+    def a256(n):
+        return (n + 255) // 256 * 256
+    g_bytes = T * 4 * H * B * es
+    c_off = a256(g_bytes)
+    c_bytes = (T + 1) * H * B * 4
+    h_off = c_off + a256(c_bytes)
+    gates = cache[:g_bytes].view(st).view(T, 4 * H, B)
+    c = cache[c_off:c_off + c_bytes].view(torch.float32).view(T + 1, H, B)
+    h = cache[h_off:h_off + (T + 1) * H * B * es].view(st).view(T + 1, H, B)
+    return gates, c, h

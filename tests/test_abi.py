@@ -1,0 +1,111 @@
+"""CPU-side checks of the C ABI: the library loads, exports every symbol the
+header declares, and its host-only entry points (size queries, argument
+validation) behave.  No GPU compute is launched here."""
+import ctypes
+import os
+import re
+
+import numpy as np
+import pytest
+
+import oracle
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "lstmss.h")
+
+
+@pytest.fixture(scope="module")
+def L():
+    import paper_1806_00512_amd.lstmss as lstmss
+    lstmss.load()
+    return lstmss
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"^\s*(?:const\s+)?\w+\s*\*?\s*(\w+)\s*\(", text, flags=re.M)))
+
+
+def test_header_symbols_exported(L):
+    names = declared_functions()
+    assert "lstm_bwd_structsparse" in names and len(names) >= 10
+    lib = ctypes.CDLL(L.LIB_PATH)
+    for n in names:
+        assert hasattr(lib, n), n
+    assert set(L.SYMBOLS) == set(names)
+    assert L.load().lstmss_version() == 1
+
+
+def test_strerror(L):
+    lib = L.load()
+    assert lib.lstmss_strerror(0) == b"success"
+    assert lib.lstmss_strerror(-3) == b"workspace too small"
+    assert lib.lstmss_strerror(-99) == b"unknown error code"
+
+
+@pytest.mark.parametrize("H,P,R,sp", [(128, 4, 8, 0.5), (650, 4, 8, 0.5), (1024, 4, 8, 0.25),
+                                      (1024, 4, 8, 0.75), (2048, 4, 8, 0.5), (4096, 4, 8, 0.5),
+                                      (650, 2, 16, 0.5), (100, 4, 32, 0.5), (33, 1, 5, 0.4),
+                                      (512, 4, 4, 0.5), (512, 4, 64, 0.25)])
+def test_kept_rows_matches_oracle(L, H, P, R, sp):
+    d = L.dims(3, 16, 32, H)
+    S = int(round(sp * R))
+    assert L.kept_rows(d, sp, L.structure(P, R)) == oracle.kept_rows(4 * H, P, R, S)
+    assert L.kept_rows(d, 0.0, L.structure(P, R)) == 4 * H
+
+
+def test_sizes(L):
+    for dt, es in ((L.F32, 4), (L.BF16, 2)):
+        d = L.dims(35, 20, 650, 650, dt)
+        cb = L.cache_bytes(d)
+        assert cb >= 35 * 4 * 650 * 20 * es + 36 * 650 * 20 * (4 + es)
+        wd = L.workspace_bytes(d, 0.0, None)
+        ws = L.workspace_bytes(d, 0.5, L.structure(4, 8))
+        # the compacted gate gradient of every step dominates the workspace
+        assert wd > ws >= 35 * 1300 * 20 * es
+
+
+@pytest.mark.parametrize("args,code", [
+    ((0, 4, 4, 8), -1), ((2, 4, 4, -1), -1), ((2, 4, 4, 8, 7), -2)])
+def test_bad_dims(L, args, code):
+    d = L.Dims(*(list(args) + [0] * (5 - len(args))))
+    n = L.load().lstmss_cache_bytes(ctypes.byref(d))
+    assert n == code
+    assert L.load().lstmss_last_error()
+
+
+@pytest.mark.parametrize("P,R,sp,code", [(3, 8, 0.5, -1), (4, 0, 0.5, -1), (4, 65, 0.5, -1),
+                                         (4, 8, 0.3, -1), (4, 8, 1.0, -1), (4, 8, -0.125, -1),
+                                         (4, 8, float("nan"), -1)])
+def test_bad_structure(L, P, R, sp, code):
+    d = L.dims(2, 4, 4, 8)
+    n = L.load().lstmss_kept_rows(ctypes.byref(d), sp, ctypes.byref(L.structure(P, R)))
+    assert n == code
+
+
+def test_fine_kind_unsupported(L):
+    d = L.dims(2, 4, 4, 8)
+    n = L.load().lstmss_kept_rows(ctypes.byref(d), 0.5, ctypes.byref(L.structure(4, 8, L.FINE)))
+    assert n == -2
+
+
+def test_null_pointers_rejected_before_launch(L):
+    lib = L.load()
+    d = L.dims(2, 4, 4, 8)
+    rc = lib.lstm_fwd_cache(ctypes.byref(d), None, None, None, None, None, None, None, None)
+    assert rc == -1
+    s = L.structure(4, 8)
+    rc = lib.lstm_bwd_structsparse(ctypes.byref(d), 0.5, ctypes.byref(s), *([None] * 14), 0, None)
+    assert rc == -1
+    rc = lib.lstm_bwd_dense(ctypes.byref(d), *([None] * 12), 0, None)
+    assert rc == -1
+    assert b"NULL" in lib.lstmss_last_error()
+
+
+def test_product_path_fails_loudly_without_library(tmp_path, monkeypatch):
+    import paper_1806_00512_amd.lstmss as lstmss
+    monkeypatch.setattr(lstmss, "_lib", None)
+    monkeypatch.setattr(lstmss, "LIB_PATH", str(tmp_path / "missing.so"))
+    with pytest.raises(RuntimeError):
+        lstmss.load()
