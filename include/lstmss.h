@@ -151,6 +151,25 @@ int32_t lstmss_select_compact(const lstmss_dims *d, float sparsity, const lstmss
                               const void *dG, void *dG_c, int32_t *idx, double *scores,
                               void *stream);
 
+/* Measurement hooks (not part of the method): when enabled, every kernel the
+ * library launches is bracketed by a pair of HIP events recorded on its own
+ * launch stream; lstmss_timing_read synchronises on the recorded events and
+ * returns the summed event-to-event time and the number of launches of one
+ * kernel kind since the last reset.  Timing adds two event records per
+ * launch, so leave it off while timing whole calls.  Not for concurrent use
+ * from several host threads while enabled. */
+enum {
+    LSTMSS_KERNEL_GATES = 0,       /* gate gradient + score/select/compact (or dense) */
+    LSTMSS_KERNEL_DATA_GRAD = 1,   /* [dx; dh] = W_c^T dG_c, split-K partials */
+    LSTMSS_KERNEL_WEIGHT_GRAD = 2, /* dW[kept rows] += dG_c [x; h]^T */
+    LSTMSS_KERNEL_AUX = 3,         /* zero fills, final reductions and copies */
+    LSTMSS_KERNEL_FORWARD = 4,     /* forward step */
+    LSTMSS_KERNEL_KINDS = 5
+};
+int32_t lstmss_timing_enable(int32_t on);
+int32_t lstmss_timing_read(int32_t kind, double *total_ms, int64_t *launches);
+int32_t lstmss_timing_reset(void);
+
 #ifdef __cplusplus
 }
 #endif

@@ -69,6 +69,7 @@ def _load():
     lib.oracle_kept_rows.restype = L
     lib.oracle_removed_in_region.argtypes = [L, i, i]
     lib.oracle_removed_in_region.restype = L
+    lib.oracle_threads.restype = i
     lib.oracle_round_bf16.argtypes = [ctypes.c_double]
     lib.oracle_round_bf16.restype = ctypes.c_double
     lib.oracle_backward.argtypes = [i, i, i, i, P, P, P, P, P, P, P, P, i, i, i, i, P,
@@ -116,6 +117,11 @@ def forward(x, W, b=None, h0=None, c0=None, bf16=False):
                             int(bool(bf16)), _ptr(gates), _ptr(c), _ptr(h))
     _check(rc, "forward")
     return gates, c, h
+
+
+def threads() -> int:
+    """Threads the oracle's parallel loops use."""
+    return int(_load().oracle_threads())
 
 
 def kept_rows(rows: int, P: int, R: int, S: int) -> int:

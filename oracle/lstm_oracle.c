@@ -54,9 +54,23 @@
 #include <stdlib.h>
 #include <string.h>
 
+#ifdef _OPENMP
+#include <omp.h>
+#endif
+
 #define ORACLE_OK 0
 #define ORACLE_EINVAL (-1)
 #define ORACLE_ENOMEM (-3)
+
+/* Number of threads the parallel loops use (1 without OpenMP). */
+int oracle_threads(void)
+{
+#ifdef _OPENMP
+    return omp_get_max_threads();
+#else
+    return 1;
+#endif
+}
 
 /* Round to the nearest bfloat16 value (8 significant bits, fp32 exponent
  * range, subnormal spacing 2^-133), ties to even.  Used only when the

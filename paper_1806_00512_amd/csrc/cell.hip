@@ -22,9 +22,9 @@ constexpr int CELL_THREADS = 256;
 //   df  = dc * c_{t-1} * f (1 - f)      and dc_{t-1} = dc * f
 //   dg  = dc * i * (1 - g^2)
 template <typename TS>
-__device__ __forceinline__ float gate_grad(const CellArgs &a, const TS *gates, int g, long u, int b) {
-    const long B = a.B, H = a.H;
-    const long e = u * B + b;
+__device__ __forceinline__ float gate_grad(const CellArgs &a, const TS *gates, int g, int u, int b) {
+    const int B = a.B, H = a.H;
+    const int e = u * B + b;
     float dh = a.dH_up[e];
     for (int s = 0; s < a.dh_nparts; ++s)
         dh += a.dh_part[s * a.dh_stride + e];
@@ -91,42 +91,63 @@ __global__ __launch_bounds__(CELL_THREADS) void cell_select_kernel(CellArgs a) {
     int *skeep = (int *)(sscore + slices_per_wg);
     int *sslot = skeep + slices_per_wg;
 
-    // Phase 1: gate gradients, one row per wavefront at a time; lane l owns
-    // batch columns l, l+64, ... (the fixed score summation order).
-    for (int lr = wave; lr < nrows; lr += NW) {
-        const long r = row0 + lr;
-        const int g = (int)(r / a.H);
-        const long u = r - (long)g * a.H;
-        double part = 0.0;
-        float rsum = 0.f;
-        for (int b = lane; b < B; b += 64) {
-            float v;
-            if (MODE == CELL_GIVEN)
-                v = st<TS>::load((const TS *)a.dG_in, r * B + b);
-            else
-                v = st<TS>::rnd(gate_grad<TS>(a, gates, g, u, b));
-            if (MODE != CELL_GIVEN && dbg)
+    // Phase 1: gate gradients, element-parallel over the work-group's rows
+    // (all loads of an element are independent, so many are in flight).
+    for (int q = tid; q < nrows * B; q += CELL_THREADS) {
+        const int lr = q / B;
+        const int b = q - lr * B;
+        const int r = (int)row0 + lr;
+        float v;
+        if (MODE == CELL_GIVEN) {
+            v = st<TS>::load((const TS *)a.dG_in, (long)r * B + b);
+        } else {
+            const int g = r / a.H;
+            v = st<TS>::rnd(gate_grad<TS>(a, gates, g, r - g * a.H, b));
+            if (dbg)
                 st<TS>::store(dbg, r * B + b, v);
-            if (MODE == CELL_DENSE) {
-                st<TS>::store(dGc, r * B + b, v);
-            } else {
-                sdG[lr * B + b] = v;
-                part += (double)v * (double)v;
+        }
+        if (MODE == CELL_DENSE)
+            st<TS>::store(dGc, r * B + b, v);
+        sdG[q] = v;
+    }
+    __syncthreads();
+
+    // Phase 1b: per-row sum of squares in the fixed order (partial l sums
+    // b = l, l+64, ... in increasing b; partials combined by index xor 32, 16,
+    // ..., 1).  With B <= 2^k < 64 every partial at index >= 2^k is zero and
+    // adding it is exact, so 2^k lanes per row give the same value; a
+    // wavefront then handles 64 / 2^k rows at once.  Row sums for the bias
+    // gradient ride along.
+    {
+        int lpr = 1;
+        while (lpr < B && lpr < 64)
+            lpr <<= 1;
+        const int rpw = 64 / lpr;
+        const int sub = lane / lpr, sl = lane - sub * lpr;
+        for (int base = wave * rpw; base < nrows; base += NW * rpw) {
+            const int lr = base + sub;
+            double part = 0.0;
+            float rsum = 0.f;
+            if (lr < nrows) {
+                for (int b = sl; b < B; b += 64) {
+                    const float v = sdG[lr * B + b];
+                    part += (double)v * (double)v;
+                    rsum += v;
+                }
             }
-            rsum += v;
-        }
-        for (int off = 32; off >= 1; off >>= 1) {
-            if (MODE != CELL_DENSE)
-                part = part + shfl_xor_f64(part, off);
-            rsum += shfl_xor_f32(rsum, off);
-        }
-        if (lane == 0) {
-            if (MODE == CELL_DENSE) {
-                if (a.db)
-                    a.db[r] += rsum;
-            } else {
-                srowsq[lr] = part;
-                srowsum[lr] = rsum;
+            for (int off = lpr >> 1; off >= 1; off >>= 1) {
+                if (MODE != CELL_DENSE)
+                    part = part + shfl_xor_f64(part, off);
+                rsum += shfl_xor_f32(rsum, off);
+            }
+            if (sl == 0 && lr < nrows) {
+                if (MODE == CELL_DENSE) {
+                    if (a.db)
+                        a.db[row0 + lr] += rsum;
+                } else {
+                    srowsq[lr] = part;
+                    srowsum[lr] = rsum;
+                }
             }
         }
     }
@@ -226,8 +247,7 @@ int grid_for(long n) { return (int)max(1L, min(4096L, ceil_div(n, 256))); }
 } // namespace
 
 size_t cell_lds_bytes(const CellArgs &a, int mode) {
-    if (mode == CELL_DENSE)
-        return 0;
+    (void)mode;
     const size_t spw = (size_t)a.regions_per_wg * a.R;
     const size_t rows = spw * a.P;
     size_t bytes = ((rows * a.B * 4 + 15) & ~(size_t)15);

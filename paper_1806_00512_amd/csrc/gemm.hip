@@ -12,6 +12,8 @@
 // Tiles are 64-wide-wavefront MFMA tiles (32x32 outputs per wave), staged
 // through LDS.  fp32 uses v_mfma_f32_32x32x2f32; bf16 uses
 // v_mfma_f32_32x32x16_bf16 with fp32 accumulation.
+#include <type_traits>
+
 #include "common.h"
 #include "kernels.h"
 
@@ -23,52 +25,155 @@ constexpr int THREADS = 256;
 
 __device__ __forceinline__ uint16_t raw(bf16_t v) { return v.bits; }
 
+// Register staging of one global -> LDS vector: VW elements of a row.
+template <typename TS, bool VEC>
+struct Vec;
+template <>
+struct Vec<float, true> {
+    static constexpr int W = 4;
+    float v[4];
+    __device__ __forceinline__ void load(const float *p, int valid) {
+        if (valid >= 4) {
+            const float4 t = *(const float4 *)p;
+            v[0] = t.x; v[1] = t.y; v[2] = t.z; v[3] = t.w;
+        } else {
+#pragma unroll
+            for (int i = 0; i < 4; ++i)
+                v[i] = i < valid ? p[i] : 0.f;
+        }
+    }
+    __device__ __forceinline__ void zero() { v[0] = v[1] = v[2] = v[3] = 0.f; }
+};
+template <>
+struct Vec<float, false> {
+    static constexpr int W = 1;
+    float v[1];
+    __device__ __forceinline__ void load(const float *p, int valid) { v[0] = valid > 0 ? p[0] : 0.f; }
+    __device__ __forceinline__ void zero() { v[0] = 0.f; }
+};
+template <>
+struct Vec<bf16_t, true> {
+    static constexpr int W = 8;
+    uint16_t v[8];
+    __device__ __forceinline__ void load(const bf16_t *p, int valid) {
+        if (valid >= 8) {
+            const u16x8 t = *(const u16x8 *)p;
+#pragma unroll
+            for (int i = 0; i < 8; ++i)
+                v[i] = t[i];
+        } else {
+#pragma unroll
+            for (int i = 0; i < 8; ++i)
+                v[i] = i < valid ? p[i].bits : (uint16_t)0;
+        }
+    }
+    __device__ __forceinline__ void zero() {
+#pragma unroll
+        for (int i = 0; i < 8; ++i)
+            v[i] = 0;
+    }
+};
+template <>
+struct Vec<bf16_t, false> {
+    static constexpr int W = 1;
+    uint16_t v[1];
+    __device__ __forceinline__ void load(const bf16_t *p, int valid) { v[0] = valid > 0 ? p[0].bits : (uint16_t)0; }
+    __device__ __forceinline__ void zero() { v[0] = 0; }
+};
+
 // --------------------------------------------------------------------------
 // Data gradient: part[z][m][n] = sum over k in split z of W[row(k)][m] G[k][n]
 // where row(k) = idx[k/P]*P + k%P (kept rows) or k (dense).
-// Work-group tile TM x TN (4 waves, 32x32 each), K staged TK at a time.
+// Work-group tile TM x TN (4 waves, 32x32 each), K staged TK at a time with
+// the next K tile prefetched into registers while MFMAs run on the current
+// one.  The gathered W row of every k of the split is looked up once into
+// LDS.
 // --------------------------------------------------------------------------
-template <typename TS, int TN, bool GATHER>
+constexpr int GEMM1_KC_MAX = 4096;
+
+template <typename TS, int TN, bool GATHER, bool VEC>
 __global__ __launch_bounds__(THREADS) void gemm1_kernel(Gemm1Args a) {
     constexpr int TM = 4096 / TN;
     constexpr int TK = GEMM1_TK;
     constexpr int WM = TM / 32;
+    using V = Vec<TS, VEC>;
+    constexpr int VW = V::W;
+    constexpr int NA = TK * TM / VW, NB = TK * TN / VW;
+    constexpr int RA = (NA + THREADS - 1) / THREADS, RB = (NB + THREADS - 1) / THREADS;
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int wm = wave % WM, wn = wave / WM;
     const int mm0 = blockIdx.x * TM;
     const int n0 = blockIdx.y * TN;
-    const long kb = blockIdx.z * a.k_chunk;
-    const long ke = min(a.Kp, kb + a.k_chunk);
-    const int M = a.M, N = a.N;
+    const int kb = blockIdx.z * (int)a.k_chunk;
+    const int ke = min((int)a.Kp, kb + (int)a.k_chunk);
+    const int M = a.M, N = a.N, ldw = (int)a.ldw;
     const TS *W = (const TS *)a.W;
     const TS *G = (const TS *)a.Gc;
+
+    __shared__ int srow[GEMM1_KC_MAX];
+    for (int i = tid; i < ke - kb; i += THREADS) {
+        const int k = kb + i;
+        srow[i] = GATHER ? a.idx[k / a.P] * a.P + k % a.P : k;
+    }
+
+    V ra[RA], rb[RB];
+    auto load = [&](int k0) {
+#pragma unroll
+        for (int i = 0; i < RA; ++i) {
+            const int q = tid + i * THREADS;
+            const int kk = q / (TM / VW), mm = (q % (TM / VW)) * VW;
+            const int k = k0 + kk, m = a.m_begin + mm0 + mm;
+            if (q < NA && k < ke && m < M)
+                ra[i].load(W + (long)srow[k - kb] * ldw + m, M - m);
+            else
+                ra[i].zero();
+        }
+#pragma unroll
+        for (int i = 0; i < RB; ++i) {
+            const int q = tid + i * THREADS;
+            const int kk = q / (TN / VW), nn = (q % (TN / VW)) * VW;
+            const int k = k0 + kk, n = n0 + nn;
+            if (q < NB && k < ke && n < N)
+                rb[i].load(G + (long)k * N + n, N - n);
+            else
+                rb[i].zero();
+        }
+    };
     f32x16 acc;
+#pragma unroll
     for (int v = 0; v < 16; ++v)
         acc[v] = 0.f;
+    __syncthreads();
+    load(kb);
 
     if constexpr (sizeof(TS) == 4) {
         // fp32: LDS as [k][row]; lanes 0-31 read k, lanes 32-63 read k+1.
-        __shared__ float As[TK][TM + 4];
-        __shared__ float Bs[TK][TN + 4];
-        for (long k0 = kb; k0 < ke; k0 += TK) {
-            for (int q = tid; q < TK * TM; q += THREADS) {
-                const int kk = q / TM, mm = q % TM;
-                const long k = k0 + kk;
-                const int m = a.m_begin + mm0 + mm;
-                float v = 0.f;
-                if (k < ke && m < M) {
-                    const long row = GATHER ? (long)a.idx[k / a.P] * a.P + k % a.P : k;
-                    v = W[row * a.ldw + m];
+        __shared__ __align__(16) float As[TK][TM + 4];
+        __shared__ __align__(16) float Bs[TK][TN + 4];
+        for (int k0 = kb; k0 < ke; k0 += TK) {
+#pragma unroll
+            for (int i = 0; i < RA; ++i) {
+                const int q = tid + i * THREADS;
+                if (q < NA) {
+                    const int kk = q / (TM / VW), mm = (q % (TM / VW)) * VW;
+#pragma unroll
+                    for (int e = 0; e < VW; ++e)
+                        As[kk][mm + e] = ra[i].v[e];
                 }
-                As[kk][mm] = v;
             }
-            for (int q = tid; q < TK * TN; q += THREADS) {
-                const int kk = q / TN, nn = q % TN;
-                const long k = k0 + kk;
-                const int n = n0 + nn;
-                Bs[kk][nn] = (k < ke && n < N) ? G[k * N + n] : 0.f;
+#pragma unroll
+            for (int i = 0; i < RB; ++i) {
+                const int q = tid + i * THREADS;
+                if (q < NB) {
+                    const int kk = q / (TN / VW), nn = (q % (TN / VW)) * VW;
+#pragma unroll
+                    for (int e = 0; e < VW; ++e)
+                        Bs[kk][nn + e] = rb[i].v[e];
+                }
             }
             __syncthreads();
+            if (k0 + TK < ke)
+                load(k0 + TK);
 #pragma unroll
             for (int kk = 0; kk < TK; kk += 2) {
                 const float av = As[kk + (lane >> 5)][wm * 32 + (lane & 31)];
@@ -81,25 +186,30 @@ __global__ __launch_bounds__(THREADS) void gemm1_kernel(Gemm1Args a) {
         // bf16: LDS as [row][k] so each lane reads 8 consecutive k (16 bytes).
         __shared__ __align__(16) uint16_t As[TM][TK + 8];
         __shared__ __align__(16) uint16_t Bs[TN][TK + 8];
-        for (long k0 = kb; k0 < ke; k0 += TK) {
-            for (int q = tid; q < TK * TM; q += THREADS) {
-                const int kk = q / TM, mm = q % TM;
-                const long k = k0 + kk;
-                const int m = a.m_begin + mm0 + mm;
-                uint16_t v = 0;
-                if (k < ke && m < M) {
-                    const long row = GATHER ? (long)a.idx[k / a.P] * a.P + k % a.P : k;
-                    v = raw(W[row * a.ldw + m]);
+        for (int k0 = kb; k0 < ke; k0 += TK) {
+#pragma unroll
+            for (int i = 0; i < RA; ++i) {
+                const int q = tid + i * THREADS;
+                if (q < NA) {
+                    const int kk = q / (TM / VW), mm = (q % (TM / VW)) * VW;
+#pragma unroll
+                    for (int e = 0; e < VW; ++e)
+                        As[mm + e][kk] = ra[i].v[e];
                 }
-                As[mm][kk] = v;
             }
-            for (int q = tid; q < TK * TN; q += THREADS) {
-                const int kk = q / TN, nn = q % TN;
-                const long k = k0 + kk;
-                const int n = n0 + nn;
-                Bs[nn][kk] = (k < ke && n < N) ? raw(G[k * N + n]) : (uint16_t)0;
+#pragma unroll
+            for (int i = 0; i < RB; ++i) {
+                const int q = tid + i * THREADS;
+                if (q < NB) {
+                    const int kk = q / (TN / VW), nn = (q % (TN / VW)) * VW;
+#pragma unroll
+                    for (int e = 0; e < VW; ++e)
+                        Bs[nn + e][kk] = rb[i].v[e];
+                }
             }
             __syncthreads();
+            if (k0 + TK < ke)
+                load(k0 + TK);
 #pragma unroll
             for (int kk = 0; kk < TK; kk += 16) {
                 const u16x8 av = *(const u16x8 *)&As[wm * 32 + (lane & 31)][kk + 8 * (lane >> 5)];
@@ -203,6 +313,245 @@ __global__ __launch_bounds__(THREADS) void gemm2_kernel(Gemm2Args a) {
             const long row = SCATTER ? (long)a.idx[m / a.P] * a.P + m % a.P : m;
             float *p = a.dW + row * NC + n;
             *p += acc[v];
+        }
+    }
+}
+
+// --------------------------------------------------------------------------
+// Weight gradient of all time steps in one launch.
+//
+// Work-group: one group of output rows x 128 features (4 waves x 32).  It
+// walks every time step (and batch chunk) and owns its dW tile, so dW is
+// written once, in a fixed summation order (deterministic, no atomics).
+//
+// Dense: a group is 32 consecutive rows; each step's product is added to the
+// accumulator.
+// Sparse: a group is `greg` consecutive regions.  Every full region keeps
+// exactly (R-S)*P rows, so at every step the group's kept rows are the same
+// contiguous range of compacted rows (at most 32*TT of them).  The MFMA
+// accumulates those into a temporary tile whose columns are kept rows; after
+// the step each accumulator column (an original row) pulls its value from the
+// temporary column holding it (ds_bpermute across lanes of the same half),
+// or nothing if its slice was dropped at that step.  The MFMA work is thus
+// only the kept rows' (no zero-filled rows).
+//
+// MFMA operands: A = [x_t; h_{t-1}] rows (features), B = gate-gradient rows;
+// accumulator column = row of dW (lane), accumulator rows = features.  Lanes
+// 0-31 consume batch columns [0, BC/2) of the chunk and lanes 32-63
+// [BC/2, BC), so each lane reads consecutive columns from LDS.
+// --------------------------------------------------------------------------
+constexpr int WG_FEAT = 128;
+constexpr int WG_BCMAX = 64;
+constexpr int WG_ATMAX = 4;
+
+template <typename TS, bool SPARSE, int TT, bool VEC>
+__global__ __launch_bounds__(THREADS) void wgrad_kernel(WgradArgs a) {
+    using E = typename std::conditional<sizeof(TS) == 4, float, uint16_t>::type;
+    constexpr int PITCH = WG_BCMAX + (sizeof(TS) == 4 ? 4 : 8);
+    constexpr int GROWS = TT * 32;
+    using V = Vec<TS, VEC>;
+    constexpr int VW = V::W;
+    constexpr int RG = (GROWS * WG_BCMAX / VW + THREADS - 1) / THREADS;
+    constexpr int RX = (WG_FEAT * WG_BCMAX / VW + THREADS - 1) / THREADS;
+    __shared__ __align__(16) E sX[WG_FEAT][PITCH];
+    __shared__ __align__(16) E sG[GROWS][PITCH];
+    __shared__ int sidx[64];
+
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int T = a.T, I = a.I, H = a.H, B = a.B, BC = a.BC;
+    const int NC = I + H, G4 = 4 * H;
+    const int n0 = blockIdx.y * WG_FEAT;
+    const TS *Gc = (const TS *)a.Gc;
+    const TS *x = (const TS *)a.x;
+    const TS *h = (const TS *)a.h;
+
+    // group geometry
+    int r0, rcount, c0, ccount, q0 = 0, qcount = 0, j0 = 0;
+    const int rp = a.R * a.P, kr = (a.R - a.S) * a.P, ks = a.R - a.S;
+    if (SPARSE) {
+        const int g = blockIdx.x;
+        r0 = g * a.greg * rp;
+        rcount = min(a.greg * rp, G4 - r0);
+        c0 = g * a.greg * kr;
+        ccount = min(a.greg * kr, a.Kp - c0);
+        q0 = g * a.greg * ks;
+        qcount = min(a.greg * ks, a.kept - q0);
+        j0 = g * a.greg * a.R;
+    } else {
+        r0 = blockIdx.x * 32;
+        rcount = min(32, G4 - r0);
+        c0 = r0;
+        ccount = rcount;
+    }
+    const int AT = SPARSE ? (rcount + 31) / 32 : 1;
+
+    const int nbc = (B + BC - 1) / BC;
+    const int niters = T * nbc;
+    const int gvec = GROWS * BC / VW, xvec = WG_FEAT * BC / VW, cpr = BC / VW;
+
+    V rg[RG], rx[RX];
+    int ridx = -1;
+    auto load = [&](int it) {
+        const int t = it / nbc, b0 = (it - t * nbc) * BC;
+        const TS *Gt = Gc + (long)t * a.Kp * B;
+#pragma unroll
+        for (int i = 0; i < RG; ++i) {
+            const int q = tid + i * THREADS;
+            const int rho = q / cpr, bb = (q - rho * cpr) * VW;
+            const int b = b0 + bb;
+            if (q < gvec && rho < ccount && b < B)
+                rg[i].load(Gt + (long)(c0 + rho) * B + b, B - b);
+            else
+                rg[i].zero();
+        }
+#pragma unroll
+        for (int i = 0; i < RX; ++i) {
+            const int q = tid + i * THREADS;
+            const int f = q / cpr, bb = (q - f * cpr) * VW;
+            const int n = n0 + f, b = b0 + bb;
+            if (q < xvec && n < NC && b < B) {
+                const TS *src = n < I ? x + ((long)t * I + n) * B : h + ((long)t * H + (n - I)) * B;
+                rx[i].load(src + b, B - b);
+            } else {
+                rx[i].zero();
+            }
+        }
+        if (SPARSE && b0 == 0 && tid < qcount)
+            ridx = a.idx[(long)t * a.kept + q0 + tid];
+    };
+
+    f32x16 acc[WG_ATMAX], tmp[TT];
+#pragma unroll
+    for (int j = 0; j < WG_ATMAX; ++j)
+#pragma unroll
+        for (int v = 0; v < 16; ++v)
+            acc[j][v] = 0.f;
+#pragma unroll
+    for (int j = 0; j < TT; ++j)
+#pragma unroll
+        for (int v = 0; v < 16; ++v)
+            tmp[j][v] = 0.f;
+
+    load(0);
+    const int hb = (lane >> 5) * (BC >> 1);
+    const int frow = wave * 32 + (lane & 31);
+    for (int it = 0; it < niters; ++it) {
+        const int bc = it % nbc;
+        // registers -> LDS
+#pragma unroll
+        for (int i = 0; i < RG; ++i) {
+            const int q = tid + i * THREADS;
+            if (q < gvec) {
+                const int rho = q / cpr, bb = (q - rho * cpr) * VW;
+#pragma unroll
+                for (int e = 0; e < VW; ++e)
+                    sG[rho][bb + e] = rg[i].v[e];
+            }
+        }
+#pragma unroll
+        for (int i = 0; i < RX; ++i) {
+            const int q = tid + i * THREADS;
+            if (q < xvec) {
+                const int f = q / cpr, bb = (q - f * cpr) * VW;
+#pragma unroll
+                for (int e = 0; e < VW; ++e)
+                    sX[f][bb + e] = rx[i].v[e];
+            }
+        }
+        if (SPARSE && bc == 0 && tid < qcount)
+            sidx[tid] = ridx;
+        __syncthreads();
+        if (it + 1 < niters)
+            load(it + 1);
+
+        // MFMA over this batch chunk
+        if constexpr (sizeof(TS) == 4) {
+            for (int s4 = 0; s4 < (BC >> 1); s4 += 4) {
+                const float4 av = *(const float4 *)&sX[frow][hb + s4];
+#pragma unroll
+                for (int tt = 0; tt < TT; ++tt) {
+                    const float4 bv = *(const float4 *)&sG[tt * 32 + (lane & 31)][hb + s4];
+                    f32x16 &c = tmp[tt];
+                    c = mfma32x32x2(av.x, bv.x, c);
+                    c = mfma32x32x2(av.y, bv.y, c);
+                    c = mfma32x32x2(av.z, bv.z, c);
+                    c = mfma32x32x2(av.w, bv.w, c);
+                }
+            }
+        } else {
+            for (int s8 = 0; s8 < (BC >> 1); s8 += 8) {
+                const u16x8 av = *(const u16x8 *)&sX[frow][hb + s8];
+#pragma unroll
+                for (int tt = 0; tt < TT; ++tt) {
+                    const u16x8 bv = *(const u16x8 *)&sG[tt * 32 + (lane & 31)][hb + s8];
+                    f32x16 &c = tmp[tt];
+                    c = mfma32x32x16bf(av, bv, c);
+                }
+            }
+        }
+
+        // dense: add this step's product; sparse: route this step's kept rows
+        // into their original rows (same summation order either way, so a
+        // sparse call that keeps every row matches the dense one bit for bit)
+        if (!SPARSE && bc == nbc - 1) {
+#pragma unroll
+            for (int v = 0; v < 16; ++v) {
+                acc[0][v] += tmp[0][v];
+                tmp[0][v] = 0.f;
+            }
+        }
+        if (SPARSE && bc == nbc - 1) {
+#pragma unroll
+            for (int at = 0; at < WG_ATMAX; ++at) {
+                if (at >= AT)
+                    break;
+                const int col = at * 32 + (lane & 31);
+                int src = -1;
+                if (col < rcount) {
+                    const int orow = r0 + col;
+                    const int js = orow / a.P;              // global slice
+                    const int reg = (js - j0) / a.R;        // region within the group
+                    const int e0 = reg * ks, e1 = min(e0 + ks, qcount);
+                    for (int e = e0; e < e1; ++e)
+                        if (sidx[e] == js)
+                            src = e * a.P + (orow - js * a.P);
+                }
+                const int saddr = (((src < 0 ? 0 : src) & 31) + (lane & 32)) << 2;
+                const int stile = src < 0 ? 0 : (src >> 5);
+#pragma unroll
+                for (int v = 0; v < 16; ++v) {
+                    float val = __int_as_float(__builtin_amdgcn_ds_bpermute(saddr, __float_as_int(tmp[0][v])));
+                    if (TT > 1) {
+                        const float v1 = __int_as_float(
+                            __builtin_amdgcn_ds_bpermute(saddr, __float_as_int(tmp[TT > 1 ? 1 : 0][v])));
+                        val = stile == 1 ? v1 : val;
+                    }
+                    acc[at][v] += src < 0 ? 0.f : val;
+                }
+            }
+#pragma unroll
+            for (int tt = 0; tt < TT; ++tt)
+#pragma unroll
+                for (int v = 0; v < 16; ++v)
+                    tmp[tt][v] = 0.f;
+        }
+        __syncthreads();
+    }
+
+    // write the owned tile of dW
+#pragma unroll
+    for (int at = 0; at < WG_ATMAX; ++at) {
+        if (at >= AT)
+            break;
+        const int col = at * 32 + (lane & 31);
+        if (col >= rcount)
+            continue;
+        float *dst = a.dW + (long)(r0 + col) * NC;
+#pragma unroll
+        for (int v = 0; v < 16; ++v) {
+            const int f = n0 + wave * 32 + acc_row(lane, v);
+            if (f < NC)
+                dst[f] = acc[at][v];
         }
     }
 }
@@ -323,16 +672,23 @@ int gemm1_tm(int N) { return 4096 / gemm1_tn(N); }
 
 hipError_t launch_gemm1(const Gemm1Args &a, bool bf16, hipStream_t s) {
     const int TN = gemm1_tn(a.N), TM = 4096 / TN;
+    if (a.k_chunk > GEMM1_KC_MAX || a.k_chunk % GEMM1_TK != 0)
+        return hipErrorInvalidValue;
     dim3 grid((unsigned)ceil_div(a.M - a.m_begin, TM), (unsigned)ceil_div(a.N, TN), (unsigned)a.splitk);
     const bool gather = a.idx != nullptr;
-#define LSTMSS_G1(TS, TNV, GA) hipLaunchKernelGGL((gemm1_kernel<TS, TNV, GA>), grid, dim3(THREADS), 0, s, a)
+    // 16-byte vector loads need 16-byte aligned rows and column offsets
+    const int vw = bf16 ? 8 : 4;
+    const bool vec = a.ldw % vw == 0 && a.m_begin % vw == 0 && a.N % vw == 0;
+#define LSTMSS_G1(TS, TNV, GA, VE) hipLaunchKernelGGL((gemm1_kernel<TS, TNV, GA, VE>), grid, dim3(THREADS), 0, s, a)
+#define LSTMSS_G1V(TS, TNV, GA) do { if (vec) LSTMSS_G1(TS, TNV, GA, true); else LSTMSS_G1(TS, TNV, GA, false); } while (0)
     if (bf16) {
-        if (TN == 32) { if (gather) LSTMSS_G1(bf16_t, 32, true); else LSTMSS_G1(bf16_t, 32, false); }
-        else { if (gather) LSTMSS_G1(bf16_t, 64, true); else LSTMSS_G1(bf16_t, 64, false); }
+        if (TN == 32) { if (gather) LSTMSS_G1V(bf16_t, 32, true); else LSTMSS_G1V(bf16_t, 32, false); }
+        else { if (gather) LSTMSS_G1V(bf16_t, 64, true); else LSTMSS_G1V(bf16_t, 64, false); }
     } else {
-        if (TN == 32) { if (gather) LSTMSS_G1(float, 32, true); else LSTMSS_G1(float, 32, false); }
-        else { if (gather) LSTMSS_G1(float, 64, true); else LSTMSS_G1(float, 64, false); }
+        if (TN == 32) { if (gather) LSTMSS_G1V(float, 32, true); else LSTMSS_G1V(float, 32, false); }
+        else { if (gather) LSTMSS_G1V(float, 64, true); else LSTMSS_G1V(float, 64, false); }
     }
+#undef LSTMSS_G1V
 #undef LSTMSS_G1
     return hipGetLastError();
 }
@@ -344,6 +700,50 @@ hipError_t launch_gemm2(const Gemm2Args &a, bool bf16, hipStream_t s) {
     if (bf16) { if (scatter) LSTMSS_G2(bf16_t, true); else LSTMSS_G2(bf16_t, false); }
     else { if (scatter) LSTMSS_G2(float, true); else LSTMSS_G2(float, false); }
 #undef LSTMSS_G2
+    return hipGetLastError();
+}
+
+// Temporary tiles (kept rows per group / 32) and accumulator tiles (original
+// rows per group / 32) of the sparse weight-gradient kernel.
+static void wgrad_tiles(int P, int R, int S, int *greg, int *tt, int *at) {
+    const int kr = (R - S) * P, rp = R * P;
+    *greg = kr <= 32 ? max(1, 32 / kr) : 1;
+    *tt = (*greg * kr + 31) / 32;
+    *at = (*greg * rp + 31) / 32;
+}
+
+bool wgrad_supported(int P, int R, int S) {
+    int greg, tt, at;
+    wgrad_tiles(P, R, S, &greg, &tt, &at);
+    return tt <= 2 && at <= WG_ATMAX && (R - S) <= 64;
+}
+
+hipError_t launch_wgrad(WgradArgs a, bool sparse, bool bf16, hipStream_t s) {
+    int tt = 1, at = 1;
+    if (sparse) {
+        if (!wgrad_supported(a.P, a.R, a.S))
+            return hipErrorNotSupported;
+        wgrad_tiles(a.P, a.R, a.S, &a.greg, &tt, &at);
+    }
+    const int step = bf16 ? 32 : 8;
+    a.BC = (int)min((long)WG_BCMAX, ceil_div(a.B, step) * step);
+    const int vw = bf16 ? 8 : 4;
+    const bool vec = a.B % vw == 0;
+    const long groups = sparse ? ceil_div(ceil_div(4L * a.H / a.P, a.R), a.greg) : ceil_div(4L * a.H, 32);
+    dim3 grid((unsigned)groups, (unsigned)ceil_div(a.I + a.H, WG_FEAT));
+#define LSTMSS_WG(TS, SP, TTV, VE) hipLaunchKernelGGL((wgrad_kernel<TS, SP, TTV, VE>), grid, dim3(THREADS), 0, s, a)
+#define LSTMSS_WGV(TS, SP, TTV) do { if (vec) LSTMSS_WG(TS, SP, TTV, true); else LSTMSS_WG(TS, SP, TTV, false); } while (0)
+    if (bf16) {
+        if (!sparse) LSTMSS_WGV(bf16_t, false, 1);
+        else if (tt == 1) LSTMSS_WGV(bf16_t, true, 1);
+        else LSTMSS_WGV(bf16_t, true, 2);
+    } else {
+        if (!sparse) LSTMSS_WGV(float, false, 1);
+        else if (tt == 1) LSTMSS_WGV(float, true, 1);
+        else LSTMSS_WGV(float, true, 2);
+    }
+#undef LSTMSS_WGV
+#undef LSTMSS_WG
     return hipGetLastError();
 }
 

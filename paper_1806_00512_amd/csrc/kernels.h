@@ -68,6 +68,22 @@ struct Gemm2Args {
     float *dW;             // [4H][I+H]
 };
 
+// Weight gradient of the whole sequence in one launch:
+//   dW = sum_t dG_t [x_t; h_{t-1}]^T   (dense: every row; sparse: the kept
+//   rows of each step are accumulated into their original rows).
+struct WgradArgs {
+    const void *Gc;        // [T][Kp][B] compacted gate gradients of every step
+    const int32_t *idx;    // [T][kept] kept slice indices (sparse) or NULL
+    const void *x;         // [T][I][B]
+    const void *h;         // [T+1][H][B] (step t reads h[t] = h_{t-1})
+    int T, I, H, B;
+    int Kp, kept;          // kept rows / kept slices per step
+    int P, R, S;
+    int greg;              // regions per work-group group (sparse)
+    int BC;                // batch columns staged per iteration
+    float *dW;             // [4H][I+H], written (not accumulated)
+};
+
 // One forward step: a = W [x_t; h_{t-1}] + b, activations, cell update.
 struct FwdArgs {
     const void *W;
@@ -86,6 +102,10 @@ hipError_t launch_cell(const CellArgs &a, int mode, bool bf16, hipStream_t s);
 size_t cell_lds_bytes(const CellArgs &a, int mode);
 hipError_t launch_gemm1(const Gemm1Args &a, bool bf16, hipStream_t s);
 hipError_t launch_gemm2(const Gemm2Args &a, bool bf16, hipStream_t s);
+// Returns hipErrorNotSupported when the structure needs more routing tiles
+// than the batched kernel holds (the caller then uses launch_gemm2 per step).
+hipError_t launch_wgrad(WgradArgs a, bool sparse, bool bf16, hipStream_t s);
+bool wgrad_supported(int P, int R, int S);
 hipError_t launch_fwd_step(const FwdArgs &a, bool bf16, hipStream_t s);
 hipError_t launch_fill(float *p, long n, float v, hipStream_t s);
 hipError_t launch_copy_in(float *dst, const float *src, long n, hipStream_t s); // src NULL -> zero

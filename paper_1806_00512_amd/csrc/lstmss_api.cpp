@@ -7,7 +7,9 @@
 #include <cstdarg>
 #include <cstdio>
 #include <cstring>
+#include <mutex>
 #include <string>
+#include <vector>
 
 #include "../../include/lstmss.h"
 #include "kernels.h"
@@ -36,11 +38,57 @@ int32_t fail(int32_t code, const char *fmt, ...) {
             return fail(LSTMSS_ERR_HIP, "%s failed: %s", #expr, hipGetErrorString(e_));        \
     } while (0)
 
+// Optional per-kernel timing with HIP events recorded on the launch stream
+// around every kernel of a given kind (enabled by lstmss_timing_enable).
+struct TimingRec {
+    int kind;
+    hipEvent_t a, b;
+};
+std::mutex g_tmu;
+bool g_timing = false;
+std::vector<TimingRec> g_pending;
+std::vector<hipEvent_t> g_event_pool;
+double g_total_ms[LSTMSS_KERNEL_KINDS];
+int64_t g_count[LSTMSS_KERNEL_KINDS];
+
+hipEvent_t pooled_event() {
+    if (!g_event_pool.empty()) {
+        hipEvent_t e = g_event_pool.back();
+        g_event_pool.pop_back();
+        return e;
+    }
+    hipEvent_t e = nullptr;
+    if (hipEventCreate(&e) != hipSuccess)
+        return nullptr;
+    return e;
+}
+
+template <class F>
+hipError_t timed(int kind, hipStream_t st, F &&launch) {
+    if (!g_timing)
+        return launch();
+    std::lock_guard<std::mutex> lk(g_tmu);
+    hipEvent_t a = pooled_event(), b = pooled_event();
+    if (!a || !b)
+        return hipErrorOutOfMemory;
+    hipError_t e = hipEventRecord(a, st);
+    if (e != hipSuccess)
+        return e;
+    e = launch();
+    if (e != hipSuccess)
+        return e;
+    e = hipEventRecord(b, st);
+    g_pending.push_back({kind, a, b});
+    return e;
+}
+
 size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
 long ceil_div(long a, long b) { return (a + b - 1) / b; }
 
 // LDS budget of the fused gate-gradient / selection kernel's work-group.
 constexpr size_t kMaxLds = 64 * 1024;
+// Largest K range one data-gradient work-group covers (its LDS row table).
+constexpr long kGemm1KcMax = 4096;
 
 int elem_bytes(int32_t dtype) { return dtype == LSTMSS_BF16 ? 2 : 4; }
 
@@ -54,6 +102,8 @@ int32_t check_dims(const lstmss_dims *d) {
         return fail(LSTMSS_ERR_UNSUPPORTED, "unknown dtype %d", d->dtype);
     // 32-bit row indices inside the kernels
     if ((int64_t)4 * d->H * ((int64_t)d->I + d->H) >= ((int64_t)1 << 31) ||
+        (int64_t)4 * d->H * d->B >= ((int64_t)1 << 31) ||
+        ((int64_t)d->I + d->H) * d->B >= ((int64_t)1 << 31) ||
         (int64_t)d->T * 4 * d->H * d->B >= ((int64_t)1 << 40))
         return fail(LSTMSS_ERR_UNSUPPORTED, "sizes too large");
     return LSTMSS_OK;
@@ -145,7 +195,7 @@ WsLayout ws_layout(const lstmss_dims *d, const Plan &p) {
     const size_t es = elem_bytes(d->dtype);
     const size_t HB = (size_t)d->H * d->B;
     WsLayout L;
-    L.splitk = splitk_for(d, p.Kp);
+    L.splitk = std::max<int>(splitk_for(d, p.Kp), (int)ceil_div(p.Kp, kGemm1KcMax));
     L.k_chunk = ceil_div(ceil_div(p.Kp, L.splitk), GEMM1_TK) * GEMM1_TK;
     L.splitk = (int)ceil_div(p.Kp, L.k_chunk);
     size_t off = 0;
@@ -194,8 +244,12 @@ int32_t backward(const lstmss_dims *d, bool dense, float sparsity, const lstmss_
     int32_t *idx_all = idx_out ? idx_out : (int32_t *)(wb + L.idx);
     float *dbp = db ? db : (float *)(wb + L.db);
 
-    HIP_TRY(launch_fill(dW, G * K, 0.f, st));
-    HIP_TRY(launch_fill(dbp, G, 0.f, st));
+    // weight gradient: one batched launch after the time loop when the
+    // structure fits its routing tiles, else a per-step accumulation
+    const bool batched = !sparse || wgrad_supported(p.P, p.R, p.S);
+    if (!batched)
+        HIP_TRY(timed(LSTMSS_KERNEL_AUX, st, [&] { return launch_fill(dW, G * K, 0.f, st); }));
+    HIP_TRY(timed(LSTMSS_KERNEL_AUX, st, [&] { return launch_fill(dbp, G, 0.f, st); }));
 
     const long part_stride = K * B;
     const int m_begin = dX ? 0 : I;
@@ -245,27 +299,36 @@ int32_t backward(const lstmss_dims *d, bool dense, float sparsity, const lstmss_
         }
         if (cell_lds_bytes(ca, sparse ? CELL_SPARSE : CELL_DENSE) > kMaxLds)
             return fail(LSTMSS_ERR_UNSUPPORTED, "R*P*B too large for one work-group's LDS");
-        HIP_TRY(launch_cell(ca, sparse ? CELL_SPARSE : CELL_DENSE, bf16, st));
+        HIP_TRY(timed(LSTMSS_KERNEL_GATES, st, [&] { return launch_cell(ca, sparse ? CELL_SPARSE : CELL_DENSE, bf16, st); }));
 
         Gemm1Args g1{};
         g1.W = W; g1.ldw = K; g1.Gc = dGc; g1.idx = sparse ? idx : nullptr; g1.P = p.P;
         g1.Kp = p.Kp; g1.M = (int)K; g1.m_begin = m_begin; g1.N = B;
         g1.part = part; g1.part_stride = part_stride; g1.splitk = L.splitk; g1.k_chunk = L.k_chunk;
-        HIP_TRY(launch_gemm1(g1, bf16, st));
+        HIP_TRY(timed(LSTMSS_KERNEL_DATA_GRAD, st, [&] { return launch_gemm1(g1, bf16, st); }));
 
-        Gemm2Args g2{};
-        g2.Gc = dGc; g2.idx = sparse ? idx : nullptr; g2.P = p.P; g2.Kp = p.Kp;
-        g2.xt = (const char *)x + (size_t)t * I * B * es;
-        g2.hp = hst + (size_t)t * HB * es;
-        g2.I = I; g2.H = H; g2.B = B; g2.dW = dW;
-        HIP_TRY(launch_gemm2(g2, bf16, st));
+        if (!batched) {
+            Gemm2Args g2{};
+            g2.Gc = dGc; g2.idx = sparse ? idx : nullptr; g2.P = p.P; g2.Kp = p.Kp;
+            g2.xt = (const char *)x + (size_t)t * I * B * es;
+            g2.hp = hst + (size_t)t * HB * es;
+            g2.I = I; g2.H = H; g2.B = B; g2.dW = dW;
+            HIP_TRY(timed(LSTMSS_KERNEL_WEIGHT_GRAD, st, [&] { return launch_gemm2(g2, bf16, st); }));
+        }
+    }
+    if (batched) {
+        WgradArgs wg{};
+        wg.Gc = dGc_all; wg.idx = sparse ? idx_all : nullptr; wg.x = x; wg.h = hst;
+        wg.T = T; wg.I = I; wg.H = H; wg.B = B; wg.Kp = (int)p.Kp; wg.kept = (int)p.kept;
+        wg.P = p.P; wg.R = p.R; wg.S = p.S; wg.dW = dW;
+        HIP_TRY(timed(LSTMSS_KERNEL_WEIGHT_GRAD, st, [&] { return launch_wgrad(wg, sparse, bf16, st); }));
     }
     if (dX)
-        HIP_TRY(launch_reduce_parts(dX, part, L.splitk, part_stride, (long)I * B, st));
+        HIP_TRY(timed(LSTMSS_KERNEL_AUX, st, [&] { return launch_reduce_parts(dX, part, L.splitk, part_stride, (long)I * B, st); }));
     if (dh0)
-        HIP_TRY(launch_reduce_parts(dh0, part + (size_t)I * B, L.splitk, part_stride, HB, st));
+        HIP_TRY(timed(LSTMSS_KERNEL_AUX, st, [&] { return launch_reduce_parts(dh0, part + (size_t)I * B, L.splitk, part_stride, HB, st); }));
     if (dc0)
-        HIP_TRY(launch_copy_in(dc0, dcbuf[0], HB, st));
+        HIP_TRY(timed(LSTMSS_KERNEL_AUX, st, [&] { return launch_copy_in(dc0, dcbuf[0], HB, st); }));
     return LSTMSS_OK;
 }
 
@@ -346,7 +409,7 @@ int32_t lstm_fwd_cache(const lstmss_dims *d, const void *x, const void *W, const
         f.cn = cst + (size_t)(t + 1) * HB;
         f.hn = hst + (size_t)(t + 1) * HB * es;
         f.hout = h_out ? (char *)h_out + (size_t)t * HB * es : nullptr;
-        HIP_TRY(launch_fwd_step(f, bf16, st));
+        HIP_TRY(timed(LSTMSS_KERNEL_FORWARD, st, [&] { return launch_fwd_step(f, bf16, st); }));
     }
     return LSTMSS_OK;
 }
@@ -392,7 +455,47 @@ int32_t lstmss_select_compact(const lstmss_dims *d, float sparsity, const lstmss
     if (cell_lds_bytes(ca, CELL_GIVEN) > kMaxLds)
         return fail(LSTMSS_ERR_UNSUPPORTED, "R*P*B too large for one work-group's LDS");
     hipStream_t st = (hipStream_t)stream;
-    HIP_TRY(launch_cell(ca, CELL_GIVEN, d->dtype == LSTMSS_BF16, st));
+    HIP_TRY(timed(LSTMSS_KERNEL_GATES, st, [&] { return launch_cell(ca, CELL_GIVEN, d->dtype == LSTMSS_BF16, st); }));
+    return LSTMSS_OK;
+}
+
+int32_t lstmss_timing_enable(int32_t on) {
+    std::lock_guard<std::mutex> lk(g_tmu);
+    g_timing = on != 0;
+    return LSTMSS_OK;
+}
+
+int32_t lstmss_timing_read(int32_t kind, double *total_ms, int64_t *launches) {
+    if (kind < 0 || kind >= LSTMSS_KERNEL_KINDS || !total_ms || !launches)
+        return fail(LSTMSS_ERR_INVALID_ARG, "bad timing query");
+    std::lock_guard<std::mutex> lk(g_tmu);
+    for (const TimingRec &r : g_pending) {
+        float ms = 0.f;
+        HIP_TRY(hipEventSynchronize(r.b));
+        HIP_TRY(hipEventElapsedTime(&ms, r.a, r.b));
+        g_total_ms[r.kind] += ms;
+        g_count[r.kind] += 1;
+        g_event_pool.push_back(r.a);
+        g_event_pool.push_back(r.b);
+    }
+    g_pending.clear();
+    *total_ms = g_total_ms[kind];
+    *launches = g_count[kind];
+    return LSTMSS_OK;
+}
+
+int32_t lstmss_timing_reset(void) {
+    std::lock_guard<std::mutex> lk(g_tmu);
+    for (const TimingRec &r : g_pending) {
+        (void)hipEventSynchronize(r.b);
+        g_event_pool.push_back(r.a);
+        g_event_pool.push_back(r.b);
+    }
+    g_pending.clear();
+    for (int k = 0; k < LSTMSS_KERNEL_KINDS; ++k) {
+        g_total_ms[k] = 0.0;
+        g_count[k] = 0;
+    }
     return LSTMSS_OK;
 }
 

@@ -31,7 +31,10 @@ ERR = {0: "ok", -1: "invalid argument", -2: "unsupported", -3: "workspace too sm
 # Exported symbols of include/lstmss.h
 SYMBOLS = ("lstmss_version", "lstmss_strerror", "lstmss_last_error", "lstmss_cache_bytes",
            "lstmss_kept_rows", "lstmss_workspace_bytes", "lstm_fwd_cache", "lstm_bwd_dense",
-           "lstm_bwd_structsparse", "lstmss_select_compact")
+           "lstm_bwd_structsparse", "lstmss_select_compact", "lstmss_timing_enable",
+           "lstmss_timing_read", "lstmss_timing_reset")
+KERNEL_KINDS = {"gates_select_compact": 0, "data_grad_gemm": 1, "weight_grad_gemm": 2, "aux": 3,
+                "forward_step": 4}
 
 
 class Dims(ctypes.Structure):
@@ -83,6 +86,12 @@ def load():
     lib.lstm_bwd_structsparse.restype = i32
     lib.lstmss_select_compact.argtypes = [pd, f, ps, vp, vp, vp, vp, vp]
     lib.lstmss_select_compact.restype = i32
+    lib.lstmss_timing_enable.argtypes = [i32]
+    lib.lstmss_timing_enable.restype = i32
+    lib.lstmss_timing_read.argtypes = [i32, ctypes.POINTER(ctypes.c_double),
+                                       ctypes.POINTER(ctypes.c_int64)]
+    lib.lstmss_timing_read.restype = i32
+    lib.lstmss_timing_reset.restype = i32
     _lib = lib
     return lib
 
@@ -277,3 +286,22 @@ def cache_views(cache, T, B, H, dtype):
     c = cache[c_off:c_off + c_bytes].view(torch.float32).view(T + 1, H, B)
     h = cache[h_off:h_off + (T + 1) * H * B * es].view(st).view(T + 1, H, B)
     return gates, c, h
+
+
+def timing_enable(on: bool = True):
+    _check(load().lstmss_timing_enable(1 if on else 0), "lstmss_timing_enable")
+
+
+def timing_reset():
+    _check(load().lstmss_timing_reset(), "lstmss_timing_reset")
+
+
+def timing_read():
+    """{kernel kind: (total ms, launches)} accumulated since the last reset."""
+    out = {}
+    for name, k in KERNEL_KINDS.items():
+        ms, n = ctypes.c_double(0), ctypes.c_int64(0)
+        _check(load().lstmss_timing_read(k, ctypes.byref(ms), ctypes.byref(n)),
+               "lstmss_timing_read")
+        out[name] = (ms.value, n.value)
+    return out

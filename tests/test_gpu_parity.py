@@ -176,6 +176,8 @@ def test_select_nan_is_kept(L):
     (3, 16, 33, 40, 0.75, 4, False),
     (2, 1, 8, 8, 0.5, 8, True),         # batch of one
     (1, 32, 128, 128, 0.5, 8, False),   # one step
+    (3, 20, 24, 64, 0.25, 16, False),   # 48 kept rows per region: two routing tiles
+    (2, 8, 16, 64, 0.5, 64, False),     # 128 kept rows per region: per-step weight gradient
 ])
 def test_layer_sparse_f32(L, T, B, I, H, sp, R, state):
     d = make_layer(T, B, I, H, seed=T * 100 + H, w_scale=0.2, state=state)
@@ -187,9 +189,15 @@ def test_layer_dense_f32(L):
     check_layer(L, d, "f32", 0.0, dense=True)
 
 
-def test_layer_sparse_bf16(L):
-    d = make_layer(4, 40, 64, 96, seed=10, w_scale=0.2, dtype="bf16")
+@pytest.mark.parametrize("T,B,I,H", [(4, 40, 64, 96), (3, 20, 36, 72)])
+def test_layer_sparse_bf16(L, T, B, I, H):
+    d = make_layer(T, B, I, H, seed=10 + B, w_scale=0.2, dtype="bf16")
     check_layer(L, d, "bf16", 0.5)
+
+
+def test_layer_dense_bf16(L):
+    d = make_layer(3, 24, 40, 64, seed=13, w_scale=0.2, dtype="bf16", state=True)
+    check_layer(L, d, "bf16", 0.0, dense=True)
 
 
 def test_sparsity_zero_equals_dense(L):
