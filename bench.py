@@ -41,24 +41,31 @@ def parse():
 
 
 def kernel_work(wl, layer, Kp, es):
-    """Algorithmic bytes and flops per launch of each backward kernel kind."""
-    I, H, B = wl.layer_input(layer), wl.hidden, wl.batch
+    """Algorithmic bytes and flops of each backward kernel kind for one layer
+    call (all T steps): what the method must read and write, not what the
+    implementation's staging (split-K partials, chunked updates) adds."""
+    I, H, B, T = wl.layer_input(layer), wl.hidden, wl.batch, wl.steps
     K, HB = I + H, H * B
     return {
-        # gates_t (4HB, storage type); c_t, c_{t-1}, dH_up[t], dh_rec, dc_t
-        # read and dc_{t-1} written (fp32); kept rows and index written
-        "gates_select_compact": {"bytes": 4 * HB * es + 6 * HB * 4 + Kp * B * es + Kp // wl.P * 4,
-                                 "flops": 0},
-        # W_c (K' x (I+H)), dG_c (K' x B) read, [dx; dh] ((I+H) x B, fp32) written
-        "data_grad_gemm": {"bytes": Kp * K * es + Kp * B * es + K * B * 4,
-                           "flops": 2 * K * B * Kp},
-        # dG_c and [x; h] read, kept rows of dW (fp32) read and written
-        "weight_grad_gemm": {"bytes": Kp * B * es + K * B * es + 2 * Kp * K * 4,
-                             "flops": 2 * Kp * K * B},
+        # per step: gates_t (4HB, storage type); c_t, c_{t-1}, dH_up[t],
+        # dh_rec, dc_t read and dc_{t-1} written (fp32); kept rows and index
+        # written
+        "gates_select_compact": {"bytes": T * (4 * HB * es + 6 * HB * 4 + Kp * B * es
+                                               + Kp // wl.P * 4), "flops": 0},
+        # per step: W_c (K' x (I+H)), dG_c (K' x B) read, [dx; dh] ((I+H) x B,
+        # fp32) written
+        "data_grad_gemm": {"bytes": T * (Kp * K * es + Kp * B * es + K * B * 4),
+                           "flops": T * 2 * K * B * Kp},
+        # every step's dG_c and [x; h] read once, dW (4H x (I+H), fp32)
+        # written once
+        "weight_grad_gemm": {"bytes": T * (Kp * B * es + K * B * es) + 4 * H * K * 4,
+                             "flops": T * 2 * Kp * K * B},
     }
 
 
 def roofline_entry(name, work, avg_s, dtype):
+    """work: algorithmic bytes/flops of one average launch; avg_s: its mean
+    event-measured duration."""
     peak_tf = PEAK["bf16_tflops"] if dtype == "bf16" else PEAK["f32_tflops"]
     t_mem = work["bytes"] / (PEAK["hbm_gbs"] * 1e9)
     t_mfma = work["flops"] / (peak_tf * 1e12)
@@ -220,9 +227,12 @@ def main():
     roofs = {}
     for name in ("gates_select_compact", "data_grad_gemm", "weight_grad_gemm"):
         ms, n = kt[name]
+        # work of one step (all layers) times the timed steps, spread over
+        # the launches of this kind: the average launch's algorithmic work
         works = [kernel_work(wl, l, sp_kps[l], es)[name] for l in range(wl.layers)]
-        work = {k: sum(w[k] for w in works) / len(works) for k in ("bytes", "flops")}
-        roofs[name] = roofline_entry(name, work, ms / 1e3 / max(n, 1), wl.dtype)
+        per_launch = {k: sum(w[k] for w in works) * args.steps / max(n, 1)
+                      for k in ("bytes", "flops")}
+        roofs[name] = roofline_entry(name, per_launch, ms / 1e3 / max(n, 1), wl.dtype)
     dominant = max(roofs, key=lambda k: kt[k][0])
 
     result = {

@@ -122,8 +122,9 @@ int32_t lstm_bwd_dense(const lstmss_dims *d, const void *x, const void *W, const
 /* Structurally sparsified backward pass (section 3, coarse-grained).  At every
  * time step the gate gradient is formed, each P-row slice is scored by its
  * squared L2 norm (same ranking as the norm) summed in fp64 in a fixed order
- * (64 strided partial sums over the batch, combined pairwise by index xor 32,
- * 16, 8, 4, 2, 1; then the P rows in increasing order), the S lowest slices of
+ * (per 64-column batch chunk the squares are combined pairwise by index xor
+ * 32, 16, 8, 4, 2, 1; the chunks of a row, then the P rows of a slice, are
+ * added in increasing order), the S lowest slices of
  * every region are dropped (ties drop the higher slice index; NaN scores rank
  * highest), the kept rows are compacted in ascending order and both gradient
  * products run on the compacted rows.  The cell-state gradient recursion uses
@@ -150,6 +151,17 @@ int32_t lstm_bwd_structsparse(const lstmss_dims *d, float sparsity, const lstmss
 int32_t lstmss_select_compact(const lstmss_dims *d, float sparsity, const lstmss_structure *s,
                               const void *dG, void *dG_c, int32_t *idx, double *scores,
                               void *stream);
+
+/* Execution options (results are identical under every setting):
+ *   LSTMSS_OPT_GRAPHS  1 (default): each backward call's launches are
+ *                      captured once into a HIP graph, keyed by every
+ *                      argument that reaches a kernel, and replayed on later
+ *                      calls with the same arguments (up to 32 per device).
+ *                      Environment variable LSTMSS_GRAPHS=0 sets it to 0.
+ * Changing an option drops the recorded graphs.  Not for use while calls
+ * are being enqueued from other threads. */
+enum { LSTMSS_OPT_GRAPHS = 0 };
+int32_t lstmss_set_option(int32_t option, int32_t value);
 
 /* Measurement hooks (not part of the method): when enabled, every kernel the
  * library launches is bracketed by a pair of HIP events recorded on its own

@@ -37,10 +37,11 @@
  *
  * Score summation order (fixed so that a GPU selector fed the same fp32 gate
  * gradient bytes can be compared bit for bit):
- *   rowsq(r): 64 partial sums, partial l = sum over b = l, l+64, l+128, ...
- *             of dG[r][b]^2 in increasing b; then the 64 partials are combined
- *             pairwise by index xor 32, 16, 8, 4, 2, 1 (every position ends
- *             with the same value since fp64 addition is commutative);
+ *   chunk c of a row holds the batch columns [64c, 64c + 64); its 64 squares
+ *             (zero past B) are combined pairwise by index xor 32, 16, 8, 4,
+ *             2, 1 (every position ends with the same value since fp64
+ *             addition is commutative);
+ *   rowsq(r) = ((chunk 0 + chunk 1) + chunk 2) + ... left fold over chunks;
  *   score(j) = (((rowsq(jP) + rowsq(jP+1)) + rowsq(jP+2)) + ...) left fold.
  * All of it in fp64; for fp32 inputs each square is exact in fp64, so whether
  * a compiler fuses multiply and add cannot change the result.
@@ -171,14 +172,12 @@ int oracle_forward(int T, int B, int I, int H, const double *x, const double *W,
 /* Slice scores (section 3: the L2 norm of each slice, compared squared).     */
 /* dG [rows][B]; rows must be a multiple of P; scores [rows / P].            */
 /* ------------------------------------------------------------------------ */
-static double row_sumsq(const double *row, int B)
+static double chunk_sumsq(const double *row, int B, int c)
 {
     double part[64], next[64];
     for (int l = 0; l < 64; ++l) {
-        double s = 0.0;
-        for (int b = l; b < B; b += 64)
-            s += row[b] * row[b];
-        part[l] = s;
+        int b = 64 * c + l;
+        part[l] = b < B ? row[b] * row[b] : 0.0;
     }
     for (int off = 32; off >= 1; off >>= 1) {
         for (int l = 0; l < 64; ++l)
@@ -186,6 +185,14 @@ static double row_sumsq(const double *row, int B)
         memcpy(part, next, sizeof(part));
     }
     return part[0];
+}
+
+static double row_sumsq(const double *row, int B)
+{
+    double s = chunk_sumsq(row, B, 0);
+    for (int c = 1; 64 * c < B; ++c)
+        s = s + chunk_sumsq(row, B, c);
+    return s;
 }
 
 int oracle_scores(long rows, int B, int P, const double *dG, double *scores)

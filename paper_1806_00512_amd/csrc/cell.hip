@@ -12,7 +12,7 @@ namespace lstmss {
 
 namespace {
 
-constexpr int CELL_THREADS = 256;
+constexpr int CELL_THREADS = 512;
 
 // Gate gradient of row r = g*H + u at batch column b for one backward step.
 //   dh  = dH_up + dh_rec                       (dL/dh_t)
@@ -25,9 +25,7 @@ template <typename TS>
 __device__ __forceinline__ float gate_grad(const CellArgs &a, const TS *gates, int g, int u, int b) {
     const int B = a.B, H = a.H;
     const int e = u * B + b;
-    float dh = a.dH_up[e];
-    for (int s = 0; s < a.dh_nparts; ++s)
-        dh += a.dh_part[s * a.dh_stride + e];
+    const float dh = sum_parts(a.dH_up[e], a.dh_part + e, a.dh_nparts, a.dh_stride);
     const float tc = tanhf(a.c_t[e]);
     const float o = st<TS>::load(gates, (3 * H + u) * B + b);
     if (g == 3)
@@ -57,18 +55,6 @@ __global__ __launch_bounds__(CELL_THREADS) void cell_select_kernel(CellArgs a) {
     constexpr int NW = CELL_THREADS / 64;
     const int B = a.B, P = a.P, R = a.R;
     const long G = 4L * a.H;
-
-    // Reduction of the previous step's dX partial sums, spread over the grid.
-    if (a.dx_out) {
-        const long chunk = ceil_div(a.dx_n, gridDim.x);
-        const long e0 = blockIdx.x * chunk, e1 = min(a.dx_n, e0 + chunk);
-        for (long e = e0 + tid; e < e1; e += CELL_THREADS) {
-            float s = 0.f;
-            for (int p = 0; p < a.dx_nparts; ++p)
-                s += a.dx_part[p * a.dx_stride + e];
-            a.dx_out[e] = s;
-        }
-    }
 
     const long slices_per_wg = (long)a.regions_per_wg * R;
     const long j0 = blockIdx.x * slices_per_wg;
@@ -112,12 +98,12 @@ __global__ __launch_bounds__(CELL_THREADS) void cell_select_kernel(CellArgs a) {
     }
     __syncthreads();
 
-    // Phase 1b: per-row sum of squares in the fixed order (partial l sums
-    // b = l, l+64, ... in increasing b; partials combined by index xor 32, 16,
-    // ..., 1).  With B <= 2^k < 64 every partial at index >= 2^k is zero and
-    // adding it is exact, so 2^k lanes per row give the same value; a
-    // wavefront then handles 64 / 2^k rows at once.  Row sums for the bias
-    // gradient ride along.
+    // Phase 1b: per-row sum of squares in the fixed order (each 64-column
+    // chunk combined by index xor 32, 16, ..., 1, chunks added in order).
+    // With B <= 2^k < 64 every square at index >= 2^k is zero and adding it is
+    // exact, so 2^k lanes per row give the same value; a wavefront then
+    // handles 64 / 2^k rows at once.  Row sums for the bias gradient ride
+    // along.
     {
         int lpr = 1;
         while (lpr < B && lpr < 64)
@@ -128,18 +114,19 @@ __global__ __launch_bounds__(CELL_THREADS) void cell_select_kernel(CellArgs a) {
             const int lr = base + sub;
             double part = 0.0;
             float rsum = 0.f;
-            if (lr < nrows) {
-                for (int b = sl; b < B; b += 64) {
-                    const float v = sdG[lr * B + b];
-                    part += (double)v * (double)v;
-                    rsum += v;
+            for (int c = 0; 64 * c < B; ++c) {  // chunks of 64 batch columns
+                const int b = 64 * c + sl;
+                const float v = (lr < nrows && b < B) ? sdG[lr * B + b] : 0.f;
+                rsum += v;
+                if (MODE != CELL_DENSE) {
+                    double q = (double)v * (double)v;
+                    for (int off = lpr >> 1; off >= 1; off >>= 1)
+                        q = q + shfl_xor_f64(q, off);
+                    part = c == 0 ? q : part + q;
                 }
             }
-            for (int off = lpr >> 1; off >= 1; off >>= 1) {
-                if (MODE != CELL_DENSE)
-                    part = part + shfl_xor_f64(part, off);
+            for (int off = lpr >> 1; off >= 1; off >>= 1)
                 rsum += shfl_xor_f32(rsum, off);
-            }
             if (sl == 0 && lr < nrows) {
                 if (MODE == CELL_DENSE) {
                     if (a.db)
@@ -217,6 +204,384 @@ __global__ __launch_bounds__(CELL_THREADS) void cell_select_kernel(CellArgs a) {
     (void)G;
 }
 
+// ---------------------------------------------------------------------------
+// Register-resident variant for small work-groups (<= 32 rows, <= 32 slices,
+// B <= 256): a row is owned by LPR lanes (the next power of two >= B, at most
+// 64), lane l holding batch columns l, l+64, ... (one per 64-column chunk);
+// with B <= LPR < 64 the squares at index >= LPR are zero, so an LPR-lane
+// butterfly gives the fixed score order exactly.  Values stay in registers from the gate-gradient
+// formula to the compacted store; one wavefront scores, selects (ballot
+// prefix within each region) and places the slices.
+// ---------------------------------------------------------------------------
+constexpr int RK_WAVES = 8;
+
+template <typename TS, int MODE, int LPR, int NJ>
+__global__ __launch_bounds__(RK_WAVES * 64) void cell_rows_kernel(CellArgs a) {
+    constexpr int RPW = 64 / LPR;                       // rows per wavefront pass
+    constexpr int NP = (32 + RK_WAVES * RPW - 1) / (RK_WAVES * RPW);
+    __shared__ double srowsq[32];
+    __shared__ int sslot[32];
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int B = a.B, H = a.H, P = a.P, R = a.R;
+    const long spw = (long)a.regions_per_wg * R;
+    const long j0 = blockIdx.x * spw;
+    const int nsl = (int)min(spw, a.nslices - j0);
+    const int row0 = (int)(j0 * P);
+    const int nrows = nsl * P;
+    const int sub = lane / LPR, sl = lane - sub * LPR;
+
+    const TS *__restrict__ gates = (const TS *)a.gates;
+    const float *__restrict__ dHup = a.dH_up;
+    const float *__restrict__ ct = a.c_t;
+    const float *__restrict__ cp = a.c_prev;
+    const float *__restrict__ dcin = a.dc_in;
+    TS *dGc = (TS *)a.dGc;
+    TS *dbg = (TS *)a.dbg;
+
+    // Phase 1: loads of every owned element first, then the formulas.
+    float v[NP][NJ];
+    float l_dh[NP][NJ], l_o[NP][NJ], l_a[NP][NJ], l_b[NP][NJ], l_ct[NP][NJ], l_x[NP][NJ];
+#pragma unroll
+    for (int p = 0; p < NP; ++p) {
+        const int lr = (p * RK_WAVES + wave) * RPW + sub;
+#pragma unroll
+        for (int j = 0; j < NJ; ++j) {
+            const int b = sl + 64 * j;
+            const bool in = lr < nrows && b < B;
+            const int r = row0 + (in ? lr : 0);
+            const int g = r / H, u = r - g * H;
+            const int e = u * B + (in ? b : 0);
+            if (MODE == CELL_GIVEN) {
+                l_x[p][j] = in ? st<TS>::load((const TS *)a.dG_in, (long)r * B + b) : 0.f;
+                continue;
+            }
+            l_dh[p][j] = in ? sum_parts(dHup[e], a.dh_part + e, a.dh_nparts, a.dh_stride) : 0.f;
+            l_ct[p][j] = in ? ct[e] : 0.f;
+            l_o[p][j] = in ? st<TS>::load(gates, (long)(3 * H + u) * B + b) : 0.f;
+            // gate-specific operands: i rows need (i, g), f rows (f, c_{t-1}),
+            // g rows (i, g); all but o rows need dc_t
+            const int ga = g == 1 ? 1 : 0, gb = 2;
+            l_a[p][j] = (in && g < 3) ? st<TS>::load(gates, (long)(ga * H + u) * B + b) : 0.f;
+            l_b[p][j] = (in && g < 3) ? (g == 1 ? cp[e] : st<TS>::load(gates, (long)(gb * H + u) * B + b)) : 0.f;
+            l_x[p][j] = (in && g < 3 && dcin) ? dcin[e] : 0.f;
+        }
+    }
+    double part[NP];
+    float rsum[NP];
+#pragma unroll
+    for (int p = 0; p < NP; ++p) {
+        const int lr = (p * RK_WAVES + wave) * RPW + sub;
+        part[p] = 0.0;
+        rsum[p] = 0.f;
+#pragma unroll
+        for (int j = 0; j < NJ; ++j) {
+            const int b = sl + 64 * j;
+            const bool in = lr < nrows && b < B;
+            float val;
+            if (MODE == CELL_GIVEN) {
+                val = l_x[p][j];
+            } else {
+                const int r = row0 + (in ? lr : 0);
+                const int g = r / H, u = r - g * H;
+                const float dh = l_dh[p][j], tc = tanhf(l_ct[p][j]), o = l_o[p][j];
+                if (g == 3) {
+                    val = dh * tc * o * (1.f - o);
+                } else {
+                    const float dcv = l_x[p][j] + dh * o * (1.f - tc * tc);
+                    if (g == 1) {
+                        const float f = l_a[p][j];
+                        if (in)
+                            a.dc_out[u * B + b] = dcv * f;
+                        val = dcv * l_b[p][j] * f * (1.f - f);
+                    } else {
+                        const float i = l_a[p][j], gg = l_b[p][j];
+                        val = g == 0 ? dcv * gg * i * (1.f - i) : dcv * i * (1.f - gg * gg);
+                    }
+                }
+                val = st<TS>::rnd(val);
+                if (in && dbg)
+                    st<TS>::store(dbg, (long)r * B + b, val);
+                if (in && MODE == CELL_DENSE)
+                    st<TS>::store(dGc, (long)r * B + b, val);
+            }
+            val = in ? val : 0.f;
+            v[p][j] = val;
+            rsum[p] += val;
+            if (MODE != CELL_DENSE) {
+                // chunk j of the row: xor butterfly, then fold into the row
+                double q = (double)val * (double)val;
+#pragma unroll
+                for (int off = LPR >> 1; off >= 1; off >>= 1)
+                    q = q + shfl_xor_f64(q, off);
+                part[p] = j == 0 ? q : part[p] + q;
+            }
+        }
+#pragma unroll
+        for (int off = LPR >> 1; off >= 1; off >>= 1)
+            rsum[p] += shfl_xor_f32(rsum[p], off);
+        if (sl == 0 && lr < nrows) {
+            if (MODE == CELL_DENSE) {
+                if (a.db)
+                    a.db[row0 + lr] += rsum[p];
+            } else {
+                srowsq[lr] = part[p];
+            }
+        }
+    }
+    if (MODE == CELL_DENSE)
+        return;
+    __syncthreads();
+
+    // Phases 2-4 in wavefront 0: lane j scores slice j, counts the slices of
+    // its region that outrank it, and takes its slot from a ballot prefix.
+    if (wave == 0) {
+        const int j = lane;
+        const bool valid = j < nsl;
+        double sc = 0.0;
+        if (valid) {
+            sc = srowsq[j * P];
+            for (int p = 1; p < P; ++p)
+                sc = sc + srowsq[j * P + p];
+            if (a.scores)
+                a.scores[j0 + j] = sc;
+        }
+        const uint64_t kj = score_key(sc);
+        const long gj = j0 + j;
+        const long rs = (gj / R) * R;
+        const int ls = (int)(rs - j0);
+        const int rlen = (int)min((long)R, a.nslices - rs);
+        const int nkeep = rlen - (a.S * rlen) / R;
+        int beaten = 0;
+        for (int i = 0; i < 32; ++i) {
+            const uint64_t ki = (uint64_t)__shfl((long long)kj, i, 64);
+            if (valid && i != j && i >= ls && i < ls + rlen && i < nsl && outranks(ki, i, kj, j))
+                ++beaten;
+        }
+        const bool keep = valid && beaten < nkeep;
+        const uint64_t ball = __ballot(keep);
+        const uint64_t below = ((j ? (~0ull >> (64 - j)) : 0ull)) & ~((ls ? (~0ull >> (64 - ls)) : 0ull));
+        const int pos = __popcll(ball & below);
+        int slot = -1;
+        if (keep) {
+            slot = (int)((gj / R) * (R - a.S) + pos);
+            a.idx[slot] = (int32_t)gj;
+        }
+        if (valid)
+            sslot[j] = slot;
+    }
+    __syncthreads();
+
+    // Phase 5: kept values from registers to the compacted matrix; bias.
+#pragma unroll
+    for (int p = 0; p < NP; ++p) {
+        const int lr = (p * RK_WAVES + wave) * RPW + sub;
+        if (lr >= nrows)
+            continue;
+        const int slot = sslot[lr / P];
+        if (slot < 0)
+            continue;
+        const long crow = (long)slot * P + lr % P;
+#pragma unroll
+        for (int j = 0; j < NJ; ++j) {
+            const int b = sl + 64 * j;
+            if (b < B)
+                st<TS>::store(dGc, crow * B + b, v[p][j]);
+        }
+        if (sl == 0 && a.db)
+            a.db[row0 + lr] += rsum[p];
+    }
+}
+
+// ---------------------------------------------------------------------------
+// Split variant for large shapes, two kernels per step.
+//
+// cell_elem_kernel: element-parallel over (8 units x one 64-column batch
+// chunk) per work-group, so every CU has loads in flight.  Each (unit, batch)
+// element is loaded once and gives all four gate gradients; wave w owns units
+// 2w, 2w+1 of the group, lane l batch column 64c + l.  It writes the gate
+// gradient (straight to the compacted matrix when nothing is dropped, else to
+// a staging matrix), dc_{t-1}, and per (row, chunk) the fp64 chunk sum of
+// squares (fixed 64-lane butterfly) and the fp32 row sum.
+//
+// cell_select_kernel2: one work-group per group of regions folds the chunk
+// sums of its rows in order, scores and selects the slices (one wavefront),
+// and copies the kept rows from the staging matrix.
+// ---------------------------------------------------------------------------
+constexpr int EK_UNITS = 8;
+constexpr int EK_WAVES = 4;
+
+template <typename TS, bool SPARSE>
+__global__ __launch_bounds__(EK_WAVES * 64) void cell_elem_kernel(CellArgs a) {
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    const int B = a.B, H = a.H;
+    const int c = blockIdx.y, nch = gridDim.y;
+    const int b = 64 * c + lane;
+    const bool bin = b < B;
+    const TS *__restrict__ gates = (const TS *)a.gates;
+    const float *__restrict__ dHup = a.dH_up;
+    const float *__restrict__ ct = a.c_t;
+    const float *__restrict__ cp = a.c_prev;
+    const float *__restrict__ dcin = a.dc_in;
+    constexpr int UPW = EK_UNITS / EK_WAVES;
+    float lg[UPW][4], ldh[UPW], lct[UPW], lcp[UPW], ldc[UPW];
+    int uu[UPW];
+    bool ok[UPW];
+#pragma unroll
+    for (int k = 0; k < UPW; ++k) {
+        const int u = blockIdx.x * EK_UNITS + wave * UPW + k;
+        uu[k] = u;
+        ok[k] = u < H && bin;
+        const int e = (u < H ? u : 0) * B + (bin ? b : 0);
+#pragma unroll
+        for (int g = 0; g < 4; ++g)
+            lg[k][g] = ok[k] ? st<TS>::load(gates, (long)(g * H + u) * B + b) : 0.f;
+        lct[k] = ok[k] ? ct[e] : 0.f;
+        lcp[k] = ok[k] ? cp[e] : 0.f;
+        ldc[k] = (ok[k] && dcin) ? dcin[e] : 0.f;
+        ldh[k] = ok[k] ? sum_parts(dHup[e], a.dh_part + e, a.dh_nparts, a.dh_stride) : 0.f;
+    }
+    TS *out = (TS *)(SPARSE ? a.stage : a.dGc);
+    TS *dbg = (TS *)a.dbg;
+#pragma unroll
+    for (int k = 0; k < UPW; ++k) {
+        const int u = uu[k];
+        const float ig = lg[k][0], fg = lg[k][1], gg = lg[k][2], og = lg[k][3];
+        const float tc = tanhf(lct[k]);
+        const float dcv = ldc[k] + ldh[k] * og * (1.f - tc * tc);
+        float v[4];
+        v[0] = st<TS>::rnd(dcv * gg * ig * (1.f - ig));
+        v[1] = st<TS>::rnd(dcv * lcp[k] * fg * (1.f - fg));
+        v[2] = st<TS>::rnd(dcv * ig * (1.f - gg * gg));
+        v[3] = st<TS>::rnd(ldh[k] * tc * og * (1.f - og));
+        if (ok[k]) {
+            a.dc_out[u * B + b] = dcv * fg;
+#pragma unroll
+            for (int g = 0; g < 4; ++g) {
+                const long r = (long)g * H + u;
+                st<TS>::store(out, r * B + b, v[g]);
+                if (dbg)
+                    st<TS>::store(dbg, r * B + b, v[g]);
+            }
+        }
+#pragma unroll
+        for (int g = 0; g < 4; ++g) {
+            const float x = ok[k] ? v[g] : 0.f;
+            double q = (double)x * (double)x;
+            float rs = x;
+#pragma unroll
+            for (int off = 32; off >= 1; off >>= 1) {
+                if (SPARSE)
+                    q = q + shfl_xor_f64(q, off);
+                rs += shfl_xor_f32(rs, off);
+            }
+            if (lane == 0 && u < H) {
+                const long r = (long)g * H + u;
+                if (SPARSE)
+                    a.chunk_sq[r * nch + c] = q;
+                a.chunk_rs[r * nch + c] = rs;
+            }
+        }
+    }
+}
+
+constexpr int SK_WAVES = 4;
+
+template <typename TS>
+__global__ __launch_bounds__(SK_WAVES * 64) void cell_select_kernel2(CellArgs a) {
+    __shared__ double srowsq[64 * 4];
+    __shared__ int sslot[64];
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int B = a.B, P = a.P, R = a.R;
+    const int nch = (B + 63) / 64;
+    const long spw = (long)a.regions_per_wg * R;
+    const long j0 = blockIdx.x * spw;
+    const int nsl = (int)min(spw, a.nslices - j0);
+    const int row0 = (int)(j0 * P);
+    const int nrows = nsl * P;
+    for (int lr = tid; lr < nrows; lr += SK_WAVES * 64) {
+        const double *q = a.chunk_sq + (long)(row0 + lr) * nch;
+        double sq = q[0];
+        for (int cc = 1; cc < nch; ++cc)
+            sq = sq + q[cc];
+        srowsq[lr] = sq;
+    }
+    __syncthreads();
+    if (wave == 0) {
+        const int j = lane;
+        const bool valid = j < nsl;
+        double sc = 0.0;
+        if (valid) {
+            sc = srowsq[j * P];
+            for (int p = 1; p < P; ++p)
+                sc = sc + srowsq[j * P + p];
+            if (a.scores)
+                a.scores[j0 + j] = sc;
+        }
+        const uint64_t kj = score_key(sc);
+        const long gj = j0 + j;
+        const long rs = (gj / R) * R;
+        const int ls = (int)(rs - j0);
+        const int rlen = (int)min((long)R, a.nslices - rs);
+        const int nkeep = rlen - (a.S * rlen) / R;
+        int beaten = 0;
+        for (int i = 0; i < 64; ++i) {
+            const uint64_t ki = (uint64_t)__shfl((long long)kj, i, 64);
+            if (valid && i != j && i >= ls && i < ls + rlen && i < nsl && outranks(ki, i, kj, j))
+                ++beaten;
+        }
+        const bool keep = valid && beaten < nkeep;
+        const uint64_t ball = __ballot(keep);
+        const uint64_t below = ((j ? (~0ull >> (64 - j)) : 0ull)) & ~((ls ? (~0ull >> (64 - ls)) : 0ull));
+        const int pos = __popcll(ball & below);
+        int slot = -1;
+        if (keep) {
+            slot = (int)((gj / R) * (R - a.S) + pos);
+            a.idx[slot] = (int32_t)gj;
+        }
+        if (valid)
+            sslot[j] = slot;
+    }
+    __syncthreads();
+    // copy kept rows (P rows of B columns per kept slice), 16-byte chunks
+    // when rows are 16-byte aligned
+    const TS *stage = (const TS *)a.stage;
+    TS *dGc = (TS *)a.dGc;
+    for (int q = tid; q < nrows * B; q += SK_WAVES * 64) {
+        const int lr = q / B, bb = q - lr * B;
+        const int slot = sslot[lr / P];
+        if (slot >= 0)
+            dGc[((long)slot * P + lr % P) * B + bb] = stage[(long)(row0 + lr) * B + bb];
+    }
+}
+
+// db[r] (+)= sum over steps [t0, t1) of the row sums of the steps where r's
+// slice was kept (all steps when idx is NULL), steps in decreasing order.
+__global__ void bias_grad_kernel(float *db, const float *chunk_rs, int nch, long G, int t0, int t1,
+                                 const int32_t *idx, int kept, int P, int R, int S, int accumulate) {
+    const long r = blockIdx.x * (long)blockDim.x + threadIdx.x;
+    if (r >= G)
+        return;
+    const long j = r / P, reg = j / R;
+    float acc = accumulate ? db[r] : 0.f;
+    for (int t = t1 - 1; t >= t0; --t) {
+        bool keep = idx == nullptr;
+        if (!keep) {
+            const int32_t *it = idx + (long)t * kept + reg * (R - S);
+            const long e1 = min((long)(R - S), kept - reg * (R - S));
+            for (long e = 0; e < e1; ++e)
+                keep |= it[e] == j;
+        }
+        if (keep) {
+            const float *q = chunk_rs + ((long)t * G + r) * nch;
+            float rs = q[0];
+            for (int cc = 1; cc < nch; ++cc)
+                rs += q[cc];
+            acc += rs;
+        }
+    }
+    db[r] = acc;
+}
+
 __global__ void fill_kernel(float *p, long n, float v) {
     for (long i = blockIdx.x * (long)blockDim.x + threadIdx.x; i < n; i += (long)gridDim.x * blockDim.x)
         p[i] = v;
@@ -228,12 +593,8 @@ __global__ void copy_in_kernel(float *dst, const float *src, long n) {
 }
 
 __global__ void reduce_parts_kernel(float *out, const float *part, int nparts, long stride, long n) {
-    for (long i = blockIdx.x * (long)blockDim.x + threadIdx.x; i < n; i += (long)gridDim.x * blockDim.x) {
-        float s = 0.f;
-        for (int p = 0; p < nparts; ++p)
-            s += part[p * stride + i];
-        out[i] = s;
-    }
+    for (long i = blockIdx.x * (long)blockDim.x + threadIdx.x; i < n; i += (long)gridDim.x * blockDim.x)
+        out[i] = sum_parts(0.f, part + i, nparts, stride);
 }
 
 template <typename TS>
@@ -257,7 +618,81 @@ size_t cell_lds_bytes(const CellArgs &a, int mode) {
     return bytes;
 }
 
+bool cell_split_ok(const CellArgs &a, int mode) {
+    if (mode == CELL_GIVEN || (long)a.H * a.B < 65536)
+        return false;
+    return mode == CELL_DENSE ||
+           ((long)a.regions_per_wg * a.R <= 64 && (long)a.regions_per_wg * a.R * a.P <= 256);
+}
+
+hipError_t launch_cell_split(const CellArgs &a, int mode, bool bf16, hipStream_t s) {
+    const int nch = (int)ceil_div(a.B, 64);
+    dim3 ge((unsigned)ceil_div(a.H, EK_UNITS), (unsigned)nch);
+    const bool sp = mode == CELL_SPARSE;
+    if (bf16) {
+        if (sp) hipLaunchKernelGGL((cell_elem_kernel<bf16_t, true>), ge, dim3(EK_WAVES * 64), 0, s, a);
+        else hipLaunchKernelGGL((cell_elem_kernel<bf16_t, false>), ge, dim3(EK_WAVES * 64), 0, s, a);
+    } else {
+        if (sp) hipLaunchKernelGGL((cell_elem_kernel<float, true>), ge, dim3(EK_WAVES * 64), 0, s, a);
+        else hipLaunchKernelGGL((cell_elem_kernel<float, false>), ge, dim3(EK_WAVES * 64), 0, s, a);
+    }
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess || !sp)
+        return e;
+    const int grid = (int)ceil_div(a.nslices, (long)a.regions_per_wg * a.R);
+    if (bf16)
+        hipLaunchKernelGGL((cell_select_kernel2<bf16_t>), dim3(grid), dim3(SK_WAVES * 64), 0, s, a);
+    else
+        hipLaunchKernelGGL((cell_select_kernel2<float>), dim3(grid), dim3(SK_WAVES * 64), 0, s, a);
+    return hipGetLastError();
+}
+
+hipError_t launch_bias_grad(float *db, const float *chunk_rs, int nch, long G, int t0, int t1,
+                            const int32_t *idx, int kept, int P, int R, int S, bool accumulate,
+                            hipStream_t s) {
+    hipLaunchKernelGGL(bias_grad_kernel, dim3((unsigned)ceil_div(G, 256)), dim3(256), 0, s, db,
+                       chunk_rs, nch, G, t0, t1, idx, kept, P, R, S, accumulate ? 1 : 0);
+    return hipGetLastError();
+}
+
+static bool cell_rows_ok(const CellArgs &a) {
+    return (long)a.regions_per_wg * a.R * a.P <= 32 && (long)a.regions_per_wg * a.R <= 32 &&
+           a.B <= 256;
+}
+
+template <typename TS, int M>
+static void launch_rows(const CellArgs &a, int grid, hipStream_t s) {
+    const int B = a.B;
+#define LSTMSS_RK(L, J) hipLaunchKernelGGL((cell_rows_kernel<TS, M, L, J>), dim3(grid), dim3(RK_WAVES * 64), 0, s, a)
+    if (B <= 1) LSTMSS_RK(1, 1);
+    else if (B <= 2) LSTMSS_RK(2, 1);
+    else if (B <= 4) LSTMSS_RK(4, 1);
+    else if (B <= 8) LSTMSS_RK(8, 1);
+    else if (B <= 16) LSTMSS_RK(16, 1);
+    else if (B <= 32) LSTMSS_RK(32, 1);
+    else if (B <= 64) LSTMSS_RK(64, 1);
+    else if (B <= 128) LSTMSS_RK(64, 2);
+    else if (B <= 192) LSTMSS_RK(64, 3);
+    else LSTMSS_RK(64, 4);
+#undef LSTMSS_RK
+}
+
 hipError_t launch_cell(const CellArgs &a, int mode, bool bf16, hipStream_t s) {
+    if (cell_split_ok(a, mode))
+        return launch_cell_split(a, mode, bf16, s);
+    if (cell_rows_ok(a)) {
+        const int grid = (int)ceil_div(a.nslices, (long)a.regions_per_wg * a.R);
+        if (bf16) {
+            if (mode == CELL_DENSE) launch_rows<bf16_t, CELL_DENSE>(a, grid, s);
+            else if (mode == CELL_SPARSE) launch_rows<bf16_t, CELL_SPARSE>(a, grid, s);
+            else launch_rows<bf16_t, CELL_GIVEN>(a, grid, s);
+        } else {
+            if (mode == CELL_DENSE) launch_rows<float, CELL_DENSE>(a, grid, s);
+            else if (mode == CELL_SPARSE) launch_rows<float, CELL_SPARSE>(a, grid, s);
+            else launch_rows<float, CELL_GIVEN>(a, grid, s);
+        }
+        return hipGetLastError();
+    }
     const long spw = (long)a.regions_per_wg * a.R;
     const int grid = (int)ceil_div(a.nslices, spw);
     const size_t lds = cell_lds_bytes(a, mode);

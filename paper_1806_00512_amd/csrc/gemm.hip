@@ -89,7 +89,6 @@ struct Vec<bf16_t, false> {
 // one.  The gathered W row of every k of the split is looked up once into
 // LDS.
 // --------------------------------------------------------------------------
-constexpr int GEMM1_KC_MAX = 4096;
 
 template <typename TS, int TN, bool GATHER, bool VEC>
 __global__ __launch_bounds__(THREADS) void gemm1_kernel(Gemm1Args a) {
@@ -104,17 +103,26 @@ __global__ __launch_bounds__(THREADS) void gemm1_kernel(Gemm1Args a) {
     const int wm = wave % WM, wn = wave / WM;
     const int mm0 = blockIdx.x * TM;
     const int n0 = blockIdx.y * TN;
-    const int kb = blockIdx.z * (int)a.k_chunk;
+    const int step = blockIdx.z / a.splitk, split = blockIdx.z - step * a.splitk;
+    const int kb = split * (int)a.k_chunk;
     const int ke = min((int)a.Kp, kb + (int)a.k_chunk);
     const int M = a.M, N = a.N, ldw = (int)a.ldw;
     const TS *W = (const TS *)a.W;
-    const TS *G = (const TS *)a.Gc;
+    const TS *G = (const TS *)a.Gc + step * a.gc_step;
+    const int32_t *idx = a.idx + (GATHER ? step * a.idx_step : 0);
 
+    // gathered W row of every k of the current super-chunk (refilled every
+    // GEMM1_KC_MAX rows)
     __shared__ int srow[GEMM1_KC_MAX];
-    for (int i = tid; i < ke - kb; i += THREADS) {
-        const int k = kb + i;
-        srow[i] = GATHER ? a.idx[k / a.P] * a.P + k % a.P : k;
-    }
+    int sc = kb;
+    auto fill_rows = [&](int s0) {
+        const int s1 = min(ke, s0 + GEMM1_KC_MAX);
+        for (int i = tid; i < s1 - s0; i += THREADS) {
+            const int k = s0 + i;
+            srow[i] = GATHER ? idx[k / a.P] * a.P + k % a.P : k;
+        }
+    };
+    fill_rows(sc);
 
     V ra[RA], rb[RB];
     auto load = [&](int k0) {
@@ -122,9 +130,9 @@ __global__ __launch_bounds__(THREADS) void gemm1_kernel(Gemm1Args a) {
         for (int i = 0; i < RA; ++i) {
             const int q = tid + i * THREADS;
             const int kk = q / (TM / VW), mm = (q % (TM / VW)) * VW;
-            const int k = k0 + kk, m = a.m_begin + mm0 + mm;
+            const int k = k0 + kk, m = a.m_lo + mm0 + mm;
             if (q < NA && k < ke && m < M)
-                ra[i].load(W + (long)srow[k - kb] * ldw + m, M - m);
+                ra[i].load(W + (long)srow[k - sc] * ldw + m, M - m);
             else
                 ra[i].zero();
         }
@@ -151,6 +159,12 @@ __global__ __launch_bounds__(THREADS) void gemm1_kernel(Gemm1Args a) {
         __shared__ __align__(16) float As[TK][TM + 4];
         __shared__ __align__(16) float Bs[TK][TN + 4];
         for (int k0 = kb; k0 < ke; k0 += TK) {
+            if (k0 == sc + GEMM1_KC_MAX) {  // next super-chunk of rows
+                sc = k0;
+                fill_rows(sc);
+                __syncthreads();
+                load(k0);
+            }
 #pragma unroll
             for (int i = 0; i < RA; ++i) {
                 const int q = tid + i * THREADS;
@@ -172,7 +186,7 @@ __global__ __launch_bounds__(THREADS) void gemm1_kernel(Gemm1Args a) {
                 }
             }
             __syncthreads();
-            if (k0 + TK < ke)
+            if (k0 + TK < ke && k0 + TK != sc + GEMM1_KC_MAX)
                 load(k0 + TK);
 #pragma unroll
             for (int kk = 0; kk < TK; kk += 2) {
@@ -187,6 +201,12 @@ __global__ __launch_bounds__(THREADS) void gemm1_kernel(Gemm1Args a) {
         __shared__ __align__(16) uint16_t As[TM][TK + 8];
         __shared__ __align__(16) uint16_t Bs[TN][TK + 8];
         for (int k0 = kb; k0 < ke; k0 += TK) {
+            if (k0 == sc + GEMM1_KC_MAX) {  // next super-chunk of rows
+                sc = k0;
+                fill_rows(sc);
+                __syncthreads();
+                load(k0);
+            }
 #pragma unroll
             for (int i = 0; i < RA; ++i) {
                 const int q = tid + i * THREADS;
@@ -208,7 +228,7 @@ __global__ __launch_bounds__(THREADS) void gemm1_kernel(Gemm1Args a) {
                 }
             }
             __syncthreads();
-            if (k0 + TK < ke)
+            if (k0 + TK < ke && k0 + TK != sc + GEMM1_KC_MAX)
                 load(k0 + TK);
 #pragma unroll
             for (int kk = 0; kk < TK; kk += 16) {
@@ -220,13 +240,13 @@ __global__ __launch_bounds__(THREADS) void gemm1_kernel(Gemm1Args a) {
         }
     }
 
-    float *out = a.part + blockIdx.z * a.part_stride;
+    float *out = a.part + step * a.out_step + split * a.part_stride;
     const int n = n0 + wn * 32 + (lane & 31);
 #pragma unroll
     for (int v = 0; v < 16; ++v) {
-        const int m = a.m_begin + mm0 + wm * 32 + acc_row(lane, v);
-        if (m < M && n < N)
-            out[(long)m * N + n] = acc[v];
+        const int m = a.m_lo + mm0 + wm * 32 + acc_row(lane, v);
+        if (m >= a.m_begin && m < M && n < N)
+            out[(long)(m - a.out_row0) * N + n] = acc[v];
     }
 }
 
@@ -321,8 +341,9 @@ __global__ __launch_bounds__(THREADS) void gemm2_kernel(Gemm2Args a) {
 // Weight gradient of all time steps in one launch.
 //
 // Work-group: one group of output rows x 128 features (4 waves x 32).  It
-// walks every time step (and batch chunk) and owns its dW tile, so dW is
-// written once, in a fixed summation order (deterministic, no atomics).
+// walks the launch's time steps (and batch chunks) and owns its dW tile, so
+// dW is written (or, for a later chunk of steps, updated) once per launch in
+// a fixed summation order (deterministic, no atomics).
 //
 // Dense: a group is 32 consecutive rows; each step's product is added to the
 // accumulator.
@@ -341,24 +362,24 @@ __global__ __launch_bounds__(THREADS) void gemm2_kernel(Gemm2Args a) {
 // [BC/2, BC), so each lane reads consecutive columns from LDS.
 // --------------------------------------------------------------------------
 constexpr int WG_FEAT = 128;
-constexpr int WG_BCMAX = 64;
 constexpr int WG_ATMAX = 4;
 
-template <typename TS, bool SPARSE, int TT, bool VEC>
+template <typename TS, bool SPARSE, int TT, bool VEC, int BC>
 __global__ __launch_bounds__(THREADS) void wgrad_kernel(WgradArgs a) {
     using E = typename std::conditional<sizeof(TS) == 4, float, uint16_t>::type;
-    constexpr int PITCH = WG_BCMAX + (sizeof(TS) == 4 ? 4 : 8);
+    constexpr int PITCH = BC + (sizeof(TS) == 4 ? 4 : 8);
     constexpr int GROWS = TT * 32;
     using V = Vec<TS, VEC>;
     constexpr int VW = V::W;
-    constexpr int RG = (GROWS * WG_BCMAX / VW + THREADS - 1) / THREADS;
-    constexpr int RX = (WG_FEAT * WG_BCMAX / VW + THREADS - 1) / THREADS;
+    constexpr int gvec = GROWS * BC / VW, xvec = WG_FEAT * BC / VW, cpr = BC / VW;
+    constexpr int RG = (gvec + THREADS - 1) / THREADS;
+    constexpr int RX = (xvec + THREADS - 1) / THREADS;
     __shared__ __align__(16) E sX[WG_FEAT][PITCH];
     __shared__ __align__(16) E sG[GROWS][PITCH];
     __shared__ int sidx[64];
 
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-    const int T = a.T, I = a.I, H = a.H, B = a.B, BC = a.BC;
+    const int I = a.I, H = a.H, B = a.B;
     const int NC = I + H, G4 = 4 * H;
     const int n0 = blockIdx.y * WG_FEAT;
     const TS *Gc = (const TS *)a.Gc;
@@ -386,13 +407,13 @@ __global__ __launch_bounds__(THREADS) void wgrad_kernel(WgradArgs a) {
     const int AT = SPARSE ? (rcount + 31) / 32 : 1;
 
     const int nbc = (B + BC - 1) / BC;
-    const int niters = T * nbc;
-    const int gvec = GROWS * BC / VW, xvec = WG_FEAT * BC / VW, cpr = BC / VW;
+    const int niters = (a.t_end - a.t_begin) * nbc;
 
     V rg[RG], rx[RX];
     int ridx = -1;
     auto load = [&](int it) {
-        const int t = it / nbc, b0 = (it - t * nbc) * BC;
+        const int tl = it / nbc, b0 = (it - tl * nbc) * BC;
+        const int t = a.t_begin + tl;
         const TS *Gt = Gc + (long)t * a.Kp * B;
 #pragma unroll
         for (int i = 0; i < RG; ++i) {
@@ -433,7 +454,8 @@ __global__ __launch_bounds__(THREADS) void wgrad_kernel(WgradArgs a) {
             tmp[j][v] = 0.f;
 
     load(0);
-    const int hb = (lane >> 5) * (BC >> 1);
+    constexpr int HALF = BC / 2;
+    const int hb = (lane >> 5) * HALF;
     const int frow = wave * 32 + (lane & 31);
     for (int it = 0; it < niters; ++it) {
         const int bc = it % nbc;
@@ -466,7 +488,8 @@ __global__ __launch_bounds__(THREADS) void wgrad_kernel(WgradArgs a) {
 
         // MFMA over this batch chunk
         if constexpr (sizeof(TS) == 4) {
-            for (int s4 = 0; s4 < (BC >> 1); s4 += 4) {
+#pragma unroll
+            for (int s4 = 0; s4 < HALF; s4 += 4) {
                 const float4 av = *(const float4 *)&sX[frow][hb + s4];
 #pragma unroll
                 for (int tt = 0; tt < TT; ++tt) {
@@ -479,7 +502,8 @@ __global__ __launch_bounds__(THREADS) void wgrad_kernel(WgradArgs a) {
                 }
             }
         } else {
-            for (int s8 = 0; s8 < (BC >> 1); s8 += 8) {
+#pragma unroll
+            for (int s8 = 0; s8 < HALF; s8 += 8) {
                 const u16x8 av = *(const u16x8 *)&sX[frow][hb + s8];
 #pragma unroll
                 for (int tt = 0; tt < TT; ++tt) {
@@ -551,7 +575,7 @@ __global__ __launch_bounds__(THREADS) void wgrad_kernel(WgradArgs a) {
         for (int v = 0; v < 16; ++v) {
             const int f = n0 + wave * 32 + acc_row(lane, v);
             if (f < NC)
-                dst[f] = acc[at][v];
+                dst[f] = a.accumulate ? dst[f] + acc[at][v] : acc[at][v];
         }
     }
 }
@@ -670,15 +694,18 @@ __global__ __launch_bounds__(THREADS) void fwd_step_kernel(FwdArgs a) {
 int gemm1_tn(int N) { return N <= 32 ? 32 : 64; }
 int gemm1_tm(int N) { return 4096 / gemm1_tn(N); }
 
-hipError_t launch_gemm1(const Gemm1Args &a, bool bf16, hipStream_t s) {
+hipError_t launch_gemm1(Gemm1Args a, bool bf16, hipStream_t s) {
     const int TN = gemm1_tn(a.N), TM = 4096 / TN;
-    if (a.k_chunk > GEMM1_KC_MAX || a.k_chunk % GEMM1_TK != 0)
+    if (a.k_chunk % GEMM1_TK != 0 || a.splitk < 1 || a.steps < 1)
         return hipErrorInvalidValue;
-    dim3 grid((unsigned)ceil_div(a.M - a.m_begin, TM), (unsigned)ceil_div(a.N, TN), (unsigned)a.splitk);
-    const bool gather = a.idx != nullptr;
-    // 16-byte vector loads need 16-byte aligned rows and column offsets
+    // 16-byte vector loads need 16-byte aligned rows; the tile origin is
+    // rounded down to the vector width and rows below m_begin are not stored
     const int vw = bf16 ? 8 : 4;
-    const bool vec = a.ldw % vw == 0 && a.m_begin % vw == 0 && a.N % vw == 0;
+    const bool vec = a.ldw % vw == 0 && a.N % vw == 0;
+    a.m_lo = vec ? a.m_begin / vw * vw : a.m_begin;
+    dim3 grid((unsigned)ceil_div(a.M - a.m_lo, TM), (unsigned)ceil_div(a.N, TN),
+              (unsigned)(a.splitk * a.steps));
+    const bool gather = a.idx != nullptr;
 #define LSTMSS_G1(TS, TNV, GA, VE) hipLaunchKernelGGL((gemm1_kernel<TS, TNV, GA, VE>), grid, dim3(THREADS), 0, s, a)
 #define LSTMSS_G1V(TS, TNV, GA) do { if (vec) LSTMSS_G1(TS, TNV, GA, true); else LSTMSS_G1(TS, TNV, GA, false); } while (0)
     if (bf16) {
@@ -725,13 +752,19 @@ hipError_t launch_wgrad(WgradArgs a, bool sparse, bool bf16, hipStream_t s) {
             return hipErrorNotSupported;
         wgrad_tiles(a.P, a.R, a.S, &a.greg, &tt, &at);
     }
-    const int step = bf16 ? 32 : 8;
-    a.BC = (int)min((long)WG_BCMAX, ceil_div(a.B, step) * step);
+    // batch columns per stage: 16/32/64 (fp32) or 32/64 (bf16, whole MFMA k-blocks)
+    int bc = a.B <= 16 ? 16 : a.B <= 32 ? 32 : 64;
+    if (bf16 && bc < 32)
+        bc = 32;
+    a.BC = bc;
     const int vw = bf16 ? 8 : 4;
     const bool vec = a.B % vw == 0;
     const long groups = sparse ? ceil_div(ceil_div(4L * a.H / a.P, a.R), a.greg) : ceil_div(4L * a.H, 32);
     dim3 grid((unsigned)groups, (unsigned)ceil_div(a.I + a.H, WG_FEAT));
-#define LSTMSS_WG(TS, SP, TTV, VE) hipLaunchKernelGGL((wgrad_kernel<TS, SP, TTV, VE>), grid, dim3(THREADS), 0, s, a)
+#define LSTMSS_WG(TS, SP, TTV, VE) do { \
+        if (bc == 16) hipLaunchKernelGGL((wgrad_kernel<TS, SP, TTV, VE, 16>), grid, dim3(THREADS), 0, s, a); \
+        else if (bc == 32) hipLaunchKernelGGL((wgrad_kernel<TS, SP, TTV, VE, 32>), grid, dim3(THREADS), 0, s, a); \
+        else hipLaunchKernelGGL((wgrad_kernel<TS, SP, TTV, VE, 64>), grid, dim3(THREADS), 0, s, a); } while (0)
 #define LSTMSS_WGV(TS, SP, TTV) do { if (vec) LSTMSS_WG(TS, SP, TTV, true); else LSTMSS_WG(TS, SP, TTV, false); } while (0)
     if (bf16) {
         if (!sparse) LSTMSS_WGV(bf16_t, false, 1);

@@ -32,28 +32,32 @@ struct CellArgs {
     float *db;             // [4H] accumulated over kept rows, or NULL
     void *dbg;             // [4H][B] or NULL
     double *scores;        // [4H/P] or NULL
-    // reduction of the previous step's input gradient (dX[t+1]) from the
-    // split-K partials of the data-gradient product
-    const float *dx_part;
-    int dx_nparts;
-    long dx_stride;
-    float *dx_out;
-    long dx_n;
+    // split variant (large shapes): staging matrix and per-(row, chunk) sums
+    void *stage;           // [4H][B] gate gradient before selection (sparse)
+    double *chunk_sq;      // [4H][ceil(B/64)] fp64 chunk sums of squares
+    float *chunk_rs;       // [4H][ceil(B/64)] fp32 chunk row sums
 };
 
 // Data gradient [dx_t; dh_{t-1}] = W_c^T dG_c, split over K into partials.
+// One launch covers `steps` consecutive time steps (grid z = step * splitk +
+// split); step s reads Gc + s*gc_step, idx + s*idx_step and writes
+// part + s*out_step + split*part_stride.
 struct Gemm1Args {
     const void *W;         // [4H][ldw]
     long ldw;              // I + H
-    const void *Gc;        // [Kp][N]
-    const int32_t *idx;    // [Kp/P] kept slices, or NULL for identity rows
+    const void *Gc;        // [Kp][N] of the first step
+    const int32_t *idx;    // [Kp/P] kept slices of the first step, or NULL (identity)
     int P;
     long Kp;
     int M, m_begin, N;     // output rows [m_begin, M), columns N = B
-    float *part;           // [splitk][M][N]
-    long part_stride;      // M * N
+    int out_row0;          // output row m is stored at row m - out_row0
+    int m_lo;              // tile origin (m_begin rounded down for aligned loads; set by the launcher)
+    float *part;           // [splitk][rows][N] per step
+    long part_stride;      // rows * N
     int splitk;
     long k_chunk;
+    int steps;
+    long gc_step, idx_step, out_step;
 };
 
 // Weight gradient dW[rows] += dG_c [x_t; h_{t-1}]^T (rows scattered by idx).
@@ -81,7 +85,9 @@ struct WgradArgs {
     int P, R, S;
     int greg;              // regions per work-group group (sparse)
     int BC;                // batch columns staged per iteration
-    float *dW;             // [4H][I+H], written (not accumulated)
+    int t_begin, t_end;    // time steps [t_begin, t_end) of this launch
+    int accumulate;        // 0: dW = sum; 1: dW += sum
+    float *dW;             // [4H][I+H]
 };
 
 // One forward step: a = W [x_t; h_{t-1}] + b, activations, cell update.
@@ -100,7 +106,13 @@ struct FwdArgs {
 
 hipError_t launch_cell(const CellArgs &a, int mode, bool bf16, hipStream_t s);
 size_t cell_lds_bytes(const CellArgs &a, int mode);
-hipError_t launch_gemm1(const Gemm1Args &a, bool bf16, hipStream_t s);
+// True when launch_cell uses the split (element kernel + select kernel) path;
+// the bias gradient then comes from chunk_rs through launch_bias_grad.
+bool cell_split_ok(const CellArgs &a, int mode);
+hipError_t launch_bias_grad(float *db, const float *chunk_rs, int nch, long G, int t0, int t1,
+                            const int32_t *idx, int kept, int P, int R, int S, bool accumulate,
+                            hipStream_t s);
+hipError_t launch_gemm1(Gemm1Args a, bool bf16, hipStream_t s);
 hipError_t launch_gemm2(const Gemm2Args &a, bool bf16, hipStream_t s);
 // Returns hipErrorNotSupported when the structure needs more routing tiles
 // than the batched kernel holds (the caller then uses launch_gemm2 per step).
@@ -115,6 +127,7 @@ hipError_t launch_h0_store(void *dst, const float *src, long n, bool bf16, hipSt
 
 // Tile constants shared by the host-side sizing code.
 constexpr int GEMM1_TK = 32;
+constexpr int GEMM1_KC_MAX = 4096;
 int gemm1_tn(int N);
 int gemm1_tm(int N);
 

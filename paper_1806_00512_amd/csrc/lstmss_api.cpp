@@ -6,7 +6,9 @@
 #include <cmath>
 #include <cstdarg>
 #include <cstdio>
+#include <cstdlib>
 #include <cstring>
+#include <map>
 #include <mutex>
 #include <string>
 #include <vector>
@@ -82,13 +84,63 @@ hipError_t timed(int kind, hipStream_t st, F &&launch) {
     return e;
 }
 
+// Per-device side stream on which the weight gradient of finished time
+// steps runs while the sequential part of the backward pass continues on the
+// caller's stream.  Default priority; joined back before each call returns.
+constexpr int kMaxWgradChunks = 4;
+struct GraphEntry {
+    std::vector<uint64_t> key;
+    hipGraphExec_t exec = nullptr;
+    uint64_t last_use = 0;
+};
+struct SideStream {
+    hipStream_t s = nullptr;
+    hipStream_t cap = nullptr;  // capture stream for graph recording
+    hipEvent_t ev[kMaxWgradChunks] = {};
+    hipEvent_t join = nullptr;
+    hipEvent_t fork = nullptr;
+    std::vector<GraphEntry> graphs;  // instantiated backward calls, LRU
+    uint64_t use_clock = 0;
+    std::mutex mu;
+};
+constexpr size_t kMaxGraphs = 32;
+bool g_graphs = true;  // replay captured graphs (LSTMSS_GRAPHS=0 disables)
+std::mutex g_side_mu;
+std::map<int, SideStream> g_side;
+
+hipError_t side_stream(SideStream **out) {
+    int dev = 0;
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess)
+        return e;
+    std::lock_guard<std::mutex> lk(g_side_mu);
+    SideStream &ss = g_side[dev];
+    if (!ss.s) {
+        const char *env = getenv("LSTMSS_GRAPHS");
+        if (env && env[0] == '0')
+            g_graphs = false;
+        e = hipStreamCreateWithFlags(&ss.s, hipStreamNonBlocking);
+        if (e != hipSuccess)
+            return e;
+        if ((e = hipStreamCreateWithFlags(&ss.cap, hipStreamNonBlocking)) != hipSuccess)
+            return e;
+        if ((e = hipEventCreateWithFlags(&ss.fork, hipEventDisableTiming)) != hipSuccess)
+            return e;
+        for (int i = 0; i < kMaxWgradChunks; ++i)
+            if ((e = hipEventCreateWithFlags(&ss.ev[i], hipEventDisableTiming)) != hipSuccess)
+                return e;
+        if ((e = hipEventCreateWithFlags(&ss.join, hipEventDisableTiming)) != hipSuccess)
+            return e;
+    }
+    *out = &ss;
+    return hipSuccess;
+}
+
 size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
 long ceil_div(long a, long b) { return (a + b - 1) / b; }
 
 // LDS budget of the fused gate-gradient / selection kernel's work-group.
 constexpr size_t kMaxLds = 64 * 1024;
-// Largest K range one data-gradient work-group covers (its LDS row table).
-constexpr long kGemm1KcMax = 4096;
 
 int elem_bytes(int32_t dtype) { return dtype == LSTMSS_BF16 ? 2 : 4; }
 
@@ -176,8 +228,10 @@ CacheLayout cache_layout(const lstmss_dims *d) {
     return L;
 }
 
+// Split of the K' reduction of the critical-path data gradient (the dh rows
+// only) so that enough work-groups run; each split handles >= 128 rows.
 int splitk_for(const lstmss_dims *d, long Kp) {
-    const long M = (long)d->I + d->H;
+    const long M = d->H;
     const long tiles = ceil_div(M, gemm1_tm(d->B)) * ceil_div(d->B, gemm1_tn(d->B));
     long sk = ceil_div(512, tiles);
     const long max_sk = std::max(1L, Kp / (4L * GEMM1_TK));
@@ -186,7 +240,7 @@ int splitk_for(const lstmss_dims *d, long Kp) {
 }
 
 struct WsLayout {
-    size_t dc0, dc1, part, dGc, idx, db, total;
+    size_t dc0, dc1, part, dGc, idx, db, stage, chunk_sq, chunk_rs, total;
     int splitk;
     long k_chunk;
 };
@@ -195,20 +249,193 @@ WsLayout ws_layout(const lstmss_dims *d, const Plan &p) {
     const size_t es = elem_bytes(d->dtype);
     const size_t HB = (size_t)d->H * d->B;
     WsLayout L;
-    L.splitk = std::max<int>(splitk_for(d, p.Kp), (int)ceil_div(p.Kp, kGemm1KcMax));
+    L.splitk = splitk_for(d, p.Kp);
     L.k_chunk = ceil_div(ceil_div(p.Kp, L.splitk), GEMM1_TK) * GEMM1_TK;
     L.splitk = (int)ceil_div(p.Kp, L.k_chunk);
     size_t off = 0;
     L.dc0 = off; off += align256(HB * 4);
     L.dc1 = off; off += align256(HB * 4);
-    L.part = off; off += align256((size_t)L.splitk * ((size_t)d->I + d->H) * d->B * 4);
+    L.part = off; off += align256((size_t)L.splitk * HB * 4);
     L.dGc = off; off += align256((size_t)d->T * p.Kp * d->B * es);
     L.idx = off; off += align256((size_t)d->T * p.kept * 4);
     L.db = off; off += align256((size_t)4 * d->H * 4);
+    // split gate-kernel path: staging matrix, chunk sums of one step, chunk
+    // row sums of every step (for the bias gradient)
+    const size_t nch = (size_t)ceil_div(d->B, 64);
+    L.stage = off; off += align256((size_t)4 * d->H * d->B * es);
+    L.chunk_sq = off; off += align256((size_t)4 * d->H * nch * 8);
+    L.chunk_rs = off; off += align256((size_t)d->T * 4 * d->H * nch * 4);
     L.total = off;
     return L;
 }
 
+// Enqueue one backward call on main stream st, with side (locked by the
+// caller) for the off-critical-path work.  Arguments already checked.
+int32_t backward_enqueue(const lstmss_dims *d, bool dense, const Plan &p, const void *x,
+                         const void *W, const void *cache, const float *dH_up, const float *dhT,
+                         const float *dcT, float *dX, float *dW, float *db, float *dh0,
+                         float *dc0, int32_t *idx_out, void *dbg, void *ws, hipStream_t st,
+                         SideStream *side) {
+    const WsLayout L = ws_layout(d, p);
+    const bool bf16 = d->dtype == LSTMSS_BF16;
+    const bool sparse = !dense;
+    const int T = d->T, B = d->B, I = d->I, H = d->H;
+    const long HB = (long)H * B, G = 4L * H, K = (long)I + H;
+    const size_t es = elem_bytes(d->dtype);
+    const CacheLayout C = cache_layout(d);
+    const char *cb = (const char *)cache;
+    const char *gates = cb + C.gates;
+    const float *cst = (const float *)(cb + C.c);
+    const char *hst = cb + C.h;
+    char *wb = (char *)ws;
+    float *dcbuf[2] = {(float *)(wb + L.dc0), (float *)(wb + L.dc1)};
+    float *part = (float *)(wb + L.part);
+    char *dGc_all = wb + L.dGc;
+    int32_t *idx_all = idx_out ? idx_out : (int32_t *)(wb + L.idx);
+    float *dbp = db ? db : (float *)(wb + L.db);
+
+    // Work off the sequential critical path runs on a side stream, in chunks
+    // of time steps launched as soon as the gate gradients of their steps
+    // exist: the weight gradient (one batched launch per chunk when the
+    // structure fits its routing tiles, else a per-step accumulation on the
+    // main stream) and the input gradient dX (a batched data-gradient GEMM
+    // over the chunk's steps).  The main stream only carries the gate kernel
+    // and the dh rows of the data gradient for every step.
+    const bool batched = !sparse || wgrad_supported(p.P, p.R, p.S);
+    if (!batched)
+        HIP_TRY(timed(LSTMSS_KERNEL_AUX, st, [&] { return launch_fill(dW, G * K, 0.f, st); }));
+    // gate kernels: the split path (large shapes) leaves the bias gradient to
+    // one kernel after the time loop; the single-kernel paths accumulate it
+    CellArgs probe{};
+    probe.B = B; probe.H = H; probe.P = sparse ? p.P : 1; probe.R = sparse ? p.R : 1;
+    probe.regions_per_wg = sparse ? std::max(1, 32 / (p.R * p.P)) : 32;
+    const bool split = cell_split_ok(probe, sparse ? CELL_SPARSE : CELL_DENSE);
+    const int nch = (int)ceil_div(B, 64);
+    float *chunk_rs_all = (float *)(wb + L.chunk_rs);
+    if (!split)
+        HIP_TRY(timed(LSTMSS_KERNEL_AUX, st, [&] { return launch_fill(dbp, G, 0.f, st); }));
+
+    const bool use_side = batched || dX;
+    int chunk_len = T, next_chunk = 0;
+    if (use_side) {
+        const int nchunks = std::max(1, std::min(kMaxWgradChunks, T / 8));
+        chunk_len = (int)ceil_div(T, nchunks);
+    }
+    WgradArgs wg{};
+    wg.Gc = dGc_all; wg.idx = sparse ? idx_all : nullptr; wg.x = x; wg.h = hst;
+    wg.T = T; wg.I = I; wg.H = H; wg.B = B; wg.Kp = (int)p.Kp; wg.kept = (int)p.kept;
+    wg.P = p.P; wg.R = p.R; wg.S = p.S; wg.dW = dW;
+
+    Gemm1Args gx{};  // dX[t] = (W_c rows [0, I))^T dG_c, several steps per launch
+    gx.W = W; gx.ldw = K; gx.P = p.P; gx.Kp = p.Kp; gx.M = I; gx.m_begin = 0; gx.N = B;
+    gx.out_row0 = 0; gx.part_stride = 0; gx.splitk = 1;
+    gx.k_chunk = ceil_div(p.Kp, GEMM1_TK) * GEMM1_TK;
+    gx.gc_step = p.Kp * B; gx.idx_step = p.kept; gx.out_step = (long)I * B;
+
+    const long part_stride = HB;
+    for (int t = T - 1; t >= 0; --t) {
+        const bool last = t == T - 1;
+        char *dGc = dGc_all + (size_t)t * p.Kp * B * es;
+        int32_t *idx = idx_all + (size_t)t * p.kept;
+
+        CellArgs ca{};
+        ca.B = B; ca.H = H; ca.I = I;
+        ca.P = sparse ? p.P : 1; ca.R = sparse ? p.R : 1; ca.S = sparse ? p.S : 0;
+        ca.nslices = sparse ? p.nslices : G;
+        if (sparse)
+            ca.regions_per_wg = std::max(1, 32 / (p.R * p.P));
+        else
+            ca.regions_per_wg = 32;  // dense: 32 rows per work-group
+        ca.gates = gates + (size_t)t * G * B * es;
+        ca.c_t = cst + (size_t)(t + 1) * HB;
+        ca.c_prev = cst + (size_t)t * HB;
+        ca.dH_up = dH_up + (size_t)t * HB;
+        if (last) {
+            ca.dh_part = dhT;
+            ca.dh_nparts = dhT ? 1 : 0;
+            ca.dh_stride = 0;
+            ca.dc_in = dcT;
+        } else {
+            ca.dh_part = part;
+            ca.dh_nparts = L.splitk;
+            ca.dh_stride = part_stride;
+            ca.dc_in = dcbuf[(t + 1) & 1];
+        }
+        ca.dc_out = dcbuf[t & 1];
+        ca.dGc = dGc;
+        ca.idx = sparse ? idx : nullptr;
+        ca.db = dbp;
+        ca.dbg = dbg ? (char *)dbg + (size_t)t * G * B * es : nullptr;
+        ca.scores = nullptr;
+        if (split) {
+            ca.db = nullptr;
+            ca.stage = wb + L.stage;
+            ca.chunk_sq = (double *)(wb + L.chunk_sq);
+            ca.chunk_rs = chunk_rs_all + (size_t)t * G * nch;
+        }
+        if (!split &&
+            cell_lds_bytes(ca, sparse ? CELL_SPARSE : CELL_DENSE) > kMaxLds)
+            return fail(LSTMSS_ERR_UNSUPPORTED, "R*P*B too large for one work-group's LDS");
+        HIP_TRY(timed(LSTMSS_KERNEL_GATES, st, [&] { return launch_cell(ca, sparse ? CELL_SPARSE : CELL_DENSE, bf16, st); }));
+
+        // chunk c covers steps [T - (c+1)*len, T - c*len); launch its side
+        // work once its lowest step has its gate gradients
+        if (use_side && t == std::max(0, T - (next_chunk + 1) * chunk_len)) {
+            const int c = next_chunk++;
+            const int hi = T - c * chunk_len;
+            HIP_TRY(hipEventRecord(side->ev[c], st));
+            HIP_TRY(hipStreamWaitEvent(side->s, side->ev[c], 0));
+            if (batched) {
+                wg.t_begin = t;
+                wg.t_end = hi;
+                wg.accumulate = c > 0;
+                HIP_TRY(timed(LSTMSS_KERNEL_WEIGHT_GRAD, side->s, [&] { return launch_wgrad(wg, sparse, bf16, side->s); }));
+            }
+            if (dX) {
+                gx.Gc = dGc;
+                gx.idx = sparse ? idx : nullptr;
+                gx.part = dX + (size_t)t * I * B;
+                gx.steps = hi - t;
+                HIP_TRY(timed(LSTMSS_KERNEL_DATA_GRAD, side->s, [&] { return launch_gemm1(gx, bf16, side->s); }));
+            }
+        }
+
+        // dh rows of the data gradient for the next (earlier) step
+        Gemm1Args g1{};
+        g1.W = W; g1.ldw = K; g1.Gc = dGc; g1.idx = sparse ? idx : nullptr; g1.P = p.P;
+        g1.Kp = p.Kp; g1.M = (int)K; g1.m_begin = I; g1.N = B; g1.out_row0 = I;
+        g1.part = part; g1.part_stride = part_stride; g1.splitk = L.splitk;
+        g1.k_chunk = L.k_chunk; g1.steps = 1;
+        HIP_TRY(timed(LSTMSS_KERNEL_DATA_GRAD, st, [&] { return launch_gemm1(g1, bf16, st); }));
+
+        if (!batched) {
+            Gemm2Args g2{};
+            g2.Gc = dGc; g2.idx = sparse ? idx : nullptr; g2.P = p.P; g2.Kp = p.Kp;
+            g2.xt = (const char *)x + (size_t)t * I * B * es;
+            g2.hp = hst + (size_t)t * HB * es;
+            g2.I = I; g2.H = H; g2.B = B; g2.dW = dW;
+            HIP_TRY(timed(LSTMSS_KERNEL_WEIGHT_GRAD, st, [&] { return launch_gemm2(g2, bf16, st); }));
+        }
+    }
+    if (use_side) {
+        HIP_TRY(hipEventRecord(side->join, side->s));
+        HIP_TRY(hipStreamWaitEvent(st, side->join, 0));
+    }
+    if (split)
+        HIP_TRY(timed(LSTMSS_KERNEL_AUX, st, [&] {
+            return launch_bias_grad(dbp, chunk_rs_all, nch, G, 0, T, sparse ? idx_all : nullptr,
+                                    (int)p.kept, p.P, p.R, p.S, false, st);
+        }));
+    if (dh0)
+        HIP_TRY(timed(LSTMSS_KERNEL_AUX, st, [&] { return launch_reduce_parts(dh0, part, L.splitk, part_stride, HB, st); }));
+    if (dc0)
+        HIP_TRY(timed(LSTMSS_KERNEL_AUX, st, [&] { return launch_copy_in(dc0, dcbuf[0], HB, st); }));
+    return LSTMSS_OK;
+}
+
+// A backward call is a fixed DAG of launches for given arguments, so it is
+// captured once into a HIP graph (main and side streams joined by events)
+// and replayed; the key is every argument that reaches a kernel.
 int32_t backward(const lstmss_dims *d, bool dense, float sparsity, const lstmss_structure *s,
                  const void *x, const void *W, const void *cache, const float *dH_up,
                  const float *dhT, const float *dcT, float *dX, float *dW, float *db, float *dh0,
@@ -227,108 +454,61 @@ int32_t backward(const lstmss_dims *d, bool dense, float sparsity, const lstmss_
     if (ws_bytes < L.total)
         return fail(LSTMSS_ERR_WORKSPACE, "workspace of %zu bytes, need %zu", ws_bytes, L.total);
     hipStream_t st = (hipStream_t)stream;
-    const bool bf16 = d->dtype == LSTMSS_BF16;
-    const bool sparse = !dense;
-    const int T = d->T, B = d->B, I = d->I, H = d->H;
-    const long HB = (long)H * B, G = 4L * H, K = (long)I + H;
-    const size_t es = elem_bytes(d->dtype);
-    const CacheLayout C = cache_layout(d);
-    const char *cb = (const char *)cache;
-    const char *gates = cb + C.gates;
-    const float *cst = (const float *)(cb + C.c);
-    const char *hst = cb + C.h;
-    char *wb = (char *)ws;
-    float *dcbuf[2] = {(float *)(wb + L.dc0), (float *)(wb + L.dc1)};
-    float *part = (float *)(wb + L.part);
-    char *dGc_all = wb + L.dGc;
-    int32_t *idx_all = idx_out ? idx_out : (int32_t *)(wb + L.idx);
-    float *dbp = db ? db : (float *)(wb + L.db);
-
-    // weight gradient: one batched launch after the time loop when the
-    // structure fits its routing tiles, else a per-step accumulation
-    const bool batched = !sparse || wgrad_supported(p.P, p.R, p.S);
-    if (!batched)
-        HIP_TRY(timed(LSTMSS_KERNEL_AUX, st, [&] { return launch_fill(dW, G * K, 0.f, st); }));
-    HIP_TRY(timed(LSTMSS_KERNEL_AUX, st, [&] { return launch_fill(dbp, G, 0.f, st); }));
-
-    const long part_stride = K * B;
-    const int m_begin = dX ? 0 : I;
-    for (int t = T - 1; t >= 0; --t) {
-        const bool last = t == T - 1;
-        char *dGc = dGc_all + (size_t)t * p.Kp * B * es;
-        int32_t *idx = idx_all + (size_t)t * p.kept;
-
-        CellArgs ca{};
-        ca.B = B; ca.H = H; ca.I = I;
-        ca.P = sparse ? p.P : 1; ca.R = sparse ? p.R : 1; ca.S = sparse ? p.S : 0;
-        ca.nslices = sparse ? p.nslices : G;
-        ca.regions_per_wg = 1;
-        if (sparse) {
-            const int rows_per_region = p.R * p.P;
-            ca.regions_per_wg = std::max(1, 32 / rows_per_region);
-        } else {
-            ca.regions_per_wg = 32;  // dense: 32 rows per work-group
-        }
-        ca.gates = gates + (size_t)t * G * B * es;
-        ca.c_t = cst + (size_t)(t + 1) * HB;
-        ca.c_prev = cst + (size_t)t * HB;
-        ca.dH_up = dH_up + (size_t)t * HB;
-        if (last) {
-            ca.dh_part = dhT;
-            ca.dh_nparts = dhT ? 1 : 0;
-            ca.dh_stride = 0;
-            ca.dc_in = dcT;
-        } else {
-            ca.dh_part = part + (size_t)I * B;
-            ca.dh_nparts = L.splitk;
-            ca.dh_stride = part_stride;
-            ca.dc_in = dcbuf[(t + 1) & 1];
-        }
-        ca.dc_out = dcbuf[t & 1];
-        ca.dGc = dGc;
-        ca.idx = sparse ? idx : nullptr;
-        ca.db = dbp;
-        ca.dbg = dbg ? (char *)dbg + (size_t)t * G * B * es : nullptr;
-        ca.scores = nullptr;
-        if (!last && dX) {
-            ca.dx_part = part;
-            ca.dx_nparts = L.splitk;
-            ca.dx_stride = part_stride;
-            ca.dx_out = dX + (size_t)(t + 1) * I * B;
-            ca.dx_n = (long)I * B;
-        }
-        if (cell_lds_bytes(ca, sparse ? CELL_SPARSE : CELL_DENSE) > kMaxLds)
-            return fail(LSTMSS_ERR_UNSUPPORTED, "R*P*B too large for one work-group's LDS");
-        HIP_TRY(timed(LSTMSS_KERNEL_GATES, st, [&] { return launch_cell(ca, sparse ? CELL_SPARSE : CELL_DENSE, bf16, st); }));
-
-        Gemm1Args g1{};
-        g1.W = W; g1.ldw = K; g1.Gc = dGc; g1.idx = sparse ? idx : nullptr; g1.P = p.P;
-        g1.Kp = p.Kp; g1.M = (int)K; g1.m_begin = m_begin; g1.N = B;
-        g1.part = part; g1.part_stride = part_stride; g1.splitk = L.splitk; g1.k_chunk = L.k_chunk;
-        HIP_TRY(timed(LSTMSS_KERNEL_DATA_GRAD, st, [&] { return launch_gemm1(g1, bf16, st); }));
-
-        if (!batched) {
-            Gemm2Args g2{};
-            g2.Gc = dGc; g2.idx = sparse ? idx : nullptr; g2.P = p.P; g2.Kp = p.Kp;
-            g2.xt = (const char *)x + (size_t)t * I * B * es;
-            g2.hp = hst + (size_t)t * HB * es;
-            g2.I = I; g2.H = H; g2.B = B; g2.dW = dW;
-            HIP_TRY(timed(LSTMSS_KERNEL_WEIGHT_GRAD, st, [&] { return launch_gemm2(g2, bf16, st); }));
-        }
+    SideStream *side = nullptr;
+    HIP_TRY(side_stream(&side));
+    std::unique_lock<std::mutex> lk(side->mu);
+    bool timing;
+    {
+        std::lock_guard<std::mutex> tl(g_tmu);
+        timing = g_timing;
     }
-    if (batched) {
-        WgradArgs wg{};
-        wg.Gc = dGc_all; wg.idx = sparse ? idx_all : nullptr; wg.x = x; wg.h = hst;
-        wg.T = T; wg.I = I; wg.H = H; wg.B = B; wg.Kp = (int)p.Kp; wg.kept = (int)p.kept;
-        wg.P = p.P; wg.R = p.R; wg.S = p.S; wg.dW = dW;
-        HIP_TRY(timed(LSTMSS_KERNEL_WEIGHT_GRAD, st, [&] { return launch_wgrad(wg, sparse, bf16, st); }));
+    if (!g_graphs || timing)
+        return backward_enqueue(d, dense, p, x, W, cache, dH_up, dhT, dcT, dX, dW, db, dh0, dc0,
+                                idx_out, dbg, ws, st, side);
+
+    auto u = [](const void *q) { return (uint64_t)(uintptr_t)q; };
+    std::vector<uint64_t> key = {(uint64_t)d->T, (uint64_t)d->B, (uint64_t)d->I, (uint64_t)d->H,
+                                 (uint64_t)d->dtype, (uint64_t)dense, (uint64_t)p.P,
+                                 (uint64_t)p.R, (uint64_t)p.S, u(x), u(W), u(cache), u(dH_up),
+                                 u(dhT), u(dcT), u(dX), u(dW), u(db), u(dh0), u(dc0), u(idx_out),
+                                 u(dbg), u(ws)};
+    GraphEntry *hit = nullptr;
+    for (GraphEntry &g : side->graphs)
+        if (g.key == key)
+            hit = &g;
+    if (!hit) {
+        // record on the private capture stream; the side stream joins the
+        // capture through the fork/join events inside backward_enqueue
+        HIP_TRY(hipStreamBeginCapture(side->cap, hipStreamCaptureModeRelaxed));
+        rc = backward_enqueue(d, dense, p, x, W, cache, dH_up, dhT, dcT, dX, dW, db, dh0, dc0,
+                              idx_out, dbg, ws, side->cap, side);
+        hipGraph_t graph = nullptr;
+        const hipError_t ec = hipStreamEndCapture(side->cap, &graph);
+        if (rc != LSTMSS_OK) {
+            if (graph)
+                (void)hipGraphDestroy(graph);
+            return rc;
+        }
+        if (ec != hipSuccess)
+            return fail(LSTMSS_ERR_HIP, "graph capture failed: %s", hipGetErrorString(ec));
+        hipGraphExec_t exec = nullptr;
+        const hipError_t ei = hipGraphInstantiate(&exec, graph, nullptr, nullptr, 0);
+        (void)hipGraphDestroy(graph);
+        if (ei != hipSuccess)
+            return fail(LSTMSS_ERR_HIP, "graph instantiation failed: %s", hipGetErrorString(ei));
+        if (side->graphs.size() >= kMaxGraphs) {
+            size_t oldest = 0;
+            for (size_t i = 1; i < side->graphs.size(); ++i)
+                if (side->graphs[i].last_use < side->graphs[oldest].last_use)
+                    oldest = i;
+            (void)hipGraphExecDestroy(side->graphs[oldest].exec);
+            side->graphs.erase(side->graphs.begin() + oldest);
+        }
+        side->graphs.push_back(GraphEntry{key, exec, 0});
+        hit = &side->graphs.back();
     }
-    if (dX)
-        HIP_TRY(timed(LSTMSS_KERNEL_AUX, st, [&] { return launch_reduce_parts(dX, part, L.splitk, part_stride, (long)I * B, st); }));
-    if (dh0)
-        HIP_TRY(timed(LSTMSS_KERNEL_AUX, st, [&] { return launch_reduce_parts(dh0, part + (size_t)I * B, L.splitk, part_stride, HB, st); }));
-    if (dc0)
-        HIP_TRY(timed(LSTMSS_KERNEL_AUX, st, [&] { return launch_copy_in(dc0, dcbuf[0], HB, st); }));
+    hit->last_use = ++side->use_clock;
+    HIP_TRY(hipGraphLaunch(hit->exec, st));
     return LSTMSS_OK;
 }
 
@@ -457,6 +637,20 @@ int32_t lstmss_select_compact(const lstmss_dims *d, float sparsity, const lstmss
     hipStream_t st = (hipStream_t)stream;
     HIP_TRY(timed(LSTMSS_KERNEL_GATES, st, [&] { return launch_cell(ca, CELL_GIVEN, d->dtype == LSTMSS_BF16, st); }));
     return LSTMSS_OK;
+}
+
+int32_t lstmss_set_option(int32_t option, int32_t value) {
+    std::lock_guard<std::mutex> lk(g_side_mu);
+    for (auto &kv : g_side) {  // graphs recorded under the old setting are dropped
+        std::lock_guard<std::mutex> l2(kv.second.mu);
+        for (GraphEntry &g : kv.second.graphs)
+            (void)hipGraphExecDestroy(g.exec);
+        kv.second.graphs.clear();
+    }
+    switch (option) {
+    case LSTMSS_OPT_GRAPHS: g_graphs = value != 0; return LSTMSS_OK;
+    default: return fail(LSTMSS_ERR_INVALID_ARG, "unknown option %d", option);
+    }
 }
 
 int32_t lstmss_timing_enable(int32_t on) {

@@ -31,8 +31,8 @@ ERR = {0: "ok", -1: "invalid argument", -2: "unsupported", -3: "workspace too sm
 # Exported symbols of include/lstmss.h
 SYMBOLS = ("lstmss_version", "lstmss_strerror", "lstmss_last_error", "lstmss_cache_bytes",
            "lstmss_kept_rows", "lstmss_workspace_bytes", "lstm_fwd_cache", "lstm_bwd_dense",
-           "lstm_bwd_structsparse", "lstmss_select_compact", "lstmss_timing_enable",
-           "lstmss_timing_read", "lstmss_timing_reset")
+           "lstm_bwd_structsparse", "lstmss_select_compact", "lstmss_set_option",
+           "lstmss_timing_enable", "lstmss_timing_read", "lstmss_timing_reset")
 KERNEL_KINDS = {"gates_select_compact": 0, "data_grad_gemm": 1, "weight_grad_gemm": 2, "aux": 3,
                 "forward_step": 4}
 
@@ -86,6 +86,8 @@ def load():
     lib.lstm_bwd_structsparse.restype = i32
     lib.lstmss_select_compact.argtypes = [pd, f, ps, vp, vp, vp, vp, vp]
     lib.lstmss_select_compact.restype = i32
+    lib.lstmss_set_option.argtypes = [i32, i32]
+    lib.lstmss_set_option.restype = i32
     lib.lstmss_timing_enable.argtypes = [i32]
     lib.lstmss_timing_enable.restype = i32
     lib.lstmss_timing_read.argtypes = [i32, ctypes.POINTER(ctypes.c_double),
@@ -286,6 +288,19 @@ def cache_views(cache, T, B, H, dtype):
     c = cache[c_off:c_off + c_bytes].view(torch.float32).view(T + 1, H, B)
     h = cache[h_off:h_off + (T + 1) * H * B * es].view(st).view(T + 1, H, B)
     return gates, c, h
+
+
+OPTIONS = {"graphs": 0}
+
+
+def set_option(name: str, value: int):
+    """Execution options of include/lstmss.h (graphs); results are identical
+    under every setting."""
+    _check(load().lstmss_set_option(OPTIONS[name], int(value)), "lstmss_set_option")
+
+
+def graphs_enable(on: bool = True):
+    set_option("graphs", 1 if on else 0)
 
 
 def timing_enable(on: bool = True):

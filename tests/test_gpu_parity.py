@@ -178,14 +178,32 @@ def test_select_nan_is_kept(L):
     (1, 32, 128, 128, 0.5, 8, False),   # one step
     (3, 20, 24, 64, 0.25, 16, False),   # 48 kept rows per region: two routing tiles
     (2, 8, 16, 64, 0.5, 64, False),     # 128 kept rows per region: per-step weight gradient
+    (2, 256, 32, 64, 0.5, 8, True),     # four 64-column passes per row
+    (3, 200, 40, 32, 0.75, 8, False),   # ragged last pass
+    (2, 130, 16, 96, 0.5, 2, False),    # small regions (R*P = 8)
 ])
 def test_layer_sparse_f32(L, T, B, I, H, sp, R, state):
     d = make_layer(T, B, I, H, seed=T * 100 + H, w_scale=0.2, state=state)
     check_layer(L, d, "f32", sp, R=R)
 
 
-def test_layer_dense_f32(L):
-    d = make_layer(5, 20, 100, 72, seed=9, w_scale=0.2, state=True)
+@pytest.mark.parametrize("T,B,I,H,sp,R,dtype,dense", [
+    (2, 256, 32, 256, 0.5, 8, "f32", False),     # H*B = 65536: split gate kernels
+    (3, 200, 40, 400, 0.25, 8, "f32", False),    # ragged last batch chunk
+    (2, 256, 24, 260, 0.5, 8, "f32", False),     # unaligned H: regions straddle gates, partial region
+    (2, 256, 64, 256, 0.5, 8, "bf16", False),
+    (2, 128, 48, 512, 0.75, 4, "f32", False),
+    (2, 256, 32, 256, 0.0, 8, "f32", True),
+    (2, 256, 32, 256, 0.0, 8, "bf16", True),
+])
+def test_layer_split_path(L, T, B, I, H, sp, R, dtype, dense):
+    d = make_layer(T, B, I, H, seed=T + B + H, w_scale=0.1, dtype=dtype, state=True)
+    check_layer(L, d, dtype, sp, R=R, dense=dense)
+
+
+@pytest.mark.parametrize("T,B,I,H", [(5, 20, 100, 72), (3, 150, 40, 64)])
+def test_layer_dense_f32(L, T, B, I, H):
+    d = make_layer(T, B, I, H, seed=9 + B, w_scale=0.2, state=True)
     check_layer(L, d, "f32", 0.0, dense=True)
 
 
@@ -212,6 +230,35 @@ def test_sparsity_zero_equals_dense(L):
     for k in ("dX", "dW", "db", "dh0", "dc0"):
         assert torch.equal(a[k], b[k]), k
     assert torch.equal(b["idx"].cpu(), torch.arange(64, dtype=torch.int32).repeat(4, 1))
+
+
+@pytest.mark.parametrize("H,sp", [(72, 0.5), (64, 0.5), (64, 0.0)])
+def test_graph_replay_matches_direct(L, H, sp):
+    """Captured-and-replayed calls give the same bits as direct launches,
+    on every replay, with other work in between."""
+    d = make_layer(4, 20, 40, H, seed=14, w_scale=0.2, state=True)
+    x, W, dH = gpu_tensor(d["x"]), gpu_tensor(d["W"]), gpu_tensor(d["dH_up"])
+    dhT, dcT = gpu_tensor(d["dhT"]), gpu_tensor(d["dcT"])
+    _, cache = L.fwd_cache(x, W)
+    L.graphs_enable(False)
+    try:
+        ref = L.bwd_structsparse(x, W, cache, dH, sp, dhT=dhT, dcT=dcT)
+        torch.cuda.synchronize()
+    finally:
+        L.graphs_enable(True)
+    d0 = L.dims(4, 20, 40, H)
+    ws = torch.empty(L.workspace_bytes(d0, sp, L.structure(4, 8) if sp else None),
+                     dtype=torch.uint8, device=dev())
+    out = {k: torch.empty_like(v) for k, v in ref.items() if v is not None}
+    for rep in range(3):
+        for v in out.values():
+            v.fill_(float("nan") if v.dtype.is_floating_point else -7)
+        torch.cuda.synchronize()
+        o = L.bwd_structsparse(x, W, cache, dH, sp, dhT=dhT, dcT=dcT, out=out, ws=ws)
+        torch.cuda.synchronize()
+        for k in ("dX", "dW", "db", "dh0", "dc0", "idx"):
+            assert torch.equal(o[k], ref[k]), (rep, k)
+        torch.randn(1000, device=dev()).sum().item()  # unrelated eager work between replays
 
 
 def test_deterministic(L):
