@@ -542,15 +542,24 @@ __global__ __launch_bounds__(SK_WAVES * 64) void cell_select_kernel2(CellArgs a)
             sslot[j] = slot;
     }
     __syncthreads();
-    // copy kept rows (P rows of B columns per kept slice), 16-byte chunks
-    // when rows are 16-byte aligned
-    const TS *stage = (const TS *)a.stage;
-    TS *dGc = (TS *)a.dGc;
-    for (int q = tid; q < nrows * B; q += SK_WAVES * 64) {
-        const int lr = q / B, bb = q - lr * B;
+    // copy kept rows (P rows of B columns per kept slice): a wavefront per
+    // row, 16-byte vectors when a row is a whole number of them
+    const char *stage = (const char *)a.stage;
+    char *dGc = (char *)a.dGc;
+    const int rowbytes = B * (int)sizeof(TS);
+    for (int lr = wave; lr < nrows; lr += SK_WAVES) {
         const int slot = sslot[lr / P];
-        if (slot >= 0)
-            dGc[((long)slot * P + lr % P) * B + bb] = stage[(long)(row0 + lr) * B + bb];
+        if (slot < 0)
+            continue;
+        const char *src = stage + (long)(row0 + lr) * rowbytes;
+        char *dst = dGc + ((long)slot * P + lr % P) * rowbytes;
+        if ((rowbytes & 15) == 0) {
+            for (int v = lane; v < rowbytes / 16; v += 64)
+                ((uint4 *)dst)[v] = ((const uint4 *)src)[v];
+        } else {
+            for (int e = lane; e < B; e += 64)
+                ((TS *)dst)[e] = ((const TS *)src)[e];
+        }
     }
 }
 

@@ -364,21 +364,43 @@ __global__ __launch_bounds__(THREADS) void gemm2_kernel(Gemm2Args a) {
 constexpr int WG_FEAT = 128;
 constexpr int WG_ATMAX = 4;
 
-template <typename TS, bool SPARSE, int TT, bool VEC, int BC>
-__global__ __launch_bounds__(THREADS) void wgrad_kernel(WgradArgs a) {
+constexpr int WG_NG = 2;   // row groups per work-group
+constexpr int WG_FT = 2;   // 32-feature tiles per wavefront
+
+// Stores a staged vector into an LDS row (one 16-byte store when whole).
+template <typename E, typename V>
+__device__ __forceinline__ void lds_store_vec(E *dst, const V &v) {
+    if constexpr (V::W * sizeof(E) == 16) {
+        typedef E e16 __attribute__((ext_vector_type(16 / sizeof(E))));
+        e16 t;
+#pragma unroll
+        for (int e = 0; e < V::W; ++e)
+            t[e] = v.v[e];
+        *(e16 *)dst = t;
+    } else {
+#pragma unroll
+        for (int e = 0; e < V::W; ++e)
+            dst[e] = v.v[e];
+    }
+}
+
+template <typename TS, bool SPARSE, int TT, int ATN, bool VEC, int BC>
+__global__ __launch_bounds__(THREADS, 2) void wgrad_kernel(WgradArgs a) {
     using E = typename std::conditional<sizeof(TS) == 4, float, uint16_t>::type;
     constexpr int PITCH = BC + (sizeof(TS) == 4 ? 4 : 8);
-    constexpr int GROWS = TT * 32;
+    constexpr int GROWS = TT * 32;                // temporary-tile rows per group
     using V = Vec<TS, VEC>;
     constexpr int VW = V::W;
-    constexpr int gvec = GROWS * BC / VW, xvec = WG_FEAT * BC / VW, cpr = BC / VW;
+    constexpr int cpr = BC / VW;
+    constexpr int gvec = WG_NG * GROWS * cpr, xvec = WG_FEAT * cpr;
     constexpr int RG = (gvec + THREADS - 1) / THREADS;
     constexpr int RX = (xvec + THREADS - 1) / THREADS;
     __shared__ __align__(16) E sX[WG_FEAT][PITCH];
-    __shared__ __align__(16) E sG[GROWS][PITCH];
-    __shared__ int sidx[64];
+    __shared__ __align__(16) E sG[WG_NG * GROWS][PITCH];
+    __shared__ int sidx[WG_NG][64];
 
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int fh = wave & 1, gi = wave >> 1;      // feature half, group of this wavefront
     const int I = a.I, H = a.H, B = a.B;
     const int NC = I + H, G4 = 4 * H;
     const int n0 = blockIdx.y * WG_FEAT;
@@ -386,25 +408,38 @@ __global__ __launch_bounds__(THREADS) void wgrad_kernel(WgradArgs a) {
     const TS *x = (const TS *)a.x;
     const TS *h = (const TS *)a.h;
 
-    // group geometry
-    int r0, rcount, c0, ccount, q0 = 0, qcount = 0, j0 = 0;
+    // geometry of group g: original rows [r0, r0 + rcount), compacted rows
+    // [c0, c0 + ccount), kept-slice entries [q0, q0 + qcount), first slice j0
     const int rp = a.R * a.P, kr = (a.R - a.S) * a.P, ks = a.R - a.S;
-    if (SPARSE) {
-        const int g = blockIdx.x;
-        r0 = g * a.greg * rp;
-        rcount = min(a.greg * rp, G4 - r0);
-        c0 = g * a.greg * kr;
-        ccount = min(a.greg * kr, a.Kp - c0);
-        q0 = g * a.greg * ks;
-        qcount = min(a.greg * ks, a.kept - q0);
-        j0 = g * a.greg * a.R;
-    } else {
-        r0 = blockIdx.x * 32;
-        rcount = min(32, G4 - r0);
-        c0 = r0;
-        ccount = rcount;
-    }
+    auto geom = [&](int g, int &r0, int &rcount, int &c0, int &ccount, int &q0, int &qcount,
+                    int &j0) {
+        if (SPARSE) {
+            r0 = g * a.greg * rp;
+            rcount = max(0, min(a.greg * rp, G4 - r0));
+            c0 = g * a.greg * kr;
+            ccount = max(0, min(a.greg * kr, a.Kp - c0));
+            q0 = g * a.greg * ks;
+            qcount = max(0, min(a.greg * ks, a.kept - q0));
+            j0 = g * a.greg * a.R;
+        } else {
+            r0 = g * 32;
+            rcount = max(0, min(32, G4 - r0));
+            c0 = r0;
+            ccount = rcount;
+            q0 = qcount = j0 = 0;
+        }
+    };
+    int r0, rcount, c0, ccount, q0, qcount, j0;
+    geom(blockIdx.x * WG_NG + gi, r0, rcount, c0, ccount, q0, qcount, j0);
     const int AT = SPARSE ? (rcount + 31) / 32 : 1;
+    // compacted-row origin and count of both groups, for the loaders
+    int lc0[WG_NG], lcc[WG_NG], lq0[WG_NG], lqc[WG_NG];
+#pragma unroll
+    for (int k = 0; k < WG_NG; ++k) {
+        int t0, t1, t2, t3;
+        geom(blockIdx.x * WG_NG + k, t0, t1, lc0[k], lcc[k], lq0[k], lqc[k], t2);
+        (void)t3;
+    }
 
     const int nbc = (B + BC - 1) / BC;
     const int niters = (a.t_end - a.t_begin) * nbc;
@@ -419,9 +454,10 @@ __global__ __launch_bounds__(THREADS) void wgrad_kernel(WgradArgs a) {
         for (int i = 0; i < RG; ++i) {
             const int q = tid + i * THREADS;
             const int rho = q / cpr, bb = (q - rho * cpr) * VW;
+            const int k = rho / GROWS, lr = rho - k * GROWS;
             const int b = b0 + bb;
-            if (q < gvec && rho < ccount && b < B)
-                rg[i].load(Gt + (long)(c0 + rho) * B + b, B - b);
+            if (q < gvec && lr < lcc[k & (WG_NG - 1)] && b < B)
+                rg[i].load(Gt + (long)(lc0[k & (WG_NG - 1)] + lr) * B + b, B - b);
             else
                 rg[i].zero();
         }
@@ -437,37 +473,38 @@ __global__ __launch_bounds__(THREADS) void wgrad_kernel(WgradArgs a) {
                 rx[i].zero();
             }
         }
-        if (SPARSE && b0 == 0 && tid < qcount)
-            ridx = a.idx[(long)t * a.kept + q0 + tid];
+        if (SPARSE && b0 == 0 && tid < WG_NG * 64) {
+            const int k = tid >> 6, e = tid & 63;
+            ridx = e < lqc[k] ? a.idx[(long)t * a.kept + lq0[k] + e] : -1;
+        }
     };
 
-    f32x16 acc[WG_ATMAX], tmp[TT];
+    f32x16 acc[WG_FT][ATN], tmp[WG_FT][TT];
 #pragma unroll
-    for (int j = 0; j < WG_ATMAX; ++j)
+    for (int ft = 0; ft < WG_FT; ++ft) {
 #pragma unroll
-        for (int v = 0; v < 16; ++v)
-            acc[j][v] = 0.f;
+        for (int j = 0; j < ATN; ++j)
 #pragma unroll
-    for (int j = 0; j < TT; ++j)
+            for (int v = 0; v < 16; ++v)
+                acc[ft][j][v] = 0.f;
 #pragma unroll
-        for (int v = 0; v < 16; ++v)
-            tmp[j][v] = 0.f;
+        for (int j = 0; j < TT; ++j)
+#pragma unroll
+            for (int v = 0; v < 16; ++v)
+                tmp[ft][j][v] = 0.f;
+    }
 
     load(0);
     constexpr int HALF = BC / 2;
     const int hb = (lane >> 5) * HALF;
-    const int frow = wave * 32 + (lane & 31);
     for (int it = 0; it < niters; ++it) {
         const int bc = it % nbc;
-        // registers -> LDS
 #pragma unroll
         for (int i = 0; i < RG; ++i) {
             const int q = tid + i * THREADS;
             if (q < gvec) {
                 const int rho = q / cpr, bb = (q - rho * cpr) * VW;
-#pragma unroll
-                for (int e = 0; e < VW; ++e)
-                    sG[rho][bb + e] = rg[i].v[e];
+                lds_store_vec(&sG[rho][bb], rg[i]);
             }
         }
 #pragma unroll
@@ -475,96 +512,115 @@ __global__ __launch_bounds__(THREADS) void wgrad_kernel(WgradArgs a) {
             const int q = tid + i * THREADS;
             if (q < xvec) {
                 const int f = q / cpr, bb = (q - f * cpr) * VW;
-#pragma unroll
-                for (int e = 0; e < VW; ++e)
-                    sX[f][bb + e] = rx[i].v[e];
+                lds_store_vec(&sX[f][bb], rx[i]);
             }
         }
-        if (SPARSE && bc == 0 && tid < qcount)
-            sidx[tid] = ridx;
+        if (SPARSE && bc == 0 && tid < WG_NG * 64)
+            sidx[tid >> 6][tid & 63] = ridx;
         __syncthreads();
         if (it + 1 < niters)
             load(it + 1);
 
-        // MFMA over this batch chunk
+        // MFMA over this batch chunk: 2 feature tiles x TT row tiles
         if constexpr (sizeof(TS) == 4) {
-#pragma unroll
+#pragma unroll 2
             for (int s4 = 0; s4 < HALF; s4 += 4) {
-                const float4 av = *(const float4 *)&sX[frow][hb + s4];
+                float4 av[WG_FT], bv[TT];
 #pragma unroll
-                for (int tt = 0; tt < TT; ++tt) {
-                    const float4 bv = *(const float4 *)&sG[tt * 32 + (lane & 31)][hb + s4];
-                    f32x16 &c = tmp[tt];
-                    c = mfma32x32x2(av.x, bv.x, c);
-                    c = mfma32x32x2(av.y, bv.y, c);
-                    c = mfma32x32x2(av.z, bv.z, c);
-                    c = mfma32x32x2(av.w, bv.w, c);
-                }
+                for (int ft = 0; ft < WG_FT; ++ft)
+                    av[ft] = *(const float4 *)&sX[fh * 64 + ft * 32 + (lane & 31)][hb + s4];
+#pragma unroll
+                for (int tt = 0; tt < TT; ++tt)
+                    bv[tt] = *(const float4 *)&sG[gi * GROWS + tt * 32 + (lane & 31)][hb + s4];
+#pragma unroll
+                for (int ft = 0; ft < WG_FT; ++ft)
+#pragma unroll
+                    for (int tt = 0; tt < TT; ++tt) {
+                        f32x16 &c = tmp[ft][tt];
+                        c = mfma32x32x2(av[ft].x, bv[tt].x, c);
+                        c = mfma32x32x2(av[ft].y, bv[tt].y, c);
+                        c = mfma32x32x2(av[ft].z, bv[tt].z, c);
+                        c = mfma32x32x2(av[ft].w, bv[tt].w, c);
+                    }
             }
         } else {
-#pragma unroll
+#pragma unroll 2
             for (int s8 = 0; s8 < HALF; s8 += 8) {
-                const u16x8 av = *(const u16x8 *)&sX[frow][hb + s8];
+                u16x8 av[WG_FT], bv[TT];
 #pragma unroll
-                for (int tt = 0; tt < TT; ++tt) {
-                    const u16x8 bv = *(const u16x8 *)&sG[tt * 32 + (lane & 31)][hb + s8];
-                    f32x16 &c = tmp[tt];
-                    c = mfma32x32x16bf(av, bv, c);
-                }
+                for (int ft = 0; ft < WG_FT; ++ft)
+                    av[ft] = *(const u16x8 *)&sX[fh * 64 + ft * 32 + (lane & 31)][hb + s8];
+#pragma unroll
+                for (int tt = 0; tt < TT; ++tt)
+                    bv[tt] = *(const u16x8 *)&sG[gi * GROWS + tt * 32 + (lane & 31)][hb + s8];
+#pragma unroll
+                for (int ft = 0; ft < WG_FT; ++ft)
+#pragma unroll
+                    for (int tt = 0; tt < TT; ++tt)
+                        tmp[ft][tt] = mfma32x32x16bf(av[ft], bv[tt], tmp[ft][tt]);
             }
         }
 
-        // dense: add this step's product; sparse: route this step's kept rows
-        // into their original rows (same summation order either way, so a
-        // sparse call that keeps every row matches the dense one bit for bit)
-        if (!SPARSE && bc == nbc - 1) {
+        // end of a step: dense adds the step's product; sparse routes each
+        // kept row of the step into its original row (same summation order
+        // either way, so a sparse call that keeps every row matches the
+        // dense one bit for bit)
+        if (bc == nbc - 1) {
+            if (!SPARSE) {
 #pragma unroll
-            for (int v = 0; v < 16; ++v) {
-                acc[0][v] += tmp[0][v];
-                tmp[0][v] = 0.f;
-            }
-        }
-        if (SPARSE && bc == nbc - 1) {
+                for (int ft = 0; ft < WG_FT; ++ft)
 #pragma unroll
-            for (int at = 0; at < WG_ATMAX; ++at) {
-                if (at >= AT)
-                    break;
-                const int col = at * 32 + (lane & 31);
-                int src = -1;
-                if (col < rcount) {
-                    const int orow = r0 + col;
-                    const int js = orow / a.P;              // global slice
-                    const int reg = (js - j0) / a.R;        // region within the group
-                    const int e0 = reg * ks, e1 = min(e0 + ks, qcount);
-                    for (int e = e0; e < e1; ++e)
-                        if (sidx[e] == js)
-                            src = e * a.P + (orow - js * a.P);
-                }
-                const int saddr = (((src < 0 ? 0 : src) & 31) + (lane & 32)) << 2;
-                const int stile = src < 0 ? 0 : (src >> 5);
-#pragma unroll
-                for (int v = 0; v < 16; ++v) {
-                    float val = __int_as_float(__builtin_amdgcn_ds_bpermute(saddr, __float_as_int(tmp[0][v])));
-                    if (TT > 1) {
-                        const float v1 = __int_as_float(
-                            __builtin_amdgcn_ds_bpermute(saddr, __float_as_int(tmp[TT > 1 ? 1 : 0][v])));
-                        val = stile == 1 ? v1 : val;
+                    for (int v = 0; v < 16; ++v) {
+                        acc[ft][0][v] += tmp[ft][0][v];
+                        tmp[ft][0][v] = 0.f;
                     }
-                    acc[at][v] += src < 0 ? 0.f : val;
+            } else {
+#pragma unroll
+                for (int at = 0; at < ATN; ++at) {
+                    if (at >= AT)
+                        break;
+                    const int col = at * 32 + (lane & 31);
+                    int src = -1;
+                    if (col < rcount) {
+                        const int orow = r0 + col;
+                        const int js = orow / a.P;
+                        const int reg = (js - j0) / a.R;
+                        const int e0 = reg * ks, e1 = min(e0 + ks, qcount);
+                        for (int e = e0; e < e1; ++e)
+                            if (sidx[gi][e] == js)
+                                src = e * a.P + (orow - js * a.P);
+                    }
+                    const int saddr = (((src < 0 ? 0 : src) & 31) + (lane & 32)) << 2;
+                    const int stile = src < 0 ? 0 : (src >> 5);
+#pragma unroll
+                    for (int ft = 0; ft < WG_FT; ++ft)
+#pragma unroll
+                        for (int v = 0; v < 16; ++v) {
+                            float val = __int_as_float(
+                                __builtin_amdgcn_ds_bpermute(saddr, __float_as_int(tmp[ft][0][v])));
+                            if (TT > 1) {
+                                const float v1 = __int_as_float(__builtin_amdgcn_ds_bpermute(
+                                    saddr, __float_as_int(tmp[ft][TT > 1 ? 1 : 0][v])));
+                                val = stile == 1 ? v1 : val;
+                            }
+                            acc[ft][at][v] += src < 0 ? 0.f : val;
+                        }
                 }
+#pragma unroll
+                for (int ft = 0; ft < WG_FT; ++ft)
+#pragma unroll
+                    for (int tt = 0; tt < TT; ++tt)
+#pragma unroll
+                        for (int v = 0; v < 16; ++v)
+                            tmp[ft][tt][v] = 0.f;
             }
-#pragma unroll
-            for (int tt = 0; tt < TT; ++tt)
-#pragma unroll
-                for (int v = 0; v < 16; ++v)
-                    tmp[tt][v] = 0.f;
         }
         __syncthreads();
     }
 
     // write the owned tile of dW
 #pragma unroll
-    for (int at = 0; at < WG_ATMAX; ++at) {
+    for (int at = 0; at < ATN; ++at) {
         if (at >= AT)
             break;
         const int col = at * 32 + (lane & 31);
@@ -572,11 +628,13 @@ __global__ __launch_bounds__(THREADS) void wgrad_kernel(WgradArgs a) {
             continue;
         float *dst = a.dW + (long)(r0 + col) * NC;
 #pragma unroll
-        for (int v = 0; v < 16; ++v) {
-            const int f = n0 + wave * 32 + acc_row(lane, v);
-            if (f < NC)
-                dst[f] = a.accumulate ? dst[f] + acc[at][v] : acc[at][v];
-        }
+        for (int ft = 0; ft < WG_FT; ++ft)
+#pragma unroll
+            for (int v = 0; v < 16; ++v) {
+                const int f = n0 + fh * 64 + ft * 32 + acc_row(lane, v);
+                if (f < NC)
+                    dst[f] = a.accumulate ? dst[f] + acc[ft][at][v] : acc[ft][at][v];
+            }
     }
 }
 
@@ -752,29 +810,32 @@ hipError_t launch_wgrad(WgradArgs a, bool sparse, bool bf16, hipStream_t s) {
             return hipErrorNotSupported;
         wgrad_tiles(a.P, a.R, a.S, &a.greg, &tt, &at);
     }
-    // batch columns per stage: 16/32/64 (fp32) or 32/64 (bf16, whole MFMA k-blocks)
-    int bc = a.B <= 16 ? 16 : a.B <= 32 ? 32 : 64;
-    if (bf16 && bc < 32)
-        bc = 32;
+    // batch columns per stage: 16/32 (fp32) or 32/64 (bf16, whole MFMA
+    // k-blocks); larger stages would not leave room for two wavefronts per SIMD
+    int bc = a.B <= 16 ? 16 : a.B <= 32 ? 32 : (bf16 ? 64 : 32);
     a.BC = bc;
     const int vw = bf16 ? 8 : 4;
     const bool vec = a.B % vw == 0;
     const long groups = sparse ? ceil_div(ceil_div(4L * a.H / a.P, a.R), a.greg) : ceil_div(4L * a.H, 32);
-    dim3 grid((unsigned)groups, (unsigned)ceil_div(a.I + a.H, WG_FEAT));
-#define LSTMSS_WG(TS, SP, TTV, VE) do { \
-        if (bc == 16) hipLaunchKernelGGL((wgrad_kernel<TS, SP, TTV, VE, 16>), grid, dim3(THREADS), 0, s, a); \
-        else if (bc == 32) hipLaunchKernelGGL((wgrad_kernel<TS, SP, TTV, VE, 32>), grid, dim3(THREADS), 0, s, a); \
-        else hipLaunchKernelGGL((wgrad_kernel<TS, SP, TTV, VE, 64>), grid, dim3(THREADS), 0, s, a); } while (0)
-#define LSTMSS_WGV(TS, SP, TTV) do { if (vec) LSTMSS_WG(TS, SP, TTV, true); else LSTMSS_WG(TS, SP, TTV, false); } while (0)
+    dim3 grid((unsigned)ceil_div(groups, WG_NG), (unsigned)ceil_div(a.I + a.H, WG_FEAT));
+#define LSTMSS_WG(TS, SP, TTV, ATV, VE) do { \
+        if (bc == 16) hipLaunchKernelGGL((wgrad_kernel<TS, SP, TTV, ATV, VE, 16>), grid, dim3(THREADS), 0, s, a); \
+        else if (bc == 32) hipLaunchKernelGGL((wgrad_kernel<TS, SP, TTV, ATV, VE, 32>), grid, dim3(THREADS), 0, s, a); \
+        else hipLaunchKernelGGL((wgrad_kernel<TS, SP, TTV, ATV, VE, 64>), grid, dim3(THREADS), 0, s, a); } while (0)
+#define LSTMSS_WGV(TS, SP, TTV, ATV) do { if (vec) LSTMSS_WG(TS, SP, TTV, ATV, true); else LSTMSS_WG(TS, SP, TTV, ATV, false); } while (0)
+#define LSTMSS_WGA(TS, TTV) do { \
+        if (at <= 1) LSTMSS_WGV(TS, true, TTV, 1); else if (at <= 2) LSTMSS_WGV(TS, true, TTV, 2); \
+        else LSTMSS_WGV(TS, true, TTV, 4); } while (0)
     if (bf16) {
-        if (!sparse) LSTMSS_WGV(bf16_t, false, 1);
-        else if (tt == 1) LSTMSS_WGV(bf16_t, true, 1);
-        else LSTMSS_WGV(bf16_t, true, 2);
+        if (!sparse) LSTMSS_WGV(bf16_t, false, 1, 1);
+        else if (tt == 1) LSTMSS_WGA(bf16_t, 1);
+        else LSTMSS_WGA(bf16_t, 2);
     } else {
-        if (!sparse) LSTMSS_WGV(float, false, 1);
-        else if (tt == 1) LSTMSS_WGV(float, true, 1);
-        else LSTMSS_WGV(float, true, 2);
+        if (!sparse) LSTMSS_WGV(float, false, 1, 1);
+        else if (tt == 1) LSTMSS_WGA(float, 1);
+        else LSTMSS_WGA(float, 2);
     }
+#undef LSTMSS_WGA
 #undef LSTMSS_WGV
 #undef LSTMSS_WG
     return hipGetLastError();
