@@ -84,20 +84,39 @@ struct Vec<bf16_t, false> {
 // --------------------------------------------------------------------------
 // Data gradient: part[z][m][n] = sum over k in split z of W[row(k)][m] G[k][n]
 // where row(k) = idx[k/P]*P + k%P (kept rows) or k (dense).
-// Work-group tile TM x TN (4 waves, 32x32 each), K staged TK at a time with
-// the next K tile prefetched into registers while MFMAs run on the current
-// one.  The gathered W row of every k of the split is looked up once into
-// LDS.
+//
+// Work-group tile TM x TN (4 wavefronts), K staged TK rows at a time through
+// two LDS buffers: while the MFMAs consume one stage, the next stage's global
+// loads are in flight in registers and are written to the other buffer, so a
+// stage costs one barrier.  The gathered W row of every k of the split is
+// looked up once into LDS.
+//   fp32: LDS [k][m]; a lane's MFMA operand is one value, k = lane / 32.
+//   bf16: the MFMA operand is 8 consecutive k of one row/column, so the
+//         staging registers hold 4 k rows x VW columns and are transposed in
+//         registers; LDS is [m][k] and a lane reads its operand as 16 bytes.
 // --------------------------------------------------------------------------
 
-template <typename TS, int TN, bool GATHER, bool VEC>
+template <typename TS, int TM, int TN>
+struct G1Shape {
+    static constexpr bool BF = sizeof(TS) == 2;
+    static constexpr int TK = BF ? 64 : GEMM1_TK;   // k rows per stage
+    static constexpr int KB = BF ? 4 : 1;           // k rows per staging group
+    static constexpr int WM = TN == 32 ? 4 : 2;     // wavefront grid
+    static constexpr int WN = 4 / WM;
+    static constexpr int MT = TM / WM / 32, NT = TN / WN / 32;  // MFMA tiles per wavefront
+    static constexpr int KSTEP = BF ? 16 : 2;       // k per MFMA
+    static_assert(MT >= 1 && NT >= 1, "tile too small for four wavefronts");
+};
+
+template <typename TS, int TM, int TN, bool GATHER, bool VEC>
 __global__ __launch_bounds__(THREADS) void gemm1_kernel(Gemm1Args a) {
-    constexpr int TM = 4096 / TN;
-    constexpr int TK = GEMM1_TK;
-    constexpr int WM = TM / 32;
+    using SH = G1Shape<TS, TM, TN>;
+    constexpr bool BF = SH::BF;
+    constexpr int TK = SH::TK, KB = SH::KB, MT = SH::MT, NT = SH::NT, WM = SH::WM;
     using V = Vec<TS, VEC>;
     constexpr int VW = V::W;
-    constexpr int NA = TK * TM / VW, NB = TK * TN / VW;
+    // staging groups (KB rows x VW columns) per stage and per thread
+    constexpr int NA = (TK / KB) * (TM / VW), NB = (TK / KB) * (TN / VW);
     constexpr int RA = (NA + THREADS - 1) / THREADS, RB = (NB + THREADS - 1) / THREADS;
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int wm = wave % WM, wn = wave / WM;
@@ -112,7 +131,7 @@ __global__ __launch_bounds__(THREADS) void gemm1_kernel(Gemm1Args a) {
     const int32_t *idx = a.idx + (GATHER ? step * a.idx_step : 0);
 
     // gathered W row of every k of the current super-chunk (refilled every
-    // GEMM1_KC_MAX rows)
+    // GEMM1_KC_MAX rows; a multiple of TK)
     __shared__ int srow[GEMM1_KC_MAX];
     int sc = kb;
     auto fill_rows = [&](int s0) {
@@ -124,47 +143,62 @@ __global__ __launch_bounds__(THREADS) void gemm1_kernel(Gemm1Args a) {
     };
     fill_rows(sc);
 
-    V ra[RA], rb[RB];
+    // staging registers
+    V ra[RA][KB], rb[RB][KB];
     auto load = [&](int k0) {
+        int rows[RA][KB];
+#pragma unroll
+        for (int i = 0; i < RA; ++i)
+#pragma unroll
+            for (int r = 0; r < KB; ++r) {
+                const int q = tid + i * THREADS;
+                const int k = k0 + (q / (TM / VW)) * KB + r;
+                rows[i][r] = q < NA && k < ke ? srow[k - sc] : -1;
+            }
 #pragma unroll
         for (int i = 0; i < RA; ++i) {
             const int q = tid + i * THREADS;
-            const int kk = q / (TM / VW), mm = (q % (TM / VW)) * VW;
-            const int k = k0 + kk, m = a.m_lo + mm0 + mm;
-            if (q < NA && k < ke && m < M)
-                ra[i].load(W + (long)srow[k - sc] * ldw + m, M - m);
-            else
-                ra[i].zero();
+            const int m = a.m_lo + mm0 + (q % (TM / VW)) * VW;
+#pragma unroll
+            for (int r = 0; r < KB; ++r) {
+                // a vector load never crosses the end of a W row: ldw is a
+                // multiple of VW and so is m - m_lo; columns >= M are loaded
+                // but never stored
+                if (rows[i][r] >= 0 && m < M)
+                    ra[i][r].load(W + (long)rows[i][r] * ldw + m, VW);
+                else
+                    ra[i][r].zero();
+            }
         }
 #pragma unroll
         for (int i = 0; i < RB; ++i) {
             const int q = tid + i * THREADS;
-            const int kk = q / (TN / VW), nn = (q % (TN / VW)) * VW;
-            const int k = k0 + kk, n = n0 + nn;
-            if (q < NB && k < ke && n < N)
-                rb[i].load(G + (long)k * N + n, N - n);
-            else
-                rb[i].zero();
+            const int n = n0 + (q % (TN / VW)) * VW;
+#pragma unroll
+            for (int r = 0; r < KB; ++r) {
+                const int k = k0 + (q / (TN / VW)) * KB + r;
+                if (q < NB && k < ke && n < N)
+                    rb[i][r].load(G + (long)k * N + n, VW);
+                else
+                    rb[i][r].zero();
+            }
         }
     };
-    f32x16 acc;
-#pragma unroll
-    for (int v = 0; v < 16; ++v)
-        acc[v] = 0.f;
-    __syncthreads();
-    load(kb);
 
-    if constexpr (sizeof(TS) == 4) {
-        // fp32: LDS as [k][row]; lanes 0-31 read k, lanes 32-63 read k+1.
-        __shared__ __align__(16) float As[TK][TM + 4];
-        __shared__ __align__(16) float Bs[TK][TN + 4];
-        for (int k0 = kb; k0 < ke; k0 += TK) {
-            if (k0 == sc + GEMM1_KC_MAX) {  // next super-chunk of rows
-                sc = k0;
-                fill_rows(sc);
-                __syncthreads();
-                load(k0);
-            }
+    f32x16 acc[MT][NT];
+#pragma unroll
+    for (int i = 0; i < MT; ++i)
+#pragma unroll
+        for (int j = 0; j < NT; ++j)
+#pragma unroll
+            for (int v = 0; v < 16; ++v)
+                acc[i][j][v] = 0.f;
+    const int mw = wm * MT * 32, nw = wn * NT * 32;  // wavefront tile origin
+
+    if constexpr (!BF) {
+        __shared__ __align__(16) float As[2][TK][TM + 4];
+        __shared__ __align__(16) float Bs[2][TK][TN + 4];
+        auto stash = [&](int buf) {
 #pragma unroll
             for (int i = 0; i < RA; ++i) {
                 const int q = tid + i * THREADS;
@@ -172,7 +206,7 @@ __global__ __launch_bounds__(THREADS) void gemm1_kernel(Gemm1Args a) {
                     const int kk = q / (TM / VW), mm = (q % (TM / VW)) * VW;
 #pragma unroll
                     for (int e = 0; e < VW; ++e)
-                        As[kk][mm + e] = ra[i].v[e];
+                        As[buf][kk][mm + e] = ra[i][0].v[e];
                 }
             }
 #pragma unroll
@@ -182,72 +216,132 @@ __global__ __launch_bounds__(THREADS) void gemm1_kernel(Gemm1Args a) {
                     const int kk = q / (TN / VW), nn = (q % (TN / VW)) * VW;
 #pragma unroll
                     for (int e = 0; e < VW; ++e)
-                        Bs[kk][nn + e] = rb[i].v[e];
+                        Bs[buf][kk][nn + e] = rb[i][0].v[e];
                 }
             }
-            __syncthreads();
-            if (k0 + TK < ke && k0 + TK != sc + GEMM1_KC_MAX)
+        };
+        __syncthreads();
+        load(kb);
+        stash(0);
+        __syncthreads();
+        int buf = 0;
+        for (int k0 = kb; k0 < ke; k0 += TK) {
+            const bool next = k0 + TK < ke;
+            if (next) {
+                if (k0 + TK == sc + GEMM1_KC_MAX) {  // next super-chunk of rows
+                    sc = k0 + TK;
+                    fill_rows(sc);
+                    __syncthreads();
+                }
                 load(k0 + TK);
-#pragma unroll
-            for (int kk = 0; kk < TK; kk += 2) {
-                const float av = As[kk + (lane >> 5)][wm * 32 + (lane & 31)];
-                const float bv = Bs[kk + (lane >> 5)][wn * 32 + (lane & 31)];
-                acc = mfma32x32x2(av, bv, acc);
             }
+            float av[TK / 2][MT], bv[TK / 2][NT];
+#pragma unroll
+            for (int kk = 0; kk < TK / 2; ++kk) {
+#pragma unroll
+                for (int i = 0; i < MT; ++i)
+                    av[kk][i] = As[buf][2 * kk + (lane >> 5)][mw + i * 32 + (lane & 31)];
+#pragma unroll
+                for (int j = 0; j < NT; ++j)
+                    bv[kk][j] = Bs[buf][2 * kk + (lane >> 5)][nw + j * 32 + (lane & 31)];
+            }
+#pragma unroll
+            for (int kk = 0; kk < TK / 2; ++kk)
+#pragma unroll
+                for (int i = 0; i < MT; ++i)
+#pragma unroll
+                    for (int j = 0; j < NT; ++j)
+                        acc[i][j] = mfma32x32x2(av[kk][i], bv[kk][j], acc[i][j]);
+            if (next)
+                stash(buf ^ 1);
             __syncthreads();
+            buf ^= 1;
         }
     } else {
-        // bf16: LDS as [row][k] so each lane reads 8 consecutive k (16 bytes).
-        __shared__ __align__(16) uint16_t As[TM][TK + 8];
-        __shared__ __align__(16) uint16_t Bs[TN][TK + 8];
-        for (int k0 = kb; k0 < ke; k0 += TK) {
-            if (k0 == sc + GEMM1_KC_MAX) {  // next super-chunk of rows
-                sc = k0;
-                fill_rows(sc);
-                __syncthreads();
-                load(k0);
-            }
+        constexpr int LDK = TK + 8;  // row pitch 144 bytes: 16-byte reads of 32 rows spread over the banks
+        __shared__ __align__(16) uint16_t As[2][TM][LDK];
+        __shared__ __align__(16) uint16_t Bs[2][TN][LDK];
+        // rows k0..k0+3 of column e packed as two dwords (k0 low)
+        auto pack4 = [](const V *r, int e) {
+            uint2 o;
+            o.x = (uint32_t)r[0].v[e] | ((uint32_t)r[1].v[e] << 16);
+            o.y = (uint32_t)r[2].v[e] | ((uint32_t)r[3].v[e] << 16);
+            return o;
+        };
+        auto stash = [&](int buf) {
 #pragma unroll
             for (int i = 0; i < RA; ++i) {
                 const int q = tid + i * THREADS;
                 if (q < NA) {
-                    const int kk = q / (TM / VW), mm = (q % (TM / VW)) * VW;
+                    const int kk = (q / (TM / VW)) * KB, mm = (q % (TM / VW)) * VW;
 #pragma unroll
                     for (int e = 0; e < VW; ++e)
-                        As[mm + e][kk] = ra[i].v[e];
+                        *(uint2 *)&As[buf][mm + e][kk] = pack4(ra[i], e);
                 }
             }
 #pragma unroll
             for (int i = 0; i < RB; ++i) {
                 const int q = tid + i * THREADS;
                 if (q < NB) {
-                    const int kk = q / (TN / VW), nn = (q % (TN / VW)) * VW;
+                    const int kk = (q / (TN / VW)) * KB, nn = (q % (TN / VW)) * VW;
 #pragma unroll
                     for (int e = 0; e < VW; ++e)
-                        Bs[nn + e][kk] = rb[i].v[e];
+                        *(uint2 *)&Bs[buf][nn + e][kk] = pack4(rb[i], e);
                 }
             }
-            __syncthreads();
-            if (k0 + TK < ke && k0 + TK != sc + GEMM1_KC_MAX)
+        };
+        __syncthreads();
+        load(kb);
+        stash(0);
+        __syncthreads();
+        int buf = 0;
+        for (int k0 = kb; k0 < ke; k0 += TK) {
+            const bool next = k0 + TK < ke;
+            if (next) {
+                if (k0 + TK == sc + GEMM1_KC_MAX) {
+                    sc = k0 + TK;
+                    fill_rows(sc);
+                    __syncthreads();
+                }
                 load(k0 + TK);
-#pragma unroll
-            for (int kk = 0; kk < TK; kk += 16) {
-                const u16x8 av = *(const u16x8 *)&As[wm * 32 + (lane & 31)][kk + 8 * (lane >> 5)];
-                const u16x8 bv = *(const u16x8 *)&Bs[wn * 32 + (lane & 31)][kk + 8 * (lane >> 5)];
-                acc = mfma32x32x16bf(av, bv, acc);
             }
+            u16x8 av[TK / 16][MT], bv[TK / 16][NT];
+#pragma unroll
+            for (int kk = 0; kk < TK / 16; ++kk) {
+#pragma unroll
+                for (int i = 0; i < MT; ++i)
+                    av[kk][i] = *(const u16x8 *)&As[buf][mw + i * 32 + (lane & 31)][16 * kk + 8 * (lane >> 5)];
+#pragma unroll
+                for (int j = 0; j < NT; ++j)
+                    bv[kk][j] = *(const u16x8 *)&Bs[buf][nw + j * 32 + (lane & 31)][16 * kk + 8 * (lane >> 5)];
+            }
+#pragma unroll
+            for (int kk = 0; kk < TK / 16; ++kk)
+#pragma unroll
+                for (int i = 0; i < MT; ++i)
+#pragma unroll
+                    for (int j = 0; j < NT; ++j)
+                        acc[i][j] = mfma32x32x16bf(av[kk][i], bv[kk][j], acc[i][j]);
+            if (next)
+                stash(buf ^ 1);
             __syncthreads();
+            buf ^= 1;
         }
     }
 
     float *out = a.part + step * a.out_step + split * a.part_stride;
-    const int n = n0 + wn * 32 + (lane & 31);
 #pragma unroll
-    for (int v = 0; v < 16; ++v) {
-        const int m = a.m_lo + mm0 + wm * 32 + acc_row(lane, v);
-        if (m >= a.m_begin && m < M && n < N)
-            out[(long)(m - a.out_row0) * N + n] = acc[v];
-    }
+    for (int i = 0; i < MT; ++i)
+#pragma unroll
+        for (int j = 0; j < NT; ++j) {
+            const int n = n0 + nw + j * 32 + (lane & 31);
+#pragma unroll
+            for (int v = 0; v < 16; ++v) {
+                const int m = a.m_lo + mm0 + mw + i * 32 + acc_row(lane, v);
+                if (m >= a.m_begin && m < M && n < N)
+                    out[(long)(m - a.out_row0) * N + n] = acc[i][j][v];
+            }
+        }
 }
 
 // --------------------------------------------------------------------------
@@ -749,11 +843,23 @@ __global__ __launch_bounds__(THREADS) void fwd_step_kernel(FwdArgs a) {
 
 } // namespace
 
-int gemm1_tn(int N) { return N <= 32 ? 32 : 64; }
-int gemm1_tm(int N) { return 4096 / gemm1_tn(N); }
+// Tile of the data-gradient GEMM.  Its operands stream from L2 / MALL, so
+// occupancy beats operand reuse: fp32 runs 64 x 64 tiles (three work-groups
+// per CU); bf16, whose MFMA is 8x faster per byte staged, runs 128 x 128.
+void gemm1_tile(bool bf16, int N, int *tm, int *tn) {
+    if (N <= 32) {
+        *tm = 128;
+        *tn = 32;
+    } else if (!bf16 || N <= 64) {
+        *tm = bf16 ? 128 : 64;
+        *tn = 64;
+    } else {
+        *tm = 128;
+        *tn = 128;
+    }
+}
 
 hipError_t launch_gemm1(Gemm1Args a, bool bf16, hipStream_t s) {
-    const int TN = gemm1_tn(a.N), TM = 4096 / TN;
     if (a.k_chunk % GEMM1_TK != 0 || a.splitk < 1 || a.steps < 1)
         return hipErrorInvalidValue;
     // 16-byte vector loads need 16-byte aligned rows; the tile origin is
@@ -761,18 +867,26 @@ hipError_t launch_gemm1(Gemm1Args a, bool bf16, hipStream_t s) {
     const int vw = bf16 ? 8 : 4;
     const bool vec = a.ldw % vw == 0 && a.N % vw == 0;
     a.m_lo = vec ? a.m_begin / vw * vw : a.m_begin;
-    dim3 grid((unsigned)ceil_div(a.M - a.m_lo, TM), (unsigned)ceil_div(a.N, TN),
-              (unsigned)(a.splitk * a.steps));
+    const long z = (long)a.splitk * a.steps;
+    int TM, TN;
+    gemm1_tile(bf16, a.N, &TM, &TN);
+    if (a.tm)
+        TM = a.tm;
+    if (a.tn)
+        TN = a.tn;
+    if (!((TN == 32 && TM == 128) || ((TN == 64 || TN == 128) && (TM == 64 || TM == 128))))
+        return hipErrorInvalidValue;
+    dim3 grid((unsigned)ceil_div(a.M - a.m_lo, TM), (unsigned)ceil_div(a.N, TN), (unsigned)z);
     const bool gather = a.idx != nullptr;
-#define LSTMSS_G1(TS, TNV, GA, VE) hipLaunchKernelGGL((gemm1_kernel<TS, TNV, GA, VE>), grid, dim3(THREADS), 0, s, a)
-#define LSTMSS_G1V(TS, TNV, GA) do { if (vec) LSTMSS_G1(TS, TNV, GA, true); else LSTMSS_G1(TS, TNV, GA, false); } while (0)
-    if (bf16) {
-        if (TN == 32) { if (gather) LSTMSS_G1V(bf16_t, 32, true); else LSTMSS_G1V(bf16_t, 32, false); }
-        else { if (gather) LSTMSS_G1V(bf16_t, 64, true); else LSTMSS_G1V(bf16_t, 64, false); }
-    } else {
-        if (TN == 32) { if (gather) LSTMSS_G1V(float, 32, true); else LSTMSS_G1V(float, 32, false); }
-        else { if (gather) LSTMSS_G1V(float, 64, true); else LSTMSS_G1V(float, 64, false); }
-    }
+#define LSTMSS_G1(TS, TMV, TNV, GA, VE) hipLaunchKernelGGL((gemm1_kernel<TS, TMV, TNV, GA, VE>), grid, dim3(THREADS), 0, s, a)
+#define LSTMSS_G1V(TS, TMV, TNV, GA) do { if (vec) LSTMSS_G1(TS, TMV, TNV, GA, true); else LSTMSS_G1(TS, TMV, TNV, GA, false); } while (0)
+#define LSTMSS_G1T(TS, GA) do { \
+        if (TN == 32) LSTMSS_G1V(TS, 128, 32, GA); \
+        else if (TN == 64) { if (TM == 128) LSTMSS_G1V(TS, 128, 64, GA); else LSTMSS_G1V(TS, 64, 64, GA); } \
+        else { if (TM == 128) LSTMSS_G1V(TS, 128, 128, GA); else LSTMSS_G1V(TS, 64, 128, GA); } } while (0)
+    if (bf16) { if (gather) LSTMSS_G1T(bf16_t, true); else LSTMSS_G1T(bf16_t, false); }
+    else { if (gather) LSTMSS_G1T(float, true); else LSTMSS_G1T(float, false); }
+#undef LSTMSS_G1T
 #undef LSTMSS_G1V
 #undef LSTMSS_G1
     return hipGetLastError();

@@ -58,6 +58,7 @@ struct Gemm1Args {
     long k_chunk;
     int steps;
     long gc_step, idx_step, out_step;
+    int tm, tn;            // tile rows / columns, 0 = chosen by the launcher
 };
 
 // Weight gradient dW[rows] += dG_c [x_t; h_{t-1}]^T (rows scattered by idx).
@@ -126,9 +127,8 @@ hipError_t launch_reduce_parts(float *out, const float *part, int nparts, long s
 hipError_t launch_h0_store(void *dst, const float *src, long n, bool bf16, hipStream_t s);
 
 // Tile constants shared by the host-side sizing code.
-constexpr int GEMM1_TK = 32;
-constexpr int GEMM1_KC_MAX = 4096;
-int gemm1_tn(int N);
-int gemm1_tm(int N);
+constexpr int GEMM1_TK = 64;       // granularity of a split's k range
+constexpr int GEMM1_KC_MAX = 2048; // gathered rows looked up into LDS at a time
+void gemm1_tile(bool bf16, int N, int *tm, int *tn);
 
 } // namespace lstmss

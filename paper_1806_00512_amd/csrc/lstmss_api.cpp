@@ -229,14 +229,18 @@ CacheLayout cache_layout(const lstmss_dims *d) {
 }
 
 // Split of the K' reduction of the critical-path data gradient (the dh rows
-// only) so that enough work-groups run; each split handles >= 128 rows.
+// only): aim at four (fp32, 64 x 64 tiles) or two (bf16, 128 x 128 tiles)
+// work-groups per CU, each split at least two k stages, at most 16 partials
+// for the gate kernel to add up.
 int splitk_for(const lstmss_dims *d, long Kp) {
-    const long M = d->H;
-    const long tiles = ceil_div(M, gemm1_tm(d->B)) * ceil_div(d->B, gemm1_tn(d->B));
-    long sk = ceil_div(512, tiles);
-    const long max_sk = std::max(1L, Kp / (4L * GEMM1_TK));
+    const bool bf16 = d->dtype == LSTMSS_BF16;
+    int tm, tn;
+    gemm1_tile(bf16, d->B, &tm, &tn);
+    const long tiles = ceil_div(d->H, tm) * ceil_div(d->B, tn);
+    long sk = ceil_div(bf16 ? 512 : 1024, tiles);
+    const long max_sk = std::max(1L, Kp / (2L * GEMM1_TK));
     sk = std::min(std::max(sk, 1L), max_sk);
-    return (int)std::min(sk, 64L);
+    return (int)std::min(sk, 16L);
 }
 
 struct WsLayout {
