@@ -6,14 +6,20 @@ One step = the backward pass through time of every layer of the workload
 layer below) with coarse structural sparsifying at the workload's sparsity.
 The forward caches are computed once before timing; inputs stay resident in
 HBM.  The same step is timed with the dense backward (the speedup
-denominator), and a third pass with per-kernel HIP events (recorded on the
-launch stream by the library) gives each kernel's average launch duration
-for the roofline figure.
+denominator), then a 9-sparse : 1-dense schedule, and a last pass with
+per-kernel HIP events (recorded on each kernel's launch stream by the
+library) gives each kernel's average launch duration for the roofline.
+
+Default workload: the 4-layer sequence-to-sequence encoder shape
+(I = H = 2048, B = 128, T = 50, fp32).  The two-layer language-model shape
+(I = H = 650, B = 20, T = 35) is measured beside it (sparse and dense step
+times only) and reported under "also".
 
 Prints ONE JSON line.  value = effective TFLOP/s: the dense backward's flops
 (16 H B (I+H) T per layer) divided by the sparse step time.
 """
 import argparse
+import hashlib
 import json
 import os
 import sys
@@ -23,20 +29,35 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
 METRIC = "LSTM backward ms/step and effective TFLOP/s at 50% structured sparsity vs dense"
-DEFAULT_WORKLOAD = "lstm2_lm_h650_b20_t35_f32"
+DEFAULT_WORKLOAD = "lstm4_enc_h2048_b128_t50_f32"
+ALSO_WORKLOADS = ("lstm2_lm_h650_b20_t35_f32",)
 PEAK = {"hbm_gbs": 8000.0, "f32_tflops": 157.3, "bf16_tflops": 2516.6}
+KINDS = ("gates_select_compact", "data_grad_gemm", "weight_grad_gemm")
+# device kernel behind each timed kind whose HBM counters may be on file
+KIND_KERNEL = {"gates_select_compact": "cell", "data_grad_gemm": "gemm1_kernel",
+               "weight_grad_gemm": "wgrad_kernel"}
+KERNEL_SOURCES = ("paper_1806_00512_amd/csrc/gemm.hip", "paper_1806_00512_amd/csrc/cell.hip",
+                  "paper_1806_00512_amd/csrc/common.h", "paper_1806_00512_amd/csrc/kernels.h",
+                  "paper_1806_00512_amd/csrc/lstmss_api.cpp")
 
 
 def parse():
     ap = argparse.ArgumentParser(description=__doc__)
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=20)
-    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--steps", type=int, default=10)
+    ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--workload", default=DEFAULT_WORKLOAD)
     ap.add_argument("--sparsity", type=float, default=None)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-also", action="store_true", help="skip the secondary workloads")
     ap.add_argument("--sparse-only", action="store_true",
                     help="time only the sparse step (for profiler runs)")
+    ap.add_argument("--serial", action="store_true",
+                    help="run the weight/input-gradient work in order on the main stream "
+                         "(isolated per-kernel durations) instead of on the side stream")
+    ap.add_argument("--calibration-copy-mib", type=int, default=0,
+                    help="first run one device-to-device copy of this many MiB (the known-size "
+                         "kernel that scales HBM counter readings)")
     return ap.parse_args()
 
 
@@ -63,31 +84,60 @@ def kernel_work(wl, layer, Kp, es):
     }
 
 
-def roofline_entry(name, work, avg_s, dtype):
+def sources_digest():
+    h = hashlib.sha256()
+    for rel in KERNEL_SOURCES:
+        with open(os.path.join(ROOT, rel), "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()[:16]
+
+
+def traffic_on_file(kind, workload):
+    """HBM bytes per launch from the committed counter summary of this kernel
+    and workload, or None when there is none or the kernel sources changed
+    since the counters were taken."""
+    path = os.path.join(ROOT, "profiles", "traffic_%s_%s.txt" % (KIND_KERNEL[kind], workload))
+    if not os.path.exists(path):
+        return None
+    rec = {}
+    with open(path) as f:
+        for line in f:
+            if ":" in line and not line.startswith((" ", "#")):
+                k, v = line.split(":", 1)
+                rec[k.strip()] = v.strip()
+    if rec.get("sources_sha256_16") != sources_digest():
+        return None
+    try:
+        return float(rec["hbm_bytes_per_launch"])
+    except (KeyError, ValueError):
+        return None
+
+
+def roofline_entry(name, work, avg_s, dtype, traffic):
     """work: algorithmic bytes/flops of one average launch; avg_s: its mean
     event-measured duration."""
     peak_tf = PEAK["bf16_tflops"] if dtype == "bf16" else PEAK["f32_tflops"]
     t_mem = work["bytes"] / (PEAK["hbm_gbs"] * 1e9)
     t_mfma = work["flops"] / (peak_tf * 1e12)
+    common = {"traffic": None if traffic is None else round(traffic),
+              "avg_launch_us": round(avg_s * 1e6, 3), "algorithmic_flops": work["flops"],
+              "algorithmic_bytes": work["bytes"]}
     if t_mfma > t_mem:
         ach = work["flops"] / avg_s / 1e12
-        return {"kernel": name, "bound": "mfma", "achieved": round(ach, 3), "peak": peak_tf,
-                "unit": "TFLOP/s", "frac": round(ach / peak_tf, 4), "traffic": None,
-                "avg_launch_us": round(avg_s * 1e6, 3), "algorithmic_flops": work["flops"],
-                "algorithmic_bytes": work["bytes"]}
+        return dict({"kernel": name, "bound": "mfma", "achieved": round(ach, 3), "peak": peak_tf,
+                     "unit": "TFLOP/s", "frac": round(ach / peak_tf, 4)}, **common)
     ach = work["bytes"] / avg_s / 1e9
-    return {"kernel": name, "bound": "hbm", "achieved": round(ach, 1), "peak": PEAK["hbm_gbs"],
-            "unit": "GB/s", "frac": round(ach / PEAK["hbm_gbs"], 4), "traffic": None,
-            "avg_launch_us": round(avg_s * 1e6, 3), "algorithmic_flops": work["flops"],
-            "algorithmic_bytes": work["bytes"]}
+    return dict({"kernel": name, "bound": "hbm", "achieved": round(ach, 1),
+                 "peak": PEAK["hbm_gbs"], "unit": "GB/s", "frac": round(ach / PEAK["hbm_gbs"], 4)},
+                **common)
 
 
-def cpu_baseline(wl, inp, sparsity, budget_s=25.0):
+def cpu_baseline(wl, inp, sparsity, budget_s=20.0):
     """Time the CPU oracle (as it stands) on a bounded sample of the workload."""
     import oracle
     S = int(round(sparsity * wl.R))
     # sample: the bottom layer's backward over the first T' steps, T' chosen
-    # so that one pass is about budget_s of work (estimated from a 1-step probe)
+    # so that one pass is about budget_s of work (estimated from a 2-step probe)
     layer = 0
     I, H, B = wl.layer_input(layer), wl.hidden, wl.batch
     x = inp["x"]
@@ -100,56 +150,49 @@ def cpu_baseline(wl, inp, sparsity, budget_s=25.0):
         oracle.backward(x[:Tp], W, gates, c, h, dH[:Tp], P=wl.P, R=wl.R, S=S)
         return time.perf_counter() - t0
 
-    t1 = run(1)
-    Tp = int(max(1, min(wl.steps, budget_s / max(t1, 1e-6))))
-    dt = run(Tp) if Tp > 1 else t1
+    # per-step cost from a 2-step probe, then as many steps as fit the budget
+    t2 = run(2)
+    Tp = int(max(2, min(wl.steps, budget_s / max(t2 / 2, 1e-6))))
+    dt = run(Tp) if Tp > 2 else t2
     flops = 16.0 * H * B * (I + H) * Tp
     return {"value": round(flops / dt / 1e12, 6), "unit": "TFLOP/s", "cores": oracle.threads(),
             "kind": "oracle",
             "sample": "fp64 oracle backward (sparsity %.2f) of layer %d over %d of %d steps, "
                       "%.2f s; effective TFLOP/s counts the dense flops 16*H*B*(I+H)*T'"
-                      % (sparsity, layer + 1, Tp, wl.steps, dt)}
+                      % (sparsity, layer + 1, Tp, wl.steps, dt),
+            "ms_per_layer_step": round(dt / Tp * 1e3, 3)}
 
 
-def main():
-    args = parse()
-    if args.gpus != 1:
-        print("bench.py: this build runs on one GPU only (--gpus 1); multi-GPU sharding is "
-              "described in DESIGN.md but not built", file=sys.stderr)
-        sys.exit(2)
-    import numpy as np
-    import torch
+class Runner:
+    """Device inputs, forward caches and output buffers of one workload."""
 
-    import paper_1806_00512_amd.lstmss as L
-    from paper_1806_00512_amd.inputs import WORKLOADS, make_inputs
+    def __init__(self, L, wl, sparsity, torch):
+        from paper_1806_00512_amd.inputs import make_inputs
+        self.L, self.wl, self.sparsity, self.torch = L, wl, sparsity, torch
+        dev = torch.device("cuda:0")
+        self.st = torch.bfloat16 if wl.dtype == "bf16" else torch.float32
+        self.inp = make_inputs(wl, seed=0)
+        self.Ws = [torch.from_numpy(w).to(dev).to(self.st) for w in self.inp["Ws"]]
+        x0 = torch.from_numpy(self.inp["x"]).to(dev).to(self.st)
+        self.dH = torch.from_numpy(self.inp["dH_up"]).to(dev)
+        # forward caches (untimed support for the backward pass)
+        self.xs, self.caches = [], []
+        inp_l = x0
+        for li in range(wl.layers):
+            h_out, cache = L.fwd_cache(inp_l, self.Ws[li])
+            self.xs.append(inp_l)
+            self.caches.append(cache)
+            inp_l = h_out
+        torch.cuda.synchronize()
+        self.sp_bufs = self._buffers(sparsity, dev)
+        self.dn_bufs = self._buffers(0.0, dev)
 
-    wl = WORKLOADS[args.workload]
-    sparsity = wl.sparsity if args.sparsity is None else args.sparsity
-    dev = torch.device("cuda:0")
-    st = torch.bfloat16 if wl.dtype == "bf16" else torch.float32
-    es = 2 if wl.dtype == "bf16" else 4
-    L.load()
-
-    inp = make_inputs(wl, seed=0)
-    Ws = [torch.from_numpy(w).to(dev).to(st) for w in inp["Ws"]]
-    x0 = torch.from_numpy(inp["x"]).to(dev).to(st)
-    dH = torch.from_numpy(inp["dH_up"]).to(dev)
-
-    # forward caches (untimed support for the backward pass)
-    xs, caches = [], []
-    inp_l = x0
-    for li in range(wl.layers):
-        h_out, cache = L.fwd_cache(inp_l, Ws[li])
-        xs.append(inp_l)
-        caches.append(cache)
-        inp_l = h_out
-    torch.cuda.synchronize()
-
-    def buffers(sp):
+    def _buffers(self, sp, dev):
+        L, wl, torch = self.L, self.wl, self.torch
         bufs = []
         for li in range(wl.layers):
             I = wl.layer_input(li)
-            d = L.dims(wl.steps, wl.batch, I, wl.hidden, st)
+            d = L.dims(wl.steps, wl.batch, I, wl.hidden, self.st)
             s = L.structure(wl.P, wl.R) if sp > 0 else None
             ws = torch.empty(L.workspace_bytes(d, sp, s), dtype=torch.uint8, device=dev)
             out = {"dX": torch.empty((wl.steps, I, wl.batch), device=dev),
@@ -163,76 +206,156 @@ def main():
             bufs.append((ws, out))
         return bufs
 
-    sp_bufs = buffers(sparsity)
-    dn_bufs = buffers(0.0)
-
-    def step(sparse):
-        up = dH
+    def step(self, sparse, marks=None):
+        """One backward step over all layers (top layer first); marks[li],
+        when given, is recorded right after layer li's call."""
+        L, wl = self.L, self.wl
+        up = self.dH
         for li in reversed(range(wl.layers)):
             if sparse:
-                ws, out = sp_bufs[li]
-                o = L.bwd_structsparse(xs[li], Ws[li], caches[li], up, sparsity=sparsity, P=wl.P,
-                                       R=wl.R, out=out, ws=ws)
+                ws, out = self.sp_bufs[li]
+                o = L.bwd_structsparse(self.xs[li], self.Ws[li], self.caches[li], up,
+                                       sparsity=self.sparsity, P=wl.P, R=wl.R, out=out, ws=ws)
             else:
-                ws, out = dn_bufs[li]
-                o = L.bwd_dense(xs[li], Ws[li], caches[li], up, out=out, ws=ws)
+                ws, out = self.dn_bufs[li]
+                o = L.bwd_dense(self.xs[li], self.Ws[li], self.caches[li], up, out=out, ws=ws)
+            if marks is not None:
+                marks[li].record()
             up = o["dX"]
 
-    def timed(sparse, K, W):
+    def timed(self, schedule, K, W):
+        """schedule: one cycle of steps (True = sparse); K cycles timed after
+        W untimed ones.  Returns mean ms per step, wall ms per step and mean
+        ms per layer call."""
+        torch, wl = self.torch, self.wl
         for _ in range(W):
-            step(sparse)
+            for sp in schedule:
+                self.step(sp)
         torch.cuda.synchronize()
-        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+
+        def ev():
+            return torch.cuda.Event(enable_timing=True)
+
+        e0, e1 = ev(), ev()
+        spans = []  # (start event, per-layer end events) of every step
         w0 = time.perf_counter()
         e0.record()
+        prev = e0
         for _ in range(K):
-            step(sparse)
+            for sp in schedule:
+                marks = [ev() for _ in range(wl.layers)]
+                self.step(sp, marks)
+                spans.append((prev, marks))
+                prev = marks[0]
         e1.record()
         torch.cuda.synchronize()
         wall = time.perf_counter() - w0
-        return e0.elapsed_time(e1) / K, wall / K * 1e3
+        n = K * len(schedule)
+        per_layer = [0.0] * wl.layers
+        for start, marks in spans:
+            for li in reversed(range(wl.layers)):  # the top layer's call ends first
+                per_layer[li] += start.elapsed_time(marks[li])
+                start = marks[li]
+        return e0.elapsed_time(e1) / n, wall / n * 1e3, [v / n for v in per_layer]
 
-    sp_ms, sp_wall = timed(True, args.steps, args.warmup)
-    print("sparse: %.4f ms/step (wall %.4f)" % (sp_ms, sp_wall), file=sys.stderr, flush=True)
-    if args.sparse_only:
-        return
-    dn_ms, dn_wall = timed(False, args.steps, args.warmup)
-    print("dense: %.4f ms/step (wall %.4f)" % (dn_ms, dn_wall), file=sys.stderr, flush=True)
 
-    # per-kernel HIP-event timing pass (same K sparse steps)
+def measure(L, torch, wl, sparsity, steps, warmup, sparse_only=False, kernels=True):
+    r = Runner(L, wl, sparsity, torch)
+    res = {"runner": r}
+    sp_ms, sp_wall, sp_layer = r.timed([True], steps, warmup)
+    print("%s sparse: %.4f ms/step (wall %.4f)" % (wl.name, sp_ms, sp_wall), file=sys.stderr,
+          flush=True)
+    res.update(sp_ms=sp_ms, sp_wall=sp_wall, sp_layer=sp_layer)
+    if sparse_only:
+        return res
+    dn_ms, dn_wall, dn_layer = r.timed([False], steps, warmup)
+    print("%s dense: %.4f ms/step (wall %.4f)" % (wl.name, dn_ms, dn_wall), file=sys.stderr,
+          flush=True)
+    res.update(dn_ms=dn_ms, dn_wall=dn_wall, dn_layer=dn_layer)
+    if not kernels:
+        return res
+    # the 9 sparse : 1 dense schedule (dense-after-sparse training phases)
+    cycles = max(1, steps // 10)
+    mx_ms, _, _ = r.timed([True] * 9 + [False], cycles, 1)
+    print("%s 9:1 schedule: %.4f ms/step" % (wl.name, mx_ms), file=sys.stderr, flush=True)
+    res.update(mix_ms=mx_ms, mix_cycles=cycles)
+    # per-kernel HIP-event timing pass (same number of sparse steps)
     L.timing_reset()
     L.timing_enable(True)
-    for _ in range(args.steps):
-        step(True)
+    for _ in range(steps):
+        r.step(True)
     torch.cuda.synchronize()
-    kt = L.timing_read()
+    res["kt"] = L.timing_read()
     L.timing_enable(False)
     L.timing_reset()
+    return res
 
-    dense_flops = sum(16.0 * wl.hidden * wl.batch * (wl.layer_input(l) + wl.hidden) * wl.steps
-                      for l in range(wl.layers))
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print("bench.py: this build runs on one GPU only (--gpus 1); multi-GPU sharding is "
+              "described in the design notes but not built", file=sys.stderr)
+        sys.exit(2)
+    import torch
+
+    import paper_1806_00512_amd.lstmss as L
+    from paper_1806_00512_amd.inputs import WORKLOADS
+
+    L.load()
+    if args.serial:
+        L.set_option("side_stream", 0)
+    wl = WORKLOADS[args.workload]
+    sparsity = wl.sparsity if args.sparsity is None else args.sparsity
+    st = torch.bfloat16 if wl.dtype == "bf16" else torch.float32
+    es = 2 if wl.dtype == "bf16" else 4
+
+    if args.calibration_copy_mib > 0:
+        n = args.calibration_copy_mib * (1 << 20) // 4
+        a = torch.ones(n, device="cuda:0")
+        b = torch.empty_like(a)
+        torch.cuda.synchronize()
+        b.copy_(a)
+        torch.cuda.synchronize()
+        print("calibration copy: %d MiB read, %d MiB written" % (args.calibration_copy_mib,
+                                                                  args.calibration_copy_mib),
+              file=sys.stderr, flush=True)
+        del a, b
+
+    m = measure(L, torch, wl, sparsity, args.steps, args.warmup, args.sparse_only)
+    if args.sparse_only:
+        return
+    sp_ms, dn_ms, kt = m["sp_ms"], m["dn_ms"], m["kt"]
+
+    def flops_of(w, frac_kept=None):
+        tot = 0.0
+        for l in range(w.layers):
+            f = 16.0 * w.hidden * w.batch * (w.layer_input(l) + w.hidden) * w.steps
+            tot += f if frac_kept is None else f * frac_kept[l]
+        return tot
+
+    dense_flops = flops_of(wl)
     sp_kps = []
     for l in range(wl.layers):
         d = L.dims(wl.steps, wl.batch, wl.layer_input(l), wl.hidden, st)
         sp_kps.append(L.kept_rows(d, sparsity, L.structure(wl.P, wl.R)))
-    exec_flops = sum(16.0 * wl.hidden * wl.batch * (wl.layer_input(l) + wl.hidden) * wl.steps
-                     * sp_kps[l] / (4 * wl.hidden) for l in range(wl.layers))
+    exec_flops = flops_of(wl, [k / (4 * wl.hidden) for k in sp_kps])
 
-    # roofline of every kernel kind (work averaged over layers), dominant first
     kernels = {}
-    for name in ("gates_select_compact", "data_grad_gemm", "weight_grad_gemm", "aux"):
+    for name in KINDS + ("aux",):
         ms, n = kt[name]
         kernels[name] = {"total_ms_per_step": round(ms / args.steps, 5), "launches": n,
                          "avg_us": round(ms / max(n, 1) * 1e3, 3)}
     roofs = {}
-    for name in ("gates_select_compact", "data_grad_gemm", "weight_grad_gemm"):
+    for name in KINDS:
         ms, n = kt[name]
         # work of one step (all layers) times the timed steps, spread over
         # the launches of this kind: the average launch's algorithmic work
         works = [kernel_work(wl, l, sp_kps[l], es)[name] for l in range(wl.layers)]
         per_launch = {k: sum(w[k] for w in works) * args.steps / max(n, 1)
                       for k in ("bytes", "flops")}
-        roofs[name] = roofline_entry(name, per_launch, ms / 1e3 / max(n, 1), wl.dtype)
+        roofs[name] = roofline_entry(name, per_launch, ms / 1e3 / max(n, 1), wl.dtype,
+                                     traffic_on_file(name, wl.name))
     dominant = max(roofs, key=lambda k: kt[k][0])
 
     result = {
@@ -251,18 +374,39 @@ def main():
         "config": {"workload": wl.name, "layers": wl.layers, "input_size": wl.input_size,
                    "hidden": wl.hidden, "batch": wl.batch, "seq_len": wl.steps,
                    "sparsity": sparsity, "P": wl.P, "R": wl.R,
-                   "S": int(round(sparsity * wl.R)), "storage": wl.dtype},
+                   "S": int(round(sparsity * wl.R)), "storage": wl.dtype,
+                   "side_stream": not args.serial},
         "dense_ms_per_step": round(dn_ms, 5),
         "speedup_vs_dense": round(dn_ms / sp_ms, 4),
         "algorithmic_tflops": round(exec_flops / (sp_ms / 1e3) / 1e12, 4),
         "dense_tflops": round(dense_flops / (dn_ms / 1e3) / 1e12, 4),
-        "wall_ms_per_step": {"sparse": round(sp_wall, 5), "dense": round(dn_wall, 5)},
+        "per_layer_ms": {"sparse": [round(v, 5) for v in m["sp_layer"]],
+                         "dense": [round(v, 5) for v in m["dn_layer"]]},
+        "mixed_9sparse_1dense": {"ms_per_step": round(m["mix_ms"], 5), "cycles": m["mix_cycles"],
+                                 "formula_ms": round((9 * sp_ms + dn_ms) / 10, 5)},
+        "wall_ms_per_step": {"sparse": round(m["sp_wall"], 5), "dense": round(m["dn_wall"], 5)},
         "kernels": kernels,
         "roofline": roofs[dominant],
         "roofline_all": roofs,
     }
     if not args.no_cpu_baseline:
-        result["cpu_baseline"] = cpu_baseline(wl, inp, sparsity)
+        result["cpu_baseline"] = cpu_baseline(wl, m["runner"].inp, sparsity)
+    del m
+    if not args.no_also:
+        also = []
+        for name in ALSO_WORKLOADS:
+            if name == wl.name:
+                continue
+            w2 = WORKLOADS[name]
+            m2 = measure(L, torch, w2, w2.sparsity, max(args.steps, 10), args.warmup,
+                         kernels=False)
+            also.append({"workload": name, "ms_per_step": round(m2["sp_ms"], 5),
+                         "dense_ms_per_step": round(m2["dn_ms"], 5),
+                         "speedup_vs_dense": round(m2["dn_ms"] / m2["sp_ms"], 4),
+                         "value": round(flops_of(w2) / (m2["sp_ms"] / 1e3) / 1e12, 4),
+                         "unit": "TFLOP/s"})
+            del m2
+        result["also"] = also
     print(json.dumps(result), flush=True)
 
 

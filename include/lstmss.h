@@ -158,9 +158,15 @@ int32_t lstmss_select_compact(const lstmss_dims *d, float sparsity, const lstmss
  *                      argument that reaches a kernel, and replayed on later
  *                      calls with the same arguments (up to 32 per device).
  *                      Environment variable LSTMSS_GRAPHS=0 sets it to 0.
+ *   LSTMSS_OPT_SIDE_STREAM  1 (default): the work off the sequential
+ *                      critical path (weight gradient, input gradient dX)
+ *                      runs on a library-owned side stream, overlapping the
+ *                      per-step gate kernel and dh GEMM; 0 enqueues it in
+ *                      order on the caller's stream (isolated per-kernel
+ *                      timing).
  * Changing an option drops the recorded graphs.  Not for use while calls
  * are being enqueued from other threads. */
-enum { LSTMSS_OPT_GRAPHS = 0 };
+enum { LSTMSS_OPT_GRAPHS = 0, LSTMSS_OPT_SIDE_STREAM = 1 };
 int32_t lstmss_set_option(int32_t option, int32_t value);
 
 /* Measurement hooks (not part of the method): when enabled, every kernel the

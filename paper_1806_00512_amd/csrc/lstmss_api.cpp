@@ -105,6 +105,7 @@ struct SideStream {
 };
 constexpr size_t kMaxGraphs = 32;
 bool g_graphs = true;  // replay captured graphs (LSTMSS_GRAPHS=0 disables)
+bool g_side_on = true; // off-critical-path work on the side stream (else in order on the caller's)
 std::mutex g_side_mu;
 std::map<int, SideStream> g_side;
 
@@ -320,6 +321,8 @@ int32_t backward_enqueue(const lstmss_dims *d, bool dense, const Plan &p, const 
         HIP_TRY(timed(LSTMSS_KERNEL_AUX, st, [&] { return launch_fill(dbp, G, 0.f, st); }));
 
     const bool use_side = batched || dX;
+    const bool concurrent = use_side && g_side_on;
+    hipStream_t sst = concurrent ? side->s : st;
     int chunk_len = T, next_chunk = 0;
     if (use_side) {
         const int nchunks = std::max(1, std::min(kMaxWgradChunks, T / 8));
@@ -387,20 +390,22 @@ int32_t backward_enqueue(const lstmss_dims *d, bool dense, const Plan &p, const 
         if (use_side && t == std::max(0, T - (next_chunk + 1) * chunk_len)) {
             const int c = next_chunk++;
             const int hi = T - c * chunk_len;
-            HIP_TRY(hipEventRecord(side->ev[c], st));
-            HIP_TRY(hipStreamWaitEvent(side->s, side->ev[c], 0));
+            if (concurrent) {
+                HIP_TRY(hipEventRecord(side->ev[c], st));
+                HIP_TRY(hipStreamWaitEvent(side->s, side->ev[c], 0));
+            }
             if (batched) {
                 wg.t_begin = t;
                 wg.t_end = hi;
                 wg.accumulate = c > 0;
-                HIP_TRY(timed(LSTMSS_KERNEL_WEIGHT_GRAD, side->s, [&] { return launch_wgrad(wg, sparse, bf16, side->s); }));
+                HIP_TRY(timed(LSTMSS_KERNEL_WEIGHT_GRAD, sst, [&] { return launch_wgrad(wg, sparse, bf16, sst); }));
             }
             if (dX) {
                 gx.Gc = dGc;
                 gx.idx = sparse ? idx : nullptr;
                 gx.part = dX + (size_t)t * I * B;
                 gx.steps = hi - t;
-                HIP_TRY(timed(LSTMSS_KERNEL_DATA_GRAD, side->s, [&] { return launch_gemm1(gx, bf16, side->s); }));
+                HIP_TRY(timed(LSTMSS_KERNEL_DATA_GRAD, sst, [&] { return launch_gemm1(gx, bf16, sst); }));
             }
         }
 
@@ -421,7 +426,7 @@ int32_t backward_enqueue(const lstmss_dims *d, bool dense, const Plan &p, const 
             HIP_TRY(timed(LSTMSS_KERNEL_WEIGHT_GRAD, st, [&] { return launch_gemm2(g2, bf16, st); }));
         }
     }
-    if (use_side) {
+    if (concurrent) {
         HIP_TRY(hipEventRecord(side->join, side->s));
         HIP_TRY(hipStreamWaitEvent(st, side->join, 0));
     }
@@ -653,6 +658,7 @@ int32_t lstmss_set_option(int32_t option, int32_t value) {
     }
     switch (option) {
     case LSTMSS_OPT_GRAPHS: g_graphs = value != 0; return LSTMSS_OK;
+    case LSTMSS_OPT_SIDE_STREAM: g_side_on = value != 0; return LSTMSS_OK;
     default: return fail(LSTMSS_ERR_INVALID_ARG, "unknown option %d", option);
     }
 }

@@ -290,7 +290,7 @@ def cache_views(cache, T, B, H, dtype):
     return gates, c, h
 
 
-OPTIONS = {"graphs": 0}
+OPTIONS = {"graphs": 0, "side_stream": 1}
 
 
 def set_option(name: str, value: int):
