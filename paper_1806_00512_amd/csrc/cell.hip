@@ -484,81 +484,104 @@ __global__ __launch_bounds__(EK_WAVES * 64) void cell_elem_kernel(CellArgs a) {
     }
 }
 
-constexpr int SK_WAVES = 4;
-
+// One wavefront per group of regions_per_wg * R slices (<= 64 slices, <= 256
+// rows), one wavefront per work-group so that the groups spread over the CUs:
+// fold the chunk sums of each row in order, score the slices, rank each
+// slice against the R slices of its region, and copy the kept rows.
 template <typename TS>
-__global__ __launch_bounds__(SK_WAVES * 64) void cell_select_kernel2(CellArgs a) {
-    __shared__ double srowsq[64 * 4];
+__global__ __launch_bounds__(64) void cell_select_kernel2(CellArgs a) {
+    __shared__ double srowsq[256];
     __shared__ int sslot[64];
-    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int lane = threadIdx.x;
     const int B = a.B, P = a.P, R = a.R;
     const int nch = (B + 63) / 64;
     const long spw = (long)a.regions_per_wg * R;
     const long j0 = blockIdx.x * spw;
     const int nsl = (int)min(spw, a.nslices - j0);
-    const int row0 = (int)(j0 * P);
+    const long row0 = j0 * P;
     const int nrows = nsl * P;
-    for (int lr = tid; lr < nrows; lr += SK_WAVES * 64) {
-        const double *q = a.chunk_sq + (long)(row0 + lr) * nch;
+    for (int lr = lane; lr < nrows; lr += 64) {
+        const double *q = a.chunk_sq + (row0 + lr) * nch;
         double sq = q[0];
         for (int cc = 1; cc < nch; ++cc)
             sq = sq + q[cc];
         srowsq[lr] = sq;
     }
     __syncthreads();
-    if (wave == 0) {
-        const int j = lane;
-        const bool valid = j < nsl;
-        double sc = 0.0;
-        if (valid) {
-            sc = srowsq[j * P];
-            for (int p = 1; p < P; ++p)
-                sc = sc + srowsq[j * P + p];
-            if (a.scores)
-                a.scores[j0 + j] = sc;
-        }
-        const uint64_t kj = score_key(sc);
-        const long gj = j0 + j;
-        const long rs = (gj / R) * R;
-        const int ls = (int)(rs - j0);
-        const int rlen = (int)min((long)R, a.nslices - rs);
-        const int nkeep = rlen - (a.S * rlen) / R;
-        int beaten = 0;
-        for (int i = 0; i < 64; ++i) {
-            const uint64_t ki = (uint64_t)__shfl((long long)kj, i, 64);
-            if (valid && i != j && i >= ls && i < ls + rlen && i < nsl && outranks(ki, i, kj, j))
-                ++beaten;
-        }
-        const bool keep = valid && beaten < nkeep;
-        const uint64_t ball = __ballot(keep);
-        const uint64_t below = ((j ? (~0ull >> (64 - j)) : 0ull)) & ~((ls ? (~0ull >> (64 - ls)) : 0ull));
-        const int pos = __popcll(ball & below);
-        int slot = -1;
-        if (keep) {
-            slot = (int)((gj / R) * (R - a.S) + pos);
-            a.idx[slot] = (int32_t)gj;
-        }
-        if (valid)
-            sslot[j] = slot;
+    const int j = lane;
+    const bool valid = j < nsl;
+    double sc = 0.0;
+    if (valid) {
+        sc = srowsq[j * P];
+        for (int p = 1; p < P; ++p)
+            sc = sc + srowsq[j * P + p];
+        if (a.scores)
+            a.scores[j0 + j] = sc;
     }
+    const uint64_t kj = score_key(sc);
+    const long gj = j0 + j;
+    // regions start at multiples of R and j0 is one, so a region's slices
+    // are the lanes [ls, ls + rlen) of this wavefront
+    const int ls = valid ? (int)((gj / R) * R - j0) : 0;
+    const int rlen = valid ? (int)min((long)R, a.nslices - (j0 + ls)) : 0;
+    const int nkeep = rlen - (a.S * rlen) / R;
+    int beaten = 0;
+    for (int i = 0; i < R; ++i) {
+        const int src = (ls + i) & 63;
+        const uint64_t ki = (uint64_t)__shfl((long long)kj, src, 64);
+        if (i < rlen && src != j && outranks(ki, src, kj, j))
+            ++beaten;
+    }
+    const bool keep = valid && beaten < nkeep;
+    const uint64_t ball = __ballot(keep);
+    const uint64_t below = ((j ? (~0ull >> (64 - j)) : 0ull)) & ~((ls ? (~0ull >> (64 - ls)) : 0ull));
+    const int pos = __popcll(ball & below);
+    int slot = -1;
+    if (keep) {
+        slot = (int)((gj / R) * (R - a.S) + pos);
+        a.idx[slot] = (int32_t)gj;
+    }
+    if (valid)
+        sslot[j] = slot;
     __syncthreads();
-    // copy kept rows (P rows of B columns per kept slice): a wavefront per
-    // row, 16-byte vectors when a row is a whole number of them
-    const char *stage = (const char *)a.stage;
-    char *dGc = (char *)a.dGc;
+    // copy the kept rows: lanes over (row, 16-byte vector) pairs, four
+    // loads in flight before their stores
     const int rowbytes = B * (int)sizeof(TS);
-    for (int lr = wave; lr < nrows; lr += SK_WAVES) {
-        const int slot = sslot[lr / P];
-        if (slot < 0)
-            continue;
-        const char *src = stage + (long)(row0 + lr) * rowbytes;
-        char *dst = dGc + ((long)slot * P + lr % P) * rowbytes;
-        if ((rowbytes & 15) == 0) {
-            for (int v = lane; v < rowbytes / 16; v += 64)
-                ((uint4 *)dst)[v] = ((const uint4 *)src)[v];
-        } else {
+    if ((rowbytes & 15) == 0) {
+        const int rv = rowbytes / 16;
+        const uint4 *__restrict__ src = (const uint4 *)a.stage + row0 * rv;
+        uint4 *__restrict__ dst = (uint4 *)a.dGc;
+        const int nv = nrows * rv;
+        for (int v0 = 0; v0 < nv; v0 += 4 * 64) {
+            uint4 buf[4];
+            long to[4];
+#pragma unroll
+            for (int u = 0; u < 4; ++u) {
+                const int v = v0 + u * 64 + lane;
+                to[u] = -1;
+                if (v < nv) {
+                    const int lr = v / rv, c = v - lr * rv;
+                    const int sl = sslot[lr / P];
+                    if (sl >= 0) {
+                        buf[u] = src[v];
+                        to[u] = ((long)sl * P + lr % P) * rv + c;
+                    }
+                }
+            }
+#pragma unroll
+            for (int u = 0; u < 4; ++u)
+                if (to[u] >= 0)
+                    dst[to[u]] = buf[u];
+        }
+    } else {
+        const TS *src = (const TS *)a.stage + row0 * B;
+        TS *dst = (TS *)a.dGc;
+        for (int lr = 0; lr < nrows; ++lr) {
+            const int sl = sslot[lr / P];
+            if (sl < 0)
+                continue;
             for (int e = lane; e < B; e += 64)
-                ((TS *)dst)[e] = ((const TS *)src)[e];
+                dst[((long)sl * P + lr % P) * B + e] = src[(long)lr * B + e];
         }
     }
 }
@@ -650,9 +673,9 @@ hipError_t launch_cell_split(const CellArgs &a, int mode, bool bf16, hipStream_t
         return e;
     const int grid = (int)ceil_div(a.nslices, (long)a.regions_per_wg * a.R);
     if (bf16)
-        hipLaunchKernelGGL((cell_select_kernel2<bf16_t>), dim3(grid), dim3(SK_WAVES * 64), 0, s, a);
+        hipLaunchKernelGGL((cell_select_kernel2<bf16_t>), dim3(grid), dim3(64), 0, s, a);
     else
-        hipLaunchKernelGGL((cell_select_kernel2<float>), dim3(grid), dim3(SK_WAVES * 64), 0, s, a);
+        hipLaunchKernelGGL((cell_select_kernel2<float>), dim3(grid), dim3(64), 0, s, a);
     return hipGetLastError();
 }
 

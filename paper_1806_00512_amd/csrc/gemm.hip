@@ -90,34 +90,46 @@ struct Vec<bf16_t, false> {
 // loads are in flight in registers and are written to the other buffer, so a
 // stage costs one barrier.  The gathered W row of every k of the split is
 // looked up once into LDS.
-//   fp32: LDS [k][m]; a lane's MFMA operand is one value, k = lane / 32.
-//   bf16: the MFMA operand is 8 consecutive k of one row/column, so the
-//         staging registers hold 4 k rows x VW columns and are transposed in
-//         registers; LDS is [m][k] and a lane reads its operand as 16 bytes.
+//
+// Both operands arrive k-major (W rows, gate-gradient rows) while an MFMA
+// operand is a run of consecutive k of one row/column, so a thread stages 4 k
+// rows x VW columns, transposes them in registers and stores each column's 4
+// k values as one vector; LDS is [m][k] and a lane reads 4 (fp32) or 8
+// (bf16) consecutive k with one 16-byte read.  fp32 MFMA c of an 8-k block
+// contracts k = 8b + c (lanes 0-31) and k = 8b + 4 + c (lanes 32-63), the
+// same for both operands.
 // --------------------------------------------------------------------------
 
 template <typename TS, int TM, int TN>
 struct G1Shape {
     static constexpr bool BF = sizeof(TS) == 2;
-    static constexpr int TK = BF ? 64 : GEMM1_TK;   // k rows per stage
-    static constexpr int KB = BF ? 4 : 1;           // k rows per staging group
+    static constexpr int TK = BF ? 64 : 32;         // k rows per stage
+    static constexpr int KB = 4;                    // k rows per staging group
     static constexpr int WM = TN == 32 ? 4 : 2;     // wavefront grid
     static constexpr int WN = 4 / WM;
     static constexpr int MT = TM / WM / 32, NT = TN / WN / 32;  // MFMA tiles per wavefront
-    static constexpr int KSTEP = BF ? 16 : 2;       // k per MFMA
+    static constexpr int LDK = TK + (BF ? 8 : 4);   // LDS row pitch (144 bytes)
     static_assert(MT >= 1 && NT >= 1, "tile too small for four wavefronts");
+    static_assert(GEMM1_TK % TK == 0 && GEMM1_KC_MAX % TK == 0, "stage must divide the split granularity");
 };
 
 template <typename TS, int TM, int TN, bool GATHER, bool VEC>
 __global__ __launch_bounds__(THREADS) void gemm1_kernel(Gemm1Args a) {
     using SH = G1Shape<TS, TM, TN>;
     constexpr bool BF = SH::BF;
-    constexpr int TK = SH::TK, KB = SH::KB, MT = SH::MT, NT = SH::NT, WM = SH::WM;
+    constexpr int TK = SH::TK, KB = SH::KB, MT = SH::MT, NT = SH::NT, WM = SH::WM, LDK = SH::LDK;
+    using E = typename std::conditional<BF, uint16_t, float>::type;
     using V = Vec<TS, VEC>;
     constexpr int VW = V::W;
-    // staging groups (KB rows x VW columns) per stage and per thread
+    // staging groups (KB rows x VW columns) per stage; when both operands'
+    // groups fit one pass, threads [0, NA) stage W and [NA, NA + NB) stage G.
+    // Consecutive threads take consecutive k groups of one column block: 8
+    // (fp32) or 16 (bf16) lanes then store into distinct LDS banks, and each
+    // row segment they load is 128 contiguous bytes
     constexpr int NA = (TK / KB) * (TM / VW), NB = (TK / KB) * (TN / VW);
-    constexpr int RA = (NA + THREADS - 1) / THREADS, RB = (NB + THREADS - 1) / THREADS;
+    constexpr bool SPLIT = NA + NB <= THREADS;
+    constexpr int RA = SPLIT ? 1 : (NA + THREADS - 1) / THREADS;
+    constexpr int RB = SPLIT ? 1 : (NB + THREADS - 1) / THREADS;
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int wm = wave % WM, wn = wave / WM;
     const int mm0 = blockIdx.x * TM;
@@ -131,7 +143,7 @@ __global__ __launch_bounds__(THREADS) void gemm1_kernel(Gemm1Args a) {
     const int32_t *idx = a.idx + (GATHER ? step * a.idx_step : 0);
 
     // gathered W row of every k of the current super-chunk (refilled every
-    // GEMM1_KC_MAX rows; a multiple of TK)
+    // GEMM1_KC_MAX rows, a multiple of TK)
     __shared__ int srow[GEMM1_KC_MAX];
     int sc = kb;
     auto fill_rows = [&](int s0) {
@@ -143,44 +155,77 @@ __global__ __launch_bounds__(THREADS) void gemm1_kernel(Gemm1Args a) {
     };
     fill_rows(sc);
 
-    // staging registers
+    auto qa = [&](int i) { return tid + i * THREADS; };
+    auto qb = [&](int i) { return SPLIT ? tid - NA : tid + i * THREADS; };
     V ra[RA][KB], rb[RB][KB];
     auto load = [&](int k0) {
-        int rows[RA][KB];
-#pragma unroll
-        for (int i = 0; i < RA; ++i)
-#pragma unroll
-            for (int r = 0; r < KB; ++r) {
-                const int q = tid + i * THREADS;
-                const int k = k0 + (q / (TM / VW)) * KB + r;
-                rows[i][r] = q < NA && k < ke ? srow[k - sc] : -1;
-            }
 #pragma unroll
         for (int i = 0; i < RA; ++i) {
-            const int q = tid + i * THREADS;
-            const int m = a.m_lo + mm0 + (q % (TM / VW)) * VW;
+            const int q = qa(i);
+            const int kg = k0 + (q % (TK / KB)) * KB;
+            const int m = a.m_lo + mm0 + (q / (TK / KB)) * VW;
+            // a vector load never crosses the end of a W row: ldw is a
+            // multiple of VW and so is m - m_lo; columns >= M are loaded but
+            // never stored
+            const bool ok = q < NA && m < M;
 #pragma unroll
             for (int r = 0; r < KB; ++r) {
-                // a vector load never crosses the end of a W row: ldw is a
-                // multiple of VW and so is m - m_lo; columns >= M are loaded
-                // but never stored
-                if (rows[i][r] >= 0 && m < M)
-                    ra[i][r].load(W + (long)rows[i][r] * ldw + m, VW);
+                const int k = kg + r;
+                if (ok && k < ke)
+                    ra[i][r].load(W + (long)srow[k - sc] * ldw + m, VW);
                 else
                     ra[i][r].zero();
             }
         }
 #pragma unroll
         for (int i = 0; i < RB; ++i) {
-            const int q = tid + i * THREADS;
-            const int n = n0 + (q % (TN / VW)) * VW;
+            const int q = qb(i);
+            const int kg = k0 + (q % (TK / KB)) * KB;
+            const int n = n0 + (q / (TK / KB)) * VW;
+            const bool ok = q >= 0 && q < NB && n < N;
 #pragma unroll
             for (int r = 0; r < KB; ++r) {
-                const int k = k0 + (q / (TN / VW)) * KB + r;
-                if (q < NB && k < ke && n < N)
+                const int k = kg + r;
+                if (ok && k < ke)
                     rb[i][r].load(G + (long)k * N + n, VW);
                 else
                     rb[i][r].zero();
+            }
+        }
+    };
+
+    __shared__ __align__(16) E As[2][TM][LDK];
+    __shared__ __align__(16) E Bs[2][TN][LDK];
+    // column e of a group: its KB = 4 k values as one vector (k lowest first)
+    auto put4 = [](E *dst, const V *r, int e) {
+        if constexpr (BF) {
+            uint2 o;
+            o.x = (uint32_t)r[0].v[e] | ((uint32_t)r[1].v[e] << 16);
+            o.y = (uint32_t)r[2].v[e] | ((uint32_t)r[3].v[e] << 16);
+            *(uint2 *)dst = o;
+        } else {
+            *(float4 *)dst = make_float4(r[0].v[e], r[1].v[e], r[2].v[e], r[3].v[e]);
+        }
+    };
+    auto stash = [&](int buf) {
+#pragma unroll
+        for (int i = 0; i < RA; ++i) {
+            const int q = qa(i);
+            if (q < NA) {
+                const int kk = (q % (TK / KB)) * KB, mm = (q / (TK / KB)) * VW;
+#pragma unroll
+                for (int e = 0; e < VW; ++e)
+                    put4(&As[buf][mm + e][kk], ra[i], e);
+            }
+        }
+#pragma unroll
+        for (int i = 0; i < RB; ++i) {
+            const int q = qb(i);
+            if (q >= 0 && q < NB) {
+                const int kk = (q % (TK / KB)) * KB, nn = (q / (TK / KB)) * VW;
+#pragma unroll
+                for (int e = 0; e < VW; ++e)
+                    put4(&Bs[buf][nn + e][kk], rb[i], e);
             }
         }
     };
@@ -195,125 +240,52 @@ __global__ __launch_bounds__(THREADS) void gemm1_kernel(Gemm1Args a) {
                 acc[i][j][v] = 0.f;
     const int mw = wm * MT * 32, nw = wn * NT * 32;  // wavefront tile origin
 
-    if constexpr (!BF) {
-        __shared__ __align__(16) float As[2][TK][TM + 4];
-        __shared__ __align__(16) float Bs[2][TK][TN + 4];
-        auto stash = [&](int buf) {
-#pragma unroll
-            for (int i = 0; i < RA; ++i) {
-                const int q = tid + i * THREADS;
-                if (q < NA) {
-                    const int kk = q / (TM / VW), mm = (q % (TM / VW)) * VW;
-#pragma unroll
-                    for (int e = 0; e < VW; ++e)
-                        As[buf][kk][mm + e] = ra[i][0].v[e];
-                }
+    __syncthreads();
+    load(kb);
+    stash(0);
+    __syncthreads();
+    int buf = 0;
+    for (int k0 = kb; k0 < ke; k0 += TK) {
+        const bool next = k0 + TK < ke;
+        if (next) {
+            if (k0 + TK == sc + GEMM1_KC_MAX) {  // next super-chunk of rows
+                sc = k0 + TK;
+                fill_rows(sc);
+                __syncthreads();
             }
+            load(k0 + TK);
+        }
+        const int half = lane >> 5;
+        if constexpr (!BF) {
+            float4 av[TK / 8][MT], bv[TK / 8][NT];
 #pragma unroll
-            for (int i = 0; i < RB; ++i) {
-                const int q = tid + i * THREADS;
-                if (q < NB) {
-                    const int kk = q / (TN / VW), nn = (q % (TN / VW)) * VW;
-#pragma unroll
-                    for (int e = 0; e < VW; ++e)
-                        Bs[buf][kk][nn + e] = rb[i][0].v[e];
-                }
-            }
-        };
-        __syncthreads();
-        load(kb);
-        stash(0);
-        __syncthreads();
-        int buf = 0;
-        for (int k0 = kb; k0 < ke; k0 += TK) {
-            const bool next = k0 + TK < ke;
-            if (next) {
-                if (k0 + TK == sc + GEMM1_KC_MAX) {  // next super-chunk of rows
-                    sc = k0 + TK;
-                    fill_rows(sc);
-                    __syncthreads();
-                }
-                load(k0 + TK);
-            }
-            float av[TK / 2][MT], bv[TK / 2][NT];
-#pragma unroll
-            for (int kk = 0; kk < TK / 2; ++kk) {
+            for (int b8 = 0; b8 < TK / 8; ++b8) {
 #pragma unroll
                 for (int i = 0; i < MT; ++i)
-                    av[kk][i] = As[buf][2 * kk + (lane >> 5)][mw + i * 32 + (lane & 31)];
+                    av[b8][i] = *(const float4 *)&As[buf][mw + i * 32 + (lane & 31)][8 * b8 + 4 * half];
 #pragma unroll
                 for (int j = 0; j < NT; ++j)
-                    bv[kk][j] = Bs[buf][2 * kk + (lane >> 5)][nw + j * 32 + (lane & 31)];
+                    bv[b8][j] = *(const float4 *)&Bs[buf][nw + j * 32 + (lane & 31)][8 * b8 + 4 * half];
             }
 #pragma unroll
-            for (int kk = 0; kk < TK / 2; ++kk)
+            for (int b8 = 0; b8 < TK / 8; ++b8)
 #pragma unroll
-                for (int i = 0; i < MT; ++i)
+                for (int c = 0; c < 4; ++c)
 #pragma unroll
-                    for (int j = 0; j < NT; ++j)
-                        acc[i][j] = mfma32x32x2(av[kk][i], bv[kk][j], acc[i][j]);
-            if (next)
-                stash(buf ^ 1);
-            __syncthreads();
-            buf ^= 1;
-        }
-    } else {
-        constexpr int LDK = TK + 8;  // row pitch 144 bytes: 16-byte reads of 32 rows spread over the banks
-        __shared__ __align__(16) uint16_t As[2][TM][LDK];
-        __shared__ __align__(16) uint16_t Bs[2][TN][LDK];
-        // rows k0..k0+3 of column e packed as two dwords (k0 low)
-        auto pack4 = [](const V *r, int e) {
-            uint2 o;
-            o.x = (uint32_t)r[0].v[e] | ((uint32_t)r[1].v[e] << 16);
-            o.y = (uint32_t)r[2].v[e] | ((uint32_t)r[3].v[e] << 16);
-            return o;
-        };
-        auto stash = [&](int buf) {
+                    for (int i = 0; i < MT; ++i)
 #pragma unroll
-            for (int i = 0; i < RA; ++i) {
-                const int q = tid + i * THREADS;
-                if (q < NA) {
-                    const int kk = (q / (TM / VW)) * KB, mm = (q % (TM / VW)) * VW;
-#pragma unroll
-                    for (int e = 0; e < VW; ++e)
-                        *(uint2 *)&As[buf][mm + e][kk] = pack4(ra[i], e);
-                }
-            }
-#pragma unroll
-            for (int i = 0; i < RB; ++i) {
-                const int q = tid + i * THREADS;
-                if (q < NB) {
-                    const int kk = (q / (TN / VW)) * KB, nn = (q % (TN / VW)) * VW;
-#pragma unroll
-                    for (int e = 0; e < VW; ++e)
-                        *(uint2 *)&Bs[buf][nn + e][kk] = pack4(rb[i], e);
-                }
-            }
-        };
-        __syncthreads();
-        load(kb);
-        stash(0);
-        __syncthreads();
-        int buf = 0;
-        for (int k0 = kb; k0 < ke; k0 += TK) {
-            const bool next = k0 + TK < ke;
-            if (next) {
-                if (k0 + TK == sc + GEMM1_KC_MAX) {
-                    sc = k0 + TK;
-                    fill_rows(sc);
-                    __syncthreads();
-                }
-                load(k0 + TK);
-            }
+                        for (int j = 0; j < NT; ++j)
+                            acc[i][j] = mfma32x32x2(av[b8][i][c], bv[b8][j][c], acc[i][j]);
+        } else {
             u16x8 av[TK / 16][MT], bv[TK / 16][NT];
 #pragma unroll
             for (int kk = 0; kk < TK / 16; ++kk) {
 #pragma unroll
                 for (int i = 0; i < MT; ++i)
-                    av[kk][i] = *(const u16x8 *)&As[buf][mw + i * 32 + (lane & 31)][16 * kk + 8 * (lane >> 5)];
+                    av[kk][i] = *(const u16x8 *)&As[buf][mw + i * 32 + (lane & 31)][16 * kk + 8 * half];
 #pragma unroll
                 for (int j = 0; j < NT; ++j)
-                    bv[kk][j] = *(const u16x8 *)&Bs[buf][nw + j * 32 + (lane & 31)][16 * kk + 8 * (lane >> 5)];
+                    bv[kk][j] = *(const u16x8 *)&Bs[buf][nw + j * 32 + (lane & 31)][16 * kk + 8 * half];
             }
 #pragma unroll
             for (int kk = 0; kk < TK / 16; ++kk)
@@ -322,11 +294,11 @@ __global__ __launch_bounds__(THREADS) void gemm1_kernel(Gemm1Args a) {
 #pragma unroll
                     for (int j = 0; j < NT; ++j)
                         acc[i][j] = mfma32x32x16bf(av[kk][i], bv[kk][j], acc[i][j]);
-            if (next)
-                stash(buf ^ 1);
-            __syncthreads();
-            buf ^= 1;
         }
+        if (next)
+            stash(buf ^ 1);
+        __syncthreads();
+        buf ^= 1;
     }
 
     float *out = a.part + step * a.out_step + split * a.part_stride;
@@ -489,9 +461,12 @@ __global__ __launch_bounds__(THREADS, 2) void wgrad_kernel(WgradArgs a) {
     constexpr int gvec = WG_NG * GROWS * cpr, xvec = WG_FEAT * cpr;
     constexpr int RG = (gvec + THREADS - 1) / THREADS;
     constexpr int RX = (xvec + THREADS - 1) / THREADS;
-    __shared__ __align__(16) E sX[WG_FEAT][PITCH];
-    __shared__ __align__(16) E sG[WG_NG * GROWS][PITCH];
-    __shared__ int sidx[WG_NG][64];
+    // two stages: the MFMAs read one while the next batch chunk is written to
+    // the other (one barrier per chunk); the kept-slice table is kept per
+    // step parity so that a step's routing never races the next step's table
+    __shared__ __align__(16) E sX[2][WG_FEAT][PITCH];
+    __shared__ __align__(16) E sG[2][WG_NG * GROWS][PITCH];
+    __shared__ int sidx[2][WG_NG][64];
 
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int fh = wave & 1, gi = wave >> 1;      // feature half, group of this wavefront
@@ -530,47 +505,85 @@ __global__ __launch_bounds__(THREADS, 2) void wgrad_kernel(WgradArgs a) {
     int lc0[WG_NG], lcc[WG_NG], lq0[WG_NG], lqc[WG_NG];
 #pragma unroll
     for (int k = 0; k < WG_NG; ++k) {
-        int t0, t1, t2, t3;
+        int t0, t1, t2;
         geom(blockIdx.x * WG_NG + k, t0, t1, lc0[k], lcc[k], lq0[k], lqc[k], t2);
-        (void)t3;
     }
 
     const int nbc = (B + BC - 1) / BC;
     const int niters = (a.t_end - a.t_begin) * nbc;
 
+    // global -> register staging of one batch chunk; a vector never crosses
+    // the end of a row (B is a multiple of VW when VEC).  Each thread's rows
+    // are fixed for the whole launch, so their offsets within a step are
+    // computed once; a chunk adds the step's base and the batch offset.
     V rg[RG], rx[RX];
+    int gofs[RG], gbb[RG], xofs[RX], xbb[RX];
+    bool gok[RG], xok[RX], xisx[RX];
+#pragma unroll
+    for (int i = 0; i < RG; ++i) {
+        const int q = tid + i * THREADS;
+        const int rho = q / cpr, bb = (q - rho * cpr) * VW;
+        const int k = rho / GROWS, lr = rho - k * GROWS;
+        gok[i] = q < gvec && lr < lcc[k & (WG_NG - 1)];
+        gofs[i] = (lc0[k & (WG_NG - 1)] + (gok[i] ? lr : 0)) * B + bb;
+        gbb[i] = bb;
+    }
+#pragma unroll
+    for (int i = 0; i < RX; ++i) {
+        const int q = tid + i * THREADS;
+        const int f = q / cpr, bb = (q - f * cpr) * VW;
+        const int n = n0 + f;
+        xok[i] = q < xvec && n < NC;
+        xisx[i] = n < I;
+        xofs[i] = (xisx[i] ? n : (xok[i] ? n - I : 0)) * B + bb;
+        xbb[i] = bb;
+    }
     int ridx = -1;
     auto load = [&](int it) {
         const int tl = it / nbc, b0 = (it - tl * nbc) * BC;
         const int t = a.t_begin + tl;
-        const TS *Gt = Gc + (long)t * a.Kp * B;
+        const TS *Gt = Gc + (long)t * a.Kp * B + b0;
+        const TS *xt = x + (long)t * I * B + b0;
+        const TS *ht = h + (long)t * H * B + b0;
 #pragma unroll
         for (int i = 0; i < RG; ++i) {
-            const int q = tid + i * THREADS;
-            const int rho = q / cpr, bb = (q - rho * cpr) * VW;
-            const int k = rho / GROWS, lr = rho - k * GROWS;
-            const int b = b0 + bb;
-            if (q < gvec && lr < lcc[k & (WG_NG - 1)] && b < B)
-                rg[i].load(Gt + (long)(lc0[k & (WG_NG - 1)] + lr) * B + b, B - b);
+            if (gok[i] && b0 + gbb[i] < B)
+                rg[i].load(Gt + gofs[i], VW);
             else
                 rg[i].zero();
         }
 #pragma unroll
         for (int i = 0; i < RX; ++i) {
-            const int q = tid + i * THREADS;
-            const int f = q / cpr, bb = (q - f * cpr) * VW;
-            const int n = n0 + f, b = b0 + bb;
-            if (q < xvec && n < NC && b < B) {
-                const TS *src = n < I ? x + ((long)t * I + n) * B : h + ((long)t * H + (n - I)) * B;
-                rx[i].load(src + b, B - b);
-            } else {
+            if (xok[i] && b0 + xbb[i] < B)
+                rx[i].load((xisx[i] ? xt : ht) + xofs[i], VW);
+            else
                 rx[i].zero();
-            }
         }
         if (SPARSE && b0 == 0 && tid < WG_NG * 64) {
             const int k = tid >> 6, e = tid & 63;
             ridx = e < lqc[k] ? a.idx[(long)t * a.kept + lq0[k] + e] : -1;
         }
+    };
+    auto stash = [&](int it, int buf) {
+        const int tl = it / nbc;
+#pragma unroll
+        for (int i = 0; i < RG; ++i) {
+            const int q = tid + i * THREADS;
+            if (q < gvec) {
+                const int rho = q / cpr, bb = (q - rho * cpr) * VW;
+                lds_store_vec(&sG[buf][rho][bb], rg[i]);
+            }
+        }
+#pragma unroll
+        for (int i = 0; i < RX; ++i) {
+            const int q = tid + i * THREADS;
+            if (q < xvec) {
+                const int f = q / cpr, bb = (q - f * cpr) * VW;
+                lds_store_vec(&sX[buf][f][bb], rx[i]);
+            }
+        }
+        if (SPARSE && it - tl * nbc == 0 && tid < WG_NG * 64)
+            sidx[tl & 1][tid >> 6][tid & 63] = ridx;
     };
 
     f32x16 acc[WG_FT][ATN], tmp[WG_FT][TT];
@@ -589,70 +602,55 @@ __global__ __launch_bounds__(THREADS, 2) void wgrad_kernel(WgradArgs a) {
     }
 
     load(0);
+    stash(0, 0);
+    __syncthreads();
     constexpr int HALF = BC / 2;
     const int hb = (lane >> 5) * HALF;
     for (int it = 0; it < niters; ++it) {
-        const int bc = it % nbc;
-#pragma unroll
-        for (int i = 0; i < RG; ++i) {
-            const int q = tid + i * THREADS;
-            if (q < gvec) {
-                const int rho = q / cpr, bb = (q - rho * cpr) * VW;
-                lds_store_vec(&sG[rho][bb], rg[i]);
-            }
-        }
-#pragma unroll
-        for (int i = 0; i < RX; ++i) {
-            const int q = tid + i * THREADS;
-            if (q < xvec) {
-                const int f = q / cpr, bb = (q - f * cpr) * VW;
-                lds_store_vec(&sX[f][bb], rx[i]);
-            }
-        }
-        if (SPARSE && bc == 0 && tid < WG_NG * 64)
-            sidx[tid >> 6][tid & 63] = ridx;
-        __syncthreads();
+        const int buf = it & 1;
+        const int tl = it / nbc, bc = it - tl * nbc;
         if (it + 1 < niters)
             load(it + 1);
 
-        // MFMA over this batch chunk: 2 feature tiles x TT row tiles
+        // MFMA over this batch chunk: WG_FT feature tiles x TT row tiles
         if constexpr (sizeof(TS) == 4) {
-#pragma unroll 2
-            for (int s4 = 0; s4 < HALF; s4 += 4) {
-                float4 av[WG_FT], bv[TT];
+            float4 av[HALF / 4][WG_FT], bv[HALF / 4][TT];
+#pragma unroll
+            for (int s = 0; s < HALF / 4; ++s) {
 #pragma unroll
                 for (int ft = 0; ft < WG_FT; ++ft)
-                    av[ft] = *(const float4 *)&sX[fh * 64 + ft * 32 + (lane & 31)][hb + s4];
+                    av[s][ft] = *(const float4 *)&sX[buf][fh * 64 + ft * 32 + (lane & 31)][hb + 4 * s];
 #pragma unroll
                 for (int tt = 0; tt < TT; ++tt)
-                    bv[tt] = *(const float4 *)&sG[gi * GROWS + tt * 32 + (lane & 31)][hb + s4];
-#pragma unroll
-                for (int ft = 0; ft < WG_FT; ++ft)
-#pragma unroll
-                    for (int tt = 0; tt < TT; ++tt) {
-                        f32x16 &c = tmp[ft][tt];
-                        c = mfma32x32x2(av[ft].x, bv[tt].x, c);
-                        c = mfma32x32x2(av[ft].y, bv[tt].y, c);
-                        c = mfma32x32x2(av[ft].z, bv[tt].z, c);
-                        c = mfma32x32x2(av[ft].w, bv[tt].w, c);
-                    }
+                    bv[s][tt] = *(const float4 *)&sG[buf][gi * GROWS + tt * 32 + (lane & 31)][hb + 4 * s];
             }
+#pragma unroll
+            for (int s = 0; s < HALF / 4; ++s)
+#pragma unroll
+                for (int c4 = 0; c4 < 4; ++c4)
+#pragma unroll
+                    for (int ft = 0; ft < WG_FT; ++ft)
+#pragma unroll
+                        for (int tt = 0; tt < TT; ++tt)
+                            tmp[ft][tt] = mfma32x32x2(av[s][ft][c4], bv[s][tt][c4], tmp[ft][tt]);
         } else {
-#pragma unroll 2
-            for (int s8 = 0; s8 < HALF; s8 += 8) {
-                u16x8 av[WG_FT], bv[TT];
+            u16x8 av[HALF / 8][WG_FT], bv[HALF / 8][TT];
+#pragma unroll
+            for (int s = 0; s < HALF / 8; ++s) {
 #pragma unroll
                 for (int ft = 0; ft < WG_FT; ++ft)
-                    av[ft] = *(const u16x8 *)&sX[fh * 64 + ft * 32 + (lane & 31)][hb + s8];
+                    av[s][ft] = *(const u16x8 *)&sX[buf][fh * 64 + ft * 32 + (lane & 31)][hb + 8 * s];
 #pragma unroll
                 for (int tt = 0; tt < TT; ++tt)
-                    bv[tt] = *(const u16x8 *)&sG[gi * GROWS + tt * 32 + (lane & 31)][hb + s8];
+                    bv[s][tt] = *(const u16x8 *)&sG[buf][gi * GROWS + tt * 32 + (lane & 31)][hb + 8 * s];
+            }
+#pragma unroll
+            for (int s = 0; s < HALF / 8; ++s)
 #pragma unroll
                 for (int ft = 0; ft < WG_FT; ++ft)
 #pragma unroll
                     for (int tt = 0; tt < TT; ++tt)
-                        tmp[ft][tt] = mfma32x32x16bf(av[ft], bv[tt], tmp[ft][tt]);
-            }
+                        tmp[ft][tt] = mfma32x32x16bf(av[s][ft], bv[s][tt], tmp[ft][tt]);
         }
 
         // end of a step: dense adds the step's product; sparse routes each
@@ -669,6 +667,7 @@ __global__ __launch_bounds__(THREADS, 2) void wgrad_kernel(WgradArgs a) {
                         tmp[ft][0][v] = 0.f;
                     }
             } else {
+                const int *tab = sidx[tl & 1][gi];
 #pragma unroll
                 for (int at = 0; at < ATN; ++at) {
                     if (at >= AT)
@@ -681,23 +680,29 @@ __global__ __launch_bounds__(THREADS, 2) void wgrad_kernel(WgradArgs a) {
                         const int reg = (js - j0) / a.R;
                         const int e0 = reg * ks, e1 = min(e0 + ks, qcount);
                         for (int e = e0; e < e1; ++e)
-                            if (sidx[gi][e] == js)
+                            if (tab[e] == js)
                                 src = e * a.P + (orow - js * a.P);
                     }
                     const int saddr = (((src < 0 ? 0 : src) & 31) + (lane & 32)) << 2;
                     const int stile = src < 0 ? 0 : (src >> 5);
+                    // all lane permutes of this tile first, then the adds
+                    float val[WG_FT][TT][16];
+#pragma unroll
+                    for (int ft = 0; ft < WG_FT; ++ft)
+#pragma unroll
+                        for (int tt = 0; tt < TT; ++tt)
+#pragma unroll
+                            for (int v = 0; v < 16; ++v)
+                                val[ft][tt][v] = __int_as_float(
+                                    __builtin_amdgcn_ds_bpermute(saddr, __float_as_int(tmp[ft][tt][v])));
 #pragma unroll
                     for (int ft = 0; ft < WG_FT; ++ft)
 #pragma unroll
                         for (int v = 0; v < 16; ++v) {
-                            float val = __int_as_float(
-                                __builtin_amdgcn_ds_bpermute(saddr, __float_as_int(tmp[ft][0][v])));
-                            if (TT > 1) {
-                                const float v1 = __int_as_float(__builtin_amdgcn_ds_bpermute(
-                                    saddr, __float_as_int(tmp[ft][TT > 1 ? 1 : 0][v])));
-                                val = stile == 1 ? v1 : val;
-                            }
-                            acc[ft][at][v] += src < 0 ? 0.f : val;
+                            float w = val[ft][0][v];
+                            if (TT > 1)
+                                w = stile == 1 ? val[ft][TT > 1 ? 1 : 0][v] : w;
+                            acc[ft][at][v] += src < 0 ? 0.f : w;  // dropped: exactly 0, even for inf/NaN
                         }
                 }
 #pragma unroll
@@ -709,6 +714,8 @@ __global__ __launch_bounds__(THREADS, 2) void wgrad_kernel(WgradArgs a) {
                             tmp[ft][tt][v] = 0.f;
             }
         }
+        if (it + 1 < niters)
+            stash(it + 1, buf ^ 1);
         __syncthreads();
     }
 
@@ -844,18 +851,23 @@ __global__ __launch_bounds__(THREADS) void fwd_step_kernel(FwdArgs a) {
 } // namespace
 
 // Tile of the data-gradient GEMM.  Its operands stream from L2 / MALL, so
-// occupancy beats operand reuse: fp32 runs 64 x 64 tiles (three work-groups
-// per CU); bf16, whose MFMA is 8x faster per byte staged, runs 128 x 128.
-void gemm1_tile(bool bf16, int N, int *tm, int *tn) {
+// occupancy matters as much as operand reuse: fp32 runs 128 x 128 tiles
+// when those still give every CU a work-group (short-k split launches),
+// else 64 x 64 (three work-groups per CU); bf16, whose MFMA is 8x faster per
+// byte staged, always runs 128-row tiles.
+void gemm1_tile(bool bf16, int N, long rows, long zdim, int *tm, int *tn) {
     if (N <= 32) {
         *tm = 128;
         *tn = 32;
-    } else if (!bf16 || N <= 64) {
+    } else if (N <= 64) {
         *tm = bf16 ? 128 : 64;
         *tn = 64;
-    } else {
+    } else if (bf16 || ceil_div(rows, 128) * ceil_div(N, 128) * zdim >= 256) {
         *tm = 128;
         *tn = 128;
+    } else {
+        *tm = 64;
+        *tn = 64;
     }
 }
 
@@ -869,7 +881,7 @@ hipError_t launch_gemm1(Gemm1Args a, bool bf16, hipStream_t s) {
     a.m_lo = vec ? a.m_begin / vw * vw : a.m_begin;
     const long z = (long)a.splitk * a.steps;
     int TM, TN;
-    gemm1_tile(bf16, a.N, &TM, &TN);
+    gemm1_tile(bf16, a.N, a.M - a.m_lo, z, &TM, &TN);
     if (a.tm)
         TM = a.tm;
     if (a.tn)

@@ -230,15 +230,23 @@ CacheLayout cache_layout(const lstmss_dims *d) {
 }
 
 // Split of the K' reduction of the critical-path data gradient (the dh rows
-// only): aim at four (fp32, 64 x 64 tiles) or two (bf16, 128 x 128 tiles)
-// work-groups per CU, each split at least two k stages, at most 16 partials
-// for the gate kernel to add up.
+// only): enough splits that the 128 x 128 tiles give every CU a work-group
+// (fp32) or two (bf16), or, with 64 x 64 tiles, four; each split at least
+// two k stages, at most 16 partials for the gate kernel to add up.
 int splitk_for(const lstmss_dims *d, long Kp) {
     const bool bf16 = d->dtype == LSTMSS_BF16;
-    int tm, tn;
-    gemm1_tile(bf16, d->B, &tm, &tn);
-    const long tiles = ceil_div(d->H, tm) * ceil_div(d->B, tn);
-    long sk = ceil_div(bf16 ? 512 : 1024, tiles);
+    long target, tiles;
+    if (d->B <= 32) {
+        tiles = ceil_div(d->H, 128);
+        target = 512;
+    } else if (d->B <= 64 && !bf16) {
+        tiles = ceil_div(d->H, 64);
+        target = 1024;
+    } else {
+        tiles = ceil_div(d->H, 128) * ceil_div(d->B, d->B <= 64 ? 64 : 128);
+        target = bf16 ? 512 : 256;
+    }
+    long sk = ceil_div(target, tiles);
     const long max_sk = std::max(1L, Kp / (2L * GEMM1_TK));
     sk = std::min(std::max(sk, 1L), max_sk);
     return (int)std::min(sk, 16L);
