@@ -375,7 +375,7 @@ def main():
                    "hidden": wl.hidden, "batch": wl.batch, "seq_len": wl.steps,
                    "sparsity": sparsity, "P": wl.P, "R": wl.R,
                    "S": int(round(sparsity * wl.R)), "storage": wl.dtype,
-                   "side_stream": not args.serial},
+                   "side_stream": "off" if args.serial else "auto"},
         "dense_ms_per_step": round(dn_ms, 5),
         "speedup_vs_dense": round(dn_ms / sp_ms, 4),
         "algorithmic_tflops": round(exec_flops / (sp_ms / 1e3) / 1e12, 4),

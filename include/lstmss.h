@@ -158,12 +158,14 @@ int32_t lstmss_select_compact(const lstmss_dims *d, float sparsity, const lstmss
  *                      argument that reaches a kernel, and replayed on later
  *                      calls with the same arguments (up to 32 per device).
  *                      Environment variable LSTMSS_GRAPHS=0 sets it to 0.
- *   LSTMSS_OPT_SIDE_STREAM  1 (default): the work off the sequential
- *                      critical path (weight gradient, input gradient dX)
- *                      runs on a library-owned side stream, overlapping the
- *                      per-step gate kernel and dh GEMM; 0 enqueues it in
- *                      order on the caller's stream (isolated per-kernel
- *                      timing).
+ *   LSTMSS_OPT_SIDE_STREAM  where the work off the sequential critical
+ *                      path (weight gradient, input gradient dX) runs:
+ *                      0 in order on the caller's stream; 1 on a
+ *                      library-owned side stream, overlapping the per-step
+ *                      gate kernel and dh GEMM; 2 (default) on the side
+ *                      stream while a step's data-gradient GEMM is below
+ *                      2^31 multiply-adds ((I+H) * B * K'), else in order
+ *                      (large GEMMs fill the GPU by themselves).
  * Changing an option drops the recorded graphs.  Not for use while calls
  * are being enqueued from other threads. */
 enum { LSTMSS_OPT_GRAPHS = 0, LSTMSS_OPT_SIDE_STREAM = 1 };

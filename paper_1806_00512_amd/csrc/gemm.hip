@@ -871,6 +871,14 @@ void gemm1_tile(bool bf16, int N, long rows, long zdim, int *tm, int *tn) {
     }
 }
 
+// Work-groups of one data-gradient tile configuration resident per CU
+// (bounded by its LDS: two stages of (TM + TN) rows of 144 bytes plus the
+// gathered-row table, out of 160 KiB).
+int gemm1_wgs_per_cu(int tm, int tn) {
+    const long lds = 2L * (tm + tn) * 144 + 4L * GEMM1_KC_MAX;
+    return (int)std::max(1L, (160L * 1024) / lds);
+}
+
 hipError_t launch_gemm1(Gemm1Args a, bool bf16, hipStream_t s) {
     if (a.k_chunk % GEMM1_TK != 0 || a.splitk < 1 || a.steps < 1)
         return hipErrorInvalidValue;

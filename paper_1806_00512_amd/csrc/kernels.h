@@ -130,5 +130,6 @@ hipError_t launch_h0_store(void *dst, const float *src, long n, bool bf16, hipSt
 constexpr int GEMM1_TK = 64;       // granularity of a split's k range
 constexpr int GEMM1_KC_MAX = 2048; // gathered rows looked up into LDS at a time
 void gemm1_tile(bool bf16, int N, long rows, long zdim, int *tm, int *tn);
+int gemm1_wgs_per_cu(int tm, int tn);
 
 } // namespace lstmss

@@ -88,6 +88,7 @@ hipError_t timed(int kind, hipStream_t st, F &&launch) {
 // steps runs while the sequential part of the backward pass continues on the
 // caller's stream.  Default priority; joined back before each call returns.
 constexpr int kMaxWgradChunks = 4;
+constexpr int kForkEvents = 8;  // fork points of one call reuse these in turn
 struct GraphEntry {
     std::vector<uint64_t> key;
     hipGraphExec_t exec = nullptr;
@@ -96,7 +97,7 @@ struct GraphEntry {
 struct SideStream {
     hipStream_t s = nullptr;
     hipStream_t cap = nullptr;  // capture stream for graph recording
-    hipEvent_t ev[kMaxWgradChunks] = {};
+    hipEvent_t ev[kForkEvents] = {};
     hipEvent_t join = nullptr;
     hipEvent_t fork = nullptr;
     std::vector<GraphEntry> graphs;  // instantiated backward calls, LRU
@@ -105,7 +106,12 @@ struct SideStream {
 };
 constexpr size_t kMaxGraphs = 32;
 bool g_graphs = true;  // replay captured graphs (LSTMSS_GRAPHS=0 disables)
-bool g_side_on = true; // off-critical-path work on the side stream (else in order on the caller's)
+// off-critical-path work: 0 in order on the caller's stream, 1 on the side
+// stream, 2 (default) side stream only while the per-step data-gradient GEMM
+// is small (large GEMMs fill the GPU on their own, and overlapping them with
+// the critical path only delays it)
+int g_side_mode = 2;
+constexpr double kSideMaxMacs = 2147483648.0;
 std::mutex g_side_mu;
 std::map<int, SideStream> g_side;
 
@@ -127,7 +133,7 @@ hipError_t side_stream(SideStream **out) {
             return e;
         if ((e = hipEventCreateWithFlags(&ss.fork, hipEventDisableTiming)) != hipSuccess)
             return e;
-        for (int i = 0; i < kMaxWgradChunks; ++i)
+        for (int i = 0; i < kForkEvents; ++i)
             if ((e = hipEventCreateWithFlags(&ss.ev[i], hipEventDisableTiming)) != hipSuccess)
                 return e;
         if ((e = hipEventCreateWithFlags(&ss.join, hipEventDisableTiming)) != hipSuccess)
@@ -252,6 +258,22 @@ int splitk_for(const lstmss_dims *d, long Kp) {
     return (int)std::min(sk, 16L);
 }
 
+// Steps per batched dX launch: whole rounds of the work-groups the GPU holds
+// at once (a launch one round too large runs its last few work-groups as a
+// nearly empty second round), close to the weight-gradient chunk length.
+int dx_chunk_len(const lstmss_dims *d, int chunk_len, int *tm, int *tn) {
+    const bool bf16 = d->dtype == LSTMSS_BF16;
+    gemm1_tile(bf16, d->B, d->I, 1, tm, tn);
+    int dev = 0, cus = 256;
+    if (hipGetDevice(&dev) == hipSuccess)
+        (void)hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev);
+    const long tiles = ceil_div(d->I, *tm) * ceil_div(d->B, *tn);
+    const long spr = std::max(1L, (long)cus * gemm1_wgs_per_cu(*tm, *tn) / tiles);
+    if (spr >= chunk_len)
+        return chunk_len;
+    return (int)(spr * std::max(1L, std::lround((double)chunk_len / spr)));
+}
+
 struct WsLayout {
     size_t dc0, dc1, part, dGc, idx, db, stage, chunk_sq, chunk_rs, total;
     int splitk;
@@ -329,13 +351,20 @@ int32_t backward_enqueue(const lstmss_dims *d, bool dense, const Plan &p, const 
         HIP_TRY(timed(LSTMSS_KERNEL_AUX, st, [&] { return launch_fill(dbp, G, 0.f, st); }));
 
     const bool use_side = batched || dX;
-    const bool concurrent = use_side && g_side_on;
+    const bool concurrent = use_side && (g_side_mode == 1 ||
+                                         (g_side_mode == 2 && (double)K * B * p.Kp < kSideMaxMacs));
     hipStream_t sst = concurrent ? side->s : st;
-    int chunk_len = T, next_chunk = 0;
+    // the weight gradient runs in chunks of chunk_len steps and dX in chunks
+    // of dx_len steps (whole rounds of resident work-groups); each launches
+    // once its lowest step has its gate gradients
+    int chunk_len = T, dx_len = T, dx_tm = 0, dx_tn = 0;
     if (use_side) {
         const int nchunks = std::max(1, std::min(kMaxWgradChunks, T / 8));
         chunk_len = (int)ceil_div(T, nchunks);
+        if (dX)
+            dx_len = dx_chunk_len(d, chunk_len, &dx_tm, &dx_tn);
     }
+    int wg_hi = T, dx_hi = T, wg_count = 0, forks = 0;
     WgradArgs wg{};
     wg.Gc = dGc_all; wg.idx = sparse ? idx_all : nullptr; wg.x = x; wg.h = hst;
     wg.T = T; wg.I = I; wg.H = H; wg.B = B; wg.Kp = (int)p.Kp; wg.kept = (int)p.kept;
@@ -346,6 +375,7 @@ int32_t backward_enqueue(const lstmss_dims *d, bool dense, const Plan &p, const 
     gx.out_row0 = 0; gx.part_stride = 0; gx.splitk = 1;
     gx.k_chunk = ceil_div(p.Kp, GEMM1_TK) * GEMM1_TK;
     gx.gc_step = p.Kp * B; gx.idx_step = p.kept; gx.out_step = (long)I * B;
+    gx.tm = dx_tm; gx.tn = dx_tn;
 
     const long part_stride = HB;
     for (int t = T - 1; t >= 0; --t) {
@@ -393,28 +423,27 @@ int32_t backward_enqueue(const lstmss_dims *d, bool dense, const Plan &p, const 
             return fail(LSTMSS_ERR_UNSUPPORTED, "R*P*B too large for one work-group's LDS");
         HIP_TRY(timed(LSTMSS_KERNEL_GATES, st, [&] { return launch_cell(ca, sparse ? CELL_SPARSE : CELL_DENSE, bf16, st); }));
 
-        // chunk c covers steps [T - (c+1)*len, T - c*len); launch its side
-        // work once its lowest step has its gate gradients
-        if (use_side && t == std::max(0, T - (next_chunk + 1) * chunk_len)) {
-            const int c = next_chunk++;
-            const int hi = T - c * chunk_len;
-            if (concurrent) {
-                HIP_TRY(hipEventRecord(side->ev[c], st));
-                HIP_TRY(hipStreamWaitEvent(side->s, side->ev[c], 0));
-            }
-            if (batched) {
-                wg.t_begin = t;
-                wg.t_end = hi;
-                wg.accumulate = c > 0;
-                HIP_TRY(timed(LSTMSS_KERNEL_WEIGHT_GRAD, sst, [&] { return launch_wgrad(wg, sparse, bf16, sst); }));
-            }
-            if (dX) {
-                gx.Gc = dGc;
-                gx.idx = sparse ? idx : nullptr;
-                gx.part = dX + (size_t)t * I * B;
-                gx.steps = hi - t;
-                HIP_TRY(timed(LSTMSS_KERNEL_DATA_GRAD, sst, [&] { return launch_gemm1(gx, bf16, sst); }));
-            }
+        const bool wg_now = use_side && batched && t == std::max(0, wg_hi - chunk_len);
+        const bool dx_now = use_side && dX && t == std::max(0, dx_hi - dx_len);
+        if ((wg_now || dx_now) && concurrent) {
+            hipEvent_t e = side->ev[forks++ % kForkEvents];
+            HIP_TRY(hipEventRecord(e, st));
+            HIP_TRY(hipStreamWaitEvent(side->s, e, 0));
+        }
+        if (wg_now) {
+            wg.t_begin = t;
+            wg.t_end = wg_hi;
+            wg.accumulate = wg_count++ > 0;
+            HIP_TRY(timed(LSTMSS_KERNEL_WEIGHT_GRAD, sst, [&] { return launch_wgrad(wg, sparse, bf16, sst); }));
+            wg_hi = t;
+        }
+        if (dx_now) {
+            gx.Gc = dGc;
+            gx.idx = sparse ? idx : nullptr;
+            gx.part = dX + (size_t)t * I * B;
+            gx.steps = dx_hi - t;
+            HIP_TRY(timed(LSTMSS_KERNEL_DATA_GRAD, sst, [&] { return launch_gemm1(gx, bf16, sst); }));
+            dx_hi = t;
         }
 
         // dh rows of the data gradient for the next (earlier) step
@@ -666,7 +695,11 @@ int32_t lstmss_set_option(int32_t option, int32_t value) {
     }
     switch (option) {
     case LSTMSS_OPT_GRAPHS: g_graphs = value != 0; return LSTMSS_OK;
-    case LSTMSS_OPT_SIDE_STREAM: g_side_on = value != 0; return LSTMSS_OK;
+    case LSTMSS_OPT_SIDE_STREAM:
+        if (value < 0 || value > 2)
+            return fail(LSTMSS_ERR_INVALID_ARG, "side-stream mode %d (0, 1 or 2)", value);
+        g_side_mode = value;
+        return LSTMSS_OK;
     default: return fail(LSTMSS_ERR_INVALID_ARG, "unknown option %d", option);
     }
 }

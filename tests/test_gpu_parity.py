@@ -263,6 +263,31 @@ def test_graph_replay_matches_direct(L, H, sp):
         torch.randn(1000, device=dev()).sum().item()  # unrelated eager work between replays
 
 
+@pytest.mark.parametrize("graphs", [True, False])
+def test_side_stream_modes_identical(L, graphs):
+    """The weight gradient and dX on the side stream (1), in order on the
+    caller's stream (0) or chosen by shape (2) give the same bits."""
+    d = make_layer(20, 64, 96, 128, seed=15, w_scale=0.2, state=True)
+    x, W, dH = gpu_tensor(d["x"]), gpu_tensor(d["W"]), gpu_tensor(d["dH_up"])
+    dhT, dcT = gpu_tensor(d["dhT"]), gpu_tensor(d["dcT"])
+    _, cache = L.fwd_cache(x, W)
+    outs = []
+    try:
+        L.graphs_enable(graphs)
+        for mode in (1, 0, 2):
+            L.set_option("side_stream", mode)
+            outs.append(L.bwd_structsparse(x, W, cache, dH, 0.5, dhT=dhT, dcT=dcT))
+            torch.cuda.synchronize()
+    finally:
+        L.set_option("side_stream", 2)
+        L.graphs_enable(True)
+    for o in outs[1:]:
+        for k in ("dX", "dW", "db", "dh0", "dc0", "idx"):
+            assert torch.equal(o[k], outs[0][k]), k
+    with pytest.raises(L.LstmssError):
+        L.set_option("side_stream", 3)
+
+
 def test_deterministic(L):
     d = make_layer(4, 20, 40, 64, seed=12, w_scale=0.2)
     x, W, dH = gpu_tensor(d["x"]), gpu_tensor(d["W"]), gpu_tensor(d["dH_up"])
