@@ -133,34 +133,43 @@ def roofline_entry(name, work, avg_s, dtype, traffic):
 
 
 def cpu_baseline(wl, inp, sparsity, budget_s=20.0):
-    """Time the CPU oracle (as it stands) on a bounded sample of the workload."""
+    """Time the CPU oracle (as it stands) on a bounded sample of the workload:
+    the backward of the first T' steps of the bottom layer, T' sized from a
+    2-step probe to about budget_s; when a whole layer is shorter than that,
+    further layers of the same call (each with the oracle's own input) are
+    added while the total stays under budget_s."""
     import oracle
     S = int(round(sparsity * wl.R))
-    # sample: the bottom layer's backward over the first T' steps, T' chosen
-    # so that one pass is about budget_s of work (estimated from a 2-step probe)
-    layer = 0
-    I, H, B = wl.layer_input(layer), wl.hidden, wl.batch
     x = inp["x"]
-    W = inp["Ws"][layer]
     dH = inp["dH_up"]
 
-    def run(Tp):
-        gates, c, h = oracle.forward(x[:Tp], W)
+    def run(layer_x, W, Tp):
+        gates, c, h = oracle.forward(layer_x[:Tp], W)
         t0 = time.perf_counter()
-        oracle.backward(x[:Tp], W, gates, c, h, dH[:Tp], P=wl.P, R=wl.R, S=S)
-        return time.perf_counter() - t0
+        oracle.backward(layer_x[:Tp], W, gates, c, h, dH[:Tp], P=wl.P, R=wl.R, S=S)
+        return time.perf_counter() - t0, h
 
-    # per-step cost from a 2-step probe, then as many steps as fit the budget
-    t2 = run(2)
-    Tp = int(max(2, min(wl.steps, budget_s / max(t2 / 2, 1e-6))))
-    dt = run(Tp) if Tp > 2 else t2
-    flops = 16.0 * H * B * (I + H) * Tp
+    Tp = 2
+    dt, h = run(x, inp["Ws"][0], Tp)
+    for _ in range(3):  # re-size from the last run (the first pays thread start-up)
+        want = int(max(2, min(wl.steps, Tp * budget_s / max(dt, 1e-6))))
+        if want <= Tp or (dt >= 0.5 * budget_s and want < 2 * Tp):
+            break
+        Tp = want
+        dt, h = run(x, inp["Ws"][0], Tp)
+    flops = 16.0 * wl.hidden * wl.batch * (wl.layer_input(0) + wl.hidden) * Tp
+    layers = 1
+    while Tp == wl.steps and layers < wl.layers and dt * (layers + 1) / layers <= budget_s:
+        d1, h = run(h[1:], inp["Ws"][layers], Tp)
+        dt += d1
+        flops += 16.0 * wl.hidden * wl.batch * (wl.layer_input(layers) + wl.hidden) * Tp
+        layers += 1
     return {"value": round(flops / dt / 1e12, 6), "unit": "TFLOP/s", "cores": oracle.threads(),
             "kind": "oracle",
-            "sample": "fp64 oracle backward (sparsity %.2f) of layer %d over %d of %d steps, "
-                      "%.2f s; effective TFLOP/s counts the dense flops 16*H*B*(I+H)*T'"
-                      % (sparsity, layer + 1, Tp, wl.steps, dt),
-            "ms_per_layer_step": round(dt / Tp * 1e3, 3)}
+            "sample": "fp64 oracle backward (sparsity %.2f) of the bottom %d layer(s) over %d of %d "
+                      "steps, %.2f s; effective TFLOP/s counts the dense flops 16*H*B*(I+H)*T' per "
+                      "layer" % (sparsity, layers, Tp, wl.steps, dt),
+            "ms_per_layer_step": round(dt / (Tp * layers) * 1e3, 3)}
 
 
 class Runner:
