@@ -516,7 +516,7 @@ __global__ __launch_bounds__(THREADS, 2) void wgrad_kernel(WgradArgs a) {
     // the end of a row (B is a multiple of VW when VEC).  Each thread's rows
     // are fixed for the whole launch, so their offsets within a step are
     // computed once; a chunk adds the step's base and the batch offset.
-    V rg[RG], rx[RX];
+    V rg[2][RG], rx[2][RX];  // two chunks in flight: loads run two chunks ahead
     int gofs[RG], gbb[RG], xofs[RX], xbb[RX];
     bool gok[RG], xok[RX], xisx[RX];
 #pragma unroll
@@ -538,8 +538,8 @@ __global__ __launch_bounds__(THREADS, 2) void wgrad_kernel(WgradArgs a) {
         xofs[i] = (xisx[i] ? n : (xok[i] ? n - I : 0)) * B + bb;
         xbb[i] = bb;
     }
-    int ridx = -1;
-    auto load = [&](int it) {
+    int ridx[2] = {-1, -1};
+    auto load = [&](int it, int set) {
         const int tl = it / nbc, b0 = (it - tl * nbc) * BC;
         const int t = a.t_begin + tl;
         const TS *Gt = Gc + (long)t * a.Kp * B + b0;
@@ -548,30 +548,30 @@ __global__ __launch_bounds__(THREADS, 2) void wgrad_kernel(WgradArgs a) {
 #pragma unroll
         for (int i = 0; i < RG; ++i) {
             if (gok[i] && b0 + gbb[i] < B)
-                rg[i].load(Gt + gofs[i], VW);
+                rg[set][i].load(Gt + gofs[i], VW);
             else
-                rg[i].zero();
+                rg[set][i].zero();
         }
 #pragma unroll
         for (int i = 0; i < RX; ++i) {
             if (xok[i] && b0 + xbb[i] < B)
-                rx[i].load((xisx[i] ? xt : ht) + xofs[i], VW);
+                rx[set][i].load((xisx[i] ? xt : ht) + xofs[i], VW);
             else
-                rx[i].zero();
+                rx[set][i].zero();
         }
         if (SPARSE && b0 == 0 && tid < WG_NG * 64) {
             const int k = tid >> 6, e = tid & 63;
-            ridx = e < lqc[k] ? a.idx[(long)t * a.kept + lq0[k] + e] : -1;
+            ridx[set] = e < lqc[k] ? a.idx[(long)t * a.kept + lq0[k] + e] : -1;
         }
     };
-    auto stash = [&](int it, int buf) {
+    auto stash = [&](int it, int set, int buf) {
         const int tl = it / nbc;
 #pragma unroll
         for (int i = 0; i < RG; ++i) {
             const int q = tid + i * THREADS;
             if (q < gvec) {
                 const int rho = q / cpr, bb = (q - rho * cpr) * VW;
-                lds_store_vec(&sG[buf][rho][bb], rg[i]);
+                lds_store_vec(&sG[buf][rho][bb], rg[set][i]);
             }
         }
 #pragma unroll
@@ -579,11 +579,11 @@ __global__ __launch_bounds__(THREADS, 2) void wgrad_kernel(WgradArgs a) {
             const int q = tid + i * THREADS;
             if (q < xvec) {
                 const int f = q / cpr, bb = (q - f * cpr) * VW;
-                lds_store_vec(&sX[buf][f][bb], rx[i]);
+                lds_store_vec(&sX[buf][f][bb], rx[set][i]);
             }
         }
         if (SPARSE && it - tl * nbc == 0 && tid < WG_NG * 64)
-            sidx[tl & 1][tid >> 6][tid & 63] = ridx;
+            sidx[tl & 1][tid >> 6][tid & 63] = ridx[set];
     };
 
     f32x16 acc[WG_FT][ATN], tmp[WG_FT][TT];
@@ -601,16 +601,22 @@ __global__ __launch_bounds__(THREADS, 2) void wgrad_kernel(WgradArgs a) {
                 tmp[ft][j][v] = 0.f;
     }
 
-    load(0);
-    stash(0, 0);
+    load(0, 0);
+    if (niters > 1)
+        load(1, 1);
+    stash(0, 0, 0);
     __syncthreads();
     constexpr int HALF = BC / 2;
     const int hb = (lane >> 5) * HALF;
-    for (int it = 0; it < niters; ++it) {
-        const int buf = it & 1;
+    // iteration it computes from LDS buffer it & 1, loads chunk it + 2 into
+    // register set it & 1 and stores chunk it + 1 (set and buffer
+    // (it + 1) & 1); the loop runs in pairs so that the sets are static
+    auto iter = [&](int it, auto sc) {
+        constexpr int S0 = decltype(sc)::value, S1 = 1 - S0;
+        const int buf = S0;
         const int tl = it / nbc, bc = it - tl * nbc;
-        if (it + 1 < niters)
-            load(it + 1);
+        if (it + 2 < niters)
+            load(it + 2, S0);
 
         // MFMA over this batch chunk: WG_FT feature tiles x TT row tiles
         if constexpr (sizeof(TS) == 4) {
@@ -715,9 +721,16 @@ __global__ __launch_bounds__(THREADS, 2) void wgrad_kernel(WgradArgs a) {
             }
         }
         if (it + 1 < niters)
-            stash(it + 1, buf ^ 1);
+            stash(it + 1, S1, S1);
         __syncthreads();
+    };
+    int it0 = 0;
+    for (; it0 + 1 < niters; it0 += 2) {
+        iter(it0, std::integral_constant<int, 0>{});
+        iter(it0 + 1, std::integral_constant<int, 1>{});
     }
+    if (it0 < niters)
+        iter(it0, std::integral_constant<int, 0>{});
 
     // write the owned tile of dW
 #pragma unroll
