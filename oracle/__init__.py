@@ -18,6 +18,11 @@ Function map (section / table of the paper each one follows):
   select         keep R-S of every R slices (section 3; Table 1 for R, S)
   kept_index     offset index array of kept slices (section 3, after Fig. 2)
   kept_rows      K' = P * number of kept slices
+  fine_scores    squared L2 norm of each My-column block of each Mx-row slice
+                 (section 3, Fig. 2(b))
+  fine_select    remove the K lowest blocks of every slice (Table 1 for K)
+  fine_kept_index  per-slice offset index of the kept blocks
+  backward_fine  back-propagation with the fine-grained structure
   round_bf16     round-to-nearest-even to bfloat16 (storage type of the bf16
                  configuration; not from the paper)
 """
@@ -75,6 +80,17 @@ def _load():
     lib.oracle_backward.argtypes = [i, i, i, i, P, P, P, P, P, P, P, P, i, i, i, i, P,
                                     P, P, P, P, P, P, P, P]
     lib.oracle_backward.restype = i
+    lib.oracle_fine_blocks.argtypes = [i, i]
+    lib.oracle_fine_blocks.restype = L
+    lib.oracle_fine_scores.argtypes = [L, i, i, i, P, P]
+    lib.oracle_fine_scores.restype = i
+    lib.oracle_fine_select.argtypes = [L, L, i, P, P]
+    lib.oracle_fine_select.restype = i
+    lib.oracle_fine_kept_index.argtypes = [L, L, i, P, P]
+    lib.oracle_fine_kept_index.restype = None
+    lib.oracle_backward_fine.argtypes = [i, i, i, i, P, P, P, P, P, P, P, P, i, i, i, i, P,
+                                         P, P, P, P, P, P, P, P]
+    lib.oracle_backward_fine.restype = i
     _lib = lib
     return lib
 
@@ -156,6 +172,75 @@ def kept_index(keep) -> np.ndarray:
     idx = np.empty(keep.shape[0], dtype=np.int32)
     n = _load().oracle_kept_index(keep.shape[0], _ptr(keep), _ptr(idx))
     return idx[:n].copy()
+
+
+def fine_blocks(B: int, My: int) -> int:
+    """Blocks of My batch columns per slice (the last one may be narrower)."""
+    return int(_load().oracle_fine_blocks(B, My))
+
+
+def fine_scores(dG, Mx: int, My: int) -> np.ndarray:
+    """[rows/Mx][nb] squared L2 norms of the My-column blocks of each slice."""
+    lib = _load()
+    dG = _f64(dG)
+    rows, B = dG.shape
+    out = np.empty((rows // Mx, fine_blocks(B, My)))
+    _check(lib.oracle_fine_scores(rows, B, Mx, My, _ptr(dG), _ptr(out)), "fine_scores")
+    return out
+
+
+def fine_select(sc, K: int) -> np.ndarray:
+    """Keep mask [nslices][nb] (uint8): the K lowest blocks of each slice removed."""
+    lib = _load()
+    sc = _f64(sc)
+    keep = np.empty(sc.shape, dtype=np.uint8)
+    _check(lib.oracle_fine_select(sc.shape[0], sc.shape[1], K, _ptr(sc), _ptr(keep)),
+           "fine_select")
+    return keep
+
+
+def fine_kept_index(keep, K: int) -> np.ndarray:
+    """Per-slice ascending kept block indices [nslices][nb - K] (-1 pads)."""
+    keep = np.ascontiguousarray(keep, dtype=np.uint8)
+    ns, nb = keep.shape
+    out = np.empty((ns, nb - K), dtype=np.int32)
+    _load().oracle_fine_kept_index(ns, nb, K, _ptr(keep), _ptr(out))
+    return out
+
+
+def backward_fine(x, W, gates, c, h, dH_up, dhT=None, dcT=None, Mx=4, My=8, K=1, bf16=False,
+                  forced_keep=None, want_dX=True, want_dG=False):
+    """One layer backward with the fine-grained structure.
+
+    Returns the dict of ``backward`` with keep [T][4H/Mx][nb] (uint8) and
+    idx [T][4H/Mx][nb - K] (int32 kept block indices per slice)."""
+    lib = _load()
+    x, W, gates, c, h, dH_up, dhT, dcT = map(_f64, (x, W, gates, c, h, dH_up, dhT, dcT))
+    T, I, B = x.shape
+    G, Kc = W.shape
+    H = G // 4
+    nsl = G // Mx
+    nb = fine_blocks(B, My)
+    out = {
+        "dX": np.empty((T, I, B)) if want_dX else None,
+        "dW": np.empty((G, Kc)),
+        "db": np.empty(G),
+        "dh0": np.empty((H, B)),
+        "dc0": np.empty((H, B)),
+        "keep": np.empty((T, nsl, nb), dtype=np.uint8),
+        "idx": np.empty((T, nsl, nb - K), dtype=np.int32),
+        "dG": np.empty((T, G, B)) if want_dG else None,
+    }
+    fk = None if forced_keep is None else np.ascontiguousarray(forced_keep, dtype=np.uint8)
+    if fk is not None:
+        assert fk.shape == (T, nsl, nb)
+    rc = lib.oracle_backward_fine(T, B, I, H, _ptr(x), _ptr(W), _ptr(gates), _ptr(c), _ptr(h),
+                                  _ptr(dH_up), _ptr(dhT), _ptr(dcT), Mx, My, K, int(bool(bf16)),
+                                  _ptr(fk), _ptr(out["dX"]), _ptr(out["dW"]), _ptr(out["db"]),
+                                  _ptr(out["dh0"]), _ptr(out["dc0"]), _ptr(out["keep"]),
+                                  _ptr(out["idx"]), _ptr(out["dG"]))
+    _check(rc, "backward_fine")
+    return out
 
 
 def backward(x, W, gates, c, h, dH_up, dhT=None, dcT=None, P=4, R=8, S=4, bf16=False,

@@ -22,7 +22,10 @@
  *   - the kept slices form a dense matrix plus an offset index array of the
  *     kept slices (section 3, the paragraph after Fig. 2); here the weight and
  *     data gradients are formed from the masked dense matrix, which is the
- *     plain definition of what the compacted products compute.
+ *     plain definition of what the compacted products compute;
+ *   - fine-grained structural sparsifying (section 3, Fig. 2(b); Table 1 for
+ *     K): a slice of Mx rows is its own region, cut into blocks of My batch
+ *     columns, and the K blocks of lowest L2 norm are removed from it.
  *
  * Readings where the paper is silent (each one is also listed in the design
  * notes of the repository):
@@ -33,7 +36,9 @@
  *   - a trailing partial region of r < R slices removes floor(S*r/R);
  *   - the cell-state recursion dc_{t-1} = dc * f uses the unsparsified dc;
  *   - the bias gradient sums the sparsified gate gradient;
- *   - a new mask is chosen at every time step.
+ *   - a new mask is chosen at every time step;
+ *   - fine: a trailing block narrower than My (when My does not divide B) is a
+ *     block like the others, scored over its columns; K counts blocks.
  *
  * Score summation order (fixed so that a GPU selector fed the same fp32 gate
  * gradient bytes can be compared bit for bit):
@@ -271,6 +276,88 @@ long oracle_kept_rows(long rows, int P, int R, int S)
 }
 
 /* ------------------------------------------------------------------------ */
+/* Fine-grained structural sparsifying (section 3, Fig. 2(b); Table 1 for K; */
+/* section 4 for M_y = 8, M_x = 4).  A slice is Mx consecutive gate rows over */
+/* the whole batch and is its own sparsifying region; it is cut into blocks  */
+/* of My consecutive batch columns (nb = ceil(B / My) of them, the last one   */
+/* narrower when My does not divide B), and the K blocks of lowest L2 norm   */
+/* (compared squared) are removed.  Sparsity = K / nb.                       */
+/*                                                                          */
+/* Block score order: for each of the Mx rows, the My squares of the block   */
+/* (zero past B) combined pairwise by position xor My/2, ..., 2, 1; the rows */
+/* then added in order.  scores [nslices][nb].                               */
+/* ------------------------------------------------------------------------ */
+static int is_pow2(int v) { return v > 0 && (v & (v - 1)) == 0; }
+
+static double block_row_sumsq(const double *row, int B, int My, int cb)
+{
+    double part[64], next[64];
+    for (int l = 0; l < My; ++l) {
+        int b = cb * My + l;
+        part[l] = b < B ? row[b] * row[b] : 0.0;
+    }
+    for (int off = My / 2; off >= 1; off >>= 1) {
+        for (int l = 0; l < My; ++l)
+            next[l] = part[l] + part[l ^ off];
+        memcpy(part, next, sizeof(double) * My);
+    }
+    return part[0];
+}
+
+long oracle_fine_blocks(int B, int My) { return My > 0 ? (B + My - 1) / My : 0; }
+
+int oracle_fine_scores(long rows, int B, int Mx, int My, const double *dG, double *scores)
+{
+    if (rows < 1 || B < 1 || Mx < 1 || rows % Mx != 0 || !is_pow2(My) || My > 64 || !dG ||
+        !scores)
+        return ORACLE_EINVAL;
+    const long nb = oracle_fine_blocks(B, My);
+    for (long s = 0; s < rows / Mx; ++s)
+        for (long cb = 0; cb < nb; ++cb) {
+            double v = block_row_sumsq(dG + (s * Mx) * B, B, My, (int)cb);
+            for (int p = 1; p < Mx; ++p)
+                v = v + block_row_sumsq(dG + (s * Mx + p) * B, B, My, (int)cb);
+            scores[s * nb + cb] = v;
+        }
+    return ORACLE_OK;
+}
+
+/* keep [nslices][nb]: in every slice the K blocks ranked lowest are removed
+ * (same order as the coarse selection: higher score first, NaN highest,
+ * equal scores -> lower block index first). */
+int oracle_fine_select(long nslices, long nb, int K, const double *scores, uint8_t *keep)
+{
+    if (nslices < 1 || nb < 1 || K < 0 || K >= nb || !scores || !keep)
+        return ORACLE_EINVAL;
+    for (long s = 0; s < nslices; ++s) {
+        const double *sc = scores + s * nb;
+        for (long j = 0; j < nb; ++j) {
+            long beaten_by = 0;
+            for (long i = 0; i < nb; ++i)
+                if (i != j && outranks(sc[i], i, sc[j], j))
+                    ++beaten_by;
+            keep[s * nb + j] = beaten_by < nb - K ? 1 : 0;
+        }
+    }
+    return ORACLE_OK;
+}
+
+/* Offset index array of the fine structure: per slice, the kept block
+ * indices in ascending order, nb - K of them (-1 pads a forced mask that keeps
+ * fewer).  bidx [nslices][nb - K]. */
+void oracle_fine_kept_index(long nslices, long nb, int K, const uint8_t *keep, int32_t *bidx)
+{
+    for (long s = 0; s < nslices; ++s) {
+        long n = 0;
+        for (long j = 0; j < nb && n < nb - K; ++j)
+            if (keep[s * nb + j])
+                bidx[s * (nb - K) + n++] = (int32_t)j;
+        while (n < nb - K)
+            bidx[s * (nb - K) + n++] = -1;
+    }
+}
+
+/* ------------------------------------------------------------------------ */
 /* Backward pass through time of one layer, dense or structurally sparse.    */
 /* Inputs are the forward cache (x, W, gates, c, h as oracle_forward made    */
 /* them), the upstream gradient dH_up [T][H][B] of the loss with respect to  */
@@ -284,29 +371,38 @@ long oracle_kept_rows(long rows, int P, int R, int S)
 /* bf16 != 0: dG is rounded to bf16 before scoring, as that is the stored    */
 /* operand the products consume.                                            */
 /* ------------------------------------------------------------------------ */
-int oracle_backward(int T, int B, int I, int H, const double *x, const double *W,
-                    const double *gates, const double *c, const double *h,
-                    const double *dH_up, const double *dhT, const double *dcT, int P, int R,
-                    int S, int bf16, const uint8_t *forced_keep, double *dX, double *dW,
-                    double *db, double *dh0, double *dc0, uint8_t *keep_out, int32_t *idx_out,
-                    double *dG_out)
+/* fine != 0 selects the fine-grained structure: slices of P = Mx rows, blocks */
+/* of My columns, K = S blocks removed per slice (R unused); forced_keep and  */
+/* keep_out are then [T][4H/P][nb] and idx_out [T][4H/P][nb - S].           */
+static int backward_impl(int T, int B, int I, int H, const double *x, const double *W,
+                         const double *gates, const double *c, const double *h,
+                         const double *dH_up, const double *dhT, const double *dcT, int fine,
+                         int P, int R, int S, int My, int bf16, const uint8_t *forced_keep,
+                         double *dX, double *dW, double *db, double *dh0, double *dc0,
+                         uint8_t *keep_out, int32_t *idx_out, double *dG_out)
 {
     const long K = (long)I + H, G = 4L * H, HB = (long)H * B;
     if (T < 1 || B < 1 || I < 1 || H < 1 || !x || !W || !gates || !c || !h || !dH_up || !dW)
         return ORACLE_EINVAL;
-    if (P < 1 || G % P != 0 || R < 1 || R > 64 || S < 0 || S >= R)
+    if (P < 1 || G % P != 0)
+        return ORACLE_EINVAL;
+    if (!fine && (R < 1 || R > 64 || S < 0 || S >= R))
+        return ORACLE_EINVAL;
+    const long nb = fine ? oracle_fine_blocks(B, My) : 1;
+    if (fine && (!is_pow2(My) || My > 64 || S < 0 || S >= nb))
         return ORACLE_EINVAL;
     const long nslices = G / P;
-    const long kept_slices = oracle_kept_rows(G, P, R, S) / P;
+    const long nunits = fine ? nslices * nb : nslices;       /* mask entries per step */
+    const long kept_slices = fine ? nslices * (nb - S) : oracle_kept_rows(G, P, R, S) / P;
 
     double *Wt = (double *)malloc(sizeof(double) * K * G);  /* W transposed */
     double *dG = (double *)malloc(sizeof(double) * G * B);
     double *dXH = (double *)malloc(sizeof(double) * K * B);
     double *dhrec = (double *)malloc(sizeof(double) * HB);
     double *dc = (double *)malloc(sizeof(double) * HB);
-    double *scores = (double *)malloc(sizeof(double) * nslices);
-    uint8_t *keep = (uint8_t *)malloc(nslices);
-    int32_t *idx = (int32_t *)malloc(sizeof(int32_t) * nslices);
+    double *scores = (double *)malloc(sizeof(double) * nunits);
+    uint8_t *keep = (uint8_t *)malloc(nunits);
+    int32_t *idx = (int32_t *)malloc(sizeof(int32_t) * nunits);
     if (!Wt || !dG || !dXH || !dhrec || !dc || !scores || !keep || !idx) {
         free(Wt); free(dG); free(dXH); free(dhrec); free(dc); free(scores); free(keep); free(idx);
         return ORACLE_ENOMEM;
@@ -358,24 +454,41 @@ int oracle_backward(int T, int B, int I, int H, const double *x, const double *W
 
         /* Structural sparsifying: score, select (or take the forced mask). */
         if (forced_keep) {
-            memcpy(keep, forced_keep + (long)t * nslices, nslices);
+            memcpy(keep, forced_keep + (long)t * nunits, nunits);
+        } else if (fine) {
+            oracle_fine_scores(G, B, P, My, dG, scores);
+            oracle_fine_select(nslices, nb, S, scores, keep);
         } else {
             oracle_scores(G, B, P, dG, scores);
             oracle_select(nslices, R, S, scores, keep);
         }
         if (keep_out)
-            memcpy(keep_out + (long)t * nslices, keep, nslices);
+            memcpy(keep_out + (long)t * nunits, keep, nunits);
         if (idx_out) {
-            long n = oracle_kept_index(nslices, keep, idx);
-            /* a forced mask may keep a different count; pad with -1 */
-            for (long k = 0; k < kept_slices; ++k)
-                idx_out[(long)t * kept_slices + k] = k < n ? idx[k] : -1;
+            if (fine) {
+                oracle_fine_kept_index(nslices, nb, S, keep, idx_out + (long)t * kept_slices);
+            } else {
+                long n = oracle_kept_index(nslices, keep, idx);
+                /* a forced mask may keep a different count; pad with -1 */
+                for (long k = 0; k < kept_slices; ++k)
+                    idx_out[(long)t * kept_slices + k] = k < n ? idx[k] : -1;
+            }
         }
-        /* Removed slices contribute nothing to any product. */
-        for (long j = 0; j < nslices; ++j)
-            if (!keep[j])
-                for (long e = j * P * B; e < (j + 1) * P * B; ++e)
-                    dG[e] = 0.0;
+        /* Removed slices (coarse) or blocks (fine) contribute nothing to any
+         * product. */
+        if (fine) {
+            for (long j = 0; j < nslices; ++j)
+                for (long cb = 0; cb < nb; ++cb)
+                    if (!keep[j * nb + cb])
+                        for (long r = j * P; r < (j + 1) * P; ++r)
+                            for (long b = cb * My; b < (cb + 1) * My && b < B; ++b)
+                                dG[r * B + b] = 0.0;
+        } else {
+            for (long j = 0; j < nslices; ++j)
+                if (!keep[j])
+                    for (long e = j * P * B; e < (j + 1) * P * B; ++e)
+                        dG[e] = 0.0;
+        }
 
         /* Data gradients [dx_t; dh_{t-1}] = W^T dG. */
 #pragma omp parallel for schedule(static)
@@ -424,4 +537,29 @@ int oracle_backward(int T, int B, int I, int H, const double *x, const double *W
         memcpy(dc0, dc, sizeof(double) * HB);
     free(Wt); free(dG); free(dXH); free(dhrec); free(dc); free(scores); free(keep); free(idx);
     return ORACLE_OK;
+}
+
+int oracle_backward(int T, int B, int I, int H, const double *x, const double *W,
+                    const double *gates, const double *c, const double *h,
+                    const double *dH_up, const double *dhT, const double *dcT, int P, int R,
+                    int S, int bf16, const uint8_t *forced_keep, double *dX, double *dW,
+                    double *db, double *dh0, double *dc0, uint8_t *keep_out, int32_t *idx_out,
+                    double *dG_out)
+{
+    return backward_impl(T, B, I, H, x, W, gates, c, h, dH_up, dhT, dcT, 0, P, R, S, 0, bf16,
+                         forced_keep, dX, dW, db, dh0, dc0, keep_out, idx_out, dG_out);
+}
+
+/* Fine-grained backward: slices of Mx rows, blocks of My columns, K blocks
+ * removed per slice.  forced_keep / keep_out [T][4H/Mx][nb], idx_out
+ * [T][4H/Mx][nb - K]. */
+int oracle_backward_fine(int T, int B, int I, int H, const double *x, const double *W,
+                         const double *gates, const double *c, const double *h,
+                         const double *dH_up, const double *dhT, const double *dcT, int Mx,
+                         int My, int K, int bf16, const uint8_t *forced_keep, double *dX,
+                         double *dW, double *db, double *dh0, double *dc0, uint8_t *keep_out,
+                         int32_t *idx_out, double *dG_out)
+{
+    return backward_impl(T, B, I, H, x, W, gates, c, h, dH_up, dhT, dcT, 1, Mx, 0, K, My, bf16,
+                         forced_keep, dX, dW, db, dh0, dc0, keep_out, idx_out, dG_out);
 }
