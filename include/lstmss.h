@@ -44,14 +44,15 @@ extern "C" {
 
 typedef enum { LSTMSS_F32 = 0, LSTMSS_BF16 = 1 } lstmss_dtype;
 
-/* Sparsifying structure kinds (section 3).  Only COARSE is built; FINE (the
- * M_y x M_x submatrix variant) returns LSTMSS_ERR_UNSUPPORTED. */
+/* Sparsifying structure kinds (section 3, Fig. 2): COARSE drops whole
+ * P-row slices inside regions of R slices; FINE drops My-column blocks of
+ * Mx-row slices, each slice being its own region. */
 typedef enum { LSTMSS_COARSE = 0, LSTMSS_FINE = 1 } lstmss_kind;
 
 enum {
     LSTMSS_OK = 0,
     LSTMSS_ERR_INVALID_ARG = -1, /* null required pointer, bad size or structure */
-    LSTMSS_ERR_UNSUPPORTED = -2, /* valid but not built (FINE, unknown dtype) */
+    LSTMSS_ERR_UNSUPPORTED = -2, /* valid but not built (a size past a kernel limit) */
     LSTMSS_ERR_WORKSPACE = -3,   /* ws_bytes smaller than the size query returned */
     LSTMSS_ERR_HIP = -4          /* a HIP runtime call failed (see lstmss_last_error) */
 };
@@ -63,11 +64,17 @@ typedef struct {
     int32_t dtype;
 } lstmss_dims;
 
-/* Coarse structure: P gate rows per slice, R slices per region (1 <= R <= 64).
+/* COARSE: P gate rows per slice, R slices per region (1 <= R <= 64).
  * The number of slices removed per region is S = sparsity * R, which must be
  * an integer (within 1e-6) with 0 <= S < R.  4H must be a multiple of P.
  * When 4H/P is not a multiple of R, the last region has r < R slices and
- * removes floor(S*r/R).  My, Mx are reserved for the FINE kind. */
+ * removes floor(S*r/R).  My, Mx are ignored.
+ * FINE: a slice is Mx consecutive gate rows (Mx in 1..16 dividing 32 and
+ * 4H) over the whole batch, cut into nb = ceil(B/My) blocks of My batch
+ * columns (My a power of two in 2..64; the last block is narrower when My
+ * does not divide B; nb <= 64, B <= 256).  In every slice the K = sparsity *
+ * nb blocks of smallest L2 norm are zeroed (K an integer within 1e-6,
+ * 0 <= K < nb).  P, R are ignored. */
 typedef struct {
     int32_t kind;
     int32_t P, R;
@@ -84,9 +91,14 @@ const char *lstmss_last_error(void);
  * [T+1][H][B] (fp32) and hidden state [T+1][H][B] (dtype).  <0 on error. */
 int64_t lstmss_cache_bytes(const lstmss_dims *d);
 
-/* K' = P x (number of kept slices per step) for the given structure and
- * sparsity; 4H when sparsity is 0.  <0 on error. */
+/* Rows of the per-step gate-gradient matrix the products run on: for
+ * COARSE K' = P x (number of kept slices per step), 4H when sparsity is 0;
+ * for FINE always 4H (removed blocks are zero in place).  <0 on error. */
 int64_t lstmss_kept_rows(const lstmss_dims *d, float sparsity, const lstmss_structure *s);
+
+/* Entries of the per-step index written by the selection: COARSE K'/P kept
+ * slice indices; FINE (4H/Mx) x (nb - K) kept block indices.  <0 on error. */
+int64_t lstmss_index_entries(const lstmss_dims *d, float sparsity, const lstmss_structure *s);
 
 /* Workspace bytes needed by lstm_bwd_structsparse with these arguments
  * (sparsity 0 gives the size for lstm_bwd_dense).  <0 on error. */
@@ -119,7 +131,7 @@ int32_t lstm_bwd_dense(const lstmss_dims *d, const void *x, const void *W, const
                        float *dW, float *db, float *dh0, float *dc0, void *ws, size_t ws_bytes,
                        void *stream);
 
-/* Structurally sparsified backward pass (section 3, coarse-grained).  At every
+/* Structurally sparsified backward pass (section 3).  COARSE: at every
  * time step the gate gradient is formed, each P-row slice is scored by its
  * squared L2 norm (same ranking as the norm) summed in fp64 in a fixed order
  * (per 64-column batch chunk the squares are combined pairwise by index xor
@@ -130,9 +142,17 @@ int32_t lstm_bwd_dense(const lstmss_dims *d, const void *x, const void *W, const
  * products run on the compacted rows.  The cell-state gradient recursion uses
  * the unsparsified gradient.  With sparsity 0 the result equals
  * lstm_bwd_dense.
+ * FINE: every My-column block of an Mx-row slice is scored by its squared L2
+ * norm in fp64 (per row, the squares of the block are combined pairwise by
+ * column index xor My/2, ..., 2, 1, columns past B adding zero; the Mx rows
+ * are added in increasing order), the K lowest blocks of every slice are
+ * zeroed (same tie and NaN rules) and the products run on the masked
+ * [4H][B] matrix; the kept block indices of slice j are listed ascending.
  * Arguments as lstm_bwd_dense, plus
  *   sparsity, s    structure (see lstmss_structure)
- *   idx_out        [T][K'/P] int32 kept slice indices per step, or NULL
+ *   idx_out        [T][lstmss_index_entries] int32 per step (COARSE: kept
+ *                  slice indices; FINE: [4H/Mx][nb-K] kept block indices),
+ *                  or NULL
  *   dbg_dgates     [T][4H][B] dtype gate gradient before sparsifying (the
  *                  exact values that were scored), or NULL
  *   ws             lstmss_workspace_bytes(d, sparsity, s) bytes. */
@@ -143,11 +163,13 @@ int32_t lstm_bwd_structsparse(const lstmss_dims *d, float sparsity, const lstmss
                               void *dbg_dgates, void *ws, size_t ws_bytes, void *stream);
 
 /* Score, select and compact one given gate-gradient matrix (the selection
- * step of lstm_bwd_structsparse on its own, same device code).
+ * step of lstm_bwd_structsparse on its own, same scoring and ranking code).
  *   dG     [4H][B] dtype (d->T is ignored)
- *   dG_c   [K'][B] dtype, kept rows in ascending order
- *   idx    [K'/P] int32 kept slice indices
- *   scores [4H/P] fp64 slice scores, or NULL */
+ *   dG_c   [K'][B] dtype: COARSE kept rows in ascending order; FINE the
+ *          masked matrix (removed blocks zero)
+ *   idx    [lstmss_index_entries] int32 (see lstm_bwd_structsparse)
+ *   scores COARSE [4H/P] fp64 slice scores; FINE [4H/Mx][nb] fp64 block
+ *          scores; or NULL */
 int32_t lstmss_select_compact(const lstmss_dims *d, float sparsity, const lstmss_structure *s,
                               const void *dG, void *dG_c, int32_t *idx, double *scores,
                               void *stream);

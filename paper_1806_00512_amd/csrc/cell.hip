@@ -586,6 +586,159 @@ __global__ __launch_bounds__(64) void cell_select_kernel2(CellArgs a) {
     }
 }
 
+// ---------------------------------------------------------------------------
+// Fine-grained structure (section 3, Fig. 2(b)): a slice of P = Mx gate rows
+// is its own region; it is cut into nb blocks of My batch columns (the last
+// block narrower when My does not divide B) and the S = K blocks of lowest
+// squared L2 norm are removed.  A work-group owns FK_ROWS rows (whole
+// slices) over every batch column: a wavefront computes a row at a time
+// (lane l holds columns l, l+64, ...), each My-lane group reduces its block's
+// squares by an xor butterfly (My/2, ..., 1), and one thread per (slice,
+// block) folds the rows in order, ranks the block inside its slice and
+// places it in the per-slice index.  The masked rows (removed blocks zeroed)
+// go to dGc in the full [4H][B] layout; the bias gradient adds each masked
+// row's sum.
+// ---------------------------------------------------------------------------
+constexpr int FK_WAVES = 4;
+constexpr int FK_ROWS = 32;
+
+template <typename TS, int MODE>
+__global__ __launch_bounds__(FK_WAVES * 64) void cell_fine_kernel(CellArgs a) {
+    __shared__ double s_blk[FK_ROWS][64];     // [row][block] row-block sums of squares
+    __shared__ double s_sc[FK_ROWS][64];      // [slice][block] scores (slices <= FK_ROWS)
+    __shared__ unsigned char s_keep[FK_ROWS][64];
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int B = a.B, H = a.H, P = a.P, My = a.My, nb = a.nb, K = a.S;
+    const long G = 4L * H;
+    const int ns = FK_ROWS / P;                   // slices per work-group
+    const long s0 = (long)blockIdx.x * ns;        // first slice
+    const long row0 = s0 * P;
+    const int nrows = (int)min((long)FK_ROWS, G - row0);
+    const int nsl = nrows / P;
+    constexpr int NJ = 4;                         // 64-column chunks (B <= 256)
+    constexpr int RPW = FK_ROWS / FK_WAVES;       // rows per wavefront
+
+    const TS *__restrict__ gates = (const TS *)a.gates;
+    const float *__restrict__ dHup = a.dH_up;
+    const float *__restrict__ ct = a.c_t;
+    const float *__restrict__ cp = a.c_prev;
+    const float *__restrict__ dcin = a.dc_in;
+    TS *dbg = (TS *)a.dbg;
+
+    float vals[RPW][NJ];
+#pragma unroll
+    for (int k = 0; k < RPW; ++k) {
+        const int lr = wave + FK_WAVES * k;
+        const bool rin = lr < nrows;
+        const long r = row0 + (rin ? lr : 0);
+        const int g = (int)(r / H), u = (int)(r - (long)g * H);
+#pragma unroll
+        for (int j = 0; j < NJ; ++j) {
+            const int b = 64 * j + lane;
+            const bool in = rin && b < B;
+            float val = 0.f;
+            if (in) {
+                if (MODE == CELL_GIVEN) {
+                    val = st<TS>::load((const TS *)a.dG_in, r * B + b);
+                } else {
+                    const int e = u * B + b;
+                    const float dh = sum_parts(dHup[e], a.dh_part + e, a.dh_nparts, a.dh_stride);
+                    const float tc = tanhf(ct[e]);
+                    const float o = st<TS>::load(gates, (long)(3 * H + u) * B + b);
+                    if (g == 3) {
+                        val = dh * tc * o * (1.f - o);
+                    } else {
+                        const float dcv = (dcin ? dcin[e] : 0.f) + dh * o * (1.f - tc * tc);
+                        if (g == 1) {
+                            const float f = st<TS>::load(gates, (long)(H + u) * B + b);
+                            a.dc_out[e] = dcv * f;
+                            val = dcv * cp[e] * f * (1.f - f);
+                        } else {
+                            const float i = st<TS>::load(gates, (long)u * B + b);
+                            const float gg = st<TS>::load(gates, (long)(2 * H + u) * B + b);
+                            val = g == 0 ? dcv * gg * i * (1.f - i) : dcv * i * (1.f - gg * gg);
+                        }
+                    }
+                    val = st<TS>::rnd(val);
+                    if (dbg)
+                        st<TS>::store(dbg, r * B + b, val);
+                }
+            }
+            vals[k][j] = val;
+            // block sums of this chunk: butterfly inside each My-lane group
+            if (64 * j < B) {
+                double q = (double)val * (double)val;
+                for (int off = My >> 1; off >= 1; off >>= 1)
+                    q = q + shfl_xor_f64(q, off);
+                if (rin && (lane & (My - 1)) == 0 && (64 * j + lane) / My < nb)
+                    s_blk[lr][(64 * j + lane) / My] = q;
+            }
+        }
+    }
+    __syncthreads();
+
+    // one thread per (slice, block): score (rows folded in order)
+    const int pairs = nsl * nb;
+    for (int pi = tid; pi < pairs; pi += FK_WAVES * 64) {
+        const int sl = pi / nb, c = pi - sl * nb;
+        double sc = s_blk[sl * P][c];
+        for (int p = 1; p < P; ++p)
+            sc = sc + s_blk[sl * P + p][c];
+        s_sc[sl][c] = sc;
+        if (a.scores)
+            a.scores[(s0 + sl) * nb + c] = sc;
+    }
+    __syncthreads();
+    // rank inside the slice: keep the blocks outranked by fewer than nb - K
+    for (int pi = tid; pi < pairs; pi += FK_WAVES * 64) {
+        const int sl = pi / nb, c = pi - sl * nb;
+        const uint64_t kc = score_key(s_sc[sl][c]);
+        int beaten = 0;
+        for (int i = 0; i < nb; ++i)
+            if (i != c && outranks(score_key(s_sc[sl][i]), i, kc, c))
+                ++beaten;
+        s_keep[sl][c] = beaten < nb - K ? 1 : 0;
+    }
+    __syncthreads();
+    // per-slice offset index of the kept blocks (ascending)
+    for (int pi = tid; pi < pairs; pi += FK_WAVES * 64) {
+        const int sl = pi / nb, c = pi - sl * nb;
+        if (s_keep[sl][c]) {
+            int pos = 0;
+            for (int i = 0; i < c; ++i)
+                pos += s_keep[sl][i];
+            a.idx[(s0 + sl) * (nb - K) + pos] = c;
+        }
+    }
+
+    // masked rows to dGc; bias gradient of the masked rows
+    TS *dGc = (TS *)a.dGc;
+#pragma unroll
+    for (int k = 0; k < RPW; ++k) {
+        const int lr = wave + FK_WAVES * k;
+        const bool rin = lr < nrows;
+        const long r = row0 + (rin ? lr : 0);
+        const int sl = (rin ? lr : 0) / P;
+        float rs = 0.f;
+#pragma unroll
+        for (int j = 0; j < NJ; ++j) {
+            const int b = 64 * j + lane;
+            const bool in = rin && b < B;
+            const float m = in && s_keep[sl][b / My] ? vals[k][j] : 0.f;
+            if (in)
+                st<TS>::store(dGc, r * B + b, m);
+            rs += m;
+        }
+        if (MODE != CELL_GIVEN && a.db) {
+#pragma unroll
+            for (int off = 32; off >= 1; off >>= 1)
+                rs += shfl_xor_f32(rs, off);
+            if (rin && lane == 0)
+                a.db[r] += rs;
+        }
+    }
+}
+
 // db[r] (+)= sum over steps [t0, t1) of the row sums of the steps where r's
 // slice was kept (all steps when idx is NULL), steps in decreasing order.
 __global__ void bias_grad_kernel(float *db, const float *chunk_rs, int nch, long G, int t0, int t1,
@@ -676,6 +829,23 @@ hipError_t launch_cell_split(const CellArgs &a, int mode, bool bf16, hipStream_t
         hipLaunchKernelGGL((cell_select_kernel2<bf16_t>), dim3(grid), dim3(64), 0, s, a);
     else
         hipLaunchKernelGGL((cell_select_kernel2<float>), dim3(grid), dim3(64), 0, s, a);
+    return hipGetLastError();
+}
+
+hipError_t launch_cell_fine(const CellArgs &a, int mode, bool bf16, hipStream_t s) {
+    if (a.P < 1 || a.P > FK_ROWS || FK_ROWS % a.P != 0 || a.My < 1 || a.My > 64 ||
+        (a.My & (a.My - 1)) != 0 || a.nb < 1 || a.nb > 64 || a.B > 256 ||
+        (mode != CELL_SPARSE && mode != CELL_GIVEN) || (4L * a.H) % a.P != 0)
+        return hipErrorInvalidValue;
+    const int ns = FK_ROWS / a.P;
+    const dim3 grid((unsigned)ceil_div(4L * a.H / a.P, ns));
+#define LSTMSS_FK(TS, M) hipLaunchKernelGGL((cell_fine_kernel<TS, M>), grid, dim3(FK_WAVES * 64), 0, s, a)
+    if (bf16) {
+        if (mode == CELL_GIVEN) LSTMSS_FK(bf16_t, CELL_GIVEN); else LSTMSS_FK(bf16_t, CELL_SPARSE);
+    } else {
+        if (mode == CELL_GIVEN) LSTMSS_FK(float, CELL_GIVEN); else LSTMSS_FK(float, CELL_SPARSE);
+    }
+#undef LSTMSS_FK
     return hipGetLastError();
 }
 

@@ -36,6 +36,10 @@ struct CellArgs {
     void *stage;           // [4H][B] gate gradient before selection (sparse)
     double *chunk_sq;      // [4H][ceil(B/64)] fp64 chunk sums of squares
     float *chunk_rs;       // [4H][ceil(B/64)] fp32 chunk row sums
+    // fine-grained structure: slices of P rows cut into nb blocks of My batch
+    // columns, S blocks removed per slice; dGc is then the masked [4H][B]
+    // matrix, idx [4H/P][nb - S] the kept blocks and scores [4H/P][nb]
+    int My, nb;
 };
 
 // Data gradient [dx_t; dh_{t-1}] = W_c^T dG_c, split over K into partials.
@@ -106,6 +110,9 @@ struct FwdArgs {
 };
 
 hipError_t launch_cell(const CellArgs &a, int mode, bool bf16, hipStream_t s);
+// Fine-grained structure (mode CELL_SPARSE or CELL_GIVEN): P <= 16, My a
+// power of two <= 64, nb <= 64, B <= 256.
+hipError_t launch_cell_fine(const CellArgs &a, int mode, bool bf16, hipStream_t s);
 size_t cell_lds_bytes(const CellArgs &a, int mode);
 // True when launch_cell uses the split (element kernel + select kernel) path;
 // the bias gradient then comes from chunk_rs through launch_bias_grad.

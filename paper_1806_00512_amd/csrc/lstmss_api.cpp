@@ -171,8 +171,13 @@ int32_t check_dims(const lstmss_dims *d) {
 struct Plan {
     int P, R, S;
     long nslices;  // 4H / P
-    long kept;     // kept slices per step
-    long Kp;       // kept rows per step
+    long kept;     // index entries per step (coarse: kept slices)
+    long Kp;       // rows of the products' gate-gradient operand per step
+    // fine-grained structure: P = Mx rows per slice, nb blocks of My batch
+    // columns, S = K blocks removed per slice; the products then run on the
+    // masked [4H][B] matrix (Kp = 4H) and kept = slices * (nb - K)
+    bool fine = false;
+    int My = 0, nb = 0;
 };
 
 // Slices removed from a region of r slices.
@@ -192,8 +197,37 @@ int32_t make_plan(const lstmss_dims *d, float sparsity, const lstmss_structure *
     }
     if (!s)
         return fail(LSTMSS_ERR_INVALID_ARG, "structure is NULL");
-    if (s->kind == LSTMSS_FINE)
-        return fail(LSTMSS_ERR_UNSUPPORTED, "fine-grained structure is not built");
+    if (s->kind == LSTMSS_FINE) {
+        if (s->Mx < 1 || s->Mx > 16 || G % s->Mx != 0 || 32 % s->Mx != 0)
+            return fail(LSTMSS_ERR_INVALID_ARG, "Mx=%d must divide 32 and 4H=%ld", s->Mx, G);
+        if (s->My < 2 || s->My > 64 || (s->My & (s->My - 1)) != 0)
+            return fail(LSTMSS_ERR_INVALID_ARG, "My=%d must be a power of two in [2, 64]", s->My);
+        if (d->B > 256)
+            return fail(LSTMSS_ERR_UNSUPPORTED, "fine-grained structure needs B <= 256");
+        const long nb = ((long)d->B + s->My - 1) / s->My;
+        if (nb > 64)
+            return fail(LSTMSS_ERR_INVALID_ARG, "%ld blocks of My=%d per slice (at most 64)", nb,
+                        s->My);
+        if (!(sparsity >= 0.f) || !(sparsity < 1.f))
+            return fail(LSTMSS_ERR_INVALID_ARG, "sparsity %g must be in [0, 1)", (double)sparsity);
+        const double kr = (double)sparsity * nb;
+        const double Kr = std::nearbyint(kr);
+        if (std::fabs(kr - Kr) > 1e-6 * std::fmax(1.0, (double)nb))
+            return fail(LSTMSS_ERR_INVALID_ARG, "sparsity %g * %ld blocks is not an integer",
+                        (double)sparsity, nb);
+        p->fine = true;
+        p->P = s->Mx;
+        p->My = s->My;
+        p->nb = (int)nb;
+        p->R = (int)nb;
+        p->S = (int)Kr;
+        if (p->S < 0 || p->S >= nb)
+            return fail(LSTMSS_ERR_INVALID_ARG, "K=%d must be in [0, %ld)", p->S, nb);
+        p->nslices = G / s->Mx;
+        p->kept = p->nslices * (nb - p->S);
+        p->Kp = G;
+        return LSTMSS_OK;
+    }
     if (s->kind != LSTMSS_COARSE)
         return fail(LSTMSS_ERR_INVALID_ARG, "unknown structure kind %d", s->kind);
     if (s->P < 1 || G % s->P != 0)
@@ -314,6 +348,10 @@ int32_t backward_enqueue(const lstmss_dims *d, bool dense, const Plan &p, const 
     const WsLayout L = ws_layout(d, p);
     const bool bf16 = d->dtype == LSTMSS_BF16;
     const bool sparse = !dense;
+    // the fine structure masks the gate gradient in place; its products run
+    // on the masked matrix like the dense ones, without a row gather
+    const bool fine = sparse && p.fine;
+    const bool gsparse = sparse && !fine;
     const int T = d->T, B = d->B, I = d->I, H = d->H;
     const long HB = (long)H * B, G = 4L * H, K = (long)I + H;
     const size_t es = elem_bytes(d->dtype);
@@ -336,7 +374,7 @@ int32_t backward_enqueue(const lstmss_dims *d, bool dense, const Plan &p, const 
     // main stream) and the input gradient dX (a batched data-gradient GEMM
     // over the chunk's steps).  The main stream only carries the gate kernel
     // and the dh rows of the data gradient for every step.
-    const bool batched = !sparse || wgrad_supported(p.P, p.R, p.S);
+    const bool batched = !gsparse || wgrad_supported(p.P, p.R, p.S);
     if (!batched)
         HIP_TRY(timed(LSTMSS_KERNEL_AUX, st, [&] { return launch_fill(dW, G * K, 0.f, st); }));
     // gate kernels: the split path (large shapes) leaves the bias gradient to
@@ -344,7 +382,7 @@ int32_t backward_enqueue(const lstmss_dims *d, bool dense, const Plan &p, const 
     CellArgs probe{};
     probe.B = B; probe.H = H; probe.P = sparse ? p.P : 1; probe.R = sparse ? p.R : 1;
     probe.regions_per_wg = sparse ? std::max(1, 32 / (p.R * p.P)) : 32;
-    const bool split = cell_split_ok(probe, sparse ? CELL_SPARSE : CELL_DENSE);
+    const bool split = !fine && cell_split_ok(probe, sparse ? CELL_SPARSE : CELL_DENSE);
     const int nch = (int)ceil_div(B, 64);
     float *chunk_rs_all = (float *)(wb + L.chunk_rs);
     if (!split)
@@ -366,7 +404,7 @@ int32_t backward_enqueue(const lstmss_dims *d, bool dense, const Plan &p, const 
     }
     int wg_hi = T, dx_hi = T, wg_count = 0, forks = 0;
     WgradArgs wg{};
-    wg.Gc = dGc_all; wg.idx = sparse ? idx_all : nullptr; wg.x = x; wg.h = hst;
+    wg.Gc = dGc_all; wg.idx = gsparse ? idx_all : nullptr; wg.x = x; wg.h = hst;
     wg.T = T; wg.I = I; wg.H = H; wg.B = B; wg.Kp = (int)p.Kp; wg.kept = (int)p.kept;
     wg.P = p.P; wg.R = p.R; wg.S = p.S; wg.dW = dW;
 
@@ -418,10 +456,15 @@ int32_t backward_enqueue(const lstmss_dims *d, bool dense, const Plan &p, const 
             ca.chunk_sq = (double *)(wb + L.chunk_sq);
             ca.chunk_rs = chunk_rs_all + (size_t)t * G * nch;
         }
-        if (!split &&
+        ca.My = p.My;
+        ca.nb = p.nb;
+        if (!split && !fine &&
             cell_lds_bytes(ca, sparse ? CELL_SPARSE : CELL_DENSE) > kMaxLds)
             return fail(LSTMSS_ERR_UNSUPPORTED, "R*P*B too large for one work-group's LDS");
-        HIP_TRY(timed(LSTMSS_KERNEL_GATES, st, [&] { return launch_cell(ca, sparse ? CELL_SPARSE : CELL_DENSE, bf16, st); }));
+        HIP_TRY(timed(LSTMSS_KERNEL_GATES, st, [&] {
+            return fine ? launch_cell_fine(ca, CELL_SPARSE, bf16, st)
+                        : launch_cell(ca, sparse ? CELL_SPARSE : CELL_DENSE, bf16, st);
+        }));
 
         const bool wg_now = use_side && batched && t == std::max(0, wg_hi - chunk_len);
         const bool dx_now = use_side && dX && t == std::max(0, dx_hi - dx_len);
@@ -434,12 +477,12 @@ int32_t backward_enqueue(const lstmss_dims *d, bool dense, const Plan &p, const 
             wg.t_begin = t;
             wg.t_end = wg_hi;
             wg.accumulate = wg_count++ > 0;
-            HIP_TRY(timed(LSTMSS_KERNEL_WEIGHT_GRAD, sst, [&] { return launch_wgrad(wg, sparse, bf16, sst); }));
+            HIP_TRY(timed(LSTMSS_KERNEL_WEIGHT_GRAD, sst, [&] { return launch_wgrad(wg, gsparse, bf16, sst); }));
             wg_hi = t;
         }
         if (dx_now) {
             gx.Gc = dGc;
-            gx.idx = sparse ? idx : nullptr;
+            gx.idx = gsparse ? idx : nullptr;
             gx.part = dX + (size_t)t * I * B;
             gx.steps = dx_hi - t;
             HIP_TRY(timed(LSTMSS_KERNEL_DATA_GRAD, sst, [&] { return launch_gemm1(gx, bf16, sst); }));
@@ -448,7 +491,7 @@ int32_t backward_enqueue(const lstmss_dims *d, bool dense, const Plan &p, const 
 
         // dh rows of the data gradient for the next (earlier) step
         Gemm1Args g1{};
-        g1.W = W; g1.ldw = K; g1.Gc = dGc; g1.idx = sparse ? idx : nullptr; g1.P = p.P;
+        g1.W = W; g1.ldw = K; g1.Gc = dGc; g1.idx = gsparse ? idx : nullptr; g1.P = p.P;
         g1.Kp = p.Kp; g1.M = (int)K; g1.m_begin = I; g1.N = B; g1.out_row0 = I;
         g1.part = part; g1.part_stride = part_stride; g1.splitk = L.splitk;
         g1.k_chunk = L.k_chunk; g1.steps = 1;
@@ -456,7 +499,7 @@ int32_t backward_enqueue(const lstmss_dims *d, bool dense, const Plan &p, const 
 
         if (!batched) {
             Gemm2Args g2{};
-            g2.Gc = dGc; g2.idx = sparse ? idx : nullptr; g2.P = p.P; g2.Kp = p.Kp;
+            g2.Gc = dGc; g2.idx = gsparse ? idx : nullptr; g2.P = p.P; g2.Kp = p.Kp;
             g2.xt = (const char *)x + (size_t)t * I * B * es;
             g2.hp = hst + (size_t)t * HB * es;
             g2.I = I; g2.H = H; g2.B = B; g2.dW = dW;
@@ -515,7 +558,8 @@ int32_t backward(const lstmss_dims *d, bool dense, float sparsity, const lstmss_
     auto u = [](const void *q) { return (uint64_t)(uintptr_t)q; };
     std::vector<uint64_t> key = {(uint64_t)d->T, (uint64_t)d->B, (uint64_t)d->I, (uint64_t)d->H,
                                  (uint64_t)d->dtype, (uint64_t)dense, (uint64_t)p.P,
-                                 (uint64_t)p.R, (uint64_t)p.S, u(x), u(W), u(cache), u(dH_up),
+                                 (uint64_t)p.R, (uint64_t)p.S, (uint64_t)p.fine, (uint64_t)p.My,
+                                 u(x), u(W), u(cache), u(dH_up),
                                  u(dhT), u(dcT), u(dX), u(dW), u(db), u(dh0), u(dc0), u(idx_out),
                                  u(dbg), u(ws)};
     GraphEntry *hit = nullptr;
@@ -593,6 +637,17 @@ int64_t lstmss_kept_rows(const lstmss_dims *d, float sparsity, const lstmss_stru
     if (rc)
         return rc;
     return p.Kp;
+}
+
+int64_t lstmss_index_entries(const lstmss_dims *d, float sparsity, const lstmss_structure *s) {
+    int32_t rc = check_dims(d);
+    if (rc)
+        return rc;
+    Plan p;
+    rc = make_plan(d, sparsity, s, false, &p);
+    if (rc)
+        return rc;
+    return p.fine ? p.kept : p.Kp / p.P;
 }
 
 int64_t lstmss_workspace_bytes(const lstmss_dims *d, float sparsity, const lstmss_structure *s) {
@@ -678,6 +733,13 @@ int32_t lstmss_select_compact(const lstmss_dims *d, float sparsity, const lstmss
     ca.dGc = dG_c;
     ca.idx = idx;
     ca.scores = scores;
+    ca.My = p.My;
+    ca.nb = p.nb;
+    if (p.fine) {
+        hipStream_t st = (hipStream_t)stream;
+        HIP_TRY(timed(LSTMSS_KERNEL_GATES, st, [&] { return launch_cell_fine(ca, CELL_GIVEN, d->dtype == LSTMSS_BF16, st); }));
+        return LSTMSS_OK;
+    }
     if (cell_lds_bytes(ca, CELL_GIVEN) > kMaxLds)
         return fail(LSTMSS_ERR_UNSUPPORTED, "R*P*B too large for one work-group's LDS");
     hipStream_t st = (hipStream_t)stream;

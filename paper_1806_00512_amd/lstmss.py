@@ -8,7 +8,7 @@ current stream.  The entry points mirror include/lstmss.h:
   bwd_dense              -> lstm_bwd_dense
   bwd_structsparse       -> lstm_bwd_structsparse
   select_compact         -> lstmss_select_compact
-  cache_bytes / kept_rows / workspace_bytes -> the size queries
+  cache_bytes / kept_rows / index_entries / workspace_bytes -> the size queries
 
 Loading fails loudly (RuntimeError) when liblstmss.so has not been built;
 there is no fallback implementation.
@@ -30,7 +30,8 @@ ERR = {0: "ok", -1: "invalid argument", -2: "unsupported", -3: "workspace too sm
 
 # Exported symbols of include/lstmss.h
 SYMBOLS = ("lstmss_version", "lstmss_strerror", "lstmss_last_error", "lstmss_cache_bytes",
-           "lstmss_kept_rows", "lstmss_workspace_bytes", "lstm_fwd_cache", "lstm_bwd_dense",
+           "lstmss_kept_rows", "lstmss_index_entries", "lstmss_workspace_bytes",
+           "lstm_fwd_cache", "lstm_bwd_dense",
            "lstm_bwd_structsparse", "lstmss_select_compact", "lstmss_set_option",
            "lstmss_timing_enable", "lstmss_timing_read", "lstmss_timing_reset")
 KERNEL_KINDS = {"gates_select_compact": 0, "data_grad_gemm": 1, "weight_grad_gemm": 2, "aux": 3,
@@ -74,6 +75,8 @@ def load():
     lib.lstmss_cache_bytes.restype = i64
     lib.lstmss_kept_rows.argtypes = [pd, f, ps]
     lib.lstmss_kept_rows.restype = i64
+    lib.lstmss_index_entries.argtypes = [pd, f, ps]
+    lib.lstmss_index_entries.restype = i64
     lib.lstmss_workspace_bytes.argtypes = [pd, f, ps]
     lib.lstmss_workspace_bytes.restype = i64
     lib.lstm_fwd_cache.argtypes = [pd, vp, vp, vp, vp, vp, vp, vp, vp]
@@ -120,8 +123,9 @@ def dims(T, B, I, H, dtype=F32) -> Dims:
     return Dims(int(T), int(B), int(I), int(H), _dt(dtype))
 
 
-def structure(P=4, R=8, kind=COARSE) -> Structure:
-    return Structure(int(kind), int(P), int(R), 0, 0)
+def structure(P=4, R=8, kind=COARSE, My=0, Mx=0) -> Structure:
+    """COARSE uses P, R; FINE uses My (block width), Mx (rows per slice)."""
+    return Structure(int(kind), int(P), int(R), int(My), int(Mx))
 
 
 def _ptr(t, dtype=None, shape=None, name="tensor"):
@@ -154,6 +158,12 @@ def cache_bytes(d: Dims) -> int:
 def kept_rows(d: Dims, sparsity: float, s: Structure) -> int:
     n = load().lstmss_kept_rows(ctypes.byref(d), float(sparsity), ctypes.byref(s))
     _check(0 if n >= 0 else int(n), "lstmss_kept_rows")
+    return int(n)
+
+
+def index_entries(d: Dims, sparsity: float, s: Structure) -> int:
+    n = load().lstmss_index_entries(ctypes.byref(d), float(sparsity), ctypes.byref(s))
+    _check(0 if n >= 0 else int(n), "lstmss_index_entries")
     return int(n)
 
 
@@ -220,19 +230,21 @@ def bwd_dense(x, W, cache, dH_up, dhT=None, dcT=None, want_dX=True, out=None, ws
 
 
 def bwd_structsparse(x, W, cache, dH_up, sparsity=0.5, P=4, R=8, dhT=None, dcT=None,
-                     want_dX=True, want_idx=True, want_dbg=False, out=None, ws=None, stream=None):
-    """Structurally sparsified backward of one layer.
+                     want_dX=True, want_idx=True, want_dbg=False, out=None, ws=None, stream=None,
+                     kind=COARSE, My=0, Mx=0):
+    """Structurally sparsified backward of one layer (COARSE: P, R; FINE: My, Mx).
 
-    Returns dict(dX, dW, db, dh0, dc0, idx [T][K'/P] int32, dbg [T][4H][B] or None)."""
+    Returns dict(dX, dW, db, dh0, dc0, idx [T][index entries] int32,
+    dbg [T][4H][B] or None)."""
     T, I, B = x.shape
     H = W.shape[0] // 4
     st = x.dtype
     d = dims(T, B, I, H, st)
-    s = structure(P, R)
+    s = structure(P, R, kind, My, Mx)
     o = _bwd_outputs(T, B, I, H, x.device, want_dX, out)
-    kp = kept_rows(d, sparsity, s)
+    ne = index_entries(d, sparsity, s)
     if want_idx and o.get("idx") is None:
-        o["idx"] = torch.empty((T, kp // P), dtype=torch.int32, device=x.device)
+        o["idx"] = torch.empty((T, ne), dtype=torch.int32, device=x.device)
     if want_dbg and o.get("dbg") is None:
         o["dbg"] = torch.empty((T, 4 * H, B), dtype=st, device=x.device)
     if ws is None:
@@ -245,24 +257,37 @@ def bwd_structsparse(x, W, cache, dH_up, sparsity=0.5, P=4, R=8, dhT=None, dcT=N
         _ptr(dcT, f32, (H, B), "dcT"), _ptr(o.get("dX"), f32, (T, I, B), "dX"),
         _ptr(o["dW"], f32, name="dW"), _ptr(o["db"], f32, name="db"),
         _ptr(o["dh0"], f32, name="dh0"), _ptr(o["dc0"], f32, name="dc0"),
-        _ptr(o.get("idx"), torch.int32, (T, kp // P), "idx"),
+        _ptr(o.get("idx"), torch.int32, (T, ne), "idx"),
         _ptr(o.get("dbg"), st, (T, 4 * H, B), "dbg"), _ptr(ws, torch.uint8, name="ws"),
         ws.numel(), _stream(stream))
     _check(rc, "lstm_bwd_structsparse")
     return o
 
 
-def select_compact(dG, sparsity=0.5, P=4, R=8, want_scores=True, stream=None):
-    """Score / select / compact one gate-gradient matrix dG [4H][B]."""
+def select_compact(dG, sparsity=0.5, P=4, R=8, want_scores=True, stream=None, kind=COARSE,
+                   My=0, Mx=0):
+    """Score / select / compact one gate-gradient matrix dG [4H][B].
+
+    COARSE: (kept rows [K'][B], kept slice indices, slice scores [4H/P]).
+    FINE: (masked matrix [4H][B], kept block indices [4H/Mx][nb-K],
+    block scores [4H/Mx][nb])."""
     G, B = dG.shape
     H = G // 4
     st = dG.dtype
     d = dims(1, B, 1, H, st)
-    s = structure(P, R)
+    s = structure(P, R, kind, My, Mx)
     kp = kept_rows(d, sparsity, s)
+    ne = index_entries(d, sparsity, s)
     dGc = torch.empty((kp, B), dtype=st, device=dG.device)
-    idx = torch.empty((kp // P,), dtype=torch.int32, device=dG.device)
-    sc = torch.empty((G // P,), dtype=torch.float64, device=dG.device) if want_scores else None
+    if kind == FINE:
+        nb = -(-B // My)
+        idx = torch.empty((G // Mx, ne // (G // Mx)), dtype=torch.int32, device=dG.device)
+        sc = (torch.empty((G // Mx, nb), dtype=torch.float64, device=dG.device)
+              if want_scores else None)
+    else:
+        idx = torch.empty((ne,), dtype=torch.int32, device=dG.device)
+        sc = (torch.empty((G // P,), dtype=torch.float64, device=dG.device)
+              if want_scores else None)
     rc = load().lstmss_select_compact(ctypes.byref(d), float(sparsity), ctypes.byref(s),
                                       _ptr(dG, st, name="dG"), _ptr(dGc), _ptr(idx), _ptr(sc),
                                       _stream(stream))

@@ -84,10 +84,42 @@ def test_bad_structure(L, P, R, sp, code):
     assert n == code
 
 
-def test_fine_kind_unsupported(L):
-    d = L.dims(2, 4, 4, 8)
-    n = L.load().lstmss_kept_rows(ctypes.byref(d), 0.5, ctypes.byref(L.structure(4, 8, L.FINE)))
-    assert n == -2
+@pytest.mark.parametrize("B,My,Mx,sp", [(128, 16, 4, 0.5), (100, 32, 4, 0.25), (256, 32, 2, 0.75),
+                                         (20, 4, 8, 0.2), (64, 64, 1, 0.0)])
+def test_fine_sizes(L, B, My, Mx, sp):
+    """Fine structure: products run on the masked [4H][B] matrix; the index
+    lists nb - K kept blocks of every Mx-row slice (section 3, Fig. 2(b))."""
+    H = 64
+    d = L.dims(3, B, 32, H)
+    s = L.structure(kind=L.FINE, My=My, Mx=Mx)
+    nb = -(-B // My)
+    K = round(sp * nb)
+    assert L.kept_rows(d, sp, s) == 4 * H
+    assert L.index_entries(d, sp, s) == (4 * H // Mx) * (nb - K)
+    assert L.workspace_bytes(d, sp, s) >= 3 * 4 * H * B * 4
+
+
+@pytest.mark.parametrize("B,My,Mx,sp,code", [
+    (128, 16, 3, 0.5, -1),    # Mx does not divide 32
+    (128, 16, 32, 0.5, -1),   # Mx above 16
+    (128, 12, 4, 0.5, -1),    # My not a power of two
+    (128, 1, 4, 0.5, -1),     # My below 2
+    (128, 128, 4, 0.5, -1),   # My above 64
+    (128, 16, 4, 0.3, -1),    # sparsity * nb not an integer
+    (128, 16, 4, 1.0, -1),    # every block removed
+    (256, 2, 4, 0.5, -1),     # 128 blocks per slice
+    (512, 64, 4, 0.5, -2)])   # batch above the fine kernel's 256 columns
+def test_bad_fine_structure(L, B, My, Mx, sp, code):
+    d = L.dims(2, B, 4, 8)
+    s = L.structure(kind=L.FINE, My=My, Mx=Mx)
+    assert L.load().lstmss_kept_rows(ctypes.byref(d), sp, ctypes.byref(s)) == code
+    assert L.load().lstmss_index_entries(ctypes.byref(d), sp, ctypes.byref(s)) == code
+
+
+def test_coarse_index_entries(L):
+    d = L.dims(2, 20, 650, 650)
+    s = L.structure(4, 8)
+    assert L.index_entries(d, 0.5, s) == L.kept_rows(d, 0.5, s) // 4
 
 
 def test_null_pointers_rejected_before_launch(L):

@@ -1,0 +1,210 @@
+"""GPU parity of the fine-grained structure (section 3, Fig. 2(b)) against the
+CPU oracle, through the C ABI.
+
+  1. standalone selection: identical gate-gradient bytes -> block scores,
+     kept block indices and the masked matrix bit-exact;
+  2. in situ: the GPU's own pre-sparsify gate gradient (debug dump) of every
+     step re-selected by the oracle gives the GPU's indices exactly;
+  3. gradients: the oracle run with the GPU's masks matches dX, dW, db, dh0,
+     dc0 to rel. L2 <= 1e-5 (fp32) / 2e-2 (bf16).
+"""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from paper_1806_00512_amd.inputs import make_layer
+
+pytestmark = pytest.mark.gpu
+
+TOL = {"f32": 1e-5, "bf16": 2e-2}
+
+
+@pytest.fixture(scope="module")
+def L():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    import paper_1806_00512_amd.lstmss as lstmss
+    lstmss.load()
+    return lstmss
+
+
+def dev():
+    return torch.device("cuda:0")
+
+
+def rel(a, b):
+    a, b = np.asarray(a, np.float64), np.asarray(b, np.float64)
+    n = np.linalg.norm(b)
+    return float(np.linalg.norm(a - b) / (n if n > 0 else 1.0))
+
+
+def to_np64(t):
+    return t.detach().float().cpu().numpy().astype(np.float64)
+
+
+def gpu_tensor(a, dtype="f32"):
+    t = torch.from_numpy(np.ascontiguousarray(a, dtype=np.float32)).to(dev())
+    return t.to(torch.bfloat16) if dtype == "bf16" else t
+
+
+def mask_of(keep, Mx, My, B):
+    """[nslices][nb] keep flags -> [nslices*Mx][B] element mask."""
+    m = np.repeat(np.repeat(keep, Mx, axis=0), My, axis=1)
+    return m[:, :B]
+
+
+def adversarial_fine(H, B, Mx, My, seed, dtype):
+    """Random rows of widely varying scale, plus blocks that tie exactly:
+    zero blocks, a block copied within its slice, and a slice whose blocks
+    are column permutations of one another."""
+    rng = np.random.default_rng(seed)
+    G = 4 * H
+    dG = (rng.standard_normal((G, B)) * np.exp(rng.uniform(-3, 3, (G, 1)))).astype(np.float32)
+    nb = -(-B // My)
+    if nb >= 3 and G // Mx >= 3 and B >= 2 * My:
+        dG[0:Mx, 0:My] = 0.0                                   # zero block
+        dG[0:Mx, My:2 * My] = 0.0                              # tied zero block
+        dG[Mx:2 * Mx, My:2 * My] = dG[Mx:2 * Mx, 0:My]         # duplicate block
+        perm = rng.permutation(My)
+        dG[2 * Mx:3 * Mx, My:2 * My] = dG[2 * Mx:3 * Mx, 0:My][:, perm]
+    if dtype == "bf16":
+        dG = torch.from_numpy(dG).to(torch.bfloat16).float().numpy()
+    return dG
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+@pytest.mark.parametrize("H,B,Mx,My,sp", [
+    (64, 128, 4, 16, 0.5),     # 8 blocks of 16 columns, two 64-column passes
+    (64, 100, 4, 32, 0.25),    # ragged last block (4 columns)
+    (650, 20, 4, 4, 0.4),      # 5 blocks; 2600 rows: last work-group partial
+    (32, 256, 2, 64, 0.75),    # four 64-column passes, one block each
+    (48, 64, 8, 8, 0.5),       # 8-row slices
+    (40, 33, 1, 2, 8 / 17),    # one-row slices, 17 blocks, last block one column
+    (16, 256, 16, 4, 0.5),     # 64 blocks per slice (the maximum)
+    (24, 7, 4, 8, 0.0),        # one block narrower than My, nothing removed
+])
+def test_fine_select_bit_exact(L, dtype, H, B, Mx, My, sp):
+    dG = adversarial_fine(H, B, Mx, My, H * 13 + B + My, dtype)
+    nb = oracle.fine_blocks(B, My)
+    K = int(round(sp * nb))
+    dGm, idx, sc = L.select_compact(gpu_tensor(dG, dtype), sparsity=sp, kind=L.FINE, My=My, Mx=Mx)
+    torch.cuda.synchronize()
+    ref_sc = oracle.fine_scores(dG.astype(np.float64), Mx, My)
+    assert np.array_equal(sc.cpu().numpy(), ref_sc)
+    keep = oracle.fine_select(ref_sc, K)
+    assert np.array_equal(idx.cpu().numpy(), oracle.fine_kept_index(keep, K))
+    ref = np.where(mask_of(keep, Mx, My, B) == 1, dG, 0.0).astype(np.float32)
+    got = dGm.float().cpu().numpy()
+    assert np.array_equal(got.view(np.uint32), ref.view(np.uint32))  # signed zeros too
+
+
+def test_fine_nan_block_is_kept(L):
+    H, B, Mx, My = 16, 64, 4, 8
+    dG = adversarial_fine(H, B, Mx, My, 5, "f32")
+    dG[4 * Mx + 2, 3 * My + 1] = np.nan
+    _, idx, _ = L.select_compact(gpu_tensor(dG), sparsity=0.75, kind=L.FINE, My=My, Mx=Mx)
+    torch.cuda.synchronize()
+    sc = oracle.fine_scores(dG.astype(np.float64), Mx, My)
+    ref = oracle.fine_kept_index(oracle.fine_select(sc, 6), 6)
+    got = idx.cpu().numpy()
+    assert np.array_equal(got, ref) and 3 in got[4]
+
+
+def check_layer_fine(L, d, dtype, sp, Mx, My):
+    T, I, B = d["x"].shape
+    H = d["W"].shape[0] // 4
+    bf16 = dtype == "bf16"
+    x, W = gpu_tensor(d["x"], dtype), gpu_tensor(d["W"], dtype)
+    b = gpu_tensor(d["b"]) if d.get("b") is not None else None
+    h0 = gpu_tensor(d["h0"]) if d.get("h0") is not None else None
+    c0 = gpu_tensor(d["c0"]) if d.get("c0") is not None else None
+    dH = gpu_tensor(d["dH_up"])
+    dhT = gpu_tensor(d["dhT"]) if d.get("dhT") is not None else None
+    dcT = gpu_tensor(d["dcT"]) if d.get("dcT") is not None else None
+    _, cache = L.fwd_cache(x, W, b, h0, c0)
+    o = L.bwd_structsparse(x, W, cache, dH, sparsity=sp, dhT=dhT, dcT=dcT, want_dbg=True,
+                           kind=L.FINE, My=My, Mx=Mx)
+    torch.cuda.synchronize()
+    gates, c, h = oracle.forward(d["x"], d["W"], d.get("b"), d.get("h0"), d.get("c0"), bf16=bf16)
+    nb = oracle.fine_blocks(B, My)
+    K = int(round(sp * nb))
+    idx = o["idx"].cpu().numpy().reshape(T, 4 * H // Mx, nb - K)
+    dbg = to_np64(o["dbg"])
+    keep = np.zeros((T, 4 * H // Mx, nb), np.uint8)
+    for t in range(T):
+        k = oracle.fine_select(oracle.fine_scores(dbg[t], Mx, My), K)
+        assert np.array_equal(oracle.fine_kept_index(k, K), idx[t]), "step %d" % t
+        keep[t] = k
+    ref = oracle.backward_fine(d["x"], d["W"], gates, c, h, d["dH_up"], d.get("dhT"),
+                               d.get("dcT"), Mx=Mx, My=My, K=K, bf16=bf16, forced_keep=keep)
+    for k in ("dX", "dW", "db", "dh0", "dc0"):
+        e = rel(to_np64(o[k]), ref[k])
+        assert e <= TOL[dtype], "%s rel L2 %.3g" % (k, e)
+    return o
+
+
+@pytest.mark.parametrize("T,B,I,H,sp,Mx,My,state", [
+    (5, 20, 100, 72, 0.4, 4, 4, False),     # 5 blocks, 288 rows: partial work-group
+    (4, 128, 64, 64, 0.5, 4, 16, True),     # initial state and dhT/dcT
+    (3, 100, 40, 64, 0.25, 8, 32, False),   # ragged last block
+    (2, 256, 32, 64, 0.75, 2, 64, True),    # four 64-column passes
+    (3, 33, 24, 40, 8 / 17, 1, 2, False),   # one-row slices, 17 blocks
+    (2, 1, 8, 8, 0.0, 4, 2, True),          # batch of one: one block, nothing removed
+])
+def test_layer_fine_f32(L, T, B, I, H, sp, Mx, My, state):
+    d = make_layer(T, B, I, H, seed=T * 31 + H + My, w_scale=0.2, state=state)
+    check_layer_fine(L, d, "f32", sp, Mx, My)
+
+
+@pytest.mark.parametrize("T,B,I,H,sp,Mx,My", [(3, 64, 48, 96, 0.5, 4, 8), (2, 200, 40, 64, 0.5, 4, 64)])
+def test_layer_fine_bf16(L, T, B, I, H, sp, Mx, My):
+    d = make_layer(T, B, I, H, seed=17 + B, w_scale=0.2, dtype="bf16", state=True)
+    check_layer_fine(L, d, "bf16", sp, Mx, My)
+
+
+def test_fine_language_model_shape(L):
+    """Two-layer 650-unit language-model layer shape (batch 20) with 4x4
+    blocks at 40% sparsity (5 blocks, 2 removed), full 35 steps."""
+    d = make_layer(35, 20, 650, 650, seed=23, w_scale=0.05, state=True)
+    check_layer_fine(L, d, "f32", 0.4, 4, 4)
+
+
+def test_fine_zero_sparsity_matches_dense(L):
+    d = make_layer(3, 48, 40, 64, seed=29, w_scale=0.2, state=True)
+    x, W, dH = gpu_tensor(d["x"]), gpu_tensor(d["W"]), gpu_tensor(d["dH_up"])
+    dhT, dcT = gpu_tensor(d["dhT"]), gpu_tensor(d["dcT"])
+    _, cache = L.fwd_cache(x, W, None, gpu_tensor(d["h0"]), gpu_tensor(d["c0"]))
+    a = L.bwd_dense(x, W, cache, dH, dhT, dcT)
+    b = L.bwd_structsparse(x, W, cache, dH, sparsity=0.0, dhT=dhT, dcT=dcT, kind=L.FINE, My=16,
+                           Mx=4)
+    torch.cuda.synchronize()
+    for k in ("dX", "dW", "db", "dh0", "dc0"):
+        assert rel(to_np64(b[k]), to_np64(a[k])) <= 1e-6, k
+    assert torch.equal(b["idx"].cpu(), torch.arange(3, dtype=torch.int32).repeat(3, 64))
+
+
+def test_fine_graph_replay_matches_direct(L):
+    d = make_layer(4, 64, 40, 64, seed=31, w_scale=0.2, state=True)
+    x, W, dH = gpu_tensor(d["x"]), gpu_tensor(d["W"]), gpu_tensor(d["dH_up"])
+    _, cache = L.fwd_cache(x, W)
+    kw = dict(sparsity=0.5, kind=L.FINE, My=8, Mx=4)
+    L.graphs_enable(False)
+    try:
+        ref = L.bwd_structsparse(x, W, cache, dH, **kw)
+        torch.cuda.synchronize()
+    finally:
+        L.graphs_enable(True)
+    d0 = L.dims(4, 64, 40, 64)
+    ws = torch.empty(L.workspace_bytes(d0, 0.5, L.structure(kind=L.FINE, My=8, Mx=4)),
+                     dtype=torch.uint8, device=dev())
+    out = {k: torch.empty_like(v) for k, v in ref.items() if v is not None}
+    for _ in range(3):
+        for v in out.values():
+            v.fill_(float("nan") if v.dtype.is_floating_point else -7)
+        torch.cuda.synchronize()
+        o = L.bwd_structsparse(x, W, cache, dH, out=out, ws=ws, **kw)
+        torch.cuda.synchronize()
+        for k, v in ref.items():
+            if v is not None:
+                assert torch.equal(o[k], v), k

@@ -365,8 +365,11 @@ def test_error_paths(L):
     with pytest.raises(L.LstmssError):
         L.kept_rows(d, 0.5, L.structure(4, 65))     # R > 64
     with pytest.raises(L.LstmssError) as e:
-        L.kept_rows(d, 0.5, L.structure(4, 8, kind=L.FINE))
-    assert e.value.code == -2
+        L.kept_rows(d, 0.5, L.structure(kind=L.FINE, My=16, Mx=0))   # Mx missing
+    assert e.value.code == -1
+    with pytest.raises(L.LstmssError) as e:
+        L.kept_rows(L.dims(2, 512, 4, 8), 0.5, L.structure(kind=L.FINE, My=64, Mx=4))
+    assert e.value.code == -2                           # batch above 256 columns
     x = torch.zeros((2, 4, 4), device=dev())
     W = torch.zeros((32, 12), device=dev())
     _, cache = L.fwd_cache(x, W)
