@@ -55,6 +55,10 @@ def parse():
     ap.add_argument("--serial", action="store_true",
                     help="run the weight/input-gradient work in order on the main stream "
                          "(isolated per-kernel durations) instead of on the side stream")
+    ap.add_argument("--no-fine", action="store_true",
+                    help="skip the fine-grained structure measurement")
+    ap.add_argument("--fine-my", type=int, default=8, help="fine structure: block width My")
+    ap.add_argument("--fine-mx", type=int, default=4, help="fine structure: rows per slice Mx")
     ap.add_argument("--calibration-copy-mib", type=int, default=0,
                     help="first run one device-to-device copy of this many MiB (the known-size "
                          "kernel that scales HBM counter readings)")
@@ -178,6 +182,7 @@ class Runner:
     def __init__(self, L, wl, sparsity, torch):
         from paper_1806_00512_amd.inputs import make_inputs
         self.L, self.wl, self.sparsity, self.torch = L, wl, sparsity, torch
+        self.kw = {"P": wl.P, "R": wl.R}  # sparsifying structure of the sparse steps
         dev = torch.device("cuda:0")
         self.st = torch.bfloat16 if wl.dtype == "bf16" else torch.float32
         self.inp = make_inputs(wl, seed=0)
@@ -196,13 +201,19 @@ class Runner:
         self.sp_bufs = self._buffers(sparsity, dev)
         self.dn_bufs = self._buffers(0.0, dev)
 
+    def set_structure(self, **kw):
+        """Switch the sparse steps to another structure (structure() keywords)."""
+        self.kw = kw
+        self.sp_bufs = None
+        self.sp_bufs = self._buffers(self.sparsity, self.torch.device("cuda:0"))
+
     def _buffers(self, sp, dev):
         L, wl, torch = self.L, self.wl, self.torch
         bufs = []
         for li in range(wl.layers):
             I = wl.layer_input(li)
             d = L.dims(wl.steps, wl.batch, I, wl.hidden, self.st)
-            s = L.structure(wl.P, wl.R) if sp > 0 else None
+            s = L.structure(**self.kw) if sp > 0 else None
             ws = torch.empty(L.workspace_bytes(d, sp, s), dtype=torch.uint8, device=dev)
             out = {"dX": torch.empty((wl.steps, I, wl.batch), device=dev),
                    "dW": torch.empty((4 * wl.hidden, I + wl.hidden), device=dev),
@@ -210,8 +221,8 @@ class Runner:
                    "dh0": torch.empty((wl.hidden, wl.batch), device=dev),
                    "dc0": torch.empty((wl.hidden, wl.batch), device=dev)}
             if sp > 0:
-                kp = L.kept_rows(d, sp, s)
-                out["idx"] = torch.empty((wl.steps, kp // wl.P), dtype=torch.int32, device=dev)
+                ne = L.index_entries(d, sp, s)
+                out["idx"] = torch.empty((wl.steps, ne), dtype=torch.int32, device=dev)
             bufs.append((ws, out))
         return bufs
 
@@ -224,7 +235,7 @@ class Runner:
             if sparse:
                 ws, out = self.sp_bufs[li]
                 o = L.bwd_structsparse(self.xs[li], self.Ws[li], self.caches[li], up,
-                                       sparsity=self.sparsity, P=wl.P, R=wl.R, out=out, ws=ws)
+                                       sparsity=self.sparsity, out=out, ws=ws, **self.kw)
             else:
                 ws, out = self.dn_bufs[li]
                 o = L.bwd_dense(self.xs[li], self.Ws[li], self.caches[li], up, out=out, ws=ws)
@@ -268,7 +279,7 @@ class Runner:
         return e0.elapsed_time(e1) / n, wall / n * 1e3, [v / n for v in per_layer]
 
 
-def measure(L, torch, wl, sparsity, steps, warmup, sparse_only=False, kernels=True):
+def measure(L, torch, wl, sparsity, steps, warmup, sparse_only=False, kernels=True, fine=None):
     r = Runner(L, wl, sparsity, torch)
     res = {"runner": r}
     sp_ms, sp_wall, sp_layer = r.timed([True], steps, warmup)
@@ -297,6 +308,20 @@ def measure(L, torch, wl, sparsity, steps, warmup, sparse_only=False, kernels=Tr
     res["kt"] = L.timing_read()
     L.timing_enable(False)
     L.timing_reset()
+    if fine is not None:
+        # fine-grained structure: My x Mx blocks, K = sparsity * nb per slice
+        r.set_structure(kind=L.FINE, My=fine[0], Mx=fine[1])
+        fn_ms, fn_wall, fn_layer = r.timed([True], steps, warmup)
+        print("%s fine (My=%d, Mx=%d): %.4f ms/step" % (wl.name, fine[0], fine[1], fn_ms),
+              file=sys.stderr, flush=True)
+        L.timing_reset()
+        L.timing_enable(True)
+        for _ in range(steps):
+            r.step(True)
+        torch.cuda.synchronize()
+        res.update(fn_ms=fn_ms, fn_wall=fn_wall, fn_layer=fn_layer, fn_kt=L.timing_read())
+        L.timing_enable(False)
+        L.timing_reset()
     return res
 
 
@@ -331,7 +356,14 @@ def main():
               file=sys.stderr, flush=True)
         del a, b
 
-    m = measure(L, torch, wl, sparsity, args.steps, args.warmup, args.sparse_only)
+    fine = None if args.no_fine else (args.fine_my, args.fine_mx)
+    if fine is not None:
+        nb = -(-wl.batch // fine[0])
+        if abs(sparsity * nb - round(sparsity * nb)) > 1e-6 * nb:
+            print("fine structure skipped: sparsity %g of %d blocks per slice is not a whole "
+                  "number of blocks" % (sparsity, nb), file=sys.stderr, flush=True)
+            fine = None
+    m = measure(L, torch, wl, sparsity, args.steps, args.warmup, args.sparse_only, fine=fine)
     if args.sparse_only:
         return
     sp_ms, dn_ms, kt = m["sp_ms"], m["dn_ms"], m["kt"]
@@ -398,6 +430,20 @@ def main():
         "roofline": roofs[dominant],
         "roofline_all": roofs,
     }
+    if fine is not None:
+        nb = -(-wl.batch // fine[0])
+        fk = {}
+        for name in KINDS + ("aux",):
+            ms, n = m["fn_kt"][name]
+            fk[name] = {"total_ms_per_step": round(ms / args.steps, 5), "launches": n,
+                        "avg_us": round(ms / max(n, 1) * 1e3, 3)}
+        result["fine"] = {"My": fine[0], "Mx": fine[1], "blocks_per_slice": nb,
+                          "K": int(round(sparsity * nb)), "ms_per_step": round(m["fn_ms"], 5),
+                          "speedup_vs_dense": round(dn_ms / m["fn_ms"], 4),
+                          "value": round(dense_flops / (m["fn_ms"] / 1e3) / 1e12, 4),
+                          "unit": "TFLOP/s",
+                          "per_layer_ms": [round(v, 5) for v in m["fn_layer"]],
+                          "kernels": fk}
     if not args.no_cpu_baseline:
         result["cpu_baseline"] = cpu_baseline(wl, m["runner"].inp, sparsity)
     del m

@@ -590,56 +590,54 @@ __global__ __launch_bounds__(64) void cell_select_kernel2(CellArgs a) {
 // Fine-grained structure (section 3, Fig. 2(b)): a slice of P = Mx gate rows
 // is its own region; it is cut into nb blocks of My batch columns (the last
 // block narrower when My does not divide B) and the S = K blocks of lowest
-// squared L2 norm are removed.  A work-group owns FK_ROWS rows (whole
-// slices) over every batch column: a wavefront computes a row at a time
-// (lane l holds columns l, l+64, ...), each My-lane group reduces its block's
-// squares by an xor butterfly (My/2, ..., 1), and one thread per (slice,
-// block) folds the rows in order, ranks the block inside its slice and
-// places it in the per-slice index.  The masked rows (removed blocks zeroed)
-// go to dGc in the full [4H][B] layout; the bias gradient adds each masked
-// row's sum.
+// squared L2 norm are removed.  One wavefront owns one slice over every
+// batch column (lane l holds columns l, l+64, ...): each My-lane group
+// reduces its block's squares row by row with an xor butterfly (My/2, ...,
+// 1) and folds the rows in order, so every lane ends with its block's score
+// in a register.  A block is ranked against the others of its slice through
+// scalar reads of their leader lanes; a ballot of the kept leaders gives the
+// per-slice offset index.  The masked rows (removed blocks zeroed) go to dGc
+// in the full [4H][B] layout; the bias gradient adds each masked row's sum.
+// SRC selects where the gate-gradient values come from: computed from the
+// cache (FS_CACHE), read from the staging matrix the element kernel wrote
+// (FS_STAGE), or a given matrix (FS_GIVEN, selection only).
 // ---------------------------------------------------------------------------
-constexpr int FK_WAVES = 4;
-constexpr int FK_ROWS = 32;
+enum { FS_CACHE = 0, FS_STAGE = 1, FS_GIVEN = 2 };
 
-template <typename TS, int MODE>
-__global__ __launch_bounds__(FK_WAVES * 64) void cell_fine_kernel(CellArgs a) {
-    __shared__ double s_blk[FK_ROWS][64];     // [row][block] row-block sums of squares
-    __shared__ double s_sc[FK_ROWS][64];      // [slice][block] scores (slices <= FK_ROWS)
-    __shared__ unsigned char s_keep[FK_ROWS][64];
-    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-    const int B = a.B, H = a.H, P = a.P, My = a.My, nb = a.nb, K = a.S;
-    const long G = 4L * H;
-    const int ns = FK_ROWS / P;                   // slices per work-group
-    const long s0 = (long)blockIdx.x * ns;        // first slice
-    const long row0 = s0 * P;
-    const int nrows = (int)min((long)FK_ROWS, G - row0);
-    const int nsl = nrows / P;
-    constexpr int NJ = 4;                         // 64-column chunks (B <= 256)
-    constexpr int RPW = FK_ROWS / FK_WAVES;       // rows per wavefront
+__device__ __forceinline__ double readlane_f64(double v, int l) {
+    const long long x = __double_as_longlong(v);
+    const int lo = __builtin_amdgcn_readlane((int)(x & 0xffffffffLL), l);
+    const int hi = __builtin_amdgcn_readlane((int)(x >> 32), l);
+    return __longlong_as_double(((long long)hi << 32) | (unsigned int)lo);
+}
 
+template <typename TS, int SRC, int MX>
+__global__ __launch_bounds__(64) void cell_fine_kernel(CellArgs a) {
+    constexpr int NJ = 4;  // 64-column chunks (B <= 256)
+    const int lane = threadIdx.x;
+    const int B = a.B, H = a.H, My = a.My, nb = a.nb, K = a.S;
+    const long j = blockIdx.x;  // slice
+    const long r0 = j * MX;
     const TS *__restrict__ gates = (const TS *)a.gates;
     const float *__restrict__ dHup = a.dH_up;
     const float *__restrict__ ct = a.c_t;
     const float *__restrict__ cp = a.c_prev;
     const float *__restrict__ dcin = a.dc_in;
+    const TS *__restrict__ src = (const TS *)(SRC == FS_STAGE ? a.stage : a.dG_in);
     TS *dbg = (TS *)a.dbg;
 
-    float vals[RPW][NJ];
+    float vals[MX][NJ];
 #pragma unroll
-    for (int k = 0; k < RPW; ++k) {
-        const int lr = wave + FK_WAVES * k;
-        const bool rin = lr < nrows;
-        const long r = row0 + (rin ? lr : 0);
+    for (int p = 0; p < MX; ++p) {
+        const long r = r0 + p;
         const int g = (int)(r / H), u = (int)(r - (long)g * H);
 #pragma unroll
-        for (int j = 0; j < NJ; ++j) {
-            const int b = 64 * j + lane;
-            const bool in = rin && b < B;
+        for (int jj = 0; jj < NJ; ++jj) {
+            const int b = 64 * jj + lane;
             float val = 0.f;
-            if (in) {
-                if (MODE == CELL_GIVEN) {
-                    val = st<TS>::load((const TS *)a.dG_in, r * B + b);
+            if (b < B) {
+                if (SRC != FS_CACHE) {
+                    val = st<TS>::load(src, r * B + b);
                 } else {
                     const int e = u * B + b;
                     const float dh = sum_parts(dHup[e], a.dh_part + e, a.dh_nparts, a.dh_stride);
@@ -664,76 +662,90 @@ __global__ __launch_bounds__(FK_WAVES * 64) void cell_fine_kernel(CellArgs a) {
                         st<TS>::store(dbg, r * B + b, val);
                 }
             }
-            vals[k][j] = val;
-            // block sums of this chunk: butterfly inside each My-lane group
-            if (64 * j < B) {
-                double q = (double)val * (double)val;
+            vals[p][jj] = val;
+        }
+    }
+
+    // block scores: per row a butterfly inside each My-lane group (columns
+    // past B add zero), rows folded in increasing order
+    double sc[NJ];
+#pragma unroll
+    for (int jj = 0; jj < NJ; ++jj) {
+        sc[jj] = 0.0;
+        if (64 * jj < B) {
+#pragma unroll
+            for (int p = 0; p < MX; ++p) {
+                double q = (double)vals[p][jj] * (double)vals[p][jj];
                 for (int off = My >> 1; off >= 1; off >>= 1)
                     q = q + shfl_xor_f64(q, off);
-                if (rin && (lane & (My - 1)) == 0 && (64 * j + lane) / My < nb)
-                    s_blk[lr][(64 * j + lane) / My] = q;
+                sc[jj] = p == 0 ? q : sc[jj] + q;
             }
         }
     }
-    __syncthreads();
-
-    // one thread per (slice, block): score (rows folded in order)
-    const int pairs = nsl * nb;
-    for (int pi = tid; pi < pairs; pi += FK_WAVES * 64) {
-        const int sl = pi / nb, c = pi - sl * nb;
-        double sc = s_blk[sl * P][c];
-        for (int p = 1; p < P; ++p)
-            sc = sc + s_blk[sl * P + p][c];
-        s_sc[sl][c] = sc;
-        if (a.scores)
-            a.scores[(s0 + sl) * nb + c] = sc;
+    const int bpc = 64 / My;  // blocks starting in one 64-column chunk
+    const bool leader = (lane & (My - 1)) == 0;
+    int cown[NJ];
+    uint64_t kown[NJ];
+#pragma unroll
+    for (int jj = 0; jj < NJ; ++jj) {
+        cown[jj] = jj * bpc + lane / My;
+        kown[jj] = score_key(sc[jj]);
+        if (a.scores && 64 * jj < B && leader && cown[jj] < nb)
+            a.scores[j * nb + cown[jj]] = sc[jj];
     }
-    __syncthreads();
-    // rank inside the slice: keep the blocks outranked by fewer than nb - K
-    for (int pi = tid; pi < pairs; pi += FK_WAVES * 64) {
-        const int sl = pi / nb, c = pi - sl * nb;
-        const uint64_t kc = score_key(s_sc[sl][c]);
-        int beaten = 0;
-        for (int i = 0; i < nb; ++i)
-            if (i != c && outranks(score_key(s_sc[sl][i]), i, kc, c))
-                ++beaten;
-        s_keep[sl][c] = beaten < nb - K ? 1 : 0;
+    // rank: a block is kept when fewer than nb - K blocks of its slice
+    // outrank it (higher score, ties to the lower index, NaN highest)
+    int beaten[NJ] = {};
+#pragma unroll
+    for (int j2 = 0; j2 < NJ; ++j2) {
+        if (64 * j2 >= B)
+            break;
+        const int n2 = min(bpc, nb - j2 * bpc);
+        for (int cb = 0; cb < n2; ++cb) {
+            const int c2 = j2 * bpc + cb;
+            const uint64_t k2 = score_key(readlane_f64(sc[j2], cb * My));
+#pragma unroll
+            for (int jj = 0; jj < NJ; ++jj)
+                if (c2 != cown[jj] && outranks(k2, c2, kown[jj], cown[jj]))
+                    ++beaten[jj];
+        }
     }
-    __syncthreads();
-    // per-slice offset index of the kept blocks (ascending)
-    for (int pi = tid; pi < pairs; pi += FK_WAVES * 64) {
-        const int sl = pi / nb, c = pi - sl * nb;
-        if (s_keep[sl][c]) {
-            int pos = 0;
-            for (int i = 0; i < c; ++i)
-                pos += s_keep[sl][i];
-            a.idx[(s0 + sl) * (nb - K) + pos] = c;
+    bool keep[NJ];
+    int base = 0;
+#pragma unroll
+    for (int jj = 0; jj < NJ; ++jj) {
+        keep[jj] = beaten[jj] < nb - K;
+        if (64 * jj < B) {
+            const bool mine = leader && cown[jj] < nb && keep[jj];
+            const uint64_t m = __ballot(mine);
+            if (mine) {
+                const int pos = base + __popcll(m & ((1ull << lane) - 1ull));
+                a.idx[j * (nb - K) + pos] = cown[jj];
+            }
+            base += __popcll(m);
         }
     }
 
     // masked rows to dGc; bias gradient of the masked rows
     TS *dGc = (TS *)a.dGc;
 #pragma unroll
-    for (int k = 0; k < RPW; ++k) {
-        const int lr = wave + FK_WAVES * k;
-        const bool rin = lr < nrows;
-        const long r = row0 + (rin ? lr : 0);
-        const int sl = (rin ? lr : 0) / P;
+    for (int p = 0; p < MX; ++p) {
+        const long r = r0 + p;
         float rs = 0.f;
 #pragma unroll
-        for (int j = 0; j < NJ; ++j) {
-            const int b = 64 * j + lane;
-            const bool in = rin && b < B;
-            const float m = in && s_keep[sl][b / My] ? vals[k][j] : 0.f;
-            if (in)
+        for (int jj = 0; jj < NJ; ++jj) {
+            const int b = 64 * jj + lane;
+            if (b < B) {
+                const float m = keep[jj] ? vals[p][jj] : 0.f;
                 st<TS>::store(dGc, r * B + b, m);
-            rs += m;
+                rs += m;
+            }
         }
-        if (MODE != CELL_GIVEN && a.db) {
+        if (SRC != FS_GIVEN && a.db) {
 #pragma unroll
             for (int off = 32; off >= 1; off >>= 1)
                 rs += shfl_xor_f32(rs, off);
-            if (rin && lane == 0)
+            if (lane == 0)
                 a.db[r] += rs;
         }
     }
@@ -832,21 +844,48 @@ hipError_t launch_cell_split(const CellArgs &a, int mode, bool bf16, hipStream_t
     return hipGetLastError();
 }
 
-hipError_t launch_cell_fine(const CellArgs &a, int mode, bool bf16, hipStream_t s) {
-    if (a.P < 1 || a.P > FK_ROWS || FK_ROWS % a.P != 0 || a.My < 1 || a.My > 64 ||
-        (a.My & (a.My - 1)) != 0 || a.nb < 1 || a.nb > 64 || a.B > 256 ||
-        (mode != CELL_SPARSE && mode != CELL_GIVEN) || (4L * a.H) % a.P != 0)
-        return hipErrorInvalidValue;
-    const int ns = FK_ROWS / a.P;
-    const dim3 grid((unsigned)ceil_div(4L * a.H / a.P, ns));
-#define LSTMSS_FK(TS, M) hipLaunchKernelGGL((cell_fine_kernel<TS, M>), grid, dim3(FK_WAVES * 64), 0, s, a)
-    if (bf16) {
-        if (mode == CELL_GIVEN) LSTMSS_FK(bf16_t, CELL_GIVEN); else LSTMSS_FK(bf16_t, CELL_SPARSE);
-    } else {
-        if (mode == CELL_GIVEN) LSTMSS_FK(float, CELL_GIVEN); else LSTMSS_FK(float, CELL_SPARSE);
+template <typename TS, int SRC>
+static void launch_fine_src(const CellArgs &a, hipStream_t s) {
+    const dim3 grid((unsigned)(4L * a.H / a.P));
+#define LSTMSS_FK(MX) hipLaunchKernelGGL((cell_fine_kernel<TS, SRC, MX>), grid, dim3(64), 0, s, a)
+    switch (a.P) {
+    case 1: LSTMSS_FK(1); break;
+    case 2: LSTMSS_FK(2); break;
+    case 4: LSTMSS_FK(4); break;
+    case 8: LSTMSS_FK(8); break;
+    default: LSTMSS_FK(16); break;
     }
 #undef LSTMSS_FK
+}
+
+template <typename TS>
+static hipError_t launch_fine_typed(const CellArgs &a, int mode, hipStream_t s) {
+    if (mode == CELL_GIVEN) {
+        launch_fine_src<TS, FS_GIVEN>(a, s);
+    } else if (a.stage && (long)a.H * a.B >= 65536) {
+        // large shapes: the element kernel forms each unit's four gate rows
+        // once (one read of dh and the cache per unit), then the slices are
+        // selected from its staging matrix
+        const int nch = (int)ceil_div(a.B, 64);
+        dim3 ge((unsigned)ceil_div(a.H, EK_UNITS), (unsigned)nch);
+        hipLaunchKernelGGL((cell_elem_kernel<TS, true>), ge, dim3(EK_WAVES * 64), 0, s, a);
+        hipError_t e = hipGetLastError();
+        if (e != hipSuccess)
+            return e;
+        launch_fine_src<TS, FS_STAGE>(a, s);
+    } else {
+        launch_fine_src<TS, FS_CACHE>(a, s);
+    }
     return hipGetLastError();
+}
+
+hipError_t launch_cell_fine(const CellArgs &a, int mode, bool bf16, hipStream_t s) {
+    if ((a.P != 1 && a.P != 2 && a.P != 4 && a.P != 8 && a.P != 16) || a.My < 2 || a.My > 64 ||
+        (a.My & (a.My - 1)) != 0 || a.nb < 1 || a.nb > 64 || a.nb != (a.B + a.My - 1) / a.My ||
+        a.B > 256 || a.S < 0 || a.S >= a.nb || (mode != CELL_SPARSE && mode != CELL_GIVEN) ||
+        (4L * a.H) % a.P != 0)
+        return hipErrorInvalidValue;
+    return bf16 ? launch_fine_typed<bf16_t>(a, mode, s) : launch_fine_typed<float>(a, mode, s);
 }
 
 hipError_t launch_bias_grad(float *db, const float *chunk_rs, int nch, long G, int t0, int t1,

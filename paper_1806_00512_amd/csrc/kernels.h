@@ -110,8 +110,11 @@ struct FwdArgs {
 };
 
 hipError_t launch_cell(const CellArgs &a, int mode, bool bf16, hipStream_t s);
-// Fine-grained structure (mode CELL_SPARSE or CELL_GIVEN): P <= 16, My a
-// power of two <= 64, nb <= 64, B <= 256.
+// Fine-grained structure (mode CELL_SPARSE or CELL_GIVEN): P in {1,2,4,8,16},
+// My a power of two in [2, 64], nb = ceil(B/My) <= 64, B <= 256.  With
+// stage set and H*B >= 65536, CELL_SPARSE runs the element kernel into stage
+// (and chunk_sq, chunk_rs) before the selection; db (when set) accumulates
+// the masked row sums.
 hipError_t launch_cell_fine(const CellArgs &a, int mode, bool bf16, hipStream_t s);
 size_t cell_lds_bytes(const CellArgs &a, int mode);
 // True when launch_cell uses the split (element kernel + select kernel) path;

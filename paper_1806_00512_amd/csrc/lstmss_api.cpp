@@ -450,12 +450,16 @@ int32_t backward_enqueue(const lstmss_dims *d, bool dense, const Plan &p, const 
         ca.db = dbp;
         ca.dbg = dbg ? (char *)dbg + (size_t)t * G * B * es : nullptr;
         ca.scores = nullptr;
-        if (split) {
-            ca.db = nullptr;
+        if (split || fine) {
+            // staging matrix of the element kernel (used by the fine
+            // structure's large-shape path too, which keeps db in its
+            // selection kernel)
             ca.stage = wb + L.stage;
             ca.chunk_sq = (double *)(wb + L.chunk_sq);
             ca.chunk_rs = chunk_rs_all + (size_t)t * G * nch;
         }
+        if (split)
+            ca.db = nullptr;
         ca.My = p.My;
         ca.nb = p.nb;
         if (!split && !fine &&
