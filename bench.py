@@ -189,13 +189,18 @@ class Runner:
         self.Ws = [torch.from_numpy(w).to(dev).to(self.st) for w in self.inp["Ws"]]
         x0 = torch.from_numpy(self.inp["x"]).to(dev).to(self.st)
         self.dH = torch.from_numpy(self.inp["dH_up"]).to(dev)
-        # forward caches (untimed support for the backward pass)
-        self.xs, self.caches = [], []
+        # forward caches (untimed support for the backward pass; the
+        # forward is timed on its own by forward_timed)
+        self.xs, self.caches, self.houts, self.fws = [], [], [], []
         inp_l = x0
         for li in range(wl.layers):
-            h_out, cache = L.fwd_cache(inp_l, self.Ws[li])
+            I = wl.layer_input(li)
+            d = L.dims(wl.steps, wl.batch, I, wl.hidden, self.st)
+            self.fws.append(torch.empty(L.fwd_workspace_bytes(d), dtype=torch.uint8, device=dev))
+            h_out, cache = L.fwd_cache(inp_l, self.Ws[li], ws=self.fws[li])
             self.xs.append(inp_l)
             self.caches.append(cache)
+            self.houts.append(h_out)
             inp_l = h_out
         torch.cuda.synchronize()
         self.sp_bufs = self._buffers(sparsity, dev)
@@ -242,6 +247,27 @@ class Runner:
             if marks is not None:
                 marks[li].record()
             up = o["dX"]
+
+    def forward(self, batched=True):
+        """Forward pass of every layer (bottom first) into the same caches."""
+        for li in range(self.wl.layers):
+            self.L.fwd_cache(self.xs[li], self.Ws[li], h_out=self.houts[li],
+                             cache=self.caches[li], ws=self.fws[li] if batched else None,
+                             batched=batched)
+
+    def forward_timed(self, K, W, batched=True):
+        """Mean ms of one forward pass over all layers (HIP events)."""
+        torch = self.torch
+        for _ in range(W):
+            self.forward(batched)
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        for _ in range(K):
+            self.forward(batched)
+        e1.record()
+        torch.cuda.synchronize()
+        return e0.elapsed_time(e1) / K
 
     def timed(self, schedule, K, W):
         """schedule: one cycle of steps (True = sparse); K cycles timed after
@@ -299,6 +325,11 @@ def measure(L, torch, wl, sparsity, steps, warmup, sparse_only=False, kernels=Tr
     mx_ms, _, _ = r.timed([True] * 9 + [False], cycles, 1)
     print("%s 9:1 schedule: %.4f ms/step" % (wl.name, mx_ms), file=sys.stderr, flush=True)
     res.update(mix_ms=mx_ms, mix_cycles=cycles)
+    # forward pass (batched path, and one pass of the fused per-step path)
+    res["fwd_ms"] = r.forward_timed(steps, 1)
+    res["fwd_fused_ms"] = r.forward_timed(1, 0, batched=False)
+    print("%s forward: %.4f ms (fused per-step kernel %.4f ms)" % (
+        wl.name, res["fwd_ms"], res["fwd_fused_ms"]), file=sys.stderr, flush=True)
     # per-kernel HIP-event timing pass (same number of sparse steps)
     L.timing_reset()
     L.timing_enable(True)
@@ -430,6 +461,13 @@ def main():
         "roofline": roofs[dominant],
         "roofline_all": roofs,
     }
+    fwd_flops = sum(8.0 * wl.hidden * wl.batch * (wl.layer_input(l) + wl.hidden) * wl.steps
+                    for l in range(wl.layers))
+    result["forward"] = {"ms_per_step": round(m["fwd_ms"], 5),
+                         "tflops": round(fwd_flops / (m["fwd_ms"] / 1e3) / 1e12, 4),
+                         "fused_per_step_kernel_ms": round(m["fwd_fused_ms"], 5),
+                         "note": "forward of every layer over all steps (fills the backward "
+                                 "cache); flops 8*H*B*(I+H)*T per layer"}
     if fine is not None:
         nb = -(-wl.batch // fine[0])
         fk = {}

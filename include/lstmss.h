@@ -104,6 +104,11 @@ int64_t lstmss_index_entries(const lstmss_dims *d, float sparsity, const lstmss_
  * (sparsity 0 gives the size for lstm_bwd_dense).  <0 on error. */
 int64_t lstmss_workspace_bytes(const lstmss_dims *d, float sparsity, const lstmss_structure *s);
 
+/* Workspace bytes for lstm_fwd_cache's batched path: the fp32 input
+ * projection of every step plus one step's recurrent split-K partials.
+ * <0 on error. */
+int64_t lstmss_fwd_workspace_bytes(const lstmss_dims *d);
+
 /* Forward pass of one LSTM layer, keeping what the backward pass reads
  * (the paper's forward computes the gate activations, section 4).
  *   a_t = W [x_t; h_{t-1}] + b;  i, f, o = sigmoid, g = tanh of a_t's blocks;
@@ -111,10 +116,16 @@ int64_t lstmss_workspace_bytes(const lstmss_dims *d, float sparsity, const lstms
  *   x      [T][I][B] dtype            W [4H][I+H] dtype
  *   b      [4H] fp32, NULL = 0        h0, c0 [H][B] fp32, NULL = 0
  *   h_out  [T][H][B] dtype (h_1..h_T), may be NULL
- *   cache  lstmss_cache_bytes(d) bytes, written. */
+ *   cache  lstmss_cache_bytes(d) bytes, written
+ *   ws     lstmss_fwd_workspace_bytes(d) bytes: the input projection W_x x_t
+ *          of all steps runs as one product, then every step runs its
+ *          recurrent product W_h h_{t-1} split over k and a cell-update
+ *          kernel; NULL: one fused product + cell-update kernel per step,
+ *          no scratch (slower on large layers).  Both give the same values
+ *          up to fp32 summation order. */
 int32_t lstm_fwd_cache(const lstmss_dims *d, const void *x, const void *W, const float *b,
-                       const float *h0, const float *c0, void *h_out, void *cache,
-                       void *stream);
+                       const float *h0, const float *c0, void *h_out, void *cache, void *ws,
+                       size_t ws_bytes, void *stream);
 
 /* Dense backward pass through time of one layer (the paper's baseline, every
  * gate-gradient row kept).  Loss convention: dH_up[t] = dL/dh_t from above,

@@ -113,8 +113,12 @@ struct G1Shape {
     static_assert(GEMM1_TK % TK == 0 && GEMM1_KC_MAX % TK == 0, "stage must divide the split granularity");
 };
 
-template <typename TS, int TM, int TN, bool GATHER, bool VEC>
+// ROWA: the forward products a = W[:, kcol0 : kcol0 + Kp] G instead, whose
+// first operand arrives row-major with k contiguous: a thread stages KB rows
+// x VW consecutive k and stores each row's vector as it is.
+template <typename TS, int TM, int TN, bool GATHER, bool VEC, bool ROWA = false>
 __global__ __launch_bounds__(THREADS) void gemm1_kernel(Gemm1Args a) {
+    static_assert(!(ROWA && GATHER), "the forward products read every row");
     using SH = G1Shape<TS, TM, TN>;
     constexpr bool BF = SH::BF;
     constexpr int TK = SH::TK, KB = SH::KB, MT = SH::MT, NT = SH::NT, WM = SH::WM, LDK = SH::LDK;
@@ -153,7 +157,8 @@ __global__ __launch_bounds__(THREADS) void gemm1_kernel(Gemm1Args a) {
             srow[i] = GATHER ? idx[k / a.P] * a.P + k % a.P : k;
         }
     };
-    fill_rows(sc);
+    if (!ROWA)
+        fill_rows(sc);
 
     auto qa = [&](int i) { return tid + i * THREADS; };
     auto qb = [&](int i) { return SPLIT ? tid - NA : tid + i * THREADS; };
@@ -162,6 +167,20 @@ __global__ __launch_bounds__(THREADS) void gemm1_kernel(Gemm1Args a) {
 #pragma unroll
         for (int i = 0; i < RA; ++i) {
             const int q = qa(i);
+            if constexpr (ROWA) {
+                // KB rows m x VW consecutive k; kcol0 and ldw are multiples
+                // of VW when VEC, so a vector never crosses a row or ke
+                const int k = k0 + (q % (TK / VW)) * VW;
+                const int m = mm0 + (q / (TK / VW)) * KB;
+#pragma unroll
+                for (int r = 0; r < KB; ++r) {
+                    if (q < NA && m + r < M && k < ke)
+                        ra[i][r].load(W + (long)(m + r) * ldw + a.kcol0 + k, ke - k);
+                    else
+                        ra[i][r].zero();
+                }
+                continue;
+            }
             const int kg = k0 + (q % (TK / KB)) * KB;
             const int m = a.m_lo + mm0 + (q / (TK / KB)) * VW;
             // a vector load never crosses the end of a W row: ldw is a
@@ -211,7 +230,25 @@ __global__ __launch_bounds__(THREADS) void gemm1_kernel(Gemm1Args a) {
 #pragma unroll
         for (int i = 0; i < RA; ++i) {
             const int q = qa(i);
-            if (q < NA) {
+            if (ROWA && q < NA) {
+                const int kk = (q % (TK / VW)) * VW, mm = (q / (TK / VW)) * KB;
+#pragma unroll
+                for (int r = 0; r < KB; ++r) {
+                    E *dst = &As[buf][mm + r][kk];
+                    if constexpr (VW == 1) {
+                        *dst = ra[i][r].v[0];
+                    } else if constexpr (BF) {
+                        u16x8 t;
+#pragma unroll
+                        for (int e = 0; e < 8; ++e)
+                            t[e] = ra[i][r].v[e];
+                        *(u16x8 *)dst = t;
+                    } else {
+                        *(float4 *)dst = make_float4(ra[i][r].v[0], ra[i][r].v[1], ra[i][r].v[2],
+                                                     ra[i][r].v[3]);
+                    }
+                }
+            } else if (q < NA) {
                 const int kk = (q % (TK / KB)) * KB, mm = (q / (TK / KB)) * VW;
 #pragma unroll
                 for (int e = 0; e < VW; ++e)
@@ -248,7 +285,7 @@ __global__ __launch_bounds__(THREADS) void gemm1_kernel(Gemm1Args a) {
     for (int k0 = kb; k0 < ke; k0 += TK) {
         const bool next = k0 + TK < ke;
         if (next) {
-            if (k0 + TK == sc + GEMM1_KC_MAX) {  // next super-chunk of rows
+            if (!ROWA && k0 + TK == sc + GEMM1_KC_MAX) {  // next super-chunk of rows
                 sc = k0 + TK;
                 fill_rows(sc);
                 __syncthreads();
@@ -861,7 +898,54 @@ __global__ __launch_bounds__(THREADS) void fwd_step_kernel(FwdArgs a) {
     }
 }
 
+// Forward cell update of one step from the pre-activation pieces:
+// a = zx + b + sum_s part[s] (input projection, bias, recurrent split-K
+// partials); i, f, o = sigmoid, g = tanh; c = f c_prev + i g; h = o tanh(c).
+// One thread per (unit, column); the stored gates and h are rounded to the
+// storage type, c stays fp32 and is formed from the unrounded gates.
+template <typename TS>
+__global__ __launch_bounds__(256) void fwd_act_kernel(FwdActArgs a) {
+    const long e = blockIdx.x * 256L + threadIdx.x;
+    const long HB = (long)a.H * a.B;
+    if (e >= HB)
+        return;
+    const int u = (int)(e / a.B), n = (int)(e - (long)u * a.B);
+    float z[4];
+#pragma unroll
+    for (int g = 0; g < 4; ++g) {
+        const long r = (long)g * a.H + u;
+        float v = a.zx[r * a.B + n] + (a.bias ? a.bias[r] : 0.f);
+        for (int sp = 0; sp < a.nparts; ++sp)
+            v += a.part[sp * a.part_stride + r * a.B + n];
+        z[g] = v;
+    }
+    const float ig = sigmoidf_(z[0]), fg = sigmoidf_(z[1]), gg = tanhf(z[2]), og = sigmoidf_(z[3]);
+    const float cv = fg * a.cp[e] + ig * gg;
+    const float hv = og * tanhf(cv);
+    a.cn[e] = cv;
+    st<TS>::store((TS *)a.hn, e, hv);
+    if (a.hout)
+        st<TS>::store((TS *)a.hout, e, hv);
+    TS *gates = (TS *)a.gates;
+    st<TS>::store(gates, (long)(0 * a.H + u) * a.B + n, ig);
+    st<TS>::store(gates, (long)(1 * a.H + u) * a.B + n, fg);
+    st<TS>::store(gates, (long)(2 * a.H + u) * a.B + n, gg);
+    st<TS>::store(gates, (long)(3 * a.H + u) * a.B + n, og);
+}
+
 } // namespace
+
+hipError_t launch_fwd_act(const FwdActArgs &a, bool bf16, hipStream_t s) {
+    const long HB = (long)a.H * a.B;
+    if (HB <= 0)
+        return hipSuccess;
+    const dim3 grid((unsigned)ceil_div(HB, 256L));
+    if (bf16)
+        hipLaunchKernelGGL(fwd_act_kernel<bf16_t>, grid, dim3(256), 0, s, a);
+    else
+        hipLaunchKernelGGL(fwd_act_kernel<float>, grid, dim3(256), 0, s, a);
+    return hipGetLastError();
+}
 
 // Tile of the data-gradient GEMM.  Its operands stream from L2 / MALL, so
 // occupancy matters as much as operand reuse: fp32 runs 128 x 128 tiles
@@ -922,6 +1006,35 @@ hipError_t launch_gemm1(Gemm1Args a, bool bf16, hipStream_t s) {
 #undef LSTMSS_G1T
 #undef LSTMSS_G1V
 #undef LSTMSS_G1
+    return hipGetLastError();
+}
+
+hipError_t launch_gemm_fwd(Gemm1Args a, bool bf16, hipStream_t s) {
+    if (a.k_chunk % GEMM1_TK != 0 || a.splitk < 1 || a.steps < 1 || a.idx || a.m_begin != 0)
+        return hipErrorInvalidValue;
+    const int vw = bf16 ? 8 : 4;
+    const bool vec = a.ldw % vw == 0 && a.kcol0 % vw == 0 && a.N % vw == 0;
+    a.m_lo = 0;
+    const long z = (long)a.splitk * a.steps;
+    int TM, TN;
+    gemm1_tile(bf16, a.N, a.M, z, &TM, &TN);
+    if (a.tm)
+        TM = a.tm;
+    if (a.tn)
+        TN = a.tn;
+    if (!((TN == 32 && TM == 128) || ((TN == 64 || TN == 128) && (TM == 64 || TM == 128))))
+        return hipErrorInvalidValue;
+    dim3 grid((unsigned)ceil_div(a.M, TM), (unsigned)ceil_div(a.N, TN), (unsigned)z);
+#define LSTMSS_GF(TS, TMV, TNV, VE) hipLaunchKernelGGL((gemm1_kernel<TS, TMV, TNV, false, VE, true>), grid, dim3(THREADS), 0, s, a)
+#define LSTMSS_GFV(TS, TMV, TNV) do { if (vec) LSTMSS_GF(TS, TMV, TNV, true); else LSTMSS_GF(TS, TMV, TNV, false); } while (0)
+#define LSTMSS_GFT(TS) do { \
+        if (TN == 32) LSTMSS_GFV(TS, 128, 32); \
+        else if (TN == 64) { if (TM == 128) LSTMSS_GFV(TS, 128, 64); else LSTMSS_GFV(TS, 64, 64); } \
+        else { if (TM == 128) LSTMSS_GFV(TS, 128, 128); else LSTMSS_GFV(TS, 64, 128); } } while (0)
+    if (bf16) LSTMSS_GFT(bf16_t); else LSTMSS_GFT(float);
+#undef LSTMSS_GFT
+#undef LSTMSS_GFV
+#undef LSTMSS_GF
     return hipGetLastError();
 }
 

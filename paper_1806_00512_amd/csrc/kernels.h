@@ -63,6 +63,7 @@ struct Gemm1Args {
     int steps;
     long gc_step, idx_step, out_step;
     int tm, tn;            // tile rows / columns, 0 = chosen by the launcher
+    int kcol0;             // launch_gemm_fwd only: first W column of the product
 };
 
 // Weight gradient dW[rows] += dG_c [x_t; h_{t-1}]^T (rows scattered by idx).
@@ -96,6 +97,21 @@ struct WgradArgs {
 };
 
 // One forward step: a = W [x_t; h_{t-1}] + b, activations, cell update.
+// Forward cell update from the pre-activation pieces of one step.
+struct FwdActArgs {
+    const float *zx;       // [4H][B] input projection W_x x_t
+    const float *part;     // [nparts][4H][B] recurrent partials W_h h_{t-1}
+    int nparts;
+    long part_stride;      // 4H * B
+    const float *bias;     // [4H] or NULL
+    const float *cp;       // [H][B] c_{t-1}
+    int H, B;
+    void *gates;           // [4H][B] activated gates (storage type)
+    float *cn;             // [H][B] c_t
+    void *hn;              // [H][B] h_t (storage type)
+    void *hout;            // [H][B] or NULL
+};
+
 struct FwdArgs {
     const void *W;
     const float *bias;     // [4H] or NULL
@@ -125,6 +141,10 @@ hipError_t launch_bias_grad(float *db, const float *chunk_rs, int nch, long G, i
                             hipStream_t s);
 hipError_t launch_gemm1(Gemm1Args a, bool bf16, hipStream_t s);
 hipError_t launch_gemm2(const Gemm2Args &a, bool bf16, hipStream_t s);
+// Forward products part[z][m][n] = sum over k in split z of
+// W[m][kcol0 + k] G[k][n] (rows m in [0, M), contraction length Kp).
+hipError_t launch_gemm_fwd(Gemm1Args a, bool bf16, hipStream_t s);
+hipError_t launch_fwd_act(const FwdActArgs &a, bool bf16, hipStream_t s);
 // Returns hipErrorNotSupported when the structure needs more routing tiles
 // than the batched kernel holds (the caller then uses launch_gemm2 per step).
 hipError_t launch_wgrad(WgradArgs a, bool sparse, bool bf16, hipStream_t s);

@@ -665,36 +665,106 @@ int64_t lstmss_workspace_bytes(const lstmss_dims *d, float sparsity, const lstms
     return (int64_t)ws_layout(d, p).total;
 }
 
+// Forward workspace: the input projection of every step and the split-K
+// partials of one step's recurrent product (both fp32).
+struct FwdPlan {
+    int splitk, tm, tn;
+    long k_chunk;
+    size_t zx, part, total;
+};
+
+FwdPlan fwd_plan(const lstmss_dims *d) {
+    FwdPlan f;
+    const bool bf16 = d->dtype == LSTMSS_BF16;
+    const long G = 4L * d->H;
+    gemm1_tile(bf16, d->B, G, 1, &f.tm, &f.tn);
+    // enough work-groups for about three per CU in the recurrent product,
+    // each split at least two 64-row stages long
+    const long tiles = ceil_div(G, f.tm) * ceil_div(d->B, f.tn);
+    const long want = ceil_div(768L, tiles);
+    const long most = std::max(1L, (long)d->H / 128);
+    long sk = std::max(1L, std::min(want, most));
+    f.k_chunk = ceil_div(ceil_div((long)d->H, sk), GEMM1_TK) * GEMM1_TK;
+    f.splitk = (int)ceil_div((long)d->H, f.k_chunk);
+    const size_t GB = (size_t)G * d->B;
+    f.zx = 0;
+    f.part = align256((size_t)d->T * GB * 4);
+    f.total = f.part + align256((size_t)f.splitk * GB * 4);
+    return f;
+}
+
+int64_t lstmss_fwd_workspace_bytes(const lstmss_dims *d) {
+    int32_t rc = check_dims(d);
+    if (rc)
+        return rc;
+    return (int64_t)fwd_plan(d).total;
+}
+
 int32_t lstm_fwd_cache(const lstmss_dims *d, const void *x, const void *W, const float *b,
-                       const float *h0, const float *c0, void *h_out, void *cache,
-                       void *stream) {
+                       const float *h0, const float *c0, void *h_out, void *cache, void *ws,
+                       size_t ws_bytes, void *stream) {
     int32_t rc = check_dims(d);
     if (rc)
         return rc;
     if (!x || !W || !cache)
         return fail(LSTMSS_ERR_INVALID_ARG, "a required pointer is NULL");
+    const FwdPlan F = fwd_plan(d);
+    if (ws && ws_bytes < F.total)
+        return fail(LSTMSS_ERR_WORKSPACE, "workspace of %zu bytes, need %zu", ws_bytes, F.total);
     hipStream_t st = (hipStream_t)stream;
     const bool bf16 = d->dtype == LSTMSS_BF16;
     const size_t es = elem_bytes(d->dtype);
-    const long HB = (long)d->H * d->B, G = 4L * d->H;
+    const long HB = (long)d->H * d->B, G = 4L * d->H, K = (long)d->I + d->H;
     const CacheLayout C = cache_layout(d);
     char *cb = (char *)cache;
     float *cst = (float *)(cb + C.c);
     char *hst = cb + C.h;
     HIP_TRY(launch_copy_in(cst, c0, HB, st));
     HIP_TRY(launch_h0_store(hst, h0, HB, bf16, st));
+    if (!ws) {
+        // no scratch: one fused product + cell-update kernel per step
+        for (int t = 0; t < d->T; ++t) {
+            FwdArgs f{};
+            f.W = W; f.bias = b;
+            f.xt = (const char *)x + (size_t)t * d->I * d->B * es;
+            f.hp = hst + (size_t)t * HB * es;
+            f.cp = cst + (size_t)t * HB;
+            f.I = d->I; f.H = d->H; f.B = d->B;
+            f.gates = cb + C.gates + (size_t)t * G * d->B * es;
+            f.cn = cst + (size_t)(t + 1) * HB;
+            f.hn = hst + (size_t)(t + 1) * HB * es;
+            f.hout = h_out ? (char *)h_out + (size_t)t * HB * es : nullptr;
+            HIP_TRY(timed(LSTMSS_KERNEL_FORWARD, st, [&] { return launch_fwd_step(f, bf16, st); }));
+        }
+        return LSTMSS_OK;
+    }
+    char *wb = (char *)ws;
+    float *zx = (float *)(wb + F.zx);
+    float *part = (float *)(wb + F.part);
+    // input projection W_x x_t of every step in one launch (steps batched)
+    Gemm1Args gi{};
+    gi.W = W; gi.ldw = K; gi.kcol0 = 0; gi.Gc = x; gi.Kp = d->I; gi.M = (int)G; gi.m_begin = 0;
+    gi.N = d->B; gi.out_row0 = 0; gi.part = zx; gi.part_stride = 0; gi.splitk = 1;
+    gi.k_chunk = ceil_div((long)d->I, GEMM1_TK) * GEMM1_TK; gi.steps = d->T;
+    gi.gc_step = (long)d->I * d->B; gi.out_step = G * d->B;
+    HIP_TRY(timed(LSTMSS_KERNEL_FORWARD, st, [&] { return launch_gemm_fwd(gi, bf16, st); }));
     for (int t = 0; t < d->T; ++t) {
-        FwdArgs f{};
-        f.W = W; f.bias = b;
-        f.xt = (const char *)x + (size_t)t * d->I * d->B * es;
-        f.hp = hst + (size_t)t * HB * es;
-        f.cp = cst + (size_t)t * HB;
-        f.I = d->I; f.H = d->H; f.B = d->B;
-        f.gates = cb + C.gates + (size_t)t * G * d->B * es;
-        f.cn = cst + (size_t)(t + 1) * HB;
-        f.hn = hst + (size_t)(t + 1) * HB * es;
-        f.hout = h_out ? (char *)h_out + (size_t)t * HB * es : nullptr;
-        HIP_TRY(timed(LSTMSS_KERNEL_FORWARD, st, [&] { return launch_fwd_step(f, bf16, st); }));
+        // recurrent product W_h h_{t-1}, split over k
+        Gemm1Args gr{};
+        gr.W = W; gr.ldw = K; gr.kcol0 = d->I; gr.Gc = hst + (size_t)t * HB * es; gr.Kp = d->H;
+        gr.M = (int)G; gr.m_begin = 0; gr.N = d->B; gr.out_row0 = 0; gr.part = part;
+        gr.part_stride = G * d->B; gr.splitk = F.splitk; gr.k_chunk = F.k_chunk; gr.steps = 1;
+        gr.tm = F.tm; gr.tn = F.tn;
+        HIP_TRY(timed(LSTMSS_KERNEL_FORWARD, st, [&] { return launch_gemm_fwd(gr, bf16, st); }));
+        FwdActArgs fa{};
+        fa.zx = zx + (size_t)t * G * d->B;
+        fa.part = part; fa.nparts = F.splitk; fa.part_stride = G * d->B;
+        fa.bias = b; fa.cp = cst + (size_t)t * HB; fa.H = d->H; fa.B = d->B;
+        fa.gates = cb + C.gates + (size_t)t * G * d->B * es;
+        fa.cn = cst + (size_t)(t + 1) * HB;
+        fa.hn = hst + (size_t)(t + 1) * HB * es;
+        fa.hout = h_out ? (char *)h_out + (size_t)t * HB * es : nullptr;
+        HIP_TRY(timed(LSTMSS_KERNEL_FORWARD, st, [&] { return launch_fwd_act(fa, bf16, st); }));
     }
     return LSTMSS_OK;
 }

@@ -31,6 +31,7 @@ ERR = {0: "ok", -1: "invalid argument", -2: "unsupported", -3: "workspace too sm
 # Exported symbols of include/lstmss.h
 SYMBOLS = ("lstmss_version", "lstmss_strerror", "lstmss_last_error", "lstmss_cache_bytes",
            "lstmss_kept_rows", "lstmss_index_entries", "lstmss_workspace_bytes",
+           "lstmss_fwd_workspace_bytes",
            "lstm_fwd_cache", "lstm_bwd_dense",
            "lstm_bwd_structsparse", "lstmss_select_compact", "lstmss_set_option",
            "lstmss_timing_enable", "lstmss_timing_read", "lstmss_timing_reset")
@@ -79,7 +80,9 @@ def load():
     lib.lstmss_index_entries.restype = i64
     lib.lstmss_workspace_bytes.argtypes = [pd, f, ps]
     lib.lstmss_workspace_bytes.restype = i64
-    lib.lstm_fwd_cache.argtypes = [pd, vp, vp, vp, vp, vp, vp, vp, vp]
+    lib.lstmss_fwd_workspace_bytes.argtypes = [pd]
+    lib.lstmss_fwd_workspace_bytes.restype = i64
+    lib.lstm_fwd_cache.argtypes = [pd, vp, vp, vp, vp, vp, vp, vp, vp, ctypes.c_size_t, vp]
     lib.lstm_fwd_cache.restype = i32
     lib.lstm_bwd_dense.argtypes = [pd, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp,
                                    ctypes.c_size_t, vp]
@@ -174,8 +177,19 @@ def workspace_bytes(d: Dims, sparsity: float = 0.0, s: Structure | None = None) 
     return int(n)
 
 
-def fwd_cache(x, W, b=None, h0=None, c0=None, h_out=None, cache=None, stream=None):
-    """x [T][I][B], W [4H][I+H] (fp32 or bf16) -> (h_out [T][H][B], cache bytes)."""
+def fwd_workspace_bytes(d: Dims) -> int:
+    n = load().lstmss_fwd_workspace_bytes(ctypes.byref(d))
+    _check(0 if n >= 0 else int(n), "lstmss_fwd_workspace_bytes")
+    return int(n)
+
+
+def fwd_cache(x, W, b=None, h0=None, c0=None, h_out=None, cache=None, stream=None, ws=None,
+              batched=True):
+    """x [T][I][B], W [4H][I+H] (fp32 or bf16) -> (h_out [T][H][B], cache bytes).
+
+    batched: the input projection of all steps as one product plus split
+    recurrent products (needs a workspace, allocated here unless ws is
+    given); False: the fused per-step kernel without scratch."""
     T, I, B = x.shape
     H = W.shape[0] // 4
     st = x.dtype
@@ -184,13 +198,19 @@ def fwd_cache(x, W, b=None, h0=None, c0=None, h_out=None, cache=None, stream=Non
         cache = torch.empty(cache_bytes(d), dtype=torch.uint8, device=x.device)
     if h_out is None:
         h_out = torch.empty((T, H, B), dtype=st, device=x.device)
+    if batched and ws is None:
+        ws = torch.empty(fwd_workspace_bytes(d), dtype=torch.uint8, device=x.device)
+    if not batched:
+        ws = None
     rc = load().lstm_fwd_cache(ctypes.byref(d), _ptr(x, st, name="x"),
                                _ptr(W, st, (4 * H, I + H), "W"),
                                _ptr(b, torch.float32, (4 * H,), "b"),
                                _ptr(h0, torch.float32, (H, B), "h0"),
                                _ptr(c0, torch.float32, (H, B), "c0"),
                                _ptr(h_out, st, (T, H, B), "h_out"),
-                               _ptr(cache, torch.uint8, name="cache"), _stream(stream))
+                               _ptr(cache, torch.uint8, name="cache"),
+                               _ptr(ws, torch.uint8, name="ws"), 0 if ws is None else ws.numel(),
+                               _stream(stream))
     _check(rc, "lstm_fwd_cache")
     return h_out, cache
 

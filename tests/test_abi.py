@@ -125,7 +125,8 @@ def test_coarse_index_entries(L):
 def test_null_pointers_rejected_before_launch(L):
     lib = L.load()
     d = L.dims(2, 4, 4, 8)
-    rc = lib.lstm_fwd_cache(ctypes.byref(d), None, None, None, None, None, None, None, None)
+    rc = lib.lstm_fwd_cache(ctypes.byref(d), None, None, None, None, None, None, None, None, 0,
+                            None)
     assert rc == -1
     s = L.structure(4, 8)
     rc = lib.lstm_bwd_structsparse(ctypes.byref(d), 0.5, ctypes.byref(s), *([None] * 14), 0, None)
