@@ -25,6 +25,11 @@ Function map (section / table of the paper each one follows):
   backward_fine  back-propagation with the fine-grained structure
   round_bf16     round-to-nearest-even to bfloat16 (storage type of the bf16
                  configuration; not from the paper)
+  mse_grad       synthetic regression loss on the top layer's hidden states
+                 and its gradient (stands in for the datasets' losses)
+  sgd            one SGD update with a fixed learning rate (section 4)
+  train_step     forward, loss, backward (sparsified or dense), SGD of a layer
+                 stack: one step of dense-after-sparse training (section 5)
 """
 from __future__ import annotations
 
@@ -305,3 +310,39 @@ def stack_backward(caches, dH_up, P=4, R=8, S=4, bf16=False, forced_keeps=None, 
         outs[li] = o
         up = o["dX"]
     return outs
+
+
+def mse_grad(h, y):
+    """L = (1 / 2B) * sum of (h - y)^2 over [T][H][B] and dL/dh = (h - y) / B.
+
+    A synthetic loss on the top layer's hidden states: the paper's losses come
+    from datasets that are not used here; any differentiable loss exercises
+    the same backward pass."""
+    h, y = _f64(h), _f64(y)
+    B = h.shape[-1]
+    dif = h - y
+    return dif / B, 0.5 * float(np.sum(dif * dif)) / B
+
+
+def sgd(W, dW, lr, bf16=False):
+    """W - lr * dW (section 4: plain SGD with a fixed learning rate), rounded to
+    bfloat16 when the weights are stored in it."""
+    out = _f64(W) - float(lr) * _f64(dW)
+    return round_bf16(out) if bf16 else out
+
+
+def train_step(x, y, Ws, bs, lr, sparse, P=4, R=8, S=4, bf16=False, forced_keeps=None):
+    """One training step of a layer stack (zero initial state): forward, loss
+    gradient at the top, backward through every layer top first (coarse
+    sparsifying when ``sparse``, else dense), SGD on every W and b.
+
+    Returns (new Ws, new bs, loss, per-layer backward outputs)."""
+    caches = stack_forward(x, Ws, bs, bf16=bf16)
+    dH, loss = mse_grad(caches[-1]["h"][1:], y)
+    if sparse:
+        outs = stack_backward(caches, dH, P=P, R=R, S=S, bf16=bf16, forced_keeps=forced_keeps)
+    else:
+        outs = stack_backward(caches, dH, P=4, R=8, S=0, bf16=bf16)
+    new_W = [sgd(W, o["dW"], lr, bf16) for W, o in zip(Ws, outs)]
+    new_b = [sgd(b, o["db"], lr) for b, o in zip(bs, outs)]
+    return new_W, new_b, loss, outs
