@@ -55,6 +55,8 @@ def parse():
     ap.add_argument("--serial", action="store_true",
                     help="run the weight/input-gradient work in order on the main stream "
                          "(isolated per-kernel durations) instead of on the side stream")
+    ap.add_argument("--no-train", action="store_true",
+                    help="skip the whole-training-step measurement")
     ap.add_argument("--no-fine", action="store_true",
                     help="skip the fine-grained structure measurement")
     ap.add_argument("--fine-my", type=int, default=8, help="fine structure: block width My")
@@ -325,6 +327,11 @@ def measure(L, torch, wl, sparsity, steps, warmup, sparse_only=False, kernels=Tr
     mx_ms, _, _ = r.timed([True] * 9 + [False], cycles, 1)
     print("%s 9:1 schedule: %.4f ms/step" % (wl.name, mx_ms), file=sys.stderr, flush=True)
     res.update(mix_ms=mx_ms, mix_cycles=cycles)
+    # the 3 sparse : 1 dense schedule of dense-after-sparse training
+    c3 = max(1, steps // 4)
+    m3_ms, _, _ = r.timed([True] * 3 + [False], c3, 1)
+    print("%s 3:1 schedule: %.4f ms/step" % (wl.name, m3_ms), file=sys.stderr, flush=True)
+    res.update(mix3_ms=m3_ms, mix3_cycles=c3)
     # forward pass (batched path, and one pass of the fused per-step path)
     res["fwd_ms"] = r.forward_timed(steps, 1)
     res["fwd_fused_ms"] = r.forward_timed(1, 0, batched=False)
@@ -353,6 +360,46 @@ def measure(L, torch, wl, sparsity, steps, warmup, sparse_only=False, kernels=Tr
         res.update(fn_ms=fn_ms, fn_wall=fn_wall, fn_layer=fn_layer, fn_kt=L.timing_read())
         L.timing_enable(False)
         L.timing_reset()
+    return res
+
+
+def measure_training(L, torch, wl, sparsity, steps):
+    """Whole training steps (forward, loss gradient, backward of every layer,
+    SGD) with the dense-after-sparse trainer: all sparse, all dense, and the
+    3 sparse : 1 dense schedule.  Returns mean ms per step of each."""
+    from paper_1806_00512_amd.inputs import make_inputs, make_target
+    from paper_1806_00512_amd.train import StackConfig, StackTrainer, dense_after_sparse
+    dev = torch.device("cuda:0")
+    st = torch.bfloat16 if wl.dtype == "bf16" else torch.float32
+    inp = make_inputs(wl, seed=0)
+    cfg = StackConfig(layers=wl.layers, input_size=wl.input_size, hidden=wl.hidden,
+                      batch=wl.batch, steps=wl.steps, dtype=st, lr=1e-3, sparsity=sparsity,
+                      P=wl.P, R=wl.R)
+    tr = StackTrainer(cfg, [torch.from_numpy(w).to(dev).to(st) for w in inp["Ws"]],
+                      [torch.from_numpy(b).to(dev) for b in inp["bs"]])
+    x = torch.from_numpy(inp["x"]).to(dev).to(st)
+    y = torch.from_numpy(make_target(wl)).to(dev)
+    del inp
+    tr.step(x, y, True)
+    tr.step(x, y, False)
+    torch.cuda.synchronize()
+
+    def run(schedule):
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        for sp in schedule:
+            tr.step(x, y, sp)
+        e1.record()
+        torch.cuda.synchronize()
+        return e0.elapsed_time(e1) / len(schedule)
+
+    n = max(4, (steps + 3) // 4 * 4)
+    res = {"sparse": run([True] * n), "dense": run([False] * n),
+           "dense_after_sparse_3to1": run(dense_after_sparse(n, 0.75)), "steps": n}
+    print("%s training step: sparse %.3f ms, dense %.3f ms, 3:1 %.3f ms" % (
+        wl.name, res["sparse"], res["dense"], res["dense_after_sparse_3to1"]), file=sys.stderr,
+        flush=True)
+    del tr
     return res
 
 
@@ -456,6 +503,9 @@ def main():
                          "dense": [round(v, 5) for v in m["dn_layer"]]},
         "mixed_9sparse_1dense": {"ms_per_step": round(m["mix_ms"], 5), "cycles": m["mix_cycles"],
                                  "formula_ms": round((9 * sp_ms + dn_ms) / 10, 5)},
+        "mixed_3sparse_1dense": {"ms_per_step": round(m["mix3_ms"], 5),
+                                 "cycles": m["mix3_cycles"],
+                                 "speedup_vs_dense": round(dn_ms / m["mix3_ms"], 4)},
         "wall_ms_per_step": {"sparse": round(m["sp_wall"], 5), "dense": round(m["dn_wall"], 5)},
         "kernels": kernels,
         "roofline": roofs[dominant],
@@ -468,6 +518,18 @@ def main():
                          "fused_per_step_kernel_ms": round(m["fwd_fused_ms"], 5),
                          "note": "forward of every layer over all steps (fills the backward "
                                  "cache); flops 8*H*B*(I+H)*T per layer"}
+    if not args.no_train:
+        tm = measure_training(L, torch, wl, sparsity, args.steps)
+        result["training"] = {
+            "ms_per_step": {k: round(tm[k], 5) for k in ("sparse", "dense",
+                                                          "dense_after_sparse_3to1")},
+            "speedup_vs_dense": {"sparse": round(tm["dense"] / tm["sparse"], 4),
+                                 "dense_after_sparse_3to1":
+                                     round(tm["dense"] / tm["dense_after_sparse_3to1"], 4)},
+            "steps_timed": tm["steps"],
+            "note": "whole training step: forward of every layer, loss gradient, backward of "
+                    "every layer (no input gradient for the bottom layer), SGD; synthetic "
+                    "regression target"}
     if fine is not None:
         nb = -(-wl.batch // fine[0])
         fk = {}

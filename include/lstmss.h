@@ -185,6 +185,23 @@ int32_t lstmss_select_compact(const lstmss_dims *d, float sparsity, const lstmss
                               const void *dG, void *dG_c, int32_t *idx, double *scores,
                               void *stream);
 
+/* Training step pieces around the backward pass (section 4: SGD with a
+ * fixed learning rate; section 5: dense-after-sparse schedules).
+ * lstmss_sgd_update: W <- W - lr dW (formed in fp32, stored in dtype,
+ *   round to nearest even for bf16) and, when b is not NULL, b <- b - lr db.
+ *   W [4H][I+H] dtype, dW [4H][I+H] fp32, b, db [4H] fp32.
+ * lstmss_mse_grad: regression loss of the top layer's hidden states against
+ *   a target, L = (1 / 2B) sum over t, u, n of (h - y)^2:
+ *   h [T][H][B] dtype, y [T][H][B] fp32, dH [T][H][B] fp32 = (h - y) / B
+ *   (the dH_up of the top layer's backward pass); loss: NULL, or a device
+ *   array of LSTMSS_LOSS_SLOTS fp64 values whose last one receives L (the
+ *   others hold partial sums), summed in a fixed order. */
+#define LSTMSS_LOSS_SLOTS 1025
+int32_t lstmss_sgd_update(const lstmss_dims *d, void *W, float *b, const float *dW,
+                          const float *db, float lr, void *stream);
+int32_t lstmss_mse_grad(const lstmss_dims *d, const void *h, const float *y, float *dH,
+                        double *loss, void *stream);
+
 /* Execution options (results are identical under every setting):
  *   LSTMSS_OPT_GRAPHS  1 (default): each backward call's launches are
  *                      captured once into a HIP graph, keyed by every

@@ -145,6 +145,13 @@ hipError_t launch_gemm2(const Gemm2Args &a, bool bf16, hipStream_t s);
 // W[m][kcol0 + k] G[k][n] (rows m in [0, M), contraction length Kp).
 hipError_t launch_gemm_fwd(Gemm1Args a, bool bf16, hipStream_t s);
 hipError_t launch_fwd_act(const FwdActArgs &a, bool bf16, hipStream_t s);
+// Training step: W -= lr dW (storage type), b -= lr db; and the regression
+// loss gradient dH = (h - y) / B with per-block loss partials (nparts <= 1024
+// blocks, their sum written to parts[nparts]).
+hipError_t launch_sgd(void *W, const float *dW, long nw, float *b, const float *db, long nb,
+                      float lr, bool bf16, hipStream_t s);
+hipError_t launch_mse(const void *h, const float *y, float *dH, long n, float inv_b,
+                      double *parts, int nparts, bool bf16, hipStream_t s);
 // Returns hipErrorNotSupported when the structure needs more routing tiles
 // than the batched kernel holds (the caller then uses launch_gemm2 per step).
 hipError_t launch_wgrad(WgradArgs a, bool sparse, bool bf16, hipStream_t s);

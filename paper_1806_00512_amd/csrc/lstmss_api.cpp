@@ -769,6 +769,40 @@ int32_t lstm_fwd_cache(const lstmss_dims *d, const void *x, const void *W, const
     return LSTMSS_OK;
 }
 
+int32_t lstmss_sgd_update(const lstmss_dims *d, void *W, float *b, const float *dW,
+                          const float *db, float lr, void *stream) {
+    int32_t rc = check_dims(d);
+    if (rc)
+        return rc;
+    if (!W || !dW || (b && !db))
+        return fail(LSTMSS_ERR_INVALID_ARG, "a required pointer is NULL");
+    if (!std::isfinite(lr))
+        return fail(LSTMSS_ERR_INVALID_ARG, "learning rate %g is not finite", (double)lr);
+    const long G = 4L * d->H;
+    hipStream_t st = (hipStream_t)stream;
+    HIP_TRY(timed(LSTMSS_KERNEL_AUX, st, [&] {
+        return launch_sgd(W, dW, G * ((long)d->I + d->H), b, db, b ? G : 0, lr,
+                          d->dtype == LSTMSS_BF16, st);
+    }));
+    return LSTMSS_OK;
+}
+
+int32_t lstmss_mse_grad(const lstmss_dims *d, const void *h, const float *y, float *dH,
+                        double *loss, void *stream) {
+    int32_t rc = check_dims(d);
+    if (rc)
+        return rc;
+    if (!h || !y || !dH)
+        return fail(LSTMSS_ERR_INVALID_ARG, "a required pointer is NULL");
+    const long n = (long)d->T * d->H * d->B;
+    hipStream_t st = (hipStream_t)stream;
+    HIP_TRY(timed(LSTMSS_KERNEL_AUX, st, [&] {
+        return launch_mse(h, y, dH, n, 1.f / (float)d->B, loss, LSTMSS_LOSS_SLOTS - 1,
+                          d->dtype == LSTMSS_BF16, st);
+    }));
+    return LSTMSS_OK;
+}
+
 int32_t lstm_bwd_dense(const lstmss_dims *d, const void *x, const void *W, const void *cache,
                        const float *dH_up, const float *dhT, const float *dcT, float *dX,
                        float *dW, float *db, float *dh0, float *dc0, void *ws, size_t ws_bytes,

@@ -98,6 +98,13 @@ def make_inputs(wl: Workload, seed: int = 0):
     return {"Ws": Ws, "bs": bs, "x": x, "dH_up": dH_up}
 
 
+def make_target(wl: Workload, seed: int = 1, std: float = 0.5) -> np.ndarray:
+    """Synthetic regression target y [T][H][B] for the top layer (float32)."""
+    rng = np.random.Generator(np.random.PCG64(seed))
+    y = rng.standard_normal((wl.steps, wl.hidden, wl.batch), dtype=np.float32)
+    return y * np.float32(std)
+
+
 def make_layer(T: int, B: int, I: int, H: int, seed: int, w_scale: float = 0.1,
                up_std: float = 1.0, dtype: str = "f32", state: bool = False):
     """One layer of random inputs of any shape (used for edge cases).

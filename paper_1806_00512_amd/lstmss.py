@@ -31,7 +31,7 @@ ERR = {0: "ok", -1: "invalid argument", -2: "unsupported", -3: "workspace too sm
 # Exported symbols of include/lstmss.h
 SYMBOLS = ("lstmss_version", "lstmss_strerror", "lstmss_last_error", "lstmss_cache_bytes",
            "lstmss_kept_rows", "lstmss_index_entries", "lstmss_workspace_bytes",
-           "lstmss_fwd_workspace_bytes",
+           "lstmss_fwd_workspace_bytes", "lstmss_sgd_update", "lstmss_mse_grad",
            "lstm_fwd_cache", "lstm_bwd_dense",
            "lstm_bwd_structsparse", "lstmss_select_compact", "lstmss_set_option",
            "lstmss_timing_enable", "lstmss_timing_read", "lstmss_timing_reset")
@@ -84,6 +84,10 @@ def load():
     lib.lstmss_fwd_workspace_bytes.restype = i64
     lib.lstm_fwd_cache.argtypes = [pd, vp, vp, vp, vp, vp, vp, vp, vp, ctypes.c_size_t, vp]
     lib.lstm_fwd_cache.restype = i32
+    lib.lstmss_sgd_update.argtypes = [pd, vp, vp, vp, vp, f, vp]
+    lib.lstmss_sgd_update.restype = i32
+    lib.lstmss_mse_grad.argtypes = [pd, vp, vp, vp, vp, vp]
+    lib.lstmss_mse_grad.restype = i32
     lib.lstm_bwd_dense.argtypes = [pd, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp,
                                    ctypes.c_size_t, vp]
     lib.lstm_bwd_dense.restype = i32
@@ -213,6 +217,38 @@ def fwd_cache(x, W, b=None, h0=None, c0=None, h_out=None, cache=None, stream=Non
                                _stream(stream))
     _check(rc, "lstm_fwd_cache")
     return h_out, cache
+
+
+LOSS_SLOTS = 1025
+
+
+def sgd_update(W, b, dW, db, lr, I, stream=None):
+    """In place: W -= lr dW (storage type of W), b -= lr db (b may be None)."""
+    G, K = W.shape
+    H = G // 4
+    d = dims(1, 1, I, H, W.dtype)
+    f32 = torch.float32
+    rc = load().lstmss_sgd_update(ctypes.byref(d), _ptr(W, W.dtype, (G, I + H), "W"),
+                                  _ptr(b, f32, (G,), "b"), _ptr(dW, f32, (G, I + H), "dW"),
+                                  _ptr(db, f32, (G,), "db"), float(lr), _stream(stream))
+    _check(rc, "lstmss_sgd_update")
+
+
+def mse_grad(h, y, dH=None, loss=None, stream=None):
+    """dH = (h - y) / B and the loss (1/2B) sum (h - y)^2 (fp64 device array of
+    LOSS_SLOTS, the loss in its last slot).  Returns (dH, loss)."""
+    T, H, B = h.shape
+    d = dims(T, B, 1, H, h.dtype)
+    if dH is None:
+        dH = torch.empty((T, H, B), dtype=torch.float32, device=h.device)
+    if loss is None:
+        loss = torch.empty(LOSS_SLOTS, dtype=torch.float64, device=h.device)
+    rc = load().lstmss_mse_grad(ctypes.byref(d), _ptr(h, h.dtype, name="h"),
+                                _ptr(y, torch.float32, (T, H, B), "y"),
+                                _ptr(dH, torch.float32, (T, H, B), "dH"),
+                                _ptr(loss, torch.float64, (LOSS_SLOTS,), "loss"), _stream(stream))
+    _check(rc, "lstmss_mse_grad")
+    return dH, loss
 
 
 def _bwd_outputs(T, B, I, H, dev, want_dX, out):
