@@ -2,13 +2,18 @@
 """Benchmark of the structurally sparsified LSTM backward pass on one MI355X.
 
 One step = the backward pass through time of every layer of the workload
-(top layer first; a layer's input gradient is the upstream gradient of the
-layer below) with coarse structural sparsifying at the workload's sparsity.
-The forward caches are computed once before timing; inputs stay resident in
-HBM.  The same step is timed with the dense backward (the speedup
-denominator), then a 9-sparse : 1-dense schedule, and a last pass with
-per-kernel HIP events (recorded on each kernel's launch stream by the
-library) gives each kernel's average launch duration for the roofline.
+(a layer's input gradient is the upstream gradient of the layer below) with
+coarse structural sparsifying at the workload's sparsity, run as one
+wavefront stack call (lstm_bwd_stack: the layers overlap in time, each
+lagging the one above by one input-gradient launch).  The forward caches are
+computed once before timing; inputs stay resident in HBM.  The same step is
+timed with the dense backward (the speedup denominator), with the layers
+called one after the other, with 9-sparse : 1-dense and 3 : 1 schedules, and
+a last pass of single-layer calls with per-kernel HIP events (recorded on
+each kernel's launch stream by the library) gives each kernel's average
+launch duration for the roofline.  The forward pass, whole training steps
+(dense-after-sparse trainer) and the fine-grained structure are timed
+beside it.
 
 Default workload: the 4-layer sequence-to-sequence encoder shape
 (I = H = 2048, B = 128, T = 50, fp32).  The two-layer language-model shape
@@ -207,12 +212,35 @@ class Runner:
         torch.cuda.synchronize()
         self.sp_bufs = self._buffers(sparsity, dev)
         self.dn_bufs = self._buffers(0.0, dev)
+        self.stack_bufs = {}
 
     def set_structure(self, **kw):
         """Switch the sparse steps to another structure (structure() keywords)."""
         self.kw = kw
         self.sp_bufs = None
+        self.stack_bufs = {}
         self.sp_bufs = self._buffers(self.sparsity, self.torch.device("cuda:0"))
+
+    def stack_step(self, sparse):
+        """One backward step over all layers as one wavefront stack call
+        (lstm_bwd_stack): same results as step(), layers overlapped in time."""
+        L, wl = self.L, self.wl
+        sp = self.sparsity if sparse else 0.0
+        if sparse not in self.stack_bufs:
+            o = L.bwd_stack(self.xs, self.Ws, self.caches, self.dH, sparsity=sp, want_dX0=True,
+                            **self.kw)
+            self.torch.cuda.synchronize()
+            ds = (L.Dims * wl.layers)(*[L.dims(wl.steps, wl.batch, wl.layer_input(l), wl.hidden,
+                                                self.st) for l in range(wl.layers)])
+            import ctypes
+            s = L.structure(**self.kw) if sp > 0 else None
+            n = L.load().lstmss_stack_workspace_bytes(wl.layers, ds, float(sp),
+                                                      ctypes.byref(s) if s else None)
+            o["ws"] = self.torch.empty(int(n), dtype=self.torch.uint8, device="cuda:0")
+            self.stack_bufs[sparse] = o
+        o = self.stack_bufs[sparse]
+        L.bwd_stack(self.xs, self.Ws, self.caches, self.dH, sparsity=sp, dXs=o["dX"],
+                    dWs=o["dW"], dbs=o["db"], idxs=o["idx"], ws=o["ws"], **self.kw)
 
     def _buffers(self, sp, dev):
         L, wl, torch = self.L, self.wl, self.torch
@@ -271,15 +299,26 @@ class Runner:
         torch.cuda.synchronize()
         return e0.elapsed_time(e1) / K
 
-    def timed(self, schedule, K, W):
+    def timed(self, schedule, K, W, stack=False):
         """schedule: one cycle of steps (True = sparse); K cycles timed after
         W untimed ones.  Returns mean ms per step, wall ms per step and mean
-        ms per layer call."""
+        ms per layer call (layer times only without stack)."""
         torch, wl = self.torch, self.wl
         for _ in range(W):
             for sp in schedule:
-                self.step(sp)
+                self.stack_step(sp) if stack else self.step(sp)
         torch.cuda.synchronize()
+        if stack:
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            w0 = time.perf_counter()
+            e0.record()
+            for _ in range(K):
+                for sp in schedule:
+                    self.stack_step(sp)
+            e1.record()
+            torch.cuda.synchronize()
+            n = K * len(schedule)
+            return e0.elapsed_time(e1) / n, (time.perf_counter() - w0) / n * 1e3, None
 
         def ev():
             return torch.cuda.Event(enable_timing=True)
@@ -308,28 +347,37 @@ class Runner:
 
 
 def measure(L, torch, wl, sparsity, steps, warmup, sparse_only=False, kernels=True, fine=None):
+    """Backward step timings.  The headline step is the wavefront stack call
+    (every layer in one lstm_bwd_stack call); the layers called one after the
+    other are timed beside it (with per-layer times)."""
     r = Runner(L, wl, sparsity, torch)
     res = {"runner": r}
-    sp_ms, sp_wall, sp_layer = r.timed([True], steps, warmup)
-    print("%s sparse: %.4f ms/step (wall %.4f)" % (wl.name, sp_ms, sp_wall), file=sys.stderr,
-          flush=True)
-    res.update(sp_ms=sp_ms, sp_wall=sp_wall, sp_layer=sp_layer)
+    sp_ms, sp_wall, _ = r.timed([True], steps, warmup, stack=True)
+    print("%s sparse (stack): %.4f ms/step (wall %.4f)" % (wl.name, sp_ms, sp_wall),
+          file=sys.stderr, flush=True)
+    res.update(sp_ms=sp_ms, sp_wall=sp_wall)
     if sparse_only:
         return res
-    dn_ms, dn_wall, dn_layer = r.timed([False], steps, warmup)
-    print("%s dense: %.4f ms/step (wall %.4f)" % (wl.name, dn_ms, dn_wall), file=sys.stderr,
-          flush=True)
-    res.update(dn_ms=dn_ms, dn_wall=dn_wall, dn_layer=dn_layer)
+    dn_ms, dn_wall, _ = r.timed([False], steps, warmup, stack=True)
+    print("%s dense (stack): %.4f ms/step (wall %.4f)" % (wl.name, dn_ms, dn_wall),
+          file=sys.stderr, flush=True)
+    res.update(dn_ms=dn_ms, dn_wall=dn_wall)
+    # the layers one after the other (graph-replayed single-layer calls)
+    sq_ms, _, sq_layer = r.timed([True], steps, warmup)
+    sqd_ms, _, sqd_layer = r.timed([False], steps, warmup)
+    print("%s sequential layers: sparse %.4f, dense %.4f ms/step" % (wl.name, sq_ms, sqd_ms),
+          file=sys.stderr, flush=True)
+    res.update(sq_ms=sq_ms, sq_layer=sq_layer, sqd_ms=sqd_ms, sqd_layer=sqd_layer)
     if not kernels:
         return res
     # the 9 sparse : 1 dense schedule (dense-after-sparse training phases)
     cycles = max(1, steps // 10)
-    mx_ms, _, _ = r.timed([True] * 9 + [False], cycles, 1)
+    mx_ms, _, _ = r.timed([True] * 9 + [False], cycles, 1, stack=True)
     print("%s 9:1 schedule: %.4f ms/step" % (wl.name, mx_ms), file=sys.stderr, flush=True)
     res.update(mix_ms=mx_ms, mix_cycles=cycles)
     # the 3 sparse : 1 dense schedule of dense-after-sparse training
     c3 = max(1, steps // 4)
-    m3_ms, _, _ = r.timed([True] * 3 + [False], c3, 1)
+    m3_ms, _, _ = r.timed([True] * 3 + [False], c3, 1, stack=True)
     print("%s 3:1 schedule: %.4f ms/step" % (wl.name, m3_ms), file=sys.stderr, flush=True)
     res.update(mix3_ms=m3_ms, mix3_cycles=c3)
     # forward pass (batched path, and one pass of the fused per-step path)
@@ -349,7 +397,7 @@ def measure(L, torch, wl, sparsity, steps, warmup, sparse_only=False, kernels=Tr
     if fine is not None:
         # fine-grained structure: My x Mx blocks, K = sparsity * nb per slice
         r.set_structure(kind=L.FINE, My=fine[0], Mx=fine[1])
-        fn_ms, fn_wall, fn_layer = r.timed([True], steps, warmup)
+        fn_ms, fn_wall, _ = r.timed([True], steps, warmup, stack=True)
         print("%s fine (My=%d, Mx=%d): %.4f ms/step" % (wl.name, fine[0], fine[1], fn_ms),
               file=sys.stderr, flush=True)
         L.timing_reset()
@@ -357,7 +405,7 @@ def measure(L, torch, wl, sparsity, steps, warmup, sparse_only=False, kernels=Tr
         for _ in range(steps):
             r.step(True)
         torch.cuda.synchronize()
-        res.update(fn_ms=fn_ms, fn_wall=fn_wall, fn_layer=fn_layer, fn_kt=L.timing_read())
+        res.update(fn_ms=fn_ms, fn_wall=fn_wall, fn_kt=L.timing_read())
         L.timing_enable(False)
         L.timing_reset()
     return res
@@ -494,13 +542,19 @@ def main():
                    "hidden": wl.hidden, "batch": wl.batch, "seq_len": wl.steps,
                    "sparsity": sparsity, "P": wl.P, "R": wl.R,
                    "S": int(round(sparsity * wl.R)), "storage": wl.dtype,
-                   "side_stream": "off" if args.serial else "auto"},
+                   "side_stream": "off" if args.serial else "auto",
+                   "schedule": "wavefront stack call (lstm_bwd_stack)"},
         "dense_ms_per_step": round(dn_ms, 5),
         "speedup_vs_dense": round(dn_ms / sp_ms, 4),
         "algorithmic_tflops": round(exec_flops / (sp_ms / 1e3) / 1e12, 4),
         "dense_tflops": round(dense_flops / (dn_ms / 1e3) / 1e12, 4),
-        "per_layer_ms": {"sparse": [round(v, 5) for v in m["sp_layer"]],
-                         "dense": [round(v, 5) for v in m["dn_layer"]]},
+        "sequential_layers": {
+            "note": "the layers' backward calls one after the other (each replayed from its "
+                    "HIP graph) instead of one wavefront stack call",
+            "ms_per_step": round(m["sq_ms"], 5), "dense_ms_per_step": round(m["sqd_ms"], 5),
+            "speedup_vs_dense": round(m["sqd_ms"] / m["sq_ms"], 4),
+            "per_layer_ms": {"sparse": [round(v, 5) for v in m["sq_layer"]],
+                             "dense": [round(v, 5) for v in m["sqd_layer"]]}},
         "mixed_9sparse_1dense": {"ms_per_step": round(m["mix_ms"], 5), "cycles": m["mix_cycles"],
                                  "formula_ms": round((9 * sp_ms + dn_ms) / 10, 5)},
         "mixed_3sparse_1dense": {"ms_per_step": round(m["mix3_ms"], 5),
@@ -542,7 +596,6 @@ def main():
                           "speedup_vs_dense": round(dn_ms / m["fn_ms"], 4),
                           "value": round(dense_flops / (m["fn_ms"] / 1e3) / 1e12, 4),
                           "unit": "TFLOP/s",
-                          "per_layer_ms": [round(v, 5) for v in m["fn_layer"]],
                           "kernels": fk}
     if not args.no_cpu_baseline:
         result["cpu_baseline"] = cpu_baseline(wl, m["runner"].inp, sparsity)
@@ -558,6 +611,8 @@ def main():
             also.append({"workload": name, "ms_per_step": round(m2["sp_ms"], 5),
                          "dense_ms_per_step": round(m2["dn_ms"], 5),
                          "speedup_vs_dense": round(m2["dn_ms"] / m2["sp_ms"], 4),
+                         "sequential_layers_ms_per_step": {"sparse": round(m2["sq_ms"], 5),
+                                                           "dense": round(m2["sqd_ms"], 5)},
                          "value": round(flops_of(w2) / (m2["sp_ms"] / 1e3) / 1e12, 4),
                          "unit": "TFLOP/s"})
             del m2

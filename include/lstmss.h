@@ -185,6 +185,33 @@ int32_t lstmss_select_compact(const lstmss_dims *d, float sparsity, const lstmss
                               const void *dG, void *dG_c, int32_t *idx, double *scores,
                               void *stream);
 
+/* Backward pass of a stack of `layers` (1..8) LSTM layers, bottom layer 0,
+ * scheduled as a wavefront (the layer-time pipelining of a stacked LSTM):
+ * layer l's input gradient dX[l] is layer l-1's upstream gradient, and
+ * every layer runs on its own library-owned streams, its step t waiting
+ * only for the input-gradient launch of layer l+1 that produced dH_up[t]
+ * (launches of LSTMSS_OPT_STACK_DX_STEPS steps), so the layers overlap in
+ * time.  Results are those of calling lstm_bwd_structsparse (or, with s
+ * NULL or sparsity 0, lstm_bwd_dense) on each layer in turn, top first,
+ * with dhT = dcT = NULL.  A stack call is enqueued directly (never
+ * recorded into a HIP graph, whatever LSTMSS_OPT_GRAPHS says).
+ *   d            [layers] dims; equal T, B, dtype; d[l].I = d[l-1].H
+ *   x, W, cache  [layers] per-layer pointers as for lstm_bwd_structsparse
+ *   dH_top       [T][H][B] fp32 upstream gradient of the top layer
+ *   dX           [layers] fp32 [T][I_l][B]; dX[0] may be NULL
+ *   dW           [layers] fp32 [4H][I_l+H]; db: NULL or [layers] fp32 [4H]
+ *                (entries may be NULL)
+ *   idx_out      NULL or [layers] (entries may be NULL), as idx_out of
+ *                lstm_bwd_structsparse
+ *   ws           lstmss_stack_workspace_bytes(...) bytes. */
+int64_t lstmss_stack_workspace_bytes(int32_t layers, const lstmss_dims *d, float sparsity,
+                                     const lstmss_structure *s);
+int32_t lstm_bwd_stack(int32_t layers, const lstmss_dims *d, float sparsity,
+                       const lstmss_structure *s, const void *const *x, const void *const *W,
+                       const void *const *cache, const float *dH_top, float *const *dX,
+                       float *const *dW, float *const *db, int32_t *const *idx_out, void *ws,
+                       size_t ws_bytes, void *stream);
+
 /* Training step pieces around the backward pass (section 4: SGD with a
  * fixed learning rate; section 5: dense-after-sparse schedules).
  * lstmss_sgd_update: W <- W - lr dW (formed in fp32, stored in dtype,
@@ -216,9 +243,12 @@ int32_t lstmss_mse_grad(const lstmss_dims *d, const void *h, const float *y, flo
  *                      stream while a step's data-gradient GEMM is below
  *                      2^31 multiply-adds ((I+H) * B * K'), else in order
  *                      (large GEMMs fill the GPU by themselves).
+ *   LSTMSS_OPT_STACK_DX_STEPS  steps per input-gradient launch inside
+ *                      lstm_bwd_stack, i.e. how many steps a layer lags the
+ *                      layer above; 0 (default) = T/4, at least 1.
  * Changing an option drops the recorded graphs.  Not for use while calls
  * are being enqueued from other threads. */
-enum { LSTMSS_OPT_GRAPHS = 0, LSTMSS_OPT_SIDE_STREAM = 1 };
+enum { LSTMSS_OPT_GRAPHS = 0, LSTMSS_OPT_SIDE_STREAM = 1, LSTMSS_OPT_STACK_DX_STEPS = 2 };
 int32_t lstmss_set_option(int32_t option, int32_t value);
 
 /* Measurement hooks (not part of the method): when enabled, every kernel the

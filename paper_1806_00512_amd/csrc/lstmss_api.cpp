@@ -143,6 +143,48 @@ hipError_t side_stream(SideStream **out) {
     return hipSuccess;
 }
 
+// Streams and events of lstm_bwd_stack (per device): one main and one side
+// stream per layer, each layer's fork ring and join event, one event per dX
+// chunk per layer.
+constexpr int kMaxStackLayers = 8;
+struct StackRes {
+    hipStream_t main[kMaxStackLayers] = {}, side[kMaxStackLayers] = {};
+    hipEvent_t ring[kMaxStackLayers][kForkEvents] = {};
+    hipEvent_t join[kMaxStackLayers] = {}, done[kMaxStackLayers] = {};
+    hipEvent_t fork = nullptr;
+    std::vector<hipEvent_t> chunk_ev[kMaxStackLayers];
+    std::mutex mu;
+};
+std::map<int, StackRes> g_stack;
+// steps per dX launch inside a stack (the wavefront lag between layers):
+// 0 = T/4 (at least 1)
+int g_stack_dx_steps = 0;
+
+hipError_t stack_res(StackRes **out) {
+    int dev = 0;
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess)
+        return e;
+    std::lock_guard<std::mutex> lk(g_side_mu);
+    StackRes &r = g_stack[dev];
+    if (!r.fork) {
+        auto ev = [&](hipEvent_t *q) { return hipEventCreateWithFlags(q, hipEventDisableTiming); };
+        for (int l = 0; l < kMaxStackLayers; ++l) {
+            if ((e = hipStreamCreateWithFlags(&r.main[l], hipStreamNonBlocking)) != hipSuccess ||
+                (e = hipStreamCreateWithFlags(&r.side[l], hipStreamNonBlocking)) != hipSuccess ||
+                (e = ev(&r.join[l])) != hipSuccess || (e = ev(&r.done[l])) != hipSuccess)
+                return e;
+            for (int i = 0; i < kForkEvents; ++i)
+                if ((e = ev(&r.ring[l][i])) != hipSuccess)
+                    return e;
+        }
+        if ((e = ev(&r.fork)) != hipSuccess)
+            return e;
+    }
+    *out = &r;
+    return hipSuccess;
+}
+
 size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
 long ceil_div(long a, long b) { return (a + b - 1) / b; }
 
@@ -338,13 +380,32 @@ WsLayout ws_layout(const lstmss_dims *d, const Plan &p) {
     return L;
 }
 
-// Enqueue one backward call on main stream st, with side (locked by the
+// Streams and events one backward call is enqueued with.  In a layer stack
+// (lstm_bwd_stack) a layer's step t waits for the dX chunk of the layer above
+// that holds its upstream gradient dH_up[t], and records an event after each
+// of its own dX chunks for the layer below.
+struct ChunkEv {
+    int t_lo, t_hi;  // steps [t_lo, t_hi)
+    hipEvent_t ev;   // recorded after the chunk's launch
+};
+struct EnqCtx {
+    hipStream_t side = nullptr;                      // off-critical-path work
+    hipEvent_t *ring = nullptr;                      // fork events, used in turn
+    int nring = 0;
+    hipEvent_t join = nullptr;                       // side -> main at the end
+    const std::vector<ChunkEv> *dH_ready = nullptr;  // chunks of the layer above
+    std::vector<ChunkEv> *dx_done = nullptr;         // this layer's dX chunks
+    std::vector<hipEvent_t> *dx_events = nullptr;    // events for them (one per chunk)
+    int max_dx_len = 0;                              // cap on steps per dX launch (0: none)
+};
+
+// Enqueue one backward call on main stream st, with ctx (locked by the
 // caller) for the off-critical-path work.  Arguments already checked.
 int32_t backward_enqueue(const lstmss_dims *d, bool dense, const Plan &p, const void *x,
                          const void *W, const void *cache, const float *dH_up, const float *dhT,
                          const float *dcT, float *dX, float *dW, float *db, float *dh0,
                          float *dc0, int32_t *idx_out, void *dbg, void *ws, hipStream_t st,
-                         SideStream *side) {
+                         const EnqCtx &ctx) {
     const WsLayout L = ws_layout(d, p);
     const bool bf16 = d->dtype == LSTMSS_BF16;
     const bool sparse = !dense;
@@ -391,7 +452,7 @@ int32_t backward_enqueue(const lstmss_dims *d, bool dense, const Plan &p, const 
     const bool use_side = batched || dX;
     const bool concurrent = use_side && (g_side_mode == 1 ||
                                          (g_side_mode == 2 && (double)K * B * p.Kp < kSideMaxMacs));
-    hipStream_t sst = concurrent ? side->s : st;
+    hipStream_t sst = concurrent ? ctx.side : st;
     // the weight gradient runs in chunks of chunk_len steps and dX in chunks
     // of dx_len steps (whole rounds of resident work-groups); each launches
     // once its lowest step has its gate gradients
@@ -401,6 +462,8 @@ int32_t backward_enqueue(const lstmss_dims *d, bool dense, const Plan &p, const 
         chunk_len = (int)ceil_div(T, nchunks);
         if (dX)
             dx_len = dx_chunk_len(d, chunk_len, &dx_tm, &dx_tn);
+        if (dX && ctx.max_dx_len > 0 && dx_len > ctx.max_dx_len)
+            dx_len = ctx.max_dx_len;
     }
     int wg_hi = T, dx_hi = T, wg_count = 0, forks = 0;
     WgradArgs wg{};
@@ -420,6 +483,11 @@ int32_t backward_enqueue(const lstmss_dims *d, bool dense, const Plan &p, const 
         const bool last = t == T - 1;
         char *dGc = dGc_all + (size_t)t * p.Kp * B * es;
         int32_t *idx = idx_all + (size_t)t * p.kept;
+
+        if (ctx.dH_ready)  // upstream gradient of this step from the layer above
+            for (const ChunkEv &c : *ctx.dH_ready)
+                if (c.t_hi - 1 == t)
+                    HIP_TRY(hipStreamWaitEvent(st, c.ev, 0));
 
         CellArgs ca{};
         ca.B = B; ca.H = H; ca.I = I;
@@ -473,9 +541,9 @@ int32_t backward_enqueue(const lstmss_dims *d, bool dense, const Plan &p, const 
         const bool wg_now = use_side && batched && t == std::max(0, wg_hi - chunk_len);
         const bool dx_now = use_side && dX && t == std::max(0, dx_hi - dx_len);
         if ((wg_now || dx_now) && concurrent) {
-            hipEvent_t e = side->ev[forks++ % kForkEvents];
+            hipEvent_t e = ctx.ring[forks++ % ctx.nring];
             HIP_TRY(hipEventRecord(e, st));
-            HIP_TRY(hipStreamWaitEvent(side->s, e, 0));
+            HIP_TRY(hipStreamWaitEvent(ctx.side, e, 0));
         }
         if (wg_now) {
             wg.t_begin = t;
@@ -490,6 +558,13 @@ int32_t backward_enqueue(const lstmss_dims *d, bool dense, const Plan &p, const 
             gx.part = dX + (size_t)t * I * B;
             gx.steps = dx_hi - t;
             HIP_TRY(timed(LSTMSS_KERNEL_DATA_GRAD, sst, [&] { return launch_gemm1(gx, bf16, sst); }));
+            if (ctx.dx_done) {
+                const size_t k = ctx.dx_done->size();
+                if (k >= ctx.dx_events->size())
+                    return fail(LSTMSS_ERR_HIP, "too few chunk events");
+                HIP_TRY(hipEventRecord((*ctx.dx_events)[k], sst));
+                ctx.dx_done->push_back(ChunkEv{t, dx_hi, (*ctx.dx_events)[k]});
+            }
             dx_hi = t;
         }
 
@@ -511,8 +586,8 @@ int32_t backward_enqueue(const lstmss_dims *d, bool dense, const Plan &p, const 
         }
     }
     if (concurrent) {
-        HIP_TRY(hipEventRecord(side->join, side->s));
-        HIP_TRY(hipStreamWaitEvent(st, side->join, 0));
+        HIP_TRY(hipEventRecord(ctx.join, ctx.side));
+        HIP_TRY(hipStreamWaitEvent(st, ctx.join, 0));
     }
     if (split)
         HIP_TRY(timed(LSTMSS_KERNEL_AUX, st, [&] {
@@ -555,9 +630,14 @@ int32_t backward(const lstmss_dims *d, bool dense, float sparsity, const lstmss_
         std::lock_guard<std::mutex> tl(g_tmu);
         timing = g_timing;
     }
+    EnqCtx ctx;
+    ctx.side = side->s;
+    ctx.ring = side->ev;
+    ctx.nring = kForkEvents;
+    ctx.join = side->join;
     if (!g_graphs || timing)
         return backward_enqueue(d, dense, p, x, W, cache, dH_up, dhT, dcT, dX, dW, db, dh0, dc0,
-                                idx_out, dbg, ws, st, side);
+                                idx_out, dbg, ws, st, ctx);
 
     auto u = [](const void *q) { return (uint64_t)(uintptr_t)q; };
     std::vector<uint64_t> key = {(uint64_t)d->T, (uint64_t)d->B, (uint64_t)d->I, (uint64_t)d->H,
@@ -575,7 +655,7 @@ int32_t backward(const lstmss_dims *d, bool dense, float sparsity, const lstmss_
         // capture through the fork/join events inside backward_enqueue
         HIP_TRY(hipStreamBeginCapture(side->cap, hipStreamCaptureModeRelaxed));
         rc = backward_enqueue(d, dense, p, x, W, cache, dH_up, dhT, dcT, dX, dW, db, dh0, dc0,
-                              idx_out, dbg, ws, side->cap, side);
+                              idx_out, dbg, ws, side->cap, ctx);
         hipGraph_t graph = nullptr;
         const hipError_t ec = hipStreamEndCapture(side->cap, &graph);
         if (rc != LSTMSS_OK) {
@@ -606,9 +686,121 @@ int32_t backward(const lstmss_dims *d, bool dense, float sparsity, const lstmss_
     return LSTMSS_OK;
 }
 
+struct StackPlan {
+    std::vector<Plan> plans;
+    std::vector<size_t> ws_off;
+    size_t total = 0;
+    bool dense = true;
+};
+
+int32_t stack_plan(int32_t layers, const lstmss_dims *d, float sparsity, const lstmss_structure *s,
+                   StackPlan *sp) {
+    if (layers < 1 || layers > kMaxStackLayers)
+        return fail(LSTMSS_ERR_INVALID_ARG, "layers=%d must be in [1, %d]", layers,
+                    kMaxStackLayers);
+    if (!d)
+        return fail(LSTMSS_ERR_INVALID_ARG, "dims is NULL");
+    sp->dense = s == nullptr || sparsity == 0.f;
+    sp->plans.assign(layers, Plan{});
+    sp->ws_off.assign(layers, 0);
+    sp->total = 0;
+    for (int l = 0; l < layers; ++l) {
+        int32_t rc = check_dims(&d[l]);
+        if (rc)
+            return rc;
+        if (d[l].T != d[0].T || d[l].B != d[0].B || d[l].dtype != d[0].dtype)
+            return fail(LSTMSS_ERR_INVALID_ARG, "layer %d: T, B and dtype must match layer 0", l);
+        if (l > 0 && d[l].I != d[l - 1].H)
+            return fail(LSTMSS_ERR_INVALID_ARG, "layer %d: I=%d must equal the H=%d below", l,
+                        d[l].I, d[l - 1].H);
+        rc = make_plan(&d[l], sparsity, s, sp->dense, &sp->plans[l]);
+        if (rc)
+            return rc;
+        sp->ws_off[l] = sp->total;
+        sp->total += align256(ws_layout(&d[l], sp->plans[l]).total);
+    }
+    return LSTMSS_OK;
+}
+
+// Wavefront backward of a layer stack: every layer runs on its own pair of
+// streams; layer l's step t waits only for the dX chunk of layer l + 1 that
+// holds its dH_up[t], so the layers overlap in time, each lagging the one
+// above by one dX chunk.
+int32_t stack_enqueue(int32_t layers, const lstmss_dims *d, const StackPlan &sp,
+                      const void *const *x, const void *const *W, const void *const *cache,
+                      const float *dH_top, float *const *dX, float *const *dW, float *const *db,
+                      int32_t *const *idx_out, void *ws, hipStream_t origin, StackRes &R) {
+    std::vector<ChunkEv> chunks[kMaxStackLayers];
+    HIP_TRY(hipEventRecord(R.fork, origin));
+    for (int l = layers - 1; l >= 0; --l) {
+        hipStream_t ms = R.main[l];
+        HIP_TRY(hipStreamWaitEvent(ms, R.fork, 0));
+        EnqCtx ctx;
+        ctx.side = R.side[l];
+        ctx.ring = R.ring[l];
+        ctx.nring = kForkEvents;
+        ctx.join = R.join[l];
+        ctx.dH_ready = l == layers - 1 ? nullptr : &chunks[l + 1];
+        ctx.dx_done = l > 0 ? &chunks[l] : nullptr;
+        ctx.dx_events = &R.chunk_ev[l];
+        ctx.max_dx_len = g_stack_dx_steps > 0 ? g_stack_dx_steps : std::max(1, d[l].T / 4);
+        const float *up = l == layers - 1 ? dH_top : dX[l + 1];
+        const int32_t rc = backward_enqueue(&d[l], sp.dense, sp.plans[l], x[l], W[l], cache[l],
+                                            up, nullptr, nullptr, dX[l], dW[l], db ? db[l] : nullptr,
+                                            nullptr, nullptr, idx_out ? idx_out[l] : nullptr,
+                                            nullptr, (char *)ws + sp.ws_off[l], ms, ctx);
+        if (rc != LSTMSS_OK)
+            return rc;
+        HIP_TRY(hipEventRecord(R.done[l], ms));
+        HIP_TRY(hipStreamWaitEvent(origin, R.done[l], 0));
+    }
+    return LSTMSS_OK;
+}
+
 } // namespace
 
 extern "C" {
+
+int64_t lstmss_stack_workspace_bytes(int32_t layers, const lstmss_dims *d, float sparsity,
+                                     const lstmss_structure *s) {
+    StackPlan sp;
+    const int32_t rc = stack_plan(layers, d, sparsity, s, &sp);
+    if (rc)
+        return rc;
+    return (int64_t)sp.total;
+}
+
+int32_t lstm_bwd_stack(int32_t layers, const lstmss_dims *d, float sparsity,
+                       const lstmss_structure *s, const void *const *x, const void *const *W,
+                       const void *const *cache, const float *dH_top, float *const *dX,
+                       float *const *dW, float *const *db, int32_t *const *idx_out, void *ws,
+                       size_t ws_bytes, void *stream) {
+    StackPlan sp;
+    int32_t rc = stack_plan(layers, d, sparsity, s, &sp);
+    if (rc)
+        return rc;
+    if (!x || !W || !cache || !dH_top || !dX || !dW || !ws)
+        return fail(LSTMSS_ERR_INVALID_ARG, "a required pointer is NULL");
+    for (int l = 0; l < layers; ++l)
+        if (!x[l] || !W[l] || !cache[l] || !dW[l] || (l > 0 && !dX[l]))
+            return fail(LSTMSS_ERR_INVALID_ARG, "layer %d: a required pointer is NULL", l);
+    if (ws_bytes < sp.total)
+        return fail(LSTMSS_ERR_WORKSPACE, "workspace of %zu bytes, need %zu", ws_bytes, sp.total);
+    StackRes *R = nullptr;
+    HIP_TRY(stack_res(&R));
+    std::unique_lock<std::mutex> lk(R->mu);
+    for (int l = 0; l < layers; ++l)  // one event per possible dX chunk
+        while ((int)R->chunk_ev[l].size() < d[l].T) {
+            hipEvent_t e = nullptr;
+            HIP_TRY(hipEventCreateWithFlags(&e, hipEventDisableTiming));
+            R->chunk_ev[l].push_back(e);
+        }
+    // enqueued directly on the layers' streams, whatever LSTMSS_OPT_GRAPHS
+    // says: recording a stack call into a HIP graph ended in a host
+    // segmentation fault whose cause is not found, so that path is off
+    return stack_enqueue(layers, d, sp, x, W, cache, dH_top, dX, dW, db, idx_out, ws,
+                         (hipStream_t)stream, *R);
+}
 
 int32_t lstmss_version(void) { return LSTMSS_VERSION; }
 
@@ -865,6 +1057,11 @@ int32_t lstmss_set_option(int32_t option, int32_t value) {
     }
     switch (option) {
     case LSTMSS_OPT_GRAPHS: g_graphs = value != 0; return LSTMSS_OK;
+    case LSTMSS_OPT_STACK_DX_STEPS:
+        if (value < 0)
+            return fail(LSTMSS_ERR_INVALID_ARG, "stack dX steps %d must be >= 0", value);
+        g_stack_dx_steps = value;
+        return LSTMSS_OK;
     case LSTMSS_OPT_SIDE_STREAM:
         if (value < 0 || value > 2)
             return fail(LSTMSS_ERR_INVALID_ARG, "side-stream mode %d (0, 1 or 2)", value);

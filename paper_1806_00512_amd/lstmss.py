@@ -32,6 +32,7 @@ ERR = {0: "ok", -1: "invalid argument", -2: "unsupported", -3: "workspace too sm
 SYMBOLS = ("lstmss_version", "lstmss_strerror", "lstmss_last_error", "lstmss_cache_bytes",
            "lstmss_kept_rows", "lstmss_index_entries", "lstmss_workspace_bytes",
            "lstmss_fwd_workspace_bytes", "lstmss_sgd_update", "lstmss_mse_grad",
+           "lstmss_stack_workspace_bytes", "lstm_bwd_stack",
            "lstm_fwd_cache", "lstm_bwd_dense",
            "lstm_bwd_structsparse", "lstmss_select_compact", "lstmss_set_option",
            "lstmss_timing_enable", "lstmss_timing_read", "lstmss_timing_reset")
@@ -88,6 +89,11 @@ def load():
     lib.lstmss_sgd_update.restype = i32
     lib.lstmss_mse_grad.argtypes = [pd, vp, vp, vp, vp, vp]
     lib.lstmss_mse_grad.restype = i32
+    lib.lstmss_stack_workspace_bytes.argtypes = [i32, pd, f, ps]
+    lib.lstmss_stack_workspace_bytes.restype = i64
+    lib.lstm_bwd_stack.argtypes = [i32, pd, f, ps, vp, vp, vp, vp, vp, vp, vp, vp, vp,
+                                   ctypes.c_size_t, vp]
+    lib.lstm_bwd_stack.restype = i32
     lib.lstm_bwd_dense.argtypes = [pd, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp,
                                    ctypes.c_size_t, vp]
     lib.lstm_bwd_dense.restype = i32
@@ -251,6 +257,54 @@ def mse_grad(h, y, dH=None, loss=None, stream=None):
     return dH, loss
 
 
+def _ptr_array(ts, name, dtype=None):
+    """ctypes array of device pointers (None entries -> NULL)."""
+    arr = (ctypes.c_void_p * len(ts))()
+    for i, t in enumerate(ts):
+        p = _ptr(t, dtype, name="%s[%d]" % (name, i))
+        arr[i] = None if p is None else p.value
+    return arr
+
+
+def bwd_stack(xs, Ws, caches, dH_top, sparsity=0.5, P=4, R=8, kind=COARSE, My=0, Mx=0,
+              dXs=None, dWs=None, dbs=None, idxs=None, ws=None, want_dX0=False, stream=None):
+    """Wavefront backward of a layer stack (layer 0 at the bottom): per-layer
+    lists xs [T][I_l][B], Ws, caches; dH_top [T][H][B].  sparsity 0 = dense.
+    Returns dict(dX, dW, db, idx) of per-layer lists."""
+    n = len(xs)
+    T, _, B = xs[0].shape
+    st = xs[0].dtype
+    dev = xs[0].device
+    f32 = torch.float32
+    ds = (Dims * n)()
+    for l in range(n):
+        ds[l] = dims(T, B, xs[l].shape[1], Ws[l].shape[0] // 4, st)
+    s = structure(P, R, kind, My, Mx) if sparsity > 0 else None
+    sp = float(sparsity)
+    if dWs is None:
+        dWs = [torch.empty(tuple(W.shape), dtype=f32, device=dev) for W in Ws]
+    if dbs is None:
+        dbs = [torch.empty(W.shape[0], dtype=f32, device=dev) for W in Ws]
+    if dXs is None:
+        dXs = [torch.empty(tuple(x.shape), dtype=f32, device=dev) if (l > 0 or want_dX0) else None
+               for l, x in enumerate(xs)]
+    if idxs is None and s is not None:
+        idxs = [torch.empty((T, index_entries(ds[l], sp, s)), dtype=torch.int32, device=dev)
+                for l in range(n)]
+    if ws is None:
+        nb = load().lstmss_stack_workspace_bytes(n, ds, sp, ctypes.byref(s) if s else None)
+        _check(0 if nb >= 0 else int(nb), "lstmss_stack_workspace_bytes")
+        ws = torch.empty(int(nb), dtype=torch.uint8, device=dev)
+    rc = load().lstm_bwd_stack(
+        n, ds, sp, ctypes.byref(s) if s else None, _ptr_array(xs, "x", st),
+        _ptr_array(Ws, "W", st), _ptr_array(caches, "cache", torch.uint8),
+        _ptr(dH_top, f32, name="dH_top"), _ptr_array(dXs, "dX", f32), _ptr_array(dWs, "dW", f32),
+        _ptr_array(dbs, "db", f32), _ptr_array(idxs, "idx", torch.int32) if idxs else None,
+        _ptr(ws, torch.uint8, name="ws"), ws.numel(), _stream(stream))
+    _check(rc, "lstm_bwd_stack")
+    return {"dX": dXs, "dW": dWs, "db": dbs, "idx": idxs}
+
+
 def _bwd_outputs(T, B, I, H, dev, want_dX, out):
     out = dict(out or {})
     f32 = torch.float32
@@ -371,7 +425,7 @@ def cache_views(cache, T, B, H, dtype):
     return gates, c, h
 
 
-OPTIONS = {"graphs": 0, "side_stream": 1}
+OPTIONS = {"graphs": 0, "side_stream": 1, "stack_dx_steps": 2}
 
 
 def set_option(name: str, value: int):

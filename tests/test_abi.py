@@ -142,3 +142,24 @@ def test_product_path_fails_loudly_without_library(tmp_path, monkeypatch):
     monkeypatch.setattr(lstmss, "LIB_PATH", str(tmp_path / "missing.so"))
     with pytest.raises(RuntimeError):
         lstmss.load()
+
+
+def test_stack_workspace_and_validation(L):
+    lib = L.load()
+    s = L.structure(4, 8)
+    ds = (L.Dims * 2)(L.dims(4, 8, 16, 32), L.dims(4, 8, 32, 32))
+    n = lib.lstmss_stack_workspace_bytes(2, ds, 0.5, ctypes.byref(s))
+    assert n >= L.workspace_bytes(ds[0], 0.5, s) + L.workspace_bytes(ds[1], 0.5, s)
+    nd = lib.lstmss_stack_workspace_bytes(2, ds, 0.0, None)
+    assert nd >= L.workspace_bytes(ds[0]) + L.workspace_bytes(ds[1])
+    bad_i = (L.Dims * 2)(L.dims(4, 8, 16, 32), L.dims(4, 8, 16, 32))   # I != H below
+    assert lib.lstmss_stack_workspace_bytes(2, bad_i, 0.5, ctypes.byref(s)) == -1
+    bad_t = (L.Dims * 2)(L.dims(4, 8, 16, 32), L.dims(5, 8, 32, 32))   # T differs
+    assert lib.lstmss_stack_workspace_bytes(2, bad_t, 0.5, ctypes.byref(s)) == -1
+    assert lib.lstmss_stack_workspace_bytes(0, ds, 0.5, ctypes.byref(s)) == -1
+    assert lib.lstmss_stack_workspace_bytes(9, ds, 0.5, ctypes.byref(s)) == -1
+    # pointer checks run before any device work
+    null = (ctypes.c_void_p * 2)()
+    rc = lib.lstm_bwd_stack(2, ds, 0.5, ctypes.byref(s), null, null, null, None, null, null,
+                            None, None, None, 0, None)
+    assert rc == -1
