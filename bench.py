@@ -230,13 +230,11 @@ class Runner:
             o = L.bwd_stack(self.xs, self.Ws, self.caches, self.dH, sparsity=sp, want_dX0=True,
                             **self.kw)
             self.torch.cuda.synchronize()
-            ds = (L.Dims * wl.layers)(*[L.dims(wl.steps, wl.batch, wl.layer_input(l), wl.hidden,
-                                                self.st) for l in range(wl.layers)])
-            import ctypes
+            ds = [L.dims(wl.steps, wl.batch, wl.layer_input(l), wl.hidden, self.st)
+                  for l in range(wl.layers)]
             s = L.structure(**self.kw) if sp > 0 else None
-            n = L.load().lstmss_stack_workspace_bytes(wl.layers, ds, float(sp),
-                                                      ctypes.byref(s) if s else None)
-            o["ws"] = self.torch.empty(int(n), dtype=self.torch.uint8, device="cuda:0")
+            o["ws"] = self.torch.empty(L.stack_workspace_bytes(ds, sp, s),
+                                       dtype=self.torch.uint8, device="cuda:0")
             self.stack_bufs[sparse] = o
         o = self.stack_bufs[sparse]
         L.bwd_stack(self.xs, self.Ws, self.caches, self.dH, sparsity=sp, dXs=o["dX"],

@@ -266,6 +266,15 @@ def _ptr_array(ts, name, dtype=None):
     return arr
 
 
+def stack_workspace_bytes(ds, sparsity: float = 0.0, s: Structure | None = None) -> int:
+    """Workspace of lstm_bwd_stack for the per-layer dims ds (list of Dims)."""
+    arr = (Dims * len(ds))(*ds)
+    n = load().lstmss_stack_workspace_bytes(len(ds), arr, float(sparsity),
+                                            ctypes.byref(s) if s is not None else None)
+    _check(0 if n >= 0 else int(n), "lstmss_stack_workspace_bytes")
+    return int(n)
+
+
 def bwd_stack(xs, Ws, caches, dH_top, sparsity=0.5, P=4, R=8, kind=COARSE, My=0, Mx=0,
               dXs=None, dWs=None, dbs=None, idxs=None, ws=None, want_dX0=False, stream=None):
     """Wavefront backward of a layer stack (layer 0 at the bottom): per-layer
@@ -292,9 +301,7 @@ def bwd_stack(xs, Ws, caches, dH_top, sparsity=0.5, P=4, R=8, kind=COARSE, My=0,
         idxs = [torch.empty((T, index_entries(ds[l], sp, s)), dtype=torch.int32, device=dev)
                 for l in range(n)]
     if ws is None:
-        nb = load().lstmss_stack_workspace_bytes(n, ds, sp, ctypes.byref(s) if s else None)
-        _check(0 if nb >= 0 else int(nb), "lstmss_stack_workspace_bytes")
-        ws = torch.empty(int(nb), dtype=torch.uint8, device=dev)
+        ws = torch.empty(stack_workspace_bytes(list(ds), sp, s), dtype=torch.uint8, device=dev)
     rc = load().lstm_bwd_stack(
         n, ds, sp, ctypes.byref(s) if s else None, _ptr_array(xs, "x", st),
         _ptr_array(Ws, "W", st), _ptr_array(caches, "cache", torch.uint8),

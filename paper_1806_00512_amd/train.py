@@ -9,14 +9,13 @@ One training step here:
   forward of every layer (bottom first) into its backward cache,
   loss gradient at the top (synthetic regression target; see
   lstmss_mse_grad),
-  backward of every layer, top first (a layer's input gradient is the
-  upstream gradient of the layer below; the bottom layer's input gradient is
-  not formed),
+  backward of every layer as one wavefront stack call (lstm_bwd_stack: a
+  layer's input gradient is the upstream gradient of the layer below, the
+  layers overlap in time; the bottom layer's input gradient is not formed),
   SGD update of every layer's W and b.
 
 Every step runs in liblstmss kernels through the C ABI; this module holds the
-buffers and the schedule.  All buffers are allocated once, so the backward
-calls replay their recorded HIP graphs from the second step on.
+buffers and the schedule.  All buffers are allocated once.
 """
 from __future__ import annotations
 
@@ -72,7 +71,7 @@ class StackTrainer:
         T, B, H = cfg.steps, cfg.batch, cfg.hidden
         f32 = torch.float32
         self.caches, self.fws, self.houts = [], [], []
-        self.sp_ws, self.dn_ws, self.outs, self.idx = [], [], [], []
+        self.outs, self.idx, ds = [], [], []
         skw = cfg.structure_kw()
         self.structure = L.structure(**skw)
         for l in range(cfg.layers):
@@ -83,19 +82,18 @@ class StackTrainer:
             self.caches.append(torch.empty(L.cache_bytes(d), dtype=torch.uint8, device=dev))
             self.fws.append(torch.empty(L.fwd_workspace_bytes(d), dtype=torch.uint8, device=dev))
             self.houts.append(torch.empty((T, H, B), dtype=cfg.dtype, device=dev))
-            self.sp_ws.append(torch.empty(L.workspace_bytes(d, cfg.sparsity, self.structure),
-                                          dtype=torch.uint8, device=dev))
-            self.dn_ws.append(torch.empty(L.workspace_bytes(d, 0.0, None), dtype=torch.uint8,
-                                          device=dev))
+            ds.append(d)
             o = {"dW": torch.empty((4 * H, I + H), dtype=f32, device=dev),
-                 "db": torch.empty(4 * H, dtype=f32, device=dev),
-                 "dh0": torch.empty((H, B), dtype=f32, device=dev),
-                 "dc0": torch.empty((H, B), dtype=f32, device=dev)}
+                 "db": torch.empty(4 * H, dtype=f32, device=dev)}
             if l > 0:
                 o["dX"] = torch.empty((T, I, B), dtype=f32, device=dev)
             self.outs.append(o)
             self.idx.append(torch.empty((T, L.index_entries(d, cfg.sparsity, self.structure)),
                                         dtype=torch.int32, device=dev))
+        self.sp_ws = torch.empty(L.stack_workspace_bytes(ds, cfg.sparsity, self.structure),
+                                 dtype=torch.uint8, device=dev)
+        self.dn_ws = torch.empty(L.stack_workspace_bytes(ds, 0.0, None), dtype=torch.uint8,
+                                 device=dev)
         self.dH = torch.empty((T, H, B), dtype=f32, device=dev)
         self.loss = torch.empty(L.LOSS_SLOTS, dtype=torch.float64, device=dev)
 
@@ -112,20 +110,12 @@ class StackTrainer:
         cfg = self.cfg
         top = self.forward(x)
         L.mse_grad(top, y, dH=self.dH, loss=self.loss)
-        up = self.dH
-        for l in reversed(range(cfg.layers)):
-            xin = x if l == 0 else self.houts[l - 1]
-            o = self.outs[l]
-            if sparse:
-                o["idx"] = self.idx[l]
-                r = L.bwd_structsparse(xin, self.Ws[l], self.caches[l], up,
-                                       sparsity=cfg.sparsity, want_dX=l > 0, out=o,
-                                       ws=self.sp_ws[l], **cfg.structure_kw())
-            else:
-                o.pop("idx", None)
-                r = L.bwd_dense(xin, self.Ws[l], self.caches[l], up, want_dX=l > 0, out=o,
-                                ws=self.dn_ws[l])
-            up = r.get("dX")
+        xs = [x] + self.houts[:-1]
+        L.bwd_stack(xs, self.Ws, self.caches, self.dH,
+                    sparsity=cfg.sparsity if sparse else 0.0,
+                    dXs=[o.get("dX") for o in self.outs], dWs=[o["dW"] for o in self.outs],
+                    dbs=[o["db"] for o in self.outs], idxs=self.idx if sparse else None,
+                    ws=self.sp_ws if sparse else self.dn_ws, **cfg.structure_kw())
         for l in range(cfg.layers):
             L.sgd_update(self.Ws[l], self.bs[l], self.outs[l]["dW"], self.outs[l]["db"], cfg.lr,
                          cfg.layer_input(l))
