@@ -383,7 +383,11 @@ def measure(L, torch, wl, sparsity, steps, warmup, sparse_only=False, kernels=Tr
     res["fwd_fused_ms"] = r.forward_timed(1, 0, batched=False)
     print("%s forward: %.4f ms (fused per-step kernel %.4f ms)" % (
         wl.name, res["fwd_ms"], res["fwd_fused_ms"]), file=sys.stderr, flush=True)
-    # per-kernel HIP-event timing pass (same number of sparse steps)
+    # per-kernel HIP-event timing pass (same number of sparse steps, the
+    # layers called in turn so that kernels do not overlap); a short spin
+    # kernel before and after marks the pass in kernel traces
+    torch.cuda.synchronize()
+    torch.cuda._sleep(1000)
     L.timing_reset()
     L.timing_enable(True)
     for _ in range(steps):
@@ -392,6 +396,8 @@ def measure(L, torch, wl, sparsity, steps, warmup, sparse_only=False, kernels=Tr
     res["kt"] = L.timing_read()
     L.timing_enable(False)
     L.timing_reset()
+    torch.cuda._sleep(1000)
+    torch.cuda.synchronize()
     if fine is not None:
         # fine-grained structure: My x Mx blocks, K = sparsity * nb per slice
         r.set_structure(kind=L.FINE, My=fine[0], Mx=fine[1])

@@ -576,9 +576,12 @@ __global__ __launch_bounds__(THREADS, 2) void wgrad_kernel(WgradArgs a) {
         xbb[i] = bb;
     }
     int ridx[2] = {-1, -1};
+    // steps run from t_end - 1 down to t_begin, and the launches of one call
+    // go down in time too, so every row of dW sums its steps in one order
+    // however the steps are split over launches
     auto load = [&](int it, int set) {
         const int tl = it / nbc, b0 = (it - tl * nbc) * BC;
-        const int t = a.t_begin + tl;
+        const int t = a.t_end - 1 - tl;
         const TS *Gt = Gc + (long)t * a.Kp * B + b0;
         const TS *xt = x + (long)t * I * B + b0;
         const TS *ht = h + (long)t * H * B + b0;
@@ -636,6 +639,27 @@ __global__ __launch_bounds__(THREADS, 2) void wgrad_kernel(WgradArgs a) {
 #pragma unroll
             for (int v = 0; v < 16; ++v)
                 tmp[ft][j][v] = 0.f;
+    }
+    // a later launch of the same call continues the sums of the earlier ones
+    // from the stored dW (the same fp32 additions as one launch)
+    if (a.accumulate) {
+#pragma unroll
+        for (int at = 0; at < ATN; ++at) {
+            if (at >= AT)
+                break;
+            const int col = at * 32 + (lane & 31);
+            if (col >= rcount)
+                continue;
+            const float *src = a.dW + (long)(r0 + col) * NC;
+#pragma unroll
+            for (int ft = 0; ft < WG_FT; ++ft)
+#pragma unroll
+                for (int v = 0; v < 16; ++v) {
+                    const int f = n0 + fh * 64 + ft * 32 + acc_row(lane, v);
+                    if (f < NC)
+                        acc[ft][at][v] = src[f];
+                }
+        }
     }
 
     load(0, 0);
@@ -784,7 +808,7 @@ __global__ __launch_bounds__(THREADS, 2) void wgrad_kernel(WgradArgs a) {
             for (int v = 0; v < 16; ++v) {
                 const int f = n0 + fh * 64 + ft * 32 + acc_row(lane, v);
                 if (f < NC)
-                    dst[f] = a.accumulate ? dst[f] + acc[ft][at][v] : acc[ft][at][v];
+                    dst[f] = acc[ft][at][v];
             }
     }
 }

@@ -92,7 +92,7 @@ struct WgradArgs {
     int greg;              // regions per work-group group (sparse)
     int BC;                // batch columns staged per iteration
     int t_begin, t_end;    // time steps [t_begin, t_end) of this launch
-    int accumulate;        // 0: dW = sum; 1: dW += sum
+    int accumulate;        // 0: dW = sum; 1: dW += sum, continuing from the stored dW
     float *dW;             // [4H][I+H]
 };
 

@@ -458,7 +458,10 @@ int32_t backward_enqueue(const lstmss_dims *d, bool dense, const Plan &p, const 
     // once its lowest step has its gate gradients
     int chunk_len = T, dx_len = T, dx_tm = 0, dx_tn = 0;
     if (use_side) {
-        const int nchunks = std::max(1, std::min(kMaxWgradChunks, T / 8));
+        // in order on the main stream one weight-gradient launch covers the
+        // whole call (dW written once); on the side stream chunks of steps
+        // start as soon as their gate gradients exist
+        const int nchunks = concurrent ? std::max(1, std::min(kMaxWgradChunks, T / 8)) : 1;
         chunk_len = (int)ceil_div(T, nchunks);
         if (dX)
             dx_len = dx_chunk_len(d, chunk_len, &dx_tm, &dx_tn);
