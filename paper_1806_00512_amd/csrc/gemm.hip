@@ -100,26 +100,27 @@ struct Vec<bf16_t, false> {
 // same for both operands.
 // --------------------------------------------------------------------------
 
-template <typename TS, int TM, int TN>
+template <typename TS, int TM, int TN, int NW = 4>
 struct G1Shape {
     static constexpr bool BF = sizeof(TS) == 2;
     static constexpr int TK = BF ? 64 : 32;         // k rows per stage
     static constexpr int KB = 4;                    // k rows per staging group
-    static constexpr int WM = TN == 32 ? 4 : 2;     // wavefront grid
-    static constexpr int WN = 4 / WM;
+    static constexpr int WM = NW == 8 ? 4 : (TN == 32 ? 4 : 2);  // wavefront grid
+    static constexpr int WN = NW / WM;
     static constexpr int MT = TM / WM / 32, NT = TN / WN / 32;  // MFMA tiles per wavefront
     static constexpr int LDK = TK + (BF ? 8 : 4);   // LDS row pitch (144 bytes)
-    static_assert(MT >= 1 && NT >= 1, "tile too small for four wavefronts");
+    static_assert(MT >= 1 && NT >= 1, "tile too small for its wavefronts");
     static_assert(GEMM1_TK % TK == 0 && GEMM1_KC_MAX % TK == 0, "stage must divide the split granularity");
 };
 
 // ROWA: the forward products a = W[:, kcol0 : kcol0 + Kp] G instead, whose
 // first operand arrives row-major with k contiguous: a thread stages KB rows
 // x VW consecutive k and stores each row's vector as it is.
-template <typename TS, int TM, int TN, bool GATHER, bool VEC, bool ROWA = false>
-__global__ __launch_bounds__(THREADS) void gemm1_kernel(Gemm1Args a) {
+template <typename TS, int TM, int TN, bool GATHER, bool VEC, bool ROWA = false, int NW = 4>
+__global__ __launch_bounds__(NW * 64) void gemm1_kernel(Gemm1Args a) {
     static_assert(!(ROWA && GATHER), "the forward products read every row");
-    using SH = G1Shape<TS, TM, TN>;
+    constexpr int THREADS = NW * 64;  // shadows the file-wide default
+    using SH = G1Shape<TS, TM, TN, NW>;
     constexpr bool BF = SH::BF;
     constexpr int TK = SH::TK, KB = SH::KB, MT = SH::MT, NT = SH::NT, WM = SH::WM, LDK = SH::LDK;
     using E = typename std::conditional<BF, uint16_t, float>::type;
@@ -1000,6 +1001,27 @@ int gemm1_wgs_per_cu(int tm, int tn) {
     return (int)std::max(1L, (160L * 1024) / lds);
 }
 
+template <typename TS, int TM, int TN, bool GA, bool VE, bool ROWA = false>
+static void launch_g1(dim3 grid, const Gemm1Args &a, bool w8, hipStream_t s) {
+    if constexpr (TM == 128 && TN == 128) {
+        if (w8) {
+            hipLaunchKernelGGL((gemm1_kernel<TS, TM, TN, GA, VE, ROWA, 8>), grid, dim3(512), 0, s, a);
+            return;
+        }
+    }
+    hipLaunchKernelGGL((gemm1_kernel<TS, TM, TN, GA, VE, ROWA>), grid, dim3(THREADS), 0, s, a);
+}
+
+// Wavefronts per work-group: 128 x 128 bf16 tiles run eight (two per SIMD
+// per work-group; bf16 MFMAs finish 8x faster per staged byte than fp32, so
+// they need more wavefronts to cover load latency: measured 1.35-1.5x on the
+// H = 4096, B = 256 products), everything else four, unless a.waves says.
+static bool use_w8(const Gemm1Args &a, bool bf16, int TM, int TN) {
+    if (TM != 128 || TN != 128)
+        return false;
+    return a.waves == 8 || (a.waves == 0 && bf16);
+}
+
 hipError_t launch_gemm1(Gemm1Args a, bool bf16, hipStream_t s) {
     if (a.k_chunk % GEMM1_TK != 0 || a.splitk < 1 || a.steps < 1)
         return hipErrorInvalidValue;
@@ -1019,7 +1041,10 @@ hipError_t launch_gemm1(Gemm1Args a, bool bf16, hipStream_t s) {
         return hipErrorInvalidValue;
     dim3 grid((unsigned)ceil_div(a.M - a.m_lo, TM), (unsigned)ceil_div(a.N, TN), (unsigned)z);
     const bool gather = a.idx != nullptr;
-#define LSTMSS_G1(TS, TMV, TNV, GA, VE) hipLaunchKernelGGL((gemm1_kernel<TS, TMV, TNV, GA, VE>), grid, dim3(THREADS), 0, s, a)
+    if (a.waves != 0 && a.waves != 4 && !(a.waves == 8 && TM == 128 && TN == 128))
+        return hipErrorInvalidValue;
+    const bool w8 = use_w8(a, bf16, TM, TN);
+#define LSTMSS_G1(TS, TMV, TNV, GA, VE) launch_g1<TS, TMV, TNV, GA, VE>(grid, a, w8, s)
 #define LSTMSS_G1V(TS, TMV, TNV, GA) do { if (vec) LSTMSS_G1(TS, TMV, TNV, GA, true); else LSTMSS_G1(TS, TMV, TNV, GA, false); } while (0)
 #define LSTMSS_G1T(TS, GA) do { \
         if (TN == 32) LSTMSS_G1V(TS, 128, 32, GA); \
@@ -1049,7 +1074,10 @@ hipError_t launch_gemm_fwd(Gemm1Args a, bool bf16, hipStream_t s) {
     if (!((TN == 32 && TM == 128) || ((TN == 64 || TN == 128) && (TM == 64 || TM == 128))))
         return hipErrorInvalidValue;
     dim3 grid((unsigned)ceil_div(a.M, TM), (unsigned)ceil_div(a.N, TN), (unsigned)z);
-#define LSTMSS_GF(TS, TMV, TNV, VE) hipLaunchKernelGGL((gemm1_kernel<TS, TMV, TNV, false, VE, true>), grid, dim3(THREADS), 0, s, a)
+    if (a.waves != 0 && a.waves != 4 && !(a.waves == 8 && TM == 128 && TN == 128))
+        return hipErrorInvalidValue;
+    const bool w8 = use_w8(a, bf16, TM, TN);
+#define LSTMSS_GF(TS, TMV, TNV, VE) launch_g1<TS, TMV, TNV, false, VE, true>(grid, a, w8, s)
 #define LSTMSS_GFV(TS, TMV, TNV) do { if (vec) LSTMSS_GF(TS, TMV, TNV, true); else LSTMSS_GF(TS, TMV, TNV, false); } while (0)
 #define LSTMSS_GFT(TS) do { \
         if (TN == 32) LSTMSS_GFV(TS, 128, 32); \

@@ -64,6 +64,7 @@ struct Gemm1Args {
     long gc_step, idx_step, out_step;
     int tm, tn;            // tile rows / columns, 0 = chosen by the launcher
     int kcol0;             // launch_gemm_fwd only: first W column of the product
+    int waves;             // wavefronts per work-group: 0 or 4, or 8 for 128-row tiles
 };
 
 // Weight gradient dW[rows] += dG_c [x_t; h_{t-1}]^T (rows scattered by idx).
