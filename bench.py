@@ -60,6 +60,8 @@ def parse():
     ap.add_argument("--serial", action="store_true",
                     help="run the weight/input-gradient work in order on the main stream "
                          "(isolated per-kernel durations) instead of on the side stream")
+    ap.add_argument("--no-bidir", action="store_true",
+                    help="skip the bidirectional-layer measurement")
     ap.add_argument("--no-train", action="store_true",
                     help="skip the whole-training-step measurement")
     ap.add_argument("--no-fine", action="store_true",
@@ -455,6 +457,68 @@ def measure_training(L, torch, wl, sparsity, steps):
     return res
 
 
+def measure_bidir(L, torch, wl, sparsity, steps):
+    """Backward of a bidirectional layer of the workload's bottom-layer shape
+    (both directions concurrently in lstm_bwd_bidir) vs the two directions'
+    calls one after the other; sparse and dense.  Mean ms per layer call."""
+    from paper_1806_00512_amd.inputs import make_inputs
+    dev = torch.device("cuda:0")
+    st = torch.bfloat16 if wl.dtype == "bf16" else torch.float32
+    inp = make_inputs(wl, seed=0)
+    x = torch.from_numpy(inp["x"]).to(dev).to(st)
+    W0 = torch.from_numpy(inp["Ws"][0]).to(dev).to(st)
+    Wr = torch.flip(W0, dims=[1]).contiguous()   # a second weight matrix of the same shape
+    del inp
+    x_rev = L.time_reverse(x)
+    _, cf = L.fwd_cache(x, W0)
+    _, cr = L.fwd_cache(x_rev, Wr)
+    g = torch.Generator(device="cpu").manual_seed(2)
+    dH = (torch.randn((wl.steps, 2 * wl.hidden, wl.batch), generator=g) * wl.up_std).to(dev)
+    dHf = dH[:, :wl.hidden].contiguous()
+    dHr = torch.flip(dH[:, wl.hidden:], dims=[0]).contiguous()
+    res = {}
+
+    def tm(f, K):
+        f()
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        for _ in range(K):
+            f()
+        e1.record()
+        torch.cuda.synchronize()
+        return e0.elapsed_time(e1) / K
+
+    for name, sp in (("sparse", sparsity), ("dense", 0.0)):
+        o = L.bwd_bidir(x, x_rev, W0, Wr, cf, cr, dH, sparsity=sp, P=wl.P, R=wl.R)
+        d = L.dims(wl.steps, wl.batch, wl.input_size, wl.hidden, st)
+        s = L.structure(wl.P, wl.R) if sp > 0 else None
+        import ctypes
+        n = L.load().lstmss_bidir_workspace_bytes(ctypes.byref(d), float(sp),
+                                                  ctypes.byref(s) if s is not None else None)
+        ws = torch.empty(int(n), dtype=torch.uint8, device=dev)
+        res[name] = tm(lambda: L.bwd_bidir(x, x_rev, W0, Wr, cf, cr, dH, sparsity=sp, P=wl.P,
+                                           R=wl.R, out=o, ws=ws), steps)
+        outs = []
+        for xx, W, cc, up in ((x, W0, cf, dHf), (x_rev, Wr, cr, dHr)):
+            wsd = torch.empty(L.workspace_bytes(d, sp, s), dtype=torch.uint8, device=dev)
+            od = (L.bwd_structsparse(xx, W, cc, up, sparsity=sp, P=wl.P, R=wl.R, ws=wsd)
+                  if sp > 0 else L.bwd_dense(xx, W, cc, up, ws=wsd))
+            outs.append((xx, W, cc, up, wsd, od))
+
+        def seq():
+            for xx, W, cc, up, wsd, od in outs:
+                if sp > 0:
+                    L.bwd_structsparse(xx, W, cc, up, sparsity=sp, P=wl.P, R=wl.R, ws=wsd, out=od)
+                else:
+                    L.bwd_dense(xx, W, cc, up, ws=wsd, out=od)
+        res[name + "_directions_in_turn"] = tm(seq, steps)
+    print("%s bidirectional bottom layer: sparse %.3f ms (directions in turn %.3f), dense %.3f "
+          "(%.3f)" % (wl.name, res["sparse"], res["sparse_directions_in_turn"], res["dense"],
+                      res["dense_directions_in_turn"]), file=sys.stderr, flush=True)
+    return res
+
+
 def main():
     args = parse()
     if args.gpus != 1:
@@ -588,6 +652,14 @@ def main():
             "note": "whole training step: forward of every layer, loss gradient, backward of "
                     "every layer (no input gradient for the bottom layer), SGD; synthetic "
                     "regression target"}
+    if not args.no_bidir:
+        bd = measure_bidir(L, torch, wl, sparsity, args.steps)
+        result["bidirectional"] = {
+            "ms_per_layer_call": {k: round(v, 5) for k, v in bd.items()},
+            "speedup_vs_dense": round(bd["dense"] / bd["sparse"], 4),
+            "note": "backward of one bidirectional layer of the bottom layer's shape (both "
+                    "directions concurrently, lstm_bwd_bidir) vs the two directions' calls in "
+                    "turn"}
     if fine is not None:
         nb = -(-wl.batch // fine[0])
         fk = {}

@@ -212,6 +212,39 @@ int32_t lstm_bwd_stack(int32_t layers, const lstmss_dims *d, float sparsity,
                        float *const *dW, float *const *db, int32_t *const *idx_out, void *ws,
                        size_t ws_bytes, void *stream);
 
+/* Bidirectional layer (section 4: the NMT encoder's first layer).  A
+ * forward-direction LSTM runs over x_1..x_T and a reverse-direction LSTM,
+ * with its own W, over x_T..x_1; the layer's output at time t is
+ * [h_fwd_t; h_rev_t] (2H rows).  The reverse direction is an ordinary layer
+ * on the time-reversed input x_rev (lstmss_time_reverse, then
+ * lstm_fwd_cache), so its cache is in its own processing order.
+ * lstmss_time_reverse: dst[s] = src[T-1-s] for T steps of step_bytes bytes
+ *   (a positive multiple of 4); src and dst must not overlap.
+ * lstmss_bidir_join: out [T][2H][B] dtype, out[t] = [h_fwd[t]; h_rev[T-1-t]]
+ *   from the two directions' h_out ([T][H][B] dtype each).
+ * lstm_bwd_bidir: the backward pass of both directions, run concurrently on
+ *   library-owned streams (enqueued directly, not recorded into a graph).
+ *   dH_up [T][2H][B] fp32 is the layer's upstream gradient in time order;
+ *   dX [T][I][B] fp32 (or NULL) receives dL/dx_t = the forward direction's
+ *   input gradient plus the reverse direction's, mapped back to time order;
+ *   dW_*, db_* (db may be NULL), idx_* (may be NULL; the reverse direction's
+ *   in its processing order) as for lstm_bwd_structsparse (s NULL or
+ *   sparsity 0: dense) for each direction; results equal that call made per
+ *   direction on the split upstream gradient.
+ *   ws: lstmss_bidir_workspace_bytes(d, sparsity, s) bytes. */
+int32_t lstmss_time_reverse(int32_t T, int64_t step_bytes, const void *src, void *dst,
+                            void *stream);
+int32_t lstmss_bidir_join(const lstmss_dims *d, const void *h_fwd, const void *h_rev, void *out,
+                          void *stream);
+int64_t lstmss_bidir_workspace_bytes(const lstmss_dims *d, float sparsity,
+                                     const lstmss_structure *s);
+int32_t lstm_bwd_bidir(const lstmss_dims *d, float sparsity, const lstmss_structure *s,
+                       const void *x, const void *x_rev, const void *W_fwd, const void *W_rev,
+                       const void *cache_fwd, const void *cache_rev, const float *dH_up, float *dX,
+                       float *dW_fwd, float *dW_rev, float *db_fwd, float *db_rev,
+                       int32_t *idx_fwd, int32_t *idx_rev, void *ws, size_t ws_bytes,
+                       void *stream);
+
 /* Training step pieces around the backward pass (section 4: SGD with a
  * fixed learning rate; section 5: dense-after-sparse schedules).
  * lstmss_sgd_update: W <- W - lr dW (formed in fp32, stored in dtype,

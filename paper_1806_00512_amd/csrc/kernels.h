@@ -153,6 +153,16 @@ hipError_t launch_sgd(void *W, const float *dW, long nw, float *b, const float *
                       float lr, bool bf16, hipStream_t s);
 hipError_t launch_mse(const void *h, const float *y, float *dH, long n, float inv_b,
                       double *parts, int nparts, bool bf16, hipStream_t s);
+// Bidirectional layer edges (time reversal of the reverse direction):
+// dst[s] = src[T-1-s] over steps of `words` 4-byte words; out[t] =
+// [hf[t]; hr[T-1-t]] ([T][2H][B]); df[t] = dH[t][:H], dr[T-1-t] = dH[t][H:];
+// out[t] = a[t] + b[T-1-t] ([T][I][B]).
+hipError_t launch_reverse(const void *src, void *dst, int T, long words, hipStream_t s);
+hipError_t launch_bidir_join(const void *hf, const void *hr, void *out, int T, long HB, bool bf16,
+                             hipStream_t s);
+hipError_t launch_bidir_split(const float *dH, float *df, float *dr, int T, long HB, hipStream_t s);
+hipError_t launch_sum_rev(const float *a, const float *b, float *out, int T, long IB,
+                          hipStream_t s);
 // Returns hipErrorNotSupported when the structure needs more routing tiles
 // than the batched kernel holds (the caller then uses launch_gemm2 per step).
 hipError_t launch_wgrad(WgradArgs a, bool sparse, bool bf16, hipStream_t s);

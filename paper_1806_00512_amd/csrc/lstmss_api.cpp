@@ -760,9 +760,140 @@ int32_t stack_enqueue(int32_t layers, const lstmss_dims *d, const StackPlan &sp,
     return LSTMSS_OK;
 }
 
+struct BidirLayout {
+    size_t ws_f, ws_r, dh_f, dh_r, dx_f, dx_r, total;
+};
+
+BidirLayout bidir_layout(const lstmss_dims *d, const Plan &p) {
+    BidirLayout B;
+    const size_t one = align256(ws_layout(d, p).total);
+    const size_t hb = align256((size_t)d->T * d->H * d->B * 4);
+    const size_t ib = align256((size_t)d->T * d->I * d->B * 4);
+    B.ws_f = 0;
+    B.ws_r = one;
+    B.dh_f = 2 * one;
+    B.dh_r = B.dh_f + hb;
+    B.dx_f = B.dh_r + hb;
+    B.dx_r = B.dx_f + ib;
+    B.total = B.dx_r + ib;
+    return B;
+}
+
+// Both directions of a bidirectional layer on their own stream pairs; the
+// upstream gradient is split (the reverse half reversed in time) first and
+// the input gradients are summed (the reverse one reversed back) last.
+int32_t bidir_enqueue(const lstmss_dims *d, bool dense, const Plan &p, const void *x,
+                      const void *x_rev, const void *W_f, const void *W_r, const void *cache_f,
+                      const void *cache_r, const float *dH_up, float *dX, float *dW_f,
+                      float *dW_r, float *db_f, float *db_r, int32_t *idx_f, int32_t *idx_r,
+                      void *ws, hipStream_t origin, StackRes &R) {
+    const BidirLayout Lb = bidir_layout(d, p);
+    char *wb = (char *)ws;
+    float *dh_f = (float *)(wb + Lb.dh_f), *dh_r = (float *)(wb + Lb.dh_r);
+    float *dx_f = dX ? (float *)(wb + Lb.dx_f) : nullptr;
+    float *dx_r = dX ? (float *)(wb + Lb.dx_r) : nullptr;
+    const long HB = (long)d->H * d->B, IB = (long)d->I * d->B;
+    HIP_TRY(timed(LSTMSS_KERNEL_AUX, origin, [&] {
+        return launch_bidir_split(dH_up, dh_f, dh_r, d->T, HB, origin);
+    }));
+    HIP_TRY(hipEventRecord(R.fork, origin));
+    for (int dir = 0; dir < 2; ++dir) {
+        hipStream_t ms = R.main[dir];
+        HIP_TRY(hipStreamWaitEvent(ms, R.fork, 0));
+        EnqCtx ctx;
+        ctx.side = R.side[dir];
+        ctx.ring = R.ring[dir];
+        ctx.nring = kForkEvents;
+        ctx.join = R.join[dir];
+        const int32_t rc =
+            dir == 0 ? backward_enqueue(d, dense, p, x, W_f, cache_f, dh_f, nullptr, nullptr, dx_f,
+                                        dW_f, db_f, nullptr, nullptr, idx_f, nullptr,
+                                        wb + Lb.ws_f, ms, ctx)
+                     : backward_enqueue(d, dense, p, x_rev, W_r, cache_r, dh_r, nullptr, nullptr,
+                                        dx_r, dW_r, db_r, nullptr, nullptr, idx_r, nullptr,
+                                        wb + Lb.ws_r, ms, ctx);
+        if (rc != LSTMSS_OK)
+            return rc;
+        HIP_TRY(hipEventRecord(R.done[dir], ms));
+        HIP_TRY(hipStreamWaitEvent(origin, R.done[dir], 0));
+    }
+    if (dX)
+        HIP_TRY(timed(LSTMSS_KERNEL_AUX, origin, [&] {
+            return launch_sum_rev(dx_f, dx_r, dX, d->T, IB, origin);
+        }));
+    return LSTMSS_OK;
+}
+
 } // namespace
 
 extern "C" {
+
+int32_t lstmss_time_reverse(int32_t T, int64_t step_bytes, const void *src, void *dst,
+                            void *stream) {
+    if (T < 1 || step_bytes <= 0 || step_bytes % 4 != 0)
+        return fail(LSTMSS_ERR_INVALID_ARG, "T=%d, step_bytes=%lld (a positive multiple of 4)",
+                    T, (long long)step_bytes);
+    if (!src || !dst || src == dst)
+        return fail(LSTMSS_ERR_INVALID_ARG, "src and dst must be distinct non-NULL buffers");
+    hipStream_t st = (hipStream_t)stream;
+    HIP_TRY(timed(LSTMSS_KERNEL_AUX, st, [&] { return launch_reverse(src, dst, T, step_bytes / 4, st); }));
+    return LSTMSS_OK;
+}
+
+int32_t lstmss_bidir_join(const lstmss_dims *d, const void *h_fwd, const void *h_rev, void *out,
+                          void *stream) {
+    int32_t rc = check_dims(d);
+    if (rc)
+        return rc;
+    if (!h_fwd || !h_rev || !out)
+        return fail(LSTMSS_ERR_INVALID_ARG, "a required pointer is NULL");
+    hipStream_t st = (hipStream_t)stream;
+    HIP_TRY(timed(LSTMSS_KERNEL_AUX, st, [&] {
+        return launch_bidir_join(h_fwd, h_rev, out, d->T, (long)d->H * d->B,
+                                 d->dtype == LSTMSS_BF16, st);
+    }));
+    return LSTMSS_OK;
+}
+
+int64_t lstmss_bidir_workspace_bytes(const lstmss_dims *d, float sparsity,
+                                     const lstmss_structure *s) {
+    int32_t rc = check_dims(d);
+    if (rc)
+        return rc;
+    Plan p;
+    rc = make_plan(d, sparsity, s, s == nullptr || sparsity == 0.f, &p);
+    if (rc)
+        return rc;
+    return (int64_t)bidir_layout(d, p).total;
+}
+
+int32_t lstm_bwd_bidir(const lstmss_dims *d, float sparsity, const lstmss_structure *s,
+                       const void *x, const void *x_rev, const void *W_fwd, const void *W_rev,
+                       const void *cache_fwd, const void *cache_rev, const float *dH_up, float *dX,
+                       float *dW_fwd, float *dW_rev, float *db_fwd, float *db_rev,
+                       int32_t *idx_fwd, int32_t *idx_rev, void *ws, size_t ws_bytes,
+                       void *stream) {
+    int32_t rc = check_dims(d);
+    if (rc)
+        return rc;
+    const bool dense = s == nullptr || sparsity == 0.f;
+    Plan p;
+    rc = make_plan(d, sparsity, s, dense, &p);
+    if (rc)
+        return rc;
+    if (!x || !x_rev || !W_fwd || !W_rev || !cache_fwd || !cache_rev || !dH_up || !dW_fwd ||
+        !dW_rev || !ws)
+        return fail(LSTMSS_ERR_INVALID_ARG, "a required pointer is NULL");
+    const BidirLayout Lb = bidir_layout(d, p);
+    if (ws_bytes < Lb.total)
+        return fail(LSTMSS_ERR_WORKSPACE, "workspace of %zu bytes, need %zu", ws_bytes, Lb.total);
+    StackRes *R = nullptr;
+    HIP_TRY(stack_res(&R));
+    std::unique_lock<std::mutex> lk(R->mu);
+    return bidir_enqueue(d, dense, p, x, x_rev, W_fwd, W_rev, cache_fwd, cache_rev, dH_up, dX,
+                         dW_fwd, dW_rev, db_fwd, db_rev, idx_fwd, idx_rev, ws, (hipStream_t)stream,
+                         *R);
+}
 
 int64_t lstmss_stack_workspace_bytes(int32_t layers, const lstmss_dims *d, float sparsity,
                                      const lstmss_structure *s) {

@@ -32,7 +32,8 @@ ERR = {0: "ok", -1: "invalid argument", -2: "unsupported", -3: "workspace too sm
 SYMBOLS = ("lstmss_version", "lstmss_strerror", "lstmss_last_error", "lstmss_cache_bytes",
            "lstmss_kept_rows", "lstmss_index_entries", "lstmss_workspace_bytes",
            "lstmss_fwd_workspace_bytes", "lstmss_sgd_update", "lstmss_mse_grad",
-           "lstmss_stack_workspace_bytes", "lstm_bwd_stack",
+           "lstmss_stack_workspace_bytes", "lstm_bwd_stack", "lstmss_time_reverse",
+           "lstmss_bidir_join", "lstmss_bidir_workspace_bytes", "lstm_bwd_bidir",
            "lstm_fwd_cache", "lstm_bwd_dense",
            "lstm_bwd_structsparse", "lstmss_select_compact", "lstmss_set_option",
            "lstmss_timing_enable", "lstmss_timing_read", "lstmss_timing_reset")
@@ -94,6 +95,14 @@ def load():
     lib.lstm_bwd_stack.argtypes = [i32, pd, f, ps, vp, vp, vp, vp, vp, vp, vp, vp, vp,
                                    ctypes.c_size_t, vp]
     lib.lstm_bwd_stack.restype = i32
+    lib.lstmss_time_reverse.argtypes = [i32, i64, vp, vp, vp]
+    lib.lstmss_time_reverse.restype = i32
+    lib.lstmss_bidir_join.argtypes = [pd, vp, vp, vp, vp]
+    lib.lstmss_bidir_join.restype = i32
+    lib.lstmss_bidir_workspace_bytes.argtypes = [pd, f, ps]
+    lib.lstmss_bidir_workspace_bytes.restype = i64
+    lib.lstm_bwd_bidir.argtypes = [pd, f, ps] + [vp] * 15 + [ctypes.c_size_t, vp]
+    lib.lstm_bwd_bidir.restype = i32
     lib.lstm_bwd_dense.argtypes = [pd, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp,
                                    ctypes.c_size_t, vp]
     lib.lstm_bwd_dense.restype = i32
@@ -310,6 +319,74 @@ def bwd_stack(xs, Ws, caches, dH_top, sparsity=0.5, P=4, R=8, kind=COARSE, My=0,
         _ptr(ws, torch.uint8, name="ws"), ws.numel(), _stream(stream))
     _check(rc, "lstm_bwd_stack")
     return {"dX": dXs, "dW": dWs, "db": dbs, "idx": idxs}
+
+
+def time_reverse(src, dst=None, stream=None):
+    """dst[s] = src[T-1-s] along the first dimension (a new tensor unless given)."""
+    if dst is None:
+        dst = torch.empty_like(src)
+    T = src.shape[0]
+    step = src[0].numel() * src.element_size()
+    rc = load().lstmss_time_reverse(int(T), int(step), _ptr(src, name="src"),
+                                    _ptr(dst, src.dtype, tuple(src.shape), "dst"), _stream(stream))
+    _check(rc, "lstmss_time_reverse")
+    return dst
+
+
+def bidir_join(h_fwd, h_rev, out=None, stream=None):
+    """[T][2H][B] output of a bidirectional layer: out[t] = [h_fwd[t]; h_rev[T-1-t]]."""
+    T, H, B = h_fwd.shape
+    d = dims(T, B, 1, H, h_fwd.dtype)
+    if out is None:
+        out = torch.empty((T, 2 * H, B), dtype=h_fwd.dtype, device=h_fwd.device)
+    rc = load().lstmss_bidir_join(ctypes.byref(d), _ptr(h_fwd, name="h_fwd"),
+                                  _ptr(h_rev, h_fwd.dtype, (T, H, B), "h_rev"),
+                                  _ptr(out, h_fwd.dtype, (T, 2 * H, B), "out"), _stream(stream))
+    _check(rc, "lstmss_bidir_join")
+    return out
+
+
+def bwd_bidir(x, x_rev, W_fwd, W_rev, cache_fwd, cache_rev, dH_up, sparsity=0.5, P=4, R=8,
+              kind=COARSE, My=0, Mx=0, want_dX=True, out=None, ws=None, stream=None):
+    """Backward of a bidirectional layer (both directions concurrently).
+    dH_up [T][2H][B].  Returns dict(dX, dW_fwd, dW_rev, db_fwd, db_rev, idx_fwd, idx_rev)."""
+    T, I, B = x.shape
+    H = W_fwd.shape[0] // 4
+    st = x.dtype
+    dev = x.device
+    f32 = torch.float32
+    d = dims(T, B, I, H, st)
+    s = structure(P, R, kind, My, Mx) if sparsity > 0 else None
+    o = dict(out or {})
+    for k, shape, dt in (("dW_fwd", (4 * H, I + H), f32), ("dW_rev", (4 * H, I + H), f32),
+                         ("db_fwd", (4 * H,), f32), ("db_rev", (4 * H,), f32)):
+        if o.get(k) is None:
+            o[k] = torch.empty(shape, dtype=dt, device=dev)
+    if want_dX and o.get("dX") is None:
+        o["dX"] = torch.empty((T, I, B), dtype=f32, device=dev)
+    if s is not None:
+        ne = index_entries(d, sparsity, s)
+        for k in ("idx_fwd", "idx_rev"):
+            if o.get(k) is None:
+                o[k] = torch.empty((T, ne), dtype=torch.int32, device=dev)
+    if ws is None:
+        n = load().lstmss_bidir_workspace_bytes(ctypes.byref(d), float(sparsity),
+                                                ctypes.byref(s) if s is not None else None)
+        _check(0 if n >= 0 else int(n), "lstmss_bidir_workspace_bytes")
+        ws = torch.empty(int(n), dtype=torch.uint8, device=dev)
+    rc = load().lstm_bwd_bidir(
+        ctypes.byref(d), float(sparsity), ctypes.byref(s) if s is not None else None,
+        _ptr(x, st, name="x"), _ptr(x_rev, st, (T, I, B), "x_rev"),
+        _ptr(W_fwd, st, (4 * H, I + H), "W_fwd"), _ptr(W_rev, st, (4 * H, I + H), "W_rev"),
+        _ptr(cache_fwd, torch.uint8, name="cache_fwd"), _ptr(cache_rev, torch.uint8, name="cache_rev"),
+        _ptr(dH_up, f32, (T, 2 * H, B), "dH_up"), _ptr(o.get("dX"), f32, (T, I, B), "dX"),
+        _ptr(o["dW_fwd"], f32, name="dW_fwd"), _ptr(o["dW_rev"], f32, name="dW_rev"),
+        _ptr(o["db_fwd"], f32, name="db_fwd"), _ptr(o["db_rev"], f32, name="db_rev"),
+        _ptr(o.get("idx_fwd"), torch.int32, name="idx_fwd"),
+        _ptr(o.get("idx_rev"), torch.int32, name="idx_rev"),
+        _ptr(ws, torch.uint8, name="ws"), ws.numel(), _stream(stream))
+    _check(rc, "lstm_bwd_bidir")
+    return o
 
 
 def _bwd_outputs(T, B, I, H, dev, want_dX, out):

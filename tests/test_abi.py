@@ -163,3 +163,15 @@ def test_stack_workspace_and_validation(L):
     rc = lib.lstm_bwd_stack(2, ds, 0.5, ctypes.byref(s), null, null, null, None, null, null,
                             None, None, None, 0, None)
     assert rc == -1
+
+
+def test_bidir_host_checks(L):
+    lib = L.load()
+    assert lib.lstmss_time_reverse(0, 16, None, None, None) == -1
+    assert lib.lstmss_time_reverse(4, 6, None, None, None) == -1      # not a multiple of 4
+    d = L.dims(4, 8, 16, 32)
+    s = L.structure(4, 8)
+    n = lib.lstmss_bidir_workspace_bytes(ctypes.byref(d), 0.5, ctypes.byref(s))
+    assert n >= 2 * L.workspace_bytes(d, 0.5, s) + 2 * 4 * 32 * 8 * 4 + 2 * 4 * 16 * 8 * 4
+    rc = lib.lstm_bwd_bidir(ctypes.byref(d), 0.5, ctypes.byref(s), *([None] * 15), 0, None)
+    assert rc == -1

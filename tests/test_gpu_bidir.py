@@ -1,0 +1,110 @@
+"""GPU: a bidirectional layer (section 4, the NMT encoder's first layer).
+The reverse direction is an ordinary layer over the time-reversed input:
+time reversal and the output join are exact copies; the two directions'
+backward run concurrently in lstm_bwd_bidir and must equal the per-direction
+calls bit for bit, and the oracle (run with the GPU's masks) to rel. L2 1e-5."""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from paper_1806_00512_amd.inputs import make_layer
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module")
+def L():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    import paper_1806_00512_amd.lstmss as lstmss
+    lstmss.load()
+    return lstmss
+
+
+def rel(a, b):
+    a, b = np.asarray(a, np.float64), np.asarray(b, np.float64)
+    n = np.linalg.norm(b)
+    return float(np.linalg.norm(a - b) / (n if n > 0 else 1.0))
+
+
+def np64(t):
+    return t.detach().float().cpu().numpy().astype(np.float64)
+
+
+def keep_from_idx(idx, nslices):
+    keep = np.zeros((idx.shape[0], nslices), np.uint8)
+    for t in range(idx.shape[0]):
+        keep[t, idx[t]] = 1
+    return keep
+
+
+@pytest.mark.parametrize("dtype", [torch.float32, torch.bfloat16])
+def test_time_reverse_exact(L, dtype):
+    x = torch.randn(7, 13, 10, device="cuda:0").to(dtype)
+    y = L.time_reverse(x)
+    torch.cuda.synchronize()
+    assert torch.equal(y.cpu(), torch.flip(x.cpu(), dims=[0]))
+
+
+def setup(L, T, B, I, H, seed, dtype=torch.float32):
+    df = make_layer(T, B, I, H, seed=seed, w_scale=0.2)
+    dr = make_layer(T, B, I, H, seed=seed + 1, w_scale=0.2)
+    dev = torch.device("cuda:0")
+    x = torch.from_numpy(df["x"]).to(dev).to(dtype)
+    Wf = torch.from_numpy(df["W"]).to(dev).to(dtype)
+    Wr = torch.from_numpy(dr["W"]).to(dev).to(dtype)
+    x_rev = L.time_reverse(x)
+    hf, cf = L.fwd_cache(x, Wf)
+    hr, cr = L.fwd_cache(x_rev, Wr)
+    rng = np.random.default_rng(seed)
+    dH = torch.from_numpy(rng.standard_normal((T, 2 * H, B)).astype(np.float32)).to(dev)
+    return df, dr, x, x_rev, Wf, Wr, hf, hr, cf, cr, dH
+
+
+def test_bidir_forward_join(L):
+    T, B, I, H = 6, 20, 40, 72
+    df, dr, x, x_rev, Wf, Wr, hf, hr, cf, cr, dH = setup(L, T, B, I, H, seed=3)
+    out = L.bidir_join(hf, hr)
+    torch.cuda.synchronize()
+    _, _, h_f = oracle.forward(df["x"], df["W"])
+    _, _, h_r = oracle.forward(df["x"][::-1], dr["W"])
+    ref = np.concatenate([h_f[1:], h_r[1:][::-1]], axis=1)
+    assert rel(np64(out), ref) <= 1e-5
+    assert torch.equal(out[:, :H].cpu(), hf.cpu())
+    assert torch.equal(out[:, H:].cpu(), torch.flip(hr, dims=[0]).cpu())
+
+
+@pytest.mark.parametrize("T,B,I,H,sparsity", [(6, 20, 40, 72, 0.5), (5, 64, 96, 128, 0.25),
+                                              (4, 32, 48, 64, 0.0)])
+def test_bidir_backward(L, T, B, I, H, sparsity):
+    df, dr, x, x_rev, Wf, Wr, hf, hr, cf, cr, dH = setup(L, T, B, I, H, seed=T + H)
+    o = L.bwd_bidir(x, x_rev, Wf, Wr, cf, cr, dH, sparsity=sparsity)
+    # per-direction calls on the split upstream gradient
+    dHf = dH[:, :H].contiguous()
+    dHr = torch.flip(dH[:, H:], dims=[0]).contiguous()
+    if sparsity > 0:
+        a = L.bwd_structsparse(x, Wf, cf, dHf, sparsity=sparsity)
+        b = L.bwd_structsparse(x_rev, Wr, cr, dHr, sparsity=sparsity)
+    else:
+        a = L.bwd_dense(x, Wf, cf, dHf)
+        b = L.bwd_dense(x_rev, Wr, cr, dHr)
+    torch.cuda.synchronize()
+    assert torch.equal(o["dW_fwd"], a["dW"]) and torch.equal(o["dW_rev"], b["dW"])
+    assert torch.equal(o["db_fwd"], a["db"]) and torch.equal(o["db_rev"], b["db"])
+    assert torch.equal(o["dX"], a["dX"] + torch.flip(b["dX"], dims=[0]))
+    if sparsity > 0:
+        assert torch.equal(o["idx_fwd"], a["idx"]) and torch.equal(o["idx_rev"], b["idx"])
+    # oracle with the GPU's masks, both directions
+    P, R = 4, 8
+    S = int(round(sparsity * R))
+    res = []
+    for xs, W, dHs, idx in ((df["x"], df["W"], np64(dHf), o.get("idx_fwd")),
+                            (df["x"][::-1], dr["W"], np64(dHr), o.get("idx_rev"))):
+        gates, c, h = oracle.forward(xs, W)
+        fk = keep_from_idx(idx.cpu().numpy(), 4 * H // P) if idx is not None else None
+        res.append(oracle.backward(xs, W, gates, c, h, dHs, P=P, R=R, S=S, forced_keep=fk))
+    assert rel(np64(o["dW_fwd"]), res[0]["dW"]) <= 1e-5
+    assert rel(np64(o["dW_rev"]), res[1]["dW"]) <= 1e-5
+    assert rel(np64(o["db_rev"]), res[1]["db"]) <= 1e-5
+    assert rel(np64(o["dX"]), res[0]["dX"] + res[1]["dX"][::-1]) <= 1e-5
