@@ -400,18 +400,27 @@ def measure(L, torch, wl, sparsity, steps, warmup, sparse_only=False, kernels=Tr
     L.timing_reset()
     torch.cuda._sleep(1000)
     torch.cuda.synchronize()
-    if fine is not None:
+    for fi, (my, mx) in enumerate(fine or []):
         # fine-grained structure: My x Mx blocks, K = sparsity * nb per slice
-        r.set_structure(kind=L.FINE, My=fine[0], Mx=fine[1])
+        r.set_structure(kind=L.FINE, My=my, Mx=mx)
         fn_ms, fn_wall, _ = r.timed([True], steps, warmup, stack=True)
-        print("%s fine (My=%d, Mx=%d): %.4f ms/step" % (wl.name, fine[0], fine[1], fn_ms),
-              file=sys.stderr, flush=True)
+        print("%s fine (My=%d, Mx=%d): %.4f ms/step" % (wl.name, my, mx, fn_ms), file=sys.stderr,
+              flush=True)
+        noskip_ms = None
+        if my == 32 and mx == 32:
+            L.set_option("fine_skip", 0)   # the same call multiplying the removed blocks' zeros
+            noskip_ms, _, _ = r.timed([True], steps, warmup, stack=True)
+            L.set_option("fine_skip", 1)
+            print("%s fine (My=%d, Mx=%d) without skipping: %.4f ms/step" % (wl.name, my, mx,
+                                                                           noskip_ms),
+                  file=sys.stderr, flush=True)
         L.timing_reset()
         L.timing_enable(True)
         for _ in range(steps):
             r.step(True)
         torch.cuda.synchronize()
-        res.update(fn_ms=fn_ms, fn_wall=fn_wall, fn_kt=L.timing_read())
+        res.setdefault("fine", []).append({"My": my, "Mx": mx, "ms": fn_ms, "noskip_ms": noskip_ms,
+                                           "kt": L.timing_read()})
         L.timing_enable(False)
         L.timing_reset()
     return res
@@ -552,11 +561,18 @@ def main():
 
     fine = None if args.no_fine else (args.fine_my, args.fine_mx)
     if fine is not None:
-        nb = -(-wl.batch // fine[0])
-        if abs(sparsity * nb - round(sparsity * nb)) > 1e-6 * nb:
-            print("fine structure skipped: sparsity %g of %d blocks per slice is not a whole "
-                  "number of blocks" % (sparsity, nb), file=sys.stderr, flush=True)
-            fine = None
+        # the paper's blocks, and blocks shaped like the 32 x 32 MFMA operand
+        # blocks (their products skip the removed blocks)
+        cand = [fine] + ([(32, 32)] if tuple(fine) != (32, 32) else [])
+        fine = []
+        for my, mx in cand:
+            nb = -(-wl.batch // my)
+            if abs(sparsity * nb - round(sparsity * nb)) > 1e-6 * nb or (4 * wl.hidden) % mx:
+                print("fine structure My=%d, Mx=%d skipped: sparsity %g of %d blocks per slice "
+                      "is not a whole number of blocks, or Mx does not divide 4H"
+                      % (my, mx, sparsity, nb), file=sys.stderr, flush=True)
+                continue
+            fine.append((my, mx))
     m = measure(L, torch, wl, sparsity, args.steps, args.warmup, args.sparse_only, fine=fine)
     if args.sparse_only:
         return
@@ -660,19 +676,26 @@ def main():
             "note": "backward of one bidirectional layer of the bottom layer's shape (both "
                     "directions concurrently, lstm_bwd_bidir) vs the two directions' calls in "
                     "turn"}
-    if fine is not None:
-        nb = -(-wl.batch // fine[0])
+    for fm in m.get("fine", []):
+        nb = -(-wl.batch // fm["My"])
         fk = {}
         for name in KINDS + ("aux",):
-            ms, n = m["fn_kt"][name]
+            ms, n = fm["kt"][name]
             fk[name] = {"total_ms_per_step": round(ms / args.steps, 5), "launches": n,
                         "avg_us": round(ms / max(n, 1) * 1e3, 3)}
-        result["fine"] = {"My": fine[0], "Mx": fine[1], "blocks_per_slice": nb,
-                          "K": int(round(sparsity * nb)), "ms_per_step": round(m["fn_ms"], 5),
-                          "speedup_vs_dense": round(dn_ms / m["fn_ms"], 4),
-                          "value": round(dense_flops / (m["fn_ms"] / 1e3) / 1e12, 4),
-                          "unit": "TFLOP/s",
-                          "kernels": fk}
+        entry = {"My": fm["My"], "Mx": fm["Mx"], "blocks_per_slice": nb,
+                 "K": int(round(sparsity * nb)), "ms_per_step": round(fm["ms"], 5),
+                 "speedup_vs_dense": round(dn_ms / fm["ms"], 4),
+                 "value": round(dense_flops / (fm["ms"] / 1e3) / 1e12, 4), "unit": "TFLOP/s",
+                 "kernels": fk}
+        if fm["noskip_ms"] is not None:
+            entry["without_skipping_ms_per_step"] = round(fm["noskip_ms"], 5)
+        if (fm["My"], fm["Mx"]) == (32, 32):
+            entry["note"] = ("blocks shaped like the 32 x 32 MFMA operand blocks: the products "
+                             "skip the removed blocks")
+            result["fine_mfma_blocks"] = entry
+        else:
+            result["fine"] = entry
     if not args.no_cpu_baseline:
         result["cpu_baseline"] = cpu_baseline(wl, m["runner"].inp, sparsity)
     del m

@@ -69,12 +69,15 @@ typedef struct {
  * an integer (within 1e-6) with 0 <= S < R.  4H must be a multiple of P.
  * When 4H/P is not a multiple of R, the last region has r < R slices and
  * removes floor(S*r/R).  My, Mx are ignored.
- * FINE: a slice is Mx consecutive gate rows (Mx in 1..16 dividing 32 and
+ * FINE: a slice is Mx consecutive gate rows (Mx in 1..32 dividing 32 and
  * 4H) over the whole batch, cut into nb = ceil(B/My) blocks of My batch
  * columns (My a power of two in 2..64; the last block is narrower when My
  * does not divide B; nb <= 64, B <= 256).  In every slice the K = sparsity *
  * nb blocks of smallest L2 norm are zeroed (K an integer within 1e-6,
- * 0 <= K < nb).  P, R are ignored. */
+ * 0 <= K < nb).  P, R are ignored.  With Mx = My = 32 (blocks shaped like
+ * the 32 x 32 MFMA operand blocks), B a multiple of 32 and 4H <= 16384, the
+ * gradient products skip the removed blocks' multiplications (same results
+ * bit for bit); other block shapes run the products on the masked matrix. */
 typedef struct {
     int32_t kind;
     int32_t P, R;
@@ -279,9 +282,17 @@ int32_t lstmss_mse_grad(const lstmss_dims *d, const void *h, const float *y, flo
  *   LSTMSS_OPT_STACK_DX_STEPS  steps per input-gradient launch inside
  *                      lstm_bwd_stack, i.e. how many steps a layer lags the
  *                      layer above; 0 (default) = T/4, at least 1.
+ *   LSTMSS_OPT_FINE_SKIP  FINE with Mx = My = 32: 1 (default) skips the
+ *                      removed blocks' multiplications, 0 multiplies the
+ *                      zeros (same bits; for checking and timing).
  * Changing an option drops the recorded graphs.  Not for use while calls
  * are being enqueued from other threads. */
-enum { LSTMSS_OPT_GRAPHS = 0, LSTMSS_OPT_SIDE_STREAM = 1, LSTMSS_OPT_STACK_DX_STEPS = 2 };
+enum {
+    LSTMSS_OPT_GRAPHS = 0,
+    LSTMSS_OPT_SIDE_STREAM = 1,
+    LSTMSS_OPT_STACK_DX_STEPS = 2,
+    LSTMSS_OPT_FINE_SKIP = 3
+};
 int32_t lstmss_set_option(int32_t option, int32_t value);
 
 /* Measurement hooks (not part of the method): when enabled, every kernel the

@@ -844,6 +844,122 @@ hipError_t launch_cell_split(const CellArgs &a, int mode, bool bf16, hipStream_t
     return hipGetLastError();
 }
 
+// 32-row slices: four wavefronts per slice (eight rows each), so that the
+// few slices (4H/32) still spread over the CUs.  Per-row block sums go to
+// LDS; one thread per block folds the 32 rows in order, ranks and indexes.
+template <typename TS, int SRC>
+__global__ __launch_bounds__(256) void cell_fine32_kernel(CellArgs a) {
+    constexpr int NJ = 4, RPW = 8;
+    __shared__ double s_blk[32][64];
+    __shared__ double s_sc[64];
+    __shared__ int s_keep[64];
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int B = a.B, H = a.H, My = a.My, nb = a.nb, K = a.S;
+    const long j = blockIdx.x;  // slice
+    const long r0 = j * 32 + wave * RPW;
+    const TS *__restrict__ gates = (const TS *)a.gates;
+    const float *__restrict__ dHup = a.dH_up;
+    const float *__restrict__ ct = a.c_t;
+    const float *__restrict__ cp = a.c_prev;
+    const float *__restrict__ dcin = a.dc_in;
+    const TS *__restrict__ src = (const TS *)(SRC == FS_STAGE ? a.stage : a.dG_in);
+    TS *dbg = (TS *)a.dbg;
+
+    float vals[RPW][NJ];
+#pragma unroll
+    for (int p = 0; p < RPW; ++p) {
+        const long r = r0 + p;
+        const int g = (int)(r / H), u = (int)(r - (long)g * H);
+#pragma unroll
+        for (int jj = 0; jj < NJ; ++jj) {
+            const int b = 64 * jj + lane;
+            float val = 0.f;
+            if (b < B) {
+                if (SRC != FS_CACHE) {
+                    val = st<TS>::load(src, r * B + b);
+                } else {
+                    const int e = u * B + b;
+                    const float dh = sum_parts(dHup[e], a.dh_part + e, a.dh_nparts, a.dh_stride);
+                    const float tc = tanhf(ct[e]);
+                    const float o = st<TS>::load(gates, (long)(3 * H + u) * B + b);
+                    if (g == 3) {
+                        val = dh * tc * o * (1.f - o);
+                    } else {
+                        const float dcv = (dcin ? dcin[e] : 0.f) + dh * o * (1.f - tc * tc);
+                        if (g == 1) {
+                            const float f = st<TS>::load(gates, (long)(H + u) * B + b);
+                            a.dc_out[e] = dcv * f;
+                            val = dcv * cp[e] * f * (1.f - f);
+                        } else {
+                            const float i = st<TS>::load(gates, (long)u * B + b);
+                            const float gg = st<TS>::load(gates, (long)(2 * H + u) * B + b);
+                            val = g == 0 ? dcv * gg * i * (1.f - i) : dcv * i * (1.f - gg * gg);
+                        }
+                    }
+                    val = st<TS>::rnd(val);
+                    if (dbg)
+                        st<TS>::store(dbg, r * B + b, val);
+                }
+            }
+            vals[p][jj] = val;
+            if (64 * jj < B) {  // this row's block sums of the chunk
+                double q = (double)val * (double)val;
+                for (int off = My >> 1; off >= 1; off >>= 1)
+                    q = q + shfl_xor_f64(q, off);
+                if ((lane & (My - 1)) == 0 && (64 * jj + lane) / My < nb)
+                    s_blk[wave * RPW + p][(64 * jj + lane) / My] = q;
+            }
+        }
+    }
+    __syncthreads();
+    if (tid < nb) {  // score: the 32 rows folded in order
+        double sc = s_blk[0][tid];
+        for (int p = 1; p < 32; ++p)
+            sc = sc + s_blk[p][tid];
+        s_sc[tid] = sc;
+        if (a.scores)
+            a.scores[j * nb + tid] = sc;
+    }
+    __syncthreads();
+    if (tid < nb) {  // kept when fewer than nb - K blocks outrank it
+        const uint64_t kc = score_key(s_sc[tid]);
+        int beaten = 0;
+        for (int i = 0; i < nb; ++i)
+            if (i != tid && outranks(score_key(s_sc[i]), i, kc, tid))
+                ++beaten;
+        s_keep[tid] = beaten < nb - K ? 1 : 0;
+    }
+    __syncthreads();
+    if (tid < nb && s_keep[tid]) {
+        int pos = 0;
+        for (int i = 0; i < tid; ++i)
+            pos += s_keep[i];
+        a.idx[j * (nb - K) + pos] = tid;
+    }
+    TS *dGc = (TS *)a.dGc;
+#pragma unroll
+    for (int p = 0; p < RPW; ++p) {
+        const long r = r0 + p;
+        float rs = 0.f;
+#pragma unroll
+        for (int jj = 0; jj < NJ; ++jj) {
+            const int b = 64 * jj + lane;
+            if (b < B) {
+                const float m = s_keep[b / My] ? vals[p][jj] : 0.f;
+                st<TS>::store(dGc, r * B + b, m);
+                rs += m;
+            }
+        }
+        if (SRC != FS_GIVEN && a.db) {
+#pragma unroll
+            for (int off = 32; off >= 1; off >>= 1)
+                rs += shfl_xor_f32(rs, off);
+            if (lane == 0)
+                a.db[r] += rs;
+        }
+    }
+}
+
 template <typename TS, int SRC>
 static void launch_fine_src(const CellArgs &a, hipStream_t s) {
     const dim3 grid((unsigned)(4L * a.H / a.P));
@@ -853,7 +969,10 @@ static void launch_fine_src(const CellArgs &a, hipStream_t s) {
     case 2: LSTMSS_FK(2); break;
     case 4: LSTMSS_FK(4); break;
     case 8: LSTMSS_FK(8); break;
-    default: LSTMSS_FK(16); break;
+    case 16: LSTMSS_FK(16); break;
+    default:
+        hipLaunchKernelGGL((cell_fine32_kernel<TS, SRC>), grid, dim3(256), 0, s, a);
+        break;
     }
 #undef LSTMSS_FK
 }
@@ -880,7 +999,8 @@ static hipError_t launch_fine_typed(const CellArgs &a, int mode, hipStream_t s) 
 }
 
 hipError_t launch_cell_fine(const CellArgs &a, int mode, bool bf16, hipStream_t s) {
-    if ((a.P != 1 && a.P != 2 && a.P != 4 && a.P != 8 && a.P != 16) || a.My < 2 || a.My > 64 ||
+    if ((a.P != 1 && a.P != 2 && a.P != 4 && a.P != 8 && a.P != 16 && a.P != 32) || a.My < 2 ||
+        a.My > 64 ||
         (a.My & (a.My - 1)) != 0 || a.nb < 1 || a.nb > 64 || a.nb != (a.B + a.My - 1) / a.My ||
         a.B > 256 || a.S < 0 || a.S >= a.nb || (mode != CELL_SPARSE && mode != CELL_GIVEN) ||
         (4L * a.H) % a.P != 0)

@@ -116,9 +116,16 @@ struct G1Shape {
 // ROWA: the forward products a = W[:, kcol0 : kcol0 + Kp] G instead, whose
 // first operand arrives row-major with k contiguous: a thread stages KB rows
 // x VW consecutive k and stores each row's vector as it is.
-template <typename TS, int TM, int TN, bool GATHER, bool VEC, bool ROWA = false, int NW = 4>
+// FN: the fine structure with 32-row slices and 32-column blocks on the
+// masked matrix, with TN = 32 (a work-group's columns are one block): the
+// work-group gathers the rows of the slices that keep its block and skips
+// the others, W rows and gate-gradient rows alike (their products are exactly
+// zero, so the result is bit-identical to multiplying them).
+template <typename TS, int TM, int TN, bool GATHER, bool VEC, bool ROWA = false, int NW = 4,
+          bool FN = false>
 __global__ __launch_bounds__(NW * 64) void gemm1_kernel(Gemm1Args a) {
     static_assert(!(ROWA && GATHER), "the forward products read every row");
+    static_assert(!(FN && (GATHER || ROWA)), "the fine fast path reads every row");
     constexpr int THREADS = NW * 64;  // shadows the file-wide default
     using SH = G1Shape<TS, TM, TN, NW>;
     constexpr bool BF = SH::BF;
@@ -141,11 +148,44 @@ __global__ __launch_bounds__(NW * 64) void gemm1_kernel(Gemm1Args a) {
     const int n0 = blockIdx.y * TN;
     const int step = blockIdx.z / a.splitk, split = blockIdx.z - step * a.splitk;
     const int kb = split * (int)a.k_chunk;
-    const int ke = min((int)a.Kp, kb + (int)a.k_chunk);
+    const int ke0 = min((int)a.Kp, kb + (int)a.k_chunk);
     const int M = a.M, N = a.N, ldw = (int)a.ldw;
     const TS *W = (const TS *)a.W;
     const TS *G = (const TS *)a.Gc + step * a.gc_step;
     const int32_t *idx = a.idx + (GATHER ? step * a.idx_step : 0);
+
+    // FN: slices of [kb, ke0) that keep this work-group's column block, in
+    // ascending order (one wavefront compacts them with ballots)
+    __shared__ int slist[FN ? FINE_MAX_SLICES : 1];
+    __shared__ int s_nact;
+    int ke = ke0;
+    if constexpr (FN) {
+        static_assert(!FN || TN == 32, "a fine work-group's columns are one block");
+        if (tid < 64) {
+            const int32_t *fi = a.fidx + step * a.fidx_step;
+            const int c = n0 >> 5, s_end = ke0 >> 5;
+            int base = 0;
+            for (int sb = kb >> 5; sb < s_end; sb += 64) {
+                const int sl = sb + tid;
+                bool kept = false;
+                if (sl < s_end) {
+                    const int32_t *e = fi + (long)sl * a.fkept;
+                    for (int q = 0; q < a.fkept; ++q)
+                        kept |= e[q] == c;
+                }
+                const uint64_t m = __ballot(kept);
+                if (kept)
+                    slist[base + __popcll(m & ((1ull << tid) - 1ull))] = sl;
+                base += __popcll(m);
+            }
+            if (tid == 0)
+                s_nact = base;
+        }
+        __syncthreads();
+        ke = kb + s_nact * 32;
+    }
+    // gate-gradient row of compacted position k (FN), else k itself
+    auto grow = [&](int k) { return FN ? slist[(k - kb) >> 5] * 32 + ((k - kb) & 31) : k; };
 
     // gathered W row of every k of the current super-chunk (refilled every
     // GEMM1_KC_MAX rows, a multiple of TK)
@@ -158,7 +198,7 @@ __global__ __launch_bounds__(NW * 64) void gemm1_kernel(Gemm1Args a) {
             srow[i] = GATHER ? idx[k / a.P] * a.P + k % a.P : k;
         }
     };
-    if (!ROWA)
+    if (!ROWA && !FN)
         fill_rows(sc);
 
     auto qa = [&](int i) { return tid + i * THREADS; };
@@ -192,7 +232,7 @@ __global__ __launch_bounds__(NW * 64) void gemm1_kernel(Gemm1Args a) {
             for (int r = 0; r < KB; ++r) {
                 const int k = kg + r;
                 if (ok && k < ke)
-                    ra[i][r].load(W + (long)srow[k - sc] * ldw + m, VW);
+                    ra[i][r].load(W + (long)(FN ? grow(k) : srow[k - sc]) * ldw + m, VW);
                 else
                     ra[i][r].zero();
             }
@@ -207,7 +247,7 @@ __global__ __launch_bounds__(NW * 64) void gemm1_kernel(Gemm1Args a) {
             for (int r = 0; r < KB; ++r) {
                 const int k = kg + r;
                 if (ok && k < ke)
-                    rb[i][r].load(G + (long)k * N + n, VW);
+                    rb[i][r].load(G + (long)grow(k) * N + n, VW);
                 else
                     rb[i][r].zero();
             }
@@ -286,7 +326,7 @@ __global__ __launch_bounds__(NW * 64) void gemm1_kernel(Gemm1Args a) {
     for (int k0 = kb; k0 < ke; k0 += TK) {
         const bool next = k0 + TK < ke;
         if (next) {
-            if (!ROWA && k0 + TK == sc + GEMM1_KC_MAX) {  // next super-chunk of rows
+            if (!ROWA && !FN && k0 + TK == sc + GEMM1_KC_MAX) {  // next super-chunk of rows
                 sc = k0 + TK;
                 fill_rows(sc);
                 __syncthreads();
@@ -488,8 +528,12 @@ __device__ __forceinline__ void lds_store_vec(E *dst, const V &v) {
     }
 }
 
-template <typename TS, bool SPARSE, int TT, int ATN, bool VEC, int BC>
+// FN (dense layout, fine structure with 32-row slices and 32-column blocks,
+// BC = 32): a row group is one slice and a batch chunk is one block, so the
+// chunks of removed blocks skip their MFMAs (exact zeros, bit-identical).
+template <typename TS, bool SPARSE, int TT, int ATN, bool VEC, int BC, bool FN = false>
 __global__ __launch_bounds__(THREADS, 2) void wgrad_kernel(WgradArgs a) {
+    static_assert(!(FN && (SPARSE || BC != 32 || TT != 1)), "fine chunks are 32-column blocks");
     using E = typename std::conditional<sizeof(TS) == 4, float, uint16_t>::type;
     constexpr int PITCH = BC + (sizeof(TS) == 4 ? 4 : 8);
     constexpr int GROWS = TT * 32;                // temporary-tile rows per group
@@ -604,6 +648,12 @@ __global__ __launch_bounds__(THREADS, 2) void wgrad_kernel(WgradArgs a) {
             const int k = tid >> 6, e = tid & 63;
             ridx[set] = e < lqc[k] ? a.idx[(long)t * a.kept + lq0[k] + e] : -1;
         }
+        if (FN && b0 == 0 && tid < WG_NG * 64) {  // kept blocks of the group's slice
+            const int k = tid >> 6, e = tid & 63;
+            const long sl = (long)blockIdx.x * WG_NG + k;
+            ridx[set] = (e < a.fkept && sl < G4 / 32)
+                            ? a.fidx[((long)t * (G4 / 32) + sl) * a.fkept + e] : -1;
+        }
     };
     auto stash = [&](int it, int set, int buf) {
         const int tl = it / nbc;
@@ -623,7 +673,7 @@ __global__ __launch_bounds__(THREADS, 2) void wgrad_kernel(WgradArgs a) {
                 lds_store_vec(&sX[buf][f][bb], rx[set][i]);
             }
         }
-        if (SPARSE && it - tl * nbc == 0 && tid < WG_NG * 64)
+        if ((SPARSE || FN) && it - tl * nbc == 0 && tid < WG_NG * 64)
             sidx[tl & 1][tid >> 6][tid & 63] = ridx[set];
     };
 
@@ -673,15 +723,33 @@ __global__ __launch_bounds__(THREADS, 2) void wgrad_kernel(WgradArgs a) {
     // iteration it computes from LDS buffer it & 1, loads chunk it + 2 into
     // register set it & 1 and stores chunk it + 1 (set and buffer
     // (it + 1) & 1); the loop runs in pairs so that the sets are static
+    uint64_t fmask = ~0ull;  // FN: kept blocks of this wavefront's slice at the current step
     auto iter = [&](int it, auto sc) {
         constexpr int S0 = decltype(sc)::value, S1 = 1 - S0;
         const int buf = S0;
         const int tl = it / nbc, bc = it - tl * nbc;
         if (it + 2 < niters)
             load(it + 2, S0);
+        if constexpr (FN) {
+            if (bc == 0) {
+                const int v = sidx[tl & 1][gi][lane];
+                uint64_t m = v >= 0 ? (1ull << v) : 0ull;
+#pragma unroll
+                for (int off = 32; off >= 1; off >>= 1) {
+                    const uint32_t lo = __shfl_xor((uint32_t)m, off, 64);
+                    const uint32_t hi = __shfl_xor((uint32_t)(m >> 32), off, 64);
+                    m |= ((uint64_t)hi << 32) | lo;
+                }
+                fmask = ((uint64_t)__builtin_amdgcn_readfirstlane((uint32_t)(m >> 32)) << 32) |
+                        __builtin_amdgcn_readfirstlane((uint32_t)m);
+            }
+        }
+        const bool run = !FN || !a.fskip || ((fmask >> bc) & 1);
 
         // MFMA over this batch chunk: WG_FT feature tiles x TT row tiles
-        if constexpr (sizeof(TS) == 4) {
+        if (!run) {
+            // removed block: its products are zero
+        } else if constexpr (sizeof(TS) == 4) {
             float4 av[HALF / 4][WG_FT], bv[HALF / 4][TT];
 #pragma unroll
             for (int s = 0; s < HALF / 4; ++s) {
@@ -1003,6 +1071,12 @@ int gemm1_wgs_per_cu(int tm, int tn) {
 
 template <typename TS, int TM, int TN, bool GA, bool VE, bool ROWA = false>
 static void launch_g1(dim3 grid, const Gemm1Args &a, bool w8, hipStream_t s) {
+    if constexpr (!GA && !ROWA && TM == 128 && TN == 32) {
+        if (a.fidx) {
+            hipLaunchKernelGGL((gemm1_kernel<TS, 128, 32, false, VE, false, 4, true>), grid, dim3(THREADS), 0, s, a);
+            return;
+        }
+    }
     if constexpr (TM == 128 && TN == 128) {
         if (w8) {
             hipLaunchKernelGGL((gemm1_kernel<TS, TM, TN, GA, VE, ROWA, 8>), grid, dim3(512), 0, s, a);
@@ -1025,6 +1099,11 @@ static bool use_w8(const Gemm1Args &a, bool bf16, int TM, int TN) {
 hipError_t launch_gemm1(Gemm1Args a, bool bf16, hipStream_t s) {
     if (a.k_chunk % GEMM1_TK != 0 || a.splitk < 1 || a.steps < 1)
         return hipErrorInvalidValue;
+    // fine fast path: no gather, whole 32-row slices, 32-column blocks, the
+    // slice masks of one split fit the work-group's table
+    if (a.fidx && (a.idx || a.P != 32 || a.fkept < 1 || a.fkept > 64 || a.N % 32 != 0 ||
+                   ceil_div(a.k_chunk, 32) > FINE_MAX_SLICES))
+        return hipErrorInvalidValue;
     // 16-byte vector loads need 16-byte aligned rows; the tile origin is
     // rounded down to the vector width and rows below m_begin are not stored
     const int vw = bf16 ? 8 : 4;
@@ -1037,6 +1116,10 @@ hipError_t launch_gemm1(Gemm1Args a, bool bf16, hipStream_t s) {
         TM = a.tm;
     if (a.tn)
         TN = a.tn;
+    if (a.fidx) {  // one column block per work-group
+        TM = 128;
+        TN = 32;
+    }
     if (!((TN == 32 && TM == 128) || ((TN == 64 || TN == 128) && (TM == 64 || TM == 128))))
         return hipErrorInvalidValue;
     dim3 grid((unsigned)ceil_div(a.M - a.m_lo, TM), (unsigned)ceil_div(a.N, TN), (unsigned)z);
@@ -1116,6 +1199,19 @@ bool wgrad_supported(int P, int R, int S) {
 }
 
 hipError_t launch_wgrad(WgradArgs a, bool sparse, bool bf16, hipStream_t s) {
+    if (a.fidx) {  // fine structure, 32-row slices x 32-column blocks
+        if (sparse || a.B % 32 != 0 || a.fkept < 1 || a.fkept > 64 || (4L * a.H) % 32 != 0)
+            return hipErrorInvalidValue;
+        a.BC = 32;
+        const bool vec = a.B % (bf16 ? 8 : 4) == 0;
+        dim3 grid((unsigned)ceil_div(ceil_div(4L * a.H, 32), WG_NG),
+                  (unsigned)ceil_div(a.I + a.H, WG_FEAT));
+#define LSTMSS_WF(TS, VE) hipLaunchKernelGGL((wgrad_kernel<TS, false, 1, 1, VE, 32, true>), grid, dim3(THREADS), 0, s, a)
+        if (bf16) { if (vec) LSTMSS_WF(bf16_t, true); else LSTMSS_WF(bf16_t, false); }
+        else { if (vec) LSTMSS_WF(float, true); else LSTMSS_WF(float, false); }
+#undef LSTMSS_WF
+        return hipGetLastError();
+    }
     int tt = 1, at = 1;
     if (sparse) {
         if (!wgrad_supported(a.P, a.R, a.S))

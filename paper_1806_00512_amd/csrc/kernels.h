@@ -65,6 +65,13 @@ struct Gemm1Args {
     int tm, tn;            // tile rows / columns, 0 = chosen by the launcher
     int kcol0;             // launch_gemm_fwd only: first W column of the product
     int waves;             // wavefronts per work-group: 0 or 4, or 8 for 128-row tiles
+    // fine structure with 32-row slices and 32-column blocks (Gc the masked
+    // matrix, no gather): kept block indices of the first step,
+    // [4H/32][fkept], fidx_step entries per step; MFMAs of removed blocks
+    // are skipped.  NULL otherwise.
+    const int32_t *fidx;
+    int fkept;
+    long fidx_step;
 };
 
 // Weight gradient dW[rows] += dG_c [x_t; h_{t-1}]^T (rows scattered by idx).
@@ -95,9 +102,14 @@ struct WgradArgs {
     int t_begin, t_end;    // time steps [t_begin, t_end) of this launch
     int accumulate;        // 0: dW = sum; 1: dW += sum, continuing from the stored dW
     float *dW;             // [4H][I+H]
+    // fine structure with 32-row slices and 32-column blocks (dense layout,
+    // Gc the masked matrix): kept block indices [T][4H/32][fkept]; a row
+    // group skips the batch chunks of its removed blocks.  NULL otherwise.
+    const int32_t *fidx;
+    int fkept;
+    int fskip;             // 1: skip removed blocks; 0: multiply them (same bits)
 };
 
-// One forward step: a = W [x_t; h_{t-1}] + b, activations, cell update.
 // Forward cell update from the pre-activation pieces of one step.
 struct FwdActArgs {
     const float *zx;       // [4H][B] input projection W_x x_t
@@ -113,6 +125,7 @@ struct FwdActArgs {
     void *hout;            // [H][B] or NULL
 };
 
+// One forward step: a = W [x_t; h_{t-1}] + b, activations, cell update.
 struct FwdArgs {
     const void *W;
     const float *bias;     // [4H] or NULL
@@ -127,7 +140,7 @@ struct FwdArgs {
 };
 
 hipError_t launch_cell(const CellArgs &a, int mode, bool bf16, hipStream_t s);
-// Fine-grained structure (mode CELL_SPARSE or CELL_GIVEN): P in {1,2,4,8,16},
+// Fine-grained structure (mode CELL_SPARSE or CELL_GIVEN): P in {1,2,4,8,16,32},
 // My a power of two in [2, 64], nb = ceil(B/My) <= 64, B <= 256.  With
 // stage set and H*B >= 65536, CELL_SPARSE runs the element kernel into stage
 // (and chunk_sq, chunk_rs) before the selection; db (when set) accumulates
@@ -177,6 +190,8 @@ hipError_t launch_h0_store(void *dst, const float *src, long n, bool bf16, hipSt
 // Tile constants shared by the host-side sizing code.
 constexpr int GEMM1_TK = 64;       // granularity of a split's k range
 constexpr int GEMM1_KC_MAX = 2048; // gathered rows looked up into LDS at a time
+// fine structure fast path: at most this many 32-row slices per product (4H <= 16384)
+constexpr int FINE_MAX_SLICES = 512;
 void gemm1_tile(bool bf16, int N, long rows, long zdim, int *tm, int *tn);
 int gemm1_wgs_per_cu(int tm, int tn);
 

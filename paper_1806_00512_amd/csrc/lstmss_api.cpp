@@ -159,6 +159,9 @@ std::map<int, StackRes> g_stack;
 // steps per dX launch inside a stack (the wavefront lag between layers):
 // 0 = T/4 (at least 1)
 int g_stack_dx_steps = 0;
+// fine structure with 32 x 32 blocks: skip the removed blocks' products (1,
+// default) or run them on the zeros (0); results are the same bits
+bool g_fine_skip = true;
 
 hipError_t stack_res(StackRes **out) {
     int dev = 0;
@@ -240,7 +243,7 @@ int32_t make_plan(const lstmss_dims *d, float sparsity, const lstmss_structure *
     if (!s)
         return fail(LSTMSS_ERR_INVALID_ARG, "structure is NULL");
     if (s->kind == LSTMSS_FINE) {
-        if (s->Mx < 1 || s->Mx > 16 || G % s->Mx != 0 || 32 % s->Mx != 0)
+        if (s->Mx < 1 || s->Mx > 32 || G % s->Mx != 0 || 32 % s->Mx != 0)
             return fail(LSTMSS_ERR_INVALID_ARG, "Mx=%d must divide 32 and 4H=%ld", s->Mx, G);
         if (s->My < 2 || s->My > 64 || (s->My & (s->My - 1)) != 0)
             return fail(LSTMSS_ERR_INVALID_ARG, "My=%d must be a power of two in [2, 64]", s->My);
@@ -413,6 +416,15 @@ int32_t backward_enqueue(const lstmss_dims *d, bool dense, const Plan &p, const 
     // on the masked matrix like the dense ones, without a row gather
     const bool fine = sparse && p.fine;
     const bool gsparse = sparse && !fine;
+    // fine blocks shaped like the MFMA operand blocks (32 gate rows x 32
+    // batch columns): the products skip the removed blocks
+    // batch chunks of 32 columns: the weight gradient takes this path (with or
+    // without skipping) whenever the blocks are 32 x 32, so that its
+    // summation order does not depend on the skip option
+    const bool fblocks = fine && p.P == 32 && p.My == 32 && d->B % 32 == 0 &&
+                         4L * d->H / 32 <= FINE_MAX_SLICES;
+    const bool ffast = fblocks && g_fine_skip;
+    const int fkept = fine ? p.nb - p.S : 0;
     const int T = d->T, B = d->B, I = d->I, H = d->H;
     const long HB = (long)H * B, G = 4L * H, K = (long)I + H;
     const size_t es = elem_bytes(d->dtype);
@@ -473,6 +485,7 @@ int32_t backward_enqueue(const lstmss_dims *d, bool dense, const Plan &p, const 
     wg.Gc = dGc_all; wg.idx = gsparse ? idx_all : nullptr; wg.x = x; wg.h = hst;
     wg.T = T; wg.I = I; wg.H = H; wg.B = B; wg.Kp = (int)p.Kp; wg.kept = (int)p.kept;
     wg.P = p.P; wg.R = p.R; wg.S = p.S; wg.dW = dW;
+    wg.fidx = fblocks ? idx_all : nullptr; wg.fkept = fkept; wg.fskip = ffast ? 1 : 0;
 
     Gemm1Args gx{};  // dX[t] = (W_c rows [0, I))^T dG_c, several steps per launch
     gx.W = W; gx.ldw = K; gx.P = p.P; gx.Kp = p.Kp; gx.M = I; gx.m_begin = 0; gx.N = B;
@@ -480,6 +493,7 @@ int32_t backward_enqueue(const lstmss_dims *d, bool dense, const Plan &p, const 
     gx.k_chunk = ceil_div(p.Kp, GEMM1_TK) * GEMM1_TK;
     gx.gc_step = p.Kp * B; gx.idx_step = p.kept; gx.out_step = (long)I * B;
     gx.tm = dx_tm; gx.tn = dx_tn;
+    gx.fkept = fkept; gx.fidx_step = p.kept;
 
     const long part_stride = HB;
     for (int t = T - 1; t >= 0; --t) {
@@ -558,6 +572,7 @@ int32_t backward_enqueue(const lstmss_dims *d, bool dense, const Plan &p, const 
         if (dx_now) {
             gx.Gc = dGc;
             gx.idx = gsparse ? idx : nullptr;
+            gx.fidx = ffast ? idx : nullptr;
             gx.part = dX + (size_t)t * I * B;
             gx.steps = dx_hi - t;
             HIP_TRY(timed(LSTMSS_KERNEL_DATA_GRAD, sst, [&] { return launch_gemm1(gx, bf16, sst); }));
@@ -577,6 +592,7 @@ int32_t backward_enqueue(const lstmss_dims *d, bool dense, const Plan &p, const 
         g1.Kp = p.Kp; g1.M = (int)K; g1.m_begin = I; g1.N = B; g1.out_row0 = I;
         g1.part = part; g1.part_stride = part_stride; g1.splitk = L.splitk;
         g1.k_chunk = L.k_chunk; g1.steps = 1;
+        g1.fidx = ffast ? idx : nullptr; g1.fkept = fkept; g1.fidx_step = p.kept;
         HIP_TRY(timed(LSTMSS_KERNEL_DATA_GRAD, st, [&] { return launch_gemm1(g1, bf16, st); }));
 
         if (!batched) {
@@ -1191,6 +1207,7 @@ int32_t lstmss_set_option(int32_t option, int32_t value) {
     }
     switch (option) {
     case LSTMSS_OPT_GRAPHS: g_graphs = value != 0; return LSTMSS_OK;
+    case LSTMSS_OPT_FINE_SKIP: g_fine_skip = value != 0; return LSTMSS_OK;
     case LSTMSS_OPT_STACK_DX_STEPS:
         if (value < 0)
             return fail(LSTMSS_ERR_INVALID_ARG, "stack dX steps %d must be >= 0", value);

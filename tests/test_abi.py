@@ -101,7 +101,7 @@ def test_fine_sizes(L, B, My, Mx, sp):
 
 @pytest.mark.parametrize("B,My,Mx,sp,code", [
     (128, 16, 3, 0.5, -1),    # Mx does not divide 32
-    (128, 16, 32, 0.5, -1),   # Mx above 16
+    (128, 16, 64, 0.5, -1),   # Mx above 32
     (128, 12, 4, 0.5, -1),    # My not a power of two
     (128, 1, 4, 0.5, -1),     # My below 2
     (128, 128, 4, 0.5, -1),   # My above 64

@@ -208,3 +208,37 @@ def test_fine_graph_replay_matches_direct(L):
         for k, v in ref.items():
             if v is not None:
                 assert torch.equal(o[k], v), k
+
+
+# ---------------------------------------------------------------------------
+# blocks shaped like the 32 x 32 MFMA operand blocks: the products skip the
+# removed blocks; same bits as multiplying the zeros, and the oracle's values
+# ---------------------------------------------------------------------------
+@pytest.mark.parametrize("T,B,I,H,sp,dtype", [
+    (3, 64, 40, 64, 0.5, "f32"),       # 2 blocks per slice, 8 slices
+    (4, 128, 64, 96, 0.5, "f32"),      # 4 blocks, unaligned I
+    (3, 128, 32, 64, 0.75, "f32"),
+    (2, 256, 48, 64, 0.25, "f32"),     # 8 blocks per slice
+    (3, 128, 64, 64, 0.5, "bf16"),
+    (2, 32, 24, 32, 0.0, "f32"),       # one block, nothing removed
+])
+def test_fine_mfma_blocks(L, T, B, I, H, sp, dtype):
+    d = make_layer(T, B, I, H, seed=T * 5 + B + H, w_scale=0.2, dtype=dtype, state=True)
+    o = check_layer_fine(L, d, dtype, sp, 32, 32)
+    x, W = gpu_tensor(d["x"], dtype), gpu_tensor(d["W"], dtype)
+    dH = gpu_tensor(d["dH_up"])
+    dhT, dcT = gpu_tensor(d["dhT"]), gpu_tensor(d["dcT"])
+    _, cache = L.fwd_cache(x, W, gpu_tensor(d["b"]), gpu_tensor(d["h0"]), gpu_tensor(d["c0"]))
+    outs = []
+    try:
+        for skip in (1, 0):
+            L.set_option("fine_skip", skip)
+            outs.append(L.bwd_structsparse(x, W, cache, dH, sparsity=sp, dhT=dhT, dcT=dcT,
+                                           kind=L.FINE, My=32, Mx=32))
+            torch.cuda.synchronize()
+    finally:
+        L.set_option("fine_skip", 1)
+    for k in ("dX", "dW", "db", "dh0", "dc0", "idx"):
+        assert torch.equal(outs[0][k], outs[1][k]), k
+    for k in ("dX", "dW", "db"):
+        assert torch.equal(outs[0][k], o[k]), k
