@@ -531,8 +531,8 @@ def measure_bidir(L, torch, wl, sparsity, steps):
 def main():
     args = parse()
     if args.gpus != 1:
-        print("bench.py: this build runs on one GPU only (--gpus 1); multi-GPU sharding is "
-              "described in the design notes but not built", file=sys.stderr)
+        print("bench.py: the library runs on one GPU (--gpus 1); sharding across GPUs is "
+              "not implemented", file=sys.stderr)
         sys.exit(2)
     import torch
 
