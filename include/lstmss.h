@@ -278,10 +278,12 @@ int32_t lstmss_mse_grad(const lstmss_dims *d, const void *h, const float *y, flo
  *                      gate kernel and dh GEMM; 2 (default) on the side
  *                      stream while a step's data-gradient GEMM is below
  *                      2^31 multiply-adds ((I+H) * B * K'), else in order
- *                      (large GEMMs fill the GPU by themselves).
+ *                      (large GEMMs fill the GPU by themselves); in stack
+ *                      and bidirectional calls mode 2 keeps every layer's
+ *                      work in order (the other layers fill the GPU).
  *   LSTMSS_OPT_STACK_DX_STEPS  steps per input-gradient launch inside
  *                      lstm_bwd_stack, i.e. how many steps a layer lags the
- *                      layer above; 0 (default) = T/4, at least 1.
+ *                      layer above; 0 (default) = 12.
  *   LSTMSS_OPT_FINE_SKIP  FINE with Mx = My = 32: 1 (default) skips the
  *                      removed blocks' multiplications, 0 multiplies the
  *                      zeros (same bits; for checking and timing).

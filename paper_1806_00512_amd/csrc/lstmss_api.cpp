@@ -157,8 +157,9 @@ struct StackRes {
 };
 std::map<int, StackRes> g_stack;
 // steps per dX launch inside a stack (the wavefront lag between layers):
-// 0 = T/4 (at least 1)
+// 0 = kStackDxSteps (measured best at T = 35 and T = 50)
 int g_stack_dx_steps = 0;
+constexpr int kStackDxSteps = 12;
 // fine structure with 32 x 32 blocks: skip the removed blocks' products (1,
 // default) or run them on the zeros (0); results are the same bits
 bool g_fine_skip = true;
@@ -400,6 +401,10 @@ struct EnqCtx {
     std::vector<ChunkEv> *dx_done = nullptr;         // this layer's dX chunks
     std::vector<hipEvent_t> *dx_events = nullptr;    // events for them (one per chunk)
     int max_dx_len = 0;                              // cap on steps per dX launch (0: none)
+    // automatic side-stream mode may use the side stream (single calls);
+    // calls that run beside other layers (stack, bidirectional) keep their
+    // work in order unless the side stream is forced
+    bool auto_side = true;
 };
 
 // Enqueue one backward call on main stream st, with ctx (locked by the
@@ -463,7 +468,8 @@ int32_t backward_enqueue(const lstmss_dims *d, bool dense, const Plan &p, const 
 
     const bool use_side = batched || dX;
     const bool concurrent = use_side && (g_side_mode == 1 ||
-                                         (g_side_mode == 2 && (double)K * B * p.Kp < kSideMaxMacs));
+                                         (g_side_mode == 2 && ctx.auto_side &&
+                                          (double)K * B * p.Kp < kSideMaxMacs));
     hipStream_t sst = concurrent ? ctx.side : st;
     // the weight gradient runs in chunks of chunk_len steps and dX in chunks
     // of dx_len steps (whole rounds of resident work-groups); each launches
@@ -762,7 +768,8 @@ int32_t stack_enqueue(int32_t layers, const lstmss_dims *d, const StackPlan &sp,
         ctx.dH_ready = l == layers - 1 ? nullptr : &chunks[l + 1];
         ctx.dx_done = l > 0 ? &chunks[l] : nullptr;
         ctx.dx_events = &R.chunk_ev[l];
-        ctx.max_dx_len = g_stack_dx_steps > 0 ? g_stack_dx_steps : std::max(1, d[l].T / 4);
+        ctx.max_dx_len = g_stack_dx_steps > 0 ? g_stack_dx_steps : kStackDxSteps;
+        ctx.auto_side = false;
         const float *up = l == layers - 1 ? dH_top : dX[l + 1];
         const int32_t rc = backward_enqueue(&d[l], sp.dense, sp.plans[l], x[l], W[l], cache[l],
                                             up, nullptr, nullptr, dX[l], dW[l], db ? db[l] : nullptr,
@@ -821,6 +828,7 @@ int32_t bidir_enqueue(const lstmss_dims *d, bool dense, const Plan &p, const voi
         ctx.ring = R.ring[dir];
         ctx.nring = kForkEvents;
         ctx.join = R.join[dir];
+        ctx.auto_side = false;
         const int32_t rc =
             dir == 0 ? backward_enqueue(d, dense, p, x, W_f, cache_f, dh_f, nullptr, nullptr, dx_f,
                                         dW_f, db_f, nullptr, nullptr, idx_f, nullptr,
