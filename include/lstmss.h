@@ -196,8 +196,9 @@ int32_t lstmss_select_compact(const lstmss_dims *d, float sparsity, const lstmss
  * (launches of LSTMSS_OPT_STACK_DX_STEPS steps), so the layers overlap in
  * time.  Results are those of calling lstm_bwd_structsparse (or, with s
  * NULL or sparsity 0, lstm_bwd_dense) on each layer in turn, top first,
- * with dhT = dcT = NULL.  A stack call is enqueued directly (never
- * recorded into a HIP graph, whatever LSTMSS_OPT_GRAPHS says).
+ * with dhT = dcT = NULL.  A stack call of two or more layers is enqueued
+ * directly (never recorded into a HIP graph, whatever LSTMSS_OPT_GRAPHS
+ * says); a one-layer call is the single-layer call itself.
  *   d            [layers] dims; equal T, B, dtype; d[l].I = d[l-1].H
  *   x, W, cache  [layers] per-layer pointers as for lstm_bwd_structsparse
  *   dH_top       [T][H][B] fp32 upstream gradient of the top layer

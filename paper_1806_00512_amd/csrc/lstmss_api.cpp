@@ -944,6 +944,10 @@ int32_t lstm_bwd_stack(int32_t layers, const lstmss_dims *d, float sparsity,
             return fail(LSTMSS_ERR_INVALID_ARG, "layer %d: a required pointer is NULL", l);
     if (ws_bytes < sp.total)
         return fail(LSTMSS_ERR_WORKSPACE, "workspace of %zu bytes, need %zu", ws_bytes, sp.total);
+    if (layers == 1)  // nothing to overlap: the single-layer call (graph-replayed)
+        return backward(&d[0], sp.dense, sparsity, s, x[0], W[0], cache[0], dH_top, nullptr,
+                        nullptr, dX[0], dW[0], db ? db[0] : nullptr, nullptr, nullptr,
+                        idx_out ? idx_out[0] : nullptr, nullptr, ws, ws_bytes, stream);
     StackRes *R = nullptr;
     HIP_TRY(stack_res(&R));
     std::unique_lock<std::mutex> lk(R->mu);

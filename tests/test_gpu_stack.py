@@ -64,6 +64,7 @@ GRAPH_SKIP = pytest.mark.skip(reason="recording a stack call into a HIP graph en
     (2, 7, 64, 32, 64, 0.5, {"kind": 1, "My": 16, "Mx": 4}, 2),  # fine structure
     (4, 16, 32, 48, 96, 0.25, {"P": 4, "R": 8}, 1),    # one step per launch
     (3, 10, 64, 64, 64, 0.5, {"kind": 1, "My": 32, "Mx": 32}, 4),  # 32 x 32 fine blocks
+    (1, 6, 32, 40, 64, 0.5, {"P": 4, "R": 8}, 0),      # one layer: the single-layer call
 ])
 def test_stack_matches_sequential(L, graphs, layers, T, B, I, H, sparsity, kw, dx_steps):
     xs, Ws, caches, dH = make_stack(L, layers, T, B, I, H, seed=layers * 10 + T)
