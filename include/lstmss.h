@@ -75,9 +75,11 @@ typedef struct {
  * does not divide B; nb <= 64, B <= 256).  In every slice the K = sparsity *
  * nb blocks of smallest L2 norm are zeroed (K an integer within 1e-6,
  * 0 <= K < nb).  P, R are ignored.  With Mx = My = 32 (blocks shaped like
- * the 32 x 32 MFMA operand blocks), B a multiple of 32 and 4H <= 16384, the
- * gradient products skip the removed blocks' multiplications (same results
- * bit for bit); other block shapes run the products on the masked matrix. */
+ * the 32 x 32 MFMA operand blocks), fp32 storage, B a multiple of 32 and
+ * 4H <= 16384, the gradient products skip the removed blocks'
+ * multiplications (same results bit for bit); other block shapes, and bf16
+ * storage (whose products are bound by their loads, not their
+ * multiplications), run the products on the masked matrix. */
 typedef struct {
     int32_t kind;
     int32_t P, R;
@@ -285,16 +287,22 @@ int32_t lstmss_mse_grad(const lstmss_dims *d, const void *h, const float *y, flo
  *   LSTMSS_OPT_STACK_DX_STEPS  steps per input-gradient launch inside
  *                      lstm_bwd_stack, i.e. how many steps a layer lags the
  *                      layer above; 0 (default) = 12.
- *   LSTMSS_OPT_FINE_SKIP  FINE with Mx = My = 32: 1 (default) skips the
+ *   LSTMSS_OPT_FINE_SKIP  FINE with Mx = My = 32 and fp32 storage: 1 (default) skips the
  *                      removed blocks' multiplications, 0 multiplies the
  *                      zeros (same bits; for checking and timing).
+ *   LSTMSS_OPT_WGRAD_DMA  1 (default): the weight-gradient kernel loads its
+ *                      batch chunks from global memory straight into LDS
+ *                      when B is a multiple of 32 (fp32) or 64 (bf16) and
+ *                      the operands are 16-byte aligned; 0 stages them
+ *                      through registers (same bits; for checking and timing).
  * Changing an option drops the recorded graphs.  Not for use while calls
  * are being enqueued from other threads. */
 enum {
     LSTMSS_OPT_GRAPHS = 0,
     LSTMSS_OPT_SIDE_STREAM = 1,
     LSTMSS_OPT_STACK_DX_STEPS = 2,
-    LSTMSS_OPT_FINE_SKIP = 3
+    LSTMSS_OPT_FINE_SKIP = 3,
+    LSTMSS_OPT_WGRAD_DMA = 4
 };
 int32_t lstmss_set_option(int32_t option, int32_t value);
 

@@ -531,11 +531,29 @@ __device__ __forceinline__ void lds_store_vec(E *dst, const V &v) {
 // FN (dense layout, fine structure with 32-row slices and 32-column blocks,
 // BC = 32): a row group is one slice and a batch chunk is one block, so the
 // chunks of removed blocks skip their MFMAs (exact zeros, bit-identical).
-template <typename TS, bool SPARSE, int TT, int ATN, bool VEC, int BC, bool FN = false>
+//
+// DMA (B a multiple of BC, BC * element size = 128 bytes): the batch chunks go
+// from global memory straight into LDS (global_load_lds_dwordx4, lane j of an
+// instruction fills bytes [16 j, 16 j + 16) of a 1 KB block = 8 rows), with no
+// register staging.  Rows are unpadded 128-byte lines whose 16-byte pieces are
+// permuted per row (piece c of row r sits at c ^ wg_swz(r)) so that the
+// operand reads of 16 consecutive rows hit distinct banks; the permutation is
+// applied on the global side (each lane loads the piece its LDS slot holds).
+// Rows past the end of the operands are clamped to a valid row: they only feed
+// output rows or columns that are never stored.
+__device__ __forceinline__ int wg_swz(int r) { return (r & 7) ^ ((r >> 3) & 1); }
+
+typedef __attribute__((address_space(3))) void lds_void_t;
+typedef __attribute__((address_space(1))) void glob_void_t;
+
+template <typename TS, bool SPARSE, int TT, int ATN, bool VEC, int BC, bool FN = false,
+          bool DMA = false>
 __global__ __launch_bounds__(THREADS, 2) void wgrad_kernel(WgradArgs a) {
     static_assert(!(FN && (SPARSE || BC != 32 || TT != 1)), "fine chunks are 32-column blocks");
+    static_assert(!DMA || (BC * sizeof(TS) == 128 && VEC), "DMA chunks are 128-byte lines");
     using E = typename std::conditional<sizeof(TS) == 4, float, uint16_t>::type;
-    constexpr int PITCH = BC + (sizeof(TS) == 4 ? 4 : 8);
+    constexpr int PITCH = DMA ? BC : BC + (sizeof(TS) == 4 ? 4 : 8);
+    constexpr int PE = 16 / sizeof(E);            // elements per 16-byte piece
     constexpr int GROWS = TT * 32;                // temporary-tile rows per group
     using V = Vec<TS, VEC>;
     constexpr int VW = V::W;
@@ -598,7 +616,31 @@ __global__ __launch_bounds__(THREADS, 2) void wgrad_kernel(WgradArgs a) {
     // the end of a row (B is a multiple of VW when VEC).  Each thread's rows
     // are fixed for the whole launch, so their offsets within a step are
     // computed once; a chunk adds the step's base and the batch offset.
-    V rg[2][RG], rx[2][RX];  // two chunks in flight: loads run two chunks ahead
+    // DMA: instruction k of a chunk fills rows [8k, 8k + 8) of sX (k < 16) or
+    // of sG (k >= 16); wavefront w issues k = w, w + 4, ...
+    constexpr int NDI = (WG_FEAT + WG_NG * GROWS) / 8, NDW = NDI / 4;
+    static_assert(!DMA || (NDI % 4 == 0 && WG_FEAT == 128), "DMA instruction split");
+    int dofs[DMA ? NDW : 1];
+    bool disx[DMA ? NDW : 1];
+    if constexpr (DMA) {
+#pragma unroll
+        for (int i = 0; i < NDW; ++i) {
+            const int k = wave + 4 * i;
+            const int rr = 8 * (k < 16 ? k : k - 16) + (lane >> 3);
+            const int pc = (lane & 7) ^ wg_swz(rr);  // the piece this lane's LDS slot holds
+            if (k < 16) {
+                const int n = min(n0 + rr, NC - 1);
+                disx[i] = n < I;
+                dofs[i] = (n < I ? n : n - I) * B + pc * PE;
+            } else {
+                const int kk = rr / GROWS, lr = rr - kk * GROWS;
+                const int crow = max(0, min(lc0[kk] + min(lr, max(lcc[kk] - 1, 0)), (int)a.Kp - 1));
+                disx[i] = false;
+                dofs[i] = crow * B + pc * PE;
+            }
+        }
+    }
+    V rg[DMA ? 1 : 2][DMA ? 1 : RG], rx[DMA ? 1 : 2][DMA ? 1 : RX];  // two chunks in flight
     int gofs[RG], gbb[RG], xofs[RX], xbb[RX];
     bool gok[RG], xok[RX], xisx[RX];
 #pragma unroll
@@ -624,25 +666,35 @@ __global__ __launch_bounds__(THREADS, 2) void wgrad_kernel(WgradArgs a) {
     // steps run from t_end - 1 down to t_begin, and the launches of one call
     // go down in time too, so every row of dW sums its steps in one order
     // however the steps are split over launches
-    auto load = [&](int it, int set) {
+    auto load = [&](int it, int set, int lbuf) {
         const int tl = it / nbc, b0 = (it - tl * nbc) * BC;
         const int t = a.t_end - 1 - tl;
         const TS *Gt = Gc + (long)t * a.Kp * B + b0;
         const TS *xt = x + (long)t * I * B + b0;
         const TS *ht = h + (long)t * H * B + b0;
+        if constexpr (DMA) {
 #pragma unroll
-        for (int i = 0; i < RG; ++i) {
-            if (gok[i] && b0 + gbb[i] < B)
-                rg[set][i].load(Gt + gofs[i], VW);
-            else
-                rg[set][i].zero();
-        }
+            for (int i = 0; i < NDW; ++i) {
+                const int k = wave + 4 * i;
+                const TS *src = k < 16 ? (disx[i] ? xt : ht) + dofs[i] : Gt + dofs[i];
+                E *dst = k < 16 ? &sX[lbuf][8 * k][0] : &sG[lbuf][8 * (k - 16)][0];
+                __builtin_amdgcn_global_load_lds((glob_void_t *)src, (lds_void_t *)dst, 16, 0, 0);
+            }
+        } else {
 #pragma unroll
-        for (int i = 0; i < RX; ++i) {
-            if (xok[i] && b0 + xbb[i] < B)
-                rx[set][i].load((xisx[i] ? xt : ht) + xofs[i], VW);
-            else
-                rx[set][i].zero();
+            for (int i = 0; i < RG; ++i) {
+                if (gok[i] && b0 + gbb[i] < B)
+                    rg[DMA ? 0 : set][i].load(Gt + gofs[i], VW);
+                else
+                    rg[DMA ? 0 : set][i].zero();
+            }
+#pragma unroll
+            for (int i = 0; i < RX; ++i) {
+                if (xok[i] && b0 + xbb[i] < B)
+                    rx[DMA ? 0 : set][i].load((xisx[i] ? xt : ht) + xofs[i], VW);
+                else
+                    rx[DMA ? 0 : set][i].zero();
+            }
         }
         if (SPARSE && b0 == 0 && tid < WG_NG * 64) {
             const int k = tid >> 6, e = tid & 63;
@@ -657,20 +709,22 @@ __global__ __launch_bounds__(THREADS, 2) void wgrad_kernel(WgradArgs a) {
     };
     auto stash = [&](int it, int set, int buf) {
         const int tl = it / nbc;
+        if constexpr (!DMA) {
 #pragma unroll
-        for (int i = 0; i < RG; ++i) {
-            const int q = tid + i * THREADS;
-            if (q < gvec) {
-                const int rho = q / cpr, bb = (q - rho * cpr) * VW;
-                lds_store_vec(&sG[buf][rho][bb], rg[set][i]);
+            for (int i = 0; i < RG; ++i) {
+                const int q = tid + i * THREADS;
+                if (q < gvec) {
+                    const int rho = q / cpr, bb = (q - rho * cpr) * VW;
+                    lds_store_vec(&sG[buf][rho][bb], rg[set][i]);
+                }
             }
-        }
 #pragma unroll
-        for (int i = 0; i < RX; ++i) {
-            const int q = tid + i * THREADS;
-            if (q < xvec) {
-                const int f = q / cpr, bb = (q - f * cpr) * VW;
-                lds_store_vec(&sX[buf][f][bb], rx[set][i]);
+            for (int i = 0; i < RX; ++i) {
+                const int q = tid + i * THREADS;
+                if (q < xvec) {
+                    const int f = q / cpr, bb = (q - f * cpr) * VW;
+                    lds_store_vec(&sX[buf][f][bb], rx[set][i]);
+                }
             }
         }
         if ((SPARSE || FN) && it - tl * nbc == 0 && tid < WG_NG * 64)
@@ -713,10 +767,12 @@ __global__ __launch_bounds__(THREADS, 2) void wgrad_kernel(WgradArgs a) {
         }
     }
 
-    load(0, 0);
-    if (niters > 1)
-        load(1, 1);
+    load(0, 0, 0);
+    if (!DMA && niters > 1)
+        load(1, 1, 1);
     stash(0, 0, 0);
+    if (DMA)
+        __builtin_amdgcn_s_waitcnt(0);
     __syncthreads();
     constexpr int HALF = BC / 2;
     const int hb = (lane >> 5) * HALF;
@@ -728,8 +784,15 @@ __global__ __launch_bounds__(THREADS, 2) void wgrad_kernel(WgradArgs a) {
         constexpr int S0 = decltype(sc)::value, S1 = 1 - S0;
         const int buf = S0;
         const int tl = it / nbc, bc = it - tl * nbc;
-        if (it + 2 < niters)
-            load(it + 2, S0);
+        if (!DMA && it + 2 < niters)
+            load(it + 2, S0, 0);
+        // DMA: the next chunk streams into the other buffer (read in the
+        // previous iteration), issued once this chunk's operands are in
+        // registers (a deeper, three-buffer pipeline measured slower)
+        auto issue_next = [&]() {
+            if (DMA && it + 1 < niters)
+                load(it + 1, S1, S1);
+        };
         if constexpr (FN) {
             if (bc == 0) {
                 const int v = sidx[tl & 1][gi][lane];
@@ -745,21 +808,29 @@ __global__ __launch_bounds__(THREADS, 2) void wgrad_kernel(WgradArgs a) {
             }
         }
         const bool run = !FN || !a.fskip || ((fmask >> bc) & 1);
+        // column (element) of the 16-byte piece p of LDS row r
+        auto pcol = [&](int r, int p) { return DMA ? (p ^ wg_swz(r)) * PE : p * PE; };
 
         // MFMA over this batch chunk: WG_FT feature tiles x TT row tiles
         if (!run) {
             // removed block: its products are zero
+            issue_next();
         } else if constexpr (sizeof(TS) == 4) {
             float4 av[HALF / 4][WG_FT], bv[HALF / 4][TT];
 #pragma unroll
             for (int s = 0; s < HALF / 4; ++s) {
 #pragma unroll
-                for (int ft = 0; ft < WG_FT; ++ft)
-                    av[s][ft] = *(const float4 *)&sX[buf][fh * 64 + ft * 32 + (lane & 31)][hb + 4 * s];
+                for (int ft = 0; ft < WG_FT; ++ft) {
+                    const int r = fh * 64 + ft * 32 + (lane & 31);
+                    av[s][ft] = *(const float4 *)&sX[buf][r][pcol(r, hb / 4 + s)];
+                }
 #pragma unroll
-                for (int tt = 0; tt < TT; ++tt)
-                    bv[s][tt] = *(const float4 *)&sG[buf][gi * GROWS + tt * 32 + (lane & 31)][hb + 4 * s];
+                for (int tt = 0; tt < TT; ++tt) {
+                    const int r = gi * GROWS + tt * 32 + (lane & 31);
+                    bv[s][tt] = *(const float4 *)&sG[buf][r][pcol(r, hb / 4 + s)];
+                }
             }
+            issue_next();  // the next chunks stream in during the MFMAs
 #pragma unroll
             for (int s = 0; s < HALF / 4; ++s)
 #pragma unroll
@@ -774,12 +845,17 @@ __global__ __launch_bounds__(THREADS, 2) void wgrad_kernel(WgradArgs a) {
 #pragma unroll
             for (int s = 0; s < HALF / 8; ++s) {
 #pragma unroll
-                for (int ft = 0; ft < WG_FT; ++ft)
-                    av[s][ft] = *(const u16x8 *)&sX[buf][fh * 64 + ft * 32 + (lane & 31)][hb + 8 * s];
+                for (int ft = 0; ft < WG_FT; ++ft) {
+                    const int r = fh * 64 + ft * 32 + (lane & 31);
+                    av[s][ft] = *(const u16x8 *)&sX[buf][r][pcol(r, hb / 8 + s)];
+                }
 #pragma unroll
-                for (int tt = 0; tt < TT; ++tt)
-                    bv[s][tt] = *(const u16x8 *)&sG[buf][gi * GROWS + tt * 32 + (lane & 31)][hb + 8 * s];
+                for (int tt = 0; tt < TT; ++tt) {
+                    const int r = gi * GROWS + tt * 32 + (lane & 31);
+                    bv[s][tt] = *(const u16x8 *)&sG[buf][r][pcol(r, hb / 8 + s)];
+                }
             }
+            issue_next();
 #pragma unroll
             for (int s = 0; s < HALF / 8; ++s)
 #pragma unroll
@@ -852,6 +928,8 @@ __global__ __launch_bounds__(THREADS, 2) void wgrad_kernel(WgradArgs a) {
         }
         if (it + 1 < niters)
             stash(it + 1, S1, S1);
+        if (DMA)  // the next chunk's lines are in LDS before anyone reads them
+            __builtin_amdgcn_s_waitcnt(0);
         __syncthreads();
     };
     int it0 = 0;
@@ -1198,7 +1276,45 @@ bool wgrad_supported(int P, int R, int S) {
     return tt <= 2 && at <= WG_ATMAX && (R - S) <= 64;
 }
 
+// One weight-gradient launch; `dma` takes the LDS-DMA variant (128-byte
+// chunks: 32 fp32 or 64 bf16 batch columns).
+template <typename TS, bool SP, int TTV, int ATV, bool FN>
+static void wg_launch(const WgradArgs &a, bool vec, bool dma, dim3 grid, hipStream_t s) {
+    constexpr int DBC = 128 / (int)sizeof(TS);
+    if constexpr (!FN || DBC == 32) {
+        if (dma) {
+            hipLaunchKernelGGL((wgrad_kernel<TS, SP, TTV, ATV, true, DBC, FN, true>), grid,
+                               dim3(THREADS), 0, s, a);
+            return;
+        }
+    }
+    if constexpr (FN) {
+        if (vec)
+            hipLaunchKernelGGL((wgrad_kernel<TS, false, 1, 1, true, 32, true>), grid, dim3(THREADS), 0, s, a);
+        else
+            hipLaunchKernelGGL((wgrad_kernel<TS, false, 1, 1, false, 32, true>), grid, dim3(THREADS), 0, s, a);
+    } else {
+#define LSTMSS_WG(VE) do { \
+        if (a.BC == 16) hipLaunchKernelGGL((wgrad_kernel<TS, SP, TTV, ATV, VE, 16>), grid, dim3(THREADS), 0, s, a); \
+        else if (a.BC == 32) hipLaunchKernelGGL((wgrad_kernel<TS, SP, TTV, ATV, VE, 32>), grid, dim3(THREADS), 0, s, a); \
+        else hipLaunchKernelGGL((wgrad_kernel<TS, SP, TTV, ATV, VE, 64>), grid, dim3(THREADS), 0, s, a); } while (0)
+        if (vec)
+            LSTMSS_WG(true);
+        else
+            LSTMSS_WG(false);
+#undef LSTMSS_WG
+    }
+}
+
+static bool aligned16(const void *p) { return ((uintptr_t)p & 15) == 0; }
+
 hipError_t launch_wgrad(WgradArgs a, bool sparse, bool bf16, hipStream_t s) {
+    const int es = bf16 ? 2 : 4;
+    // the LDS-DMA variant: whole 128-byte chunks of 16-byte aligned rows
+    auto dma_ok = [&](int bc) {
+        return a.dma && bc * es == 128 && a.B % bc == 0 && aligned16(a.Gc) && aligned16(a.x) &&
+               aligned16(a.h);
+    };
     if (a.fidx) {  // fine structure, 32-row slices x 32-column blocks
         if (sparse || a.B % 32 != 0 || a.fkept < 1 || a.fkept > 64 || (4L * a.H) % 32 != 0)
             return hipErrorInvalidValue;
@@ -1206,10 +1322,10 @@ hipError_t launch_wgrad(WgradArgs a, bool sparse, bool bf16, hipStream_t s) {
         const bool vec = a.B % (bf16 ? 8 : 4) == 0;
         dim3 grid((unsigned)ceil_div(ceil_div(4L * a.H, 32), WG_NG),
                   (unsigned)ceil_div(a.I + a.H, WG_FEAT));
-#define LSTMSS_WF(TS, VE) hipLaunchKernelGGL((wgrad_kernel<TS, false, 1, 1, VE, 32, true>), grid, dim3(THREADS), 0, s, a)
-        if (bf16) { if (vec) LSTMSS_WF(bf16_t, true); else LSTMSS_WF(bf16_t, false); }
-        else { if (vec) LSTMSS_WF(float, true); else LSTMSS_WF(float, false); }
-#undef LSTMSS_WF
+        if (bf16)
+            wg_launch<bf16_t, false, 1, 1, true>(a, vec, false, grid, s);
+        else
+            wg_launch<float, false, 1, 1, true>(a, vec, dma_ok(32), grid, s);
         return hipGetLastError();
     }
     int tt = 1, at = 1;
@@ -1220,32 +1336,27 @@ hipError_t launch_wgrad(WgradArgs a, bool sparse, bool bf16, hipStream_t s) {
     }
     // batch columns per stage: 16/32 (fp32) or 32/64 (bf16, whole MFMA
     // k-blocks); larger stages would not leave room for two wavefronts per SIMD
-    int bc = a.B <= 16 ? 16 : a.B <= 32 ? 32 : (bf16 ? 64 : 32);
+    const int bc = a.B <= 16 ? 16 : a.B <= 32 ? 32 : (bf16 ? 64 : 32);
     a.BC = bc;
     const int vw = bf16 ? 8 : 4;
     const bool vec = a.B % vw == 0;
+    const bool dma = dma_ok(bc);
     const long groups = sparse ? ceil_div(ceil_div(4L * a.H / a.P, a.R), a.greg) : ceil_div(4L * a.H, 32);
     dim3 grid((unsigned)ceil_div(groups, WG_NG), (unsigned)ceil_div(a.I + a.H, WG_FEAT));
-#define LSTMSS_WG(TS, SP, TTV, ATV, VE) do { \
-        if (bc == 16) hipLaunchKernelGGL((wgrad_kernel<TS, SP, TTV, ATV, VE, 16>), grid, dim3(THREADS), 0, s, a); \
-        else if (bc == 32) hipLaunchKernelGGL((wgrad_kernel<TS, SP, TTV, ATV, VE, 32>), grid, dim3(THREADS), 0, s, a); \
-        else hipLaunchKernelGGL((wgrad_kernel<TS, SP, TTV, ATV, VE, 64>), grid, dim3(THREADS), 0, s, a); } while (0)
-#define LSTMSS_WGV(TS, SP, TTV, ATV) do { if (vec) LSTMSS_WG(TS, SP, TTV, ATV, true); else LSTMSS_WG(TS, SP, TTV, ATV, false); } while (0)
 #define LSTMSS_WGA(TS, TTV) do { \
-        if (at <= 1) LSTMSS_WGV(TS, true, TTV, 1); else if (at <= 2) LSTMSS_WGV(TS, true, TTV, 2); \
-        else LSTMSS_WGV(TS, true, TTV, 4); } while (0)
+        if (at <= 1) wg_launch<TS, true, TTV, 1, false>(a, vec, dma, grid, s); \
+        else if (at <= 2) wg_launch<TS, true, TTV, 2, false>(a, vec, dma, grid, s); \
+        else wg_launch<TS, true, TTV, 4, false>(a, vec, dma, grid, s); } while (0)
     if (bf16) {
-        if (!sparse) LSTMSS_WGV(bf16_t, false, 1, 1);
+        if (!sparse) wg_launch<bf16_t, false, 1, 1, false>(a, vec, dma, grid, s);
         else if (tt == 1) LSTMSS_WGA(bf16_t, 1);
         else LSTMSS_WGA(bf16_t, 2);
     } else {
-        if (!sparse) LSTMSS_WGV(float, false, 1, 1);
+        if (!sparse) wg_launch<float, false, 1, 1, false>(a, vec, dma, grid, s);
         else if (tt == 1) LSTMSS_WGA(float, 1);
         else LSTMSS_WGA(float, 2);
     }
 #undef LSTMSS_WGA
-#undef LSTMSS_WGV
-#undef LSTMSS_WG
     return hipGetLastError();
 }
 

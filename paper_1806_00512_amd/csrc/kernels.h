@@ -108,6 +108,8 @@ struct WgradArgs {
     const int32_t *fidx;
     int fkept;
     int fskip;             // 1: skip removed blocks; 0: multiply them (same bits)
+    int dma;               // 1: chunks go global -> LDS directly where the shape allows
+                           // (same bits as the register-staged loads of 0)
 };
 
 // Forward cell update from the pre-activation pieces of one step.

@@ -163,6 +163,7 @@ constexpr int kStackDxSteps = 12;
 // fine structure with 32 x 32 blocks: skip the removed blocks' products (1,
 // default) or run them on the zeros (0); results are the same bits
 bool g_fine_skip = true;
+bool g_wgrad_dma = true;
 
 hipError_t stack_res(StackRes **out) {
     int dev = 0;
@@ -425,9 +426,11 @@ int32_t backward_enqueue(const lstmss_dims *d, bool dense, const Plan &p, const 
     // batch columns): the products skip the removed blocks
     // batch chunks of 32 columns: the weight gradient takes this path (with or
     // without skipping) whenever the blocks are 32 x 32, so that its
-    // summation order does not depend on the skip option
-    const bool fblocks = fine && p.P == 32 && p.My == 32 && d->B % 32 == 0 &&
-                         4L * d->H / 32 <= FINE_MAX_SLICES;
+    // summation order does not depend on the skip option.  fp32 only: the
+    // bf16 products are bound by their loads, and the dense kernels on the
+    // masked matrix measured faster than skipping there
+    const bool fblocks = fine && d->dtype == LSTMSS_F32 && p.P == 32 && p.My == 32 &&
+                         d->B % 32 == 0 && 4L * d->H / 32 <= FINE_MAX_SLICES;
     const bool ffast = fblocks && g_fine_skip;
     const int fkept = fine ? p.nb - p.S : 0;
     const int T = d->T, B = d->B, I = d->I, H = d->H;
@@ -492,6 +495,7 @@ int32_t backward_enqueue(const lstmss_dims *d, bool dense, const Plan &p, const 
     wg.T = T; wg.I = I; wg.H = H; wg.B = B; wg.Kp = (int)p.Kp; wg.kept = (int)p.kept;
     wg.P = p.P; wg.R = p.R; wg.S = p.S; wg.dW = dW;
     wg.fidx = fblocks ? idx_all : nullptr; wg.fkept = fkept; wg.fskip = ffast ? 1 : 0;
+    wg.dma = g_wgrad_dma ? 1 : 0;
 
     Gemm1Args gx{};  // dX[t] = (W_c rows [0, I))^T dG_c, several steps per launch
     gx.W = W; gx.ldw = K; gx.P = p.P; gx.Kp = p.Kp; gx.M = I; gx.m_begin = 0; gx.N = B;
@@ -1220,6 +1224,7 @@ int32_t lstmss_set_option(int32_t option, int32_t value) {
     switch (option) {
     case LSTMSS_OPT_GRAPHS: g_graphs = value != 0; return LSTMSS_OK;
     case LSTMSS_OPT_FINE_SKIP: g_fine_skip = value != 0; return LSTMSS_OK;
+    case LSTMSS_OPT_WGRAD_DMA: g_wgrad_dma = value != 0; return LSTMSS_OK;
     case LSTMSS_OPT_STACK_DX_STEPS:
         if (value < 0)
             return fail(LSTMSS_ERR_INVALID_ARG, "stack dX steps %d must be >= 0", value);

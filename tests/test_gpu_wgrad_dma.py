@@ -1,0 +1,102 @@
+"""Weight-gradient chunk loads straight into LDS (LSTMSS_OPT_WGRAD_DMA) give
+the same bits as the register-staged loads, through the C ABI.
+
+The direct loads apply when B is a multiple of 32 (fp32) or 64 (bf16); rows
+and features past the ends of the operands are clamped to valid rows, so the
+cases include ragged row groups (H not a multiple of 16), feature tiles that
+end inside a tile (I + H not a multiple of 128), several batch chunks per
+step and several steps per launch.  Agreement with the oracle at the default
+setting is covered by the parity tests; here both settings must agree bit for
+bit on dX, dW, db, dh0, dc0 and the kept indices.
+"""
+import pytest
+import torch
+
+from paper_1806_00512_amd.inputs import make_layer
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module")
+def L():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    import paper_1806_00512_amd.lstmss as lstmss
+    lstmss.load()
+    return lstmss
+
+
+def gpu(a, dtype="f32"):
+    t = torch.from_numpy(a).to("cuda:0")
+    return t.to(torch.bfloat16) if dtype == "bf16" else t
+
+
+def run_both(L, fn):
+    outs = []
+    try:
+        for dma in (1, 0):
+            L.set_option("wgrad_dma", dma)
+            outs.append(fn())
+            torch.cuda.synchronize()
+    finally:
+        L.set_option("wgrad_dma", 1)
+    return outs
+
+
+@pytest.mark.parametrize("T,B,I,H,sp,dtype,struct", [
+    (5, 64, 40, 72, 0.5, "f32", {"P": 4, "R": 8}),      # ragged groups, NC = 112
+    (4, 128, 96, 64, 0.5, "f32", {"P": 4, "R": 8}),     # 4 chunks per step
+    (3, 96, 64, 64, 0.25, "f32", {"P": 2, "R": 8}),     # 3 chunks, two row tiles per group
+    (4, 128, 64, 64, 0.0, "f32", None),                 # dense
+    (3, 128, 72, 64, 0.5, "bf16", {"P": 4, "R": 8}),    # 2 bf16 chunks per step
+    (3, 64, 64, 40, 0.0, "bf16", None),                 # dense bf16, ragged rows
+    (3, 128, 64, 64, 0.5, "f32", {"kind": 1, "My": 32, "Mx": 32}),  # 32 x 32 fine blocks
+    (3, 70, 40, 64, 0.5, "f32", {"P": 4, "R": 8}),      # ragged B: staged loads either way
+])
+def test_wgrad_dma_same_bits(L, T, B, I, H, sp, dtype, struct):
+    d = make_layer(T, B, I, H, seed=11 * T + B + H, w_scale=0.2, dtype=dtype, state=True)
+    x, W = gpu(d["x"], dtype), gpu(d["W"], dtype)
+    dH = gpu(d["dH_up"])
+    dhT, dcT = gpu(d["dhT"]), gpu(d["dcT"])
+    _, cache = L.fwd_cache(x, W, gpu(d["b"]), gpu(d["h0"]), gpu(d["c0"]))
+    torch.cuda.synchronize()
+    if struct is None:
+        outs = run_both(L, lambda: L.bwd_dense(x, W, cache, dH, dhT=dhT, dcT=dcT))
+        keys = ("dX", "dW", "db", "dh0", "dc0")
+    else:
+        kw = dict(struct)
+        outs = run_both(L, lambda: L.bwd_structsparse(x, W, cache, dH, sparsity=sp, dhT=dhT,
+                                                      dcT=dcT, **kw))
+        keys = ("dX", "dW", "db", "dh0", "dc0", "idx")
+    for k in keys:
+        assert torch.equal(outs[0][k], outs[1][k]), k
+    assert torch.isfinite(outs[0]["dW"]).all()
+
+
+def test_wgrad_dma_stack_same_bits(L):
+    # a two-layer stack call: the weight gradient runs in chunks of steps that
+    # continue from the stored dW
+    T, B, H, I0 = 14, 64, 64, 48
+    ds, xs, Ws, caches = [], [], [], []
+    inp = None
+    for l in range(2):
+        I = I0 if l == 0 else H
+        d = make_layer(T, B, I, H, seed=40 + l, w_scale=0.2)
+        x = gpu(d["x"]) if l == 0 else inp
+        W = gpu(d["W"])
+        h_out, cache = L.fwd_cache(x, W, gpu(d["b"]))
+        xs.append(x); Ws.append(W); caches.append(cache); ds.append(d)
+        inp = h_out
+    dH = gpu(ds[-1]["dH_up"])
+    torch.cuda.synchronize()
+
+    def call():
+        dWs = [torch.empty_like(w, dtype=torch.float32) for w in Ws]
+        dbs = [torch.empty(w.shape[0], dtype=torch.float32, device="cuda:0") for w in Ws]
+        dXs = [None, torch.empty((T, H, B), dtype=torch.float32, device="cuda:0")]
+        L.bwd_stack(xs, Ws, caches, dH, sparsity=0.5, dXs=dXs, dWs=dWs, dbs=dbs)
+        return dWs + dbs + dXs[1:]
+
+    a, b = run_both(L, call)
+    for u, v in zip(a, b):
+        assert torch.equal(u, v)
