@@ -121,11 +121,26 @@ struct G1Shape {
 // work-group gathers the rows of the slices that keep its block and skips
 // the others, W rows and gate-gradient rows alike (their products are exactly
 // zero, so the result is bit-identical to multiplying them).
+typedef __attribute__((address_space(3))) void lds_void_t;
+typedef __attribute__((address_space(1))) void glob_void_t;
+
+// DMA (fp32, whole 32-row k stages): the stages go from global memory
+// straight into LDS (global_load_lds_dwordx4) in the operands' own layout,
+// [k][m] and [k][n] with m, n contiguous, instead of being transposed through
+// registers; a lane then reads its one k of each MFMA operand with a 4-byte
+// read.  The 128-byte halves of every row are swapped in alternate groups of
+// 4 rows (k and k + 4 are read together), on the global side of the copy.
+// Columns past M or N are clamped to the last whole piece of the row (their
+// outputs are not stored).
+__device__ __forceinline__ int g1_swz(int k) { return ((k >> 2) & 1) * 8; }  // in 16-byte pieces
+
 template <typename TS, int TM, int TN, bool GATHER, bool VEC, bool ROWA = false, int NW = 4,
-          bool FN = false>
+          bool FN = false, bool DMA = false>
 __global__ __launch_bounds__(NW * 64) void gemm1_kernel(Gemm1Args a) {
     static_assert(!(ROWA && GATHER), "the forward products read every row");
     static_assert(!(FN && (GATHER || ROWA)), "the fine fast path reads every row");
+    static_assert(!DMA || (sizeof(TS) == 4 && !ROWA && !FN && VEC && NW == 4),
+                  "DMA stages: fp32 data-gradient products");
     constexpr int THREADS = NW * 64;  // shadows the file-wide default
     using SH = G1Shape<TS, TM, TN, NW>;
     constexpr bool BF = SH::BF;
@@ -254,8 +269,35 @@ __global__ __launch_bounds__(NW * 64) void gemm1_kernel(Gemm1Args a) {
         }
     };
 
-    __shared__ __align__(16) E As[2][TM][LDK];
-    __shared__ __align__(16) E Bs[2][TN][LDK];
+    __shared__ __align__(16) E As[2][DMA ? 1 : TM][LDK];
+    __shared__ __align__(16) E Bs[2][DMA ? 1 : TN][LDK];
+    __shared__ __align__(16) E Ad[2][DMA ? TK * TM : 1];  // DMA: [k][m]
+    __shared__ __align__(16) E Bd[2][DMA ? TK * TN : 1];  // DMA: [k][n]
+    // DMA copy of the stage starting at k0 into buffer b: instruction q fills
+    // bytes [1024 q, 1024 q + 1024) of Ad (q < NIA) or of Bd
+    constexpr int NIA = TK * TM / 256, NIB = TK * TN / 256, NIW = (NIA + NIB) / NW;
+    static_assert(!DMA || (NIA + NIB) % NW == 0, "DMA instruction split");
+    auto dload = [&](int k0, int b) {
+#pragma unroll
+        for (int i = 0; i < NIW; ++i) {
+            const int q = wave + NW * i;
+            const bool isa = q < NIA;
+            const int off = (isa ? q : q - NIA) * 256 + lane * 4;  // element offset in the stage
+            const int rowlen = isa ? TM : TN;
+            const int kl = off / rowlen, pc = (off - kl * rowlen) >> 2;
+            const int col = ((pc ^ g1_swz(kl)) << 2);  // first column this lane's slot holds
+            const TS *src;
+            if (isa) {
+                const int m = min(a.m_lo + mm0 + col, ((M - 1) & ~3));
+                src = W + (long)srow[k0 + kl - sc] * ldw + m;
+            } else {
+                const int n = min(n0 + col, N - 4);
+                src = G + (long)(k0 + kl) * N + n;
+            }
+            E *dst = isa ? &Ad[b][q * 256] : &Bd[b][(q - NIA) * 256];
+            __builtin_amdgcn_global_load_lds((glob_void_t *)src, (lds_void_t *)dst, 16, 0, 0);
+        }
+    };
     // column e of a group: its KB = 4 k values as one vector (k lowest first)
     auto put4 = [](E *dst, const V *r, int e) {
         if constexpr (BF) {
@@ -319,8 +361,13 @@ __global__ __launch_bounds__(NW * 64) void gemm1_kernel(Gemm1Args a) {
     const int mw = wm * MT * 32, nw = wn * NT * 32;  // wavefront tile origin
 
     __syncthreads();
-    load(kb);
-    stash(0);
+    if constexpr (DMA) {
+        dload(kb, 0);
+        __builtin_amdgcn_s_waitcnt(0);
+    } else {
+        load(kb);
+        stash(0);
+    }
     __syncthreads();
     int buf = 0;
     for (int k0 = kb; k0 < ke; k0 += TK) {
@@ -331,10 +378,42 @@ __global__ __launch_bounds__(NW * 64) void gemm1_kernel(Gemm1Args a) {
                 fill_rows(sc);
                 __syncthreads();
             }
-            load(k0 + TK);
+            if (!DMA)
+                load(k0 + TK);
         }
         const int half = lane >> 5;
-        if constexpr (!BF) {
+        if constexpr (DMA) {
+            // operand k of MFMA c of 8-k block b8: 8 b8 + c (lanes 0-31) and
+            // 8 b8 + 4 + c (lanes 32-63), as in the transposed layout
+            float av[TK / 8][4][MT], bv[TK / 8][4][NT];
+#pragma unroll
+            for (int b8 = 0; b8 < TK / 8; ++b8)
+#pragma unroll
+                for (int c = 0; c < 4; ++c) {
+                    const int k = 8 * b8 + 4 * half + c;
+#pragma unroll
+                    for (int i = 0; i < MT; ++i) {
+                        const int m = mw + i * 32 + (lane & 31);
+                        av[b8][c][i] = Ad[buf][k * TM + ((((m >> 2) ^ g1_swz(k))) << 2) + (m & 3)];
+                    }
+#pragma unroll
+                    for (int j = 0; j < NT; ++j) {
+                        const int n = nw + j * 32 + (lane & 31);
+                        bv[b8][c][j] = Bd[buf][k * TN + ((((n >> 2) ^ g1_swz(k))) << 2) + (n & 3)];
+                    }
+                }
+            if (next)  // the next stage streams in during the MFMAs
+                dload(k0 + TK, buf ^ 1);
+#pragma unroll
+            for (int b8 = 0; b8 < TK / 8; ++b8)
+#pragma unroll
+                for (int c = 0; c < 4; ++c)
+#pragma unroll
+                    for (int i = 0; i < MT; ++i)
+#pragma unroll
+                        for (int j = 0; j < NT; ++j)
+                            acc[i][j] = mfma32x32x2(av[b8][c][i], bv[b8][c][j], acc[i][j]);
+        } else if constexpr (!BF) {
             float4 av[TK / 8][MT], bv[TK / 8][NT];
 #pragma unroll
             for (int b8 = 0; b8 < TK / 8; ++b8) {
@@ -373,7 +452,9 @@ __global__ __launch_bounds__(NW * 64) void gemm1_kernel(Gemm1Args a) {
                     for (int j = 0; j < NT; ++j)
                         acc[i][j] = mfma32x32x16bf(av[kk][i], bv[kk][j], acc[i][j]);
         }
-        if (next)
+        if (DMA)  // the next stage's lines are in LDS before anyone reads them
+            __builtin_amdgcn_s_waitcnt(0);
+        else if (next)
             stash(buf ^ 1);
         __syncthreads();
         buf ^= 1;
@@ -543,8 +624,6 @@ __device__ __forceinline__ void lds_store_vec(E *dst, const V &v) {
 // output rows or columns that are never stored.
 __device__ __forceinline__ int wg_swz(int r) { return (r & 7) ^ ((r >> 3) & 1); }
 
-typedef __attribute__((address_space(3))) void lds_void_t;
-typedef __attribute__((address_space(1))) void glob_void_t;
 
 template <typename TS, bool SPARSE, int TT, int ATN, bool VEC, int BC, bool FN = false,
           bool DMA = false>
@@ -780,6 +859,60 @@ __global__ __launch_bounds__(THREADS, 2) void wgrad_kernel(WgradArgs a) {
     // register set it & 1 and stores chunk it + 1 (set and buffer
     // (it + 1) & 1); the loop runs in pairs so that the sets are static
     uint64_t fmask = ~0ull;  // FN: kept blocks of this wavefront's slice at the current step
+
+    // sparse routing: csrc[at] is the temporary column (kept row) that
+    // accumulator column at * 32 + lane pulls at the current step, -1 if its
+    // slice was dropped.  (Routing a step during the next step's first chunk,
+    // to overlap the permutes with MFMAs, measured no faster.)
+    int csrc[ATN];
+    auto lookup = [&](int tl) {
+        const int *tab = sidx[tl & 1][gi];
+#pragma unroll
+        for (int at = 0; at < ATN; ++at) {
+            const int col = at * 32 + (lane & 31);
+            int src = -1;
+            if (col < rcount) {
+                const int orow = r0 + col;
+                const int js = orow / a.P;
+                const int reg = (js - j0) / a.R;
+                const int e0 = reg * ks, e1 = min(e0 + ks, qcount);
+                for (int e = e0; e < e1; ++e)
+                    if (tab[e] == js)
+                        src = e * a.P + (orow - js * a.P);
+            }
+            csrc[at] = src;
+        }
+    };
+    // acc[:, at] += t routed by srcs (accumulator tiles past the group's rows
+    // have src -1 everywhere and stay zero)
+    auto route = [&](const f32x16 (&t)[WG_FT][TT], const int (&srcs)[ATN]) {
+#pragma unroll
+        for (int at = 0; at < ATN; ++at) {
+            const int src = srcs[at];
+            const int saddr = (((src < 0 ? 0 : src) & 31) + (lane & 32)) << 2;
+            const int stile = src < 0 ? 0 : (src >> 5);
+            // all lane permutes of this tile first, then the adds
+            float val[WG_FT][TT][16];
+#pragma unroll
+            for (int ft = 0; ft < WG_FT; ++ft)
+#pragma unroll
+                for (int tt = 0; tt < TT; ++tt)
+#pragma unroll
+                    for (int v = 0; v < 16; ++v)
+                        val[ft][tt][v] = __int_as_float(
+                            __builtin_amdgcn_ds_bpermute(saddr, __float_as_int(t[ft][tt][v])));
+#pragma unroll
+            for (int ft = 0; ft < WG_FT; ++ft)
+#pragma unroll
+                for (int v = 0; v < 16; ++v) {
+                    float w = val[ft][0][v];
+                    if (TT > 1)
+                        w = stile == 1 ? val[ft][TT > 1 ? 1 : 0][v] : w;
+                    acc[ft][at][v] += src < 0 ? 0.f : w;  // dropped: exactly 0, even for inf/NaN
+                }
+        }
+    };
+
     auto iter = [&](int it, auto sc) {
         constexpr int S0 = decltype(sc)::value, S1 = 1 - S0;
         const int buf = S0;
@@ -879,44 +1012,8 @@ __global__ __launch_bounds__(THREADS, 2) void wgrad_kernel(WgradArgs a) {
                         tmp[ft][0][v] = 0.f;
                     }
             } else {
-                const int *tab = sidx[tl & 1][gi];
-#pragma unroll
-                for (int at = 0; at < ATN; ++at) {
-                    if (at >= AT)
-                        break;
-                    const int col = at * 32 + (lane & 31);
-                    int src = -1;
-                    if (col < rcount) {
-                        const int orow = r0 + col;
-                        const int js = orow / a.P;
-                        const int reg = (js - j0) / a.R;
-                        const int e0 = reg * ks, e1 = min(e0 + ks, qcount);
-                        for (int e = e0; e < e1; ++e)
-                            if (tab[e] == js)
-                                src = e * a.P + (orow - js * a.P);
-                    }
-                    const int saddr = (((src < 0 ? 0 : src) & 31) + (lane & 32)) << 2;
-                    const int stile = src < 0 ? 0 : (src >> 5);
-                    // all lane permutes of this tile first, then the adds
-                    float val[WG_FT][TT][16];
-#pragma unroll
-                    for (int ft = 0; ft < WG_FT; ++ft)
-#pragma unroll
-                        for (int tt = 0; tt < TT; ++tt)
-#pragma unroll
-                            for (int v = 0; v < 16; ++v)
-                                val[ft][tt][v] = __int_as_float(
-                                    __builtin_amdgcn_ds_bpermute(saddr, __float_as_int(tmp[ft][tt][v])));
-#pragma unroll
-                    for (int ft = 0; ft < WG_FT; ++ft)
-#pragma unroll
-                        for (int v = 0; v < 16; ++v) {
-                            float w = val[ft][0][v];
-                            if (TT > 1)
-                                w = stile == 1 ? val[ft][TT > 1 ? 1 : 0][v] : w;
-                            acc[ft][at][v] += src < 0 ? 0.f : w;  // dropped: exactly 0, even for inf/NaN
-                        }
-                }
+                lookup(tl);
+                route(tmp, csrc);
 #pragma unroll
                 for (int ft = 0; ft < WG_FT; ++ft)
 #pragma unroll
@@ -1148,7 +1245,14 @@ int gemm1_wgs_per_cu(int tm, int tn) {
 }
 
 template <typename TS, int TM, int TN, bool GA, bool VE, bool ROWA = false>
-static void launch_g1(dim3 grid, const Gemm1Args &a, bool w8, hipStream_t s) {
+static void launch_g1(dim3 grid, const Gemm1Args &a, bool w8, hipStream_t s, bool dma = false) {
+    if constexpr (sizeof(TS) == 4 && VE && !ROWA && TN != 32) {
+        if (dma && !w8) {
+            hipLaunchKernelGGL((gemm1_kernel<TS, TM, TN, GA, true, false, 4, false, true>), grid,
+                               dim3(THREADS), 0, s, a);
+            return;
+        }
+    }
     if constexpr (!GA && !ROWA && TM == 128 && TN == 32) {
         if (a.fidx) {
             hipLaunchKernelGGL((gemm1_kernel<TS, 128, 32, false, VE, false, 4, true>), grid, dim3(THREADS), 0, s, a);
@@ -1188,8 +1292,15 @@ hipError_t launch_gemm1(Gemm1Args a, bool bf16, hipStream_t s) {
     const bool vec = a.ldw % vw == 0 && a.N % vw == 0;
     a.m_lo = vec ? a.m_begin / vw * vw : a.m_begin;
     const long z = (long)a.splitk * a.steps;
+    // DMA stages: fp32, whole 32-row stages, 16-byte aligned rows
+    const bool dma_shape = a.dma && !bf16 && vec && !a.fidx && a.Kp % 32 == 0 &&
+                           ((uintptr_t)a.W & 15) == 0 && ((uintptr_t)a.Gc & 15) == 0;
     int TM, TN;
     gemm1_tile(bf16, a.N, a.M - a.m_lo, z, &TM, &TN);
+    if (dma_shape && a.N > 32) {  // with DMA stages the 64 x 64 tile measured best throughout
+        TM = 64;
+        TN = 64;
+    }
     if (a.tm)
         TM = a.tm;
     if (a.tn)
@@ -1205,7 +1316,8 @@ hipError_t launch_gemm1(Gemm1Args a, bool bf16, hipStream_t s) {
     if (a.waves != 0 && a.waves != 4 && !(a.waves == 8 && TM == 128 && TN == 128))
         return hipErrorInvalidValue;
     const bool w8 = use_w8(a, bf16, TM, TN);
-#define LSTMSS_G1(TS, TMV, TNV, GA, VE) launch_g1<TS, TMV, TNV, GA, VE>(grid, a, w8, s)
+    const bool dma = dma_shape && TN != 32;
+#define LSTMSS_G1(TS, TMV, TNV, GA, VE) launch_g1<TS, TMV, TNV, GA, VE>(grid, a, w8, s, dma)
 #define LSTMSS_G1V(TS, TMV, TNV, GA) do { if (vec) LSTMSS_G1(TS, TMV, TNV, GA, true); else LSTMSS_G1(TS, TMV, TNV, GA, false); } while (0)
 #define LSTMSS_G1T(TS, GA) do { \
         if (TN == 32) LSTMSS_G1V(TS, 128, 32, GA); \

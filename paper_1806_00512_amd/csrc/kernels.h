@@ -72,6 +72,8 @@ struct Gemm1Args {
     const int32_t *fidx;
     int fkept;
     long fidx_step;
+    int dma;               // 1: fp32 stages go global -> LDS directly where the shape allows
+                           // (same bits as the register-staged loads of 0)
 };
 
 // Weight gradient dW[rows] += dG_c [x_t; h_{t-1}]^T (rows scattered by idx).

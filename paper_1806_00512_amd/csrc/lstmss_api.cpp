@@ -163,7 +163,7 @@ constexpr int kStackDxSteps = 12;
 // fine structure with 32 x 32 blocks: skip the removed blocks' products (1,
 // default) or run them on the zeros (0); results are the same bits
 bool g_fine_skip = true;
-bool g_wgrad_dma = true;
+bool g_gemm_dma = true;
 
 hipError_t stack_res(StackRes **out) {
     int dev = 0;
@@ -495,7 +495,7 @@ int32_t backward_enqueue(const lstmss_dims *d, bool dense, const Plan &p, const 
     wg.T = T; wg.I = I; wg.H = H; wg.B = B; wg.Kp = (int)p.Kp; wg.kept = (int)p.kept;
     wg.P = p.P; wg.R = p.R; wg.S = p.S; wg.dW = dW;
     wg.fidx = fblocks ? idx_all : nullptr; wg.fkept = fkept; wg.fskip = ffast ? 1 : 0;
-    wg.dma = g_wgrad_dma ? 1 : 0;
+    wg.dma = g_gemm_dma ? 1 : 0;
 
     Gemm1Args gx{};  // dX[t] = (W_c rows [0, I))^T dG_c, several steps per launch
     gx.W = W; gx.ldw = K; gx.P = p.P; gx.Kp = p.Kp; gx.M = I; gx.m_begin = 0; gx.N = B;
@@ -504,6 +504,7 @@ int32_t backward_enqueue(const lstmss_dims *d, bool dense, const Plan &p, const 
     gx.gc_step = p.Kp * B; gx.idx_step = p.kept; gx.out_step = (long)I * B;
     gx.tm = dx_tm; gx.tn = dx_tn;
     gx.fkept = fkept; gx.fidx_step = p.kept;
+    gx.dma = g_gemm_dma ? 1 : 0;
 
     const long part_stride = HB;
     for (int t = T - 1; t >= 0; --t) {
@@ -603,6 +604,7 @@ int32_t backward_enqueue(const lstmss_dims *d, bool dense, const Plan &p, const 
         g1.part = part; g1.part_stride = part_stride; g1.splitk = L.splitk;
         g1.k_chunk = L.k_chunk; g1.steps = 1;
         g1.fidx = ffast ? idx : nullptr; g1.fkept = fkept; g1.fidx_step = p.kept;
+        g1.dma = g_gemm_dma ? 1 : 0;
         HIP_TRY(timed(LSTMSS_KERNEL_DATA_GRAD, st, [&] { return launch_gemm1(g1, bf16, st); }));
 
         if (!batched) {
@@ -1224,7 +1226,7 @@ int32_t lstmss_set_option(int32_t option, int32_t value) {
     switch (option) {
     case LSTMSS_OPT_GRAPHS: g_graphs = value != 0; return LSTMSS_OK;
     case LSTMSS_OPT_FINE_SKIP: g_fine_skip = value != 0; return LSTMSS_OK;
-    case LSTMSS_OPT_WGRAD_DMA: g_wgrad_dma = value != 0; return LSTMSS_OK;
+    case LSTMSS_OPT_GEMM_DMA: g_gemm_dma = value != 0; return LSTMSS_OK;
     case LSTMSS_OPT_STACK_DX_STEPS:
         if (value < 0)
             return fail(LSTMSS_ERR_INVALID_ARG, "stack dX steps %d must be >= 0", value);

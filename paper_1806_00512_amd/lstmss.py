@@ -509,7 +509,7 @@ def cache_views(cache, T, B, H, dtype):
     return gates, c, h
 
 
-OPTIONS = {"graphs": 0, "side_stream": 1, "stack_dx_steps": 2, "fine_skip": 3, "wgrad_dma": 4}
+OPTIONS = {"graphs": 0, "side_stream": 1, "stack_dx_steps": 2, "fine_skip": 3, "gemm_dma": 4}
 
 
 def set_option(name: str, value: int):

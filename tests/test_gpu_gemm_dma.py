@@ -1,11 +1,13 @@
-"""Weight-gradient chunk loads straight into LDS (LSTMSS_OPT_WGRAD_DMA) give
-the same bits as the register-staged loads, through the C ABI.
+"""Operand tiles loaded straight into LDS (LSTMSS_OPT_GEMM_DMA) give the same
+bits as the register-staged loads, in both gradient products, through the C
+ABI.
 
-The direct loads apply when B is a multiple of 32 (fp32) or 64 (bf16); rows
-and features past the ends of the operands are clamped to valid rows, so the
-cases include ragged row groups (H not a multiple of 16), feature tiles that
-end inside a tile (I + H not a multiple of 128), several batch chunks per
-step and several steps per launch.  Agreement with the oracle at the default
+Weight gradient: B a multiple of 32 (fp32) or 64 (bf16).  Data gradient:
+fp32, K' a multiple of 32.  Rows and columns past the ends of the operands
+are clamped to valid ones, so the cases include ragged row groups (H not a
+multiple of 16), tiles that end inside the operands (I + H not a multiple of
+the tile), several batch chunks per step, several steps per launch and gathered
+rows spanning more than one table refill (K' > 2048).  Agreement with the oracle at the default
 setting is covered by the parity tests; here both settings must agree bit for
 bit on dX, dW, db, dh0, dc0 and the kept indices.
 """
@@ -35,11 +37,11 @@ def run_both(L, fn):
     outs = []
     try:
         for dma in (1, 0):
-            L.set_option("wgrad_dma", dma)
+            L.set_option("gemm_dma", dma)
             outs.append(fn())
             torch.cuda.synchronize()
     finally:
-        L.set_option("wgrad_dma", 1)
+        L.set_option("gemm_dma", 1)
     return outs
 
 
@@ -52,8 +54,11 @@ def run_both(L, fn):
     (3, 64, 64, 40, 0.0, "bf16", None),                 # dense bf16, ragged rows
     (3, 128, 64, 64, 0.5, "f32", {"kind": 1, "My": 32, "Mx": 32}),  # 32 x 32 fine blocks
     (3, 70, 40, 64, 0.5, "f32", {"P": 4, "R": 8}),      # ragged B: staged loads either way
+    (2, 64, 96, 1096, 0.0, "f32", None),                # dense, K' = 4384 > 2048 gathered rows
+    (2, 32, 64, 1088, 0.25, "f32", {"P": 4, "R": 8}),   # K' = 3264: table refills, ragged tiles
+    (3, 20, 40, 72, 0.5, "f32", {"P": 4, "R": 8}),      # K' = 144: a 16-row tail, staged either way
 ])
-def test_wgrad_dma_same_bits(L, T, B, I, H, sp, dtype, struct):
+def test_gemm_dma_same_bits(L, T, B, I, H, sp, dtype, struct):
     d = make_layer(T, B, I, H, seed=11 * T + B + H, w_scale=0.2, dtype=dtype, state=True)
     x, W = gpu(d["x"], dtype), gpu(d["W"], dtype)
     dH = gpu(d["dH_up"])
@@ -73,7 +78,7 @@ def test_wgrad_dma_same_bits(L, T, B, I, H, sp, dtype, struct):
     assert torch.isfinite(outs[0]["dW"]).all()
 
 
-def test_wgrad_dma_stack_same_bits(L):
+def test_gemm_dma_stack_same_bits(L):
     # a two-layer stack call: the weight gradient runs in chunks of steps that
     # continue from the stored dW
     T, B, H, I0 = 14, 64, 64, 48
