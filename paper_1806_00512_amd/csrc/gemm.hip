@@ -625,9 +625,17 @@ __device__ __forceinline__ void lds_store_vec(E *dst, const V &v) {
 __device__ __forceinline__ int wg_swz(int r) { return (r & 7) ^ ((r >> 3) & 1); }
 
 
+// Sparse fp32 with DMA chunks and one 32-row temporary tile: operands staged
+// half a chunk at a time and three wavefronts per SIMD (register-bound
+// otherwise at two; measured 4 % faster at H = 2048 despite 36 bytes of
+// spilled registers per lane).
+template <typename TS, bool SPARSE, bool DMA, int TT, int ATN>
+constexpr bool wg_splitop() { return SPARSE && DMA && sizeof(TS) == 4 && TT == 1 && ATN <= 2; }
+
 template <typename TS, bool SPARSE, int TT, int ATN, bool VEC, int BC, bool FN = false,
           bool DMA = false>
-__global__ __launch_bounds__(THREADS, 2) void wgrad_kernel(WgradArgs a) {
+__global__ __launch_bounds__(THREADS, (wg_splitop<TS, SPARSE, DMA, TT, ATN>() ? 3 : 2)) void wgrad_kernel(WgradArgs a) {
+    constexpr bool SPLITOP = wg_splitop<TS, SPARSE, DMA, TT, ATN>();
     static_assert(!(FN && (SPARSE || BC != 32 || TT != 1)), "fine chunks are 32-column blocks");
     static_assert(!DMA || (BC * sizeof(TS) == 128 && VEC), "DMA chunks are 128-byte lines");
     using E = typename std::conditional<sizeof(TS) == 4, float, uint16_t>::type;
@@ -891,25 +899,24 @@ __global__ __launch_bounds__(THREADS, 2) void wgrad_kernel(WgradArgs a) {
             const int src = srcs[at];
             const int saddr = (((src < 0 ? 0 : src) & 31) + (lane & 32)) << 2;
             const int stile = src < 0 ? 0 : (src >> 5);
-            // all lane permutes of this tile first, then the adds
-            float val[WG_FT][TT][16];
 #pragma unroll
-            for (int ft = 0; ft < WG_FT; ++ft)
+            for (int ft = 0; ft < WG_FT; ++ft) {
+                // all lane permutes of this feature tile first, then the adds
+                float val[TT][16];
 #pragma unroll
                 for (int tt = 0; tt < TT; ++tt)
 #pragma unroll
                     for (int v = 0; v < 16; ++v)
-                        val[ft][tt][v] = __int_as_float(
+                        val[tt][v] = __int_as_float(
                             __builtin_amdgcn_ds_bpermute(saddr, __float_as_int(t[ft][tt][v])));
 #pragma unroll
-            for (int ft = 0; ft < WG_FT; ++ft)
-#pragma unroll
                 for (int v = 0; v < 16; ++v) {
-                    float w = val[ft][0][v];
+                    float w = val[0][v];
                     if (TT > 1)
-                        w = stile == 1 ? val[ft][TT > 1 ? 1 : 0][v] : w;
+                        w = stile == 1 ? val[TT > 1 ? 1 : 0][v] : w;
                     acc[ft][at][v] += src < 0 ? 0.f : w;  // dropped: exactly 0, even for inf/NaN
                 }
+            }
         }
     };
 
@@ -948,6 +955,35 @@ __global__ __launch_bounds__(THREADS, 2) void wgrad_kernel(WgradArgs a) {
         if (!run) {
             // removed block: its products are zero
             issue_next();
+        } else if constexpr (sizeof(TS) == 4 && SPLITOP) {
+            // operands of half the chunk at a time (fewer live registers)
+            issue_next();  // the next chunks stream in during the MFMAs
+#pragma unroll
+            for (int sh = 0; sh < HALF / 4; sh += 2) {
+                float4 av[2][WG_FT], bv[2][TT];
+#pragma unroll
+                for (int s2 = 0; s2 < 2; ++s2) {
+#pragma unroll
+                    for (int ft = 0; ft < WG_FT; ++ft) {
+                        const int r = fh * 64 + ft * 32 + (lane & 31);
+                        av[s2][ft] = *(const float4 *)&sX[buf][r][pcol(r, hb / 4 + sh + s2)];
+                    }
+#pragma unroll
+                    for (int tt = 0; tt < TT; ++tt) {
+                        const int r = gi * GROWS + tt * 32 + (lane & 31);
+                        bv[s2][tt] = *(const float4 *)&sG[buf][r][pcol(r, hb / 4 + sh + s2)];
+                    }
+                }
+#pragma unroll
+                for (int s2 = 0; s2 < 2; ++s2)
+#pragma unroll
+                    for (int c4 = 0; c4 < 4; ++c4)
+#pragma unroll
+                        for (int ft = 0; ft < WG_FT; ++ft)
+#pragma unroll
+                            for (int tt = 0; tt < TT; ++tt)
+                                tmp[ft][tt] = mfma32x32x2(av[s2][ft][c4], bv[s2][tt][c4], tmp[ft][tt]);
+            }
         } else if constexpr (sizeof(TS) == 4) {
             float4 av[HALF / 4][WG_FT], bv[HALF / 4][TT];
 #pragma unroll
