@@ -175,3 +175,27 @@ def test_bidir_host_checks(L):
     assert n >= 2 * L.workspace_bytes(d, 0.5, s) + 2 * 4 * 32 * 8 * 4 + 2 * 4 * 16 * 8 * 4
     rc = lib.lstm_bwd_bidir(ctypes.byref(d), 0.5, ctypes.byref(s), *([None] * 15), 0, None)
     assert rc == -1
+
+
+def test_options_match_header_and_validate(L):
+    # the binding's option table is the header's enum; the setter validates
+    text = open(HEADER).read()
+    enum = dict((k, int(v)) for k, v in re.findall(r"LSTMSS_OPT_(\w+)\s*=\s*(\d+)", text))
+    assert {k.lower(): v for k, v in enum.items()} == L.OPTIONS
+    lib = L.load()
+    defaults = {"graphs": 0 if os.environ.get("LSTMSS_GRAPHS") == "0" else 1, "side_stream": 2,
+                "stack_dx_steps": 0, "fine_skip": 1, "gemm_dma": 1}
+    assert set(defaults) == set(L.OPTIONS)
+    try:
+        for name in ("fine_skip", "gemm_dma", "graphs"):
+            for v in (0, 1):
+                assert lib.lstmss_set_option(L.OPTIONS[name], v) == 0
+        for v in (0, 1, 2):
+            assert lib.lstmss_set_option(L.OPTIONS["side_stream"], v) == 0
+        assert lib.lstmss_set_option(L.OPTIONS["side_stream"], 3) == -1
+        assert lib.lstmss_set_option(L.OPTIONS["stack_dx_steps"], -1) == -1
+        assert lib.lstmss_set_option(L.OPTIONS["stack_dx_steps"], 6) == 0
+        assert lib.lstmss_set_option(max(L.OPTIONS.values()) + 1, 1) == -1
+    finally:
+        for name, v in defaults.items():
+            assert lib.lstmss_set_option(L.OPTIONS[name], v) == 0
