@@ -492,6 +492,8 @@ template <typename TS>
 __global__ __launch_bounds__(64) void cell_select_kernel2(CellArgs a) {
     __shared__ double srowsq[256];
     __shared__ int sslot[64];
+    __shared__ int sinv[64];  // kept slice (local index) of each local slot
+    __shared__ int s_nkept;
     const int lane = threadIdx.x;
     const int B = a.B, P = a.P, R = a.R;
     const int nch = (B + 63) / 64;
@@ -537,41 +539,45 @@ __global__ __launch_bounds__(64) void cell_select_kernel2(CellArgs a) {
     const uint64_t below = ((j ? (~0ull >> (64 - j)) : 0ull)) & ~((ls ? (~0ull >> (64 - ls)) : 0ull));
     const int pos = __popcll(ball & below);
     int slot = -1;
+    // the group's kept slices fill a contiguous run of slots from slot0
+    // (regions start at multiples of R, each region's slots at R - S times
+    // its number)
+    const long slot0 = (j0 / R) * (R - a.S);
     if (keep) {
         slot = (int)((gj / R) * (R - a.S) + pos);
         a.idx[slot] = (int32_t)gj;
+        sinv[slot - slot0] = j;
     }
     if (valid)
         sslot[j] = slot;
+    if (lane == 0)
+        s_nkept = __popcll(ball);
     __syncthreads();
-    // copy the kept rows: lanes over (row, 16-byte vector) pairs, four
-    // loads in flight before their stores
+    // copy the kept rows into their contiguous slots: lanes over the
+    // destination's 16-byte vectors, eight loads in flight before their
+    // stores
     const int rowbytes = B * (int)sizeof(TS);
     if ((rowbytes & 15) == 0) {
-        const int rv = rowbytes / 16;
+        const int rv = rowbytes / 16, sv = P * rv;  // vectors per row / per slice
         const uint4 *__restrict__ src = (const uint4 *)a.stage + row0 * rv;
-        uint4 *__restrict__ dst = (uint4 *)a.dGc;
-        const int nv = nrows * rv;
-        for (int v0 = 0; v0 < nv; v0 += 4 * 64) {
-            uint4 buf[4];
-            long to[4];
+        uint4 *__restrict__ dst = (uint4 *)a.dGc + slot0 * sv;
+        const int nv = s_nkept * sv;
+        for (int v0 = 0; v0 < nv; v0 += 8 * 64) {
+            uint4 buf[8];
 #pragma unroll
-            for (int u = 0; u < 4; ++u) {
+            for (int u = 0; u < 8; ++u) {
                 const int v = v0 + u * 64 + lane;
-                to[u] = -1;
                 if (v < nv) {
-                    const int lr = v / rv, c = v - lr * rv;
-                    const int sl = sslot[lr / P];
-                    if (sl >= 0) {
-                        buf[u] = src[v];
-                        to[u] = ((long)sl * P + lr % P) * rv + c;
-                    }
+                    const int q = v / sv, r = v - q * sv;  // local slot, vector within it
+                    buf[u] = src[(long)sinv[q] * sv + r];
                 }
             }
 #pragma unroll
-            for (int u = 0; u < 4; ++u)
-                if (to[u] >= 0)
-                    dst[to[u]] = buf[u];
+            for (int u = 0; u < 8; ++u) {
+                const int v = v0 + u * 64 + lane;
+                if (v < nv)
+                    dst[v] = buf[u];
+            }
         }
     } else {
         const TS *src = (const TS *)a.stage + row0 * B;
