@@ -124,23 +124,36 @@ struct G1Shape {
 typedef __attribute__((address_space(3))) void lds_void_t;
 typedef __attribute__((address_space(1))) void glob_void_t;
 
-// DMA (fp32, whole 32-row k stages): the stages go from global memory
-// straight into LDS (global_load_lds_dwordx4) in the operands' own layout,
-// [k][m] and [k][n] with m, n contiguous, instead of being transposed through
-// registers; a lane then reads its one k of each MFMA operand with a 4-byte
-// read.  The 128-byte halves of every row are swapped in alternate groups of
-// 4 rows (k and k + 4 are read together), on the global side of the copy.
-// Columns past M or N are clamped to the last whole piece of the row (their
-// outputs are not stored).
+// DMA (whole k stages): the stages go from global memory straight into LDS
+// (global_load_lds_dwordx4) in the operands' own layout, [k][m] and [k][n]
+// with m, n contiguous, instead of being transposed through registers.
+//   fp32: a lane reads its one k of each MFMA operand with a 4-byte read; the
+//   128-byte halves of every row are swapped in alternate groups of 4 rows (k
+//   and k + 4 are read together).
+//   bf16 (128 x 128 tiles, eight wavefronts): a lane needs 8 consecutive k of
+//   one column, which two transposed reads (ds_read_b64_tr_b16) deliver: in
+//   each group of 16 lanes, lane s points at row kbase + s / 4, columns
+//   mbase + 4 (s % 4) .. + 3, and lane i receives rows kbase .. kbase + 3 of
+//   column mbase + i.  Row r's 16-byte pieces are permuted by g1_swz16(r), so
+//   that the 4 rows x 2 pieces a group reads, and the 16 pieces two groups
+//   read together, fall on distinct banks.
+// The permutations are applied on the global side of the copy.  Columns past
+// M or N are clamped to the last whole piece of the row (their outputs are
+// not stored).
 __device__ __forceinline__ int g1_swz(int k) { return ((k >> 2) & 1) * 8; }  // in 16-byte pieces
+__device__ __forceinline__ int g1_swz16(int k) { return ((k & 3) << 2) ^ (((k >> 1) & 1) << 1); }
+typedef __attribute__((__vector_size__(4 * sizeof(__bf16)))) __bf16 g1_bf16x4;
+typedef __attribute__((address_space(3))) g1_bf16x4 g1_lds_bf16x4;
+typedef short g1_s16x4 __attribute__((ext_vector_type(4)));
 
 template <typename TS, int TM, int TN, bool GATHER, bool VEC, bool ROWA = false, int NW = 4,
           bool FN = false, bool DMA = false>
 __global__ __launch_bounds__(NW * 64) void gemm1_kernel(Gemm1Args a) {
     static_assert(!(ROWA && GATHER), "the forward products read every row");
     static_assert(!(FN && (GATHER || ROWA)), "the fine fast path reads every row");
-    static_assert(!DMA || (sizeof(TS) == 4 && !ROWA && !FN && VEC && NW == 4),
-                  "DMA stages: fp32 data-gradient products");
+    static_assert(!DMA || (!ROWA && !FN && VEC &&
+                           (sizeof(TS) == 4 ? NW == 4 : (NW == 8 && TM == 128 && TN == 128))),
+                  "DMA stages: fp32 products, or bf16 128 x 128 tiles of eight wavefronts");
     constexpr int THREADS = NW * 64;  // shadows the file-wide default
     using SH = G1Shape<TS, TM, TN, NW>;
     constexpr bool BF = SH::BF;
@@ -275,26 +288,28 @@ __global__ __launch_bounds__(NW * 64) void gemm1_kernel(Gemm1Args a) {
     __shared__ __align__(16) E Bd[2][DMA ? TK * TN : 1];  // DMA: [k][n]
     // DMA copy of the stage starting at k0 into buffer b: instruction q fills
     // bytes [1024 q, 1024 q + 1024) of Ad (q < NIA) or of Bd
-    constexpr int NIA = TK * TM / 256, NIB = TK * TN / 256, NIW = (NIA + NIB) / NW;
+    constexpr int PEL = 16 / (int)sizeof(E), IEL = 1024 / (int)sizeof(E);  // elements per piece / instruction
+    constexpr int NIA = TK * TM / IEL, NIB = TK * TN / IEL, NIW = (NIA + NIB) / NW;
     static_assert(!DMA || (NIA + NIB) % NW == 0, "DMA instruction split");
+    auto swz = [](int k) { return BF ? g1_swz16(k) : g1_swz(k); };
     auto dload = [&](int k0, int b) {
 #pragma unroll
         for (int i = 0; i < NIW; ++i) {
             const int q = wave + NW * i;
             const bool isa = q < NIA;
-            const int off = (isa ? q : q - NIA) * 256 + lane * 4;  // element offset in the stage
+            const int off = (isa ? q : q - NIA) * IEL + lane * PEL;  // element offset in the stage
             const int rowlen = isa ? TM : TN;
-            const int kl = off / rowlen, pc = (off - kl * rowlen) >> 2;
-            const int col = ((pc ^ g1_swz(kl)) << 2);  // first column this lane's slot holds
+            const int kl = off / rowlen, pc = (off - kl * rowlen) / PEL;
+            const int col = (pc ^ swz(kl)) * PEL;  // first column this lane's slot holds
             const TS *src;
             if (isa) {
-                const int m = min(a.m_lo + mm0 + col, ((M - 1) & ~3));
+                const int m = min(a.m_lo + mm0 + col, ((M - 1) & ~(PEL - 1)));
                 src = W + (long)srow[k0 + kl - sc] * ldw + m;
             } else {
-                const int n = min(n0 + col, N - 4);
+                const int n = min(n0 + col, N - PEL);
                 src = G + (long)(k0 + kl) * N + n;
             }
-            E *dst = isa ? &Ad[b][q * 256] : &Bd[b][(q - NIA) * 256];
+            E *dst = isa ? &Ad[b][q * IEL] : &Bd[b][(q - NIA) * IEL];
             __builtin_amdgcn_global_load_lds((glob_void_t *)src, (lds_void_t *)dst, 16, 0, 0);
         }
     };
@@ -382,7 +397,51 @@ __global__ __launch_bounds__(NW * 64) void gemm1_kernel(Gemm1Args a) {
                 load(k0 + TK);
         }
         const int half = lane >> 5;
-        if constexpr (DMA) {
+        if constexpr (DMA && BF) {
+            // two transposed reads per operand and 16-k block: rows
+            // 16 kk + 8 half + 4 h + (0..3) of column (lane % 32)
+            const int g = lane >> 4, sl = lane & 15;
+            auto trd = [](const E *p) {
+                return __builtin_bit_cast(
+                    g1_s16x4, __builtin_amdgcn_ds_read_tr16_b64_v4bf16((g1_lds_bf16x4 *)(p)));
+            };
+            u16x8 av[TK / 16][MT], bv[TK / 16][NT];
+#pragma unroll
+            for (int kk = 0; kk < TK / 16; ++kk) {
+                g1_s16x4 ra[2][MT], rb[2][NT];
+#pragma unroll
+                for (int h = 0; h < 2; ++h) {
+                    const int k = 16 * kk + 8 * (g >> 1) + 4 * h + (sl >> 2);
+#pragma unroll
+                    for (int i = 0; i < MT; ++i) {
+                        const int m = mw + i * 32 + 16 * (g & 1) + 4 * (sl & 3);
+                        ra[h][i] = trd(&Ad[buf][k * TM + (((m >> 3) ^ g1_swz16(k)) << 3) + (m & 7)]);
+                    }
+#pragma unroll
+                    for (int j = 0; j < NT; ++j) {
+                        const int n = nw + j * 32 + 16 * (g & 1) + 4 * (sl & 3);
+                        rb[h][j] = trd(&Bd[buf][k * TN + (((n >> 3) ^ g1_swz16(k)) << 3) + (n & 7)]);
+                    }
+                }
+#pragma unroll
+                for (int i = 0; i < MT; ++i)
+                    av[kk][i] = __builtin_bit_cast(
+                        u16x8, __builtin_shufflevector(ra[0][i], ra[1][i], 0, 1, 2, 3, 4, 5, 6, 7));
+#pragma unroll
+                for (int j = 0; j < NT; ++j)
+                    bv[kk][j] = __builtin_bit_cast(
+                        u16x8, __builtin_shufflevector(rb[0][j], rb[1][j], 0, 1, 2, 3, 4, 5, 6, 7));
+            }
+            if (next)  // the next stage streams in during the MFMAs
+                dload(k0 + TK, buf ^ 1);
+#pragma unroll
+            for (int kk = 0; kk < TK / 16; ++kk)
+#pragma unroll
+                for (int i = 0; i < MT; ++i)
+#pragma unroll
+                    for (int j = 0; j < NT; ++j)
+                        acc[i][j] = mfma32x32x16bf(av[kk][i], bv[kk][j], acc[i][j]);
+        } else if constexpr (DMA) {
             // operand k of MFMA c of 8-k block b8: 8 b8 + c (lanes 0-31) and
             // 8 b8 + 4 + c (lanes 32-63), as in the transposed layout
             float av[TK / 8][4][MT], bv[TK / 8][4][NT];
@@ -1289,6 +1348,13 @@ static void launch_g1(dim3 grid, const Gemm1Args &a, bool w8, hipStream_t s, boo
             return;
         }
     }
+    if constexpr (sizeof(TS) == 2 && VE && !ROWA && TM == 128 && TN == 128) {
+        if (dma && w8) {
+            hipLaunchKernelGGL((gemm1_kernel<TS, 128, 128, GA, true, false, 8, false, true>), grid,
+                               dim3(512), 0, s, a);
+            return;
+        }
+    }
     if constexpr (!GA && !ROWA && TM == 128 && TN == 32) {
         if (a.fidx) {
             hipLaunchKernelGGL((gemm1_kernel<TS, 128, 32, false, VE, false, 4, true>), grid, dim3(THREADS), 0, s, a);
@@ -1328,12 +1394,12 @@ hipError_t launch_gemm1(Gemm1Args a, bool bf16, hipStream_t s) {
     const bool vec = a.ldw % vw == 0 && a.N % vw == 0;
     a.m_lo = vec ? a.m_begin / vw * vw : a.m_begin;
     const long z = (long)a.splitk * a.steps;
-    // DMA stages: fp32, whole 32-row stages, 16-byte aligned rows
-    const bool dma_shape = a.dma && !bf16 && vec && !a.fidx && a.Kp % 32 == 0 &&
+    // DMA stages: whole k stages (32 fp32 or 64 bf16 rows), 16-byte aligned rows
+    const bool dma_shape = a.dma && vec && !a.fidx && a.Kp % (bf16 ? 64 : 32) == 0 &&
                            ((uintptr_t)a.W & 15) == 0 && ((uintptr_t)a.Gc & 15) == 0;
     int TM, TN;
     gemm1_tile(bf16, a.N, a.M - a.m_lo, z, &TM, &TN);
-    if (dma_shape && a.N > 32) {  // with DMA stages the 64 x 64 tile measured best throughout
+    if (dma_shape && !bf16 && a.N > 32) {  // fp32 DMA stages: the 64 x 64 tile measured best throughout
         TM = 64;
         TN = 64;
     }
@@ -1352,7 +1418,7 @@ hipError_t launch_gemm1(Gemm1Args a, bool bf16, hipStream_t s) {
     if (a.waves != 0 && a.waves != 4 && !(a.waves == 8 && TM == 128 && TN == 128))
         return hipErrorInvalidValue;
     const bool w8 = use_w8(a, bf16, TM, TN);
-    const bool dma = dma_shape && TN != 32;
+    const bool dma = dma_shape && (bf16 ? (w8 && TM == 128 && TN == 128) : TN != 32);
 #define LSTMSS_G1(TS, TMV, TNV, GA, VE) launch_g1<TS, TMV, TNV, GA, VE>(grid, a, w8, s, dma)
 #define LSTMSS_G1V(TS, TMV, TNV, GA) do { if (vec) LSTMSS_G1(TS, TMV, TNV, GA, true); else LSTMSS_G1(TS, TMV, TNV, GA, false); } while (0)
 #define LSTMSS_G1T(TS, GA) do { \
