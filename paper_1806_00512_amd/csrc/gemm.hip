@@ -142,6 +142,10 @@ typedef __attribute__((address_space(1))) void glob_void_t;
 // not stored).
 __device__ __forceinline__ int g1_swz(int k) { return ((k >> 2) & 1) * 8; }  // in 16-byte pieces
 __device__ __forceinline__ int g1_swz16(int k) { return ((k & 3) << 2) ^ (((k >> 1) & 1) << 1); }
+// ROWA (forward products): the first operand's rows are k-contiguous 128-byte
+// lines ([m][k], TK elements), read 16 bytes at a time like the weight
+// gradient's; piece c of row r sits at c ^ g1_swzr(r).
+__device__ __forceinline__ int g1_swzr(int r) { return (r & 7) ^ ((r >> 3) & 1); }
 typedef __attribute__((__vector_size__(4 * sizeof(__bf16)))) __bf16 g1_bf16x4;
 typedef __attribute__((address_space(3))) g1_bf16x4 g1_lds_bf16x4;
 typedef short g1_s16x4 __attribute__((ext_vector_type(4)));
@@ -151,7 +155,7 @@ template <typename TS, int TM, int TN, bool GATHER, bool VEC, bool ROWA = false,
 __global__ __launch_bounds__(NW * 64) void gemm1_kernel(Gemm1Args a) {
     static_assert(!(ROWA && GATHER), "the forward products read every row");
     static_assert(!(FN && (GATHER || ROWA)), "the fine fast path reads every row");
-    static_assert(!DMA || (!ROWA && !FN && VEC &&
+    static_assert(!DMA || (!FN && VEC &&
                            (sizeof(TS) == 4 ? NW == 4 : (NW == 8 && TM == 128 && TN == 128))),
                   "DMA stages: fp32 products, or bf16 128 x 128 tiles of eight wavefronts");
     constexpr int THREADS = NW * 64;  // shadows the file-wide default
@@ -302,7 +306,12 @@ __global__ __launch_bounds__(NW * 64) void gemm1_kernel(Gemm1Args a) {
             const int kl = off / rowlen, pc = (off - kl * rowlen) / PEL;
             const int col = (pc ^ swz(kl)) * PEL;  // first column this lane's slot holds
             const TS *src;
-            if (isa) {
+            if (isa && ROWA) {
+                // row kl' = off / TK of the [m][k] tile, piece pc' of it
+                const int ml = off / TK, pr = (off - ml * TK) / PEL;
+                const int m = min(mm0 + ml, M - 1);
+                src = W + (long)m * ldw + a.kcol0 + k0 + (pr ^ g1_swzr(ml)) * PEL;
+            } else if (isa) {
                 const int m = min(a.m_lo + mm0 + col, ((M - 1) & ~(PEL - 1)));
                 src = W + (long)srow[k0 + kl - sc] * ldw + m;
             } else {
@@ -414,6 +423,8 @@ __global__ __launch_bounds__(NW * 64) void gemm1_kernel(Gemm1Args a) {
                     const int k = 16 * kk + 8 * (g >> 1) + 4 * h + (sl >> 2);
 #pragma unroll
                     for (int i = 0; i < MT; ++i) {
+                        if constexpr (ROWA)
+                            break;  // k-contiguous rows: one 16-byte read below
                         const int m = mw + i * 32 + 16 * (g & 1) + 4 * (sl & 3);
                         ra[h][i] = trd(&Ad[buf][k * TM + (((m >> 3) ^ g1_swz16(k)) << 3) + (m & 7)]);
                     }
@@ -424,9 +435,15 @@ __global__ __launch_bounds__(NW * 64) void gemm1_kernel(Gemm1Args a) {
                     }
                 }
 #pragma unroll
-                for (int i = 0; i < MT; ++i)
-                    av[kk][i] = __builtin_bit_cast(
-                        u16x8, __builtin_shufflevector(ra[0][i], ra[1][i], 0, 1, 2, 3, 4, 5, 6, 7));
+                for (int i = 0; i < MT; ++i) {
+                    if constexpr (ROWA) {
+                        const int m = mw + i * 32 + (lane & 31);
+                        av[kk][i] = *(const u16x8 *)&Ad[buf][m * TK + (((2 * kk + half) ^ g1_swzr(m)) << 3)];
+                    } else {
+                        av[kk][i] = __builtin_bit_cast(
+                            u16x8, __builtin_shufflevector(ra[0][i], ra[1][i], 0, 1, 2, 3, 4, 5, 6, 7));
+                    }
+                }
 #pragma unroll
                 for (int j = 0; j < NT; ++j)
                     bv[kk][j] = __builtin_bit_cast(
@@ -445,6 +462,20 @@ __global__ __launch_bounds__(NW * 64) void gemm1_kernel(Gemm1Args a) {
             // operand k of MFMA c of 8-k block b8: 8 b8 + c (lanes 0-31) and
             // 8 b8 + 4 + c (lanes 32-63), as in the transposed layout
             float av[TK / 8][4][MT], bv[TK / 8][4][NT];
+            if constexpr (ROWA) {  // k-contiguous rows: one 16-byte read per 8-k block
+#pragma unroll
+                for (int b8 = 0; b8 < TK / 8; ++b8)
+#pragma unroll
+                    for (int i = 0; i < MT; ++i) {
+                        const int m = mw + i * 32 + (lane & 31);
+                        const float4 v =
+                            *(const float4 *)&Ad[buf][m * TK + (((2 * b8 + half) ^ g1_swzr(m)) << 2)];
+                        av[b8][0][i] = v.x;
+                        av[b8][1][i] = v.y;
+                        av[b8][2][i] = v.z;
+                        av[b8][3][i] = v.w;
+                    }
+            }
 #pragma unroll
             for (int b8 = 0; b8 < TK / 8; ++b8)
 #pragma unroll
@@ -452,6 +483,8 @@ __global__ __launch_bounds__(NW * 64) void gemm1_kernel(Gemm1Args a) {
                     const int k = 8 * b8 + 4 * half + c;
 #pragma unroll
                     for (int i = 0; i < MT; ++i) {
+                        if constexpr (ROWA)
+                            break;
                         const int m = mw + i * 32 + (lane & 31);
                         av[b8][c][i] = Ad[buf][k * TM + ((((m >> 2) ^ g1_swz(k))) << 2) + (m & 3)];
                     }
@@ -1341,16 +1374,16 @@ int gemm1_wgs_per_cu(int tm, int tn) {
 
 template <typename TS, int TM, int TN, bool GA, bool VE, bool ROWA = false>
 static void launch_g1(dim3 grid, const Gemm1Args &a, bool w8, hipStream_t s, bool dma = false) {
-    if constexpr (sizeof(TS) == 4 && VE && !ROWA && TN != 32) {
+    if constexpr (sizeof(TS) == 4 && VE && TN != 32) {
         if (dma && !w8) {
-            hipLaunchKernelGGL((gemm1_kernel<TS, TM, TN, GA, true, false, 4, false, true>), grid,
+            hipLaunchKernelGGL((gemm1_kernel<TS, TM, TN, GA, true, ROWA, 4, false, true>), grid,
                                dim3(THREADS), 0, s, a);
             return;
         }
     }
-    if constexpr (sizeof(TS) == 2 && VE && !ROWA && TM == 128 && TN == 128) {
+    if constexpr (sizeof(TS) == 2 && VE && TM == 128 && TN == 128) {
         if (dma && w8) {
-            hipLaunchKernelGGL((gemm1_kernel<TS, 128, 128, GA, true, false, 8, false, true>), grid,
+            hipLaunchKernelGGL((gemm1_kernel<TS, 128, 128, GA, true, ROWA, 8, false, true>), grid,
                                dim3(512), 0, s, a);
             return;
         }
@@ -1440,8 +1473,16 @@ hipError_t launch_gemm_fwd(Gemm1Args a, bool bf16, hipStream_t s) {
     const bool vec = a.ldw % vw == 0 && a.kcol0 % vw == 0 && a.N % vw == 0;
     a.m_lo = 0;
     const long z = (long)a.splitk * a.steps;
+    // DMA stages: whole k stages of the product (K' = a.Kp rows), 16-byte aligned rows
+    const bool dma_shape = a.dma && vec && a.Kp % (bf16 ? 64 : 32) == 0 &&
+                           a.k_chunk % (bf16 ? 64 : 32) == 0 && ((uintptr_t)a.W & 15) == 0 &&
+                           ((uintptr_t)a.Gc & 15) == 0;
     int TM, TN;
     gemm1_tile(bf16, a.N, a.M, z, &TM, &TN);
+    if (dma_shape && !bf16 && a.N > 32) {  // fp32 DMA stages: 64 x 64 tiles, as in launch_gemm1
+        TM = 64;
+        TN = 64;
+    }
     if (a.tm)
         TM = a.tm;
     if (a.tn)
@@ -1452,7 +1493,8 @@ hipError_t launch_gemm_fwd(Gemm1Args a, bool bf16, hipStream_t s) {
     if (a.waves != 0 && a.waves != 4 && !(a.waves == 8 && TM == 128 && TN == 128))
         return hipErrorInvalidValue;
     const bool w8 = use_w8(a, bf16, TM, TN);
-#define LSTMSS_GF(TS, TMV, TNV, VE) launch_g1<TS, TMV, TNV, false, VE, true>(grid, a, w8, s)
+    const bool dma = dma_shape && (bf16 ? (w8 && TM == 128 && TN == 128) : TN != 32);
+#define LSTMSS_GF(TS, TMV, TNV, VE) launch_g1<TS, TMV, TNV, false, VE, true>(grid, a, w8, s, dma)
 #define LSTMSS_GFV(TS, TMV, TNV) do { if (vec) LSTMSS_GF(TS, TMV, TNV, true); else LSTMSS_GF(TS, TMV, TNV, false); } while (0)
 #define LSTMSS_GFT(TS) do { \
         if (TN == 32) LSTMSS_GFV(TS, 128, 32); \

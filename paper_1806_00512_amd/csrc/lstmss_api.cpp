@@ -1107,6 +1107,7 @@ int32_t lstm_fwd_cache(const lstmss_dims *d, const void *x, const void *W, const
     gi.N = d->B; gi.out_row0 = 0; gi.part = zx; gi.part_stride = 0; gi.splitk = 1;
     gi.k_chunk = ceil_div((long)d->I, GEMM1_TK) * GEMM1_TK; gi.steps = d->T;
     gi.gc_step = (long)d->I * d->B; gi.out_step = G * d->B;
+    gi.dma = g_gemm_dma ? 1 : 0;
     HIP_TRY(timed(LSTMSS_KERNEL_FORWARD, st, [&] { return launch_gemm_fwd(gi, bf16, st); }));
     for (int t = 0; t < d->T; ++t) {
         // recurrent product W_h h_{t-1}, split over k
@@ -1114,7 +1115,7 @@ int32_t lstm_fwd_cache(const lstmss_dims *d, const void *x, const void *W, const
         gr.W = W; gr.ldw = K; gr.kcol0 = d->I; gr.Gc = hst + (size_t)t * HB * es; gr.Kp = d->H;
         gr.M = (int)G; gr.m_begin = 0; gr.N = d->B; gr.out_row0 = 0; gr.part = part;
         gr.part_stride = G * d->B; gr.splitk = F.splitk; gr.k_chunk = F.k_chunk; gr.steps = 1;
-        gr.tm = F.tm; gr.tn = F.tn;
+        gr.tm = F.tm; gr.tn = F.tn; gr.dma = g_gemm_dma ? 1 : 0;
         HIP_TRY(timed(LSTMSS_KERNEL_FORWARD, st, [&] { return launch_gemm_fwd(gr, bf16, st); }));
         FwdActArgs fa{};
         fa.zx = zx + (size_t)t * G * d->B;

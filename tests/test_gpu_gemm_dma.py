@@ -105,3 +105,19 @@ def test_gemm_dma_stack_same_bits(L):
     a, b = run_both(L, call)
     for u, v in zip(a, b):
         assert torch.equal(u, v)
+
+
+@pytest.mark.parametrize("T,B,I,H,dtype", [
+    (4, 64, 96, 64, "f32"),     # both forward products take DMA stages
+    (3, 128, 40, 96, "f32"),    # I not a multiple of 32: staged input projection
+    (3, 128, 64, 128, "bf16"),  # 128 x 128 bf16 tiles
+    (2, 128, 72, 64, "bf16"),   # I not a multiple of 64: staged input projection
+])
+def test_gemm_dma_forward_same_bits(L, T, B, I, H, dtype):
+    d = make_layer(T, B, I, H, seed=3 * T + B + I, w_scale=0.2, dtype=dtype, state=True)
+    x, W = gpu(d["x"], dtype), gpu(d["W"], dtype)
+    args = (x, W, gpu(d["b"]), gpu(d["h0"]), gpu(d["c0"]))
+    outs = run_both(L, lambda: L.fwd_cache(*args))
+    assert torch.equal(outs[0][0], outs[1][0])
+    assert torch.equal(outs[0][1], outs[1][1])
+    assert torch.isfinite(outs[0][0].float()).all()
