@@ -57,6 +57,7 @@ def run_both(L, fn):
     (2, 64, 96, 1096, 0.0, "f32", None),                # dense, K' = 4384 > 2048 gathered rows
     (2, 32, 64, 1088, 0.25, "f32", {"P": 4, "R": 8}),   # K' = 3264: table refills, ragged tiles
     (3, 20, 40, 72, 0.5, "f32", {"P": 4, "R": 8}),      # K' = 144: a 16-row tail, staged either way
+    (2, 128, 64, 1088, 0.5, "bf16", {"P": 4, "R": 8}),  # bf16, K' = 2176: splits and a table refill
 ])
 def test_gemm_dma_same_bits(L, T, B, I, H, sp, dtype, struct):
     d = make_layer(T, B, I, H, seed=11 * T + B + H, w_scale=0.2, dtype=dtype, state=True)
