@@ -35,7 +35,7 @@ sys.path.insert(0, ROOT)
 
 METRIC = "LSTM backward ms/step and effective TFLOP/s at 50% structured sparsity vs dense"
 DEFAULT_WORKLOAD = "lstm4_enc_h2048_b128_t50_f32"
-ALSO_WORKLOADS = ("lstm2_lm_h650_b20_t35_f32",)
+ALSO_WORKLOADS = ("lstm2_lm_h650_b20_t35_f32", "lstm2_h1024_b64_t35_f32")
 PEAK = {"hbm_gbs": 8000.0, "f32_tflops": 157.3, "bf16_tflops": 2516.6}
 KINDS = ("gates_select_compact", "data_grad_gemm", "weight_grad_gemm")
 # device kernel behind each timed kind whose HBM counters may be on file
@@ -368,6 +368,22 @@ def measure(L, torch, wl, sparsity, steps, warmup, sparse_only=False, kernels=Tr
     print("%s sequential layers: sparse %.4f, dense %.4f ms/step" % (wl.name, sq_ms, sqd_ms),
           file=sys.stderr, flush=True)
     res.update(sq_ms=sq_ms, sq_layer=sq_layer, sqd_ms=sqd_ms, sqd_layer=sqd_layer)
+    if wl.sweep:
+        # the workload's sparsity sweep (coarse structure, stack calls)
+        pts = []
+        for s in wl.sweep:
+            if s == 0.0:
+                ms = dn_ms
+            elif abs(s - sparsity) < 1e-9:
+                ms = sp_ms
+            else:
+                r.sparsity, r.stack_bufs = s, {}
+                ms, _, _ = r.timed([True], steps, warmup, stack=True)
+            pts.append((s, ms))
+            print("%s sweep sparsity %.2f: %.4f ms/step" % (wl.name, s, ms), file=sys.stderr,
+                  flush=True)
+        r.sparsity, r.stack_bufs = sparsity, {}
+        res["sweep"] = pts
     if not kernels:
         return res
     # the 9 sparse : 1 dense schedule (dense-after-sparse training phases)
@@ -424,6 +440,13 @@ def measure(L, torch, wl, sparsity, steps, warmup, sparse_only=False, kernels=Tr
         L.timing_enable(False)
         L.timing_reset()
     return res
+
+
+def sweep_entries(m):
+    """Sparsity sweep points of a measure() result: ms per step of the stack
+    call and its speedup over the dense call."""
+    return [{"sparsity": s, "ms_per_step": round(ms, 5),
+             "speedup_vs_dense": round(m["dn_ms"] / ms, 4)} for s, ms in m["sweep"]]
 
 
 def measure_training(L, torch, wl, sparsity, steps):
@@ -696,6 +719,8 @@ def main():
             result["fine_mfma_blocks"] = entry
         else:
             result["fine"] = entry
+    if "sweep" in m:
+        result["sparsity_sweep"] = sweep_entries(m)
     if not args.no_cpu_baseline:
         result["cpu_baseline"] = cpu_baseline(wl, m["runner"].inp, sparsity)
     del m
@@ -714,6 +739,8 @@ def main():
                                                            "dense": round(m2["sqd_ms"], 5)},
                          "value": round(flops_of(w2) / (m2["sp_ms"] / 1e3) / 1e12, 4),
                          "unit": "TFLOP/s"})
+            if "sweep" in m2:
+                also[-1]["sparsity_sweep"] = sweep_entries(m2)
             del m2
         result["also"] = also
     print(json.dumps(result), flush=True)

@@ -58,3 +58,15 @@ def test_dense_after_sparse_schedule():
     assert dense_after_sparse(3, 0.0) == [False] * 3
     with pytest.raises(ValueError):
         dense_after_sparse(4, 1.5)
+
+
+def test_sweep_entries_and_integer_removals():
+    # the H = 1024 workload's sweep removes a whole number of slices per region
+    wl = WORKLOADS["lstm2_h1024_b64_t35_f32"]
+    assert wl.sweep == (0.0, 0.25, 0.5, 0.75)
+    for s in wl.sweep:
+        assert abs(s * wl.R - round(s * wl.R)) < 1e-9
+    assert "lstm2_h1024_b64_t35_f32" in bench.ALSO_WORKLOADS
+    e = bench.sweep_entries({"dn_ms": 2.0, "sweep": [(0.0, 2.0), (0.5, 1.6), (0.75, 1.25)]})
+    assert [p["sparsity"] for p in e] == [0.0, 0.5, 0.75]
+    assert [p["speedup_vs_dense"] for p in e] == [1.0, 1.25, 1.6]
