@@ -290,13 +290,15 @@ int32_t lstmss_mse_grad(const lstmss_dims *d, const void *h, const float *y, flo
  *   LSTMSS_OPT_FINE_SKIP  FINE with Mx = My = 32 and fp32 storage: 1 (default) skips the
  *                      removed blocks' multiplications, 0 multiplies the
  *                      zeros (same bits; for checking and timing).
- *   LSTMSS_OPT_GEMM_DMA  1 (default): the gradient products load their
- *                      operand tiles from global memory straight into LDS
- *                      where the shape allows (weight gradient: B a multiple
- *                      of 32 for fp32 or 64 for bf16; data gradient: fp32,
- *                      K' a multiple of 32, I + H and B multiples of 4; the
- *                      operands 16-byte aligned); 0 stages them through
- *                      registers (same bits; for checking and timing).
+ *   LSTMSS_OPT_GEMM_DMA  1 (default): the products load their operand
+ *                      tiles from global memory straight into LDS where the
+ *                      shape allows (weight gradient: B a multiple of 32 for
+ *                      fp32 or 64 for bf16; data gradient and the forward
+ *                      products: the contraction length a multiple of 32
+ *                      (fp32) or 64 (bf16), rows a multiple of 16 bytes,
+ *                      bf16 only with B > 64; the operands 16-byte aligned);
+ *                      0 stages them through registers (same bits; for
+ *                      checking and timing).
  * Changing an option drops the recorded graphs.  Not for use while calls
  * are being enqueued from other threads. */
 enum {
