@@ -718,15 +718,18 @@ __device__ __forceinline__ int wg_swz(int r) { return (r & 7) ^ ((r >> 3) & 1); 
 
 
 // Sparse fp32 with DMA chunks and one 32-row temporary tile: operands staged
-// half a chunk at a time and three wavefronts per SIMD (register-bound
-// otherwise at two; measured 4 % faster at H = 2048 despite 36 bytes of
-// spilled registers per lane).
+// half a chunk at a time; with at most two accumulator tiles three wavefronts
+// per SIMD (register-bound otherwise at two; measured 4 % faster at H = 2048
+// despite 36 bytes of spilled registers per lane), with four (75 % sparsity)
+// two, which the half-chunk staging keeps from spilling.
 template <typename TS, bool SPARSE, bool DMA, int TT, int ATN>
-constexpr bool wg_splitop() { return SPARSE && DMA && sizeof(TS) == 4 && TT == 1 && ATN <= 2; }
+constexpr bool wg_splitop() { return SPARSE && DMA && sizeof(TS) == 4 && TT == 1; }
+template <typename TS, bool SPARSE, bool DMA, int TT, int ATN>
+constexpr int wg_occupancy() { return wg_splitop<TS, SPARSE, DMA, TT, ATN>() && ATN <= 2 ? 3 : 2; }
 
 template <typename TS, bool SPARSE, int TT, int ATN, bool VEC, int BC, bool FN = false,
           bool DMA = false>
-__global__ __launch_bounds__(THREADS, (wg_splitop<TS, SPARSE, DMA, TT, ATN>() ? 3 : 2)) void wgrad_kernel(WgradArgs a) {
+__global__ __launch_bounds__(THREADS, (wg_occupancy<TS, SPARSE, DMA, TT, ATN>())) void wgrad_kernel(WgradArgs a) {
     constexpr bool SPLITOP = wg_splitop<TS, SPARSE, DMA, TT, ATN>();
     static_assert(!(FN && (SPARSE || BC != 32 || TT != 1)), "fine chunks are 32-column blocks");
     static_assert(!DMA || (BC * sizeof(TS) == 128 && VEC), "DMA chunks are 128-byte lines");
