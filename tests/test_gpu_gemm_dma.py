@@ -122,3 +122,25 @@ def test_gemm_dma_forward_same_bits(L, T, B, I, H, dtype):
     assert torch.equal(outs[0][0], outs[1][0])
     assert torch.equal(outs[0][1], outs[1][1])
     assert torch.isfinite(outs[0][0].float()).all()
+
+
+def test_gemm_dma_misaligned_operands_fall_back(L):
+    # an input that starts 4 bytes into its allocation cannot be copied in
+    # 16-byte pieces: the products stage it through registers, same bits
+    T, B, I, H = 3, 64, 96, 64
+    d = make_layer(T, B, I, H, seed=77, w_scale=0.2, state=True)
+    x = gpu(d["x"])
+    buf = torch.empty(x.numel() + 1, dtype=x.dtype, device=x.device)
+    xm = buf[1:].view(T, I, B)
+    xm.copy_(x)
+    assert xm.data_ptr() % 16 != 0
+    W, dH = gpu(d["W"]), gpu(d["dH_up"])
+    _, cache = L.fwd_cache(x, W, gpu(d["b"]), gpu(d["h0"]), gpu(d["c0"]))
+    _, cache_m = L.fwd_cache(xm, W, gpu(d["b"]), gpu(d["h0"]), gpu(d["c0"]))
+    torch.cuda.synchronize()
+    assert torch.equal(cache, cache_m)
+    a = L.bwd_structsparse(x, W, cache, dH, sparsity=0.5)
+    b = L.bwd_structsparse(xm, W, cache_m, dH, sparsity=0.5)
+    torch.cuda.synchronize()
+    for k in ("dX", "dW", "db", "dh0", "dc0", "idx"):
+        assert torch.equal(a[k], b[k]), k
