@@ -407,7 +407,7 @@ __global__ __launch_bounds__(RK_WAVES * 64) void cell_rows_kernel(CellArgs a) {
 // sums of its rows in order, scores and selects the slices (one wavefront),
 // and copies the kept rows from the staging matrix.
 // ---------------------------------------------------------------------------
-constexpr int EK_UNITS = 8;
+constexpr int EK_UNITS = 4;
 constexpr int EK_WAVES = 4;
 
 template <typename TS, bool SPARSE>
