@@ -41,9 +41,9 @@ KINDS = ("gates_select_compact", "data_grad_gemm", "weight_grad_gemm")
 # device kernel behind each timed kind whose HBM counters may be on file
 KIND_KERNEL = {"gates_select_compact": "cell", "data_grad_gemm": "gemm1_kernel",
                "weight_grad_gemm": "wgrad_kernel"}
-KERNEL_SOURCES = ("paper_1806_00512_amd/csrc/gemm.hip", "paper_1806_00512_amd/csrc/cell.hip",
-                  "paper_1806_00512_amd/csrc/common.h", "paper_1806_00512_amd/csrc/kernels.h",
-                  "paper_1806_00512_amd/csrc/lstmss_api.cpp")
+KERNEL_SOURCES = tuple("paper_1806_00512_amd/csrc/" + f for f in (
+    "gemm_common.h", "gemm1.hip", "wgrad.h", "wgrad_f32.hip", "wgrad_bf16.hip", "gemm.hip",
+    "cell.hip", "common.h", "kernels.h", "lstmss_api.cpp"))
 
 
 def parse():

@@ -10,7 +10,8 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 CSRC = os.path.join(HERE, "csrc")
 ROOT = os.path.dirname(HERE)
 LIB = os.path.join(HERE, "liblstmss.so")
-SOURCES = ["lstmss_api.cpp", "cell.hip", "gemm.hip", "train.hip", "bidir.hip"]
+SOURCES = ["lstmss_api.cpp", "cell.hip", "gemm1.hip", "wgrad_f32.hip", "wgrad_bf16.hip", "gemm.hip",
+           "train.hip", "bidir.hip"]
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 
 

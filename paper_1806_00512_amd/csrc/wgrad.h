@@ -1,0 +1,641 @@
+// Time-batched weight-gradient MFMA product on the compacted gate gradient
+// (kernel template and launcher template; instantiated per storage type in
+// wgrad_f32.hip and wgrad_bf16.hip).
+//
+// Paper: after sparsifying, the kept slices of the gate gradient are a dense
+// matrix plus an offset index array, and the weight gradient
+// dW[kept rows] += dG_c [x_t; h_{t-1}]^T runs on that matrix (section 3 after
+// Fig. 2, section 4).
+#pragma once
+
+#include "gemm_common.h"
+
+namespace lstmss {
+
+namespace {
+
+// --------------------------------------------------------------------------
+// Weight gradient of all time steps in one launch.
+//
+// Work-group: one group of output rows x 128 features (4 waves x 32).  It
+// walks the launch's time steps (and batch chunks) and owns its dW tile, so
+// dW is written (or, for a later chunk of steps, updated) once per launch in
+// a fixed summation order (deterministic, no atomics).
+//
+// Dense: a group is 32 consecutive rows; each step's product is added to the
+// accumulator.
+// Sparse: a group is `greg` consecutive regions.  Every full region keeps
+// exactly (R-S)*P rows, so at every step the group's kept rows are the same
+// contiguous range of compacted rows (at most 32*TT of them).  The MFMA
+// accumulates those into a temporary tile whose columns are kept rows; after
+// the step each accumulator column (an original row) pulls its value from the
+// temporary column holding it (ds_bpermute across lanes of the same half),
+// or nothing if its slice was dropped at that step.  The MFMA work is thus
+// only the kept rows' (no zero-filled rows).
+//
+// MFMA operands: A = [x_t; h_{t-1}] rows (features), B = gate-gradient rows;
+// accumulator column = row of dW (lane), accumulator rows = features.  Lanes
+// 0-31 consume batch columns [0, BC/2) of the chunk and lanes 32-63
+// [BC/2, BC), so each lane reads consecutive columns from LDS.
+// --------------------------------------------------------------------------
+constexpr int WG_FEAT = 128;
+constexpr int WG_ATMAX = 4;
+
+constexpr int WG_NG = 2;   // row groups per work-group
+constexpr int WG_FT = 2;   // 32-feature tiles per wavefront
+
+// Stores a staged vector into an LDS row (one 16-byte store when whole).
+template <typename E, typename V>
+__device__ __forceinline__ void lds_store_vec(E *dst, const V &v) {
+    if constexpr (V::W * sizeof(E) == 16) {
+        typedef E e16 __attribute__((ext_vector_type(16 / sizeof(E))));
+        e16 t;
+#pragma unroll
+        for (int e = 0; e < V::W; ++e)
+            t[e] = v.v[e];
+        *(e16 *)dst = t;
+    } else {
+#pragma unroll
+        for (int e = 0; e < V::W; ++e)
+            dst[e] = v.v[e];
+    }
+}
+
+// FN (dense layout, fine structure with 32-row slices and 32-column blocks,
+// BC = 32): a row group is one slice and a batch chunk is one block, so the
+// chunks of removed blocks skip their MFMAs (exact zeros, bit-identical).
+//
+// DMA (B a multiple of BC, BC * element size = 128 bytes): the batch chunks go
+// from global memory straight into LDS (global_load_lds_dwordx4, lane j of an
+// instruction fills bytes [16 j, 16 j + 16) of a 1 KB block = 8 rows), with no
+// register staging.  Rows are unpadded 128-byte lines whose 16-byte pieces are
+// permuted per row (piece c of row r sits at c ^ wg_swz(r)) so that the
+// operand reads of 16 consecutive rows hit distinct banks; the permutation is
+// applied on the global side (each lane loads the piece its LDS slot holds).
+// Rows past the end of the operands are clamped to a valid row: they only feed
+// output rows or columns that are never stored.
+__device__ __forceinline__ int wg_swz(int r) { return (r & 7) ^ ((r >> 3) & 1); }
+
+
+// Sparse fp32 with DMA chunks and one 32-row temporary tile: operands staged
+// half a chunk at a time; with at most two accumulator tiles three wavefronts
+// per SIMD (register-bound otherwise at two; measured 4 % faster at H = 2048
+// despite 36 bytes of spilled registers per lane), with four (75 % sparsity)
+// two, which the half-chunk staging keeps from spilling.
+template <typename TS, bool SPARSE, bool DMA, int TT, int ATN>
+constexpr bool wg_splitop() { return SPARSE && DMA && sizeof(TS) == 4 && TT == 1; }
+template <typename TS, bool SPARSE, bool DMA, int TT, int ATN>
+constexpr int wg_occupancy() { return wg_splitop<TS, SPARSE, DMA, TT, ATN>() && ATN <= 2 ? 3 : 2; }
+
+template <typename TS, bool SPARSE, int TT, int ATN, bool VEC, int BC, bool FN = false,
+          bool DMA = false>
+__global__ __launch_bounds__(THREADS, (wg_occupancy<TS, SPARSE, DMA, TT, ATN>())) void wgrad_kernel(WgradArgs a) {
+    constexpr bool SPLITOP = wg_splitop<TS, SPARSE, DMA, TT, ATN>();
+    static_assert(!(FN && (SPARSE || BC != 32 || TT != 1)), "fine chunks are 32-column blocks");
+    static_assert(!DMA || (BC * sizeof(TS) == 128 && VEC), "DMA chunks are 128-byte lines");
+    using E = typename std::conditional<sizeof(TS) == 4, float, uint16_t>::type;
+    constexpr int PITCH = DMA ? BC : BC + (sizeof(TS) == 4 ? 4 : 8);
+    constexpr int PE = 16 / sizeof(E);            // elements per 16-byte piece
+    constexpr int GROWS = TT * 32;                // temporary-tile rows per group
+    using V = Vec<TS, VEC>;
+    constexpr int VW = V::W;
+    constexpr int cpr = BC / VW;
+    constexpr int gvec = WG_NG * GROWS * cpr, xvec = WG_FEAT * cpr;
+    constexpr int RG = (gvec + THREADS - 1) / THREADS;
+    constexpr int RX = (xvec + THREADS - 1) / THREADS;
+    // two stages: the MFMAs read one while the next batch chunk is written to
+    // the other (one barrier per chunk); the kept-slice table is kept per
+    // step parity so that a step's routing never races the next step's table
+    __shared__ __align__(16) E sX[2][WG_FEAT][PITCH];
+    __shared__ __align__(16) E sG[2][WG_NG * GROWS][PITCH];
+    __shared__ int sidx[2][WG_NG][64];
+
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int fh = wave & 1, gi = wave >> 1;      // feature half, group of this wavefront
+    const int I = a.I, H = a.H, B = a.B;
+    const int NC = I + H, G4 = 4 * H;
+    const int n0 = blockIdx.y * WG_FEAT;
+    const TS *Gc = (const TS *)a.Gc;
+    const TS *x = (const TS *)a.x;
+    const TS *h = (const TS *)a.h;
+
+    // geometry of group g: original rows [r0, r0 + rcount), compacted rows
+    // [c0, c0 + ccount), kept-slice entries [q0, q0 + qcount), first slice j0
+    const int rp = a.R * a.P, kr = (a.R - a.S) * a.P, ks = a.R - a.S;
+    auto geom = [&](int g, int &r0, int &rcount, int &c0, int &ccount, int &q0, int &qcount,
+                    int &j0) {
+        if (SPARSE) {
+            r0 = g * a.greg * rp;
+            rcount = max(0, min(a.greg * rp, G4 - r0));
+            c0 = g * a.greg * kr;
+            ccount = max(0, min(a.greg * kr, a.Kp - c0));
+            q0 = g * a.greg * ks;
+            qcount = max(0, min(a.greg * ks, a.kept - q0));
+            j0 = g * a.greg * a.R;
+        } else {
+            r0 = g * 32;
+            rcount = max(0, min(32, G4 - r0));
+            c0 = r0;
+            ccount = rcount;
+            q0 = qcount = j0 = 0;
+        }
+    };
+    int r0, rcount, c0, ccount, q0, qcount, j0;
+    geom(blockIdx.x * WG_NG + gi, r0, rcount, c0, ccount, q0, qcount, j0);
+    const int AT = SPARSE ? (rcount + 31) / 32 : 1;
+    // compacted-row origin and count of both groups, for the loaders
+    int lc0[WG_NG], lcc[WG_NG], lq0[WG_NG], lqc[WG_NG];
+#pragma unroll
+    for (int k = 0; k < WG_NG; ++k) {
+        int t0, t1, t2;
+        geom(blockIdx.x * WG_NG + k, t0, t1, lc0[k], lcc[k], lq0[k], lqc[k], t2);
+    }
+
+    const int nbc = (B + BC - 1) / BC;
+    const int niters = (a.t_end - a.t_begin) * nbc;
+
+    // global -> register staging of one batch chunk; a vector never crosses
+    // the end of a row (B is a multiple of VW when VEC).  Each thread's rows
+    // are fixed for the whole launch, so their offsets within a step are
+    // computed once; a chunk adds the step's base and the batch offset.
+    // DMA: instruction k of a chunk fills rows [8k, 8k + 8) of sX (k < 16) or
+    // of sG (k >= 16); wavefront w issues k = w, w + 4, ...
+    constexpr int NDI = (WG_FEAT + WG_NG * GROWS) / 8, NDW = NDI / 4;
+    static_assert(!DMA || (NDI % 4 == 0 && WG_FEAT == 128), "DMA instruction split");
+    int dofs[DMA ? NDW : 1];
+    bool disx[DMA ? NDW : 1];
+    if constexpr (DMA) {
+#pragma unroll
+        for (int i = 0; i < NDW; ++i) {
+            const int k = wave + 4 * i;
+            const int rr = 8 * (k < 16 ? k : k - 16) + (lane >> 3);
+            const int pc = (lane & 7) ^ wg_swz(rr);  // the piece this lane's LDS slot holds
+            if (k < 16) {
+                const int n = min(n0 + rr, NC - 1);
+                disx[i] = n < I;
+                dofs[i] = (n < I ? n : n - I) * B + pc * PE;
+            } else {
+                const int kk = rr / GROWS, lr = rr - kk * GROWS;
+                const int crow = max(0, min(lc0[kk] + min(lr, max(lcc[kk] - 1, 0)), (int)a.Kp - 1));
+                disx[i] = false;
+                dofs[i] = crow * B + pc * PE;
+            }
+        }
+    }
+    V rg[DMA ? 1 : 2][DMA ? 1 : RG], rx[DMA ? 1 : 2][DMA ? 1 : RX];  // two chunks in flight
+    int gofs[RG], gbb[RG], xofs[RX], xbb[RX];
+    bool gok[RG], xok[RX], xisx[RX];
+#pragma unroll
+    for (int i = 0; i < RG; ++i) {
+        const int q = tid + i * THREADS;
+        const int rho = q / cpr, bb = (q - rho * cpr) * VW;
+        const int k = rho / GROWS, lr = rho - k * GROWS;
+        gok[i] = q < gvec && lr < lcc[k & (WG_NG - 1)];
+        gofs[i] = (lc0[k & (WG_NG - 1)] + (gok[i] ? lr : 0)) * B + bb;
+        gbb[i] = bb;
+    }
+#pragma unroll
+    for (int i = 0; i < RX; ++i) {
+        const int q = tid + i * THREADS;
+        const int f = q / cpr, bb = (q - f * cpr) * VW;
+        const int n = n0 + f;
+        xok[i] = q < xvec && n < NC;
+        xisx[i] = n < I;
+        xofs[i] = (xisx[i] ? n : (xok[i] ? n - I : 0)) * B + bb;
+        xbb[i] = bb;
+    }
+    int ridx[2] = {-1, -1};
+    // steps run from t_end - 1 down to t_begin, and the launches of one call
+    // go down in time too, so every row of dW sums its steps in one order
+    // however the steps are split over launches
+    auto load = [&](int it, int set, int lbuf) {
+        const int tl = it / nbc, b0 = (it - tl * nbc) * BC;
+        const int t = a.t_end - 1 - tl;
+        const TS *Gt = Gc + (long)t * a.Kp * B + b0;
+        const TS *xt = x + (long)t * I * B + b0;
+        const TS *ht = h + (long)t * H * B + b0;
+        if constexpr (DMA) {
+#pragma unroll
+            for (int i = 0; i < NDW; ++i) {
+                const int k = wave + 4 * i;
+                const TS *src = k < 16 ? (disx[i] ? xt : ht) + dofs[i] : Gt + dofs[i];
+                E *dst = k < 16 ? &sX[lbuf][8 * k][0] : &sG[lbuf][8 * (k - 16)][0];
+                __builtin_amdgcn_global_load_lds((glob_void_t *)src, (lds_void_t *)dst, 16, 0, 0);
+            }
+        } else {
+#pragma unroll
+            for (int i = 0; i < RG; ++i) {
+                if (gok[i] && b0 + gbb[i] < B)
+                    rg[DMA ? 0 : set][i].load(Gt + gofs[i], VW);
+                else
+                    rg[DMA ? 0 : set][i].zero();
+            }
+#pragma unroll
+            for (int i = 0; i < RX; ++i) {
+                if (xok[i] && b0 + xbb[i] < B)
+                    rx[DMA ? 0 : set][i].load((xisx[i] ? xt : ht) + xofs[i], VW);
+                else
+                    rx[DMA ? 0 : set][i].zero();
+            }
+        }
+        if (SPARSE && b0 == 0 && tid < WG_NG * 64) {
+            const int k = tid >> 6, e = tid & 63;
+            ridx[set] = e < lqc[k] ? a.idx[(long)t * a.kept + lq0[k] + e] : -1;
+        }
+        if (FN && b0 == 0 && tid < WG_NG * 64) {  // kept blocks of the group's slice
+            const int k = tid >> 6, e = tid & 63;
+            const long sl = (long)blockIdx.x * WG_NG + k;
+            ridx[set] = (e < a.fkept && sl < G4 / 32)
+                            ? a.fidx[((long)t * (G4 / 32) + sl) * a.fkept + e] : -1;
+        }
+    };
+    auto stash = [&](int it, int set, int buf) {
+        const int tl = it / nbc;
+        if constexpr (!DMA) {
+#pragma unroll
+            for (int i = 0; i < RG; ++i) {
+                const int q = tid + i * THREADS;
+                if (q < gvec) {
+                    const int rho = q / cpr, bb = (q - rho * cpr) * VW;
+                    lds_store_vec(&sG[buf][rho][bb], rg[set][i]);
+                }
+            }
+#pragma unroll
+            for (int i = 0; i < RX; ++i) {
+                const int q = tid + i * THREADS;
+                if (q < xvec) {
+                    const int f = q / cpr, bb = (q - f * cpr) * VW;
+                    lds_store_vec(&sX[buf][f][bb], rx[set][i]);
+                }
+            }
+        }
+        if ((SPARSE || FN) && it - tl * nbc == 0 && tid < WG_NG * 64)
+            sidx[tl & 1][tid >> 6][tid & 63] = ridx[set];
+    };
+
+    f32x16 acc[WG_FT][ATN], tmp[WG_FT][TT];
+#pragma unroll
+    for (int ft = 0; ft < WG_FT; ++ft) {
+#pragma unroll
+        for (int j = 0; j < ATN; ++j)
+#pragma unroll
+            for (int v = 0; v < 16; ++v)
+                acc[ft][j][v] = 0.f;
+#pragma unroll
+        for (int j = 0; j < TT; ++j)
+#pragma unroll
+            for (int v = 0; v < 16; ++v)
+                tmp[ft][j][v] = 0.f;
+    }
+    // a later launch of the same call continues the sums of the earlier ones
+    // from the stored dW (the same fp32 additions as one launch)
+    if (a.accumulate) {
+#pragma unroll
+        for (int at = 0; at < ATN; ++at) {
+            if (at >= AT)
+                break;
+            const int col = at * 32 + (lane & 31);
+            if (col >= rcount)
+                continue;
+            const float *src = a.dW + (long)(r0 + col) * NC;
+#pragma unroll
+            for (int ft = 0; ft < WG_FT; ++ft)
+#pragma unroll
+                for (int v = 0; v < 16; ++v) {
+                    const int f = n0 + fh * 64 + ft * 32 + acc_row(lane, v);
+                    if (f < NC)
+                        acc[ft][at][v] = src[f];
+                }
+        }
+    }
+
+    load(0, 0, 0);
+    if (!DMA && niters > 1)
+        load(1, 1, 1);
+    stash(0, 0, 0);
+    if (DMA)
+        __builtin_amdgcn_s_waitcnt(0);
+    __syncthreads();
+    constexpr int HALF = BC / 2;
+    const int hb = (lane >> 5) * HALF;
+    // iteration it computes from LDS buffer it & 1, loads chunk it + 2 into
+    // register set it & 1 and stores chunk it + 1 (set and buffer
+    // (it + 1) & 1); the loop runs in pairs so that the sets are static
+    uint64_t fmask = ~0ull;  // FN: kept blocks of this wavefront's slice at the current step
+
+    // sparse routing: csrc[at] is the temporary column (kept row) that
+    // accumulator column at * 32 + lane pulls at the current step, -1 if its
+    // slice was dropped.  (Routing a step during the next step's first chunk,
+    // to overlap the permutes with MFMAs, measured no faster.)
+    int csrc[ATN];
+    auto lookup = [&](int tl) {
+        const int *tab = sidx[tl & 1][gi];
+#pragma unroll
+        for (int at = 0; at < ATN; ++at) {
+            const int col = at * 32 + (lane & 31);
+            int src = -1;
+            if (col < rcount) {
+                const int orow = r0 + col;
+                const int js = orow / a.P;
+                const int reg = (js - j0) / a.R;
+                const int e0 = reg * ks, e1 = min(e0 + ks, qcount);
+                for (int e = e0; e < e1; ++e)
+                    if (tab[e] == js)
+                        src = e * a.P + (orow - js * a.P);
+            }
+            csrc[at] = src;
+        }
+    };
+    // acc[:, at] += t routed by srcs (accumulator tiles past the group's rows
+    // have src -1 everywhere and stay zero)
+    auto route = [&](const f32x16 (&t)[WG_FT][TT], const int (&srcs)[ATN]) {
+#pragma unroll
+        for (int at = 0; at < ATN; ++at) {
+            const int src = srcs[at];
+            const int saddr = (((src < 0 ? 0 : src) & 31) + (lane & 32)) << 2;
+            const int stile = src < 0 ? 0 : (src >> 5);
+#pragma unroll
+            for (int ft = 0; ft < WG_FT; ++ft) {
+                // all lane permutes of this feature tile first, then the adds
+                float val[TT][16];
+#pragma unroll
+                for (int tt = 0; tt < TT; ++tt)
+#pragma unroll
+                    for (int v = 0; v < 16; ++v)
+                        val[tt][v] = __int_as_float(
+                            __builtin_amdgcn_ds_bpermute(saddr, __float_as_int(t[ft][tt][v])));
+#pragma unroll
+                for (int v = 0; v < 16; ++v) {
+                    float w = val[0][v];
+                    if (TT > 1)
+                        w = stile == 1 ? val[TT > 1 ? 1 : 0][v] : w;
+                    acc[ft][at][v] += src < 0 ? 0.f : w;  // dropped: exactly 0, even for inf/NaN
+                }
+            }
+        }
+    };
+
+    auto iter = [&](int it, auto sc) {
+        constexpr int S0 = decltype(sc)::value, S1 = 1 - S0;
+        const int buf = S0;
+        const int tl = it / nbc, bc = it - tl * nbc;
+        if (!DMA && it + 2 < niters)
+            load(it + 2, S0, 0);
+        // DMA: the next chunk streams into the other buffer (read in the
+        // previous iteration), issued once this chunk's operands are in
+        // registers (a deeper, three-buffer pipeline measured slower)
+        auto issue_next = [&]() {
+            if (DMA && it + 1 < niters)
+                load(it + 1, S1, S1);
+        };
+        if constexpr (FN) {
+            if (bc == 0) {
+                const int v = sidx[tl & 1][gi][lane];
+                uint64_t m = v >= 0 ? (1ull << v) : 0ull;
+#pragma unroll
+                for (int off = 32; off >= 1; off >>= 1) {
+                    const uint32_t lo = __shfl_xor((uint32_t)m, off, 64);
+                    const uint32_t hi = __shfl_xor((uint32_t)(m >> 32), off, 64);
+                    m |= ((uint64_t)hi << 32) | lo;
+                }
+                fmask = ((uint64_t)__builtin_amdgcn_readfirstlane((uint32_t)(m >> 32)) << 32) |
+                        __builtin_amdgcn_readfirstlane((uint32_t)m);
+            }
+        }
+        const bool run = !FN || !a.fskip || ((fmask >> bc) & 1);
+        // column (element) of the 16-byte piece p of LDS row r
+        auto pcol = [&](int r, int p) { return DMA ? (p ^ wg_swz(r)) * PE : p * PE; };
+
+        // MFMA over this batch chunk: WG_FT feature tiles x TT row tiles
+        if (!run) {
+            // removed block: its products are zero
+            issue_next();
+        } else if constexpr (sizeof(TS) == 4 && SPLITOP) {
+            // operands of half the chunk at a time (fewer live registers)
+            issue_next();  // the next chunks stream in during the MFMAs
+#pragma unroll
+            for (int sh = 0; sh < HALF / 4; sh += 2) {
+                float4 av[2][WG_FT], bv[2][TT];
+#pragma unroll
+                for (int s2 = 0; s2 < 2; ++s2) {
+#pragma unroll
+                    for (int ft = 0; ft < WG_FT; ++ft) {
+                        const int r = fh * 64 + ft * 32 + (lane & 31);
+                        av[s2][ft] = *(const float4 *)&sX[buf][r][pcol(r, hb / 4 + sh + s2)];
+                    }
+#pragma unroll
+                    for (int tt = 0; tt < TT; ++tt) {
+                        const int r = gi * GROWS + tt * 32 + (lane & 31);
+                        bv[s2][tt] = *(const float4 *)&sG[buf][r][pcol(r, hb / 4 + sh + s2)];
+                    }
+                }
+#pragma unroll
+                for (int s2 = 0; s2 < 2; ++s2)
+#pragma unroll
+                    for (int c4 = 0; c4 < 4; ++c4)
+#pragma unroll
+                        for (int ft = 0; ft < WG_FT; ++ft)
+#pragma unroll
+                            for (int tt = 0; tt < TT; ++tt)
+                                tmp[ft][tt] = mfma32x32x2(av[s2][ft][c4], bv[s2][tt][c4], tmp[ft][tt]);
+            }
+        } else if constexpr (sizeof(TS) == 4) {
+            float4 av[HALF / 4][WG_FT], bv[HALF / 4][TT];
+#pragma unroll
+            for (int s = 0; s < HALF / 4; ++s) {
+#pragma unroll
+                for (int ft = 0; ft < WG_FT; ++ft) {
+                    const int r = fh * 64 + ft * 32 + (lane & 31);
+                    av[s][ft] = *(const float4 *)&sX[buf][r][pcol(r, hb / 4 + s)];
+                }
+#pragma unroll
+                for (int tt = 0; tt < TT; ++tt) {
+                    const int r = gi * GROWS + tt * 32 + (lane & 31);
+                    bv[s][tt] = *(const float4 *)&sG[buf][r][pcol(r, hb / 4 + s)];
+                }
+            }
+            issue_next();  // the next chunks stream in during the MFMAs
+#pragma unroll
+            for (int s = 0; s < HALF / 4; ++s)
+#pragma unroll
+                for (int c4 = 0; c4 < 4; ++c4)
+#pragma unroll
+                    for (int ft = 0; ft < WG_FT; ++ft)
+#pragma unroll
+                        for (int tt = 0; tt < TT; ++tt)
+                            tmp[ft][tt] = mfma32x32x2(av[s][ft][c4], bv[s][tt][c4], tmp[ft][tt]);
+        } else {
+            u16x8 av[HALF / 8][WG_FT], bv[HALF / 8][TT];
+#pragma unroll
+            for (int s = 0; s < HALF / 8; ++s) {
+#pragma unroll
+                for (int ft = 0; ft < WG_FT; ++ft) {
+                    const int r = fh * 64 + ft * 32 + (lane & 31);
+                    av[s][ft] = *(const u16x8 *)&sX[buf][r][pcol(r, hb / 8 + s)];
+                }
+#pragma unroll
+                for (int tt = 0; tt < TT; ++tt) {
+                    const int r = gi * GROWS + tt * 32 + (lane & 31);
+                    bv[s][tt] = *(const u16x8 *)&sG[buf][r][pcol(r, hb / 8 + s)];
+                }
+            }
+            issue_next();
+#pragma unroll
+            for (int s = 0; s < HALF / 8; ++s)
+#pragma unroll
+                for (int ft = 0; ft < WG_FT; ++ft)
+#pragma unroll
+                    for (int tt = 0; tt < TT; ++tt)
+                        tmp[ft][tt] = mfma32x32x16bf(av[s][ft], bv[s][tt], tmp[ft][tt]);
+        }
+
+        // end of a step: dense adds the step's product; sparse routes each
+        // kept row of the step into its original row (same summation order
+        // either way, so a sparse call that keeps every row matches the
+        // dense one bit for bit)
+        if (bc == nbc - 1) {
+            if (!SPARSE) {
+#pragma unroll
+                for (int ft = 0; ft < WG_FT; ++ft)
+#pragma unroll
+                    for (int v = 0; v < 16; ++v) {
+                        acc[ft][0][v] += tmp[ft][0][v];
+                        tmp[ft][0][v] = 0.f;
+                    }
+            } else {
+                lookup(tl);
+                route(tmp, csrc);
+#pragma unroll
+                for (int ft = 0; ft < WG_FT; ++ft)
+#pragma unroll
+                    for (int tt = 0; tt < TT; ++tt)
+#pragma unroll
+                        for (int v = 0; v < 16; ++v)
+                            tmp[ft][tt][v] = 0.f;
+            }
+        }
+        if (it + 1 < niters)
+            stash(it + 1, S1, S1);
+        if (DMA)  // the next chunk's lines are in LDS before anyone reads them
+            __builtin_amdgcn_s_waitcnt(0);
+        __syncthreads();
+    };
+    int it0 = 0;
+    for (; it0 + 1 < niters; it0 += 2) {
+        iter(it0, std::integral_constant<int, 0>{});
+        iter(it0 + 1, std::integral_constant<int, 1>{});
+    }
+    if (it0 < niters)
+        iter(it0, std::integral_constant<int, 0>{});
+
+    // write the owned tile of dW
+#pragma unroll
+    for (int at = 0; at < ATN; ++at) {
+        if (at >= AT)
+            break;
+        const int col = at * 32 + (lane & 31);
+        if (col >= rcount)
+            continue;
+        float *dst = a.dW + (long)(r0 + col) * NC;
+#pragma unroll
+        for (int ft = 0; ft < WG_FT; ++ft)
+#pragma unroll
+            for (int v = 0; v < 16; ++v) {
+                const int f = n0 + fh * 64 + ft * 32 + acc_row(lane, v);
+                if (f < NC)
+                    dst[f] = acc[ft][at][v];
+            }
+    }
+}
+
+// Temporary tiles (kept rows per group / 32) and accumulator tiles (original
+// rows per group / 32) of the sparse weight-gradient kernel.
+void wgrad_tiles(int P, int R, int S, int *greg, int *tt, int *at) {
+    const int kr = (R - S) * P, rp = R * P;
+    *greg = kr <= 32 ? max(1, 32 / kr) : 1;
+    *tt = (*greg * kr + 31) / 32;
+    *at = (*greg * rp + 31) / 32;
+}
+
+// One weight-gradient launch; `dma` takes the LDS-DMA variant (128-byte
+// chunks: 32 fp32 or 64 bf16 batch columns).
+template <typename TS, bool SP, int TTV, int ATV, bool FN>
+void wg_launch(const WgradArgs &a, bool vec, bool dma, dim3 grid, hipStream_t s) {
+    constexpr int DBC = 128 / (int)sizeof(TS);
+    if constexpr (!FN || DBC == 32) {
+        if (dma) {
+            hipLaunchKernelGGL((wgrad_kernel<TS, SP, TTV, ATV, true, DBC, FN, true>), grid,
+                               dim3(THREADS), 0, s, a);
+            return;
+        }
+    }
+    if constexpr (FN) {
+        if (vec)
+            hipLaunchKernelGGL((wgrad_kernel<TS, false, 1, 1, true, 32, true>), grid, dim3(THREADS), 0, s, a);
+        else
+            hipLaunchKernelGGL((wgrad_kernel<TS, false, 1, 1, false, 32, true>), grid, dim3(THREADS), 0, s, a);
+    } else {
+#define LSTMSS_WG(VE) do { \
+        if (a.BC == 16) hipLaunchKernelGGL((wgrad_kernel<TS, SP, TTV, ATV, VE, 16>), grid, dim3(THREADS), 0, s, a); \
+        else if (a.BC == 32) hipLaunchKernelGGL((wgrad_kernel<TS, SP, TTV, ATV, VE, 32>), grid, dim3(THREADS), 0, s, a); \
+        else hipLaunchKernelGGL((wgrad_kernel<TS, SP, TTV, ATV, VE, 64>), grid, dim3(THREADS), 0, s, a); } while (0)
+        if (vec)
+            LSTMSS_WG(true);
+        else
+            LSTMSS_WG(false);
+#undef LSTMSS_WG
+    }
+}
+
+bool aligned16(const void *p) { return ((uintptr_t)p & 15) == 0; }
+
+// One weight-gradient call in storage type TS (the instantiations live in
+// wgrad_f32.hip and wgrad_bf16.hip, so that the two compile in parallel).
+template <typename TS>
+hipError_t launch_wgrad_t(WgradArgs a, bool sparse, hipStream_t s) {
+    constexpr bool bf16 = sizeof(TS) == 2;
+    const int es = bf16 ? 2 : 4;
+    // the LDS-DMA variant: whole 128-byte chunks of 16-byte aligned rows
+    auto dma_ok = [&](int bc) {
+        return a.dma && bc * es == 128 && a.B % bc == 0 && aligned16(a.Gc) && aligned16(a.x) &&
+               aligned16(a.h);
+    };
+    if (a.fidx) {  // fine structure, 32-row slices x 32-column blocks
+        if (sparse || a.B % 32 != 0 || a.fkept < 1 || a.fkept > 64 || (4L * a.H) % 32 != 0)
+            return hipErrorInvalidValue;
+        a.BC = 32;
+        const bool vec = a.B % (bf16 ? 8 : 4) == 0;
+        dim3 grid((unsigned)ceil_div(ceil_div(4L * a.H, 32), WG_NG),
+                  (unsigned)ceil_div(a.I + a.H, WG_FEAT));
+        wg_launch<TS, false, 1, 1, true>(a, vec, bf16 ? false : dma_ok(32), grid, s);
+        return hipGetLastError();
+    }
+    int tt = 1, at = 1;
+    if (sparse) {
+        if (!wgrad_supported(a.P, a.R, a.S))
+            return hipErrorNotSupported;
+        wgrad_tiles(a.P, a.R, a.S, &a.greg, &tt, &at);
+    }
+    // batch columns per stage: 16/32 (fp32) or 32/64 (bf16, whole MFMA
+    // k-blocks); larger stages would not leave room for two wavefronts per SIMD
+    const int bc = a.B <= 16 ? 16 : a.B <= 32 ? 32 : (bf16 ? 64 : 32);
+    a.BC = bc;
+    const int vw = bf16 ? 8 : 4;
+    const bool vec = a.B % vw == 0;
+    const bool dma = dma_ok(bc);
+    const long groups = sparse ? ceil_div(ceil_div(4L * a.H / a.P, a.R), a.greg) : ceil_div(4L * a.H, 32);
+    dim3 grid((unsigned)ceil_div(groups, WG_NG), (unsigned)ceil_div(a.I + a.H, WG_FEAT));
+#define LSTMSS_WGA(TTV) do { \
+        if (at <= 1) wg_launch<TS, true, TTV, 1, false>(a, vec, dma, grid, s); \
+        else if (at <= 2) wg_launch<TS, true, TTV, 2, false>(a, vec, dma, grid, s); \
+        else wg_launch<TS, true, TTV, 4, false>(a, vec, dma, grid, s); } while (0)
+    if (!sparse) wg_launch<TS, false, 1, 1, false>(a, vec, dma, grid, s);
+    else if (tt == 1) LSTMSS_WGA(1);
+    else LSTMSS_WGA(2);
+#undef LSTMSS_WGA
+    return hipGetLastError();
+}
+
+} // namespace
+
+} // namespace lstmss
