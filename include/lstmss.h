@@ -132,9 +132,11 @@ int32_t lstm_fwd_cache(const lstmss_dims *d, const void *x, const void *W, const
                        const float *h0, const float *c0, void *h_out, void *cache, void *ws,
                        size_t ws_bytes, void *stream);
 
-/* Dense backward pass through time of one layer (the paper's baseline, every
- * gate-gradient row kept).  Loss convention: dH_up[t] = dL/dh_t from above,
- * dhT, dcT = dL/dh_T, dL/dc_T from later time (NULL = 0).
+/* Dense backward pass through time of one layer: every gate-gradient row
+ * kept, the baseline the paper's speedups are measured against (section 5.5;
+ * the dense products of its custom operation, section 4).  Loss convention:
+ * dH_up[t] = dL/dh_t from above, dhT, dcT = dL/dh_T, dL/dc_T from later time
+ * (NULL = 0).
  *   x, W, cache as given to / written by lstm_fwd_cache
  *   dH_up  [T][H][B] fp32
  *   dX     [T][I][B] fp32 (dL/dx_t), NULL skips the input-gradient rows
@@ -178,17 +180,27 @@ int32_t lstm_bwd_structsparse(const lstmss_dims *d, float sparsity, const lstmss
                               float *dW, float *db, float *dh0, float *dc0, int32_t *idx_out,
                               void *dbg_dgates, void *ws, size_t ws_bytes, void *stream);
 
-/* Score, select and compact one given gate-gradient matrix (the selection
- * step of lstm_bwd_structsparse on its own, same scoring and ranking code).
+/* Score, select and compact one given gate-gradient matrix: the selection
+ * step of lstm_bwd_structsparse on its own (section 3: slice scores by L2
+ * norm, the S lowest slices of every region dropped, kept slices compacted
+ * with an offset index), run by the same kernels the backward pass uses at
+ * this shape.
  *   dG     [4H][B] dtype (d->T is ignored)
  *   dG_c   [K'][B] dtype: COARSE kept rows in ascending order; FINE the
  *          masked matrix (removed blocks zero)
  *   idx    [lstmss_index_entries] int32 (see lstm_bwd_structsparse)
  *   scores COARSE [4H/P] fp64 slice scores; FINE [4H/Mx][nb] fp64 block
- *          scores; or NULL */
+ *          scores; or NULL
+ *   ws     lstmss_select_workspace_bytes(d, sparsity, s) bytes of scratch
+ *          (the per-row, per-64-column-chunk sums of squares of the
+ *          two-kernel path that the backward pass takes at H*B >= 65536);
+ *          may be NULL when that size is 0.  LSTMSS_ERR_WORKSPACE when it is
+ *          missing or too small. */
+int64_t lstmss_select_workspace_bytes(const lstmss_dims *d, float sparsity,
+                                      const lstmss_structure *s);
 int32_t lstmss_select_compact(const lstmss_dims *d, float sparsity, const lstmss_structure *s,
-                              const void *dG, void *dG_c, int32_t *idx, double *scores,
-                              void *stream);
+                              const void *dG, void *dG_c, int32_t *idx, double *scores, void *ws,
+                              size_t ws_bytes, void *stream);
 
 /* Backward pass of a stack of `layers` (1..8) LSTM layers, bottom layer 0,
  * scheduled as a wavefront (the layer-time pipelining of a stacked LSTM):

@@ -395,13 +395,16 @@ __global__ __launch_bounds__(RK_WAVES * 64) void cell_rows_kernel(CellArgs a) {
 // ---------------------------------------------------------------------------
 // Split variant for large shapes, two kernels per step.
 //
-// cell_elem_kernel: element-parallel over (8 units x one 64-column batch
-// chunk) per work-group, so every CU has loads in flight.  Each (unit, batch)
-// element is loaded once and gives all four gate gradients; wave w owns units
-// 2w, 2w+1 of the group, lane l batch column 64c + l.  It writes the gate
+// cell_elem_kernel: element-parallel over (4 units x one 64-column batch
+// chunk) per work-group, one unit per wavefront, lane l holding batch column
+// 64c + l, so every CU has loads in flight.  Each (unit, batch) element is
+// loaded once and gives all four gate gradients.  It writes the gate
 // gradient (straight to the compacted matrix when nothing is dropped, else to
 // a staging matrix), dc_{t-1}, and per (row, chunk) the fp64 chunk sum of
-// squares (fixed 64-lane butterfly) and the fp32 row sum.
+// squares (fixed 64-lane butterfly) and the fp32 row sum.  MODE CELL_GIVEN
+// reads the four rows of each unit from a given gate-gradient matrix instead
+// (the standalone selection) and writes only the chunk sums of squares; the
+// given matrix is then the select kernel's staging matrix.
 //
 // cell_select_kernel2: one work-group per group of regions folds the chunk
 // sums of its rows in order, scores and selects the slices (one wavefront),
@@ -410,8 +413,9 @@ __global__ __launch_bounds__(RK_WAVES * 64) void cell_rows_kernel(CellArgs a) {
 constexpr int EK_UNITS = 4;
 constexpr int EK_WAVES = 4;
 
-template <typename TS, bool SPARSE>
+template <typename TS, int MODE>
 __global__ __launch_bounds__(EK_WAVES * 64) void cell_elem_kernel(CellArgs a) {
+    constexpr bool SPARSE = MODE != CELL_DENSE, GIVEN = MODE == CELL_GIVEN;
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
     const int B = a.B, H = a.H;
     const int c = blockIdx.y, nch = gridDim.y;
@@ -432,6 +436,12 @@ __global__ __launch_bounds__(EK_WAVES * 64) void cell_elem_kernel(CellArgs a) {
         uu[k] = u;
         ok[k] = u < H && bin;
         const int e = (u < H ? u : 0) * B + (bin ? b : 0);
+        if (GIVEN) {  // the unit's four rows of the given matrix
+#pragma unroll
+            for (int g = 0; g < 4; ++g)
+                lg[k][g] = ok[k] ? st<TS>::load((const TS *)a.dG_in, (long)(g * H + u) * B + b) : 0.f;
+            continue;
+        }
 #pragma unroll
         for (int g = 0; g < 4; ++g)
             lg[k][g] = ok[k] ? st<TS>::load(gates, (long)(g * H + u) * B + b) : 0.f;
@@ -445,16 +455,23 @@ __global__ __launch_bounds__(EK_WAVES * 64) void cell_elem_kernel(CellArgs a) {
 #pragma unroll
     for (int k = 0; k < UPW; ++k) {
         const int u = uu[k];
-        const float ig = lg[k][0], fg = lg[k][1], gg = lg[k][2], og = lg[k][3];
-        const float tc = tanhf(lct[k]);
-        const float dcv = ldc[k] + ldh[k] * og * (1.f - tc * tc);
         float v[4];
-        v[0] = st<TS>::rnd(dcv * gg * ig * (1.f - ig));
-        v[1] = st<TS>::rnd(dcv * lcp[k] * fg * (1.f - fg));
-        v[2] = st<TS>::rnd(dcv * ig * (1.f - gg * gg));
-        v[3] = st<TS>::rnd(ldh[k] * tc * og * (1.f - og));
-        if (ok[k]) {
-            a.dc_out[u * B + b] = dcv * fg;
+        if (GIVEN) {
+#pragma unroll
+            for (int g = 0; g < 4; ++g)
+                v[g] = lg[k][g];
+        } else {
+            const float ig = lg[k][0], fg = lg[k][1], gg = lg[k][2], og = lg[k][3];
+            const float tc = tanhf(lct[k]);
+            const float dcv = ldc[k] + ldh[k] * og * (1.f - tc * tc);
+            v[0] = st<TS>::rnd(dcv * gg * ig * (1.f - ig));
+            v[1] = st<TS>::rnd(dcv * lcp[k] * fg * (1.f - fg));
+            v[2] = st<TS>::rnd(dcv * ig * (1.f - gg * gg));
+            v[3] = st<TS>::rnd(ldh[k] * tc * og * (1.f - og));
+            if (ok[k])
+                a.dc_out[u * B + b] = dcv * fg;
+        }
+        if (ok[k] && !GIVEN) {
 #pragma unroll
             for (int g = 0; g < 4; ++g) {
                 const long r = (long)g * H + u;
@@ -472,13 +489,15 @@ __global__ __launch_bounds__(EK_WAVES * 64) void cell_elem_kernel(CellArgs a) {
             for (int off = 32; off >= 1; off >>= 1) {
                 if (SPARSE)
                     q = q + shfl_xor_f64(q, off);
-                rs += shfl_xor_f32(rs, off);
+                if (!GIVEN)
+                    rs += shfl_xor_f32(rs, off);
             }
             if (lane == 0 && u < H) {
                 const long r = (long)g * H + u;
                 if (SPARSE)
                     a.chunk_sq[r * nch + c] = q;
-                a.chunk_rs[r * nch + c] = rs;
+                if (!GIVEN)
+                    a.chunk_rs[r * nch + c] = rs;
             }
         }
     }
@@ -822,25 +841,39 @@ size_t cell_lds_bytes(const CellArgs &a, int mode) {
 }
 
 bool cell_split_ok(const CellArgs &a, int mode) {
-    if (mode == CELL_GIVEN || (long)a.H * a.B < 65536)
+    if ((long)a.H * a.B < 65536)
         return false;
     return mode == CELL_DENSE ||
            ((long)a.regions_per_wg * a.R <= 64 && (long)a.regions_per_wg * a.R * a.P <= 256);
 }
 
-hipError_t launch_cell_split(const CellArgs &a, int mode, bool bf16, hipStream_t s) {
+template <typename TS>
+static void launch_elem(const CellArgs &a, int mode, dim3 grid, hipStream_t s) {
+    if (mode == CELL_SPARSE)
+        hipLaunchKernelGGL((cell_elem_kernel<TS, CELL_SPARSE>), grid, dim3(EK_WAVES * 64), 0, s, a);
+    else if (mode == CELL_GIVEN)
+        hipLaunchKernelGGL((cell_elem_kernel<TS, CELL_GIVEN>), grid, dim3(EK_WAVES * 64), 0, s, a);
+    else
+        hipLaunchKernelGGL((cell_elem_kernel<TS, CELL_DENSE>), grid, dim3(EK_WAVES * 64), 0, s, a);
+}
+
+// CELL_GIVEN: the element kernel forms the chunk sums of squares of the given
+// matrix (chunk_sq must be set), and the select kernel copies the kept rows
+// from that matrix.
+static hipError_t launch_cell_split(CellArgs a, int mode, bool bf16, hipStream_t s) {
     const int nch = (int)ceil_div(a.B, 64);
     dim3 ge((unsigned)ceil_div(a.H, EK_UNITS), (unsigned)nch);
-    const bool sp = mode == CELL_SPARSE;
-    if (bf16) {
-        if (sp) hipLaunchKernelGGL((cell_elem_kernel<bf16_t, true>), ge, dim3(EK_WAVES * 64), 0, s, a);
-        else hipLaunchKernelGGL((cell_elem_kernel<bf16_t, false>), ge, dim3(EK_WAVES * 64), 0, s, a);
-    } else {
-        if (sp) hipLaunchKernelGGL((cell_elem_kernel<float, true>), ge, dim3(EK_WAVES * 64), 0, s, a);
-        else hipLaunchKernelGGL((cell_elem_kernel<float, false>), ge, dim3(EK_WAVES * 64), 0, s, a);
+    if (mode == CELL_GIVEN) {
+        if (!a.chunk_sq || !a.dG_in)
+            return hipErrorInvalidValue;
+        a.stage = const_cast<void *>(a.dG_in);
     }
+    if (bf16)
+        launch_elem<bf16_t>(a, mode, ge, s);
+    else
+        launch_elem<float>(a, mode, ge, s);
     hipError_t e = hipGetLastError();
-    if (e != hipSuccess || !sp)
+    if (e != hipSuccess || mode == CELL_DENSE)
         return e;
     const int grid = (int)ceil_div(a.nslices, (long)a.regions_per_wg * a.R);
     if (bf16)
@@ -993,7 +1026,7 @@ static hipError_t launch_fine_typed(const CellArgs &a, int mode, hipStream_t s) 
         // selected from its staging matrix
         const int nch = (int)ceil_div(a.B, 64);
         dim3 ge((unsigned)ceil_div(a.H, EK_UNITS), (unsigned)nch);
-        hipLaunchKernelGGL((cell_elem_kernel<TS, true>), ge, dim3(EK_WAVES * 64), 0, s, a);
+        hipLaunchKernelGGL((cell_elem_kernel<TS, CELL_SPARSE>), ge, dim3(EK_WAVES * 64), 0, s, a);
         hipError_t e = hipGetLastError();
         if (e != hipSuccess)
             return e;
@@ -1045,7 +1078,8 @@ static void launch_rows(const CellArgs &a, int grid, hipStream_t s) {
 }
 
 hipError_t launch_cell(const CellArgs &a, int mode, bool bf16, hipStream_t s) {
-    if (cell_split_ok(a, mode))
+    // the split path of a given matrix needs the caller's chunk-sum scratch
+    if (cell_split_ok(a, mode) && (mode != CELL_GIVEN || a.chunk_sq))
         return launch_cell_split(a, mode, bf16, s);
     if (cell_rows_ok(a)) {
         const int grid = (int)ceil_div(a.nslices, (long)a.regions_per_wg * a.R);

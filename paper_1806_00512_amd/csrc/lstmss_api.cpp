@@ -385,6 +385,20 @@ WsLayout ws_layout(const lstmss_dims *d, const Plan &p) {
     return L;
 }
 
+// Scratch of the standalone selection: the per-(row, 64-column chunk) sums of
+// squares of the element kernel when the shape takes the two-kernel path of
+// the backward pass (coarse structure), else nothing.
+size_t select_ws_bytes(const lstmss_dims *d, const Plan &p) {
+    if (p.fine)
+        return 0;
+    CellArgs probe{};
+    probe.B = d->B; probe.H = d->H; probe.P = p.P; probe.R = p.R;
+    probe.regions_per_wg = std::max(1, 32 / (p.R * p.P));
+    if (!cell_split_ok(probe, CELL_GIVEN))
+        return 0;
+    return align256((size_t)4 * d->H * ceil_div(d->B, 64) * 8);
+}
+
 // Streams and events one backward call is enqueued with.  In a layer stack
 // (lstm_bwd_stack) a layer's step t waits for the dX chunk of the layer above
 // that holds its upstream gradient dH_up[t], and records an event after each
@@ -1181,9 +1195,21 @@ int32_t lstm_bwd_structsparse(const lstmss_dims *d, float sparsity, const lstmss
                     idx_out, dbg_dgates, ws, ws_bytes, stream);
 }
 
+int64_t lstmss_select_workspace_bytes(const lstmss_dims *d, float sparsity,
+                                      const lstmss_structure *s) {
+    int32_t rc = check_dims(d);
+    if (rc)
+        return rc;
+    Plan p;
+    rc = make_plan(d, sparsity, s, false, &p);
+    if (rc)
+        return rc;
+    return (int64_t)select_ws_bytes(d, p);
+}
+
 int32_t lstmss_select_compact(const lstmss_dims *d, float sparsity, const lstmss_structure *s,
-                              const void *dG, void *dG_c, int32_t *idx, double *scores,
-                              void *stream) {
+                              const void *dG, void *dG_c, int32_t *idx, double *scores, void *ws,
+                              size_t ws_bytes, void *stream) {
     int32_t rc = check_dims(d);
     if (rc)
         return rc;
@@ -1193,6 +1219,10 @@ int32_t lstmss_select_compact(const lstmss_dims *d, float sparsity, const lstmss
         return rc;
     if (!dG || !dG_c || !idx)
         return fail(LSTMSS_ERR_INVALID_ARG, "a required pointer is NULL");
+    const size_t need = select_ws_bytes(d, p);
+    if (need > 0 && (!ws || ws_bytes < need))
+        return fail(LSTMSS_ERR_WORKSPACE, "workspace of %zu bytes, need %zu", ws ? ws_bytes : 0,
+                    need);
     CellArgs ca{};
     ca.B = d->B; ca.H = d->H; ca.I = d->I;
     ca.P = p.P; ca.R = p.R; ca.S = p.S;
@@ -1209,7 +1239,9 @@ int32_t lstmss_select_compact(const lstmss_dims *d, float sparsity, const lstmss
         HIP_TRY(timed(LSTMSS_KERNEL_GATES, st, [&] { return launch_cell_fine(ca, CELL_GIVEN, d->dtype == LSTMSS_BF16, st); }));
         return LSTMSS_OK;
     }
-    if (cell_lds_bytes(ca, CELL_GIVEN) > kMaxLds)
+    if (need > 0)  // the two-kernel path of the backward pass at this shape
+        ca.chunk_sq = (double *)ws;
+    else if (cell_lds_bytes(ca, CELL_GIVEN) > kMaxLds)
         return fail(LSTMSS_ERR_UNSUPPORTED, "R*P*B too large for one work-group's LDS");
     hipStream_t st = (hipStream_t)stream;
     HIP_TRY(timed(LSTMSS_KERNEL_GATES, st, [&] { return launch_cell(ca, CELL_GIVEN, d->dtype == LSTMSS_BF16, st); }));

@@ -35,7 +35,8 @@ SYMBOLS = ("lstmss_version", "lstmss_strerror", "lstmss_last_error", "lstmss_cac
            "lstmss_stack_workspace_bytes", "lstm_bwd_stack", "lstmss_time_reverse",
            "lstmss_bidir_join", "lstmss_bidir_workspace_bytes", "lstm_bwd_bidir",
            "lstm_fwd_cache", "lstm_bwd_dense",
-           "lstm_bwd_structsparse", "lstmss_select_compact", "lstmss_set_option",
+           "lstm_bwd_structsparse", "lstmss_select_workspace_bytes", "lstmss_select_compact",
+           "lstmss_set_option",
            "lstmss_timing_enable", "lstmss_timing_read", "lstmss_timing_reset")
 KERNEL_KINDS = {"gates_select_compact": 0, "data_grad_gemm": 1, "weight_grad_gemm": 2, "aux": 3,
                 "forward_step": 4}
@@ -109,7 +110,9 @@ def load():
     lib.lstm_bwd_structsparse.argtypes = [pd, f, ps, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp,
                                           vp, vp, vp, ctypes.c_size_t, vp]
     lib.lstm_bwd_structsparse.restype = i32
-    lib.lstmss_select_compact.argtypes = [pd, f, ps, vp, vp, vp, vp, vp]
+    lib.lstmss_select_workspace_bytes.argtypes = [pd, f, ps]
+    lib.lstmss_select_workspace_bytes.restype = i64
+    lib.lstmss_select_compact.argtypes = [pd, f, ps, vp, vp, vp, vp, vp, ctypes.c_size_t, vp]
     lib.lstmss_select_compact.restype = i32
     lib.lstmss_set_option.argtypes = [i32, i32]
     lib.lstmss_set_option.restype = i32
@@ -193,6 +196,14 @@ def workspace_bytes(d: Dims, sparsity: float = 0.0, s: Structure | None = None) 
     n = load().lstmss_workspace_bytes(ctypes.byref(d), float(sparsity),
                                       ctypes.byref(s) if s is not None else None)
     _check(0 if n >= 0 else int(n), "lstmss_workspace_bytes")
+    return int(n)
+
+
+def select_workspace_bytes(d: Dims, sparsity: float, s: Structure) -> int:
+    """Scratch of lstmss_select_compact (0 unless the shape takes the
+    two-kernel path of the backward pass)."""
+    n = load().lstmss_select_workspace_bytes(ctypes.byref(d), float(sparsity), ctypes.byref(s))
+    _check(0 if n >= 0 else int(n), "lstmss_select_workspace_bytes")
     return int(n)
 
 
@@ -460,7 +471,9 @@ def bwd_structsparse(x, W, cache, dH_up, sparsity=0.5, P=4, R=8, dhT=None, dcT=N
 
 def select_compact(dG, sparsity=0.5, P=4, R=8, want_scores=True, stream=None, kind=COARSE,
                    My=0, Mx=0):
-    """Score / select / compact one gate-gradient matrix dG [4H][B].
+    """Score / select / compact one gate-gradient matrix dG [4H][B] with the
+    kernels the backward pass runs at this shape (the two-kernel path, with
+    its chunk-sum scratch allocated here, at H*B >= 65536).
 
     COARSE: (kept rows [K'][B], kept slice indices, slice scores [4H/P]).
     FINE: (masked matrix [4H][B], kept block indices [4H/Mx][nb-K],
@@ -482,9 +495,12 @@ def select_compact(dG, sparsity=0.5, P=4, R=8, want_scores=True, stream=None, ki
         idx = torch.empty((ne,), dtype=torch.int32, device=dG.device)
         sc = (torch.empty((G // P,), dtype=torch.float64, device=dG.device)
               if want_scores else None)
+    n = select_workspace_bytes(d, sparsity, s)
+    ws = torch.empty(n, dtype=torch.uint8, device=dG.device) if n > 0 else None
     rc = load().lstmss_select_compact(ctypes.byref(d), float(sparsity), ctypes.byref(s),
                                       _ptr(dG, st, name="dG"), _ptr(dGc), _ptr(idx), _ptr(sc),
-                                      _stream(stream))
+                                      _ptr(ws, torch.uint8, name="ws"),
+                                      0 if ws is None else ws.numel(), _stream(stream))
     _check(rc, "lstmss_select_compact")
     return dGc, idx, sc
 

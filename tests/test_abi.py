@@ -66,6 +66,27 @@ def test_sizes(L):
         assert wd > ws >= 35 * 1300 * 20 * es
 
 
+@pytest.mark.parametrize("H,B,P,R,sp,split", [
+    (2048, 128, 4, 8, 0.5, True), (4096, 256, 4, 8, 0.5, True), (260, 256, 4, 8, 0.5, True),
+    (1024, 64, 4, 8, 0.75, True), (128, 16, 4, 8, 0.5, False), (1023, 64, 4, 8, 0.5, False),
+    (2048, 128, 4, 128, 0.5, None), (2048, 128, 16, 32, 0.5, False)])
+def test_select_workspace(L, H, B, P, R, sp, split):
+    """The standalone selection needs scratch exactly where the backward pass
+    takes the two-kernel gate path (H*B >= 65536 and a region group that fits
+    the select kernel): one fp64 sum of squares per row and 64-column chunk."""
+    d = L.dims(1, B, 1, H)
+    if split is None:
+        with pytest.raises(L.LstmssError):
+            L.select_workspace_bytes(d, sp, L.structure(P, R))
+        return
+    n = L.select_workspace_bytes(d, sp, L.structure(P, R))
+    if split:
+        assert n >= 4 * H * (-(-B // 64)) * 8 and n % 256 == 0
+    else:
+        assert n == 0
+    assert L.select_workspace_bytes(d, 0.5, L.structure(kind=L.FINE, My=8, Mx=4)) == 0
+
+
 @pytest.mark.parametrize("args,code", [
     ((0, 4, 4, 8), -1), ((2, 4, 4, -1), -1), ((2, 4, 4, 8, 7), -2)])
 def test_bad_dims(L, args, code):

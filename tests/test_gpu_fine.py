@@ -13,7 +13,7 @@ import pytest
 import torch
 
 import oracle
-from paper_1806_00512_amd.inputs import make_layer
+from paper_1806_00512_amd.inputs import WORKLOADS, make_inputs, make_layer
 
 pytestmark = pytest.mark.gpu
 
@@ -161,6 +161,27 @@ def test_layer_fine_f32(L, T, B, I, H, sp, Mx, My, state):
 def test_layer_fine_bf16(L, T, B, I, H, sp, Mx, My):
     d = make_layer(T, B, I, H, seed=17 + B, w_scale=0.2, dtype="bf16", state=True)
     check_layer_fine(L, d, "bf16", sp, Mx, My)
+
+
+@pytest.mark.parametrize("T,B,I,H,Mx,My,dtype", [
+    (3, 128, 2048, 2048, 4, 8, "f32"),    # the 4-layer workload's layer shape, the paper's blocks
+    (3, 128, 2048, 2048, 32, 32, "f32"),  # same shape, MFMA-shaped blocks (products skip)
+    (2, 256, 64, 256, 4, 8, "f32"),
+    (2, 256, 64, 256, 4, 8, "bf16"),
+    (2, 256, 64, 256, 32, 32, "f32"),
+    (2, 256, 64, 256, 32, 32, "bf16"),
+])
+def test_fine_large_shape(L, T, B, I, H, Mx, My, dtype):
+    """Shapes with H*B >= 65536, where the element kernel forms the gate
+    gradient into the staging matrix and the fine selection reads it (the
+    path the benchmark's fine-structure rows time); at the 4-layer workload's
+    layer shape the weights and inputs are that workload's (T cut to 3)."""
+    if H == 2048:
+        inp = make_inputs(WORKLOADS["lstm4_enc_h2048_b128_t50_f32"].truncated(T), seed=0)
+        d = {"x": inp["x"], "W": inp["Ws"][0], "b": None, "dH_up": inp["dH_up"]}
+    else:
+        d = make_layer(T, B, I, H, seed=H + My + Mx, w_scale=0.1, dtype=dtype, state=True)
+    check_layer_fine(L, d, dtype, 0.5, Mx, My)
 
 
 def test_fine_language_model_shape(L):

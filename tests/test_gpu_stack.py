@@ -1,11 +1,22 @@
 """GPU: the wavefront backward of a layer stack (lstm_bwd_stack) gives the
 same bits as the layers' backward calls made one after the other, top layer
-first; with graphs and without, for the coarse, fine and dense cases."""
+first; with graphs and without, for the coarse, fine and dense cases; and at
+the benchmark's own shape it matches the oracle layer by layer."""
 import numpy as np
 import pytest
 import torch
 
+import oracle
+from paper_1806_00512_amd.inputs import WORKLOADS, make_inputs
+
 pytestmark = pytest.mark.gpu
+
+
+def rel(a, b):
+    a = a.double().cpu().numpy() if isinstance(a, torch.Tensor) else np.asarray(a, np.float64)
+    b = np.asarray(b, np.float64)
+    n = np.linalg.norm(b)
+    return float(np.linalg.norm(a - b) / (n if n > 0 else 1.0))
 
 
 @pytest.fixture(scope="module")
@@ -85,6 +96,84 @@ def test_stack_matches_sequential(L, graphs, layers, T, B, I, H, sparsity, kw, d
     finally:
         L.graphs_enable(True)
         L.set_option("stack_dx_steps", 0)
+
+
+def workload_stack(L, name, layers, T):
+    """GPU tensors of the first `layers` layers of a workload (T steps): the
+    per-layer inputs (layer l > 0 takes the h_out of the layer below),
+    weights and caches, and the top layer's upstream gradient."""
+    wl = WORKLOADS[name].truncated(T)
+    inp = make_inputs(wl, seed=0)
+    dev = torch.device("cuda:0")
+    xs, Ws, caches = [], [], []
+    x = torch.from_numpy(inp["x"]).to(dev)
+    for l in range(layers):
+        W = torch.from_numpy(inp["Ws"][l]).to(dev)
+        h, cache = L.fwd_cache(x, W)
+        xs.append(x)
+        Ws.append(W)
+        caches.append(cache)
+        x = h
+    dH = torch.from_numpy(inp["dH_up"]).to(dev)
+    return xs, Ws, caches, dH
+
+
+def test_stack_headline_shape_matches_sequential(L):
+    """The benchmark's step call at its layer shape (I = H = 2048, B = 128):
+    two layers over T = 26 steps, so each layer's input gradient comes in
+    launches of 12, 12 and 2 steps under the cross-layer waits, with the
+    two-kernel gate path and 64 x 64 DMA tiles; the bottom layer's input
+    gradient too (the benchmark asks for it).  Same bits as the layers'
+    calls in turn."""
+    xs, Ws, caches, dH = workload_stack(L, "lstm4_enc_h2048_b128_t50_f32", 2, 26)
+    kw = {"P": 4, "R": 8}
+    ref = sequential(L, xs, Ws, caches, dH, 0.5, kw)
+    ref[0] = L.bwd_structsparse(xs[0], Ws[0], caches[0], ref[1]["dX"], sparsity=0.5, **kw)
+    got = L.bwd_stack(xs, Ws, caches, dH, sparsity=0.5, want_dX0=True, **kw)
+    torch.cuda.synchronize()
+    for l in range(2):
+        for k in ("dW", "db", "dX", "idx"):
+            assert torch.equal(got[k][l], ref[l][k]), (k, l)
+
+
+def test_stack_headline_shape_oracle(L):
+    """The benchmark's step call, the four-layer wavefront stack at the
+    4-layer workload's shape with T = 14 (one 12-step and one 2-step input-
+    gradient launch per layer), against the oracle: every layer's masks in
+    situ (the stack's indices equal those of the layers' calls in turn,
+    whose pre-sparsify gate gradients the oracle re-selects bit for bit),
+    and every layer's dW, db and dX against the oracle run with those masks
+    on the stack's own upstream gradient, to rel. L2 <= 1e-5."""
+    layers, T, P, R, S = 4, 14, 4, 8, 4
+    xs, Ws, caches, dH = workload_stack(L, "lstm4_enc_h2048_b128_t50_f32", layers, T)
+    got = L.bwd_stack(xs, Ws, caches, dH, sparsity=0.5, P=P, R=R, want_dX0=True)
+    torch.cuda.synchronize()
+    H = Ws[0].shape[0] // 4
+    up = dH
+    for l in reversed(range(layers)):
+        # in situ: the layer's own call (same kernels) with its gate gradients
+        o = L.bwd_structsparse(xs[l], Ws[l], caches[l], up, sparsity=0.5, P=P, R=R,
+                               want_dbg=True)
+        torch.cuda.synchronize()
+        assert torch.equal(o["idx"], got["idx"][l]), l
+        assert torch.equal(o["dW"], got["dW"][l]), l
+        idx = got["idx"][l].cpu().numpy()
+        dbg = o["dbg"].double().cpu().numpy()
+        keep = np.zeros((T, 4 * H // P), np.uint8)
+        for t in range(T):
+            k = oracle.select(oracle.scores(dbg[t], P), R, S)
+            assert np.array_equal(oracle.kept_index(k), idx[t]), (l, t)
+            keep[t] = k
+        # gradients against the oracle with the stack's masks
+        x_np = xs[l].double().cpu().numpy()
+        W_np = Ws[l].double().cpu().numpy()
+        gates, c, h = oracle.forward(x_np, W_np)
+        ref = oracle.backward(x_np, W_np, gates, c, h, up.double().cpu().numpy(), P=P, R=R, S=S,
+                              forced_keep=keep)
+        for k in ("dW", "db", "dX"):
+            e = rel(got[k][l], ref[k])
+            assert e <= 1e-5, (l, k, e)
+        up = got["dX"][l]
 
 
 def test_stack_bf16(L):
