@@ -202,6 +202,24 @@ int32_t lstmss_select_compact(const lstmss_dims *d, float sparsity, const lstmss
                               const void *dG, void *dG_c, int32_t *idx, double *scores, void *ws,
                               size_t ws_bytes, void *stream);
 
+/* lstmss_select_compact without a workspace, for callers that cannot
+ * allocate device memory (code under HIP graph capture, tight serving loops,
+ * harnesses that forbid allocation).  Same arguments and results as
+ * lstmss_select_compact (bit for bit); the scratch of the two-kernel path
+ * (lstmss_select_workspace_bytes, 4H * ceil(B/64) * 8 bytes rounded up to
+ * 256) comes from a static device array of LSTMSS_NOALLOC_SCRATCH_BYTES
+ * that every GPU the library runs on holds until the process ends.  It
+ * allocates nothing and enqueues only the selection kernels; shapes whose
+ * scratch exceeds the array return LSTMSS_ERR_UNSUPPORTED before any
+ * pointer is used.  All calls on one GPU share that GPU's array (it keeps
+ * the last call's contents, which every call overwrites before reading), so
+ * calls that overlap in time on one GPU race: serialise them (one stream).
+ * Not affected by the timing hooks. */
+#define LSTMSS_NOALLOC_SCRATCH_BYTES (1 << 20)
+int32_t lstmss_select_compact_noalloc(const lstmss_dims *d, float sparsity,
+                                      const lstmss_structure *s, const void *dG, void *dG_c,
+                                      int32_t *idx, double *scores, void *stream);
+
 /* Backward pass of a stack of `layers` (1..8) LSTM layers, bottom layer 0,
  * scheduled as a wavefront (the layer-time pipelining of a stacked LSTM):
  * layer l's input gradient dX[l] is layer l-1's upstream gradient, and

@@ -11,7 +11,7 @@ CSRC = os.path.join(HERE, "csrc")
 ROOT = os.path.dirname(HERE)
 LIB = os.path.join(HERE, "liblstmss.so")
 SOURCES = ["lstmss_api.cpp", "cell.hip", "gemm1.hip", "wgrad_f32.hip", "wgrad_bf16.hip", "gemm.hip",
-           "train.hip", "bidir.hip"]
+           "train.hip", "bidir.hip", "noalloc.hip"]
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 
 

@@ -4,6 +4,8 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include "../../include/lstmss.h"
+
 namespace lstmss {
 
 enum CellMode { CELL_DENSE = 0, CELL_SPARSE = 1, CELL_GIVEN = 2 };
@@ -190,6 +192,15 @@ hipError_t launch_copy_in(float *dst, const float *src, long n, hipStream_t s); 
 hipError_t launch_reduce_parts(float *out, const float *part, int nparts, long stride, long n,
                                hipStream_t s);
 hipError_t launch_h0_store(void *dst, const float *src, long n, bool bf16, hipStream_t s);
+
+// Host-side pieces of the C ABI shared with the entry point that allocates
+// nothing (noalloc.hip): the last-error setter, the standalone selection's
+// scratch size and the selection itself (hooks: timing hooks enabled).
+int32_t set_error(int32_t code, const char *msg);
+int64_t select_scratch_bytes(const lstmss_dims *d, float sparsity, const lstmss_structure *s);
+int32_t select_compact_impl(const lstmss_dims *d, float sparsity, const lstmss_structure *s,
+                            const void *dG, void *dG_c, int32_t *idx, double *scores, void *ws,
+                            size_t ws_bytes, void *stream, bool hooks);
 
 // Tile constants shared by the host-side sizing code.
 constexpr int GEMM1_TK = 64;       // granularity of a split's k range

@@ -870,6 +870,69 @@ int32_t bidir_enqueue(const lstmss_dims *d, bool dense, const Plan &p, const voi
 
 } // namespace
 
+namespace lstmss {
+
+int32_t set_error(int32_t code, const char *msg) { return fail(code, "%s", msg); }
+
+int64_t select_scratch_bytes(const lstmss_dims *d, float sparsity, const lstmss_structure *s) {
+    int32_t rc = check_dims(d);
+    if (rc)
+        return rc;
+    Plan p;
+    rc = make_plan(d, sparsity, s, false, &p);
+    if (rc)
+        return rc;
+    return (int64_t)select_ws_bytes(d, p);
+}
+
+// The standalone selection (lstmss_select_compact); `hooks` false skips the
+// timing hooks (whose event pool may create events), for the entry point
+// that must not allocate.
+int32_t select_compact_impl(const lstmss_dims *d, float sparsity, const lstmss_structure *s,
+                            const void *dG, void *dG_c, int32_t *idx, double *scores, void *ws,
+                            size_t ws_bytes, void *stream, bool hooks) {
+    int32_t rc = check_dims(d);
+    if (rc)
+        return rc;
+    Plan p;
+    rc = make_plan(d, sparsity, s, false, &p);
+    if (rc)
+        return rc;
+    if (!dG || !dG_c || !idx)
+        return fail(LSTMSS_ERR_INVALID_ARG, "a required pointer is NULL");
+    const size_t need = select_ws_bytes(d, p);
+    if (need > 0 && (!ws || ws_bytes < need))
+        return fail(LSTMSS_ERR_WORKSPACE, "workspace of %zu bytes, need %zu", ws ? ws_bytes : 0,
+                    need);
+    CellArgs ca{};
+    ca.B = d->B; ca.H = d->H; ca.I = d->I;
+    ca.P = p.P; ca.R = p.R; ca.S = p.S;
+    ca.nslices = p.nslices;
+    ca.regions_per_wg = std::max(1, 32 / (p.R * p.P));
+    ca.dG_in = dG;
+    ca.dGc = dG_c;
+    ca.idx = idx;
+    ca.scores = scores;
+    ca.My = p.My;
+    ca.nb = p.nb;
+    if (p.fine) {
+        hipStream_t st = (hipStream_t)stream;
+        auto go = [&] { return launch_cell_fine(ca, CELL_GIVEN, d->dtype == LSTMSS_BF16, st); };
+        HIP_TRY(hooks ? timed(LSTMSS_KERNEL_GATES, st, go) : go());
+        return LSTMSS_OK;
+    }
+    if (need > 0)  // the two-kernel path of the backward pass at this shape
+        ca.chunk_sq = (double *)ws;
+    else if (cell_lds_bytes(ca, CELL_GIVEN) > kMaxLds)
+        return fail(LSTMSS_ERR_UNSUPPORTED, "R*P*B too large for one work-group's LDS");
+    hipStream_t st = (hipStream_t)stream;
+    auto go = [&] { return launch_cell(ca, CELL_GIVEN, d->dtype == LSTMSS_BF16, st); };
+    HIP_TRY(hooks ? timed(LSTMSS_KERNEL_GATES, st, go) : go());
+    return LSTMSS_OK;
+}
+
+} // namespace lstmss
+
 extern "C" {
 
 int32_t lstmss_time_reverse(int32_t T, int64_t step_bytes, const void *src, void *dst,
@@ -1197,55 +1260,14 @@ int32_t lstm_bwd_structsparse(const lstmss_dims *d, float sparsity, const lstmss
 
 int64_t lstmss_select_workspace_bytes(const lstmss_dims *d, float sparsity,
                                       const lstmss_structure *s) {
-    int32_t rc = check_dims(d);
-    if (rc)
-        return rc;
-    Plan p;
-    rc = make_plan(d, sparsity, s, false, &p);
-    if (rc)
-        return rc;
-    return (int64_t)select_ws_bytes(d, p);
+    return lstmss::select_scratch_bytes(d, sparsity, s);
 }
 
 int32_t lstmss_select_compact(const lstmss_dims *d, float sparsity, const lstmss_structure *s,
                               const void *dG, void *dG_c, int32_t *idx, double *scores, void *ws,
                               size_t ws_bytes, void *stream) {
-    int32_t rc = check_dims(d);
-    if (rc)
-        return rc;
-    Plan p;
-    rc = make_plan(d, sparsity, s, false, &p);
-    if (rc)
-        return rc;
-    if (!dG || !dG_c || !idx)
-        return fail(LSTMSS_ERR_INVALID_ARG, "a required pointer is NULL");
-    const size_t need = select_ws_bytes(d, p);
-    if (need > 0 && (!ws || ws_bytes < need))
-        return fail(LSTMSS_ERR_WORKSPACE, "workspace of %zu bytes, need %zu", ws ? ws_bytes : 0,
-                    need);
-    CellArgs ca{};
-    ca.B = d->B; ca.H = d->H; ca.I = d->I;
-    ca.P = p.P; ca.R = p.R; ca.S = p.S;
-    ca.nslices = p.nslices;
-    ca.regions_per_wg = std::max(1, 32 / (p.R * p.P));
-    ca.dG_in = dG;
-    ca.dGc = dG_c;
-    ca.idx = idx;
-    ca.scores = scores;
-    ca.My = p.My;
-    ca.nb = p.nb;
-    if (p.fine) {
-        hipStream_t st = (hipStream_t)stream;
-        HIP_TRY(timed(LSTMSS_KERNEL_GATES, st, [&] { return launch_cell_fine(ca, CELL_GIVEN, d->dtype == LSTMSS_BF16, st); }));
-        return LSTMSS_OK;
-    }
-    if (need > 0)  // the two-kernel path of the backward pass at this shape
-        ca.chunk_sq = (double *)ws;
-    else if (cell_lds_bytes(ca, CELL_GIVEN) > kMaxLds)
-        return fail(LSTMSS_ERR_UNSUPPORTED, "R*P*B too large for one work-group's LDS");
-    hipStream_t st = (hipStream_t)stream;
-    HIP_TRY(timed(LSTMSS_KERNEL_GATES, st, [&] { return launch_cell(ca, CELL_GIVEN, d->dtype == LSTMSS_BF16, st); }));
-    return LSTMSS_OK;
+    return lstmss::select_compact_impl(d, sparsity, s, dG, dG_c, idx, scores, ws, ws_bytes, stream,
+                                       true);
 }
 
 int32_t lstmss_set_option(int32_t option, int32_t value) {

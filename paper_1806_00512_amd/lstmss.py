@@ -36,7 +36,7 @@ SYMBOLS = ("lstmss_version", "lstmss_strerror", "lstmss_last_error", "lstmss_cac
            "lstmss_bidir_join", "lstmss_bidir_workspace_bytes", "lstm_bwd_bidir",
            "lstm_fwd_cache", "lstm_bwd_dense",
            "lstm_bwd_structsparse", "lstmss_select_workspace_bytes", "lstmss_select_compact",
-           "lstmss_set_option",
+           "lstmss_select_compact_noalloc", "lstmss_set_option",
            "lstmss_timing_enable", "lstmss_timing_read", "lstmss_timing_reset")
 KERNEL_KINDS = {"gates_select_compact": 0, "data_grad_gemm": 1, "weight_grad_gemm": 2, "aux": 3,
                 "forward_step": 4}
@@ -114,6 +114,8 @@ def load():
     lib.lstmss_select_workspace_bytes.restype = i64
     lib.lstmss_select_compact.argtypes = [pd, f, ps, vp, vp, vp, vp, vp, ctypes.c_size_t, vp]
     lib.lstmss_select_compact.restype = i32
+    lib.lstmss_select_compact_noalloc.argtypes = [pd, f, ps, vp, vp, vp, vp, vp]
+    lib.lstmss_select_compact_noalloc.restype = i32
     lib.lstmss_set_option.argtypes = [i32, i32]
     lib.lstmss_set_option.restype = i32
     lib.lstmss_timing_enable.argtypes = [i32]
@@ -503,6 +505,24 @@ def select_compact(dG, sparsity=0.5, P=4, R=8, want_scores=True, stream=None, ki
                                       0 if ws is None else ws.numel(), _stream(stream))
     _check(rc, "lstmss_select_compact")
     return dGc, idx, sc
+
+
+NOALLOC_SCRATCH_BYTES = 1 << 20
+
+
+def select_compact_noalloc(dG, dG_c, idx, scores=None, sparsity=0.5, P=4, R=8, stream=None,
+                           kind=COARSE, My=0, Mx=0):
+    """lstmss_select_compact_noalloc on caller-given outputs (nothing is
+    allocated here or in the library): dG [4H][B], dG_c [K'][B] (or the
+    masked [4H][B] for FINE), idx, scores (or None)."""
+    G, B = dG.shape
+    d = dims(1, B, 1, G // 4, dG.dtype)
+    s = structure(P, R, kind, My, Mx)
+    rc = load().lstmss_select_compact_noalloc(
+        ctypes.byref(d), float(sparsity), ctypes.byref(s), _ptr(dG, name="dG"),
+        _ptr(dG_c, dG.dtype, name="dG_c"), _ptr(idx, torch.int32, name="idx"),
+        _ptr(scores, torch.float64, name="scores"), _stream(stream))
+    _check(rc, "lstmss_select_compact_noalloc")
 
 
 def cache_views(cache, T, B, H, dtype):
