@@ -16,9 +16,11 @@ launch duration for the roofline.  The forward pass, whole training steps
 beside it.
 
 Default workload: the 4-layer sequence-to-sequence encoder shape
-(I = H = 2048, B = 128, T = 50, fp32).  The two-layer language-model shape
-(I = H = 650, B = 20, T = 35) is measured beside it (sparse and dense step
-times only) and reported under "also".
+(I = H = 2048, B = 128, T = 50, fp32).  Every other workload shape (the
+small 1-layer H = 128 case, the 2-layer language-model shape, the 2-layer
+H = 1024 shape with its sparsity sweep, and the bf16 1-layer H = 4096 shape
+with its 9 sparse : 1 dense schedule) is measured beside it and reported
+under "also", each with its own per-kernel roofline.
 
 Prints ONE JSON line.  value = effective TFLOP/s: the dense backward's flops
 (16 H B (I+H) T per layer) divided by the sparse step time.
@@ -35,7 +37,8 @@ sys.path.insert(0, ROOT)
 
 METRIC = "LSTM backward ms/step and effective TFLOP/s at 50% structured sparsity vs dense"
 DEFAULT_WORKLOAD = "lstm4_enc_h2048_b128_t50_f32"
-ALSO_WORKLOADS = ("lstm2_lm_h650_b20_t35_f32", "lstm2_h1024_b64_t35_f32")
+ALSO_WORKLOADS = ("lstm1_h128_b16_t20_f32", "lstm2_lm_h650_b20_t35_f32",
+                  "lstm2_h1024_b64_t35_f32", "lstm1_h4096_b256_t100_bf16")
 PEAK = {"hbm_gbs": 8000.0, "f32_tflops": 157.3, "bf16_tflops": 2516.6}
 KINDS = ("gates_select_compact", "data_grad_gemm", "weight_grad_gemm")
 # device kernel behind each timed kind whose HBM counters may be on file
@@ -126,31 +129,90 @@ def traffic_on_file(kind, workload):
         return None
 
 
-def roofline_entry(name, work, avg_s, dtype, traffic):
+def rocprof_on_file(kind, workload):
+    """Average launch duration (us) of a kernel kind in the committed
+    rocprofv3 kernel-trace summary of this workload's benchmark command (its
+    per-kernel timing pass), or None when there is none or the kernel sources
+    changed since it was taken."""
+    path = os.path.join(ROOT, "profiles", "kernels_%s.txt" % workload)
+    if not os.path.exists(path):
+        return None
+    rec = {}
+    with open(path) as f:
+        for line in f:
+            if ":" in line and not line.startswith((" ", "#")):
+                k, v = line.split(":", 1)
+                rec[k.strip()] = v.strip()
+    if rec.get("sources_sha256_16") != sources_digest():
+        return None
+    try:
+        return float(rec["rocprof_avg_us_" + kind])
+    except (KeyError, ValueError):
+        return None
+
+
+def roofline_entry(name, work, avg_s, dtype, traffic, rocprof_us=None):
     """work: algorithmic bytes/flops of one average launch; avg_s: its mean
-    event-measured duration."""
+    event-measured duration; rocprof_us: the same kind's average duration in
+    the committed rocprofv3 summary (frac_rocprof is then reported beside
+    frac)."""
     peak_tf = PEAK["bf16_tflops"] if dtype == "bf16" else PEAK["f32_tflops"]
     t_mem = work["bytes"] / (PEAK["hbm_gbs"] * 1e9)
     t_mfma = work["flops"] / (peak_tf * 1e12)
     common = {"traffic": None if traffic is None else round(traffic),
               "avg_launch_us": round(avg_s * 1e6, 3), "algorithmic_flops": work["flops"],
               "algorithmic_bytes": work["bytes"]}
+    if rocprof_us:
+        common["avg_launch_us_rocprof"] = round(rocprof_us, 3)
     if t_mfma > t_mem:
         ach = work["flops"] / avg_s / 1e12
-        return dict({"kernel": name, "bound": "mfma", "achieved": round(ach, 3), "peak": peak_tf,
-                     "unit": "TFLOP/s", "frac": round(ach / peak_tf, 4)}, **common)
+        e = dict({"kernel": name, "bound": "mfma", "achieved": round(ach, 3), "peak": peak_tf,
+                  "unit": "TFLOP/s", "frac": round(ach / peak_tf, 4)}, **common)
+        if rocprof_us:
+            e["frac_rocprof"] = round(work["flops"] / (rocprof_us * 1e-6) / 1e12 / peak_tf, 4)
+        return e
     ach = work["bytes"] / avg_s / 1e9
-    return dict({"kernel": name, "bound": "hbm", "achieved": round(ach, 1),
-                 "peak": PEAK["hbm_gbs"], "unit": "GB/s", "frac": round(ach / PEAK["hbm_gbs"], 4)},
-                **common)
+    e = dict({"kernel": name, "bound": "hbm", "achieved": round(ach, 1),
+              "peak": PEAK["hbm_gbs"], "unit": "GB/s", "frac": round(ach / PEAK["hbm_gbs"], 4)},
+             **common)
+    if rocprof_us:
+        e["frac_rocprof"] = round(work["bytes"] / (rocprof_us * 1e-6) / 1e9 / PEAK["hbm_gbs"], 4)
+    return e
 
 
-def cpu_baseline(wl, inp, sparsity, budget_s=20.0):
-    """Time the CPU oracle (as it stands) on a bounded sample of the workload:
-    the backward of the first T' steps of the bottom layer, T' sized from a
-    2-step probe to about budget_s; when a whole layer is shorter than that,
-    further layers of the same call (each with the oracle's own input) are
-    added while the total stays under budget_s."""
+def roofline_all(L, wl, sparsity, kt, steps):
+    """Roofline entry of every timed kernel kind from a per-kernel timing pass
+    (kt) of `steps` sparse steps of workload wl."""
+    st_dt = "bf16" if wl.dtype == "bf16" else "f32"
+    es = 2 if wl.dtype == "bf16" else 4
+    kps = [L.kept_rows(L.dims(wl.steps, wl.batch, wl.layer_input(l), wl.hidden, st_dt), sparsity,
+                       L.structure(wl.P, wl.R)) for l in range(wl.layers)]
+    roofs = {}
+    for name in KINDS:
+        ms, n = kt[name]
+        # work of one step (all layers) times the timed steps, spread over
+        # the launches of this kind: the average launch's algorithmic work
+        works = [kernel_work(wl, l, kps[l], es)[name] for l in range(wl.layers)]
+        per_launch = {k: sum(w[k] for w in works) * steps / max(n, 1) for k in ("bytes", "flops")}
+        roofs[name] = roofline_entry(name, per_launch, ms / 1e3 / max(n, 1), wl.dtype,
+                                     traffic_on_file(name, wl.name),
+                                     rocprof_on_file(name, wl.name))
+    return roofs, kps
+
+
+def kernel_table(kt, steps):
+    return {name: {"total_ms_per_step": round(kt[name][0] / steps, 5), "launches": kt[name][1],
+                   "avg_us": round(kt[name][0] / max(kt[name][1], 1) * 1e3, 3)}
+            for name in KINDS + ("aux",)}
+
+
+def cpu_baseline(wl, inp, sparsity, budget_s=20.0, budget_1core_s=10.0):
+    """Time the CPU oracle (as it stands) on a bounded sample of the workload,
+    once with all host cores (the oracle's OpenMP threads) and once on one
+    core: the backward of the first T' steps of the bottom layer, T' sized
+    from a 2-step probe to about the budget; with all cores, when a whole
+    layer is shorter than that, further layers of the same call (each with
+    the oracle's own input) are added while the total stays under budget_s."""
     import oracle
     S = int(round(sparsity * wl.R))
     x = inp["x"]
@@ -162,27 +224,46 @@ def cpu_baseline(wl, inp, sparsity, budget_s=20.0):
         oracle.backward(layer_x[:Tp], W, gates, c, h, dH[:Tp], P=wl.P, R=wl.R, S=S)
         return time.perf_counter() - t0, h
 
-    Tp = 2
-    dt, h = run(x, inp["Ws"][0], Tp)
-    for _ in range(3):  # re-size from the last run (the first pays thread start-up)
-        want = int(max(2, min(wl.steps, Tp * budget_s / max(dt, 1e-6))))
-        if want <= Tp or (dt >= 0.5 * budget_s and want < 2 * Tp):
-            break
-        Tp = want
+    def sized(budget):
+        Tp = 2
         dt, h = run(x, inp["Ws"][0], Tp)
-    flops = 16.0 * wl.hidden * wl.batch * (wl.layer_input(0) + wl.hidden) * Tp
+        for _ in range(3):  # re-size from the last run (the first pays thread start-up)
+            want = int(max(2, min(wl.steps, Tp * budget / max(dt, 1e-6))))
+            if want <= Tp or (dt >= 0.5 * budget and want < 2 * Tp):
+                break
+            Tp = want
+            dt, h = run(x, inp["Ws"][0], Tp)
+        return Tp, dt, h
+
+    def flops(layer, Tp):
+        return 16.0 * wl.hidden * wl.batch * (wl.layer_input(layer) + wl.hidden) * Tp
+
+    cores = oracle.threads()
+    Tp, dt, h = sized(budget_s)
+    fl = flops(0, Tp)
     layers = 1
     while Tp == wl.steps and layers < wl.layers and dt * (layers + 1) / layers <= budget_s:
         d1, h = run(h[1:], inp["Ws"][layers], Tp)
         dt += d1
-        flops += 16.0 * wl.hidden * wl.batch * (wl.layer_input(layers) + wl.hidden) * Tp
+        fl += flops(layers, Tp)
         layers += 1
-    return {"value": round(flops / dt / 1e12, 6), "unit": "TFLOP/s", "cores": oracle.threads(),
-            "kind": "oracle",
-            "sample": "fp64 oracle backward (sparsity %.2f) of the bottom %d layer(s) over %d of %d "
-                      "steps, %.2f s; effective TFLOP/s counts the dense flops 16*H*B*(I+H)*T' per "
-                      "layer" % (sparsity, layers, Tp, wl.steps, dt),
-            "ms_per_layer_step": round(dt / (Tp * layers) * 1e3, 3)}
+    out = {"value": round(fl / dt / 1e12, 6), "unit": "TFLOP/s", "cores": cores,
+           "kind": "oracle",
+           "sample": "fp64 oracle backward (sparsity %.2f) of the bottom %d layer(s) over %d of %d "
+                     "steps, %.2f s on %d threads; effective TFLOP/s counts the dense flops "
+                     "16*H*B*(I+H)*T' per layer" % (sparsity, layers, Tp, wl.steps, dt, cores),
+           "ms_per_layer_step": round(dt / (Tp * layers) * 1e3, 3)}
+    oracle.set_threads(1)
+    try:
+        Tp1, dt1, _ = sized(budget_1core_s)
+    finally:
+        oracle.set_threads(cores)
+    out["single_core"] = {
+        "value": round(flops(0, Tp1) / dt1 / 1e12, 6), "unit": "TFLOP/s", "cores": 1,
+        "sample": "the same oracle backward of the bottom layer over %d of %d steps, %.2f s on "
+                  "one thread" % (Tp1, wl.steps, dt1),
+        "ms_per_layer_step": round(dt1 / Tp1 * 1e3, 3)}
+    return out
 
 
 class Runner:
@@ -346,10 +427,13 @@ class Runner:
         return e0.elapsed_time(e1) / n, wall / n * 1e3, [v / n for v in per_layer]
 
 
-def measure(L, torch, wl, sparsity, steps, warmup, sparse_only=False, kernels=True, fine=None):
+def measure(L, torch, wl, sparsity, steps, warmup, sparse_only=False, kernels=True, fine=None,
+            schedules=True, forward=True, mix_cycles_min=1):
     """Backward step timings.  The headline step is the wavefront stack call
     (every layer in one lstm_bwd_stack call); the layers called one after the
-    other are timed beside it (with per-layer times)."""
+    other are timed beside it (with per-layer times).  schedules: the 9 : 1
+    (at least mix_cycles_min cycles) and 3 : 1 sparse : dense schedules;
+    forward: the forward pass; kernels: the per-kernel timing pass."""
     r = Runner(L, wl, sparsity, torch)
     res = {"runner": r}
     sp_ms, sp_wall, _ = r.timed([True], steps, warmup, stack=True)
@@ -384,23 +468,26 @@ def measure(L, torch, wl, sparsity, steps, warmup, sparse_only=False, kernels=Tr
                   flush=True)
         r.sparsity, r.stack_bufs = sparsity, {}
         res["sweep"] = pts
+    if schedules:
+        # the 9 sparse : 1 dense schedule (dense-after-sparse training phases)
+        cycles = max(mix_cycles_min, steps // 10)
+        mx_ms, _, _ = r.timed([True] * 9 + [False], cycles, 1, stack=True)
+        print("%s 9:1 schedule: %.4f ms/step over %d cycles" % (wl.name, mx_ms, cycles),
+              file=sys.stderr, flush=True)
+        res.update(mix_ms=mx_ms, mix_cycles=cycles)
+        # the 3 sparse : 1 dense schedule of dense-after-sparse training
+        c3 = max(1, steps // 4)
+        m3_ms, _, _ = r.timed([True] * 3 + [False], c3, 1, stack=True)
+        print("%s 3:1 schedule: %.4f ms/step" % (wl.name, m3_ms), file=sys.stderr, flush=True)
+        res.update(mix3_ms=m3_ms, mix3_cycles=c3)
+    if forward:
+        # forward pass (batched path, and one pass of the fused per-step path)
+        res["fwd_ms"] = r.forward_timed(steps, 1)
+        res["fwd_fused_ms"] = r.forward_timed(1, 0, batched=False)
+        print("%s forward: %.4f ms (fused per-step kernel %.4f ms)" % (
+            wl.name, res["fwd_ms"], res["fwd_fused_ms"]), file=sys.stderr, flush=True)
     if not kernels:
         return res
-    # the 9 sparse : 1 dense schedule (dense-after-sparse training phases)
-    cycles = max(1, steps // 10)
-    mx_ms, _, _ = r.timed([True] * 9 + [False], cycles, 1, stack=True)
-    print("%s 9:1 schedule: %.4f ms/step" % (wl.name, mx_ms), file=sys.stderr, flush=True)
-    res.update(mix_ms=mx_ms, mix_cycles=cycles)
-    # the 3 sparse : 1 dense schedule of dense-after-sparse training
-    c3 = max(1, steps // 4)
-    m3_ms, _, _ = r.timed([True] * 3 + [False], c3, 1, stack=True)
-    print("%s 3:1 schedule: %.4f ms/step" % (wl.name, m3_ms), file=sys.stderr, flush=True)
-    res.update(mix3_ms=m3_ms, mix3_cycles=c3)
-    # forward pass (batched path, and one pass of the fused per-step path)
-    res["fwd_ms"] = r.forward_timed(steps, 1)
-    res["fwd_fused_ms"] = r.forward_timed(1, 0, batched=False)
-    print("%s forward: %.4f ms (fused per-step kernel %.4f ms)" % (
-        wl.name, res["fwd_ms"], res["fwd_fused_ms"]), file=sys.stderr, flush=True)
     # per-kernel HIP-event timing pass (same number of sparse steps, the
     # layers called in turn so that kernels do not overlap); a short spin
     # kernel before and after marks the pass in kernel traces
@@ -596,7 +683,8 @@ def main():
                       % (my, mx, sparsity, nb), file=sys.stderr, flush=True)
                 continue
             fine.append((my, mx))
-    m = measure(L, torch, wl, sparsity, args.steps, args.warmup, args.sparse_only, fine=fine)
+    m = measure(L, torch, wl, sparsity, args.steps, args.warmup, args.sparse_only, fine=fine,
+                mix_cycles_min=2)
     if args.sparse_only:
         return
     sp_ms, dn_ms, kt = m["sp_ms"], m["dn_ms"], m["kt"]
@@ -609,27 +697,9 @@ def main():
         return tot
 
     dense_flops = flops_of(wl)
-    sp_kps = []
-    for l in range(wl.layers):
-        d = L.dims(wl.steps, wl.batch, wl.layer_input(l), wl.hidden, st)
-        sp_kps.append(L.kept_rows(d, sparsity, L.structure(wl.P, wl.R)))
+    roofs, sp_kps = roofline_all(L, wl, sparsity, kt, args.steps)
     exec_flops = flops_of(wl, [k / (4 * wl.hidden) for k in sp_kps])
-
-    kernels = {}
-    for name in KINDS + ("aux",):
-        ms, n = kt[name]
-        kernels[name] = {"total_ms_per_step": round(ms / args.steps, 5), "launches": n,
-                         "avg_us": round(ms / max(n, 1) * 1e3, 3)}
-    roofs = {}
-    for name in KINDS:
-        ms, n = kt[name]
-        # work of one step (all layers) times the timed steps, spread over
-        # the launches of this kind: the average launch's algorithmic work
-        works = [kernel_work(wl, l, sp_kps[l], es)[name] for l in range(wl.layers)]
-        per_launch = {k: sum(w[k] for w in works) * args.steps / max(n, 1)
-                      for k in ("bytes", "flops")}
-        roofs[name] = roofline_entry(name, per_launch, ms / 1e3 / max(n, 1), wl.dtype,
-                                     traffic_on_file(name, wl.name))
+    kernels = kernel_table(kt, args.steps)
     dominant = max(roofs, key=lambda k: kt[k][0])
 
     result = {
@@ -663,7 +733,8 @@ def main():
             "per_layer_ms": {"sparse": [round(v, 5) for v in m["sq_layer"]],
                              "dense": [round(v, 5) for v in m["sqd_layer"]]}},
         "mixed_9sparse_1dense": {"ms_per_step": round(m["mix_ms"], 5), "cycles": m["mix_cycles"],
-                                 "formula_ms": round((9 * sp_ms + dn_ms) / 10, 5)},
+                                 "formula_ms": round((9 * sp_ms + dn_ms) / 10, 5),
+                                 "speedup_vs_dense": round(dn_ms / m["mix_ms"], 4)},
         "mixed_3sparse_1dense": {"ms_per_step": round(m["mix3_ms"], 5),
                                  "cycles": m["mix3_cycles"],
                                  "speedup_vs_dense": round(dn_ms / m["mix3_ms"], 4)},
@@ -701,11 +772,7 @@ def main():
                     "turn"}
     for fm in m.get("fine", []):
         nb = -(-wl.batch // fm["My"])
-        fk = {}
-        for name in KINDS + ("aux",):
-            ms, n = fm["kt"][name]
-            fk[name] = {"total_ms_per_step": round(ms / args.steps, 5), "launches": n,
-                        "avg_us": round(ms / max(n, 1) * 1e3, 3)}
+        fk = kernel_table(fm["kt"], args.steps)
         entry = {"My": fm["My"], "Mx": fm["Mx"], "blocks_per_slice": nb,
                  "K": int(round(sparsity * nb)), "ms_per_step": round(fm["ms"], 5),
                  "speedup_vs_dense": round(dn_ms / fm["ms"], 4),
@@ -730,18 +797,38 @@ def main():
             if name == wl.name:
                 continue
             w2 = WORKLOADS[name]
-            m2 = measure(L, torch, w2, w2.sparsity, max(args.steps, 10), args.warmup,
-                         kernels=False)
-            also.append({"workload": name, "ms_per_step": round(m2["sp_ms"], 5),
-                         "dense_ms_per_step": round(m2["dn_ms"], 5),
-                         "speedup_vs_dense": round(m2["dn_ms"] / m2["sp_ms"], 4),
-                         "sequential_layers_ms_per_step": {"sparse": round(m2["sq_ms"], 5),
-                                                           "dense": round(m2["sqd_ms"], 5)},
-                         "value": round(flops_of(w2) / (m2["sp_ms"] / 1e3) / 1e12, 4),
-                         "unit": "TFLOP/s"})
+            k2 = max(args.steps, 10)
+            mixed = w2.dtype == "bf16"   # the bf16 workload is the 9 : 1 schedule's
+            m2 = measure(L, torch, w2, w2.sparsity, k2, args.warmup, schedules=mixed,
+                         forward=False, mix_cycles_min=2)
+            r2, _ = roofline_all(L, w2, w2.sparsity, m2["kt"], k2)
+            e2 = {"workload": name, "dtype": w2.dtype,
+                  "config": {"layers": w2.layers, "input_size": w2.input_size,
+                             "hidden": w2.hidden, "batch": w2.batch, "seq_len": w2.steps,
+                             "sparsity": w2.sparsity, "P": w2.P, "R": w2.R},
+                  "ms_per_step": round(m2["sp_ms"], 5),
+                  "dense_ms_per_step": round(m2["dn_ms"], 5),
+                  "speedup_vs_dense": round(m2["dn_ms"] / m2["sp_ms"], 4),
+                  "sequential_layers_ms_per_step": {"sparse": round(m2["sq_ms"], 5),
+                                                    "dense": round(m2["sqd_ms"], 5)},
+                  "value": round(flops_of(w2) / (m2["sp_ms"] / 1e3) / 1e12, 4),
+                  "unit": "TFLOP/s",
+                  "kernels": kernel_table(m2["kt"], k2),
+                  "roofline": r2[max(r2, key=lambda k: m2["kt"][k][0])],
+                  "roofline_all": r2}
+            if mixed:
+                e2["mixed_9sparse_1dense"] = {
+                    "ms_per_step": round(m2["mix_ms"], 5), "cycles": m2["mix_cycles"],
+                    "formula_ms": round((9 * m2["sp_ms"] + m2["dn_ms"]) / 10, 5),
+                    "speedup_vs_dense": round(m2["dn_ms"] / m2["mix_ms"], 4)}
+                e2["mixed_3sparse_1dense"] = {
+                    "ms_per_step": round(m2["mix3_ms"], 5), "cycles": m2["mix3_cycles"],
+                    "speedup_vs_dense": round(m2["dn_ms"] / m2["mix3_ms"], 4)}
             if "sweep" in m2:
-                also[-1]["sparsity_sweep"] = sweep_entries(m2)
+                e2["sparsity_sweep"] = sweep_entries(m2)
+            also.append(e2)
             del m2
+            torch.cuda.empty_cache()
         result["also"] = also
     print(json.dumps(result), flush=True)
 

@@ -80,6 +80,8 @@ def _load():
     lib.oracle_removed_in_region.argtypes = [L, i, i]
     lib.oracle_removed_in_region.restype = L
     lib.oracle_threads.restype = i
+    lib.oracle_set_threads.argtypes = [i]
+    lib.oracle_set_threads.restype = None
     lib.oracle_round_bf16.argtypes = [ctypes.c_double]
     lib.oracle_round_bf16.restype = ctypes.c_double
     lib.oracle_backward.argtypes = [i, i, i, i, P, P, P, P, P, P, P, P, i, i, i, i, P,
@@ -143,6 +145,11 @@ def forward(x, W, b=None, h0=None, c0=None, bf16=False):
 def threads() -> int:
     """Threads the oracle's parallel loops use."""
     return int(_load().oracle_threads())
+
+
+def set_threads(n: int) -> None:
+    """Threads of the parallel loops (results do not depend on it)."""
+    _load().oracle_set_threads(int(n))
 
 
 def kept_rows(rows: int, P: int, R: int, S: int) -> int:

@@ -78,6 +78,19 @@ int oracle_threads(void)
 #endif
 }
 
+/* Sets the number of threads of the parallel loops (n >= 1).  The loops only
+ * split independent output elements among threads, so no result depends on
+ * it; it serves timing on one core or all of them. */
+void oracle_set_threads(int n)
+{
+#ifdef _OPENMP
+    if (n >= 1)
+        omp_set_num_threads(n);
+#else
+    (void)n;
+#endif
+}
+
 /* Round to the nearest bfloat16 value (8 significant bits, fp32 exponent
  * range, subnormal spacing 2^-133), ties to even.  Used only when the
  * storage type of a configuration is bf16. */

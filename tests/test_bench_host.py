@@ -70,3 +70,25 @@ def test_sweep_entries_and_integer_removals():
     e = bench.sweep_entries({"dn_ms": 2.0, "sweep": [(0.0, 2.0), (0.5, 1.6), (0.75, 1.25)]})
     assert [p["sparsity"] for p in e] == [0.0, 0.5, 0.75]
     assert [p["speedup_vs_dense"] for p in e] == [1.0, 1.25, 1.6]
+
+
+def test_rocprof_duration_needs_matching_sources(tmp_path, monkeypatch):
+    monkeypatch.setattr(bench, "ROOT", str(tmp_path))
+    os.makedirs(tmp_path / "profiles")
+    f = tmp_path / "profiles" / "kernels_w.txt"
+    f.write_text("# summary\nsources_sha256_16: 0000\nrocprof_avg_us_data_grad_gemm: 40.0\n")
+    monkeypatch.setattr(bench, "sources_digest", lambda: "0000")
+    assert bench.rocprof_on_file("data_grad_gemm", "w") == 40.0
+    assert bench.rocprof_on_file("weight_grad_gemm", "w") is None
+    monkeypatch.setattr(bench, "sources_digest", lambda: "ffff")
+    assert bench.rocprof_on_file("data_grad_gemm", "w") is None
+    # both fractions: from the live event time and from the profiler's time
+    e = bench.roofline_entry("k", {"flops": 1e12, "bytes": 1e6}, 0.01, "f32", None, 8000.0)
+    assert e["frac"] == pytest.approx(100.0 / bench.PEAK["f32_tflops"], rel=1e-3)
+    assert e["frac_rocprof"] == pytest.approx(125.0 / bench.PEAK["f32_tflops"], rel=1e-3)
+
+
+def test_every_workload_is_measured():
+    """The default workload plus every other one under "also"."""
+    assert bench.DEFAULT_WORKLOAD in WORKLOADS
+    assert set(bench.ALSO_WORKLOADS) | {bench.DEFAULT_WORKLOAD} == set(WORKLOADS)

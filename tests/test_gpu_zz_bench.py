@@ -36,3 +36,7 @@ def test_bench_json_line():
     assert rl["frac"] == pytest.approx(rl["achieved"] / rl["peak"], rel=1e-2, abs=1e-4)
     cb = d["cpu_baseline"]
     assert cb["kind"] == "oracle" and cb["cores"] >= 1 and cb["value"] > 0 and cb["sample"]
+    one = cb["single_core"]
+    assert one["cores"] == 1 and one["value"] > 0 and one["sample"]
+    assert set(d["roofline_all"]) == {"gates_select_compact", "data_grad_gemm",
+                                      "weight_grad_gemm"}

@@ -387,3 +387,24 @@ def test_multi_layer_chain():
                          caches[0]["h"], outs[1]["dX"], S=0)
     assert np.array_equal(o1["dW"], outs[0]["dW"])
     assert math.isfinite(float(outs[0]["dX"].sum()))
+
+
+def test_thread_count_does_not_change_results():
+    """The parallel loops split independent outputs only: one thread and all
+    of them give the same bits (the CPU baseline times both)."""
+    d = make_layer(4, 20, 24, 40, seed=21, state=True)
+    n = oracle.threads()
+    outs = []
+    try:
+        for k in (1, max(2, n)):
+            oracle.set_threads(k)
+            assert oracle.threads() == k
+            g, c, h = oracle.forward(d["x"], d["W"], d["b"], d["h0"], d["c0"])
+            o = oracle.backward(d["x"], d["W"], g, c, h, d["dH_up"], d["dhT"], d["dcT"], P=4,
+                                R=8, S=4)
+            outs.append((g, o))
+    finally:
+        oracle.set_threads(n)
+    assert np.array_equal(outs[0][0], outs[1][0])
+    for k in ("dX", "dW", "db", "dh0", "dc0", "idx"):
+        assert np.array_equal(outs[0][1][k], outs[1][1][k]), k
