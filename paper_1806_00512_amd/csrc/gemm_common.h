@@ -75,6 +75,35 @@ struct Vec<bf16_t, false> {
 typedef __attribute__((address_space(3))) void lds_void_t;
 typedef __attribute__((address_space(1))) void glob_void_t;
 
+// Work-group barrier for LDS traffic: this wavefront's LDS operations are
+// complete, then all wavefronts meet.  Unlike __syncthreads() it does not
+// wait for outstanding global loads (whose release fence would drain a
+// multi-stage global -> LDS copy pipeline); the callers wait for the copies a
+// stage needs with explicit vmcnt waits before it.
+__device__ __forceinline__ void lds_barrier() {
+    asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
+}
+
+// One global -> LDS copy of 16 bytes per lane (global_load_lds_dwordx4): lane
+// j writes bytes [16 j, 16 j + 16) of the 1 KB LDS block at lds_dst (the
+// same block for the whole wavefront).  Issued as inline assembly so that the
+// compiler does not take it for an LDS store that every later LDS read has
+// to wait for (it would drain the copy pipeline before each stage's reads);
+// callers order it with explicit vmcnt waits and lds_barrier().  It sets m0,
+// which the kernels using it hold nothing else in (no other m0 use in their
+// code).
+__device__ __forceinline__ void dma16(const void *gsrc, lds_void_t *lds_dst) {
+    const int lds = __builtin_amdgcn_readfirstlane((int)(uintptr_t)lds_dst);
+    asm volatile("s_mov_b32 m0, %1\n\tglobal_load_lds_dwordx4 %0, off"
+                 :
+                 : "v"(gsrc), "s"(lds)
+                 : "memory", "m0");
+}
+
+// s_waitcnt immediate that waits until at most n vector-memory operations of
+// this wavefront are outstanding (the other counters left at their maxima).
+constexpr int vmcnt_imm(int n) { return (n & 0xf) | ((n >> 4) << 14) | (0x7 << 4) | (0xf << 8); }
+
 } // namespace
 
 } // namespace lstmss

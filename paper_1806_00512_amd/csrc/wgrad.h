@@ -87,6 +87,8 @@ constexpr bool wg_splitop() { return SPARSE && DMA && sizeof(TS) == 4 && TT == 1
 template <typename TS, bool SPARSE, bool DMA, int TT, int ATN>
 constexpr int wg_occupancy() { return wg_splitop<TS, SPARSE, DMA, TT, ATN>() && ATN <= 2 ? 3 : 2; }
 
+template <typename TS, bool SPARSE, bool DMA>
+constexpr int wg_stages() { return DMA && SPARSE && sizeof(TS) == 2 ? 3 : 2; }
 template <typename TS, bool SPARSE, int TT, int ATN, bool VEC, int BC, bool FN = false,
           bool DMA = false>
 __global__ __launch_bounds__(THREADS, (wg_occupancy<TS, SPARSE, DMA, TT, ATN>())) void wgrad_kernel(WgradArgs a) {
@@ -106,8 +108,9 @@ __global__ __launch_bounds__(THREADS, (wg_occupancy<TS, SPARSE, DMA, TT, ATN>())
     // two stages: the MFMAs read one while the next batch chunk is written to
     // the other (one barrier per chunk); the kept-slice table is kept per
     // step parity so that a step's routing never races the next step's table
-    __shared__ __align__(16) E sX[2][WG_FEAT][PITCH];
-    __shared__ __align__(16) E sG[2][WG_NG * GROWS][PITCH];
+    constexpr int NS = wg_stages<TS, SPARSE, DMA>();
+    __shared__ __align__(16) E sX[NS][WG_FEAT][PITCH];
+    __shared__ __align__(16) E sG[NS][WG_NG * GROWS][PITCH];
     __shared__ int sidx[2][WG_NG][64];
 
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
@@ -220,7 +223,7 @@ __global__ __launch_bounds__(THREADS, (wg_occupancy<TS, SPARSE, DMA, TT, ATN>())
                 const int k = wave + 4 * i;
                 const TS *src = k < 16 ? (disx[i] ? xt : ht) + dofs[i] : Gt + dofs[i];
                 E *dst = k < 16 ? &sX[lbuf][8 * k][0] : &sG[lbuf][8 * (k - 16)][0];
-                __builtin_amdgcn_global_load_lds((glob_void_t *)src, (lds_void_t *)dst, 16, 0, 0);
+                dma16(src, (lds_void_t *)dst);
             }
         } else {
 #pragma unroll
@@ -238,16 +241,24 @@ __global__ __launch_bounds__(THREADS, (wg_occupancy<TS, SPARSE, DMA, TT, ATN>())
                     rx[DMA ? 0 : set][i].zero();
             }
         }
+        // the step's kept-slice entries, from a clamped (always valid)
+        // position; entries past the group's count become -1 when stashed, so
+        // that nothing waits for this load before then
         if (SPARSE && b0 == 0 && tid < WG_NG * 64) {
             const int k = tid >> 6, e = tid & 63;
-            ridx[set] = e < lqc[k] ? a.idx[(long)t * a.kept + lq0[k] + e] : -1;
+            ridx[set] = a.idx[(long)t * a.kept + (lqc[k] > 0 ? lq0[k] + min(e, lqc[k] - 1) : 0)];
         }
         if (FN && b0 == 0 && tid < WG_NG * 64) {  // kept blocks of the group's slice
             const int k = tid >> 6, e = tid & 63;
-            const long sl = (long)blockIdx.x * WG_NG + k;
-            ridx[set] = (e < a.fkept && sl < G4 / 32)
-                            ? a.fidx[((long)t * (G4 / 32) + sl) * a.fkept + e] : -1;
+            const long sl = min((long)blockIdx.x * WG_NG + k, (long)G4 / 32 - 1);
+            ridx[set] = a.fidx[((long)t * (G4 / 32) + sl) * a.fkept + min(e, a.fkept - 1)];
         }
+    };
+    // whether entry e of group k's list at a step is a real entry
+    auto entry_ok = [&](int k, int e) {
+        if (SPARSE)
+            return e < lqc[k];
+        return e < a.fkept && (long)blockIdx.x * WG_NG + k < G4 / 32;
     };
     auto stash = [&](int it, int set, int buf) {
         const int tl = it / nbc;
@@ -270,7 +281,7 @@ __global__ __launch_bounds__(THREADS, (wg_occupancy<TS, SPARSE, DMA, TT, ATN>())
             }
         }
         if ((SPARSE || FN) && it - tl * nbc == 0 && tid < WG_NG * 64)
-            sidx[tl & 1][tid >> 6][tid & 63] = ridx[set];
+            sidx[tl & 1][tid >> 6][tid & 63] = entry_ok(tid >> 6, tid & 63) ? ridx[set] : -1;
     };
 
     f32x16 acc[WG_FT][ATN], tmp[WG_FT][TT];
@@ -307,15 +318,24 @@ __global__ __launch_bounds__(THREADS, (wg_occupancy<TS, SPARSE, DMA, TT, ATN>())
                         acc[ft][at][v] = src[f];
                 }
         }
+        // the stored sums are in registers before the loop (the compiler
+        // would otherwise keep a full wait for them inside it)
+        __builtin_amdgcn_s_waitcnt(0);
     }
 
     load(0, 0, 0);
-    if (!DMA && niters > 1)
+    if (niters > 1 && (!DMA || NS > 2))
         load(1, 1, 1);
     stash(0, 0, 0);
-    if (DMA)
-        __builtin_amdgcn_s_waitcnt(0);
-    __syncthreads();
+    if (DMA) {
+        if (NS > 2 && niters > 1)
+            __builtin_amdgcn_s_waitcnt(vmcnt_imm(NDW));
+        else
+            __builtin_amdgcn_s_waitcnt(0);
+        lds_barrier();
+    } else {
+        __syncthreads();
+    }
     constexpr int HALF = BC / 2;
     const int hb = (lane >> 5) * HALF;
     // iteration it computes from LDS buffer it & 1, loads chunk it + 2 into
@@ -377,7 +397,7 @@ __global__ __launch_bounds__(THREADS, (wg_occupancy<TS, SPARSE, DMA, TT, ATN>())
 
     auto iter = [&](int it, auto sc) {
         constexpr int S0 = decltype(sc)::value, S1 = 1 - S0;
-        const int buf = S0;
+        const int buf = NS == 2 ? S0 : it % NS;
         const int tl = it / nbc, bc = it - tl * nbc;
         if (!DMA && it + 2 < niters)
             load(it + 2, S0, 0);
@@ -385,8 +405,8 @@ __global__ __launch_bounds__(THREADS, (wg_occupancy<TS, SPARSE, DMA, TT, ATN>())
         // previous iteration), issued once this chunk's operands are in
         // registers (a deeper, three-buffer pipeline measured slower)
         auto issue_next = [&]() {
-            if (DMA && it + 1 < niters)
-                load(it + 1, S1, S1);
+            if (DMA && it + NS - 1 < niters)
+                load(it + NS - 1, NS == 2 ? S1 : S0, (it + NS - 1) % NS);
         };
         if constexpr (FN) {
             if (bc == 0) {
@@ -516,9 +536,15 @@ __global__ __launch_bounds__(THREADS, (wg_occupancy<TS, SPARSE, DMA, TT, ATN>())
         }
         if (it + 1 < niters)
             stash(it + 1, S1, S1);
-        if (DMA)  // the next chunk's lines are in LDS before anyone reads them
-            __builtin_amdgcn_s_waitcnt(0);
-        __syncthreads();
+        if (DMA) {
+            if (NS > 2 && it + 2 < niters)
+                __builtin_amdgcn_s_waitcnt(vmcnt_imm(NDW));
+            else
+                __builtin_amdgcn_s_waitcnt(0);
+            lds_barrier();
+        } else {
+            __syncthreads();
+        }
     };
     int it0 = 0;
     for (; it0 + 1 < niters; it0 += 2) {

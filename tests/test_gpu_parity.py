@@ -202,6 +202,9 @@ def adversarial_regions(H, B, P, R, seed, dtype):
     (512, 128, 4, 4, 0.5, "f32"),      # two regions per select work-group
     (2048, 128, 2, 16, 0.5, "f32"),
     (520, 128, 1, 64, 0.5, "f32"),     # 64-slice regions, partial last region of 32
+    (2056, 128, 4, 8, 0.5, "f32"),     # H not a multiple of P*R
+    (4104, 256, 4, 8, 0.5, "bf16"),
+    (1024, 256, 16, 4, 0.25, "f32"),   # four 64-column chunks, 64-row slices
 ])
 def test_select_split_path_bit_exact(L, H, B, P, R, sp, dtype):
     """Standalone selection on the two-kernel path the backward pass takes at
@@ -227,7 +230,8 @@ def test_select_split_path_bit_exact(L, H, B, P, R, sp, dtype):
 
 
 @pytest.mark.parametrize("T,B,I,H,dtype", [
-    (2, 256, 32, 256, "f32"), (2, 256, 24, 260, "f32"), (2, 256, 64, 256, "bf16")])
+    (2, 256, 32, 256, "f32"), (2, 256, 24, 260, "f32"), (2, 256, 64, 256, "bf16"),
+    (2, 128, 40, 1000, "f32")])
 def test_split_path_exact_ties_in_situ(L, T, B, I, H, dtype):
     """W = 0, no bias, zero initial state: the i, f and o rows of every gate
     gradient are exactly zero, so every region inside those gate blocks is
@@ -315,6 +319,22 @@ def test_layer_sparse_bf16(L, T, B, I, H):
 def test_layer_dense_bf16(L):
     d = make_layer(3, 24, 40, 64, seed=13, w_scale=0.2, dtype="bf16", state=True)
     check_layer(L, d, "bf16", 0.0, dense=True)
+
+
+@pytest.mark.parametrize("B,H,dtype", [(256, 256, "f32"), (128, 512, "bf16"), (200, 400, "f32")])
+def test_sparsity_zero_equals_dense_large(L, B, H, dtype):
+    """At shapes with H*B >= 65536 (two-kernel gate path) the sparse pass with
+    nothing removed gives the dense pass's bits."""
+    d = make_layer(3, B, 48, H, seed=B + H, w_scale=0.1, dtype=dtype, state=True)
+    x, W = gpu_tensor(d["x"], dtype), gpu_tensor(d["W"], dtype)
+    dH = gpu_tensor(d["dH_up"])
+    dhT, dcT = gpu_tensor(d["dhT"]), gpu_tensor(d["dcT"])
+    _, cache = L.fwd_cache(x, W, gpu_tensor(d["b"]), gpu_tensor(d["h0"]), gpu_tensor(d["c0"]))
+    a = L.bwd_dense(x, W, cache, dH, dhT, dcT)
+    b = L.bwd_structsparse(x, W, cache, dH, sparsity=0.0, P=4, R=8, dhT=dhT, dcT=dcT)
+    torch.cuda.synchronize()
+    for k in ("dX", "dW", "db", "dh0", "dc0"):
+        assert torch.equal(a[k], b[k]), k
 
 
 def test_sparsity_zero_equals_dense(L):
