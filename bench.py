@@ -46,7 +46,7 @@ KIND_KERNEL = {"gates_select_compact": "cell", "data_grad_gemm": "gemm1_kernel",
                "weight_grad_gemm": "wgrad_kernel"}
 KERNEL_SOURCES = tuple("paper_1806_00512_amd/csrc/" + f for f in (
     "gemm_common.h", "gemm1.hip", "wgrad.h", "wgrad_f32.hip", "wgrad_bf16.hip", "gemm.hip",
-    "cell.hip", "common.h", "kernels.h", "lstmss_api.cpp"))
+    "cell.hip", "select.h", "common.h", "kernels.h", "lstmss_api.cpp"))
 
 
 def parse():
@@ -77,21 +77,26 @@ def parse():
     return ap.parse_args()
 
 
-def kernel_work(wl, layer, Kp, es):
+def kernel_work(wl, layer, Kp, es, select_in_product=False):
     """Algorithmic bytes and flops of each backward kernel kind for one layer
     call (all T steps): what the method must read and write, not what the
-    implementation's staging (split-K partials, chunked updates) adds."""
+    implementation's staging (split-K partials, chunked updates) adds.  The
+    kept rows and the offset index are written by the gate kernels, or by
+    the dh product when the selection runs inside it (select_in_product)."""
     I, H, B, T = wl.layer_input(layer), wl.hidden, wl.batch, wl.steps
     K, HB = I + H, H * B
+    compact = Kp * B * es + Kp // wl.P * 4
     return {
         # per step: gates_t (4HB, storage type); c_t, c_{t-1}, dH_up[t],
         # dh_rec, dc_t read and dc_{t-1} written (fp32); kept rows and index
-        # written
-        "gates_select_compact": {"bytes": T * (4 * HB * es + 6 * HB * 4 + Kp * B * es
-                                               + Kp // wl.P * 4), "flops": 0},
+        # written (unless the dh product writes them)
+        "gates_select_compact": {"bytes": T * (4 * HB * es + 6 * HB * 4
+                                               + (0 if select_in_product else compact)),
+                                 "flops": 0},
         # per step: W_c (K' x (I+H)), dG_c (K' x B) read, [dx; dh] ((I+H) x B,
-        # fp32) written
-        "data_grad_gemm": {"bytes": T * (Kp * K * es + Kp * B * es + K * B * 4),
+        # fp32) written; kept rows and index written when it selects
+        "data_grad_gemm": {"bytes": T * (Kp * K * es + Kp * B * es + K * B * 4
+                                         + (compact if select_in_product else 0)),
                            "flops": T * 2 * K * B * Kp},
         # every step's dG_c and [x; h] read once, dW (4H x (I+H), fp32)
         # written once
@@ -185,18 +190,21 @@ def roofline_all(L, wl, sparsity, kt, steps):
     (kt) of `steps` sparse steps of workload wl."""
     st_dt = "bf16" if wl.dtype == "bf16" else "f32"
     es = 2 if wl.dtype == "bf16" else 4
-    kps = [L.kept_rows(L.dims(wl.steps, wl.batch, wl.layer_input(l), wl.hidden, st_dt), sparsity,
-                       L.structure(wl.P, wl.R)) for l in range(wl.layers)]
+    dims = [L.dims(wl.steps, wl.batch, wl.layer_input(l), wl.hidden, st_dt)
+            for l in range(wl.layers)]
+    kps = [L.kept_rows(d, sparsity, L.structure(wl.P, wl.R)) for d in dims]
+    sel = [L.bwd_info(d, sparsity, L.structure(wl.P, wl.R))["select_in_product"] for d in dims]
     roofs = {}
     for name in KINDS:
         ms, n = kt[name]
         # work of one step (all layers) times the timed steps, spread over
         # the launches of this kind: the average launch's algorithmic work
-        works = [kernel_work(wl, l, kps[l], es)[name] for l in range(wl.layers)]
+        works = [kernel_work(wl, l, kps[l], es, sel[l])[name] for l in range(wl.layers)]
         per_launch = {k: sum(w[k] for w in works) * steps / max(n, 1) for k in ("bytes", "flops")}
         roofs[name] = roofline_entry(name, per_launch, ms / 1e3 / max(n, 1), wl.dtype,
                                      traffic_on_file(name, wl.name),
                                      rocprof_on_file(name, wl.name))
+        roofs[name]["select_in_product"] = any(sel)
     return roofs, kps
 
 

@@ -101,6 +101,19 @@ int64_t lstmss_cache_bytes(const lstmss_dims *d);
  * for FINE always 4H (removed blocks are zero in place).  <0 on error. */
 int64_t lstmss_kept_rows(const lstmss_dims *d, float sparsity, const lstmss_structure *s);
 
+/* How lstm_bwd_structsparse runs the gate path of a call with these
+ * arguments under the current options, for a 256-byte aligned weight matrix
+ * and workspace: *flags gets LSTMSS_INFO_SPLIT_GATES when the gate gradient
+ * and the selection of section 3 are computed by an element kernel and a
+ * selection step (H * B >= 65536), and LSTMSS_INFO_SELECT_IN_PRODUCT when
+ * that selection and the compaction run inside the per-step dh product
+ * (LSTMSS_OPT_GEMM_SELECT) instead of a kernel of their own.  Results are
+ * the same bits either way; this is for profiling and accounting.  0 or a
+ * negative error code (no GPU work). */
+enum { LSTMSS_INFO_SPLIT_GATES = 1, LSTMSS_INFO_SELECT_IN_PRODUCT = 2 };
+int32_t lstmss_bwd_info(const lstmss_dims *d, float sparsity, const lstmss_structure *s,
+                        int32_t *flags);
+
 /* Entries of the per-step index written by the selection: COARSE K'/P kept
  * slice indices; FINE (4H/Mx) x (nb - K) kept block indices.  <0 on error. */
 int64_t lstmss_index_entries(const lstmss_dims *d, float sparsity, const lstmss_structure *s);
@@ -329,6 +342,15 @@ int32_t lstmss_mse_grad(const lstmss_dims *d, const void *h, const float *y, flo
  *                      bf16 only with B > 64; the operands 16-byte aligned);
  *                      0 stages them through registers (same bits; for
  *                      checking and timing).
+ *   LSTMSS_OPT_GEMM_SELECT  1 (default): on the two-kernel gate path of
+ *                      the coarse structure (H * B >= 65536) with DMA data-
+ *                      gradient stages, the per-step dh product ranks the
+ *                      slices itself (splits of whole regions), reads both
+ *                      operands through the kept rows of the element
+ *                      kernel's staging matrix and writes the compacted
+ *                      matrix and offset index, in place of a separate
+ *                      selection launch; 0 always launches the selection
+ *                      kernel (same bits; for checking and timing).
  * Changing an option drops the recorded graphs.  Not for use while calls
  * are being enqueued from other threads. */
 enum {
@@ -336,7 +358,8 @@ enum {
     LSTMSS_OPT_SIDE_STREAM = 1,
     LSTMSS_OPT_STACK_DX_STEPS = 2,
     LSTMSS_OPT_FINE_SKIP = 3,
-    LSTMSS_OPT_GEMM_DMA = 4
+    LSTMSS_OPT_GEMM_DMA = 4,
+    LSTMSS_OPT_GEMM_SELECT = 5
 };
 int32_t lstmss_set_option(int32_t option, int32_t value);
 

@@ -7,6 +7,7 @@
 // data flow is the one of Fig. 1 for the standard LSTM cell.
 #include "common.h"
 #include "kernels.h"
+#include "select.h"
 
 namespace lstmss {
 
@@ -41,11 +42,6 @@ __device__ __forceinline__ float gate_grad(const CellArgs &a, const TS *gates, i
     if (g == 0)
         return dcv * gg * i * (1.f - i);
     return dcv * i * (1.f - gg * gg);
-}
-
-// True if slice i (score si) ranks above slice j (score sj) in a region.
-__device__ __forceinline__ bool outranks(uint64_t ki, long i, uint64_t kj, long j) {
-    return ki > kj || (ki == kj && i < j);
 }
 
 template <typename TS, int MODE>
@@ -509,7 +505,6 @@ __global__ __launch_bounds__(EK_WAVES * 64) void cell_elem_kernel(CellArgs a) {
 // slice against the R slices of its region, and copy the kept rows.
 template <typename TS>
 __global__ __launch_bounds__(64) void cell_select_kernel2(CellArgs a) {
-    __shared__ double srowsq[256];
     __shared__ int sslot[64];
     __shared__ int sinv[64];  // kept slice (local index) of each local slot
     __shared__ int s_nkept;
@@ -521,56 +516,22 @@ __global__ __launch_bounds__(64) void cell_select_kernel2(CellArgs a) {
     const int nsl = (int)min(spw, a.nslices - j0);
     const long row0 = j0 * P;
     const int nrows = nsl * P;
-    for (int lr = lane; lr < nrows; lr += 64) {
-        const double *q = a.chunk_sq + (row0 + lr) * nch;
-        double sq = q[0];
-        for (int cc = 1; cc < nch; ++cc)
-            sq = sq + q[cc];
-        srowsq[lr] = sq;
-    }
-    __syncthreads();
+    const SliceSel sel = select_slices(a.chunk_sq, nch, j0, nsl, P, R, a.S, a.nslices);
     const int j = lane;
-    const bool valid = j < nsl;
-    double sc = 0.0;
-    if (valid) {
-        sc = srowsq[j * P];
-        for (int p = 1; p < P; ++p)
-            sc = sc + srowsq[j * P + p];
-        if (a.scores)
-            a.scores[j0 + j] = sc;
-    }
-    const uint64_t kj = score_key(sc);
-    const long gj = j0 + j;
-    // regions start at multiples of R and j0 is one, so a region's slices
-    // are the lanes [ls, ls + rlen) of this wavefront
-    const int ls = valid ? (int)((gj / R) * R - j0) : 0;
-    const int rlen = valid ? (int)min((long)R, a.nslices - (j0 + ls)) : 0;
-    const int nkeep = rlen - (a.S * rlen) / R;
-    int beaten = 0;
-    for (int i = 0; i < R; ++i) {
-        const int src = (ls + i) & 63;
-        const uint64_t ki = (uint64_t)__shfl((long long)kj, src, 64);
-        if (i < rlen && src != j && outranks(ki, src, kj, j))
-            ++beaten;
-    }
-    const bool keep = valid && beaten < nkeep;
-    const uint64_t ball = __ballot(keep);
-    const uint64_t below = ((j ? (~0ull >> (64 - j)) : 0ull)) & ~((ls ? (~0ull >> (64 - ls)) : 0ull));
-    const int pos = __popcll(ball & below);
-    int slot = -1;
+    if (j < nsl && a.scores)
+        a.scores[j0 + j] = sel.score;
     // the group's kept slices fill a contiguous run of slots from slot0
     // (regions start at multiples of R, each region's slots at R - S times
     // its number)
     const long slot0 = (j0 / R) * (R - a.S);
-    if (keep) {
-        slot = (int)((gj / R) * (R - a.S) + pos);
-        a.idx[slot] = (int32_t)gj;
-        sinv[slot - slot0] = j;
+    if (sel.slot >= 0) {
+        a.idx[sel.slot] = (int32_t)(j0 + j);
+        sinv[sel.slot - slot0] = j;
     }
-    if (valid)
-        sslot[j] = slot;
+    if (j < nsl)
+        sslot[j] = sel.slot;
     if (lane == 0)
-        s_nkept = __popcll(ball);
+        s_nkept = sel.nkept;
     __syncthreads();
     // copy the kept rows into their contiguous slots: lanes over the
     // destination's 16-byte vectors, eight loads in flight before their
@@ -873,7 +834,7 @@ static hipError_t launch_cell_split(CellArgs a, int mode, bool bf16, hipStream_t
     else
         launch_elem<float>(a, mode, ge, s);
     hipError_t e = hipGetLastError();
-    if (e != hipSuccess || mode == CELL_DENSE)
+    if (e != hipSuccess || mode == CELL_DENSE || (mode == CELL_SPARSE && a.defer_select))
         return e;
     const int grid = (int)ceil_div(a.nslices, (long)a.regions_per_wg * a.R);
     if (bf16)

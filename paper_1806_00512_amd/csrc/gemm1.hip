@@ -12,6 +12,7 @@
 // through LDS.  fp32 uses v_mfma_f32_32x32x2f32; bf16 uses
 // v_mfma_f32_32x32x16_bf16 with fp32 accumulation.
 #include "gemm_common.h"
+#include "select.h"
 
 namespace lstmss {
 
@@ -84,10 +85,20 @@ typedef __attribute__((__vector_size__(4 * sizeof(__bf16)))) __bf16 g1_bf16x4;
 typedef __attribute__((address_space(3))) g1_bf16x4 g1_lds_bf16x4;
 typedef short g1_s16x4 __attribute__((ext_vector_type(4)));
 
+// SEL: the coarse selection of one step inside its dh product.  Every
+// work-group ranks the slices of its split's regions (whole regions: the
+// split length is a multiple of P (R - S) kept rows) from the element
+// kernel's chunk sums of squares, with the same wavefront routines as the
+// select kernel, and gathers the rows of both operands through the result:
+// W rows and the staging matrix's rows (Gc).  The split's work-groups share
+// out the copy of its kept rows to the compacted matrix (after their
+// product, from the staging matrix); those of tile (0, 0) also write the
+// split's slots of the offset index.
 template <typename TS, int TM, int TN, bool GATHER, bool VEC, bool ROWA = false, int NW = 4,
-          bool FN = false, bool DMA = false>
+          bool FN = false, bool DMA = false, bool SEL = false>
 __global__ __launch_bounds__(NW * 64) void gemm1_kernel(Gemm1Args a) {
     static_assert(!(ROWA && GATHER), "the forward products read every row");
+    static_assert(!SEL || (DMA && GATHER), "selection in the product: gathered DMA stages");
     static_assert(!(FN && (GATHER || ROWA)), "the fine fast path reads every row");
     static_assert(!DMA || (!FN && VEC &&
                            (sizeof(TS) == 4 ? NW == 4 : (NW == 8 && TM == 128 && TN == 128))),
@@ -164,8 +175,82 @@ __global__ __launch_bounds__(NW * 64) void gemm1_kernel(Gemm1Args a) {
             srow[i] = GATHER ? idx[k / a.P] * a.P + k % a.P : k;
         }
     };
-    if (!ROWA && !FN)
+    __shared__ __align__(16) E As[2][DMA ? 1 : TM][LDK];
+    __shared__ __align__(16) E Bs[2][DMA ? 1 : TN][LDK];
+    __shared__ __align__(16) E Ad[2][DMA ? TK * TM : 1];  // DMA: [k][m]
+    __shared__ __align__(16) E Bd[2][DMA ? TK * TN : 1];  // DMA: [k][n]
+    if constexpr (SEL) {
+        const int P = a.P, R = a.sel_R, S = a.sel_S, kr = P * (R - S), nch = a.sel_nch;
+        const long s_lo = (long)(kb / kr) * R;
+        const long s_hi = ke0 == a.Kp ? a.sel_nslices : min(a.sel_nslices, (long)(ke0 / kr) * R);
+        const int gs = (64 / R) * R;  // whole regions per wavefront
+        const int ng = (int)((s_hi - s_lo + gs - 1) / gs);
+        const bool write_idx = blockIdx.x == 0 && blockIdx.y == 0;
+        // A group's chunk sums (L per slice) are one contiguous run: a
+        // wavefront reads it coalesced into its own region of the stage
+        // buffers (free until the first stage), lane j's slice at row j,
+        // its entries permuted by j when L is a power of two so that the
+        // lanes' reads of one entry fall on distinct banks; then each lane
+        // folds its slice as select_slices does.  With fewer than 16 entries
+        // per slice (measured faster so), or without room for a region, the
+        // lanes read their slices directly.
+        const int L = P * nch, rsb = 64 * L * (int)sizeof(double);
+        const int na = (int)(sizeof(Ad) / rsb);
+        const int nact = L < 16 ? 0 : min(NW, na + (int)(sizeof(Bd) / rsb));
+        const bool pow2 = (L & (L - 1)) == 0;
+        const int lg = __builtin_ctz(L);
+        auto pos = [&](int j, int e) { return j * L + (pow2 ? e ^ (j & (L - 1)) : e); };
+        const int gstep = nact > 0 ? nact : NW;
+        for (int g = wave; wave < gstep && g < ng; g += gstep) {
+            const long j0 = s_lo + (long)g * gs;
+            const int nsl = (int)min((long)gs, s_hi - j0);
+            SliceSel sl;
+            if (nact > 0) {
+                double *sq = (double *)(wave < na ? (char *)&Ad[0][0] + wave * rsb
+                                                  : (char *)&Bd[0][0] + (wave - na) * rsb);
+                const double *src = a.sel_sq + j0 * P * nch;
+                const int n = nsl * L;
+                asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");  // the previous group's reads
+                for (int x0 = 0; x0 < n; x0 += 8 * 64) {
+                    double v[8];
+#pragma unroll
+                    for (int u = 0; u < 8; ++u) {
+                        const int x = x0 + u * 64 + lane;
+                        v[u] = x < n ? src[x] : 0.0;
+                    }
+#pragma unroll
+                    for (int u = 0; u < 8; ++u) {
+                        const int x = x0 + u * 64 + lane;
+                        const int j = pow2 ? x >> lg : x / L;
+                        if (x < n)
+                            sq[pos(j, x - j * L)] = v[u];
+                    }
+                }
+                asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");  // the wavefront's writes landed
+                double scv = 0.0;
+                if (lane < nsl) {
+                    for (int p = 0; p < P; ++p) {
+                        double rs = sq[pos(lane, p * nch)];
+                        for (int c = 1; c < nch; ++c)
+                            rs = rs + sq[pos(lane, p * nch + c)];
+                        scv = p == 0 ? rs : scv + rs;
+                    }
+                }
+                sl = rank_slices(scv, j0, nsl, R, S, a.sel_nslices);
+            } else {
+                sl = select_slices(a.sel_sq, nch, j0, nsl, P, R, S, a.sel_nslices);
+            }
+            if (sl.slot >= 0) {
+                const int j = (int)(j0 + lane);
+                for (int p = 0; p < P; ++p)
+                    srow[sl.slot * P + p - kb] = j * P + p;
+                if (write_idx)
+                    a.sel_idx[sl.slot] = j;
+            }
+        }
+    } else if (!ROWA && !FN) {
         fill_rows(sc);
+    }
 
     auto qa = [&](int i) { return tid + i * THREADS; };
     auto qb = [&](int i) { return SPLIT ? tid - NA : tid + i * THREADS; };
@@ -220,10 +305,6 @@ __global__ __launch_bounds__(NW * 64) void gemm1_kernel(Gemm1Args a) {
         }
     };
 
-    __shared__ __align__(16) E As[2][DMA ? 1 : TM][LDK];
-    __shared__ __align__(16) E Bs[2][DMA ? 1 : TN][LDK];
-    __shared__ __align__(16) E Ad[2][DMA ? TK * TM : 1];  // DMA: [k][m]
-    __shared__ __align__(16) E Bd[2][DMA ? TK * TN : 1];  // DMA: [k][n]
     // DMA copy of the stage starting at k0 into buffer b: instruction q fills
     // bytes [1024 q, 1024 q + 1024) of Ad (q < NIA) or of Bd
     constexpr int PEL = 16 / (int)sizeof(E), IEL = 1024 / (int)sizeof(E);  // elements per piece / instruction
@@ -250,7 +331,7 @@ __global__ __launch_bounds__(NW * 64) void gemm1_kernel(Gemm1Args a) {
                 src = W + (long)srow[k0 + kl - sc] * ldw + m;
             } else {
                 const int n = min(n0 + col, N - PEL);
-                src = G + (long)(k0 + kl) * N + n;
+                src = G + (long)(SEL ? srow[k0 + kl - sc] : k0 + kl) * N + n;
             }
             E *dst = isa ? &Ad[b][q * IEL] : &Bd[b][(q - NIA) * IEL];
             __builtin_amdgcn_global_load_lds((glob_void_t *)src, (lds_void_t *)dst, 16, 0, 0);
@@ -331,7 +412,7 @@ __global__ __launch_bounds__(NW * 64) void gemm1_kernel(Gemm1Args a) {
     for (int k0 = kb; k0 < ke; k0 += TK) {
         const bool next = k0 + TK < ke;
         if (next) {
-            if (!ROWA && !FN && k0 + TK == sc + GEMM1_KC_MAX) {  // next super-chunk of rows
+            if (!ROWA && !FN && !SEL && k0 + TK == sc + GEMM1_KC_MAX) {  // next super-chunk of rows
                 sc = k0 + TK;
                 fill_rows(sc);
                 __syncthreads();
@@ -499,6 +580,20 @@ __global__ __launch_bounds__(NW * 64) void gemm1_kernel(Gemm1Args a) {
                     out[(long)(m - a.out_row0) * N + n] = acc[i][j][v];
             }
         }
+    if constexpr (SEL) {
+        // compacted rows: the split's rows are shared out over its m-tiles,
+        // each work-group copying its share (its columns) from the staging
+        // matrix, last, so that no stage waits for these stores
+        constexpr int PPR = TN / PEL;  // 16-byte pieces per tile row
+        const int nr = ke0 - kb, nmt = (int)gridDim.x;
+        const int r0 = (int)((long)nr * blockIdx.x / nmt), r1 = (int)((long)nr * (blockIdx.x + 1) / nmt);
+        TS *gc = (TS *)a.sel_gc;
+        for (int e = tid; e < (r1 - r0) * PPR; e += THREADS) {
+            const int k = kb + r0 + e / PPR, n = n0 + (e % PPR) * PEL;
+            if (n < N)
+                *(uint4 *)(gc + (long)k * N + n) = *(const uint4 *)(G + (long)srow[k - sc] * N + n);
+        }
+    }
 }
 
 } // namespace
@@ -536,6 +631,13 @@ template <typename TS, int TM, int TN, bool GA, bool VE, bool ROWA = false>
 static void launch_g1(dim3 grid, const Gemm1Args &a, bool w8, hipStream_t s, bool dma = false) {
     if constexpr (sizeof(TS) == 4 && VE && TN != 32) {
         if (dma && !w8) {
+            if constexpr (GA && !ROWA) {
+                if (a.sel_sq) {
+                    hipLaunchKernelGGL((gemm1_kernel<TS, TM, TN, true, true, false, 4, false, true, true>),
+                                       grid, dim3(THREADS), 0, s, a);
+                    return;
+                }
+            }
             hipLaunchKernelGGL((gemm1_kernel<TS, TM, TN, GA, true, ROWA, 4, false, true>), grid,
                                dim3(THREADS), 0, s, a);
             return;
@@ -543,6 +645,13 @@ static void launch_g1(dim3 grid, const Gemm1Args &a, bool w8, hipStream_t s, boo
     }
     if constexpr (sizeof(TS) == 2 && VE && TM == 128 && TN == 128) {
         if (dma && w8) {
+            if constexpr (GA && !ROWA) {
+                if (a.sel_sq) {
+                    hipLaunchKernelGGL((gemm1_kernel<TS, 128, 128, true, true, false, 8, false, true, true>),
+                                       grid, dim3(512), 0, s, a);
+                    return;
+                }
+            }
             hipLaunchKernelGGL((gemm1_kernel<TS, 128, 128, GA, true, ROWA, 8, false, true>), grid,
                                dim3(512), 0, s, a);
             return;
@@ -573,13 +682,20 @@ static bool use_w8(const Gemm1Args &a, bool bf16, int TM, int TN) {
     return a.waves == 8 || (a.waves == 0 && bf16);
 }
 
-hipError_t launch_gemm1(Gemm1Args a, bool bf16, hipStream_t s) {
+// Launch configuration of a data-gradient product (sets a.m_lo).
+struct G1Plan {
+    int TM, TN;
+    bool vec, w8, dma;
+    dim3 grid;
+};
+
+static hipError_t g1_plan(Gemm1Args &a, bool bf16, G1Plan *pl) {
     if (a.k_chunk % GEMM1_TK != 0 || a.splitk < 1 || a.steps < 1)
         return hipErrorInvalidValue;
     // fine fast path: no gather, whole 32-row slices, 32-column blocks, the
     // slice masks of one split fit the work-group's table
-    if (a.fidx && (a.idx || a.P != 32 || a.fkept < 1 || a.fkept > 64 || a.N % 32 != 0 ||
-                   ceil_div(a.k_chunk, 32) > FINE_MAX_SLICES))
+    if (a.fidx && (a.idx || a.sel_sq || a.P != 32 || a.fkept < 1 || a.fkept > 64 ||
+                   a.N % 32 != 0 || ceil_div(a.k_chunk, 32) > FINE_MAX_SLICES))
         return hipErrorInvalidValue;
     // 16-byte vector loads need 16-byte aligned rows; the tile origin is
     // rounded down to the vector width and rows below m_begin are not stored
@@ -606,12 +722,41 @@ hipError_t launch_gemm1(Gemm1Args a, bool bf16, hipStream_t s) {
     }
     if (!((TN == 32 && TM == 128) || ((TN == 64 || TN == 128) && (TM == 64 || TM == 128))))
         return hipErrorInvalidValue;
-    dim3 grid((unsigned)ceil_div(a.M - a.m_lo, TM), (unsigned)ceil_div(a.N, TN), (unsigned)z);
-    const bool gather = a.idx != nullptr;
     if (a.waves != 0 && a.waves != 4 && !(a.waves == 8 && TM == 128 && TN == 128))
         return hipErrorInvalidValue;
-    const bool w8 = use_w8(a, bf16, TM, TN);
-    const bool dma = dma_shape && (bf16 ? (w8 && TM == 128 && TN == 128) : TN != 32);
+    pl->TM = TM;
+    pl->TN = TN;
+    pl->vec = vec;
+    pl->w8 = use_w8(a, bf16, TM, TN);
+    pl->dma = dma_shape && (bf16 ? (pl->w8 && TM == 128 && TN == 128) : TN != 32);
+    pl->grid = dim3((unsigned)ceil_div(a.M - a.m_lo, TM), (unsigned)ceil_div(a.N, TN), (unsigned)z);
+    // selection inside the product: one step on DMA stages, splits of whole
+    // regions whose gathered rows fit one table
+    if (a.sel_sq) {
+        const int R = a.sel_R, S = a.sel_S;
+        if (a.idx || !pl->dma || a.steps != 1 || R < 1 || R > 64 || S < 1 || S >= R || a.P < 1 ||
+            a.k_chunk > GEMM1_KC_MAX || a.k_chunk % ((long)a.P * (R - S)) != 0 ||
+            a.sel_nch < 1 || !a.sel_gc || !a.sel_idx ||
+            (((uintptr_t)a.sel_gc) & 15) != 0)
+            return hipErrorInvalidValue;
+    }
+    return hipSuccess;
+}
+
+bool gemm1_select_ok(Gemm1Args a, bool bf16) {
+    G1Plan pl;
+    return a.sel_sq && g1_plan(a, bf16, &pl) == hipSuccess;
+}
+
+hipError_t launch_gemm1(Gemm1Args a, bool bf16, hipStream_t s) {
+    G1Plan pl;
+    const hipError_t e = g1_plan(a, bf16, &pl);
+    if (e != hipSuccess)
+        return e;
+    const int TM = pl.TM, TN = pl.TN;
+    const bool vec = pl.vec, w8 = pl.w8, dma = pl.dma;
+    const dim3 grid = pl.grid;
+    const bool gather = a.idx != nullptr || a.sel_sq != nullptr;
 #define LSTMSS_G1(TS, TMV, TNV, GA, VE) launch_g1<TS, TMV, TNV, GA, VE>(grid, a, w8, s, dma)
 #define LSTMSS_G1V(TS, TMV, TNV, GA) do { if (vec) LSTMSS_G1(TS, TMV, TNV, GA, true); else LSTMSS_G1(TS, TMV, TNV, GA, false); } while (0)
 #define LSTMSS_G1T(TS, GA) do { \

@@ -34,6 +34,7 @@ struct CellArgs {
     float *db;             // [4H] accumulated over kept rows, or NULL
     void *dbg;             // [4H][B] or NULL
     double *scores;        // [4H/P] or NULL
+    int defer_select;      // split path: element kernel only, the dh product selects
     // split variant (large shapes): staging matrix and per-(row, chunk) sums
     void *stage;           // [4H][B] gate gradient before selection (sparse)
     double *chunk_sq;      // [4H][ceil(B/64)] fp64 chunk sums of squares
@@ -76,6 +77,16 @@ struct Gemm1Args {
     long fidx_step;
     int dma;               // 1: fp32 stages go global -> LDS directly where the shape allows
                            // (same bits as the register-staged loads of 0)
+    // coarse selection inside the product (one step, DMA stages, idx NULL):
+    // Gc is then the staging matrix [4H][N] of the step; the product ranks
+    // the slices of its splits' regions from sel_sq, gathers both operands
+    // through the kept rows and writes the compacted matrix sel_gc
+    // [Kp][N] and the offset index sel_idx [kept].  NULL otherwise.
+    const double *sel_sq;  // [4H][sel_nch] chunk sums of squares
+    int sel_nch, sel_R, sel_S;
+    long sel_nslices;
+    void *sel_gc;
+    int32_t *sel_idx;
 };
 
 // Weight gradient dW[rows] += dG_c [x_t; h_{t-1}]^T (rows scattered by idx).
@@ -160,6 +171,8 @@ hipError_t launch_bias_grad(float *db, const float *chunk_rs, int nch, long G, i
                             const int32_t *idx, int kept, int P, int R, int S, bool accumulate,
                             hipStream_t s);
 hipError_t launch_gemm1(Gemm1Args a, bool bf16, hipStream_t s);
+// True when launch_gemm1 accepts a (selection inside the product, sel_sq set).
+bool gemm1_select_ok(Gemm1Args a, bool bf16);
 hipError_t launch_gemm2(const Gemm2Args &a, bool bf16, hipStream_t s);
 // Forward products part[z][m][n] = sum over k in split z of
 // W[m][kcol0 + k] G[k][n] (rows m in [0, M), contraction length Kp).

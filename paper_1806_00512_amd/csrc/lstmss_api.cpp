@@ -164,6 +164,9 @@ constexpr int kStackDxSteps = 12;
 // default) or run them on the zeros (0); results are the same bits
 bool g_fine_skip = true;
 bool g_gemm_dma = true;
+// coarse selection inside the dh product where the shape allows (1) or in
+// its own kernel (0); same bits
+bool g_gemm_select = true;
 
 hipError_t stack_res(StackRes **out) {
     int dev = 0;
@@ -422,6 +425,44 @@ struct EnqCtx {
     bool auto_side = true;
 };
 
+// Whether the coarse structure's gate path splits into the element kernel
+// and a selection (large shapes), and whether that selection then runs
+// inside the per-step dh product (LSTMSS_OPT_GEMM_SELECT, DMA stages, splits
+// of whole regions).  W, ws: the call's weight and workspace pointers (their
+// alignment decides the DMA stages).
+struct GatePath {
+    bool split, select_in_product;
+};
+
+GatePath gate_path(const lstmss_dims *d, const Plan &p, bool dense, const void *W, const void *ws) {
+    const bool sparse = !dense, fine = sparse && p.fine, gsparse = sparse && !fine;
+    CellArgs probe{};
+    probe.B = d->B; probe.H = d->H; probe.P = sparse ? p.P : 1; probe.R = sparse ? p.R : 1;
+    probe.regions_per_wg = sparse ? std::max(1, 32 / (p.R * p.P)) : 32;
+    GatePath g;
+    g.split = !fine && cell_split_ok(probe, sparse ? CELL_SPARSE : CELL_DENSE);
+    g.select_in_product = false;
+    if (!g.split || !gsparse || !g_gemm_select)
+        return g;
+    const WsLayout L = ws_layout(d, p);
+    const long K = (long)d->I + d->H;
+    const char *wb = (const char *)ws;
+    Gemm1Args a{};
+    a.W = W; a.ldw = K; a.P = p.P; a.Kp = p.Kp; a.M = (int)K; a.m_begin = d->I; a.N = d->B;
+    a.out_row0 = d->I; a.splitk = L.splitk; a.k_chunk = L.k_chunk; a.steps = 1;
+    a.dma = g_gemm_dma ? 1 : 0;
+    a.Gc = wb + L.stage;
+    a.sel_sq = (const double *)(wb + L.chunk_sq);
+    a.sel_nch = (int)ceil_div(d->B, 64); a.sel_R = p.R; a.sel_S = p.S; a.sel_nslices = p.nslices;
+    a.sel_gc = const_cast<char *>(wb + L.dGc);
+    a.sel_idx = (int32_t *)const_cast<char *>(wb + L.idx);
+    // every step's compacted matrix starts Kp * B elements after the last
+    if (((size_t)p.Kp * d->B * elem_bytes(d->dtype)) % 16 != 0)
+        return g;
+    g.select_in_product = gemm1_select_ok(a, d->dtype == LSTMSS_BF16);
+    return g;
+}
+
 // Enqueue one backward call on main stream st, with ctx (locked by the
 // caller) for the off-critical-path work.  Arguments already checked.
 int32_t backward_enqueue(const lstmss_dims *d, bool dense, const Plan &p, const void *x,
@@ -474,10 +515,8 @@ int32_t backward_enqueue(const lstmss_dims *d, bool dense, const Plan &p, const 
         HIP_TRY(timed(LSTMSS_KERNEL_AUX, st, [&] { return launch_fill(dW, G * K, 0.f, st); }));
     // gate kernels: the split path (large shapes) leaves the bias gradient to
     // one kernel after the time loop; the single-kernel paths accumulate it
-    CellArgs probe{};
-    probe.B = B; probe.H = H; probe.P = sparse ? p.P : 1; probe.R = sparse ? p.R : 1;
-    probe.regions_per_wg = sparse ? std::max(1, 32 / (p.R * p.P)) : 32;
-    const bool split = !fine && cell_split_ok(probe, sparse ? CELL_SPARSE : CELL_DENSE);
+    const GatePath gp = gate_path(d, p, dense, W, ws);
+    const bool split = gp.split;
     const int nch = (int)ceil_div(B, 64);
     float *chunk_rs_all = (float *)(wb + L.chunk_rs);
     if (!split)
@@ -521,6 +560,32 @@ int32_t backward_enqueue(const lstmss_dims *d, bool dense, const Plan &p, const 
     gx.dma = g_gemm_dma ? 1 : 0;
 
     const long part_stride = HB;
+    // dh rows of the data gradient for the next (earlier) step
+    Gemm1Args g1{};
+    g1.W = W; g1.ldw = K; g1.P = p.P;
+    g1.Kp = p.Kp; g1.M = (int)K; g1.m_begin = I; g1.N = B; g1.out_row0 = I;
+    g1.part = part; g1.part_stride = part_stride; g1.splitk = L.splitk;
+    g1.k_chunk = L.k_chunk; g1.steps = 1;
+    g1.fkept = fkept; g1.fidx_step = p.kept;
+    g1.dma = g_gemm_dma ? 1 : 0;
+    // coarse structure on the two-kernel gate path: the dh product selects
+    // (from the element kernel's chunk sums) and compacts, so no selection
+    // kernel runs between the two; the off-path work of a step is then
+    // forked after the product, which writes its compacted rows and index
+    const bool sel_gemm = gp.select_in_product;
+    auto launch_dh = [&](char *dGc, int32_t *idx) -> int32_t {
+        if (sel_gemm) {
+            g1.Gc = wb + L.stage; g1.idx = nullptr;
+            g1.sel_sq = (const double *)(wb + L.chunk_sq);
+            g1.sel_nch = nch; g1.sel_R = p.R; g1.sel_S = p.S; g1.sel_nslices = p.nslices;
+            g1.sel_gc = dGc; g1.sel_idx = idx;
+        } else {
+            g1.Gc = dGc; g1.idx = gsparse ? idx : nullptr;
+        }
+        g1.fidx = ffast ? idx : nullptr;
+        HIP_TRY(timed(LSTMSS_KERNEL_DATA_GRAD, st, [&] { return launch_gemm1(g1, bf16, st); }));
+        return LSTMSS_OK;
+    };
     for (int t = T - 1; t >= 0; --t) {
         const bool last = t == T - 1;
         char *dGc = dGc_all + (size_t)t * p.Kp * B * es;
@@ -570,6 +635,7 @@ int32_t backward_enqueue(const lstmss_dims *d, bool dense, const Plan &p, const 
         }
         if (split)
             ca.db = nullptr;
+        ca.defer_select = sel_gemm ? 1 : 0;
         ca.My = p.My;
         ca.nb = p.nb;
         if (!split && !fine &&
@@ -579,6 +645,12 @@ int32_t backward_enqueue(const lstmss_dims *d, bool dense, const Plan &p, const 
             return fine ? launch_cell_fine(ca, CELL_SPARSE, bf16, st)
                         : launch_cell(ca, sparse ? CELL_SPARSE : CELL_DENSE, bf16, st);
         }));
+
+        if (sel_gemm) {
+            const int32_t rc = launch_dh(dGc, idx);
+            if (rc)
+                return rc;
+        }
 
         const bool wg_now = use_side && batched && t == std::max(0, wg_hi - chunk_len);
         const bool dx_now = use_side && dX && t == std::max(0, dx_hi - dx_len);
@@ -611,15 +683,11 @@ int32_t backward_enqueue(const lstmss_dims *d, bool dense, const Plan &p, const 
             dx_hi = t;
         }
 
-        // dh rows of the data gradient for the next (earlier) step
-        Gemm1Args g1{};
-        g1.W = W; g1.ldw = K; g1.Gc = dGc; g1.idx = gsparse ? idx : nullptr; g1.P = p.P;
-        g1.Kp = p.Kp; g1.M = (int)K; g1.m_begin = I; g1.N = B; g1.out_row0 = I;
-        g1.part = part; g1.part_stride = part_stride; g1.splitk = L.splitk;
-        g1.k_chunk = L.k_chunk; g1.steps = 1;
-        g1.fidx = ffast ? idx : nullptr; g1.fkept = fkept; g1.fidx_step = p.kept;
-        g1.dma = g_gemm_dma ? 1 : 0;
-        HIP_TRY(timed(LSTMSS_KERNEL_DATA_GRAD, st, [&] { return launch_gemm1(g1, bf16, st); }));
+        if (!sel_gemm) {
+            const int32_t rc = launch_dh(dGc, idx);
+            if (rc)
+                return rc;
+        }
 
         if (!batched) {
             Gemm2Args g2{};
@@ -1080,6 +1148,25 @@ int64_t lstmss_kept_rows(const lstmss_dims *d, float sparsity, const lstmss_stru
     return p.Kp;
 }
 
+int32_t lstmss_bwd_info(const lstmss_dims *d, float sparsity, const lstmss_structure *s,
+                        int32_t *flags) {
+    if (!flags)
+        return fail(LSTMSS_ERR_INVALID_ARG, "flags is NULL");
+    int32_t rc = check_dims(d);
+    if (rc)
+        return rc;
+    Plan p;
+    rc = make_plan(d, sparsity, s, false, &p);
+    if (rc)
+        return rc;
+    // a 256-byte aligned weight matrix and workspace
+    const GatePath g = gate_path(d, p, false, (const void *)(uintptr_t)256,
+                                 (const void *)(uintptr_t)256);
+    *flags = (g.split ? LSTMSS_INFO_SPLIT_GATES : 0) |
+             (g.select_in_product ? LSTMSS_INFO_SELECT_IN_PRODUCT : 0);
+    return LSTMSS_OK;
+}
+
 int64_t lstmss_index_entries(const lstmss_dims *d, float sparsity, const lstmss_structure *s) {
     int32_t rc = check_dims(d);
     if (rc)
@@ -1282,6 +1369,7 @@ int32_t lstmss_set_option(int32_t option, int32_t value) {
     case LSTMSS_OPT_GRAPHS: g_graphs = value != 0; return LSTMSS_OK;
     case LSTMSS_OPT_FINE_SKIP: g_fine_skip = value != 0; return LSTMSS_OK;
     case LSTMSS_OPT_GEMM_DMA: g_gemm_dma = value != 0; return LSTMSS_OK;
+    case LSTMSS_OPT_GEMM_SELECT: g_gemm_select = value != 0; return LSTMSS_OK;
     case LSTMSS_OPT_STACK_DX_STEPS:
         if (value < 0)
             return fail(LSTMSS_ERR_INVALID_ARG, "stack dX steps %d must be >= 0", value);

@@ -30,7 +30,7 @@ ERR = {0: "ok", -1: "invalid argument", -2: "unsupported", -3: "workspace too sm
 
 # Exported symbols of include/lstmss.h
 SYMBOLS = ("lstmss_version", "lstmss_strerror", "lstmss_last_error", "lstmss_cache_bytes",
-           "lstmss_kept_rows", "lstmss_index_entries", "lstmss_workspace_bytes",
+           "lstmss_kept_rows", "lstmss_bwd_info", "lstmss_index_entries", "lstmss_workspace_bytes",
            "lstmss_fwd_workspace_bytes", "lstmss_sgd_update", "lstmss_mse_grad",
            "lstmss_stack_workspace_bytes", "lstm_bwd_stack", "lstmss_time_reverse",
            "lstmss_bidir_join", "lstmss_bidir_workspace_bytes", "lstm_bwd_bidir",
@@ -79,6 +79,8 @@ def load():
     lib.lstmss_cache_bytes.restype = i64
     lib.lstmss_kept_rows.argtypes = [pd, f, ps]
     lib.lstmss_kept_rows.restype = i64
+    lib.lstmss_bwd_info.argtypes = [pd, f, ps, ctypes.POINTER(ctypes.c_int32)]
+    lib.lstmss_bwd_info.restype = ctypes.c_int32
     lib.lstmss_index_entries.argtypes = [pd, f, ps]
     lib.lstmss_index_entries.restype = i64
     lib.lstmss_workspace_bytes.argtypes = [pd, f, ps]
@@ -186,6 +188,20 @@ def kept_rows(d: Dims, sparsity: float, s: Structure) -> int:
     n = load().lstmss_kept_rows(ctypes.byref(d), float(sparsity), ctypes.byref(s))
     _check(0 if n >= 0 else int(n), "lstmss_kept_rows")
     return int(n)
+
+
+INFO_SPLIT_GATES = 1
+INFO_SELECT_IN_PRODUCT = 2
+
+
+def bwd_info(d: Dims, sparsity: float, s: Structure) -> dict:
+    """How the backward runs the gate path for these arguments (current
+    options): {"split_gates": bool, "select_in_product": bool}."""
+    f = ctypes.c_int32(0)
+    _check(load().lstmss_bwd_info(ctypes.byref(d), float(sparsity), ctypes.byref(s),
+                                  ctypes.byref(f)), "lstmss_bwd_info")
+    return {"split_gates": bool(f.value & INFO_SPLIT_GATES),
+            "select_in_product": bool(f.value & INFO_SELECT_IN_PRODUCT)}
 
 
 def index_entries(d: Dims, sparsity: float, s: Structure) -> int:
@@ -545,7 +561,7 @@ def cache_views(cache, T, B, H, dtype):
     return gates, c, h
 
 
-OPTIONS = {"graphs": 0, "side_stream": 1, "stack_dx_steps": 2, "fine_skip": 3, "gemm_dma": 4}
+OPTIONS = {"graphs": 0, "side_stream": 1, "stack_dx_steps": 2, "fine_skip": 3, "gemm_dma": 4, "gemm_select": 5}
 
 
 def set_option(name: str, value: int):

@@ -205,10 +205,10 @@ def test_options_match_header_and_validate(L):
     assert {k.lower(): v for k, v in enum.items()} == L.OPTIONS
     lib = L.load()
     defaults = {"graphs": 0 if os.environ.get("LSTMSS_GRAPHS") == "0" else 1, "side_stream": 2,
-                "stack_dx_steps": 0, "fine_skip": 1, "gemm_dma": 1}
+                "stack_dx_steps": 0, "fine_skip": 1, "gemm_dma": 1, "gemm_select": 1}
     assert set(defaults) == set(L.OPTIONS)
     try:
-        for name in ("fine_skip", "gemm_dma", "graphs"):
+        for name in ("fine_skip", "gemm_dma", "gemm_select", "graphs"):
             for v in (0, 1):
                 assert lib.lstmss_set_option(L.OPTIONS[name], v) == 0
         for v in (0, 1, 2):
@@ -220,3 +220,33 @@ def test_options_match_header_and_validate(L):
     finally:
         for name, v in defaults.items():
             assert lib.lstmss_set_option(L.OPTIONS[name], v) == 0
+
+
+@pytest.mark.parametrize("T,B,I,H,sp,P,R,dtype,split,sel", [
+    (50, 128, 2048, 2048, 0.5, 4, 8, "f32", True, True),     # 4-layer encoder shape
+    (50, 128, 2048, 2048, 0.25, 4, 8, "f32", True, True),
+    (35, 64, 1024, 1024, 0.75, 4, 8, "f32", True, True),
+    (100, 256, 4096, 4096, 0.5, 4, 8, "bf16", True, True),
+    (3, 64, 1041, 1039, 0.5, 4, 8, "f32", True, True),      # trailing partial region
+    (3, 128, 256, 512, 0.5, 8, 8, "f32", True, True),       # 8-row slices
+    (3, 320, 64, 256, 0.5, 4, 8, "f32", True, True),        # five column chunks
+    (3, 200, 40, 400, 0.25, 4, 8, "f32", True, False),      # K' = 1200: no whole DMA stages
+    (20, 16, 128, 128, 0.5, 4, 8, "f32", False, False),     # H * B < 65536: one gate kernel
+    (35, 64, 1024, 1024, 0.0, 4, 8, "f32", True, False),    # nothing removed
+])
+def test_bwd_info(L, T, B, I, H, sp, P, R, dtype, split, sel):
+    """Which gate path a backward call takes (host logic, no GPU work); the
+    selection leaves the product when the option is off or DMA stages are."""
+    d = L.dims(T, B, I, H, dtype)
+    s = L.structure(P, R)
+    assert L.bwd_info(d, sp, s) == {"split_gates": split, "select_in_product": sel}
+    try:
+        for opt in ("gemm_select", "gemm_dma"):
+            L.set_option(opt, 0)
+            assert L.bwd_info(d, sp, s) == {"split_gates": split, "select_in_product": False}
+            L.set_option(opt, 1)
+    finally:
+        L.set_option("gemm_select", 1)
+        L.set_option("gemm_dma", 1)
+    with pytest.raises(L.LstmssError):
+        L.bwd_info(d, 0.3, s)

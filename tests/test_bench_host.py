@@ -38,6 +38,13 @@ def test_kernel_work_counts():
     assert w["weight_grad_gemm"]["flops"] == 2 * T * Kp * (I + H) * B
     # dW is written once per layer call (fp32)
     assert w["weight_grad_gemm"]["bytes"] >= 4 * H * (I + H) * 4
+    # the kept rows and index move from the gate kernels to the dh product
+    # when the selection runs inside it; the total stays the same
+    ws = bench.kernel_work(wl, 1, Kp, 4, select_in_product=True)
+    compact = T * (Kp * B * 4 + Kp // 4 * 4)
+    assert w["gates_select_compact"]["bytes"] - ws["gates_select_compact"]["bytes"] == compact
+    assert ws["data_grad_gemm"]["bytes"] - w["data_grad_gemm"]["bytes"] == compact
+    assert ws["data_grad_gemm"]["flops"] == w["data_grad_gemm"]["flops"]
 
 
 def test_traffic_needs_matching_sources(tmp_path, monkeypatch):
