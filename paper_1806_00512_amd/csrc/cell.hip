@@ -739,28 +739,64 @@ __global__ __launch_bounds__(64) void cell_fine_kernel(CellArgs a) {
 
 // db[r] (+)= sum over steps [t0, t1) of the row sums of the steps where r's
 // slice was kept (all steps when idx is NULL), steps in decreasing order.
-__global__ void bias_grad_kernel(float *db, const float *chunk_rs, int nch, long G, int t0, int t1,
-                                 const int32_t *idx, int kept, int P, int R, int S, int accumulate) {
-    const long r = blockIdx.x * (long)blockDim.x + threadIdx.x;
+// db[r] (+)= the sum over steps t = t1 - 1 down to t0 (fp32, in that order)
+// of row r's sum at step t (its chunk sums in chunk order) when the row's
+// slice is kept at t.  The loads of eight steps are issued together; with
+// EMAX / CMAX > 0 the kept-slice entries of the row's region (at most EMAX)
+// and its chunk sums (at most CMAX) are read in unrolled loops.
+template <int EMAX, int CMAX>
+__global__ __launch_bounds__(64) void bias_grad_kernel(float *db, const float *chunk_rs, int nch,
+                                                       long G, int t0, int t1, const int32_t *idx,
+                                                       int kept, int P, int R, int S, int accumulate) {
+    const long r = blockIdx.x * 64L + threadIdx.x;
     if (r >= G)
         return;
-    const long j = r / P, reg = j / R;
+    const long j = r / P;
+    const int ks = R - S;
+    const long eb = (j / R) * ks;
+    const int e1 = (int)min((long)ks, kept - eb);
     float acc = accumulate ? db[r] : 0.f;
-    for (int t = t1 - 1; t >= t0; --t) {
-        bool keep = idx == nullptr;
-        if (!keep) {
-            const int32_t *it = idx + (long)t * kept + reg * (R - S);
-            const long e1 = min((long)(R - S), kept - reg * (R - S));
-            for (long e = 0; e < e1; ++e)
-                keep |= it[e] == j;
-        }
-        if (keep) {
+    for (int tb = t1 - 1; tb >= t0; tb -= 8) {
+        float rsv[8];
+        bool kp[8];
+#pragma unroll
+        for (int u = 0; u < 8; ++u) {
+            const int t = tb - u;
+            rsv[u] = 0.f;
+            kp[u] = false;
+            if (t < t0)
+                continue;
             const float *q = chunk_rs + ((long)t * G + r) * nch;
             float rs = q[0];
-            for (int cc = 1; cc < nch; ++cc)
-                rs += q[cc];
-            acc += rs;
+            if constexpr (CMAX > 0) {
+#pragma unroll
+                for (int cc = 1; cc < CMAX; ++cc)
+                    if (cc < nch)
+                        rs += q[cc];
+            } else {
+                for (int cc = 1; cc < nch; ++cc)
+                    rs += q[cc];
+            }
+            bool keep = idx == nullptr;
+            if (!keep) {
+                const int32_t *it = idx + (long)t * kept + eb;
+                if constexpr (EMAX > 0) {
+#pragma unroll
+                    for (int e = 0; e < EMAX; ++e)
+                        if (e < e1)
+                            keep |= it[e] == j;
+                } else {
+                    for (int e = 0; e < e1; ++e)
+                        keep |= it[e] == j;
+                }
+            }
+            rsv[u] = rs;
+            kp[u] = keep;
         }
+#pragma unroll
+        for (int u = 0; u < 8; ++u)
+            if (kp[u])
+                acc += rsv[u];
     }
     db[r] = acc;
 }
@@ -1011,8 +1047,13 @@ hipError_t launch_cell_fine(const CellArgs &a, int mode, bool bf16, hipStream_t 
 hipError_t launch_bias_grad(float *db, const float *chunk_rs, int nch, long G, int t0, int t1,
                             const int32_t *idx, int kept, int P, int R, int S, bool accumulate,
                             hipStream_t s) {
-    hipLaunchKernelGGL(bias_grad_kernel, dim3((unsigned)ceil_div(G, 256)), dim3(256), 0, s, db,
-                       chunk_rs, nch, G, t0, t1, idx, kept, P, R, S, accumulate ? 1 : 0);
+    const dim3 grid((unsigned)ceil_div(G, 64)), blk(64);
+    if ((!idx || R - S <= 8) && nch <= 4)
+        hipLaunchKernelGGL((bias_grad_kernel<8, 4>), grid, blk, 0, s, db, chunk_rs, nch, G, t0, t1,
+                           idx, kept, P, R, S, accumulate ? 1 : 0);
+    else
+        hipLaunchKernelGGL((bias_grad_kernel<0, 0>), grid, blk, 0, s, db, chunk_rs, nch, G, t0, t1,
+                           idx, kept, P, R, S, accumulate ? 1 : 0);
     return hipGetLastError();
 }
 
