@@ -343,12 +343,14 @@ __global__ __launch_bounds__(THREADS, (wg_occupancy<TS, SPARSE, DMA, TT, ATN>())
     // (it + 1) & 1); the loop runs in pairs so that the sets are static
     uint64_t fmask = ~0ull;  // FN: kept blocks of this wavefront's slice at the current step
 
+    // (the lambdas that touch the tile arrays are forced inline: a call would
+    // take the arrays' addresses and keep them in scratch memory)
     // sparse routing: csrc[at] is the temporary column (kept row) that
     // accumulator column at * 32 + lane pulls at the current step, -1 if its
     // slice was dropped.  (Routing a step during the next step's first chunk,
     // to overlap the permutes with MFMAs, measured no faster.)
     int csrc[ATN];
-    auto lookup = [&](int tl) {
+    auto lookup = [&](int tl) __attribute__((always_inline)) {
         const int *tab = sidx[tl & 1][gi];
 #pragma unroll
         for (int at = 0; at < ATN; ++at) {
@@ -366,36 +368,35 @@ __global__ __launch_bounds__(THREADS, (wg_occupancy<TS, SPARSE, DMA, TT, ATN>())
             csrc[at] = src;
         }
     };
-    // acc[:, at] += t routed by srcs (accumulator tiles past the group's rows
-    // have src -1 everywhere and stay zero)
-    auto route = [&](const f32x16 (&t)[WG_FT][TT], const int (&srcs)[ATN]) {
+    // acc[:, at] += tmp routed by csrc (accumulator tiles past the group's
+    // rows have src -1 everywhere and stay zero)
+    auto route = [&]() __attribute__((always_inline)) {
 #pragma unroll
         for (int at = 0; at < ATN; ++at) {
-            const int src = srcs[at];
+            const int src = csrc[at];
             const int saddr = (((src < 0 ? 0 : src) & 31) + (lane & 32)) << 2;
             const int stile = src < 0 ? 0 : (src >> 5);
 #pragma unroll
             for (int ft = 0; ft < WG_FT; ++ft) {
-                // all lane permutes of this feature tile first, then the adds
-                float val[TT][16];
+                // the permute of each temporary tile, blended by the tile
+                // that holds the source (no array indexed by it)
+                f32x16 w;
 #pragma unroll
                 for (int tt = 0; tt < TT; ++tt)
 #pragma unroll
-                    for (int v = 0; v < 16; ++v)
-                        val[tt][v] = __int_as_float(
-                            __builtin_amdgcn_ds_bpermute(saddr, __float_as_int(t[ft][tt][v])));
+                    for (int v = 0; v < 16; ++v) {
+                        const float y = __int_as_float(
+                            __builtin_amdgcn_ds_bpermute(saddr, __float_as_int(tmp[ft][tt][v])));
+                        w[v] = tt == 0 ? y : (stile == tt ? y : w[v]);
+                    }
 #pragma unroll
-                for (int v = 0; v < 16; ++v) {
-                    float w = val[0][v];
-                    if (TT > 1)
-                        w = stile == 1 ? val[TT > 1 ? 1 : 0][v] : w;
-                    acc[ft][at][v] += src < 0 ? 0.f : w;  // dropped: exactly 0, even for inf/NaN
-                }
+                for (int v = 0; v < 16; ++v)
+                    acc[ft][at][v] += src < 0 ? 0.f : w[v];  // dropped: exactly 0, even for inf/NaN
             }
         }
     };
 
-    auto iter = [&](int it, auto sc) {
+    auto iter = [&](int it, auto sc) __attribute__((always_inline)) {
         constexpr int S0 = decltype(sc)::value, S1 = 1 - S0;
         const int buf = NS == 2 ? S0 : it % NS;
         const int tl = it / nbc, bc = it - tl * nbc;
@@ -524,7 +525,7 @@ __global__ __launch_bounds__(THREADS, (wg_occupancy<TS, SPARSE, DMA, TT, ATN>())
                     }
             } else {
                 lookup(tl);
-                route(tmp, csrc);
+                route();
 #pragma unroll
                 for (int ft = 0; ft < WG_FT; ++ft)
 #pragma unroll
@@ -575,7 +576,10 @@ __global__ __launch_bounds__(THREADS, (wg_occupancy<TS, SPARSE, DMA, TT, ATN>())
 }
 
 // Temporary tiles (kept rows per group / 32) and accumulator tiles (original
-// rows per group / 32) of the sparse weight-gradient kernel.
+// rows per group / 32) of the sparse weight-gradient kernel.  (Grouping four
+// regions of 24 kept rows into three exactly filled tiles needs 224
+// accumulator registers, one wavefront per SIMD: measured 1.14-1.3x slower
+// than the 24-of-32 tiles at 25 % sparsity.)
 void wgrad_tiles(int P, int R, int S, int *greg, int *tt, int *at) {
     const int kr = (R - S) * P, rp = R * P;
     *greg = kr <= 32 ? max(1, 32 / kr) : 1;
@@ -601,10 +605,11 @@ void wg_launch(const WgradArgs &a, bool vec, bool dma, dim3 grid, hipStream_t s)
         else
             hipLaunchKernelGGL((wgrad_kernel<TS, false, 1, 1, false, 32, true>), grid, dim3(THREADS), 0, s, a);
     } else {
+        // 64-column chunks: bf16 only (fp32 stages 16 or 32 columns)
 #define LSTMSS_WG(VE) do { \
         if (a.BC == 16) hipLaunchKernelGGL((wgrad_kernel<TS, SP, TTV, ATV, VE, 16>), grid, dim3(THREADS), 0, s, a); \
-        else if (a.BC == 32) hipLaunchKernelGGL((wgrad_kernel<TS, SP, TTV, ATV, VE, 32>), grid, dim3(THREADS), 0, s, a); \
-        else hipLaunchKernelGGL((wgrad_kernel<TS, SP, TTV, ATV, VE, 64>), grid, dim3(THREADS), 0, s, a); } while (0)
+        else if (sizeof(TS) == 4 || a.BC == 32) hipLaunchKernelGGL((wgrad_kernel<TS, SP, TTV, ATV, VE, 32>), grid, dim3(THREADS), 0, s, a); \
+        else hipLaunchKernelGGL((wgrad_kernel<TS, SP, TTV, ATV, VE, sizeof(TS) == 4 ? 32 : 64>), grid, dim3(THREADS), 0, s, a); } while (0)
         if (vec)
             LSTMSS_WG(true);
         else

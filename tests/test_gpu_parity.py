@@ -296,6 +296,10 @@ def test_layer_sparse_f32(L, T, B, I, H, sp, R, state):
     (2, 256, 24, 260, 0.5, 8, "f32", False),     # unaligned H: regions straddle gates, partial region
     (2, 256, 64, 256, 0.5, 8, "bf16", False),
     (2, 128, 48, 512, 0.75, 4, "f32", False),
+    (2, 256, 64, 256, 0.25, 8, "bf16", False),   # 24 kept rows per region: weight-gradient groups
+                                                  # of four regions fill three 32-row tiles
+    (2, 128, 48, 512, 0.25, 4, "f32", False),    # R = 4, S = 1: 12 kept rows, eight-region groups
+    (2, 256, 24, 260, 0.25, 8, "f32", False),    # the last four-region group partial
     (2, 256, 32, 256, 0.0, 8, "f32", True),
     (2, 256, 32, 256, 0.0, 8, "bf16", True),
 ])
