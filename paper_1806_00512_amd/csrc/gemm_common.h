@@ -100,6 +100,16 @@ __device__ __forceinline__ void dma16(const void *gsrc, lds_void_t *lds_dst) {
                  : "memory", "m0");
 }
 
+// The same for 4 bytes per lane (global_load_lds_dword): lane j writes bytes
+// [4 j, 4 j + 4) of the 256-byte LDS block at lds_dst.
+__device__ __forceinline__ void dma4(const void *gsrc, lds_void_t *lds_dst) {
+    const int lds = __builtin_amdgcn_readfirstlane((int)(uintptr_t)lds_dst);
+    asm volatile("s_mov_b32 m0, %1\n\tglobal_load_lds_dword %0, off"
+                 :
+                 : "v"(gsrc), "s"(lds)
+                 : "memory", "m0");
+}
+
 // s_waitcnt immediate that waits until at most n vector-memory operations of
 // this wavefront are outstanding (the other counters left at their maxima).
 constexpr int vmcnt_imm(int n) { return (n & 0xf) | ((n >> 4) << 14) | (0x7 << 4) | (0xf << 8); }

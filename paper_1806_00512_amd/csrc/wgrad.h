@@ -87,11 +87,18 @@ constexpr bool wg_splitop() { return SPARSE && DMA && sizeof(TS) == 4 && TT == 1
 template <typename TS, bool SPARSE, bool DMA, int TT, int ATN>
 constexpr int wg_occupancy() { return wg_splitop<TS, SPARSE, DMA, TT, ATN>() && ATN <= 2 ? 3 : 2; }
 
-template <typename TS, bool SPARSE, bool DMA>
-constexpr int wg_stages() { return DMA && SPARSE && sizeof(TS) == 2 ? 3 : 2; }
+// Stages of DMA chunks: bf16 with four row groups per work-group four (three
+// chunks in flight: 128 KB dense, 112 KB sparse), other sparse bf16 three
+// (chunks two ahead), the rest two.
+template <typename TS, bool SPARSE, bool DMA, int NG = WG_NG>
+constexpr int wg_stages() {
+    return !DMA || sizeof(TS) != 2 ? 2 : NG > WG_NG ? 4 : SPARSE ? 3 : 2;
+}
 template <typename TS, bool SPARSE, int TT, int ATN, bool VEC, int BC, bool FN = false,
-          bool DMA = false>
-__global__ __launch_bounds__(THREADS, (wg_occupancy<TS, SPARSE, DMA, TT, ATN>())) void wgrad_kernel(WgradArgs a) {
+          bool DMA = false, int NG = WG_NG>
+__global__ __launch_bounds__(NG * 128, (wg_occupancy<TS, SPARSE, DMA, TT, ATN>())) void wgrad_kernel(WgradArgs a) {
+    // NG row groups per work-group, two wavefronts (feature halves) each
+    constexpr int NWV = 2 * NG, THREADS = 64 * NWV;  // THREADS shadows the file-wide default
     constexpr bool SPLITOP = wg_splitop<TS, SPARSE, DMA, TT, ATN>();
     static_assert(!(FN && (SPARSE || BC != 32 || TT != 1)), "fine chunks are 32-column blocks");
     static_assert(!DMA || (BC * sizeof(TS) == 128 && VEC), "DMA chunks are 128-byte lines");
@@ -102,16 +109,21 @@ __global__ __launch_bounds__(THREADS, (wg_occupancy<TS, SPARSE, DMA, TT, ATN>())
     using V = Vec<TS, VEC>;
     constexpr int VW = V::W;
     constexpr int cpr = BC / VW;
-    constexpr int gvec = WG_NG * GROWS * cpr, xvec = WG_FEAT * cpr;
+    constexpr int gvec = NG * GROWS * cpr, xvec = WG_FEAT * cpr;
     constexpr int RG = (gvec + THREADS - 1) / THREADS;
     constexpr int RX = (xvec + THREADS - 1) / THREADS;
     // two stages: the MFMAs read one while the next batch chunk is written to
     // the other (one barrier per chunk); the kept-slice table is kept per
     // step parity so that a step's routing never races the next step's table
-    constexpr int NS = wg_stages<TS, SPARSE, DMA>();
+    constexpr int NS = wg_stages<TS, SPARSE, DMA, NG>();
+    static_assert(NS <= 3 || !FN, "more than three stages: not the fine structure");
     __shared__ __align__(16) E sX[NS][WG_FEAT][PITCH];
-    __shared__ __align__(16) E sG[NS][WG_NG * GROWS][PITCH];
-    __shared__ int sidx[2][WG_NG][64];
+    __shared__ __align__(16) E sG[NS][NG * GROWS][PITCH];
+    // kept-slice entries of the steps in flight: sparse DMA chunks copy a
+    // step's entries into slot (step mod NSLOT) with its first chunk (at most
+    // NS steps are between loaded and routed); otherwise two slots by parity
+    constexpr int NSLOT = SPARSE && DMA ? NS : 2;
+    __shared__ int sidx[NSLOT][NG][64];
 
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int fh = wave & 1, gi = wave >> 1;      // feature half, group of this wavefront
@@ -144,14 +156,14 @@ __global__ __launch_bounds__(THREADS, (wg_occupancy<TS, SPARSE, DMA, TT, ATN>())
         }
     };
     int r0, rcount, c0, ccount, q0, qcount, j0;
-    geom(blockIdx.x * WG_NG + gi, r0, rcount, c0, ccount, q0, qcount, j0);
+    geom(blockIdx.x * NG + gi, r0, rcount, c0, ccount, q0, qcount, j0);
     const int AT = SPARSE ? (rcount + 31) / 32 : 1;
     // compacted-row origin and count of both groups, for the loaders
-    int lc0[WG_NG], lcc[WG_NG], lq0[WG_NG], lqc[WG_NG];
+    int lc0[NG], lcc[NG], lq0[NG], lqc[NG];
 #pragma unroll
-    for (int k = 0; k < WG_NG; ++k) {
+    for (int k = 0; k < NG; ++k) {
         int t0, t1, t2;
-        geom(blockIdx.x * WG_NG + k, t0, t1, lc0[k], lcc[k], lq0[k], lqc[k], t2);
+        geom(blockIdx.x * NG + k, t0, t1, lc0[k], lcc[k], lq0[k], lqc[k], t2);
     }
 
     const int nbc = (B + BC - 1) / BC;
@@ -162,15 +174,15 @@ __global__ __launch_bounds__(THREADS, (wg_occupancy<TS, SPARSE, DMA, TT, ATN>())
     // are fixed for the whole launch, so their offsets within a step are
     // computed once; a chunk adds the step's base and the batch offset.
     // DMA: instruction k of a chunk fills rows [8k, 8k + 8) of sX (k < 16) or
-    // of sG (k >= 16); wavefront w issues k = w, w + 4, ...
-    constexpr int NDI = (WG_FEAT + WG_NG * GROWS) / 8, NDW = NDI / 4;
-    static_assert(!DMA || (NDI % 4 == 0 && WG_FEAT == 128), "DMA instruction split");
+    // of sG (k >= 16); wavefront w issues k = w, w + NWV, ...
+    constexpr int NDI = (WG_FEAT + NG * GROWS) / 8, NDW = NDI / NWV;
+    static_assert(!DMA || (NDI % NWV == 0 && WG_FEAT == 128), "DMA instruction split");
     int dofs[DMA ? NDW : 1];
     bool disx[DMA ? NDW : 1];
     if constexpr (DMA) {
 #pragma unroll
         for (int i = 0; i < NDW; ++i) {
-            const int k = wave + 4 * i;
+            const int k = wave + NWV * i;
             const int rr = 8 * (k < 16 ? k : k - 16) + (lane >> 3);
             const int pc = (lane & 7) ^ wg_swz(rr);  // the piece this lane's LDS slot holds
             if (k < 16) {
@@ -193,8 +205,8 @@ __global__ __launch_bounds__(THREADS, (wg_occupancy<TS, SPARSE, DMA, TT, ATN>())
         const int q = tid + i * THREADS;
         const int rho = q / cpr, bb = (q - rho * cpr) * VW;
         const int k = rho / GROWS, lr = rho - k * GROWS;
-        gok[i] = q < gvec && lr < lcc[k & (WG_NG - 1)];
-        gofs[i] = (lc0[k & (WG_NG - 1)] + (gok[i] ? lr : 0)) * B + bb;
+        gok[i] = q < gvec && lr < lcc[k & (NG - 1)];
+        gofs[i] = (lc0[k & (NG - 1)] + (gok[i] ? lr : 0)) * B + bb;
         gbb[i] = bb;
     }
 #pragma unroll
@@ -220,7 +232,7 @@ __global__ __launch_bounds__(THREADS, (wg_occupancy<TS, SPARSE, DMA, TT, ATN>())
         if constexpr (DMA) {
 #pragma unroll
             for (int i = 0; i < NDW; ++i) {
-                const int k = wave + 4 * i;
+                const int k = wave + NWV * i;
                 const TS *src = k < 16 ? (disx[i] ? xt : ht) + dofs[i] : Gt + dofs[i];
                 E *dst = k < 16 ? &sX[lbuf][8 * k][0] : &sG[lbuf][8 * (k - 16)][0];
                 dma16(src, (lds_void_t *)dst);
@@ -242,15 +254,21 @@ __global__ __launch_bounds__(THREADS, (wg_occupancy<TS, SPARSE, DMA, TT, ATN>())
             }
         }
         // the step's kept-slice entries, from a clamped (always valid)
-        // position; entries past the group's count become -1 when stashed, so
-        // that nothing waits for this load before then
-        if (SPARSE && b0 == 0 && tid < WG_NG * 64) {
+        // position: with DMA chunks copied straight into the step's table
+        // slot (the routing reads only the group's real entries), else into
+        // a register whose entries past the group's count become -1 when
+        // stashed, so that nothing waits for this load before then
+        if (SPARSE && b0 == 0 && tid < NG * 64) {
             const int k = tid >> 6, e = tid & 63;
-            ridx[set] = a.idx[(long)t * a.kept + (lqc[k] > 0 ? lq0[k] + min(e, lqc[k] - 1) : 0)];
+            const int32_t *src = a.idx + (long)t * a.kept + (lqc[k] > 0 ? lq0[k] + min(e, lqc[k] - 1) : 0);
+            if constexpr (DMA)
+                dma4(src, (lds_void_t *)&sidx[tl % NSLOT][k][0]);
+            else
+                ridx[set] = *src;
         }
-        if (FN && b0 == 0 && tid < WG_NG * 64) {  // kept blocks of the group's slice
+        if (FN && b0 == 0 && tid < NG * 64) {  // kept blocks of the group's slice
             const int k = tid >> 6, e = tid & 63;
-            const long sl = min((long)blockIdx.x * WG_NG + k, (long)G4 / 32 - 1);
+            const long sl = min((long)blockIdx.x * NG + k, (long)G4 / 32 - 1);
             ridx[set] = a.fidx[((long)t * (G4 / 32) + sl) * a.fkept + min(e, a.fkept - 1)];
         }
     };
@@ -258,7 +276,7 @@ __global__ __launch_bounds__(THREADS, (wg_occupancy<TS, SPARSE, DMA, TT, ATN>())
     auto entry_ok = [&](int k, int e) {
         if (SPARSE)
             return e < lqc[k];
-        return e < a.fkept && (long)blockIdx.x * WG_NG + k < G4 / 32;
+        return e < a.fkept && (long)blockIdx.x * NG + k < G4 / 32;
     };
     auto stash = [&](int it, int set, int buf) {
         const int tl = it / nbc;
@@ -280,7 +298,7 @@ __global__ __launch_bounds__(THREADS, (wg_occupancy<TS, SPARSE, DMA, TT, ATN>())
                 }
             }
         }
-        if ((SPARSE || FN) && it - tl * nbc == 0 && tid < WG_NG * 64)
+        if (((SPARSE && !DMA) || FN) && it - tl * nbc == 0 && tid < NG * 64)
             sidx[tl & 1][tid >> 6][tid & 63] = entry_ok(tid >> 6, tid & 63) ? ridx[set] : -1;
     };
 
@@ -323,15 +341,24 @@ __global__ __launch_bounds__(THREADS, (wg_occupancy<TS, SPARSE, DMA, TT, ATN>())
         __builtin_amdgcn_s_waitcnt(0);
     }
 
-    load(0, 0, 0);
-    if (niters > 1 && (!DMA || NS > 2))
-        load(1, 1, 1);
-    stash(0, 0, 0);
-    if (DMA) {
-        if (NS > 2 && niters > 1)
+    // DMA with NS stages: chunks 0 .. NS - 2 in flight before the loop;
+    // wait_chunks(n) waits until at most n chunks' copies are outstanding
+    auto wait_chunks = [&](int n) {
+        if (NS > 3 && n >= 2)
+            __builtin_amdgcn_s_waitcnt(vmcnt_imm((NS > 3 ? 2 : 0) * NDW));
+        else if (NS > 2 && n >= 1)
             __builtin_amdgcn_s_waitcnt(vmcnt_imm(NDW));
         else
             __builtin_amdgcn_s_waitcnt(0);
+    };
+    load(0, 0, 0);
+    if (niters > 1 && (!DMA || NS > 2))
+        load(1, 1, 1);
+    if (DMA && NS > 3 && niters > 2)
+        load(2, 0, 2);
+    stash(0, 0, 0);
+    if (DMA) {
+        wait_chunks(min(NS - 2, niters - 1));
         lds_barrier();
     } else {
         __syncthreads();
@@ -351,7 +378,7 @@ __global__ __launch_bounds__(THREADS, (wg_occupancy<TS, SPARSE, DMA, TT, ATN>())
     // to overlap the permutes with MFMAs, measured no faster.)
     int csrc[ATN];
     auto lookup = [&](int tl) __attribute__((always_inline)) {
-        const int *tab = sidx[tl & 1][gi];
+        const int *tab = sidx[SPARSE && DMA ? tl % NSLOT : tl & 1][gi];
 #pragma unroll
         for (int at = 0; at < ATN; ++at) {
             const int col = at * 32 + (lane & 31);
@@ -538,10 +565,8 @@ __global__ __launch_bounds__(THREADS, (wg_occupancy<TS, SPARSE, DMA, TT, ATN>())
         if (it + 1 < niters)
             stash(it + 1, S1, S1);
         if (DMA) {
-            if (NS > 2 && it + 2 < niters)
-                __builtin_amdgcn_s_waitcnt(vmcnt_imm(NDW));
-            else
-                __builtin_amdgcn_s_waitcnt(0);
+            // chunk it + 1 has landed; chunks it + 2 .. it + NS - 1 may be in flight
+            wait_chunks(min(NS - 2, niters - 2 - it));
             lds_barrier();
         } else {
             __syncthreads();
@@ -589,9 +614,14 @@ void wgrad_tiles(int P, int R, int S, int *greg, int *tt, int *at) {
 
 // One weight-gradient launch; `dma` takes the LDS-DMA variant (128-byte
 // chunks: 32 fp32 or 64 bf16 batch columns).
-template <typename TS, bool SP, int TTV, int ATV, bool FN>
+template <typename TS, bool SP, int TTV, int ATV, bool FN, int NG = WG_NG>
 void wg_launch(const WgradArgs &a, bool vec, bool dma, dim3 grid, hipStream_t s) {
     constexpr int DBC = 128 / (int)sizeof(TS);
+    if constexpr (NG != WG_NG) {  // other group counts: DMA chunks only
+        hipLaunchKernelGGL((wgrad_kernel<TS, SP, TTV, ATV, true, DBC, FN, true, NG>), grid,
+                           dim3(NG * 128), 0, s, a);
+        return;
+    }
     if constexpr (!FN || DBC == 32) {
         if (dma) {
             hipLaunchKernelGGL((wgrad_kernel<TS, SP, TTV, ATV, true, DBC, FN, true>), grid,
@@ -655,12 +685,20 @@ hipError_t launch_wgrad_t(WgradArgs a, bool sparse, hipStream_t s) {
     const bool vec = a.B % vw == 0;
     const bool dma = dma_ok(bc);
     const long groups = sparse ? ceil_div(ceil_div(4L * a.H / a.P, a.R), a.greg) : ceil_div(4L * a.H, 32);
-    dim3 grid((unsigned)ceil_div(groups, WG_NG), (unsigned)ceil_div(a.I + a.H, WG_FEAT));
+    // bf16 with DMA chunks: four row groups per work-group of eight wavefronts
+    // (one per CU), so that every staged feature row feeds twice the kept
+    // rows: the bf16 MFMAs outrun the rate the stages reach LDS
+    const bool ng4 = bf16 && dma && (!sparse || (tt == 1 && at <= 2));
+    const int ng = ng4 ? 4 : WG_NG;
+    dim3 grid((unsigned)ceil_div(groups, ng), (unsigned)ceil_div(a.I + a.H, WG_FEAT));
 #define LSTMSS_WGA(TTV) do { \
-        if (at <= 1) wg_launch<TS, true, TTV, 1, false>(a, vec, dma, grid, s); \
-        else if (at <= 2) wg_launch<TS, true, TTV, 2, false>(a, vec, dma, grid, s); \
+        if (at <= 1) { if (TTV == 1 && ng4) wg_launch<TS, true, TTV, 1, false, TTV == 1 ? 4 : WG_NG>(a, vec, dma, grid, s); \
+                       else wg_launch<TS, true, TTV, 1, false>(a, vec, dma, grid, s); } \
+        else if (at <= 2) { if (TTV == 1 && ng4) wg_launch<TS, true, TTV, 2, false, TTV == 1 ? 4 : WG_NG>(a, vec, dma, grid, s); \
+                            else wg_launch<TS, true, TTV, 2, false>(a, vec, dma, grid, s); } \
         else wg_launch<TS, true, TTV, 4, false>(a, vec, dma, grid, s); } while (0)
-    if (!sparse) wg_launch<TS, false, 1, 1, false>(a, vec, dma, grid, s);
+    if (!sparse) { if (ng4) wg_launch<TS, false, 1, 1, false, 4>(a, vec, dma, grid, s);
+                   else wg_launch<TS, false, 1, 1, false>(a, vec, dma, grid, s); }
     else if (tt == 1) LSTMSS_WGA(1);
     else LSTMSS_WGA(2);
 #undef LSTMSS_WGA
