@@ -153,6 +153,12 @@ struct StackRes {
     hipEvent_t join[kMaxStackLayers] = {}, done[kMaxStackLayers] = {};
     hipEvent_t fork = nullptr;
     std::vector<hipEvent_t> chunk_ev[kMaxStackLayers];
+#if LSTMSS_STACK_GRAPHS
+    // recorded stack calls (LRU), captured on their own stream
+    hipStream_t cap = nullptr;
+    std::vector<GraphEntry> graphs;
+    uint64_t use_clock = 0;
+#endif
     std::mutex mu;
 };
 std::map<int, StackRes> g_stack;
@@ -188,6 +194,10 @@ hipError_t stack_res(StackRes **out) {
         }
         if ((e = ev(&r.fork)) != hipSuccess)
             return e;
+#if LSTMSS_STACK_GRAPHS
+        if ((e = hipStreamCreateWithFlags(&r.cap, hipStreamNonBlocking)) != hipSuccess)
+            return e;
+#endif
     }
     *out = &r;
     return hipSuccess;
@@ -1108,9 +1118,73 @@ int32_t lstm_bwd_stack(int32_t layers, const lstmss_dims *d, float sparsity,
             HIP_TRY(hipEventCreateWithFlags(&e, hipEventDisableTiming));
             R->chunk_ev[l].push_back(e);
         }
+#if LSTMSS_STACK_GRAPHS
+    // recorded into a HIP graph (built only for checking the capture against
+    // a model of the stream-capture rules on the CPU)
+    bool timing;
+    {
+        std::lock_guard<std::mutex> tl(g_tmu);
+        timing = g_timing;
+    }
+    if (g_graphs && !timing) {
+        auto u = [](const void *q) { return (uint64_t)(uintptr_t)q; };
+        uint32_t spb;
+        std::memcpy(&spb, &sparsity, 4);
+        std::vector<uint64_t> key = {(uint64_t)layers, spb, u(dH_top), u(ws),
+                                     (uint64_t)g_stack_dx_steps, (uint64_t)g_side_mode,
+                                     s ? (uint64_t)s->kind : 99u, s ? (uint64_t)s->P : 0u,
+                                     s ? (uint64_t)s->R : 0u, s ? (uint64_t)s->My : 0u,
+                                     s ? (uint64_t)s->Mx : 0u};
+        for (int l = 0; l < layers; ++l)
+            for (uint64_t v : {(uint64_t)d[l].T, (uint64_t)d[l].B, (uint64_t)d[l].I,
+                               (uint64_t)d[l].H, (uint64_t)d[l].dtype, u(x[l]), u(W[l]),
+                               u(cache[l]), u(dX[l]), u(dW[l]), u(db ? db[l] : nullptr),
+                               u(idx_out ? idx_out[l] : nullptr)})
+                key.push_back(v);
+        GraphEntry *hit = nullptr;
+        for (GraphEntry &g : R->graphs)
+            if (g.key == key)
+                hit = &g;
+        if (!hit) {
+            HIP_TRY(hipStreamBeginCapture(R->cap, hipStreamCaptureModeRelaxed));
+            rc = stack_enqueue(layers, d, sp, x, W, cache, dH_top, dX, dW, db, idx_out, ws, R->cap,
+                               *R);
+            hipGraph_t graph = nullptr;
+            const hipError_t ec = hipStreamEndCapture(R->cap, &graph);
+            if (rc != LSTMSS_OK) {
+                if (graph)
+                    (void)hipGraphDestroy(graph);
+                return rc;
+            }
+            if (ec != hipSuccess)
+                return fail(LSTMSS_ERR_HIP, "stack capture failed: %s", hipGetErrorString(ec));
+            hipGraphExec_t exec = nullptr;
+            const hipError_t ei = hipGraphInstantiate(&exec, graph, nullptr, nullptr, 0);
+            (void)hipGraphDestroy(graph);
+            if (ei != hipSuccess)
+                return fail(LSTMSS_ERR_HIP, "stack graph instantiation failed: %s",
+                            hipGetErrorString(ei));
+            if (R->graphs.size() >= kMaxGraphs) {
+                size_t oldest = 0;
+                for (size_t i = 1; i < R->graphs.size(); ++i)
+                    if (R->graphs[i].last_use < R->graphs[oldest].last_use)
+                        oldest = i;
+                (void)hipGraphExecDestroy(R->graphs[oldest].exec);
+                R->graphs.erase(R->graphs.begin() + oldest);
+            }
+            R->graphs.push_back(GraphEntry{key, exec, 0});
+            hit = &R->graphs.back();
+        }
+        hit->last_use = ++R->use_clock;
+        HIP_TRY(hipGraphLaunch(hit->exec, (hipStream_t)stream));
+        return LSTMSS_OK;
+    }
+#endif
     // enqueued directly on the layers' streams, whatever LSTMSS_OPT_GRAPHS
     // says: recording a stack call into a HIP graph ended in a host
-    // segmentation fault whose cause is not found, so that path is off
+    // segmentation fault on the GPU whose cause is not found (the capture
+    // sequence satisfies the stream-capture rules as modelled on the CPU), so
+    // that path is built only for the model
     return stack_enqueue(layers, d, sp, x, W, cache, dH_top, dX, dW, db, idx_out, ws,
                          (hipStream_t)stream, *R);
 }
@@ -1365,6 +1439,14 @@ int32_t lstmss_set_option(int32_t option, int32_t value) {
             (void)hipGraphExecDestroy(g.exec);
         kv.second.graphs.clear();
     }
+#if LSTMSS_STACK_GRAPHS
+    for (auto &kv : g_stack) {
+        std::lock_guard<std::mutex> l2(kv.second.mu);
+        for (GraphEntry &g : kv.second.graphs)
+            (void)hipGraphExecDestroy(g.exec);
+        kv.second.graphs.clear();
+    }
+#endif
     switch (option) {
     case LSTMSS_OPT_GRAPHS: g_graphs = value != 0; return LSTMSS_OK;
     case LSTMSS_OPT_FINE_SKIP: g_fine_skip = value != 0; return LSTMSS_OK;

@@ -62,8 +62,10 @@ def sequential(L, xs, Ws, caches, dH, sparsity, kw):
 
 
 GRAPH_SKIP = pytest.mark.skip(reason="recording a stack call into a HIP graph ended in a host "
-                              "segmentation fault (cause not found); the library enqueues stack "
-                              "calls directly")
+                              "segmentation fault on the GPU; its capture sequence follows the "
+                              "stream-capture rules as modelled on the CPU "
+                              "(tests/test_capture_model.py), so the cause is not found and the "
+                              "library enqueues stack calls directly")
 
 
 @pytest.mark.parametrize("graphs", [pytest.param(True, marks=GRAPH_SKIP), False])
