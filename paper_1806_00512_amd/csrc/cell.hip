@@ -741,10 +741,10 @@ __global__ __launch_bounds__(64) void cell_fine_kernel(CellArgs a) {
 // slice was kept (all steps when idx is NULL), steps in decreasing order.
 // db[r] (+)= the sum over steps t = t1 - 1 down to t0 (fp32, in that order)
 // of row r's sum at step t (its chunk sums in chunk order) when the row's
-// slice is kept at t.  The loads of eight steps are issued together; with
+// slice is kept at t.  The loads of BS steps are issued together; with
 // EMAX / CMAX > 0 the kept-slice entries of the row's region (at most EMAX)
 // and its chunk sums (at most CMAX) are read in unrolled loops.
-template <int EMAX, int CMAX>
+template <int EMAX, int CMAX, int BS = 16>
 __global__ __launch_bounds__(64) void bias_grad_kernel(float *db, const float *chunk_rs, int nch,
                                                        long G, int t0, int t1, const int32_t *idx,
                                                        int kept, int P, int R, int S, int accumulate) {
@@ -756,11 +756,11 @@ __global__ __launch_bounds__(64) void bias_grad_kernel(float *db, const float *c
     const long eb = (j / R) * ks;
     const int e1 = (int)min((long)ks, kept - eb);
     float acc = accumulate ? db[r] : 0.f;
-    for (int tb = t1 - 1; tb >= t0; tb -= 8) {
-        float rsv[8];
-        bool kp[8];
+    for (int tb = t1 - 1; tb >= t0; tb -= BS) {
+        float rsv[BS];
+        bool kp[BS];
 #pragma unroll
-        for (int u = 0; u < 8; ++u) {
+        for (int u = 0; u < BS; ++u) {
             const int t = tb - u;
             rsv[u] = 0.f;
             kp[u] = false;
@@ -794,7 +794,7 @@ __global__ __launch_bounds__(64) void bias_grad_kernel(float *db, const float *c
             kp[u] = keep;
         }
 #pragma unroll
-        for (int u = 0; u < 8; ++u)
+        for (int u = 0; u < BS; ++u)
             if (kp[u])
                 acc += rsv[u];
     }
