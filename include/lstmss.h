@@ -351,6 +351,12 @@ int32_t lstmss_mse_grad(const lstmss_dims *d, const void *h, const float *y, flo
  *                      matrix and offset index, in place of a separate
  *                      selection launch; 0 always launches the selection
  *                      kernel (same bits; for checking and timing).
+ *   LSTMSS_OPT_FINE_FUSED  1 (default): FINE with Mx = 4, H a multiple of 4
+ *                      and H * B >= 65536 forms the gate gradient and
+ *                      selects the blocks in one kernel per step (each
+ *                      work-group holds four whole slices); 0 forms it into
+ *                      the staging matrix and selects in a second kernel
+ *                      (same bits; for checking and timing).
  * Changing an option drops the recorded graphs.  Not for use while calls
  * are being enqueued from other threads. */
 enum {
@@ -359,7 +365,8 @@ enum {
     LSTMSS_OPT_STACK_DX_STEPS = 2,
     LSTMSS_OPT_FINE_SKIP = 3,
     LSTMSS_OPT_GEMM_DMA = 4,
-    LSTMSS_OPT_GEMM_SELECT = 5
+    LSTMSS_OPT_GEMM_SELECT = 5,
+    LSTMSS_OPT_FINE_FUSED = 6
 };
 int32_t lstmss_set_option(int32_t option, int32_t value);
 

@@ -444,7 +444,7 @@ __global__ __launch_bounds__(EK_WAVES * 64) void cell_elem_kernel(CellArgs a) {
         lct[k] = ok[k] ? ct[e] : 0.f;
         lcp[k] = ok[k] ? cp[e] : 0.f;
         ldc[k] = (ok[k] && dcin) ? dcin[e] : 0.f;
-        ldh[k] = ok[k] ? sum_parts(dHup[e], a.dh_part + e, a.dh_nparts, a.dh_stride) : 0.f;
+        ldh[k] = ok[k] ? sum_parts<16>(dHup[e], a.dh_part + e, a.dh_nparts, a.dh_stride) : 0.f;
     }
     TS *out = (TS *)(SPARSE ? a.stage : a.dGc);
     TS *dbg = (TS *)a.dbg;
@@ -691,9 +691,8 @@ __global__ __launch_bounds__(64) void cell_fine_kernel(CellArgs a) {
             const int c2 = j2 * bpc + cb;
             const uint64_t k2 = score_key(readlane_f64(sc[j2], cb * My));
 #pragma unroll
-            for (int jj = 0; jj < NJ; ++jj)
-                if (c2 != cown[jj] && outranks(k2, c2, kown[jj], cown[jj]))
-                    ++beaten[jj];
+            for (int jj = 0; jj < NJ; ++jj)  // a block never outranks itself
+                beaten[jj] += outranks_n(k2, c2, kown[jj], cown[jj]);
         }
     }
     bool keep[NJ];
@@ -996,6 +995,179 @@ __global__ __launch_bounds__(256) void cell_fine32_kernel(CellArgs a) {
     }
 }
 
+// cell_fine4_kernel: 4-row slices with H % 4 == 0 at large shapes, the
+// element kernel and the fine selection in one launch.  Work-group x covers
+// units u0 = 4x .. 4x + 3 over all NCH = ceil(B / 64) batch chunks, one
+// (unit, chunk) per wavefront (wavefront w: unit u0 + w % 4, chunk w / 4,
+// lane l holding batch column 64 (w / 4) + l), as many loads in flight as the
+// element kernel.  Rows g H + u0 .. g H + u0 + 3 are the whole slice
+// (g H + u0) / 4, so the work-group holds four slices, one per gate.  Each
+// wavefront forms its four gate values exactly as the element kernel does
+// and puts each row's block sums (the butterfly inside My-lane groups) in
+// LDS.  Wavefront g < 4 then scores the blocks of gate g's slice (the four
+// rows folded in increasing order), ranks them by the total order
+// cell_fine_kernel uses, with the comparisons shared out over all 64 lanes,
+// and publishes a mask of the kept blocks.  Every wavefront stores its
+// masked values; each row's masked values are summed per lane over the
+// chunks in order, then over the 64 lanes, and added to db.  Values, scores,
+// the order of every sum and the selection are those of the element kernel
+// followed by cell_fine_kernel<TS, FS_STAGE, 4>.
+template <typename TS, int NCH>
+__global__ __launch_bounds__(256 * NCH) void cell_fine4_kernel(CellArgs a) {
+    constexpr int NW = 4 * NCH;               // wavefronts
+    constexpr int RPW = (16 + NW - 1) / NW;   // bias rows per wavefront (at most)
+    __shared__ double s_q[4][4][64];          // [gate][row of the slice][block]
+    __shared__ uint64_t s_keep[4];            // [gate]: kept blocks
+    __shared__ float s_m[4][4][NCH][64];      // [gate][row][chunk][lane]: masked values
+    const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+    const int B = a.B, H = a.H, My = a.My, nb = a.nb, K = a.S;
+    const int p = w & 3, c = w >> 2;
+    const int u0 = blockIdx.x * 4, u = u0 + p;  // H % 4 == 0: every unit is inside
+    const int b = 64 * c + lane;
+    const bool ok = b < B;
+    float *db = a.db;
+
+    float v[4];
+    {
+        const TS *__restrict__ gates = (const TS *)a.gates;
+        const int e = u * B + (ok ? b : 0);
+        float lg[4];
+#pragma unroll
+        for (int g = 0; g < 4; ++g)
+            lg[g] = ok ? st<TS>::load(gates, (long)(g * H + u) * B + b) : 0.f;
+        const float lct = ok ? a.c_t[e] : 0.f;
+        const float lcp = ok ? a.c_prev[e] : 0.f;
+        const float ldc = (ok && a.dc_in) ? a.dc_in[e] : 0.f;
+        const float ldh =
+            ok ? sum_parts<16>(a.dH_up[e], a.dh_part + e, a.dh_nparts, a.dh_stride) : 0.f;
+        const float ig = lg[0], fg = lg[1], gg = lg[2], og = lg[3];
+        const float tc = tanhf(lct);
+        const float dcv = ldc + ldh * og * (1.f - tc * tc);
+        v[0] = st<TS>::rnd(dcv * gg * ig * (1.f - ig));
+        v[1] = st<TS>::rnd(dcv * lcp * fg * (1.f - fg));
+        v[2] = st<TS>::rnd(dcv * ig * (1.f - gg * gg));
+        v[3] = st<TS>::rnd(ldh * tc * og * (1.f - og));
+        if (ok) {
+            a.dc_out[u * B + b] = dcv * fg;
+            TS *dbg = (TS *)a.dbg;
+            if (dbg) {
+#pragma unroll
+                for (int g = 0; g < 4; ++g)
+                    st<TS>::store(dbg, (long)(g * H + u) * B + b, v[g]);
+            }
+        } else {
+#pragma unroll
+            for (int g = 0; g < 4; ++g)
+                v[g] = 0.f;
+        }
+    }
+
+    // db of the rows this wavefront finishes (row rr = 4 g + p of the
+    // work-group), loaded now so that the loads complete during the selection
+    float dbv[RPW];
+#pragma unroll
+    for (int k = 0; k < RPW; ++k) {
+        const int rr = w + NW * k;
+        dbv[k] = (db && rr < 16 && lane == 0) ? db[(long)(rr >> 2) * H + u0 + (rr & 3)] : 0.f;
+    }
+
+    // this row's block sums of squares in chunk c (columns past B add zero)
+    {
+        const int blk = c * (64 / My) + lane / My;
+        double q[4];
+#pragma unroll
+        for (int g = 0; g < 4; ++g)
+            q[g] = (double)v[g] * (double)v[g];
+        for (int off = My >> 1; off >= 1; off >>= 1) {
+#pragma unroll
+            for (int g = 0; g < 4; ++g)
+                q[g] = q[g] + shfl_xor_f64(q[g], off);
+        }
+        if ((lane & (My - 1)) == 0 && blk < nb) {
+#pragma unroll
+            for (int g = 0; g < 4; ++g)
+                s_q[g][p][blk] = q[g];
+        }
+    }
+    __syncthreads();
+
+    if (w < 4) {  // wavefront g selects the blocks of gate g's slice
+        // lane = q nbp + l (nbp: nb rounded up to a power of two) holds block
+        // l and counts the blocks of the q-th share of the slice that
+        // outrank it; the shares' counts are then added
+        const int g = w;
+        const long j = (long)g * (H / 4) + blockIdx.x;
+        int nbp = 1;
+        while (nbp < nb)
+            nbp <<= 1;
+        const int l = lane & (nbp - 1), share = lane / nbp;
+        const int len = (nb + 64 / nbp - 1) / (64 / nbp);
+        auto score = [&](int blk) {  // the four rows folded in increasing order
+            double sc = s_q[g][0][blk];
+#pragma unroll
+            for (int r = 1; r < 4; ++r)
+                sc = sc + s_q[g][r][blk];
+            return sc;
+        };
+        const bool own = l < nb;
+        const double sc = own ? score(l) : 0.0;
+        if (own && share == 0 && a.scores)
+            a.scores[j * nb + l] = sc;
+        const uint64_t kown = score_key(sc);
+        int beaten = 0;  // a block never outranks itself
+        const int c1 = min(nb, (share + 1) * len);
+#pragma unroll 4
+        for (int c2 = share * len; c2 < c1; ++c2)
+            beaten += outranks_n(score_key(score(c2)), c2, kown, l);
+        for (int off = nbp; off < 64; off <<= 1)
+            beaten += __shfl_xor(beaten, off, 64);
+        // kept when fewer than nb - K blocks of the slice outrank it
+        const bool mine = lane < nb && beaten < nb - K;  // lanes below nbp: share 0, l = lane
+        const uint64_t m = __ballot(mine);
+        if (mine)
+            a.idx[j * (nb - K) + __popcll(m & ((1ull << lane) - 1ull))] = lane;
+        if (lane == 0)
+            s_keep[g] = m;
+    }
+    __syncthreads();
+
+    // masked values to dGc and to LDS for the row sums
+    TS *dGc = (TS *)a.dGc;
+#pragma unroll
+    for (int g = 0; g < 4; ++g) {
+        const float m = ((s_keep[g] >> (b / My)) & 1ull) ? v[g] : 0.f;
+        if (ok)
+            st<TS>::store(dGc, (long)(g * H + u) * B + b, m);
+        s_m[g][p][c][lane] = m;
+    }
+    if (!db)
+        return;
+    __syncthreads();
+    // bias gradient: per lane the chunks in order, then the 64 lanes
+    float rs[RPW];
+#pragma unroll
+    for (int k = 0; k < RPW; ++k) {
+        const int rr = min(w + NW * k, 15);
+        rs[k] = 0.f;
+#pragma unroll
+        for (int jj = 0; jj < NCH; ++jj)
+            if (64 * jj + lane < B)
+                rs[k] += s_m[rr >> 2][rr & 3][jj][lane];
+    }
+#pragma unroll
+    for (int off = 32; off >= 1; off >>= 1) {
+#pragma unroll
+        for (int k = 0; k < RPW; ++k)
+            rs[k] += shfl_xor_f32(rs[k], off);
+    }
+#pragma unroll
+    for (int k = 0; k < RPW; ++k) {
+        const int rr = w + NW * k;
+        if (rr < 16 && lane == 0)
+            db[(long)(rr >> 2) * H + u0 + (rr & 3)] = dbv[k] + rs[k];
+    }
+}
+
 template <typename TS, int SRC>
 static void launch_fine_src(const CellArgs &a, hipStream_t s) {
     const dim3 grid((unsigned)(4L * a.H / a.P));
@@ -1017,13 +1189,25 @@ template <typename TS>
 static hipError_t launch_fine_typed(const CellArgs &a, int mode, hipStream_t s) {
     if (mode == CELL_GIVEN) {
         launch_fine_src<TS, FS_GIVEN>(a, s);
+    } else if (a.fine_fused && a.P == 4 && a.H % 4 == 0 && (long)a.H * a.B >= 65536) {
+        const dim3 grid((unsigned)(a.H / 4));
+        switch (ceil_div(a.B, 64)) {
+        case 1: hipLaunchKernelGGL((cell_fine4_kernel<TS, 1>), grid, dim3(256), 0, s, a); break;
+        case 2: hipLaunchKernelGGL((cell_fine4_kernel<TS, 2>), grid, dim3(512), 0, s, a); break;
+        case 3: hipLaunchKernelGGL((cell_fine4_kernel<TS, 3>), grid, dim3(768), 0, s, a); break;
+        default: hipLaunchKernelGGL((cell_fine4_kernel<TS, 4>), grid, dim3(1024), 0, s, a); break;
+        }
     } else if (a.stage && (long)a.H * a.B >= 65536) {
         // large shapes: the element kernel forms each unit's four gate rows
         // once (one read of dh and the cache per unit), then the slices are
-        // selected from its staging matrix
+        // selected from its staging matrix.  It runs in its dense mode with
+        // the staging matrix as output: the coarse chunk sums of squares are
+        // not needed here
         const int nch = (int)ceil_div(a.B, 64);
         dim3 ge((unsigned)ceil_div(a.H, EK_UNITS), (unsigned)nch);
-        hipLaunchKernelGGL((cell_elem_kernel<TS, CELL_SPARSE>), ge, dim3(EK_WAVES * 64), 0, s, a);
+        CellArgs ea = a;
+        ea.dGc = a.stage;
+        hipLaunchKernelGGL((cell_elem_kernel<TS, CELL_DENSE>), ge, dim3(EK_WAVES * 64), 0, s, ea);
         hipError_t e = hipGetLastError();
         if (e != hipSuccess)
             return e;

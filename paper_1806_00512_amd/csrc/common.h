@@ -74,26 +74,27 @@ __device__ __forceinline__ uint64_t score_key(double s) {
 __host__ __device__ __forceinline__ long ceil_div(long a, long b) { return (a + b - 1) / b; }
 
 // init + p[0] + p[stride] + ... + p[(n-1)*stride], added in that order; the
-// loads are issued eight at a time so their latencies overlap.
+// loads are issued NB at a time so their latencies overlap.
+template <int NB = 8>
 __device__ __forceinline__ float sum_parts(float init, const float *p, int n, long stride) {
     float s = init;
     int i = 0;
-    for (; i + 8 <= n; i += 8) {
-        float v[8];
+    for (; i + NB <= n; i += NB) {
+        float v[NB];
 #pragma unroll
-        for (int j = 0; j < 8; ++j)
+        for (int j = 0; j < NB; ++j)
             v[j] = p[(long)(i + j) * stride];
 #pragma unroll
-        for (int j = 0; j < 8; ++j)
+        for (int j = 0; j < NB; ++j)
             s += v[j];
     }
     if (i < n) {
-        float v[8];
+        float v[NB];
 #pragma unroll
-        for (int j = 0; j < 8; ++j)
+        for (int j = 0; j < NB; ++j)
             v[j] = i + j < n ? p[(long)(i + j) * stride] : 0.f;
 #pragma unroll
-        for (int j = 0; j < 8; ++j)
+        for (int j = 0; j < NB; ++j)
             if (i + j < n)
                 s += v[j];
     }

@@ -43,6 +43,7 @@ struct CellArgs {
     // columns, S blocks removed per slice; dGc is then the masked [4H][B]
     // matrix, idx [4H/P][nb - S] the kept blocks and scores [4H/P][nb]
     int My, nb;
+    int fine_fused;        // 4-row slices, H % 4 == 0, large shapes: one fused kernel
 };
 
 // Data gradient [dx_t; dh_{t-1}] = W_c^T dG_c, split over K into partials.

@@ -173,6 +173,9 @@ bool g_gemm_dma = true;
 // coarse selection inside the dh product where the shape allows (1) or in
 // its own kernel (0); same bits
 bool g_gemm_select = true;
+// fine structure with 4-row slices at large shapes: gate gradient and block
+// selection in one kernel (1) or two (0); same bits
+bool g_fine_fused = true;
 
 hipError_t stack_res(StackRes **out) {
     int dev = 0;
@@ -648,6 +651,7 @@ int32_t backward_enqueue(const lstmss_dims *d, bool dense, const Plan &p, const 
         ca.defer_select = sel_gemm ? 1 : 0;
         ca.My = p.My;
         ca.nb = p.nb;
+        ca.fine_fused = g_fine_fused ? 1 : 0;
         if (!split && !fine &&
             cell_lds_bytes(ca, sparse ? CELL_SPARSE : CELL_DENSE) > kMaxLds)
             return fail(LSTMSS_ERR_UNSUPPORTED, "R*P*B too large for one work-group's LDS");
@@ -1452,6 +1456,7 @@ int32_t lstmss_set_option(int32_t option, int32_t value) {
     case LSTMSS_OPT_FINE_SKIP: g_fine_skip = value != 0; return LSTMSS_OK;
     case LSTMSS_OPT_GEMM_DMA: g_gemm_dma = value != 0; return LSTMSS_OK;
     case LSTMSS_OPT_GEMM_SELECT: g_gemm_select = value != 0; return LSTMSS_OK;
+    case LSTMSS_OPT_FINE_FUSED: g_fine_fused = value != 0; return LSTMSS_OK;
     case LSTMSS_OPT_STACK_DX_STEPS:
         if (value < 0)
             return fail(LSTMSS_ERR_INVALID_ARG, "stack dX steps %d must be >= 0", value);

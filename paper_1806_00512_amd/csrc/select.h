@@ -15,6 +15,11 @@ __device__ __forceinline__ bool outranks(uint64_t ki, long i, uint64_t kj, long 
     return ki > kj || (ki == kj && i < j);
 }
 
+// outranks() as 0 / 1 without branches, for counting in unrolled loops
+__device__ __forceinline__ int outranks_n(uint64_t ki, int i, uint64_t kj, int j) {
+    return (int)((ki > kj) | ((ki == kj) & (i < j)));
+}
+
 struct SliceSel {
     double score;  // squared L2 norm of the lane's slice
     int slot;      // its slot in the step's offset index, -1 when dropped

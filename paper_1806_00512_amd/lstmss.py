@@ -561,7 +561,8 @@ def cache_views(cache, T, B, H, dtype):
     return gates, c, h
 
 
-OPTIONS = {"graphs": 0, "side_stream": 1, "stack_dx_steps": 2, "fine_skip": 3, "gemm_dma": 4, "gemm_select": 5}
+OPTIONS = {"graphs": 0, "side_stream": 1, "stack_dx_steps": 2, "fine_skip": 3, "gemm_dma": 4, "gemm_select": 5,
+           "fine_fused": 6}
 
 
 def set_option(name: str, value: int):

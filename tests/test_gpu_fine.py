@@ -263,3 +263,36 @@ def test_fine_mfma_blocks(L, T, B, I, H, sp, dtype):
         assert torch.equal(outs[0][k], outs[1][k]), k
     for k in ("dX", "dW", "db"):
         assert torch.equal(outs[0][k], o[k]), k
+
+
+# ---------------------------------------------------------------------------
+# 4-row slices at large shapes: the gate gradient and the block selection in
+# one kernel (option fine_fused = 1, the default) against the element kernel
+# followed by the selection kernel (0): every output the same bits
+# ---------------------------------------------------------------------------
+@pytest.mark.parametrize("T,B,I,H,sp,My,dtype", [
+    (3, 128, 2048, 2048, 0.5, 8, "f32"),    # the 4-layer workload's layer shape, 8 x 4 blocks
+    (2, 256, 64, 256, 0.5, 4, "f32"),       # 64 blocks per slice, four column chunks
+    (2, 200, 64, 512, 0.36, 8, "f32"),      # ragged last block and chunk (9 of 25 removed)
+    (3, 64, 96, 1024, 0.75, 16, "f32"),     # one column chunk
+    (2, 100, 64, 1024, 0.5, 64, "f32"),     # blocks as wide as a chunk, ragged
+    (2, 256, 64, 256, 0.5, 8, "bf16"),
+    (2, 192, 64, 512, 0.5, 4, "bf16"),
+])
+def test_fine_fused_same_bits(L, T, B, I, H, sp, My, dtype):
+    d = make_layer(T, B, I, H, seed=H + B + My, w_scale=0.1, dtype=dtype, state=True)
+    x, W = gpu_tensor(d["x"], dtype), gpu_tensor(d["W"], dtype)
+    dH = gpu_tensor(d["dH_up"])
+    dhT, dcT = gpu_tensor(d["dhT"]), gpu_tensor(d["dcT"])
+    _, cache = L.fwd_cache(x, W, gpu_tensor(d["b"]), gpu_tensor(d["h0"]), gpu_tensor(d["c0"]))
+    outs = []
+    try:
+        for fused in (1, 0):
+            L.set_option("fine_fused", fused)
+            outs.append(L.bwd_structsparse(x, W, cache, dH, sparsity=sp, dhT=dhT, dcT=dcT,
+                                           want_dbg=True, kind=L.FINE, My=My, Mx=4))
+            torch.cuda.synchronize()
+    finally:
+        L.set_option("fine_fused", 1)
+    for k in ("dX", "dW", "db", "dh0", "dc0", "idx", "dbg"):
+        assert torch.equal(outs[0][k], outs[1][k]), k
