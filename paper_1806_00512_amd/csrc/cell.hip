@@ -1012,15 +1012,34 @@ __global__ __launch_bounds__(256) void cell_fine32_kernel(CellArgs a) {
 // chunks in order, then over the 64 lanes, and added to db.  Values, scores,
 // the order of every sum and the selection are those of the element kernel
 // followed by cell_fine_kernel<TS, FS_STAGE, 4>.
+// Lane i receives lane i + N of its 16-lane row (a DPP row shift; lanes
+// whose source leaves the row receive 0).  Used for the steps off = 8, 4, 2,
+// 1 of a butterfly (each lane adds the value of lane i ^ off to its own):
+// the lanes that feed the first lane of an aligned group of 2 off lanes have
+// i ^ off = i + off, so that first lane gets the butterfly's bits.
+template <int N>
+__device__ __forceinline__ float row_down_f32(float v) {
+    return __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), 0x100 + N, 0xf, 0xf, true));
+}
+template <int N>
+__device__ __forceinline__ double row_down_f64(double v) {
+    const long long x = __double_as_longlong(v);
+    const int lo = __builtin_amdgcn_update_dpp(0, (int)(x & 0xffffffffLL), 0x100 + N, 0xf, 0xf, true);
+    const int hi = __builtin_amdgcn_update_dpp(0, (int)(x >> 32), 0x100 + N, 0xf, 0xf, true);
+    return __longlong_as_double(((long long)hi << 32) | (unsigned int)lo);
+}
+
 template <typename TS, int NCH>
 __global__ __launch_bounds__(256 * NCH) void cell_fine4_kernel(CellArgs a) {
     constexpr int NW = 4 * NCH;               // wavefronts
     constexpr int RPW = (16 + NW - 1) / NW;   // bias rows per wavefront (at most)
     __shared__ double s_q[4][4][64];          // [gate][row of the slice][block]
     __shared__ uint64_t s_keep[4];            // [gate]: kept blocks
-    __shared__ float s_m[4][4][NCH][64];      // [gate][row][chunk][lane]: masked values
+    __shared__ double s_sc[4][64];            // [gate][block]: scores
+    __shared__ float s_v[4][4][NCH][64];      // [gate][row][chunk][lane]: values
     const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
     const int B = a.B, H = a.H, My = a.My, nb = a.nb, K = a.S;
+    const int lmy = __builtin_ctz(My);  // My is a power of two
     const int p = w & 3, c = w >> 2;
     const int u0 = blockIdx.x * 4, u = u0 + p;  // H % 4 == 0: every unit is inside
     const int b = 64 * c + lane;
@@ -1071,23 +1090,39 @@ __global__ __launch_bounds__(256 * NCH) void cell_fine4_kernel(CellArgs a) {
         dbv[k] = (db && rr < 16 && lane == 0) ? db[(long)(rr >> 2) * H + u0 + (rr & 3)] : 0.f;
     }
 
-    // this row's block sums of squares in chunk c (columns past B add zero)
+    // this row's block sums of squares in chunk c (columns past B add zero):
+    // the My-lane butterfly of cell_fine_kernel, in each block's first lane
     {
-        const int blk = c * (64 / My) + lane / My;
+        const int blk = c * (64 >> lmy) + (lane >> lmy);
         double q[4];
 #pragma unroll
         for (int g = 0; g < 4; ++g)
             q[g] = (double)v[g] * (double)v[g];
-        for (int off = My >> 1; off >= 1; off >>= 1) {
+        for (int off = My >> 1; off >= 16; off >>= 1) {
 #pragma unroll
             for (int g = 0; g < 4; ++g)
                 q[g] = q[g] + shfl_xor_f64(q[g], off);
+        }
+#pragma unroll
+        for (int g = 0; g < 4; ++g) {
+            if (My >= 16)
+                q[g] = q[g] + row_down_f64<8>(q[g]);
+            if (My >= 8)
+                q[g] = q[g] + row_down_f64<4>(q[g]);
+            if (My >= 4)
+                q[g] = q[g] + row_down_f64<2>(q[g]);
+            q[g] = q[g] + row_down_f64<1>(q[g]);
         }
         if ((lane & (My - 1)) == 0 && blk < nb) {
 #pragma unroll
             for (int g = 0; g < 4; ++g)
                 s_q[g][p][blk] = q[g];
         }
+    }
+    if (db) {
+#pragma unroll
+        for (int g = 0; g < 4; ++g)
+            s_v[g][p][c][lane] = v[g];
     }
     __syncthreads();
 
@@ -1097,28 +1132,32 @@ __global__ __launch_bounds__(256 * NCH) void cell_fine4_kernel(CellArgs a) {
         // outrank it; the shares' counts are then added
         const int g = w;
         const long j = (long)g * (H / 4) + blockIdx.x;
-        int nbp = 1;
-        while (nbp < nb)
-            nbp <<= 1;
-        const int l = lane & (nbp - 1), share = lane / nbp;
-        const int len = (nb + 64 / nbp - 1) / (64 / nbp);
-        auto score = [&](int blk) {  // the four rows folded in increasing order
-            double sc = s_q[g][0][blk];
+        const int lnbp = nb > 1 ? 32 - __builtin_clz(nb - 1) : 0;  // nbp = 2^lnbp <= 64
+        const int nbp = 1 << lnbp;
+        const int l = lane & (nbp - 1), share = lane >> lnbp;
+        const int len = (nb + (64 >> lnbp) - 1) >> (6 - lnbp);  // shares of 64 / nbp
+        const bool own = l < nb;
+        double sc = 0.0;
+        if (own) {  // the four rows folded in increasing order
+            sc = s_q[g][0][l];
 #pragma unroll
             for (int r = 1; r < 4; ++r)
-                sc = sc + s_q[g][r][blk];
-            return sc;
-        };
-        const bool own = l < nb;
-        const double sc = own ? score(l) : 0.0;
-        if (own && share == 0 && a.scores)
-            a.scores[j * nb + l] = sc;
+                sc = sc + s_q[g][r][l];
+            if (share == 0) {
+                s_sc[g][l] = sc;  // read back below by this wavefront only
+                if (a.scores)
+                    a.scores[j * nb + l] = sc;
+            }
+        }
+        __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+        __builtin_amdgcn_wave_barrier();
+        __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
         const uint64_t kown = score_key(sc);
         int beaten = 0;  // a block never outranks itself
         const int c1 = min(nb, (share + 1) * len);
 #pragma unroll 4
         for (int c2 = share * len; c2 < c1; ++c2)
-            beaten += outranks_n(score_key(score(c2)), c2, kown, l);
+            beaten += outranks_n(score_key(s_sc[g][c2]), c2, kown, l);
         for (int off = nbp; off < 64; off <<= 1)
             beaten += __shfl_xor(beaten, off, 64);
         // kept when fewer than nb - K blocks of the slice outrank it
@@ -1131,34 +1170,39 @@ __global__ __launch_bounds__(256 * NCH) void cell_fine4_kernel(CellArgs a) {
     }
     __syncthreads();
 
-    // masked values to dGc and to LDS for the row sums
+    // masked values to dGc
     TS *dGc = (TS *)a.dGc;
 #pragma unroll
     for (int g = 0; g < 4; ++g) {
-        const float m = ((s_keep[g] >> (b / My)) & 1ull) ? v[g] : 0.f;
+        const float m = ((s_keep[g] >> (b >> lmy)) & 1ull) ? v[g] : 0.f;
         if (ok)
             st<TS>::store(dGc, (long)(g * H + u) * B + b, m);
-        s_m[g][p][c][lane] = m;
     }
     if (!db)
         return;
-    __syncthreads();
-    // bias gradient: per lane the chunks in order, then the 64 lanes
+    // bias gradient: the masked values per lane over the chunks in order,
+    // then over the 64 lanes
     float rs[RPW];
 #pragma unroll
     for (int k = 0; k < RPW; ++k) {
         const int rr = min(w + NW * k, 15);
+        const uint64_t keep = s_keep[rr >> 2];
         rs[k] = 0.f;
 #pragma unroll
-        for (int jj = 0; jj < NCH; ++jj)
-            if (64 * jj + lane < B)
-                rs[k] += s_m[rr >> 2][rr & 3][jj][lane];
+        for (int jj = 0; jj < NCH; ++jj) {
+            const int bj = 64 * jj + lane;
+            if (bj < B)
+                rs[k] += ((keep >> (bj >> lmy)) & 1ull) ? s_v[rr >> 2][rr & 3][jj][lane] : 0.f;
+        }
     }
 #pragma unroll
-    for (int off = 32; off >= 1; off >>= 1) {
-#pragma unroll
-        for (int k = 0; k < RPW; ++k)
-            rs[k] += shfl_xor_f32(rs[k], off);
+    for (int k = 0; k < RPW; ++k) {  // the 64-lane butterfly's sum in lane 0
+        rs[k] = rs[k] + shfl_xor_f32(rs[k], 32);
+        rs[k] = rs[k] + shfl_xor_f32(rs[k], 16);
+        rs[k] = rs[k] + row_down_f32<8>(rs[k]);
+        rs[k] = rs[k] + row_down_f32<4>(rs[k]);
+        rs[k] = rs[k] + row_down_f32<2>(rs[k]);
+        rs[k] = rs[k] + row_down_f32<1>(rs[k]);
     }
 #pragma unroll
     for (int k = 0; k < RPW; ++k) {
