@@ -1029,6 +1029,25 @@ __device__ __forceinline__ double row_down_f64(double v) {
     return __longlong_as_double(((long long)hi << 32) | (unsigned int)lo);
 }
 
+// Lane i receives lane i ^ 32 (X = 32) or lane i ^ 16 (X = 16): the swap of
+// the two halves of the wavefront, or of its odd and even 16-lane rows.
+template <int X>
+__device__ __forceinline__ unsigned lane_xor_swap(unsigned v) {
+    static_assert(X == 16 || X == 32, "16 or 32");
+    const int lane = threadIdx.x & 63;
+    if (X == 32) {
+        const auto r = __builtin_amdgcn_permlane32_swap(v, v, false, false);
+        return lane < 32 ? r[1] : r[0];
+    } else {
+        const auto r = __builtin_amdgcn_permlane16_swap(v, v, false, false);
+        return (lane & 16) ? r[0] : r[1];
+    }
+}
+template <int X>
+__device__ __forceinline__ float lane_xor_f32(float v) {
+    return __uint_as_float(lane_xor_swap<X>(__float_as_uint(v)));
+}
+
 template <typename TS, int NCH>
 __global__ __launch_bounds__(256 * NCH) void cell_fine4_kernel(CellArgs a) {
     constexpr int NW = 4 * NCH;               // wavefronts
@@ -1158,7 +1177,11 @@ __global__ __launch_bounds__(256 * NCH) void cell_fine4_kernel(CellArgs a) {
 #pragma unroll 4
         for (int c2 = share * len; c2 < c1; ++c2)
             beaten += outranks_n(score_key(s_sc[g][c2]), c2, kown, l);
-        for (int off = nbp; off < 64; off <<= 1)
+        if (nbp <= 16)
+            beaten += (int)lane_xor_swap<16>((unsigned)beaten);
+        if (nbp <= 32)
+            beaten += (int)lane_xor_swap<32>((unsigned)beaten);
+        for (int off = nbp; off < 16; off <<= 1)
             beaten += __shfl_xor(beaten, off, 64);
         // kept when fewer than nb - K blocks of the slice outrank it
         const bool mine = lane < nb && beaten < nb - K;  // lanes below nbp: share 0, l = lane
@@ -1197,8 +1220,8 @@ __global__ __launch_bounds__(256 * NCH) void cell_fine4_kernel(CellArgs a) {
     }
 #pragma unroll
     for (int k = 0; k < RPW; ++k) {  // the 64-lane butterfly's sum in lane 0
-        rs[k] = rs[k] + shfl_xor_f32(rs[k], 32);
-        rs[k] = rs[k] + shfl_xor_f32(rs[k], 16);
+        rs[k] = rs[k] + lane_xor_f32<32>(rs[k]);
+        rs[k] = rs[k] + lane_xor_f32<16>(rs[k]);
         rs[k] = rs[k] + row_down_f32<8>(rs[k]);
         rs[k] = rs[k] + row_down_f32<4>(rs[k]);
         rs[k] = rs[k] + row_down_f32<2>(rs[k]);
