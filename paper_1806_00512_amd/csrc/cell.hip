@@ -736,68 +736,102 @@ __global__ __launch_bounds__(64) void cell_fine_kernel(CellArgs a) {
     }
 }
 
-// db[r] (+)= sum over steps [t0, t1) of the row sums of the steps where r's
-// slice was kept (all steps when idx is NULL), steps in decreasing order.
 // db[r] (+)= the sum over steps t = t1 - 1 down to t0 (fp32, in that order)
 // of row r's sum at step t (its chunk sums in chunk order) when the row's
-// slice is kept at t.  The loads of BS steps are issued together; with
-// EMAX / CMAX > 0 the kept-slice entries of the row's region (at most EMAX)
-// and its chunk sums (at most CMAX) are read in unrolled loops.
-template <int EMAX, int CMAX, int BS = 16>
-__global__ __launch_bounds__(64) void bias_grad_kernel(float *db, const float *chunk_rs, int nch,
-                                                       long G, int t0, int t1, const int32_t *idx,
-                                                       int kept, int P, int R, int S, int accumulate) {
-    const long r = blockIdx.x * 64L + threadIdx.x;
-    if (r >= G)
-        return;
-    const long j = r / P;
+// slice is kept at t (every step when idx is NULL).  Work-group x covers rows
+// 64x .. 64x + 63, one per lane; its BG_WAVES wavefronts share out the steps
+// of a pass of up to 64 (wavefront w: the pass's steps w, w + BG_WAVES, ...),
+// so the loads of all of them are in flight together, and put each step's
+// term in LDS (-0.0 when the slice was dropped, which adds nothing to any
+// value); wavefront 0 then adds the pass's terms in decreasing step order.
+// With EMAX / CMAX > 0 the kept-slice entries of the row's region (at most
+// EMAX) and its chunk sums (at most CMAX) are read in unrolled loops.
+constexpr int BG_WAVES = 8;
+
+// Row r's term at step t of the bias gradient: its sum at step t (chunk sums
+// in chunk order) when valid and its slice j is kept (every step when idx is
+// NULL), else -0.0, which adds nothing to any value.  r and t must be in
+// range also when not valid: the unrolled loops load unconditionally, from
+// clamped positions, so that the loads of all steps are in flight together.
+template <int EMAX, int CMAX, bool IDX>
+__device__ __forceinline__ float bias_term(const float *chunk_rs, int nch, long G, long r, int t,
+                                           bool valid, const int32_t *idx, int kept, long eb,
+                                           int e1, long j) {
+    const float *q = chunk_rs + ((long)t * G + r) * nch;
+    float rs;
+    if constexpr (CMAX > 0) {
+        float qv[CMAX];
+#pragma unroll
+        for (int cc = 0; cc < CMAX; ++cc)
+            qv[cc] = q[min(cc, nch - 1)];
+        rs = qv[0];
+#pragma unroll
+        for (int cc = 1; cc < CMAX; ++cc)
+            if (cc < nch)
+                rs += qv[cc];
+    } else {
+        rs = q[0];
+        for (int cc = 1; cc < nch; ++cc)
+            rs += q[cc];
+    }
+    int hit = IDX ? 0 : 1;
+    if constexpr (IDX) {  // e1 >= 1: the row's region has kept entries
+        const int32_t *it = idx + (long)t * kept + eb;
+        if constexpr (EMAX > 0) {
+            int32_t iv[EMAX];
+#pragma unroll
+            for (int e = 0; e < EMAX; ++e)
+                iv[e] = it[min(e, e1 - 1)];
+#pragma unroll
+            for (int e = 0; e < EMAX; ++e)
+                hit |= (e < e1 && iv[e] == j) ? 1 : 0;
+        } else {
+            for (int e = 0; e < e1; ++e)
+                hit |= it[e] == j ? 1 : 0;
+        }
+    }
+    return (valid && hit) ? rs : -0.f;
+}
+
+
+template <int EMAX, int CMAX, bool IDX>
+__global__ __launch_bounds__(64 * BG_WAVES) void bias_grad_kernel(float *db, const float *chunk_rs,
+                                                                  int nch, long G, int t0, int t1,
+                                                                  const int32_t *idx, int kept, int P,
+                                                                  int R, int S, int accumulate) {
+    constexpr int SPW = 64 / BG_WAVES;  // steps per wavefront and pass
+    __shared__ float s_x[64][64];       // [step of the pass][row]
+    const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+    const long r = blockIdx.x * 64L + lane;
+    const bool in = r < G;
+    const long rc = in ? r : G - 1;  // lanes past G read row G - 1's data
+    const long j = rc / P;
     const int ks = R - S;
     const long eb = (j / R) * ks;
     const int e1 = (int)min((long)ks, kept - eb);
-    float acc = accumulate ? db[r] : 0.f;
-    for (int tb = t1 - 1; tb >= t0; tb -= BS) {
-        float rsv[BS];
-        bool kp[BS];
+    float acc = (w == 0 && in && accumulate) ? db[r] : 0.f;
+    for (int tb = t1 - 1; tb >= t0; tb -= 64) {
+        float x[SPW];
 #pragma unroll
-        for (int u = 0; u < BS; ++u) {
-            const int t = tb - u;
-            rsv[u] = 0.f;
-            kp[u] = false;
-            if (t < t0)
-                continue;
-            const float *q = chunk_rs + ((long)t * G + r) * nch;
-            float rs = q[0];
-            if constexpr (CMAX > 0) {
-#pragma unroll
-                for (int cc = 1; cc < CMAX; ++cc)
-                    if (cc < nch)
-                        rs += q[cc];
-            } else {
-                for (int cc = 1; cc < nch; ++cc)
-                    rs += q[cc];
-            }
-            bool keep = idx == nullptr;
-            if (!keep) {
-                const int32_t *it = idx + (long)t * kept + eb;
-                if constexpr (EMAX > 0) {
-#pragma unroll
-                    for (int e = 0; e < EMAX; ++e)
-                        if (e < e1)
-                            keep |= it[e] == j;
-                } else {
-                    for (int e = 0; e < e1; ++e)
-                        keep |= it[e] == j;
-                }
-            }
-            rsv[u] = rs;
-            kp[u] = keep;
+        for (int k = 0; k < SPW; ++k) {
+            const int t = tb - (w + BG_WAVES * k);
+            const bool valid = t >= t0 && in;
+            x[k] = bias_term<EMAX, CMAX, IDX>(chunk_rs, nch, G, rc, t >= t0 ? t : t0, valid, idx, kept,
+                                         eb, e1, j);
         }
 #pragma unroll
-        for (int u = 0; u < BS; ++u)
-            if (kp[u])
-                acc += rsv[u];
+        for (int k = 0; k < SPW; ++k)
+            s_x[w + BG_WAVES * k][lane] = x[k];
+        __syncthreads();
+        if (w == 0) {
+            const int n = min(64, tb - t0 + 1);
+            for (int i = 0; i < n; ++i)
+                acc += s_x[i][lane];
+        }
+        __syncthreads();
     }
-    db[r] = acc;
+    if (w == 0 && in)
+        db[r] = acc;
 }
 
 __global__ void fill_kernel(float *p, long n, float v) {
@@ -1298,13 +1332,20 @@ hipError_t launch_cell_fine(const CellArgs &a, int mode, bool bf16, hipStream_t 
 hipError_t launch_bias_grad(float *db, const float *chunk_rs, int nch, long G, int t0, int t1,
                             const int32_t *idx, int kept, int P, int R, int S, bool accumulate,
                             hipStream_t s) {
-    const dim3 grid((unsigned)ceil_div(G, 64)), blk(64);
-    if ((!idx || R - S <= 8) && nch <= 4)
-        hipLaunchKernelGGL((bias_grad_kernel<8, 4>), grid, blk, 0, s, db, chunk_rs, nch, G, t0, t1,
-                           idx, kept, P, R, S, accumulate ? 1 : 0);
+    const dim3 grid((unsigned)ceil_div(G, 64)), blk(64 * BG_WAVES);
+    const bool unrolled = (!idx || R - S <= 8) && nch <= 4;
+#define LSTMSS_BG(E, C, I)                                                                        \
+    hipLaunchKernelGGL((bias_grad_kernel<E, C, I>), grid, blk, 0, s, db, chunk_rs, nch, G, t0, t1, \
+                       idx, kept, P, R, S, accumulate ? 1 : 0)
+    if (unrolled && idx)
+        LSTMSS_BG(8, 4, true);
+    else if (unrolled)
+        LSTMSS_BG(8, 4, false);
+    else if (idx)
+        LSTMSS_BG(0, 0, true);
     else
-        hipLaunchKernelGGL((bias_grad_kernel<0, 0>), grid, blk, 0, s, db, chunk_rs, nch, G, t0, t1,
-                           idx, kept, P, R, S, accumulate ? 1 : 0);
+        LSTMSS_BG(0, 0, false);
+#undef LSTMSS_BG
     return hipGetLastError();
 }
 
