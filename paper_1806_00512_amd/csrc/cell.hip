@@ -388,6 +388,68 @@ __global__ __launch_bounds__(RK_WAVES * 64) void cell_rows_kernel(CellArgs a) {
     }
 }
 
+// Lane i receives lane i + N of its 16-lane row (a DPP row shift; lanes
+// whose source leaves the row receive 0).  Used for the steps off = 8, 4, 2,
+// 1 of a butterfly (each lane adds the value of lane i ^ off to its own):
+// the lanes that feed the first lane of an aligned group of 2 off lanes have
+// i ^ off = i + off, so that first lane gets the butterfly's bits.
+template <int N>
+__device__ __forceinline__ float row_down_f32(float v) {
+    return __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), 0x100 + N, 0xf, 0xf, true));
+}
+template <int N>
+__device__ __forceinline__ double row_down_f64(double v) {
+    const long long x = __double_as_longlong(v);
+    const int lo = __builtin_amdgcn_update_dpp(0, (int)(x & 0xffffffffLL), 0x100 + N, 0xf, 0xf, true);
+    const int hi = __builtin_amdgcn_update_dpp(0, (int)(x >> 32), 0x100 + N, 0xf, 0xf, true);
+    return __longlong_as_double(((long long)hi << 32) | (unsigned int)lo);
+}
+
+// Lane i receives lane i ^ 32 (X = 32) or lane i ^ 16 (X = 16): the swap of
+// the two halves of the wavefront, or of its odd and even 16-lane rows.
+template <int X>
+__device__ __forceinline__ unsigned lane_xor_swap(unsigned v) {
+    static_assert(X == 16 || X == 32, "16 or 32");
+    const int lane = threadIdx.x & 63;
+    if (X == 32) {
+        const auto r = __builtin_amdgcn_permlane32_swap(v, v, false, false);
+        return lane < 32 ? r[1] : r[0];
+    } else {
+        const auto r = __builtin_amdgcn_permlane16_swap(v, v, false, false);
+        return (lane & 16) ? r[0] : r[1];
+    }
+}
+template <int X>
+__device__ __forceinline__ float lane_xor_f32(float v) {
+    return __uint_as_float(lane_xor_swap<X>(__float_as_uint(v)));
+}
+
+template <int X>
+__device__ __forceinline__ double lane_xor_f64(double v) {
+    const long long x = __double_as_longlong(v);
+    const unsigned lo = lane_xor_swap<X>((unsigned)(x & 0xffffffffLL));
+    const unsigned hi = lane_xor_swap<X>((unsigned)((unsigned long long)x >> 32));
+    return __longlong_as_double((long long)(((unsigned long long)hi << 32) | lo));
+}
+
+// Step OFF of a 64-lane butterfly, for the lanes that feed lane 0 (and the
+// first lane of every aligned group of 2 OFF lanes): the value of lane
+// i ^ OFF, moved by lane swaps (OFF = 32, 16) or DPP row shifts (OFF <= 8).
+template <int OFF>
+__device__ __forceinline__ float bfly_f32(float v) {
+    if constexpr (OFF >= 16)
+        return lane_xor_f32<OFF>(v);
+    else
+        return row_down_f32<OFF>(v);
+}
+template <int OFF>
+__device__ __forceinline__ double bfly_f64(double v) {
+    if constexpr (OFF >= 16)
+        return lane_xor_f64<OFF>(v);
+    else
+        return row_down_f64<OFF>(v);
+}
+
 // ---------------------------------------------------------------------------
 // Split variant for large shapes, two kernels per step.
 //
@@ -476,24 +538,33 @@ __global__ __launch_bounds__(EK_WAVES * 64) void cell_elem_kernel(CellArgs a) {
                     st<TS>::store(dbg, r * B + b, v[g]);
             }
         }
+        // per row the 64-lane butterflies' sums (lane 0's bits)
+        double q[4];
+        float rs[4];
 #pragma unroll
         for (int g = 0; g < 4; ++g) {
             const float x = ok[k] ? v[g] : 0.f;
-            double q = (double)x * (double)x;
-            float rs = x;
+            q[g] = (double)x * (double)x;
+            rs[g] = x;
+        }
+#define LSTMSS_EK_STEP(O)                                                                          \
+    _Pragma("unroll") for (int g = 0; g < 4; ++g) {                                               \
+        if (SPARSE)                                                                               \
+            q[g] = q[g] + bfly_f64<O>(q[g]);                                                      \
+        if (!GIVEN)                                                                               \
+            rs[g] = rs[g] + bfly_f32<O>(rs[g]);                                                   \
+    }
+        LSTMSS_EK_STEP(32) LSTMSS_EK_STEP(16) LSTMSS_EK_STEP(8)
+        LSTMSS_EK_STEP(4) LSTMSS_EK_STEP(2) LSTMSS_EK_STEP(1)
+#undef LSTMSS_EK_STEP
+        if (lane == 0 && u < H) {
 #pragma unroll
-            for (int off = 32; off >= 1; off >>= 1) {
-                if (SPARSE)
-                    q = q + shfl_xor_f64(q, off);
-                if (!GIVEN)
-                    rs += shfl_xor_f32(rs, off);
-            }
-            if (lane == 0 && u < H) {
+            for (int g = 0; g < 4; ++g) {
                 const long r = (long)g * H + u;
                 if (SPARSE)
-                    a.chunk_sq[r * nch + c] = q;
+                    a.chunk_sq[r * nch + c] = q[g];
                 if (!GIVEN)
-                    a.chunk_rs[r * nch + c] = rs;
+                    a.chunk_rs[r * nch + c] = rs[g];
             }
         }
     }
@@ -1046,42 +1117,6 @@ __global__ __launch_bounds__(256) void cell_fine32_kernel(CellArgs a) {
 // chunks in order, then over the 64 lanes, and added to db.  Values, scores,
 // the order of every sum and the selection are those of the element kernel
 // followed by cell_fine_kernel<TS, FS_STAGE, 4>.
-// Lane i receives lane i + N of its 16-lane row (a DPP row shift; lanes
-// whose source leaves the row receive 0).  Used for the steps off = 8, 4, 2,
-// 1 of a butterfly (each lane adds the value of lane i ^ off to its own):
-// the lanes that feed the first lane of an aligned group of 2 off lanes have
-// i ^ off = i + off, so that first lane gets the butterfly's bits.
-template <int N>
-__device__ __forceinline__ float row_down_f32(float v) {
-    return __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), 0x100 + N, 0xf, 0xf, true));
-}
-template <int N>
-__device__ __forceinline__ double row_down_f64(double v) {
-    const long long x = __double_as_longlong(v);
-    const int lo = __builtin_amdgcn_update_dpp(0, (int)(x & 0xffffffffLL), 0x100 + N, 0xf, 0xf, true);
-    const int hi = __builtin_amdgcn_update_dpp(0, (int)(x >> 32), 0x100 + N, 0xf, 0xf, true);
-    return __longlong_as_double(((long long)hi << 32) | (unsigned int)lo);
-}
-
-// Lane i receives lane i ^ 32 (X = 32) or lane i ^ 16 (X = 16): the swap of
-// the two halves of the wavefront, or of its odd and even 16-lane rows.
-template <int X>
-__device__ __forceinline__ unsigned lane_xor_swap(unsigned v) {
-    static_assert(X == 16 || X == 32, "16 or 32");
-    const int lane = threadIdx.x & 63;
-    if (X == 32) {
-        const auto r = __builtin_amdgcn_permlane32_swap(v, v, false, false);
-        return lane < 32 ? r[1] : r[0];
-    } else {
-        const auto r = __builtin_amdgcn_permlane16_swap(v, v, false, false);
-        return (lane & 16) ? r[0] : r[1];
-    }
-}
-template <int X>
-__device__ __forceinline__ float lane_xor_f32(float v) {
-    return __uint_as_float(lane_xor_swap<X>(__float_as_uint(v)));
-}
-
 template <typename TS, int NCH>
 __global__ __launch_bounds__(256 * NCH) void cell_fine4_kernel(CellArgs a) {
     constexpr int NW = 4 * NCH;               // wavefronts
