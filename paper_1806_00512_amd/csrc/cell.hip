@@ -618,10 +618,12 @@ __global__ __launch_bounds__(64) void cell_select_kernel2(CellArgs a) {
 #pragma unroll
             for (int u = 0; u < 8; ++u) {
                 const int v = v0 + u * 64 + lane;
+                uint4 x = make_uint4(0, 0, 0, 0);
                 if (v < nv) {
                     const int q = v / sv, r = v - q * sv;  // local slot, vector within it
-                    buf[u] = src[(long)sinv[q] * sv + r];
+                    x = src[(long)sinv[q] * sv + r];
                 }
+                buf[u] = x;
             }
 #pragma unroll
             for (int u = 0; u < 8; ++u) {

@@ -567,6 +567,29 @@ __global__ __launch_bounds__(NW * 64) void gemm1_kernel(Gemm1Args a) {
         buf ^= 1;
     }
 
+    // SEL: compacted rows.  The split's rows are shared out over its
+    // m-tiles, each work-group copying its share (its columns) from the
+    // staging matrix after its product, so that no stage waits for these
+    // stores; the first pieces are loaded before the partial sums are
+    // stored, so that waiting for them does not wait for those stores.
+    constexpr int PPR = TN / PEL;  // 16-byte pieces per tile row
+    constexpr int CPB = SEL ? 2 : 1;
+    uint4 cbuf[CPB];
+    int c_r0 = 0, c_np = 0;
+    if constexpr (SEL) {
+        const int nr = ke0 - kb, nmt = (int)gridDim.x;
+        c_r0 = (int)((long)nr * blockIdx.x / nmt);
+        c_np = ((int)((long)nr * (blockIdx.x + 1) / nmt) - c_r0) * PPR;
+#pragma unroll
+        for (int i = 0; i < CPB; ++i) {
+            const int e = tid + i * THREADS;
+            const int k = kb + c_r0 + e / PPR, n = n0 + (e % PPR) * PEL;
+            cbuf[i] = make_uint4(0, 0, 0, 0);
+            if (e < c_np && n < N)
+                cbuf[i] = *(const uint4 *)(G + (long)srow[k - sc] * N + n);
+        }
+    }
+
     float *out = a.part + step * a.out_step + split * a.part_stride;
 #pragma unroll
     for (int i = 0; i < MT; ++i)
@@ -581,15 +604,16 @@ __global__ __launch_bounds__(NW * 64) void gemm1_kernel(Gemm1Args a) {
             }
         }
     if constexpr (SEL) {
-        // compacted rows: the split's rows are shared out over its m-tiles,
-        // each work-group copying its share (its columns) from the staging
-        // matrix, last, so that no stage waits for these stores
-        constexpr int PPR = TN / PEL;  // 16-byte pieces per tile row
-        const int nr = ke0 - kb, nmt = (int)gridDim.x;
-        const int r0 = (int)((long)nr * blockIdx.x / nmt), r1 = (int)((long)nr * (blockIdx.x + 1) / nmt);
         TS *gc = (TS *)a.sel_gc;
-        for (int e = tid; e < (r1 - r0) * PPR; e += THREADS) {
-            const int k = kb + r0 + e / PPR, n = n0 + (e % PPR) * PEL;
+#pragma unroll
+        for (int i = 0; i < CPB; ++i) {
+            const int e = tid + i * THREADS;
+            const int k = kb + c_r0 + e / PPR, n = n0 + (e % PPR) * PEL;
+            if (e < c_np && n < N)
+                *(uint4 *)(gc + (long)k * N + n) = cbuf[i];
+        }
+        for (int e = tid + CPB * THREADS; e < c_np; e += THREADS) {
+            const int k = kb + c_r0 + e / PPR, n = n0 + (e % PPR) * PEL;
             if (n < N)
                 *(uint4 *)(gc + (long)k * N + n) = *(const uint4 *)(G + (long)srow[k - sc] * N + n);
         }

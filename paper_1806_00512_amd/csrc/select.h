@@ -30,14 +30,36 @@ struct SliceSel {
 // Score of slice j: the chunk sums of each of its P rows added in chunk
 // order, then the rows in order (chunk_sq is [rows][nch], row r of slice j
 // being j * P + p).
+// The slice's P nch sums are contiguous; up to 16 of them are loaded at once
+// (from clamped positions) and folded in the same order.
 __device__ __forceinline__ double slice_score(const double *__restrict__ chunk_sq, int nch, long j,
                                               int P) {
+    const int L = P * nch;
+    const double *q = chunk_sq + j * L;
+    if (L <= 16) {
+        double v[16];
+#pragma unroll
+        for (int e = 0; e < 16; ++e)
+            v[e] = q[min(e, L - 1)];
+        double sc = 0.0, rs = 0.0;
+        int end = nch - 1;  // last entry of the current row
+#pragma unroll
+        for (int e = 0; e < 16; ++e) {
+            const bool in = e < L, start = e == end - nch + 1;
+            rs = !in ? rs : start ? v[e] : rs + v[e];
+            if (in && e == end) {  // row e / nch complete
+                sc = e == nch - 1 ? rs : sc + rs;
+                end += nch;
+            }
+        }
+        return sc;
+    }
     double sc = 0.0;
     for (int p = 0; p < P; ++p) {
-        const double *q = chunk_sq + (j * P + p) * nch;
-        double rs = q[0];
+        const double *qr = q + p * nch;
+        double rs = qr[0];
         for (int c = 1; c < nch; ++c)
-            rs = rs + q[c];
+            rs = rs + qr[c];
         sc = p == 0 ? rs : sc + rs;
     }
     return sc;
@@ -63,12 +85,12 @@ __device__ __forceinline__ SliceSel rank_slices(double sc, long j0, int nsl, int
     const int ls = valid ? (int)((gj / R) * R - j0) : 0;
     const int rlen = valid ? (int)min((long)R, nslices - (j0 + ls)) : 0;
     const int nkeep = rlen - (S * rlen) / R;
-    int beaten = 0;
+    int beaten = 0;  // a slice never outranks itself
+#pragma unroll 8
     for (int i = 0; i < R; ++i) {
         const int src = (ls + i) & 63;
         const uint64_t ki = (uint64_t)__shfl((long long)kj, src, 64);
-        if (i < rlen && src != j && outranks(ki, src, kj, j))
-            ++beaten;
+        beaten += i < rlen ? outranks_n(ki, src, kj, j) : 0;
     }
     const bool keep = valid && beaten < nkeep;
     const uint64_t ball = __ballot(keep);
