@@ -200,6 +200,103 @@ __global__ __launch_bounds__(CELL_THREADS) void cell_select_kernel(CellArgs a) {
     (void)G;
 }
 
+// Lane i receives lane i + N of its 16-lane row (a DPP row shift; lanes
+// whose source leaves the row receive 0).  Used for the steps off = 8, 4, 2,
+// 1 of a butterfly (each lane adds the value of lane i ^ off to its own):
+// the lanes that feed the first lane of an aligned group of 2 off lanes have
+// i ^ off = i + off, so that first lane gets the butterfly's bits.
+template <int N>
+__device__ __forceinline__ float row_down_f32(float v) {
+    return __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), 0x100 + N, 0xf, 0xf, true));
+}
+template <int N>
+__device__ __forceinline__ double row_down_f64(double v) {
+    const long long x = __double_as_longlong(v);
+    const int lo = __builtin_amdgcn_update_dpp(0, (int)(x & 0xffffffffLL), 0x100 + N, 0xf, 0xf, true);
+    const int hi = __builtin_amdgcn_update_dpp(0, (int)(x >> 32), 0x100 + N, 0xf, 0xf, true);
+    return __longlong_as_double(((long long)hi << 32) | (unsigned int)lo);
+}
+
+// Lane i receives lane i ^ 32 (X = 32) or lane i ^ 16 (X = 16): the swap of
+// the two halves of the wavefront, or of its odd and even 16-lane rows.
+template <int X>
+__device__ __forceinline__ unsigned lane_xor_swap(unsigned v) {
+    static_assert(X == 16 || X == 32, "16 or 32");
+    const int lane = threadIdx.x & 63;
+    if (X == 32) {
+        const auto r = __builtin_amdgcn_permlane32_swap(v, v, false, false);
+        return lane < 32 ? r[1] : r[0];
+    } else {
+        const auto r = __builtin_amdgcn_permlane16_swap(v, v, false, false);
+        return (lane & 16) ? r[0] : r[1];
+    }
+}
+template <int X>
+__device__ __forceinline__ float lane_xor_f32(float v) {
+    return __uint_as_float(lane_xor_swap<X>(__float_as_uint(v)));
+}
+
+template <int X>
+__device__ __forceinline__ double lane_xor_f64(double v) {
+    const long long x = __double_as_longlong(v);
+    const unsigned lo = lane_xor_swap<X>((unsigned)(x & 0xffffffffLL));
+    const unsigned hi = lane_xor_swap<X>((unsigned)((unsigned long long)x >> 32));
+    return __longlong_as_double((long long)(((unsigned long long)hi << 32) | lo));
+}
+
+// Step OFF of a 64-lane butterfly, for the lanes that feed lane 0 (and the
+// first lane of every aligned group of 2 OFF lanes): the value of lane
+// i ^ OFF, moved by lane swaps (OFF = 32, 16) or DPP row shifts (OFF <= 8).
+template <int OFF>
+__device__ __forceinline__ float bfly_f32(float v) {
+    if constexpr (OFF >= 16)
+        return lane_xor_f32<OFF>(v);
+    else
+        return row_down_f32<OFF>(v);
+}
+template <int OFF>
+__device__ __forceinline__ double bfly_f64(double v) {
+    if constexpr (OFF >= 16)
+        return lane_xor_f64<OFF>(v);
+    else
+        return row_down_f64<OFF>(v);
+}
+
+// The sum a W-lane xor butterfly (offsets W / 2, ..., 1) leaves in the first
+// lane of every aligned group of W lanes (the other lanes hold partial sums).
+template <int W>
+__device__ __forceinline__ double lead_sum_f64(double v) {
+    if constexpr (W >= 64)
+        v = v + bfly_f64<32>(v);
+    if constexpr (W >= 32)
+        v = v + bfly_f64<16>(v);
+    if constexpr (W >= 16)
+        v = v + bfly_f64<8>(v);
+    if constexpr (W >= 8)
+        v = v + bfly_f64<4>(v);
+    if constexpr (W >= 4)
+        v = v + bfly_f64<2>(v);
+    if constexpr (W >= 2)
+        v = v + bfly_f64<1>(v);
+    return v;
+}
+template <int W>
+__device__ __forceinline__ float lead_sum_f32(float v) {
+    if constexpr (W >= 64)
+        v = v + bfly_f32<32>(v);
+    if constexpr (W >= 32)
+        v = v + bfly_f32<16>(v);
+    if constexpr (W >= 16)
+        v = v + bfly_f32<8>(v);
+    if constexpr (W >= 8)
+        v = v + bfly_f32<4>(v);
+    if constexpr (W >= 4)
+        v = v + bfly_f32<2>(v);
+    if constexpr (W >= 2)
+        v = v + bfly_f32<1>(v);
+    return v;
+}
+
 // ---------------------------------------------------------------------------
 // Register-resident variant for small work-groups (<= 32 rows, <= 32 slices,
 // B <= 256): a row is owned by LPR lanes (the next power of two >= B, at most
@@ -304,17 +401,13 @@ __global__ __launch_bounds__(RK_WAVES * 64) void cell_rows_kernel(CellArgs a) {
             v[p][j] = val;
             rsum[p] += val;
             if (MODE != CELL_DENSE) {
-                // chunk j of the row: xor butterfly, then fold into the row
-                double q = (double)val * (double)val;
-#pragma unroll
-                for (int off = LPR >> 1; off >= 1; off >>= 1)
-                    q = q + shfl_xor_f64(q, off);
+                // chunk j of the row: the LPR-lane butterfly's sum in the
+                // row's first lane, then fold into the row
+                const double q = lead_sum_f64<LPR>((double)val * (double)val);
                 part[p] = j == 0 ? q : part[p] + q;
             }
         }
-#pragma unroll
-        for (int off = LPR >> 1; off >= 1; off >>= 1)
-            rsum[p] += shfl_xor_f32(rsum[p], off);
+        rsum[p] = lead_sum_f32<LPR>(rsum[p]);  // used by the row's first lane
         if (sl == 0 && lr < nrows) {
             if (MODE == CELL_DENSE) {
                 if (a.db)
@@ -341,29 +434,11 @@ __global__ __launch_bounds__(RK_WAVES * 64) void cell_rows_kernel(CellArgs a) {
             if (a.scores)
                 a.scores[j0 + j] = sc;
         }
-        const uint64_t kj = score_key(sc);
-        const long gj = j0 + j;
-        const long rs = (gj / R) * R;
-        const int ls = (int)(rs - j0);
-        const int rlen = (int)min((long)R, a.nslices - rs);
-        const int nkeep = rlen - (a.S * rlen) / R;
-        int beaten = 0;
-        for (int i = 0; i < 32; ++i) {
-            const uint64_t ki = (uint64_t)__shfl((long long)kj, i, 64);
-            if (valid && i != j && i >= ls && i < ls + rlen && i < nsl && outranks(ki, i, kj, j))
-                ++beaten;
-        }
-        const bool keep = valid && beaten < nkeep;
-        const uint64_t ball = __ballot(keep);
-        const uint64_t below = ((j ? (~0ull >> (64 - j)) : 0ull)) & ~((ls ? (~0ull >> (64 - ls)) : 0ull));
-        const int pos = __popcll(ball & below);
-        int slot = -1;
-        if (keep) {
-            slot = (int)((gj / R) * (R - a.S) + pos);
-            a.idx[slot] = (int32_t)gj;
-        }
+        const SliceSel sel = rank_slices(sc, j0, nsl, R, a.S, a.nslices);
+        if (sel.slot >= 0)
+            a.idx[sel.slot] = (int32_t)(j0 + j);
         if (valid)
-            sslot[j] = slot;
+            sslot[j] = sel.slot;
     }
     __syncthreads();
 
@@ -386,68 +461,6 @@ __global__ __launch_bounds__(RK_WAVES * 64) void cell_rows_kernel(CellArgs a) {
         if (sl == 0 && a.db)
             a.db[row0 + lr] += rsum[p];
     }
-}
-
-// Lane i receives lane i + N of its 16-lane row (a DPP row shift; lanes
-// whose source leaves the row receive 0).  Used for the steps off = 8, 4, 2,
-// 1 of a butterfly (each lane adds the value of lane i ^ off to its own):
-// the lanes that feed the first lane of an aligned group of 2 off lanes have
-// i ^ off = i + off, so that first lane gets the butterfly's bits.
-template <int N>
-__device__ __forceinline__ float row_down_f32(float v) {
-    return __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), 0x100 + N, 0xf, 0xf, true));
-}
-template <int N>
-__device__ __forceinline__ double row_down_f64(double v) {
-    const long long x = __double_as_longlong(v);
-    const int lo = __builtin_amdgcn_update_dpp(0, (int)(x & 0xffffffffLL), 0x100 + N, 0xf, 0xf, true);
-    const int hi = __builtin_amdgcn_update_dpp(0, (int)(x >> 32), 0x100 + N, 0xf, 0xf, true);
-    return __longlong_as_double(((long long)hi << 32) | (unsigned int)lo);
-}
-
-// Lane i receives lane i ^ 32 (X = 32) or lane i ^ 16 (X = 16): the swap of
-// the two halves of the wavefront, or of its odd and even 16-lane rows.
-template <int X>
-__device__ __forceinline__ unsigned lane_xor_swap(unsigned v) {
-    static_assert(X == 16 || X == 32, "16 or 32");
-    const int lane = threadIdx.x & 63;
-    if (X == 32) {
-        const auto r = __builtin_amdgcn_permlane32_swap(v, v, false, false);
-        return lane < 32 ? r[1] : r[0];
-    } else {
-        const auto r = __builtin_amdgcn_permlane16_swap(v, v, false, false);
-        return (lane & 16) ? r[0] : r[1];
-    }
-}
-template <int X>
-__device__ __forceinline__ float lane_xor_f32(float v) {
-    return __uint_as_float(lane_xor_swap<X>(__float_as_uint(v)));
-}
-
-template <int X>
-__device__ __forceinline__ double lane_xor_f64(double v) {
-    const long long x = __double_as_longlong(v);
-    const unsigned lo = lane_xor_swap<X>((unsigned)(x & 0xffffffffLL));
-    const unsigned hi = lane_xor_swap<X>((unsigned)((unsigned long long)x >> 32));
-    return __longlong_as_double((long long)(((unsigned long long)hi << 32) | lo));
-}
-
-// Step OFF of a 64-lane butterfly, for the lanes that feed lane 0 (and the
-// first lane of every aligned group of 2 OFF lanes): the value of lane
-// i ^ OFF, moved by lane swaps (OFF = 32, 16) or DPP row shifts (OFF <= 8).
-template <int OFF>
-__device__ __forceinline__ float bfly_f32(float v) {
-    if constexpr (OFF >= 16)
-        return lane_xor_f32<OFF>(v);
-    else
-        return row_down_f32<OFF>(v);
-}
-template <int OFF>
-__device__ __forceinline__ double bfly_f64(double v) {
-    if constexpr (OFF >= 16)
-        return lane_xor_f64<OFF>(v);
-    else
-        return row_down_f64<OFF>(v);
 }
 
 // ---------------------------------------------------------------------------
