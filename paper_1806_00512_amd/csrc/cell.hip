@@ -5,6 +5,8 @@
 // Paper: section 3 (coarse-grained structural sparsifying of the gate
 // gradient dnet, offset index array of the kept slices); the gate-gradient
 // data flow is the one of Fig. 1 for the standard LSTM cell.
+#include <type_traits>
+
 #include "common.h"
 #include "kernels.h"
 #include "select.h"
@@ -1057,12 +1059,43 @@ __global__ __launch_bounds__(256) void cell_fine32_kernel(CellArgs a) {
                 }
             }
             vals[p][jj] = val;
-            if (64 * jj < B) {  // this row's block sums of the chunk
-                double q = (double)val * (double)val;
-                for (int off = My >> 1; off >= 1; off >>= 1)
-                    q = q + shfl_xor_f64(q, off);
-                if ((lane & (My - 1)) == 0 && (64 * jj + lane) / My < nb)
-                    s_blk[wave * RPW + p][(64 * jj + lane) / My] = q;
+        }
+    }
+    // this wavefront's rows' block sums (the My-lane butterfly's sum in each
+    // block's first lane; columns past B add zero), all rows and chunks
+    // interleaved
+    {
+        double q[RPW][NJ];
+#pragma unroll
+        for (int p = 0; p < RPW; ++p)
+#pragma unroll
+            for (int jj = 0; jj < NJ; ++jj)
+                q[p][jj] = (double)vals[p][jj] * (double)vals[p][jj];
+        auto sums = [&](auto w) {
+            constexpr int W = decltype(w)::value;
+#pragma unroll
+            for (int p = 0; p < RPW; ++p)
+#pragma unroll
+                for (int jj = 0; jj < NJ; ++jj)
+                    if (64 * jj < B)
+                        q[p][jj] = lead_sum_f64<W>(q[p][jj]);
+        };
+        switch (My) {
+        case 2: sums(std::integral_constant<int, 2>()); break;
+        case 4: sums(std::integral_constant<int, 4>()); break;
+        case 8: sums(std::integral_constant<int, 8>()); break;
+        case 16: sums(std::integral_constant<int, 16>()); break;
+        case 32: sums(std::integral_constant<int, 32>()); break;
+        default: sums(std::integral_constant<int, 64>()); break;
+        }
+        const int lmy = __builtin_ctz(My);
+#pragma unroll
+        for (int jj = 0; jj < NJ; ++jj) {
+            const int blk = (64 * jj + lane) >> lmy;
+            if (64 * jj < B && (lane & (My - 1)) == 0 && blk < nb) {
+#pragma unroll
+                for (int p = 0; p < RPW; ++p)
+                    s_blk[wave * RPW + p][blk] = q[p][jj];
             }
         }
     }
@@ -1106,9 +1139,7 @@ __global__ __launch_bounds__(256) void cell_fine32_kernel(CellArgs a) {
             }
         }
         if (SRC != FS_GIVEN && a.db) {
-#pragma unroll
-            for (int off = 32; off >= 1; off >>= 1)
-                rs += shfl_xor_f32(rs, off);
+            rs = lead_sum_f32<64>(rs);  // the 64-lane butterfly's sum in lane 0
             if (lane == 0)
                 a.db[r] += rs;
         }
