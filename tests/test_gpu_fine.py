@@ -83,6 +83,12 @@ def adversarial_fine(H, B, Mx, My, seed, dtype):
     (40, 33, 1, 2, 8 / 17),    # one-row slices, 17 blocks, last block one column
     (16, 256, 16, 4, 0.5),     # 64 blocks per slice (the maximum)
     (24, 7, 4, 8, 0.0),        # one block narrower than My, nothing removed
+    # 32-row slices (the four-wavefront kernel), every block width
+    (64, 128, 32, 16, 0.5),    # 8 blocks
+    (40, 100, 32, 8, 4 / 13),  # 13 blocks, ragged last block and chunk
+    (32, 256, 32, 64, 0.75),   # 4 blocks, one per chunk
+    (16, 96, 32, 4, 0.5),      # 24 blocks
+    (24, 30, 32, 2, 0.4),      # 15 blocks of 2 columns
 ])
 def test_fine_select_bit_exact(L, dtype, H, B, Mx, My, sp):
     dG = adversarial_fine(H, B, Mx, My, H * 13 + B + My, dtype)
