@@ -119,7 +119,8 @@ int32_t lstmss_bwd_info(const lstmss_dims *d, float sparsity, const lstmss_struc
 int64_t lstmss_index_entries(const lstmss_dims *d, float sparsity, const lstmss_structure *s);
 
 /* Workspace bytes needed by lstm_bwd_structsparse with these arguments
- * (sparsity 0 gives the size for lstm_bwd_dense).  <0 on error. */
+ * (sparsity 0 gives a size that serves both lstm_bwd_dense and
+ * lstm_bwd_structsparse at sparsity 0).  <0 on error. */
 int64_t lstmss_workspace_bytes(const lstmss_dims *d, float sparsity, const lstmss_structure *s);
 
 /* Workspace bytes for lstm_fwd_cache's batched path: the fp32 input

@@ -486,8 +486,13 @@ __global__ __launch_bounds__(RK_WAVES * 64) void cell_rows_kernel(CellArgs a) {
 constexpr int EK_UNITS = 4;
 constexpr int EK_WAVES = 4;
 
-template <typename TS, int MODE>
+// FBLK (dense mode, the fine structure with 32-row slices): instead of the
+// chunk row sums, each row's per-block sums of squares (fp64, the My-lane
+// butterfly of the block's squares) and sums (fp32, the same butterfly of its
+// values) go to blk_sq / blk_rs [4H][nb], from each block's first lane.
+template <typename TS, int MODE, bool FBLK = false>
 __global__ __launch_bounds__(EK_WAVES * 64) void cell_elem_kernel(CellArgs a) {
+    static_assert(!FBLK || MODE == CELL_DENSE, "block sums: dense mode");
     constexpr bool SPARSE = MODE != CELL_DENSE, GIVEN = MODE == CELL_GIVEN;
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
     const int B = a.B, H = a.H;
@@ -552,6 +557,43 @@ __global__ __launch_bounds__(EK_WAVES * 64) void cell_elem_kernel(CellArgs a) {
                 if (dbg)
                     st<TS>::store(dbg, r * B + b, v[g]);
             }
+        }
+        if constexpr (FBLK) {
+            double q[4];
+            float rs[4];
+#pragma unroll
+            for (int g = 0; g < 4; ++g) {
+                const float x = ok[k] ? v[g] : 0.f;
+                q[g] = (double)x * (double)x;
+                rs[g] = x;
+            }
+            auto sums = [&](auto w) {
+                constexpr int W = decltype(w)::value;
+#pragma unroll
+                for (int g = 0; g < 4; ++g) {
+                    q[g] = lead_sum_f64<W>(q[g]);
+                    rs[g] = lead_sum_f32<W>(rs[g]);
+                }
+            };
+            const int My = a.My, nb = a.nb;
+            switch (My) {
+            case 2: sums(std::integral_constant<int, 2>()); break;
+            case 4: sums(std::integral_constant<int, 4>()); break;
+            case 8: sums(std::integral_constant<int, 8>()); break;
+            case 16: sums(std::integral_constant<int, 16>()); break;
+            case 32: sums(std::integral_constant<int, 32>()); break;
+            default: sums(std::integral_constant<int, 64>()); break;
+            }
+            const int bi = (64 * c + lane) >> __builtin_ctz(My);
+            if ((lane & (My - 1)) == 0 && bi < nb && u < H) {
+#pragma unroll
+                for (int g = 0; g < 4; ++g) {
+                    const long r = (long)g * H + u;
+                    a.blk_sq[r * nb + bi] = q[g];
+                    a.blk_rs[r * nb + bi] = rs[g];
+                }
+            }
+            continue;
         }
         // per row the 64-lane butterflies' sums (lane 0's bits)
         double q[4];
@@ -1350,6 +1392,72 @@ __global__ __launch_bounds__(256 * NCH) void cell_fine4_kernel(CellArgs a) {
     }
 }
 
+// cell_fine32_sel_kernel: the selection of 32-row slices at large shapes
+// from the element kernel's per-(row, block) sums (blk_sq, blk_rs), one
+// wavefront per slice, lane b holding block b.  A block's score is its rows'
+// sums of squares folded in increasing row order (the same values, in the
+// same order, as cell_fine32_kernel's); a block is kept when fewer than
+// nb - K blocks of the slice outrank it.  The element kernel wrote the gate
+// gradient to dGc; the removed blocks are zeroed there in place.  Each row's
+// bias term is the sum of its kept blocks' sums by the 64-lane butterfly over
+// the blocks (dropped ones add zero), added to db step by step.
+template <typename TS>
+__global__ __launch_bounds__(64) void cell_fine32_sel_kernel(CellArgs a) {
+    constexpr int MX = 32;
+    const int lane = threadIdx.x;
+    const int B = a.B, My = a.My, nb = a.nb, K = a.S;
+    const long j = blockIdx.x;  // slice
+    const long r0 = j * MX;
+    const bool own = lane < nb;
+    const int bl = own ? lane : 0;  // lanes past the blocks read block 0
+    double sq[MX];
+    float rsv[MX];
+#pragma unroll
+    for (int p = 0; p < MX; ++p) {
+        sq[p] = a.blk_sq[(r0 + p) * nb + bl];
+        rsv[p] = a.blk_rs[(r0 + p) * nb + bl];
+    }
+    double sc = sq[0];
+#pragma unroll
+    for (int p = 1; p < MX; ++p)
+        sc = sc + sq[p];
+    if (!own)
+        sc = 0.0;
+    if (own && a.scores)
+        a.scores[j * nb + lane] = sc;
+    const uint64_t kown = score_key(sc);
+    int beaten = 0;  // a block never outranks itself
+    for (int c2 = 0; c2 < nb; ++c2)
+        beaten += outranks_n(score_key(readlane_f64(sc, c2)), c2, kown, lane);
+    const bool keep = own && beaten < nb - K;
+    const uint64_t m = __ballot(keep);
+    if (keep)
+        a.idx[j * (nb - K) + __popcll(m & ((1ull << lane) - 1ull))] = lane;
+    if (a.db) {
+        float rs[MX];
+#pragma unroll
+        for (int p = 0; p < MX; ++p)
+            rs[p] = lead_sum_f32<64>(keep ? rsv[p] : 0.f);
+        if (lane == 0) {
+#pragma unroll
+            for (int p = 0; p < MX; ++p)
+                a.db[r0 + p] += rs[p];
+        }
+    }
+    // zero the removed blocks of the slice's rows
+    TS *dGc = (TS *)a.dGc;
+    const int lmy = __builtin_ctz(My);
+    const int nch = (B + 63) / 64;
+    for (int jj = 0; jj < nch; ++jj) {
+        const int b = 64 * jj + lane;
+        if (b < B && !((m >> (b >> lmy)) & 1ull)) {
+#pragma unroll 8
+            for (int p = 0; p < MX; ++p)
+                st<TS>::store(dGc, (r0 + p) * B + b, 0.f);
+        }
+    }
+}
+
 template <typename TS, int SRC>
 static void launch_fine_src(const CellArgs &a, hipStream_t s) {
     const dim3 grid((unsigned)(4L * a.H / a.P));
@@ -1379,6 +1487,17 @@ static hipError_t launch_fine_typed(const CellArgs &a, int mode, hipStream_t s) 
         case 3: hipLaunchKernelGGL((cell_fine4_kernel<TS, 3>), grid, dim3(768), 0, s, a); break;
         default: hipLaunchKernelGGL((cell_fine4_kernel<TS, 4>), grid, dim3(1024), 0, s, a); break;
         }
+    } else if (a.P == 32 && a.blk_sq && a.blk_rs && (long)a.H * a.B >= 65536) {
+        // 32-row slices at large shapes: the element kernel writes the gate
+        // gradient and the per-block sums; the selection reads only the sums
+        const int nch = (int)ceil_div(a.B, 64);
+        dim3 ge((unsigned)ceil_div(a.H, EK_UNITS), (unsigned)nch);
+        hipLaunchKernelGGL((cell_elem_kernel<TS, CELL_DENSE, true>), ge, dim3(EK_WAVES * 64), 0, s, a);
+        hipError_t e = hipGetLastError();
+        if (e != hipSuccess)
+            return e;
+        hipLaunchKernelGGL((cell_fine32_sel_kernel<TS>), dim3((unsigned)(4L * a.H / 32)), dim3(64), 0,
+                           s, a);
     } else if (a.stage && (long)a.H * a.B >= 65536) {
         // large shapes: the element kernel forms each unit's four gate rows
         // once (one read of dh and the cache per unit), then the slices are

@@ -44,6 +44,10 @@ struct CellArgs {
     // matrix, idx [4H/P][nb - S] the kept blocks and scores [4H/P][nb]
     int My, nb;
     int fine_fused;        // 4-row slices, H % 4 == 0, large shapes: one fused kernel
+    // 32-row slices at large shapes: per (row, block) sums of squares and
+    // sums of one step, [4H][nb], written by the element kernel
+    double *blk_sq;
+    float *blk_rs;
 };
 
 // Data gradient [dx_t; dh_{t-1}] = W_c^T dG_c, split over K into partials.

@@ -372,10 +372,19 @@ int dx_chunk_len(const lstmss_dims *d, int chunk_len, int *tm, int *tn) {
 }
 
 struct WsLayout {
-    size_t dc0, dc1, part, dGc, idx, db, stage, chunk_sq, chunk_rs, total;
+    size_t dc0, dc1, part, dGc, idx, db, stage, chunk_sq, chunk_rs, blk, total;
     int splitk;
     long k_chunk;
 };
+
+// Bytes of the fine structure's per-step block sums: [4H][nb] doubles, then
+// [4H][nb] floats.
+size_t blk_sq_bytes(const lstmss_dims *d, const Plan &p) {
+    return align256((size_t)4 * d->H * p.nb * 8);
+}
+size_t blk_bytes(const lstmss_dims *d, const Plan &p) {
+    return blk_sq_bytes(d, p) + align256((size_t)4 * d->H * p.nb * 4);
+}
 
 WsLayout ws_layout(const lstmss_dims *d, const Plan &p) {
     const size_t es = elem_bytes(d->dtype);
@@ -397,6 +406,9 @@ WsLayout ws_layout(const lstmss_dims *d, const Plan &p) {
     L.stage = off; off += align256((size_t)4 * d->H * d->B * es);
     L.chunk_sq = off; off += align256((size_t)4 * d->H * nch * 8);
     L.chunk_rs = off; off += align256((size_t)d->T * 4 * d->H * nch * 4);
+    // fine structure: per (row, block) sums of squares (fp64) and sums (fp32)
+    // of one step
+    L.blk = off; off += p.fine ? blk_bytes(d, p) : 0;
     L.total = off;
     return L;
 }
@@ -652,6 +664,10 @@ int32_t backward_enqueue(const lstmss_dims *d, bool dense, const Plan &p, const 
         ca.My = p.My;
         ca.nb = p.nb;
         ca.fine_fused = g_fine_fused ? 1 : 0;
+        if (fine) {
+            ca.blk_sq = (double *)(wb + L.blk);
+            ca.blk_rs = (float *)(wb + L.blk + blk_sq_bytes(d, p));
+        }
         if (!split && !fine &&
             cell_lds_bytes(ca, sparse ? CELL_SPARSE : CELL_DENSE) > kMaxLds)
             return fail(LSTMSS_ERR_UNSUPPORTED, "R*P*B too large for one work-group's LDS");
@@ -1264,7 +1280,16 @@ int64_t lstmss_workspace_bytes(const lstmss_dims *d, float sparsity, const lstms
     rc = make_plan(d, sparsity, s, s == nullptr || sparsity == 0.f, &p);
     if (rc)
         return rc;
-    return (int64_t)ws_layout(d, p).total;
+    size_t total = ws_layout(d, p).total;
+    if (s && sparsity == 0.f) {
+        // lstm_bwd_structsparse at sparsity 0 runs its structure's plan (the
+        // fine one indexes (4H / Mx) nb blocks and keeps block sums), which
+        // may need more than the dense call
+        Plan q;
+        if (make_plan(d, sparsity, s, false, &q) == LSTMSS_OK)
+            total = std::max(total, ws_layout(d, q).total);
+    }
+    return (int64_t)total;
 }
 
 // Forward workspace: the input projection of every step and the split-K

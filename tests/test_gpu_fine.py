@@ -302,3 +302,24 @@ def test_fine_fused_same_bits(L, T, B, I, H, sp, My, dtype):
         L.set_option("fine_fused", 1)
     for k in ("dX", "dW", "db", "dh0", "dc0", "idx", "dbg"):
         assert torch.equal(outs[0][k], outs[1][k]), k
+
+
+@pytest.mark.parametrize("T,B,I,H,Mx,My", [
+    (2, 64, 16, 32, 2, 2),      # 32 blocks per 2-row slice: the index outgrows the dense one
+    (2, 256, 64, 256, 32, 32),  # 32-row slices at H*B >= 65536 (per-block sums in the workspace)
+])
+def test_fine_zero_sparsity_workspace(L, T, B, I, H, Mx, My):
+    """lstm_bwd_structsparse at sparsity 0 runs the structure's own plan: the
+    workspace query must cover it (the binding sizes the workspace with it),
+    every block is kept and the gradients match the dense call."""
+    d = make_layer(T, B, I, H, seed=B + H + Mx, w_scale=0.2, state=True)
+    x, W, dH = gpu_tensor(d["x"]), gpu_tensor(d["W"]), gpu_tensor(d["dH_up"])
+    _, cache = L.fwd_cache(x, W)
+    a = L.bwd_dense(x, W, cache, dH)
+    b = L.bwd_structsparse(x, W, cache, dH, sparsity=0.0, kind=L.FINE, My=My, Mx=Mx)
+    torch.cuda.synchronize()
+    nb = oracle.fine_blocks(B, My)
+    idx = b["idx"].cpu().numpy().reshape(T, 4 * H // Mx, nb)
+    assert np.array_equal(idx, np.broadcast_to(np.arange(nb, dtype=np.int32), idx.shape))
+    for k in ("dX", "dW", "db"):
+        assert rel(to_np64(b[k]), to_np64(a[k])) <= 1e-6, k
