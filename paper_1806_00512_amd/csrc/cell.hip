@@ -1392,18 +1392,18 @@ __global__ __launch_bounds__(256 * NCH) void cell_fine4_kernel(CellArgs a) {
     }
 }
 
-// cell_fine32_sel_kernel: the selection of 32-row slices at large shapes
+// cell_fine_sel_kernel: the selection of MX-row slices at large shapes
 // from the element kernel's per-(row, block) sums (blk_sq, blk_rs), one
 // wavefront per slice, lane b holding block b.  A block's score is its rows'
 // sums of squares folded in increasing row order (the same values, in the
-// same order, as cell_fine32_kernel's); a block is kept when fewer than
+// same order, as cell_fine_kernel's and cell_fine32_kernel's); a block is
+// kept when fewer than
 // nb - K blocks of the slice outrank it.  The element kernel wrote the gate
 // gradient to dGc; the removed blocks are zeroed there in place.  Each row's
 // bias term is the sum of its kept blocks' sums by the 64-lane butterfly over
 // the blocks (dropped ones add zero), added to db step by step.
-template <typename TS>
-__global__ __launch_bounds__(64) void cell_fine32_sel_kernel(CellArgs a) {
-    constexpr int MX = 32;
+template <typename TS, int MX>
+__global__ __launch_bounds__(64) void cell_fine_sel_kernel(CellArgs a) {
     const int lane = threadIdx.x;
     const int B = a.B, My = a.My, nb = a.nb, K = a.S;
     const long j = blockIdx.x;  // slice
@@ -1487,17 +1487,27 @@ static hipError_t launch_fine_typed(const CellArgs &a, int mode, hipStream_t s) 
         case 3: hipLaunchKernelGGL((cell_fine4_kernel<TS, 3>), grid, dim3(768), 0, s, a); break;
         default: hipLaunchKernelGGL((cell_fine4_kernel<TS, 4>), grid, dim3(1024), 0, s, a); break;
         }
-    } else if (a.P == 32 && a.blk_sq && a.blk_rs && (long)a.H * a.B >= 65536) {
-        // 32-row slices at large shapes: the element kernel writes the gate
-        // gradient and the per-block sums; the selection reads only the sums
+    } else if (a.P != 4 && a.blk_sq && a.blk_rs && (long)a.H * a.B >= 65536) {
+        // slices of 1, 2, 8, 16 or 32 rows at large shapes: the element
+        // kernel writes the gate gradient and the per-block sums; the
+        // selection reads only the sums (4-row slices take the fused kernel,
+        // or the staging matrix and cell_fine_kernel)
         const int nch = (int)ceil_div(a.B, 64);
         dim3 ge((unsigned)ceil_div(a.H, EK_UNITS), (unsigned)nch);
         hipLaunchKernelGGL((cell_elem_kernel<TS, CELL_DENSE, true>), ge, dim3(EK_WAVES * 64), 0, s, a);
         hipError_t e = hipGetLastError();
         if (e != hipSuccess)
             return e;
-        hipLaunchKernelGGL((cell_fine32_sel_kernel<TS>), dim3((unsigned)(4L * a.H / 32)), dim3(64), 0,
-                           s, a);
+        const dim3 gs((unsigned)(4L * a.H / a.P));
+#define LSTMSS_FS(MX) hipLaunchKernelGGL((cell_fine_sel_kernel<TS, MX>), gs, dim3(64), 0, s, a)
+        switch (a.P) {
+        case 1: LSTMSS_FS(1); break;
+        case 2: LSTMSS_FS(2); break;
+        case 8: LSTMSS_FS(8); break;
+        case 16: LSTMSS_FS(16); break;
+        default: LSTMSS_FS(32); break;
+        }
+#undef LSTMSS_FS
     } else if (a.stage && (long)a.H * a.B >= 65536) {
         // large shapes: the element kernel forms each unit's four gate rows
         // once (one read of dh and the cache per unit), then the slices are

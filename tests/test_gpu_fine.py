@@ -176,6 +176,9 @@ def test_layer_fine_bf16(L, T, B, I, H, sp, Mx, My):
     (2, 256, 64, 256, 4, 8, "bf16"),
     (2, 256, 64, 256, 32, 32, "f32"),
     (2, 256, 64, 256, 32, 32, "bf16"),
+    (2, 256, 64, 256, 8, 16, "f32"),      # 8- and 16-row slices: per-block sums, then one
+    (2, 256, 64, 256, 16, 4, "bf16"),     # wavefront per slice
+    (2, 128, 64, 512, 2, 8, "f32"),
 ])
 def test_fine_large_shape(L, T, B, I, H, Mx, My, dtype):
     """Shapes with H*B >= 65536, where the element kernel forms the gate
