@@ -100,9 +100,10 @@ __global__ __launch_bounds__(NW * 64) void gemm1_kernel(Gemm1Args a) {
     static_assert(!(ROWA && GATHER), "the forward products read every row");
     static_assert(!SEL || (DMA && GATHER), "selection in the product: gathered DMA stages");
     static_assert(!(FN && (GATHER || ROWA)), "the fine fast path reads every row");
-    static_assert(!DMA || (!FN && VEC &&
+    static_assert(!DMA || (VEC && (!FN || (sizeof(TS) == 4 && TM == 128 && TN == 32)) &&
                            (sizeof(TS) == 4 ? NW == 4 : (NW == 8 && TM == 128 && TN == 128))),
-                  "DMA stages: fp32 products, or bf16 128 x 128 tiles of eight wavefronts");
+                  "DMA stages: fp32 products (the fine path with 128 x 32 tiles), or bf16 "
+                  "128 x 128 tiles of eight wavefronts");
     constexpr int THREADS = NW * 64;  // shadows the file-wide default
     using SH = G1Shape<TS, TM, TN, NW>;
     constexpr bool BF = SH::BF;
@@ -172,7 +173,7 @@ __global__ __launch_bounds__(NW * 64) void gemm1_kernel(Gemm1Args a) {
         const int s1 = min(ke, s0 + GEMM1_KC_MAX);
         for (int i = tid; i < s1 - s0; i += THREADS) {
             const int k = s0 + i;
-            srow[i] = GATHER ? idx[k / a.P] * a.P + k % a.P : k;
+            srow[i] = GATHER ? idx[k / a.P] * a.P + k % a.P : (FN ? grow(k) : k);
         }
     };
     __shared__ __align__(16) E As[2][DMA ? 1 : TM][LDK];
@@ -248,7 +249,7 @@ __global__ __launch_bounds__(NW * 64) void gemm1_kernel(Gemm1Args a) {
                     a.sel_idx[sl.slot] = j;
             }
         }
-    } else if (!ROWA && !FN) {
+    } else if (!ROWA && (!FN || DMA)) {  // FN with DMA stages: the kept slices' rows
         fill_rows(sc);
     }
 
@@ -319,7 +320,13 @@ __global__ __launch_bounds__(NW * 64) void gemm1_kernel(Gemm1Args a) {
             const int off = (isa ? q : q - NIA) * IEL + lane * PEL;  // element offset in the stage
             const int rowlen = isa ? TM : TN;
             const int kl = off / rowlen, pc = (off - kl * rowlen) / PEL;
-            const int col = (pc ^ swz(kl)) * PEL;  // first column this lane's slot holds
+            // 32-column rows (128 bytes) cannot be split: the second operand's
+            // rows go to the slots of each group of 8 in the order k, k + 4,
+            // k + 1, k + 5, ..., so that the rows k and k + 4 a wavefront reads
+            // together are adjacent (distinct banks); the slot kl holds row kg
+            const bool nsw = !isa && TN == 32;
+            const int kg = nsw ? (kl & ~7) + ((kl & 7) >> 1) + 4 * (kl & 1) : kl;
+            const int col = (nsw ? pc : pc ^ swz(kl)) * PEL;  // first column this lane's slot holds
             const TS *src;
             if (isa && ROWA) {
                 // row kl' = off / TK of the [m][k] tile, piece pc' of it
@@ -331,7 +338,7 @@ __global__ __launch_bounds__(NW * 64) void gemm1_kernel(Gemm1Args a) {
                 src = W + (long)srow[k0 + kl - sc] * ldw + m;
             } else {
                 const int n = min(n0 + col, N - PEL);
-                src = G + (long)(SEL ? srow[k0 + kl - sc] : k0 + kl) * N + n;
+                src = G + (long)((SEL || FN) ? srow[k0 + kg - sc] : k0 + kg) * N + n;
             }
             E *dst = isa ? &Ad[b][q * IEL] : &Bd[b][(q - NIA) * IEL];
             __builtin_amdgcn_global_load_lds((glob_void_t *)src, (lds_void_t *)dst, 16, 0, 0);
@@ -401,7 +408,8 @@ __global__ __launch_bounds__(NW * 64) void gemm1_kernel(Gemm1Args a) {
 
     __syncthreads();
     if constexpr (DMA) {
-        dload(kb, 0);
+        if (ke > kb)  // FN: a block no slice of the range keeps has no stages
+            dload(kb, 0);
         __builtin_amdgcn_s_waitcnt(0);
     } else {
         load(kb);
@@ -412,7 +420,7 @@ __global__ __launch_bounds__(NW * 64) void gemm1_kernel(Gemm1Args a) {
     for (int k0 = kb; k0 < ke; k0 += TK) {
         const bool next = k0 + TK < ke;
         if (next) {
-            if (!ROWA && !FN && !SEL && k0 + TK == sc + GEMM1_KC_MAX) {  // next super-chunk of rows
+            if (!ROWA && (!FN || DMA) && !SEL && k0 + TK == sc + GEMM1_KC_MAX) {  // next super-chunk of rows
                 sc = k0 + TK;
                 fill_rows(sc);
                 __syncthreads();
@@ -506,7 +514,10 @@ __global__ __launch_bounds__(NW * 64) void gemm1_kernel(Gemm1Args a) {
 #pragma unroll
                     for (int j = 0; j < NT; ++j) {
                         const int n = nw + j * 32 + (lane & 31);
-                        bv[b8][c][j] = Bd[buf][k * TN + ((((n >> 2) ^ g1_swz(k))) << 2) + (n & 3)];
+                        if constexpr (TN == 32)  // row k in slot (k & ~7) + 2 (k & 3) + ((k >> 2) & 1)
+                            bv[b8][c][j] = Bd[buf][((k & ~7) + 2 * (k & 3) + ((k >> 2) & 1)) * TN + n];
+                        else
+                            bv[b8][c][j] = Bd[buf][k * TN + ((((n >> 2) ^ g1_swz(k))) << 2) + (n & 3)];
                     }
                 }
             if (next)  // the next stage streams in during the MFMAs
@@ -683,6 +694,13 @@ static void launch_g1(dim3 grid, const Gemm1Args &a, bool w8, hipStream_t s, boo
     }
     if constexpr (!GA && !ROWA && TM == 128 && TN == 32) {
         if (a.fidx) {
+            if constexpr (sizeof(TS) == 4 && VE) {
+                if (dma) {
+                    hipLaunchKernelGGL((gemm1_kernel<TS, 128, 32, false, true, false, 4, true, true>), grid,
+                                       dim3(THREADS), 0, s, a);
+                    return;
+                }
+            }
             hipLaunchKernelGGL((gemm1_kernel<TS, 128, 32, false, VE, false, 4, true>), grid, dim3(THREADS), 0, s, a);
             return;
         }
@@ -728,7 +746,7 @@ static hipError_t g1_plan(Gemm1Args &a, bool bf16, G1Plan *pl) {
     a.m_lo = vec ? a.m_begin / vw * vw : a.m_begin;
     const long z = (long)a.splitk * a.steps;
     // DMA stages: whole k stages (32 fp32 or 64 bf16 rows), 16-byte aligned rows
-    const bool dma_shape = a.dma && vec && !a.fidx && a.Kp % (bf16 ? 64 : 32) == 0 &&
+    const bool dma_shape = a.dma && vec && (!a.fidx || !bf16) && a.Kp % (bf16 ? 64 : 32) == 0 &&
                            ((uintptr_t)a.W & 15) == 0 && ((uintptr_t)a.Gc & 15) == 0;
     int TM, TN;
     gemm1_tile(bf16, a.N, a.M - a.m_lo, z, &TM, &TN);
@@ -752,7 +770,8 @@ static hipError_t g1_plan(Gemm1Args &a, bool bf16, G1Plan *pl) {
     pl->TN = TN;
     pl->vec = vec;
     pl->w8 = use_w8(a, bf16, TM, TN);
-    pl->dma = dma_shape && (bf16 ? (pl->w8 && TM == 128 && TN == 128) : TN != 32);
+    // fp32 DMA stages: 64- and 128-column tiles, and the fine path's 128 x 32
+    pl->dma = dma_shape && (bf16 ? (pl->w8 && TM == 128 && TN == 128) : (TN != 32 || a.fidx));
     pl->grid = dim3((unsigned)ceil_div(a.M - a.m_lo, TM), (unsigned)ceil_div(a.N, TN), (unsigned)z);
     // selection inside the product: one step on DMA stages, splits of whole
     // regions whose gathered rows fit one table
