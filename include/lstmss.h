@@ -358,6 +358,15 @@ int32_t lstmss_mse_grad(const lstmss_dims *d, const void *h, const float *y, flo
  *                      work-group holds four whole slices); 0 forms it into
  *                      the staging matrix and selects in a second kernel
  *                      (same bits; for checking and timing).
+ *   LSTMSS_OPT_WGRAD_BIG  1 (default): the bf16 weight gradient with 128-byte
+ *                      batch chunks (B a multiple of 64) runs on 256-row x
+ *                      256-feature tiles, the dropped rows of a coarse
+ *                      structure multiplied as zeros (regions of P * R rows
+ *                      dividing 256, a multiple of 64 kept rows per tile);
+ *                      0 runs the 32-row-group kernel that multiplies only
+ *                      the kept rows.  The two sum in different orders
+ *                      (both fixed; each matches the oracle to the bf16
+ *                      tolerance).
  * Changing an option drops the recorded graphs.  Not for use while calls
  * are being enqueued from other threads. */
 enum {
@@ -367,7 +376,8 @@ enum {
     LSTMSS_OPT_FINE_SKIP = 3,
     LSTMSS_OPT_GEMM_DMA = 4,
     LSTMSS_OPT_GEMM_SELECT = 5,
-    LSTMSS_OPT_FINE_FUSED = 6
+    LSTMSS_OPT_FINE_FUSED = 6,
+    LSTMSS_OPT_WGRAD_BIG = 7
 };
 int32_t lstmss_set_option(int32_t option, int32_t value);
 

@@ -112,6 +112,31 @@ __device__ __forceinline__ void dma4(const void *gsrc, lds_void_t *lds_dst) {
 
 // s_waitcnt immediate that waits until at most n vector-memory operations of
 // this wavefront are outstanding (the other counters left at their maxima).
+// Buffer resource of raw bytes from base (gfx9 layout: stride 0,
+// `bytes` records, the data-format word of untyped buffer access).
+typedef int i32x4 __attribute__((ext_vector_type(4)));
+__device__ __forceinline__ i32x4 buf_rsrc(const void *base, uint32_t bytes) {
+    const uint64_t p = (uint64_t)(uintptr_t)base;
+    i32x4 r;
+    r[0] = (int)(uint32_t)p;
+    r[1] = (int)((uint32_t)(p >> 32) & 0xffffu);
+    r[2] = (int)bytes;
+    r[3] = 0x00020000;
+    return r;
+}
+
+// dma16 through a buffer resource: lane j copies the 16 bytes at
+// base + soff + voff (voff its own byte offset) to bytes [16 j, 16 j + 16) of
+// the 1 KB LDS block at lds_dst.  Only the 32-bit offset lives in a vector
+// register.  Same ordering rules as dma16.
+__device__ __forceinline__ void dma16_buf(i32x4 rsrc, int voff, int soff, lds_void_t *lds_dst) {
+    const int lds = __builtin_amdgcn_readfirstlane((int)(uintptr_t)lds_dst);
+    asm volatile("s_mov_b32 m0, %1\n\tbuffer_load_dwordx4 %0, %2, %3 offen lds"
+                 :
+                 : "v"(voff), "s"(lds), "s"(rsrc), "s"(soff)
+                 : "memory", "m0");
+}
+
 constexpr int vmcnt_imm(int n) { return (n & 0xf) | ((n >> 4) << 14) | (0x7 << 4) | (0xf << 8); }
 
 } // namespace

@@ -130,6 +130,8 @@ struct WgradArgs {
     int fskip;             // 1: skip removed blocks; 0: multiply them (same bits)
     int dma;               // 1: chunks go global -> LDS directly where the shape allows
                            // (same bits as the register-staged loads of 0)
+    int big;               // bf16 with DMA chunks: 1 takes the 256 x 256-tile kernel
+                           // where it applies (its own summation order)
 };
 
 // Forward cell update from the pre-activation pieces of one step.

@@ -176,6 +176,9 @@ bool g_gemm_select = true;
 // fine structure with 4-row slices at large shapes: gate gradient and block
 // selection in one kernel (1) or two (0); same bits
 bool g_fine_fused = true;
+// bf16 weight gradient: the 256 x 256-tile kernel where it applies (1) or the
+// 32-row-group kernel everywhere (0)
+bool g_wgrad_big = true;
 
 hipError_t stack_res(StackRes **out) {
     int dev = 0;
@@ -574,6 +577,7 @@ int32_t backward_enqueue(const lstmss_dims *d, bool dense, const Plan &p, const 
     wg.P = p.P; wg.R = p.R; wg.S = p.S; wg.dW = dW;
     wg.fidx = fblocks ? idx_all : nullptr; wg.fkept = fkept; wg.fskip = ffast ? 1 : 0;
     wg.dma = g_gemm_dma ? 1 : 0;
+    wg.big = g_wgrad_big ? 1 : 0;
 
     Gemm1Args gx{};  // dX[t] = (W_c rows [0, I))^T dG_c, several steps per launch
     gx.W = W; gx.ldw = K; gx.P = p.P; gx.Kp = p.Kp; gx.M = I; gx.m_begin = 0; gx.N = B;
@@ -1482,6 +1486,7 @@ int32_t lstmss_set_option(int32_t option, int32_t value) {
     case LSTMSS_OPT_GEMM_DMA: g_gemm_dma = value != 0; return LSTMSS_OK;
     case LSTMSS_OPT_GEMM_SELECT: g_gemm_select = value != 0; return LSTMSS_OK;
     case LSTMSS_OPT_FINE_FUSED: g_fine_fused = value != 0; return LSTMSS_OK;
+    case LSTMSS_OPT_WGRAD_BIG: g_wgrad_big = value != 0; return LSTMSS_OK;
     case LSTMSS_OPT_STACK_DX_STEPS:
         if (value < 0)
             return fail(LSTMSS_ERR_INVALID_ARG, "stack dX steps %d must be >= 0", value);

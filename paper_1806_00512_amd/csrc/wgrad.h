@@ -648,6 +648,313 @@ void wg_launch(const WgradArgs &a, bool vec, bool dma, dim3 grid, hipStream_t s)
     }
 }
 
+// --------------------------------------------------------------------------
+// bf16 weight gradient with large tiles (DMA chunks of 64 batch columns).
+//
+// Work-group: 256 original dW rows x 256 features, eight wavefronts of 128
+// rows x 64 features (2 x 4 MFMA tiles, accumulated in registers across all
+// steps).  Per chunk the staged operands are 256 feature rows and the tile's
+// KRT compacted gate-gradient rows; a wavefront reads 0.75 KB of LDS per
+// MFMA (the 32-row-group kernel above reads 1.5 KB, which makes it bound by
+// LDS bandwidth).
+// Sparse: the tile covers whole regions (P * R divides 256), so its kept rows
+// are the contiguous compacted rows [KRT * tile, KRT * (tile + 1)) at every
+// step.  Instead of routing a product of the kept rows, each lane's B operand
+// row is, for the step, the compacted row holding its original row or a row
+// of zeros in LDS when the row's slice was dropped: the MFMAs run over the
+// original rows, a dropped row adding products with zero (twice the MFMAs of
+// the kept rows at 50 %, in exchange for no temporary tile and no routing).
+// Every row of dW sums its steps from the last down, one MFMA per 16 batch
+// columns, in a fixed order (deterministic; the launches of one call continue
+// from the stored dW).  Non-finite x or h make a dropped row's product NaN
+// (0 * inf), where the routing kernel adds nothing.
+// --------------------------------------------------------------------------
+constexpr int WB_ROWS = 256, WB_FEAT = 256, WB_THREADS = 512;
+
+template <int KRT>
+constexpr int wb_stages() { return KRT <= 128 ? 3 : 2; }
+
+template <int KRT, bool SP>
+__global__ __launch_bounds__(WB_THREADS, 2) void wgrad_big_kernel(WgradArgs a) {
+    constexpr int NS = wb_stages<KRT>();
+    constexpr int NDI = (WB_FEAT + KRT) / 8;      // 1 KB copies per chunk
+    constexpr int NDW = NDI / 8;                  // per wavefront
+    static_assert(NDI % 8 == 0 && KRT % 64 == 0, "whole copies per wavefront");
+    constexpr int NQ = SP ? KRT : 1;              // kept-slice entries per step (at most KRT / P)
+    __shared__ __align__(16) uint16_t sX[NS][WB_FEAT][64];
+    __shared__ __align__(16) uint16_t sG[NS][KRT + 1][64];  // row KRT: zeros
+    __shared__ int sidx[SP ? NS : 1][NQ];
+
+    const int tid = threadIdx.x, lane = tid & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);  // uniform: descriptors stay scalar
+    const int rh = wave & 1, fq = wave >> 1;      // row half, feature quarter
+    const int I = a.I, H = a.H, B = a.B;
+    const int NC = I + H, G4 = 4 * H;
+    const int r0 = blockIdx.x * WB_ROWS, n0 = blockIdx.y * WB_FEAT;
+    const bf16_t *Gc = (const bf16_t *)a.Gc;
+    const bf16_t *x = (const bf16_t *)a.x;
+    const bf16_t *h = (const bf16_t *)a.h;
+    // sparse geometry: regions of the tile, their kept-slice entries and rows
+    const int ks = SP ? a.R - a.S : 0;
+    const int rpw = SP ? WB_ROWS / (a.P * a.R) : 0;
+    const int q0 = blockIdx.x * rpw * ks;         // first kept-slice entry
+    const int c0 = SP ? blockIdx.x * KRT : r0;    // first compacted row
+    const int nq = rpw * ks;                      // entries of the tile (<= NQ)
+
+    if (tid < NS * 8)
+        *(u16x8 *)&sG[tid >> 3][KRT][8 * (tid & 7)] = u16x8{0, 0, 0, 0, 0, 0, 0, 0};
+
+    // copies: instruction k fills 8 rows of sX (k < 32) or sG; wavefront w
+    // issues k = w, w + 8, ...; lane j fills 16-byte piece j & 7 of row j >> 3.
+    // Byte offsets within a step's operand (x or h by the instruction's
+    // first feature, all 8 rows on the same side since I % 8 == 0)
+    int voff[NDW];
+#pragma unroll
+    for (int i = 0; i < NDW; ++i) {
+        const int k = wave + 8 * i;
+        const int rr = 8 * (k < 32 ? k : k - 32) + (lane >> 3);
+        const int pc = (lane & 7) ^ wg_swz(rr);
+        if (k < 32) {
+            const int n = min(n0 + rr, NC - 1);
+            voff[i] = 2 * ((n < I ? n : n - I) * B + pc * 8);
+        } else {
+            voff[i] = 2 * (min(c0 + rr, a.Kp - 1) * B + pc * 8);
+        }
+    }
+    const int nbc = B / 64;
+    const int niters = (a.t_end - a.t_begin) * nbc;
+    auto load = [&](int it) __attribute__((always_inline)) {
+        const int tl = it / nbc, b0 = (it - tl * nbc) * 64;
+        const int t = a.t_end - 1 - tl;
+        const int buf = it % NS;
+        const i32x4 rx = buf_rsrc(x + (long)t * I * B, 2u * I * B);
+        const i32x4 rhh = buf_rsrc(h + (long)t * H * B, 2u * H * B);
+        const i32x4 rg = buf_rsrc(Gc + (long)t * a.Kp * B, 2u * a.Kp * B);
+#pragma unroll
+        for (int i = 0; i < NDW; ++i) {
+            const int k = wave + 8 * i;
+            if (k < 32)
+                dma16_buf(n0 + 8 * k < I ? rx : rhh, voff[i], 2 * b0, (lds_void_t *)&sX[buf][8 * k][0]);
+            else
+                dma16_buf(rg, voff[i], 2 * b0, (lds_void_t *)&sG[buf][8 * (k - 32)][0]);
+        }
+        if constexpr (SP) {
+            // the step's kept-slice entries of the tile's regions, with its first chunk
+            if (b0 == 0 && wave * 64 < nq) {
+                const int e = min(q0 + wave * 64 + lane, a.kept - 1);
+                dma4(a.idx + (long)t * a.kept + e, (lds_void_t *)&sidx[tl % NS][wave * 64]);
+            }
+        }
+    };
+    auto wait_chunks = [&](int n) {
+        if (NS > 2 && n >= 2)
+            __builtin_amdgcn_s_waitcnt(vmcnt_imm((NS > 2 ? 2 : 0) * NDW));
+        else if (n >= 1)
+            __builtin_amdgcn_s_waitcnt(vmcnt_imm(NDW));
+        else
+            __builtin_amdgcn_s_waitcnt(0);
+    };
+
+    f32x16 acc[2][4];
+#pragma unroll
+    for (int ft = 0; ft < 2; ++ft)
+#pragma unroll
+        for (int rt = 0; rt < 4; ++rt)
+#pragma unroll
+            for (int v = 0; v < 16; ++v)
+                acc[ft][rt][v] = 0.f;
+    // accumulator tile (ft, rt): column = dW row r0 + rh * 128 + rt * 32 +
+    // lane % 32, register v = feature n0 + fq * 64 + ft * 32 + acc_row(lane, v)
+    if (a.accumulate) {
+#pragma unroll
+        for (int rt = 0; rt < 4; ++rt) {
+            const int row = r0 + rh * 128 + rt * 32 + (lane & 31);
+            if (row >= G4)
+                continue;
+            const float *src = a.dW + (long)row * NC;
+#pragma unroll
+            for (int ft = 0; ft < 2; ++ft)
+#pragma unroll
+                for (int v = 0; v < 16; ++v) {
+                    const int f = n0 + fq * 64 + ft * 32 + acc_row(lane, v);
+                    if (f < NC)
+                        acc[ft][rt][v] = src[f];
+                }
+        }
+        __builtin_amdgcn_s_waitcnt(0);
+    }
+
+    // every buffer in flight before the loop: chunks 0 .. NS - 1
+#pragma unroll
+    for (int c = 0; c < NS; ++c)
+        if (c < niters)
+            load(c);
+
+    // LDS element offsets of this lane's operand rows (A: features, fixed;
+    // B: the step's row map) and their piece permutation
+    const int hp = (lane >> 5) * 4;               // first 16-byte piece of this half
+    int aoff[2], asw[2], boff[4], bsw[4];
+#pragma unroll
+    for (int ft = 0; ft < 2; ++ft) {
+        const int f = fq * 64 + ft * 32 + (lane & 31);
+        aoff[ft] = f * 64;
+        asw[ft] = wg_swz(f);
+    }
+#pragma unroll
+    for (int rt = 0; rt < 4; ++rt) {
+        const int slot = rh * 128 + rt * 32 + (lane & 31);
+        boff[rt] = slot * 64;
+        bsw[rt] = wg_swz(slot);
+    }
+    // the row map of step tl (sparse): the compacted row holding each of this
+    // lane's original rows at that step, or the zero row
+    auto row_map = [&](int tl) __attribute__((always_inline)) {
+        if constexpr (SP) {
+            const int *tab = sidx[tl % NS];
+#pragma unroll
+            for (int rt = 0; rt < 4; ++rt) {
+                const int r = r0 + rh * 128 + rt * 32 + (lane & 31);
+                int slot = KRT;
+                if (r < G4) {
+                    const int js = r / a.P, reg = js / a.R;
+                    const int e0 = reg * ks, e1 = min(e0 + ks, a.kept);
+                    for (int e = e0; e < e1; ++e)
+                        if (tab[e - q0] == js)
+                            slot = e * a.P + (r - js * a.P) - c0;
+                }
+                boff[rt] = slot * 64;
+                bsw[rt] = wg_swz(slot);
+            }
+        }
+    };
+    // operands of k-step s (16 batch columns: 8 per lane half) of buffer buf
+    // into register set st
+    u16x8 fa[2][2], fb[2][4];
+    auto rd = [&](int buf, int s, auto setc) __attribute__((always_inline)) {
+        constexpr int st = decltype(setc)::value;
+        const uint16_t *xb = &sX[buf][0][0];
+        const uint16_t *gb = &sG[buf][0][0];
+#pragma unroll
+        for (int ft = 0; ft < 2; ++ft)
+            fa[st][ft] = *(const u16x8 *)(xb + aoff[ft] + (((hp + s) ^ asw[ft]) << 3));
+#pragma unroll
+        for (int rt = 0; rt < 4; ++rt)
+            fb[st][rt] = *(const u16x8 *)(gb + boff[rt] + (((hp + s) ^ bsw[rt]) << 3));
+    };
+    // (the scheduler keeps each group in place: reading the next operands
+    // into a set ahead of the MFMAs that still use it costs registers)
+    auto mma = [&](auto setc) __attribute__((always_inline)) {
+        constexpr int st = decltype(setc)::value;
+        __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+        for (int ft = 0; ft < 2; ++ft)
+#pragma unroll
+            for (int rt = 0; rt < 4; ++rt)
+                acc[ft][rt] = mfma32x32x16bf(fa[st][ft], fb[st][rt], acc[ft][rt]);
+        __builtin_amdgcn_sched_barrier(0);
+    };
+    constexpr std::integral_constant<int, 0> S0{};
+    constexpr std::integral_constant<int, 1> S1{};
+
+    if (niters > 0) {
+        wait_chunks(min(NS - 1, niters - 1));
+        lds_barrier();
+        row_map(0);
+        rd(0, 0, S0);
+        rd(0, 1, S1);
+    }
+    // Iteration it multiplies chunk it (k-steps 0 and 1 already in registers)
+    // and, between its last two k-steps, meets the other wavefronts once
+    // chunk it + 1 has landed: chunk it's buffer then takes chunk it + NS, and
+    // the first k-steps of chunk it + 1 are read while the last MFMAs run.
+    for (int it = 0; it + 1 < niters; ++it) {
+        const int buf = it % NS;
+        mma(S0);
+        rd(buf, 2, S0);
+        mma(S1);
+        rd(buf, 3, S1);
+        mma(S0);
+        // chunk it + 1 has landed; chunks it + 2 .. it + NS - 1 may be in flight
+        wait_chunks(min(NS - 2, niters - 2 - it));
+        lds_barrier();
+        if (it + NS < niters)
+            load(it + NS);
+        const int nb = (it + 1) % NS;
+        if ((it + 1) % nbc == 0)
+            row_map((it + 1) / nbc);
+        rd(nb, 0, S0);
+        mma(S1);
+        rd(nb, 1, S1);
+    }
+    if (niters > 0) {  // the last chunk
+        const int buf = (niters - 1) % NS;
+        mma(S0);
+        rd(buf, 2, S0);
+        mma(S1);
+        rd(buf, 3, S1);
+        mma(S0);
+        mma(S1);
+    }
+
+#pragma unroll
+    for (int rt = 0; rt < 4; ++rt) {
+        const int row = r0 + rh * 128 + rt * 32 + (lane & 31);
+        if (row >= G4)
+            continue;
+        float *dst = a.dW + (long)row * NC;
+#pragma unroll
+        for (int ft = 0; ft < 2; ++ft)
+#pragma unroll
+            for (int v = 0; v < 16; ++v) {
+                const int f = n0 + fq * 64 + ft * 32 + acc_row(lane, v);
+                if (f < NC)
+                    dst[f] = acc[ft][rt][v];
+            }
+    }
+}
+
+// The large-tile bf16 kernel for this call, if its conditions hold: DMA
+// chunks, I a multiple of 8, the dense product or a coarse structure whose
+// regions tile 256 rows and keep 128 or 192 of them per tile.  Returns false
+// otherwise (the caller launches the routing kernel).
+bool wgrad_big_launch(const WgradArgs &a, bool sparse, hipStream_t s) {
+    // per-step operands addressed with 32-bit byte offsets; x / h chosen per
+    // 8 feature rows
+    if (a.I % 8 != 0 || 2L * a.Kp * a.B >= (1L << 31) || 2L * a.I * a.B >= (1L << 31) ||
+        2L * a.H * a.B >= (1L << 31))
+        return false;
+    // sparsity 0 keeps every slice in order: the dense product, bit for bit
+    if (sparse && a.S == 0)
+        sparse = false;
+    int krt = WB_ROWS;
+    if (sparse) {
+        const int pr = a.P * a.R;
+        if (pr <= 0 || pr > WB_ROWS || WB_ROWS % pr != 0 || a.S >= a.R)
+            return false;
+        krt = WB_ROWS / a.R * (a.R - a.S);
+        if (WB_ROWS % a.R != 0 || krt % 64 != 0)
+            return false;
+    }
+    dim3 grid((unsigned)ceil_div(4L * a.H, WB_ROWS), (unsigned)ceil_div(a.I + a.H, WB_FEAT));
+    // sparse: the zero rows' MFMAs cost more than the routing kernel's
+    // permutes below half the rows kept (75 % sparsity: 1.88 vs 1.67 ms at
+    // H = 4096, B = 256, T = 25), and with fewer tiles than CUs the routing
+    // kernel's smaller tiles fill the GPU better (H = 1024, B = 64)
+    if (sparse && (krt < WB_ROWS / 2 || (long)grid.x * grid.y < 256))
+        return false;
+    if (!sparse)
+        hipLaunchKernelGGL((wgrad_big_kernel<256, false>), grid, dim3(WB_THREADS), 0, s, a);
+    else if (krt == 192)
+        hipLaunchKernelGGL((wgrad_big_kernel<192, true>), grid, dim3(WB_THREADS), 0, s, a);
+    else if (krt == 128)
+        hipLaunchKernelGGL((wgrad_big_kernel<128, true>), grid, dim3(WB_THREADS), 0, s, a);
+    else if (krt == 64)
+        hipLaunchKernelGGL((wgrad_big_kernel<64, true>), grid, dim3(WB_THREADS), 0, s, a);
+    else
+        return false;
+    return true;
+}
+
 bool aligned16(const void *p) { return ((uintptr_t)p & 15) == 0; }
 
 // One weight-gradient call in storage type TS (the instantiations live in
@@ -670,6 +977,10 @@ hipError_t launch_wgrad_t(WgradArgs a, bool sparse, hipStream_t s) {
                   (unsigned)ceil_div(a.I + a.H, WG_FEAT));
         wg_launch<TS, false, 1, 1, true>(a, vec, bf16 ? false : dma_ok(32), grid, s);
         return hipGetLastError();
+    }
+    if constexpr (bf16) {
+        if (a.big && dma_ok(64) && wgrad_big_launch(a, sparse, s))
+            return hipGetLastError();
     }
     int tt = 1, at = 1;
     if (sparse) {

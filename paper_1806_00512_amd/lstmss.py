@@ -562,7 +562,7 @@ def cache_views(cache, T, B, H, dtype):
 
 
 OPTIONS = {"graphs": 0, "side_stream": 1, "stack_dx_steps": 2, "fine_skip": 3, "gemm_dma": 4, "gemm_select": 5,
-           "fine_fused": 6}
+           "fine_fused": 6, "wgrad_big": 7}
 
 
 def set_option(name: str, value: int):

@@ -206,10 +206,10 @@ def test_options_match_header_and_validate(L):
     lib = L.load()
     defaults = {"graphs": 0 if os.environ.get("LSTMSS_GRAPHS") == "0" else 1, "side_stream": 2,
                 "stack_dx_steps": 0, "fine_skip": 1, "gemm_dma": 1, "gemm_select": 1,
-                "fine_fused": 1}
+                "fine_fused": 1, "wgrad_big": 1}
     assert set(defaults) == set(L.OPTIONS)
     try:
-        for name in ("fine_skip", "gemm_dma", "gemm_select", "fine_fused", "graphs"):
+        for name in ("fine_skip", "gemm_dma", "gemm_select", "fine_fused", "wgrad_big", "graphs"):
             for v in (0, 1):
                 assert lib.lstmss_set_option(L.OPTIONS[name], v) == 0
         for v in (0, 1, 2):

@@ -9,7 +9,9 @@ multiple of 16), tiles that end inside the operands (I + H not a multiple of
 the tile), several batch chunks per step, several steps per launch and gathered
 rows spanning more than one table refill (K' > 2048).  Agreement with the oracle at the default
 setting is covered by the parity tests; here both settings must agree bit for
-bit on dX, dW, db, dh0, dc0 and the kept indices.
+bit on dX, dW, db, dh0, dc0 and the kept indices.  The bf16 weight gradient on
+256 x 256 tiles (LSTMSS_OPT_WGRAD_BIG) exists only with DMA chunks and sums in
+its own order, so these comparisons switch it off.
 """
 import pytest
 import torch
@@ -36,12 +38,14 @@ def gpu(a, dtype="f32"):
 def run_both(L, fn):
     outs = []
     try:
+        L.set_option("wgrad_big", 0)
         for dma in (1, 0):
             L.set_option("gemm_dma", dma)
             outs.append(fn())
             torch.cuda.synchronize()
     finally:
         L.set_option("gemm_dma", 1)
+        L.set_option("wgrad_big", 1)
     return outs
 
 

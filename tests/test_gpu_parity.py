@@ -384,6 +384,43 @@ def test_graph_replay_matches_direct(L, H, sp):
         torch.randn(1000, device=dev()).sum().item()  # unrelated eager work between replays
 
 
+@pytest.mark.parametrize("T,B,I,H,sp,big", [
+    (3, 64, 1024, 2048, 0.5, 1),     # 256 x 256 tiles, 128 kept rows each
+    (3, 64, 1024, 2048, 0.5, 0),     # the routing kernel on the same shape
+    (3, 64, 1000, 2050, 0.25, 1),    # 192 kept rows; ragged tiles, a partial last region
+    (3, 128, 1000, 2050, 0.0, 1),    # dense, ragged tiles
+])
+def test_wgrad_big_bf16(L, T, B, I, H, sp, big):
+    """The bf16 weight gradient on 256-row x 256-feature tiles (dropped rows
+    multiplied as zeros) and the kernel that routes the kept rows' products,
+    each against the oracle."""
+    d = make_layer(T, B, I, H, seed=T + B + H, w_scale=0.1, dtype="bf16", state=True)
+    try:
+        L.set_option("wgrad_big", big)
+        check_layer(L, d, "bf16", sp, dense=sp == 0.0, own=False)
+    finally:
+        L.set_option("wgrad_big", 1)
+
+
+def test_side_stream_modes_identical_bf16_big(L):
+    """Steps of the 256 x 256-tile bf16 weight gradient split over side-stream
+    launches (each continuing the stored sums) give the bits of one launch."""
+    d = make_layer(20, 64, 1024, 2048, seed=16, w_scale=0.1, dtype="bf16", state=True)
+    x, W = gpu_tensor(d["x"], "bf16"), gpu_tensor(d["W"], "bf16")
+    dH, dhT, dcT = gpu_tensor(d["dH_up"]), gpu_tensor(d["dhT"]), gpu_tensor(d["dcT"])
+    _, cache = L.fwd_cache(x, W)
+    outs = []
+    try:
+        for mode in (1, 0):
+            L.set_option("side_stream", mode)
+            outs.append(L.bwd_structsparse(x, W, cache, dH, 0.5, dhT=dhT, dcT=dcT))
+            torch.cuda.synchronize()
+    finally:
+        L.set_option("side_stream", 2)
+    for k in ("dX", "dW", "db", "dh0", "dc0", "idx"):
+        assert torch.equal(outs[1][k], outs[0][k]), k
+
+
 @pytest.mark.parametrize("graphs", [True, False])
 def test_side_stream_modes_identical(L, graphs):
     """The weight gradient and dX on the side stream (1), in order on the
