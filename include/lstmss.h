@@ -359,14 +359,16 @@ int32_t lstmss_mse_grad(const lstmss_dims *d, const void *h, const float *y, flo
  *                      the staging matrix and selects in a second kernel
  *                      (same bits; for checking and timing).
  *   LSTMSS_OPT_WGRAD_BIG  1 (default): the bf16 weight gradient with 128-byte
- *                      batch chunks (B a multiple of 64) runs on 256-row x
- *                      256-feature tiles, the dropped rows of a coarse
- *                      structure multiplied as zeros (regions of P * R rows
- *                      dividing 256, a multiple of 64 kept rows per tile);
- *                      0 runs the 32-row-group kernel that multiplies only
- *                      the kept rows.  The two sum in different orders
- *                      (both fixed; each matches the oracle to the bf16
- *                      tolerance).
+ *                      batch chunks (B a multiple of 64, I a multiple of 8)
+ *                      runs on 256-row x 256-feature tiles when it is dense
+ *                      (sparsity 0 included) or when a coarse structure's
+ *                      regions of P * R rows divide 256 and keep 128 or 192
+ *                      rows of each tile, with at least 256 tiles; the
+ *                      dropped rows are then multiplied as zeros.  0 (and
+ *                      every other case) runs the 32-row-group kernel that
+ *                      multiplies only the kept rows.  The two sum in
+ *                      different orders (both fixed; each matches the oracle
+ *                      to the bf16 tolerance).
  * Changing an option drops the recorded graphs.  Not for use while calls
  * are being enqueued from other threads. */
 enum {
