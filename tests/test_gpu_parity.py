@@ -389,6 +389,8 @@ def test_graph_replay_matches_direct(L, H, sp):
     (3, 64, 1024, 2048, 0.5, 0),     # the routing kernel on the same shape
     (3, 64, 1000, 2050, 0.25, 1),    # 192 kept rows; ragged tiles, a partial last region
     (3, 128, 1000, 2050, 0.0, 1),    # dense, ragged tiles
+    (3, 64, 1024, 2048, 0.75, 1),    # 64 kept rows per tile: the routing kernel
+    (3, 64, 512, 512, 0.5, 1),       # 32 tiles, fewer than 256: the routing kernel
 ])
 def test_wgrad_big_bf16(L, T, B, I, H, sp, big):
     """The bf16 weight gradient on 256-row x 256-feature tiles (dropped rows
