@@ -655,8 +655,9 @@ void wg_launch(const WgradArgs &a, bool vec, bool dma, dim3 grid, hipStream_t s)
 // rows x 64 features (2 x 4 MFMA tiles, accumulated in registers across all
 // steps).  Per chunk the staged operands are 256 feature rows and the tile's
 // KRT compacted gate-gradient rows; a wavefront reads 0.75 KB of LDS per
-// MFMA (the 32-row-group kernel above reads 1.5 KB, which makes it bound by
-// LDS bandwidth).
+// MFMA (the 32-row-group kernel above reads 1.5 KB), and each staged byte
+// feeds twice the MFMA work, so fewer chunk copies and reads are waited for
+// per MFMA.
 // Sparse: the tile covers whole regions (P * R divides 256), so its kept rows
 // are the contiguous compacted rows [KRT * tile, KRT * (tile + 1)) at every
 // step.  Instead of routing a product of the kept rows, each lane's B operand
