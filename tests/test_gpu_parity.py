@@ -517,6 +517,65 @@ def test_bf16_h4096(L):
     check_layer(L, d, wl.dtype, wl.sparsity, P=wl.P, R=wl.R, own=False)
 
 
+def test_bf16_h4096_full_length_sampled(L):
+    """The bf16 H = 4096, B = 256, T = 100 layer call as the benchmark makes it
+    (one weight-gradient launch over all 100 steps, batched dX launches):
+    sampled entries of dW, dX and db, each summed in fp64 from the GPU's own
+    gate gradients, masks and cached inputs (sections 3 and 4: dW sums
+    dG_t [x_t; h_{t-1}]^T over the kept rows, dX_t = W_x^T dG_t over the kept
+    rows), and the masks of a few steps against the oracle's selection."""
+    wl = WORKLOADS["lstm1_h4096_b256_t100_bf16"]
+    inp = make_inputs(wl, seed=0)
+    T, B, I, H, P, R = wl.steps, wl.batch, wl.input_size, wl.hidden, wl.P, wl.R
+    S = int(round(wl.sparsity * R))
+    x, W = gpu_tensor(inp["x"], "bf16"), gpu_tensor(inp["Ws"][0], "bf16")
+    dH = gpu_tensor(inp["dH_up"])
+    _, cache = L.fwd_cache(x, W)
+    o = L.bwd_structsparse(x, W, cache, dH, sparsity=wl.sparsity, P=P, R=R, want_dbg=True)
+    torch.cuda.synchronize()
+    _, _, h = L.cache_views(cache, T, B, H, "bf16")
+    idx = o["idx"].cpu().numpy()
+    keep = keep_from_idx(idx, 4 * H // P)                          # [T][slices]
+    assert np.all(keep.sum(1) * P == oracle.kept_rows(4 * H, P, R, S))
+    for t in (0, T // 2, T - 1):                                    # masks, bit-exact
+        k = oracle.select(oracle.scores(to_np64(o["dbg"][t]), P), R, S)
+        assert np.array_equal(oracle.kept_index(k), idx[t]), t
+    rng = np.random.default_rng(7)
+    n = 48
+    rows = torch.from_numpy(rng.integers(0, 4 * H, n)).to(dev())
+    cols = rng.integers(0, I + H, n)
+    g = o["dbg"].index_select(1, rows).double().cpu().numpy()      # [T][n][B]
+    rows = rows.cpu().numpy()
+    xh = np.empty((T, n, B))
+    for j, c in enumerate(cols):
+        src = x[:, c, :] if c < I else h[:T, c - I, :]              # h[t] = h_{t-1}
+        xh[:, j, :] = src.double().cpu().numpy()
+    kr = keep[:, rows // P].astype(np.float64)                      # [T][n]
+    terms = kr[:, :, None] * g * xh
+    ref = terms.sum(axis=(0, 2))
+    got = o["dW"][torch.from_numpy(rows).to(dev()), torch.from_numpy(cols).to(dev())]
+    err = np.abs(got.double().cpu().numpy() - ref)
+    mag = np.abs(terms).sum(axis=(0, 2))
+    # bf16 x bf16 products are exact in fp32; the fp32 sums of 25600 of them
+    # stay far below this bound, while one step missing or misplaced (about a
+    # hundredth of a sum of random signs) exceeds it
+    print("dW sample error / sum |terms|: max %.3g" % (err / mag).max())
+    assert np.all(err <= 2e-5 * mag + 1e-30), (err / mag).max()
+    # db: each kept step's row sum
+    dbr = (kr[:, :, None] * g).sum(axis=(0, 2))
+    assert np.allclose(o["db"][torch.from_numpy(rows).to(dev())].double().cpu().numpy(), dbr,
+                       rtol=1e-4, atol=1e-4 * np.abs(kr[:, :, None] * g).sum(axis=(0, 2)).max())
+    # dX: sampled (t, i, b) over all kept rows of step t
+    ts, ii, bb = rng.integers(0, T, n), rng.integers(0, I, n), rng.integers(0, B, n)
+    Wx = W[:, torch.from_numpy(ii).to(dev())].double().cpu().numpy()          # [4H][n]
+    for j in range(n):
+        t = ts[j]
+        gt = o["dbg"][t, :, bb[j]].double().cpu().numpy()                       # [4H]
+        m = np.repeat(keep[t], P).astype(np.float64)
+        tj = m * gt * Wx[:, j]
+        assert abs(o["dX"][t, ii[j], bb[j]].item() - tj.sum()) <= 1e-4 * np.abs(tj).sum() + 1e-30, j
+
+
 def test_error_paths(L):
     d = L.dims(2, 4, 4, 8)
     assert L.kept_rows(d, 0.5, L.structure(4, 8)) == 16
