@@ -178,6 +178,60 @@ def test_stack_headline_shape_oracle(L):
         up = got["dX"][l]
 
 
+def test_stack_headline_full_length_sampled(L):
+    """The benchmark's timed call itself: the four-layer stack at I = H = 2048,
+    B = 128, T = 50 (input-gradient launches of 12, 12, 12, 12 and 2 steps).
+    Every layer equals its own call in turn on the stack's upstream gradient
+    (dW, db, dX and idx bit for bit); each layer's masks at three steps
+    against the oracle's selection; sampled dW and dX entries summed in fp64
+    from the layer's gate gradients, masks and inputs (sections 3 and 4)."""
+    layers, T, P, R, S = 4, 50, 4, 8, 4
+    xs, Ws, caches, dH = workload_stack(L, "lstm4_enc_h2048_b128_t50_f32", layers, T)
+    got = L.bwd_stack(xs, Ws, caches, dH, sparsity=0.5, P=P, R=R, want_dX0=True)
+    torch.cuda.synchronize()
+    H = Ws[0].shape[0] // 4
+    B = dH.shape[2]
+    dev = torch.device("cuda:0")
+    rng = np.random.default_rng(11)
+    n = 32
+    up = dH
+    for l in reversed(range(layers)):
+        I = xs[l].shape[1]
+        o = L.bwd_structsparse(xs[l], Ws[l], caches[l], up, sparsity=0.5, P=P, R=R,
+                               want_dbg=True)
+        torch.cuda.synchronize()
+        for k in ("dW", "db", "dX", "idx"):
+            assert torch.equal(o[k], got[k][l]), (l, k)
+        idx = got["idx"][l].cpu().numpy()
+        for t in (0, T // 2, T - 1):
+            k = oracle.select(oracle.scores(o["dbg"][t].double().cpu().numpy(), P), R, S)
+            assert np.array_equal(oracle.kept_index(k), idx[t]), (l, t)
+        keep = np.zeros((T, 4 * H // P), np.uint8)
+        for t in range(T):
+            keep[t, idx[t]] = 1
+        _, _, h = L.cache_views(caches[l], T, B, H, "f32")
+        rows = rng.integers(0, 4 * H, n)
+        cols = rng.integers(0, I + H, n)
+        g = o["dbg"].index_select(1, torch.from_numpy(rows).to(dev)).double().cpu().numpy()
+        xh = np.empty((T, n, B))
+        for j, c in enumerate(cols):
+            src = xs[l][:, c, :] if c < I else h[:T, c - I, :]       # h[t] = h_{t-1}
+            xh[:, j, :] = src.double().cpu().numpy()
+        terms = keep[:, rows // P].astype(np.float64)[:, :, None] * g * xh
+        gotw = got["dW"][l][torch.from_numpy(rows).to(dev), torch.from_numpy(cols).to(dev)]
+        err = np.abs(gotw.double().cpu().numpy() - terms.sum(axis=(0, 2)))
+        assert np.all(err <= 2e-5 * np.abs(terms).sum(axis=(0, 2)) + 1e-30), (l, err.max())
+        ts, ii, bb = rng.integers(0, T, n), rng.integers(0, I, n), rng.integers(0, B, n)
+        Wx = Ws[l][:, torch.from_numpy(ii).to(dev)].double().cpu().numpy()
+        for j in range(n):
+            t = ts[j]
+            tj = (np.repeat(keep[t], P).astype(np.float64) *
+                  o["dbg"][t, :, bb[j]].double().cpu().numpy() * Wx[:, j])
+            e = abs(got["dX"][l][t, ii[j], bb[j]].item() - tj.sum())
+            assert e <= 2e-5 * np.abs(tj).sum() + 1e-30, (l, j, e)
+        up = got["dX"][l]
+
+
 def test_stack_bf16(L):
     xs, Ws, caches, dH = make_stack(L, 2, 6, 64, 64, 128, seed=3, dtype=torch.bfloat16)
     ref = sequential(L, xs, Ws, caches, dH, 0.5, {"P": 4, "R": 8})
