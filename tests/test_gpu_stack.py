@@ -178,16 +178,26 @@ def test_stack_headline_shape_oracle(L):
         up = got["dX"][l]
 
 
-def test_stack_headline_full_length_sampled(L):
-    """The benchmark's timed call itself: the four-layer stack at I = H = 2048,
-    B = 128, T = 50 (input-gradient launches of 12, 12, 12, 12 and 2 steps).
-    Every layer equals its own call in turn on the stack's upstream gradient
-    (dW, db, dX and idx bit for bit); each layer's masks at three steps
-    against the oracle's selection; sampled dW and dX entries summed in fp64
-    from the layer's gate gradients, masks and inputs (sections 3 and 4)."""
-    layers, T, P, R, S = 4, 50, 4, 8, 4
+@pytest.mark.parametrize("struct", [
+    {"P": 4, "R": 8},                                  # the benchmark's coarse structure
+    {"kind": 1, "My": 8, "Mx": 4},                     # the fine 8 x 4 blocks it also times
+    {"kind": 1, "My": 32, "Mx": 32},                   # and the 32 x 32 blocks
+])
+def test_stack_headline_full_length_sampled(L, struct):
+    """The benchmark's timed calls themselves: the four-layer stack at
+    I = H = 2048, B = 128, T = 50 (input-gradient launches of 12, 12, 12, 12
+    and 2 steps), coarse and fine.  Every layer equals its own call in turn on
+    the stack's upstream gradient (dW, db, dX and idx bit for bit); each
+    layer's masks at three steps against the oracle's selection; sampled dW
+    and dX entries summed in fp64 from the layer's gate gradients, masks and
+    inputs (sections 3 and 4: the products run over the kept rows or blocks)."""
+    layers, T = 4, 50
+    fine = struct.get("kind") == 1
     xs, Ws, caches, dH = workload_stack(L, "lstm4_enc_h2048_b128_t50_f32", layers, T)
-    got = L.bwd_stack(xs, Ws, caches, dH, sparsity=0.5, P=P, R=R, want_dX0=True)
+    kw = dict(struct)
+    if fine:
+        kw["kind"] = L.FINE
+    got = L.bwd_stack(xs, Ws, caches, dH, sparsity=0.5, want_dX0=True, **kw)
     torch.cuda.synchronize()
     H = Ws[0].shape[0] // 4
     B = dH.shape[2]
@@ -197,18 +207,35 @@ def test_stack_headline_full_length_sampled(L):
     up = dH
     for l in reversed(range(layers)):
         I = xs[l].shape[1]
-        o = L.bwd_structsparse(xs[l], Ws[l], caches[l], up, sparsity=0.5, P=P, R=R,
-                               want_dbg=True)
+        o = L.bwd_structsparse(xs[l], Ws[l], caches[l], up, sparsity=0.5, want_dbg=True, **kw)
         torch.cuda.synchronize()
         for k in ("dW", "db", "dX", "idx"):
             assert torch.equal(o[k], got[k][l]), (l, k)
         idx = got["idx"][l].cpu().numpy()
-        for t in (0, T // 2, T - 1):
-            k = oracle.select(oracle.scores(o["dbg"][t].double().cpu().numpy(), P), R, S)
-            assert np.array_equal(oracle.kept_index(k), idx[t]), (l, t)
-        keep = np.zeros((T, 4 * H // P), np.uint8)
-        for t in range(T):
-            keep[t, idx[t]] = 1
+        # row mask [T][4H][B] of the kept entries, checked at three steps
+        if fine:
+            My, Mx = struct["My"], struct["Mx"]
+            nb = oracle.fine_blocks(B, My)
+            K = int(round(0.5 * nb))
+            idx = idx.reshape(T, 4 * H // Mx, nb - K)
+            for t in (0, T // 2, T - 1):
+                k = oracle.fine_select(oracle.fine_scores(o["dbg"][t].double().cpu().numpy(), Mx, My), K)
+                assert np.array_equal(oracle.fine_kept_index(k, K), idx[t]), (l, t)
+            keep = np.zeros((T, 4 * H // Mx, nb), np.uint8)
+            for t in range(T):
+                for sl in range(4 * H // Mx):
+                    keep[t, sl, idx[t, sl][idx[t, sl] >= 0]] = 1
+            mask = np.repeat(np.repeat(keep, Mx, axis=1), My, axis=2)[:, :, :B]
+        else:
+            P, R = struct["P"], struct["R"]
+            S = int(round(0.5 * R))
+            for t in (0, T // 2, T - 1):
+                k = oracle.select(oracle.scores(o["dbg"][t].double().cpu().numpy(), P), R, S)
+                assert np.array_equal(oracle.kept_index(k), idx[t]), (l, t)
+            keep = np.zeros((T, 4 * H // P), np.uint8)
+            for t in range(T):
+                keep[t, idx[t]] = 1
+            mask = np.broadcast_to(np.repeat(keep, P, axis=1)[:, :, None], (T, 4 * H, B))
         _, _, h = L.cache_views(caches[l], T, B, H, "f32")
         rows = rng.integers(0, 4 * H, n)
         cols = rng.integers(0, I + H, n)
@@ -217,7 +244,7 @@ def test_stack_headline_full_length_sampled(L):
         for j, c in enumerate(cols):
             src = xs[l][:, c, :] if c < I else h[:T, c - I, :]       # h[t] = h_{t-1}
             xh[:, j, :] = src.double().cpu().numpy()
-        terms = keep[:, rows // P].astype(np.float64)[:, :, None] * g * xh
+        terms = mask[:, rows, :].astype(np.float64) * g * xh
         gotw = got["dW"][l][torch.from_numpy(rows).to(dev), torch.from_numpy(cols).to(dev)]
         err = np.abs(gotw.double().cpu().numpy() - terms.sum(axis=(0, 2)))
         assert np.all(err <= 2e-5 * np.abs(terms).sum(axis=(0, 2)) + 1e-30), (l, err.max())
@@ -225,7 +252,7 @@ def test_stack_headline_full_length_sampled(L):
         Wx = Ws[l][:, torch.from_numpy(ii).to(dev)].double().cpu().numpy()
         for j in range(n):
             t = ts[j]
-            tj = (np.repeat(keep[t], P).astype(np.float64) *
+            tj = (mask[t, :, bb[j]].astype(np.float64) *
                   o["dbg"][t, :, bb[j]].double().cpu().numpy() * Wx[:, j])
             e = abs(got["dX"][l][t, ii[j], bb[j]].item() - tj.sum())
             assert e <= 2e-5 * np.abs(tj).sum() + 1e-30, (l, j, e)
