@@ -108,3 +108,22 @@ def test_bidir_backward(L, T, B, I, H, sparsity):
     assert rel(np64(o["dW_rev"]), res[1]["dW"]) <= 1e-5
     assert rel(np64(o["db_rev"]), res[1]["db"]) <= 1e-5
     assert rel(np64(o["dX"]), res[0]["dX"] + res[1]["dX"][::-1]) <= 1e-5
+
+
+def test_bidir_backward_benchmark_shape(L):
+    """The bidirectional layer the benchmark times (I = H = 2048, B = 128,
+    T = 50, 50 %): both directions run concurrently and equal the two
+    direction calls bit for bit (each of those is the single-layer call whose
+    parity at this shape the single-layer tests establish)."""
+    T, B, I, H = 50, 128, 2048, 2048
+    df, dr, x, x_rev, Wf, Wr, hf, hr, cf, cr, dH = setup(L, T, B, I, H, seed=5)
+    o = L.bwd_bidir(x, x_rev, Wf, Wr, cf, cr, dH, sparsity=0.5)
+    dHf = dH[:, :H].contiguous()
+    dHr = torch.flip(dH[:, H:], dims=[0]).contiguous()
+    a = L.bwd_structsparse(x, Wf, cf, dHf, sparsity=0.5)
+    b = L.bwd_structsparse(x_rev, Wr, cr, dHr, sparsity=0.5)
+    torch.cuda.synchronize()
+    assert torch.equal(o["dW_fwd"], a["dW"]) and torch.equal(o["dW_rev"], b["dW"])
+    assert torch.equal(o["db_fwd"], a["db"]) and torch.equal(o["db_rev"], b["db"])
+    assert torch.equal(o["idx_fwd"], a["idx"]) and torch.equal(o["idx_rev"], b["idx"])
+    assert torch.equal(o["dX"], a["dX"] + torch.flip(b["dX"], dims=[0]))
